@@ -1,0 +1,155 @@
+"""Seeded synthetic inputs for MALA attention, shared by the HIP path's tests and
+benchmark and by the oracle's tests.  This module holds none of the method's
+arithmetic: it only draws random numbers and rounds them to bf16.
+
+The paper measures operator latency on unspecified inputs and operator fidelity
+on hidden states of a 14B checkpoint that is not available; these generators
+stand in for both.  Recipe (identical for every configuration):
+
+  * one independent PCG64 stream per (tensor, batch, head), seeded with
+    ``numpy.random.default_rng([seed, config_id, tensor_id, b, h])``, so any
+    single head can be regenerated without drawing the others;
+  * values drawn in float64 and rounded to bf16 with round-to-nearest-even;
+  * K and V ~ N(0, 1); dO ~ N(0, 1);
+  * planted-needle queries: Q_i = g_i + beta * K_{r(i)} with g ~ N(0, 1) and
+    r(i) uniform on {0..i}, built from the ROUNDED K of the head's KV head and
+    rounded again; optional local term Q_i += alpha * K_{i-1};
+  * decode queries: q = g + beta * sum of K at 4 distinct random positions.
+
+Arrays are returned as uint16 bf16 bit patterns in [B, H, N, D] layout.
+"""
+from __future__ import annotations
+
+import math
+from concurrent.futures import ThreadPoolExecutor
+
+import numpy as np
+
+# tensor ids of the per-slice streams
+_T_K, _T_V, _T_Q, _T_DO, _T_BETA, _T_POS = 1, 2, 3, 4, 5, 6
+
+# The five workloads.  "kind": "train" (fwd + bwd) or "decode".
+CONFIGS = {
+    1: dict(kind="train", B=1, Hq=1, Hkv=1, N=1024, D=64, beta=2.0, local=0.0,
+            taus=(0.0, 1e-4, 1e-3), desc="causal fwd+bwd, 1x1x1024x64, needle beta=2"),
+    2: dict(kind="train", B=1, Hq=16, Hkv=16, N=8192, D=128, beta=2.0, local=1.0,
+            taus=(0.0, 1e-4, 1e-3), desc="causal fwd+bwd, MHA 16 heads, 8192x128, needle beta=2 + local 1.0"),
+    3: dict(kind="train", B=1, Hq=32, Hkv=8, N=32768, D=128, beta=(0.5, 3.0), local=0.0,
+            taus=(0.0, 1e-4), desc="causal fwd+bwd, GQA 32/8, 32768x128, per-head beta~U[0.5,3]"),
+    4: dict(kind="train", B=1, Hq=8, Hkv=2, N=131072, D=128, beta=2.0, local=0.0,
+            taus=(0.0, 1e-4), desc="causal fwd+bwd, GQA 8/2 (one TP=8 share), 131072x128, beta=2"),
+    5: dict(kind="decode", B=16, Hq=32, Hkv=8, N=131072, D=128, beta=3.0, needles=4,
+            taus=(0.0, 1e-4), desc="decode, 16 x GQA 32/8 over 131072-token caches, 4 needles beta=3"),
+}
+
+
+def bf16_round(x: np.ndarray) -> np.ndarray:
+    """Round float64 values to bf16 (round-to-nearest-even); return uint16 bits."""
+    x = np.asarray(x, dtype=np.float64)
+    m, e = np.frexp(x)                      # x = m * 2**e, 0.5 <= |m| < 1
+    # bf16 keeps 8 significant bits: quantum 2**(e - 8) for |x| in [2**(e-1), 2**e)
+    r = np.ldexp(np.round(np.ldexp(m, 8)), e - 8)   # np.round: half to even, exact scaling
+    bits = r.astype(np.float32).view(np.uint32)     # exact: r has <= 8 significant bits
+    return (bits >> 16).astype(np.uint16)
+
+
+def bf16_to_f64(bits: np.ndarray) -> np.ndarray:
+    """Widen bf16 bit patterns to float64 (exact)."""
+    b = np.asarray(bits, dtype=np.uint16).astype(np.uint32) << 16
+    return b.view(np.float32).astype(np.float64)
+
+
+def _rng(seed, cfg_id, tensor, b, h):
+    return np.random.default_rng([int(seed), int(cfg_id), tensor, int(b), int(h)])
+
+
+def _normal_bits(seed, cfg_id, tensor, b, h, shape):
+    return bf16_round(_rng(seed, cfg_id, tensor, b, h).standard_normal(shape))
+
+
+class Workload:
+    """Lazily generated inputs of one configuration (any subset of heads)."""
+
+    def __init__(self, cfg, seed: int = 0, **overrides):
+        if isinstance(cfg, int):
+            self.cfg_id = cfg
+            spec = dict(CONFIGS[cfg])
+        else:
+            spec = dict(cfg)
+            self.cfg_id = int(spec.pop("id", 0))
+        spec.update(overrides)
+        self.spec = spec
+        self.seed = seed
+        self.kind = spec["kind"]
+        self.B, self.Hq, self.Hkv = spec["B"], spec["Hq"], spec["Hkv"]
+        self.N, self.D = spec["N"], spec["D"]
+        self.g = self.Hq // self.Hkv
+        self.scale = 1.0 / math.sqrt(self.D)
+        self._k = {}
+
+    # ---- per-slice generators -------------------------------------------
+    def k_head(self, b, hkv):
+        key = (b, hkv)
+        if key not in self._k:
+            self._k[key] = _normal_bits(self.seed, self.cfg_id, _T_K, b, hkv, (self.N, self.D))
+        return self._k[key]
+
+    def v_head(self, b, hkv):
+        return _normal_bits(self.seed, self.cfg_id, _T_V, b, hkv, (self.N, self.D))
+
+    def do_head(self, b, h):
+        return _normal_bits(self.seed, self.cfg_id, _T_DO, b, h, (self.N, self.D))
+
+    def beta(self, h):
+        beta = self.spec["beta"]
+        if isinstance(beta, tuple):
+            lo, hi = beta
+            return float(_rng(self.seed, self.cfg_id, _T_BETA, 0, h).uniform(lo, hi))
+        return float(beta)
+
+    def q_head(self, b, h):
+        """Planted-needle query rows for a training workload (or the decode query)."""
+        kf = bf16_to_f64(self.k_head(b, h // self.g))
+        rng = _rng(self.seed, self.cfg_id, _T_Q, b, h)
+        beta = self.beta(h)
+        if self.kind == "decode":
+            g = rng.standard_normal(self.D)
+            n = self.spec.get("needles", 4)
+            pos = rng.choice(self.N, size=n, replace=False)
+            return bf16_round(g + beta * kf[pos].sum(axis=0))
+        N = self.N
+        g = rng.standard_normal((N, self.D))
+        r = rng.integers(0, np.arange(1, N + 1))        # r(i) uniform on {0..i}
+        q = g + beta * kf[r]
+        alpha = float(self.spec.get("local", 0.0))
+        if alpha:
+            q[1:] += alpha * kf[:-1]
+        return bf16_round(q)
+
+    def needle_positions(self, b, h):
+        """Decode only: the planted positions of query head (b, h)."""
+        rng = _rng(self.seed, self.cfg_id, _T_Q, b, h)
+        rng.standard_normal(self.D)
+        return np.sort(rng.choice(self.N, size=self.spec.get("needles", 4), replace=False))
+
+    # ---- whole tensors ---------------------------------------------------
+    def _stack(self, fn, H, threads):
+        idx = [(b, h) for b in range(self.B) for h in range(H)]
+        with ThreadPoolExecutor(max_workers=max(1, threads)) as ex:
+            parts = list(ex.map(lambda bh: fn(*bh), idx))
+        shape = parts[0].shape
+        out = np.empty((self.B, H) + shape, dtype=np.uint16)
+        for (b, h), p in zip(idx, parts):
+            out[b, h] = p
+        return out
+
+    def tensors(self, threads: int = 8, with_do: bool = True):
+        """All inputs as uint16 bf16 bits: q [B,Hq,N,D] (decode: [B,Hq,D]), k, v [B,Hkv,N,D], do."""
+        k = self._stack(self.k_head, self.Hkv, threads)
+        v = self._stack(self.v_head, self.Hkv, threads)
+        q = self._stack(self.q_head, self.Hq, threads)
+        out = dict(q=q, k=k, v=v)
+        if with_do and self.kind == "train":
+            out["do"] = self._stack(self.do_head, self.Hq, threads)
+        self._k.clear()
+        return out
