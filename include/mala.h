@@ -1,0 +1,158 @@
+/*
+ * mala.h — C ABI of the MI355X (gfx950) MALA causal-attention library (libmala.so).
+ *
+ * MALA ("MassAlloc Attention") computes the QK score tile of EVERY causally legal
+ * tile and runs the post-score work of a tile only when the tile's normalized
+ * contribution reaches the length-aware tolerance tau / L_q (Methodology,
+ * "Attention as a Compute Allocator": L_q is the number of keys visible to query
+ * row q).
+ *   - forward: Algorithm 1 with the online test (Eq. online test) against the
+ *     running max m and normalizer l of the retained tiles; tiles are visited from
+ *     the diagonal towards earlier keys; an empty row always retains;
+ *   - backward: Algorithm 2 with the offline test (Eq. offline test) against the
+ *     saved log-normalizer (LSE);
+ *   - decode: the forward rule applied per split of the KV cache with the
+ *     threshold of the full context (L = Nk), splits merged by the
+ *     normalizer-aware reduction (Fused Execution section and its appendix).
+ *
+ * Conventions shared by every entry point
+ *   - All tensor arguments are DEVICE pointers, owned by the caller, contiguous,
+ *     in BHSD layout (batch, head, sequence, head_dim).  The library never
+ *     allocates, frees or retains them.
+ *   - Q, K, V, dO, the KV caches and the decode query are bf16 (passed as void*);
+ *     O, LSE and the gradients are fp32; LSE is the natural-log normalizer
+ *     z_q = log sum_{k in R_q} exp(s_qk) of the retained set R_q.
+ *   - scale multiplies Q.K in fp32 (the paper absorbs it into Q; it is never
+ *     re-rounded to bf16 here); tau >= 0 (tau = 0 runs every tile: dense
+ *     attention through the same kernels).
+ *   - GQA: query head h reads key/value head h / (Hq / Hkv).
+ *   - Causal masking is bottom-right aligned: row q sees keys k <= q + Nk - Nq, so
+ *     L_q = q + 1 + Nk - Nq (L_q = q + 1 when Nq == Nk; L = Nk for decode).
+ *   - Decision geometry: the forward and backward share one tile partition
+ *     (B_q x B_k, reported by mala_geometry), which the support-nesting property
+ *     of the backward needs.  Decode tiles are 1 x B_k per query head.
+ *   - Calls validate synchronously, then enqueue kernels on `stream` (a
+ *     hipStream_t; NULL = the default stream) and return without waiting.  The
+ *     return value reports validation and launch errors only; a device fault is
+ *     reported by the caller's next synchronisation.  Calls are re-entrant; the
+ *     library keeps no state between calls.
+ *   - Statistics pointers (row_tiles, head_tiles, counters) may be NULL.  When
+ *     given they are OVERWRITTEN by the call (the library clears them first on
+ *     the same stream).  No mask or retained-tile index is ever materialised.
+ */
+#ifndef MALA_H
+#define MALA_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Status codes (0 = success, negative = error). */
+typedef enum {
+  MALA_OK = 0,
+  MALA_ERR_INVALID_ARG = -1, /* null required pointer, non-positive size, Hq % Hkv != 0,
+                                Nq > Nk, tau < 0 or NaN, scale not finite or <= 0,
+                                num_splits < 1 */
+  MALA_ERR_UNSUPPORTED = -2, /* head_dim not in {64, 128}, or causal == 0 (the paper's
+                                traversal is defined for causal attention only) */
+  MALA_ERR_WORKSPACE = -3,   /* workspace NULL or smaller than the *_workspace_size query */
+  MALA_ERR_HIP = -4          /* a HIP launch/runtime call failed; see mala_last_error() */
+} mala_status;
+
+/* Indices into the int64 counters[4] array that every entry point can fill. */
+enum {
+  MALA_CNT_LEGAL = 0,    /* decision tiles holding at least one legal (causal) entry,
+                            per query head */
+  MALA_CNT_RETAINED = 1, /* of those, tiles whose post-score path ran */
+  MALA_CNT_V_TILES = 2,  /* forward: V tiles of B_k keys staged by the kernel;
+                            backward: dO tiles of B_q rows staged;
+                            decode: V tiles of B_k keys read (once per GQA group) */
+  MALA_CNT_SLOTS = 3     /* post-score key slots summed over query rows: a retained
+                            B_q x B_k tile adds B_k slots to each of its valid rows
+                            (Attention Cost section; mean slots per query =
+                            counters[3] / number of query rows) */
+};
+
+enum { MALA_PASS_FWD = 0, MALA_PASS_BWD = 1, MALA_PASS_DECODE = 2 };
+
+/* Decision tile of a pass: B_q query rows x B_k keys. */
+typedef struct {
+  int32_t block_q;
+  int32_t block_k;
+} mala_geometry_t;
+
+/* Decision geometry used by `pass` (MALA_PASS_*) at head_dim (64 or 128).
+ * Returns {0, 0} for an unsupported pass or head_dim. */
+mala_geometry_t mala_geometry(int head_dim, int pass);
+
+/* Static description of a status code; never NULL. */
+const char* mala_strerror(int status);
+
+/* Detail of the last error raised on the calling thread ("" if none). */
+const char* mala_last_error(void);
+
+/*
+ * MALA forward (Algorithm 1), also the prefill operator.
+ *   q:  bf16 [B, Hq,  Nq, D]        k, v: bf16 [B, Hkv, Nk, D]
+ *   o:  fp32 [B, Hq, Nq, D]  out    softmax output renormalised over the retained set
+ *   lse: fp32 [B, Hq, Nq]    out    natural-log normalizer z_q = m_q + log l_q
+ *   row_tiles: int32 [B, Hq, Nq] or NULL   out: retained tiles in which the row has a
+ *              legal key
+ *   counters:  int64 [4] or NULL          out: see MALA_CNT_*
+ *   causal must be 1.  Requires Nq <= Nk, D in {64, 128}.
+ */
+int mala_fwd(const void* q, const void* k, const void* v, float* o, float* lse,
+             int32_t* row_tiles, int64_t* counters, int B, int Hq, int Hkv, int Nq, int Nk,
+             int D, int causal, float scale, float tau, void* stream);
+
+/* Bytes of device workspace mala_bwd needs for this shape (the per-row
+ * D_q = rowsum(O_q * dO_q) vector of Algorithm 2). */
+size_t mala_bwd_workspace_size(int B, int Hq, int Hkv, int Nq, int Nk, int D);
+
+/*
+ * MALA backward (Algorithm 2): gradients of <O, dO> restricted to the tiles that
+ * pass the offline test against the saved lse.
+ *   q: bf16 [B, Hq, Nq, D]; k, v: bf16 [B, Hkv, Nk, D]; o: fp32 [B, Hq, Nq, D] and
+ *   lse: fp32 [B, Hq, Nq] as returned by mala_fwd; dout: bf16 [B, Hq, Nq, D].
+ *   dq: fp32 [B, Hq, Nq, D] out (accumulated with fp32 atomics after the library
+ *       clears it; summation order, and so the last bits, may vary run to run);
+ *   dk, dv: fp32 [B, Hkv, Nk, D] out (summed over the GQA group inside one
+ *       workgroup, no atomics: bitwise reproducible);
+ *   row_tiles: int32 [B, Hq, Nq] or NULL out; counters: int64 [4] or NULL out.
+ *   workspace: device memory of at least mala_bwd_workspace_size(...) bytes,
+ *   16-byte aligned, owned by the caller, not read by the caller afterwards.
+ */
+int mala_bwd(const void* q, const void* k, const void* v, const float* o, const float* lse,
+             const void* dout, float* dq, float* dk, float* dv, int32_t* row_tiles,
+             int64_t* counters, void* workspace, size_t workspace_bytes, int B, int Hq, int Hkv,
+             int Nq, int Nk, int D, int causal, float scale, float tau, void* stream);
+
+/* Bytes of device workspace mala_decode needs: fp32 split partials
+ * [B, Hq, num_splits, D + 2]. */
+size_t mala_decode_workspace_size(int B, int Hq, int D, int num_splits);
+
+/*
+ * MALA split-KV decode of one new query token per (batch, query head) against a
+ * KV cache of Nk tokens that already includes the token's own key/value.
+ *   q: bf16 [B, Hq, D]; k_cache, v_cache: bf16 [B, Hkv, Nk, D]
+ *   o: fp32 [B, Hq, D] out; lse: fp32 [B, Hq] out
+ *   head_tiles: int32 [B, Hq] or NULL out (retained tiles summed over splits)
+ *   counters: int64 [4] or NULL out
+ *   num_splits >= 1: the key tiles (ceil(Nk / B_k) of them) are cut into
+ *   num_splits contiguous ranges of ceil(T / num_splits) tiles; each range starts
+ *   from an empty normalizer, so the retained set depends on num_splits.
+ *   workspace: at least mala_decode_workspace_size(...) bytes.
+ */
+int mala_decode(const void* q, const void* k_cache, const void* v_cache, float* o, float* lse,
+                int32_t* head_tiles, int64_t* counters, int num_splits, void* workspace,
+                size_t workspace_bytes, int B, int Hq, int Hkv, int Nk, int D, float scale,
+                float tau, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* MALA_H */

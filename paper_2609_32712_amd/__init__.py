@@ -1,0 +1,205 @@
+"""Python binding of libmala.so, the MI355X (gfx950) MALA causal-attention library.
+
+Argument marshalling only: every step of forward, backward and decode runs in the
+HIP kernels behind the C ABI of include/mala.h.  PyTorch provides device memory
+and the current stream.  There is no fallback: if libmala.so is missing or no
+GPU is present, the calls raise.
+
+Low-level functions carry the C names and arguments (mala_fwd, mala_bwd,
+mala_decode, mala_geometry, mala_bwd_workspace_size, mala_decode_workspace_size);
+fwd / bwd / decode allocate their outputs and return them in a dict.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libmala.so")
+
+MALA_OK, MALA_ERR_INVALID_ARG, MALA_ERR_UNSUPPORTED, MALA_ERR_WORKSPACE, MALA_ERR_HIP = 0, -1, -2, -3, -4
+PASS_FWD, PASS_BWD, PASS_DECODE = 0, 1, 2
+CNT_LEGAL, CNT_RETAINED, CNT_V_TILES, CNT_SLOTS = 0, 1, 2, 3
+
+EXPORTS = ("mala_geometry", "mala_strerror", "mala_last_error", "mala_fwd",
+           "mala_bwd_workspace_size", "mala_bwd", "mala_decode_workspace_size", "mala_decode")
+
+
+class MalaError(RuntimeError):
+    def __init__(self, status, detail):
+        super().__init__("libmala status %d: %s" % (status, detail))
+        self.status = status
+
+
+class _Geometry(ctypes.Structure):
+    _fields_ = [("block_q", ctypes.c_int32), ("block_k", ctypes.c_int32)]
+
+
+_lib = None
+
+
+def load_library():
+    """Load libmala.so (raises if it has not been built)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise RuntimeError("libmala.so not found at %s; build it with "
+                           "`python paper_2609_32712_amd/build.py`" % LIB_PATH)
+    lib = ctypes.CDLL(LIB_PATH)
+    vp, i, f, sz = ctypes.c_void_p, ctypes.c_int, ctypes.c_float, ctypes.c_size_t
+    lib.mala_geometry.argtypes = [i, i]
+    lib.mala_geometry.restype = _Geometry
+    lib.mala_strerror.argtypes = [i]
+    lib.mala_strerror.restype = ctypes.c_char_p
+    lib.mala_last_error.argtypes = []
+    lib.mala_last_error.restype = ctypes.c_char_p
+    lib.mala_fwd.argtypes = [vp] * 7 + [i] * 7 + [f, f, vp]
+    lib.mala_fwd.restype = i
+    lib.mala_bwd_workspace_size.argtypes = [i] * 6
+    lib.mala_bwd_workspace_size.restype = sz
+    lib.mala_bwd.argtypes = [vp] * 12 + [sz] + [i] * 7 + [f, f, vp]
+    lib.mala_bwd.restype = i
+    lib.mala_decode_workspace_size.argtypes = [i] * 4
+    lib.mala_decode_workspace_size.restype = sz
+    lib.mala_decode.argtypes = [vp] * 7 + [i, vp, sz] + [i] * 5 + [f, f, vp]
+    lib.mala_decode.restype = i
+    _lib = lib
+    return lib
+
+
+def _ptr(t):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(stream):
+    s = torch.cuda.current_stream() if stream is None else stream
+    return ctypes.c_void_p(s.cuda_stream)
+
+
+def _check(status):
+    if status != MALA_OK:
+        lib = load_library()
+        detail = lib.mala_last_error().decode() or lib.mala_strerror(status).decode()
+        raise MalaError(status, detail)
+
+
+def _dev(t, dtype, name, dims):
+    if not isinstance(t, torch.Tensor) or not t.is_cuda:
+        raise TypeError("%s must be a CUDA (HIP) tensor" % name)
+    if t.dtype != dtype or not t.is_contiguous() or t.dim() != dims:
+        raise TypeError("%s must be a contiguous %d-d %s tensor" % (name, dims, dtype))
+    return t
+
+
+# ---------------------------------------------------------------- C names
+def mala_geometry(head_dim, pass_):
+    g = load_library().mala_geometry(head_dim, pass_)
+    return int(g.block_q), int(g.block_k)
+
+
+def mala_bwd_workspace_size(B, Hq, Hkv, Nq, Nk, D):
+    return int(load_library().mala_bwd_workspace_size(B, Hq, Hkv, Nq, Nk, D))
+
+
+def mala_decode_workspace_size(B, Hq, D, num_splits):
+    return int(load_library().mala_decode_workspace_size(B, Hq, D, num_splits))
+
+
+def mala_fwd(q, k, v, o, lse, row_tiles, counters, scale, tau, causal=1, stream=None):
+    _dev(q, torch.bfloat16, "q", 4), _dev(k, torch.bfloat16, "k", 4), _dev(v, torch.bfloat16, "v", 4)
+    _dev(o, torch.float32, "o", 4), _dev(lse, torch.float32, "lse", 3)
+    B, Hq, Nq, D = q.shape
+    Hkv, Nk = k.shape[1], k.shape[2]
+    if tuple(v.shape) != tuple(k.shape) or tuple(o.shape) != tuple(q.shape) or tuple(lse.shape) != (B, Hq, Nq):
+        raise ValueError("inconsistent shapes")
+    if row_tiles is not None:
+        _dev(row_tiles, torch.int32, "row_tiles", 3)
+    if counters is not None:
+        _dev(counters, torch.int64, "counters", 1)
+    _check(load_library().mala_fwd(_ptr(q), _ptr(k), _ptr(v), _ptr(o), _ptr(lse), _ptr(row_tiles),
+                                   _ptr(counters), B, Hq, Hkv, Nq, Nk, D, causal, scale, tau,
+                                   _stream(stream)))
+
+
+def mala_bwd(q, k, v, o, lse, dout, dq, dk, dv, row_tiles, counters, workspace, scale, tau,
+             causal=1, stream=None):
+    for t, n, dt, nd in ((q, "q", torch.bfloat16, 4), (k, "k", torch.bfloat16, 4),
+                         (v, "v", torch.bfloat16, 4), (o, "o", torch.float32, 4),
+                         (lse, "lse", torch.float32, 3), (dout, "dout", torch.bfloat16, 4),
+                         (dq, "dq", torch.float32, 4), (dk, "dk", torch.float32, 4),
+                         (dv, "dv", torch.float32, 4)):
+        _dev(t, dt, n, nd)
+    B, Hq, Nq, D = q.shape
+    Hkv, Nk = k.shape[1], k.shape[2]
+    if (tuple(dq.shape) != tuple(q.shape) or tuple(dout.shape) != tuple(q.shape)
+            or tuple(dk.shape) != tuple(k.shape) or tuple(dv.shape) != tuple(k.shape)):
+        raise ValueError("inconsistent shapes")
+    _check(load_library().mala_bwd(_ptr(q), _ptr(k), _ptr(v), _ptr(o), _ptr(lse), _ptr(dout),
+                                   _ptr(dq), _ptr(dk), _ptr(dv), _ptr(row_tiles), _ptr(counters),
+                                   _ptr(workspace), workspace.numel() * workspace.element_size(),
+                                   B, Hq, Hkv, Nq, Nk, D, causal, scale, tau, _stream(stream)))
+
+
+def mala_decode(q, k_cache, v_cache, o, lse, head_tiles, counters, num_splits, workspace, scale,
+                tau, stream=None):
+    _dev(q, torch.bfloat16, "q", 3), _dev(k_cache, torch.bfloat16, "k_cache", 4)
+    _dev(v_cache, torch.bfloat16, "v_cache", 4), _dev(o, torch.float32, "o", 3)
+    _dev(lse, torch.float32, "lse", 2)
+    B, Hq, D = q.shape
+    Hkv, Nk = k_cache.shape[1], k_cache.shape[2]
+    _check(load_library().mala_decode(_ptr(q), _ptr(k_cache), _ptr(v_cache), _ptr(o), _ptr(lse),
+                                      _ptr(head_tiles), _ptr(counters), num_splits,
+                                      _ptr(workspace),
+                                      workspace.numel() * workspace.element_size(), B, Hq, Hkv,
+                                      Nk, D, scale, tau, _stream(stream)))
+
+
+# ---------------------------------------------------------------- allocating wrappers
+def fwd(q, k, v, scale, tau, stats=True, stream=None):
+    B, Hq, Nq, D = q.shape
+    o = torch.empty((B, Hq, Nq, D), dtype=torch.float32, device=q.device)
+    lse = torch.empty((B, Hq, Nq), dtype=torch.float32, device=q.device)
+    rt = torch.empty((B, Hq, Nq), dtype=torch.int32, device=q.device) if stats else None
+    cnt = torch.empty(4, dtype=torch.int64, device=q.device) if stats else None
+    mala_fwd(q, k, v, o, lse, rt, cnt, scale, tau, stream=stream)
+    return dict(o=o, lse=lse, row_tiles=rt, counters=cnt)
+
+
+def bwd(q, k, v, o, lse, dout, scale, tau, stats=True, workspace=None, stream=None):
+    B, Hq, Nq, D = q.shape
+    Hkv, Nk = k.shape[1], k.shape[2]
+    dq = torch.empty((B, Hq, Nq, D), dtype=torch.float32, device=q.device)
+    dk = torch.empty((B, Hkv, Nk, D), dtype=torch.float32, device=q.device)
+    dv = torch.empty((B, Hkv, Nk, D), dtype=torch.float32, device=q.device)
+    rt = torch.empty((B, Hq, Nq), dtype=torch.int32, device=q.device) if stats else None
+    cnt = torch.empty(4, dtype=torch.int64, device=q.device) if stats else None
+    if workspace is None:
+        n = mala_bwd_workspace_size(B, Hq, Hkv, Nq, Nk, D)
+        workspace = torch.empty(max(n, 16), dtype=torch.uint8, device=q.device)
+    mala_bwd(q, k, v, o, lse, dout, dq, dk, dv, rt, cnt, workspace, scale, tau, stream=stream)
+    return dict(dq=dq, dk=dk, dv=dv, row_tiles=rt, counters=cnt)
+
+
+def decode(q, k_cache, v_cache, scale, tau, num_splits, stats=True, workspace=None, stream=None):
+    B, Hq, D = q.shape
+    o = torch.empty((B, Hq, D), dtype=torch.float32, device=q.device)
+    lse = torch.empty((B, Hq), dtype=torch.float32, device=q.device)
+    ht = torch.empty((B, Hq), dtype=torch.int32, device=q.device) if stats else None
+    cnt = torch.empty(4, dtype=torch.int64, device=q.device) if stats else None
+    if workspace is None:
+        n = mala_decode_workspace_size(B, Hq, D, num_splits)
+        workspace = torch.empty(max(n, 16), dtype=torch.uint8, device=q.device)
+    mala_decode(q, k_cache, v_cache, o, lse, ht, cnt, num_splits, workspace, scale, tau,
+                stream=stream)
+    return dict(o=o, lse=lse, head_tiles=ht, counters=cnt)
+
+
+def default_num_splits(B, Hkv, Nk, num_cus=256, waves_per_cu=8):
+    """Splits that give about num_cus * waves_per_cu decode wavefronts, capped so
+    that each split keeps at least 16 tiles of 32 keys."""
+    tiles = -(-Nk // 32)
+    want = max(1, (num_cus * waves_per_cu) // max(1, B * Hkv))
+    return int(max(1, min(want, tiles // 16 if tiles >= 16 else 1)))

@@ -1,0 +1,200 @@
+// C ABI of libmala.so: argument validation, workspace sizing and kernel launches.
+// Declarations and the contract of every entry point are in include/mala.h.
+#include <math.h>
+#include <stdarg.h>
+#include <stdio.h>
+#include <string.h>
+
+#include "mala.h"
+#include "mala_device.h"
+#include "mala_kernels.h"
+
+namespace {
+
+thread_local char g_err[512] = "";
+
+int fail(int status, const char* fmt, ...) {
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(g_err, sizeof(g_err), fmt, ap);
+  va_end(ap);
+  return status;
+}
+
+int hip_fail(hipError_t e, const char* where) {
+  snprintf(g_err, sizeof(g_err), "%s: %s", where, hipGetErrorString(e));
+  return MALA_ERR_HIP;
+}
+
+size_t round_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
+
+int check_common(int B, int Hq, int Hkv, int Nq, int Nk, int D, int causal, float scale, float tau) {
+  if (B <= 0 || Hq <= 0 || Hkv <= 0 || Nq <= 0 || Nk <= 0)
+    return fail(MALA_ERR_INVALID_ARG, "non-positive size (B, Hq, Hkv, Nq, Nk)");
+  if (Hq % Hkv != 0) return fail(MALA_ERR_INVALID_ARG, "Hq (%d) is not a multiple of Hkv (%d)", Hq, Hkv);
+  if (Nq > Nk) return fail(MALA_ERR_INVALID_ARG, "Nq (%d) > Nk (%d)", Nq, Nk);
+  if (!(tau >= 0.f) || isinf(tau)) return fail(MALA_ERR_INVALID_ARG, "tau must be finite and >= 0");
+  if (!(scale > 0.f) || isinf(scale)) return fail(MALA_ERR_INVALID_ARG, "scale must be finite and > 0");
+  if (causal != 1) return fail(MALA_ERR_UNSUPPORTED, "only causal attention is supported");
+  if (D != 64 && D != 128) return fail(MALA_ERR_UNSUPPORTED, "head_dim %d not in {64, 128}", D);
+  return MALA_OK;
+}
+
+float log2_tau(float tau) { return tau > 0.f ? log2f(tau) : -INFINITY; }
+
+}  // namespace
+
+extern "C" {
+
+mala_geometry_t mala_geometry(int head_dim, int pass) {
+  mala_geometry_t g = {0, 0};
+  if (head_dim != 64 && head_dim != 128) return g;
+  if (pass == MALA_PASS_FWD || pass == MALA_PASS_BWD) {
+    g.block_q = mala::kBq;
+    g.block_k = mala::kBk;
+  } else if (pass == MALA_PASS_DECODE) {
+    g.block_q = 1;
+    g.block_k = mala::kDecBk;
+  }
+  return g;
+}
+
+const char* mala_strerror(int status) {
+  switch (status) {
+    case MALA_OK: return "success";
+    case MALA_ERR_INVALID_ARG: return "invalid argument";
+    case MALA_ERR_UNSUPPORTED: return "unsupported configuration";
+    case MALA_ERR_WORKSPACE: return "workspace missing or too small";
+    case MALA_ERR_HIP: return "HIP runtime error";
+    default: return "unknown status";
+  }
+}
+
+const char* mala_last_error(void) { return g_err; }
+
+int mala_fwd(const void* q, const void* k, const void* v, float* o, float* lse, int32_t* row_tiles,
+             int64_t* counters, int B, int Hq, int Hkv, int Nq, int Nk, int D, int causal,
+             float scale, float tau, void* stream) {
+  g_err[0] = 0;
+  if (!q || !k || !v || !o || !lse) return fail(MALA_ERR_INVALID_ARG, "null q, k, v, o or lse");
+  int st = check_common(B, Hq, Hkv, Nq, Nk, D, causal, scale, tau);
+  if (st) return st;
+  hipStream_t s = (hipStream_t)stream;
+  if (counters) {
+    hipError_t e = mala::launch_fill_zero(counters, 4 * sizeof(int64_t), s);
+    if (e != hipSuccess) return hip_fail(e, "mala_fwd: clearing counters");
+  }
+  mala::FwdParams p;
+  p.q = (const __bf16*)q;
+  p.k = (const __bf16*)k;
+  p.v = (const __bf16*)v;
+  p.o = o;
+  p.lse = lse;
+  p.row_tiles = row_tiles;
+  p.counters = (unsigned long long*)counters;
+  p.B = B; p.Hq = Hq; p.Hkv = Hkv; p.Nq = Nq; p.Nk = Nk;
+  p.scale2 = scale * mala::kLog2e;
+  p.log2tau = log2_tau(tau);
+  p.nqblk = (Nq + mala::kFwdRows - 1) / mala::kFwdRows;
+  hipError_t e = mala::launch_fwd(p, D, s);
+  if (e != hipSuccess) return hip_fail(e, "mala_fwd: kernel launch");
+  return MALA_OK;
+}
+
+size_t mala_bwd_workspace_size(int B, int Hq, int Hkv, int Nq, int Nk, int D) {
+  (void)Hkv; (void)Nk; (void)D;
+  if (B <= 0 || Hq <= 0 || Nq <= 0) return 0;
+  return round_up((size_t)B * Hq * Nq * sizeof(float), 256);
+}
+
+int mala_bwd(const void* q, const void* k, const void* v, const float* o, const float* lse,
+             const void* dout, float* dq, float* dk, float* dv, int32_t* row_tiles,
+             int64_t* counters, void* workspace, size_t workspace_bytes, int B, int Hq, int Hkv,
+             int Nq, int Nk, int D, int causal, float scale, float tau, void* stream) {
+  g_err[0] = 0;
+  if (!q || !k || !v || !o || !lse || !dout || !dq || !dk || !dv)
+    return fail(MALA_ERR_INVALID_ARG, "null tensor argument");
+  int st = check_common(B, Hq, Hkv, Nq, Nk, D, causal, scale, tau);
+  if (st) return st;
+  const size_t need = mala_bwd_workspace_size(B, Hq, Hkv, Nq, Nk, D);
+  if (!workspace || workspace_bytes < need)
+    return fail(MALA_ERR_WORKSPACE, "mala_bwd needs %zu workspace bytes, got %zu", need, workspace_bytes);
+  if (((uintptr_t)workspace) % 16) return fail(MALA_ERR_WORKSPACE, "workspace not 16-byte aligned");
+  hipStream_t s = (hipStream_t)stream;
+  hipError_t e;
+  const long rows = (long)B * Hq * Nq;
+  if ((e = mala::launch_fill_zero(dq, (size_t)rows * D * sizeof(float), s)) != hipSuccess)
+    return hip_fail(e, "mala_bwd: clearing dq");
+  if (row_tiles && (e = mala::launch_fill_zero(row_tiles, (size_t)rows * sizeof(int32_t), s)) != hipSuccess)
+    return hip_fail(e, "mala_bwd: clearing row_tiles");
+  if (counters && (e = mala::launch_fill_zero(counters, 4 * sizeof(int64_t), s)) != hipSuccess)
+    return hip_fail(e, "mala_bwd: clearing counters");
+  float* dvec = (float*)workspace;
+  if ((e = mala::launch_bwd_preprocess(o, (const __bf16*)dout, dvec, rows, D, s)) != hipSuccess)
+    return hip_fail(e, "mala_bwd: preprocess launch");
+  mala::BwdParams p;
+  p.q = (const __bf16*)q;
+  p.k = (const __bf16*)k;
+  p.v = (const __bf16*)v;
+  p.dout = (const __bf16*)dout;
+  p.lse = lse;
+  p.dvec = dvec;
+  p.dq = dq; p.dk = dk; p.dv = dv;
+  p.row_tiles = row_tiles;
+  p.counters = (unsigned long long*)counters;
+  p.B = B; p.Hq = Hq; p.Hkv = Hkv; p.Nq = Nq; p.Nk = Nk;
+  p.scale = scale;
+  p.scale2 = scale * mala::kLog2e;
+  p.log2tau = log2_tau(tau);
+  p.nkblk = (Nk + mala::kBwdKeys - 1) / mala::kBwdKeys;
+  if ((e = mala::launch_bwd(p, D, s)) != hipSuccess) return hip_fail(e, "mala_bwd: kernel launch");
+  return MALA_OK;
+}
+
+size_t mala_decode_workspace_size(int B, int Hq, int D, int num_splits) {
+  if (B <= 0 || Hq <= 0 || num_splits <= 0 || (D != 64 && D != 128)) return 0;
+  return round_up((size_t)B * Hq * num_splits * (D + mala::kDecStride) * sizeof(float), 256);
+}
+
+int mala_decode(const void* q, const void* k_cache, const void* v_cache, float* o, float* lse,
+                int32_t* head_tiles, int64_t* counters, int num_splits, void* workspace,
+                size_t workspace_bytes, int B, int Hq, int Hkv, int Nk, int D, float scale,
+                float tau, void* stream) {
+  g_err[0] = 0;
+  if (!q || !k_cache || !v_cache || !o || !lse)
+    return fail(MALA_ERR_INVALID_ARG, "null q, k_cache, v_cache, o or lse");
+  int st = check_common(B, Hq, Hkv, 1, Nk, D, 1, scale, tau);
+  if (st) return st;
+  if (num_splits < 1) return fail(MALA_ERR_INVALID_ARG, "num_splits must be >= 1");
+  if (Hq / Hkv > 16)
+    return fail(MALA_ERR_UNSUPPORTED, "decode supports at most 16 query heads per KV head");
+  const size_t need = mala_decode_workspace_size(B, Hq, D, num_splits);
+  if (!workspace || workspace_bytes < need)
+    return fail(MALA_ERR_WORKSPACE, "mala_decode needs %zu workspace bytes, got %zu", need,
+                workspace_bytes);
+  if (((uintptr_t)workspace) % 16) return fail(MALA_ERR_WORKSPACE, "workspace not 16-byte aligned");
+  hipStream_t s = (hipStream_t)stream;
+  hipError_t e;
+  if (counters && (e = mala::launch_fill_zero(counters, 4 * sizeof(int64_t), s)) != hipSuccess)
+    return hip_fail(e, "mala_decode: clearing counters");
+  const int T = (Nk + mala::kDecBk - 1) / mala::kDecBk;
+  mala::DecParams p;
+  p.q = (const __bf16*)q;
+  p.k = (const __bf16*)k_cache;
+  p.v = (const __bf16*)v_cache;
+  p.part = (float*)workspace;
+  p.counters = (unsigned long long*)counters;
+  p.B = B; p.Hq = Hq; p.Hkv = Hkv; p.Nk = Nk;
+  p.S = num_splits;
+  p.T = T;
+  p.tps = (T + num_splits - 1) / num_splits;
+  p.scale2 = scale * mala::kLog2e;
+  p.thr2 = log2_tau(tau) - log2f((float)Nk);
+  if ((e = mala::launch_decode(p, D, s)) != hipSuccess) return hip_fail(e, "mala_decode: split launch");
+  if ((e = mala::launch_decode_combine((float*)workspace, o, lse, head_tiles, p.counters, B * Hq,
+                                       num_splits, D, s)) != hipSuccess)
+    return hip_fail(e, "mala_decode: combine launch");
+  return MALA_OK;
+}
+
+}  // extern "C"

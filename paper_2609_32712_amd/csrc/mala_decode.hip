@@ -1,0 +1,210 @@
+// MALA split-KV decode for gfx950 (Fused Execution section and its appendix:
+// each split tests its tiles against its own partial normalizer, with L = Nk).
+//
+// One wavefront (= one workgroup) owns one split of one (batch, KV head) and
+// serves all query heads of the GQA group at once, so the K and V bytes of a
+// tile are read once per group.  Decode is HBM-bound: K is always read (score
+// discovery), V only when at least one head of the group retains the tile.
+//
+// Per 32-key tile, in descending order inside the split:
+//   S^T = K_t Q^T     2 x 4 (D = 128) MFMAs 16x16x32, K loaded straight from HBM
+//                     into the A operand; lane (g, col) holds query head col and
+//                     8 of the 32 keys; the next tile's K is prefetched meanwhile
+//   test              per head against that head's running (m, l) of the split
+//   retained (any)    V tile -> LDS; per head P = exp2(S - m_new) (0 for heads that
+//                     skip); O^T += V^T P^T with V^T through ds_read_b64_tr_b16.
+// Partials (O / l, lse, count) go to the workspace; a second kernel merges the
+// splits with the normalizer-aware (log-sum-exp weighted) reduction.
+#include "mala_device.h"
+#include "mala_kernels.h"
+
+namespace mala {
+
+template <int D>
+__global__ __launch_bounds__(64) void mala_decode_split_kernel(DecParams p) {
+  constexpr int KS = D / 32;   // k-steps of 32 over head_dim
+  constexpr int NDB = D / 16;  // 16-row blocks of O^T
+  constexpr int LD = D + 8;
+  __shared__ bf16 Vs[kDecBk * LD];
+
+  const int lane = threadIdx.x, g = lane >> 4, col = lane & 15;
+  const int s = blockIdx.x % p.S;
+  const int bhk = blockIdx.x / p.S;
+  const int b = bhk / p.Hkv, hkv = bhk % p.Hkv, grp = p.Hq / p.Hkv;
+  const int t_lo = s * p.tps, t_hi = min(p.T, t_lo + p.tps);
+  const bool head_valid = col < grp;
+  const int hq = hkv * grp + col;
+
+  bf16x8 qreg[KS];
+#pragma unroll
+  for (int kk = 0; kk < KS; ++kk)
+    qreg[kk] = head_valid ? load8(p.q + ((long)b * p.Hq + hq) * D + 32 * kk + 8 * g) : zero8();
+
+  const bf16* Kp = p.k + (long)bhk * p.Nk * D;
+  const bf16* Vp = p.v + (long)bhk * p.Nk * D;
+
+  float m = kNegInf, l = 0.f;
+  f32x4 acc[NDB];
+#pragma unroll
+  for (int db = 0; db < NDB; ++db) acc[db] = f32x4{0.f, 0.f, 0.f, 0.f};
+  int cnt = 0;
+  unsigned vloads = 0;
+
+  // K operand of tile t: rows kb + col (block 0) and kb + 16 + col (block 1)
+  bf16x8 ka[KS], kb1[KS];
+  auto load_k = [&](int t) {
+    const long k0 = (long)t * kDecBk + col, k1 = k0 + 16;
+#pragma unroll
+    for (int kk = 0; kk < KS; ++kk) {
+      ka[kk] = k0 < p.Nk ? load8(Kp + k0 * D + 32 * kk + 8 * g) : zero8();
+      kb1[kk] = k1 < p.Nk ? load8(Kp + k1 * D + 32 * kk + 8 * g) : zero8();
+    }
+  };
+  if (t_hi > t_lo) load_k(t_hi - 1);
+
+  for (int t = t_hi - 1; t >= t_lo; --t) {
+    f32x4 s0 = {0.f, 0.f, 0.f, 0.f}, s1 = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int kk = 0; kk < KS; ++kk) {
+      s0 = mfma16(ka[kk], qreg[kk], s0);
+      s1 = mfma16(kb1[kk], qreg[kk], s1);
+    }
+    if (t > t_lo) load_k(t - 1);   // prefetch the next (lower) tile's K
+
+    const long kb = (long)t * kDecBk;
+    float sv[8];
+    float mt = kNegInf;
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      float x0 = s0[r] * p.scale2, x1 = s1[r] * p.scale2;
+      if (kb + 4 * g + r >= p.Nk) x0 = kNegInf;
+      if (kb + 16 + 4 * g + r >= p.Nk) x1 = kNegInf;
+      sv[r] = x0;
+      sv[4 + r] = x1;
+      mt = fmaxf(mt, fmaxf(x0, x1));
+    }
+    mt = fmaxf(mt, __shfl_xor(mt, 16));
+    mt = fmaxf(mt, __shfl_xor(mt, 32));
+    const bool demand = head_valid && (l == 0.f || (mt - m - log2f(l) >= p.thr2));
+    if (!wave_any(demand)) continue;
+
+    // V tile -> LDS (rows beyond Nk are zero)
+    __syncthreads();
+    for (int ch = lane; ch < kDecBk * D / 8; ch += 64) {
+      const int row = ch / (D / 8), c8 = (ch % (D / 8)) * 8;
+      const long kk = kb + row;
+      store8(Vs + row * LD + c8, kk < p.Nk ? load8(Vp + kk * D + c8) : zero8());
+    }
+    __syncthreads();
+    ++vloads;
+
+    float alpha = 1.f, m_new = m;
+    if (demand) {
+      m_new = fmaxf(m, mt);
+      alpha = exp2f(m - m_new);
+    }
+    float ps = 0.f;
+#pragma unroll
+    for (int r = 0; r < 8; ++r) {
+      const float e = demand ? exp2f(sv[r] - m_new) : 0.f;
+      sv[r] = e;
+      ps += e;
+    }
+    ps += __shfl_xor(ps, 16);
+    ps += __shfl_xor(ps, 32);
+    if (demand) {
+      l = alpha * l + ps;
+      m = m_new;
+      ++cnt;
+    }
+    bf16x8 ph, pl;
+    split_bf16x8(sv, ph, pl);
+#pragma unroll
+    for (int db = 0; db < NDB; ++db) {
+      const bf16* vr = Vs + (4 * g + (col >> 2)) * LD + 16 * db + 4 * (col & 3);
+      const bf16x8 a = cat(lds_read_tr(vr), lds_read_tr(vr + 16 * LD));
+      acc[db] = mfma16(a, ph, acc[db] * alpha);
+      acc[db] = mfma16(a, pl, acc[db]);
+    }
+  }
+
+  // partial of this split: O / l, lse (natural log) and the retained-tile count
+  float* pp = p.part + (((long)b * p.Hq + hq) * p.S + s) * (D + kDecStride);
+  if (head_valid) {
+    const float inv = l > 0.f ? 1.f / l : 0.f;
+#pragma unroll
+    for (int db = 0; db < NDB; ++db)
+      *reinterpret_cast<f32x4*>(pp + 16 * db + 4 * g) = acc[db] * inv;
+    if (g == 0) {
+      pp[D] = l > 0.f ? (m + log2f(l)) * kLn2 : kNegInf;
+      pp[D + 1] = __int_as_float(cnt);
+    }
+  }
+  if (p.counters) {
+    if (head_valid && g == 0 && cnt) {
+      atomicAdd(&p.counters[1], (unsigned long long)cnt);
+      atomicAdd(&p.counters[3], (unsigned long long)cnt * kDecBk);
+    }
+    if (lane == 0) {
+      atomicAdd(&p.counters[0], (unsigned long long)(t_hi > t_lo ? t_hi - t_lo : 0) * grp);
+      if (vloads) atomicAdd(&p.counters[2], (unsigned long long)vloads);
+    }
+  }
+}
+
+// Normalizer-aware merge of the split partials: lse = logsumexp_s lse_s,
+// o = sum_s exp(lse_s - lse) o_s.  One workgroup per (batch, query head).
+template <int D>
+__global__ __launch_bounds__(64) void mala_decode_combine_kernel(const float* part, float* o,
+                                                                 float* lse, int32_t* head_tiles,
+                                                                 int S) {
+  const long bh = blockIdx.x;
+  const float* pp = part + bh * S * (D + kDecStride);
+  float mx = kNegInf;
+  for (int s = 0; s < S; ++s) mx = fmaxf(mx, pp[(long)s * (D + kDecStride) + D]);
+  float z = 0.f;
+  int cnt = 0;
+  for (int s = 0; s < S; ++s) {
+    const float ls = pp[(long)s * (D + kDecStride) + D];
+    if (ls != kNegInf) z += expf(ls - mx);
+    cnt += __float_as_int(pp[(long)s * (D + kDecStride) + D + 1]);
+  }
+  const float L = mx + logf(z);
+  for (int d = threadIdx.x; d < D; d += 64) {
+    float acc = 0.f;
+    for (int s = 0; s < S; ++s) {
+      const float ls = pp[(long)s * (D + kDecStride) + D];
+      if (ls != kNegInf) acc += expf(ls - L) * pp[(long)s * (D + kDecStride) + d];
+    }
+    o[bh * D + d] = acc;
+  }
+  if (threadIdx.x == 0) {
+    lse[bh] = L;
+    if (head_tiles) head_tiles[bh] = cnt;
+  }
+}
+
+hipError_t launch_decode(const DecParams& p, int D, hipStream_t st) {
+  dim3 grid((unsigned)p.B * p.Hkv * p.S), block(64);
+  if (D == 128)
+    hipLaunchKernelGGL(mala_decode_split_kernel<128>, grid, block, 0, st, p);
+  else
+    hipLaunchKernelGGL(mala_decode_split_kernel<64>, grid, block, 0, st, p);
+  return hipGetLastError();
+}
+
+hipError_t launch_decode_combine(const float* part, float* o, float* lse, int32_t* head_tiles,
+                                 unsigned long long* counters, int BH, int S, int D,
+                                 hipStream_t st) {
+  (void)counters;
+  dim3 grid((unsigned)BH), block(64);
+  if (D == 128)
+    hipLaunchKernelGGL(mala_decode_combine_kernel<128>, grid, block, 0, st, part, o, lse,
+                       head_tiles, S);
+  else
+    hipLaunchKernelGGL(mala_decode_combine_kernel<64>, grid, block, 0, st, part, o, lse,
+                       head_tiles, S);
+  return hipGetLastError();
+}
+
+}  // namespace mala

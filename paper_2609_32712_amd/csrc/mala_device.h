@@ -1,0 +1,96 @@
+// Device-side building blocks shared by the MALA kernels (gfx950 / CDNA4 only).
+//
+// Lane layouts used throughout (wave64; h = lane / 32, c = lane % 32):
+//   v_mfma_f32_32x32x16_bf16  C[32x32] += A[32x16] * B[16x32]
+//     A: lane holds row c, k = 8h .. 8h+7          (8 bf16)
+//     B: lane holds column c, k = 8h .. 8h+7       (8 bf16)
+//     C: lane holds column c, rows 8*(r/4) + 4h + r%4, r = 0..15
+//   v_mfma_f32_16x16x32_bf16  C[16x16] += A[16x32] * B[32x16]   (g = lane / 16)
+//     A: lane holds row lane%16, k = 8g .. 8g+7;  B: column lane%16, same k;
+//     C: lane holds column lane%16, rows 4g + r, r = 0..3
+//   ds_read_b64_tr_b16: within each group of 16 lanes, lane t receives element
+//     t%4 of the 8-byte chunks addressed by lanes 4n + t/4 (n = 0..3).  If lane i
+//     of the group addresses row (R + i/4), columns (C0 + 4*(i%4)) .. +3 of a
+//     row-major bf16 tile, lane t receives the column C0 + t of rows R .. R+3,
+//     i.e. a 4-deep slice along the row dimension: the operand of an MFMA whose
+//     contraction runs along the tile's rows.
+// Because the contraction index of an MFMA may be permuted freely (as long as A
+// and B agree), the probabilities of a 32x32 C tile are fed back as an operand
+// without any register shuffle: k-step ks uses C registers 8ks .. 8ks+7, which
+// hold the rows {16ks + 4h + 0..3} and {16ks + 8 + 4h + 0..3}.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace mala {
+
+typedef __bf16 bf16;
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+
+constexpr float kLog2e = 1.4426950408889634f;
+constexpr float kLn2 = 0.6931471805599453f;
+constexpr float kNegInf = -__builtin_huge_valf();
+
+__device__ __forceinline__ f32x16 mfma32(bf16x8 a, bf16x8 b, f32x16 c) {
+  return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
+}
+__device__ __forceinline__ f32x4 mfma16(bf16x8 a, bf16x8 b, f32x4 c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
+}
+
+// Transposed 4x16 LDS read (see the header comment).
+__device__ __forceinline__ bf16x4 lds_read_tr(const bf16* p) {
+  return __builtin_amdgcn_ds_read_tr16_b64_v4bf16(
+      (__attribute__((address_space(3))) bf16x4*)(p));
+}
+__device__ __forceinline__ bf16x8 cat(bf16x4 a, bf16x4 b) {
+  return bf16x8{a[0], a[1], a[2], a[3], b[0], b[1], b[2], b[3]};
+}
+
+// Reductions between lane l and lane l ^ 32 (the two halves of a 32x32 C column).
+__device__ __forceinline__ float halves_max(float x) {
+  auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+__device__ __forceinline__ float halves_sum(float x) {
+  auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+
+__device__ __forceinline__ bool wave_any(bool p) { return __builtin_amdgcn_ballot_w64(p) != 0; }
+
+__device__ __forceinline__ bf16x8 zero8() {
+  bf16x8 z;
+#pragma unroll
+  for (int i = 0; i < 8; ++i) z[i] = (bf16)0.0f;
+  return z;
+}
+
+__device__ __forceinline__ bf16x8 load8(const bf16* p) { return *reinterpret_cast<const bf16x8*>(p); }
+__device__ __forceinline__ void store8(bf16* p, bf16x8 v) { *reinterpret_cast<bf16x8*>(p) = v; }
+
+// fp32 -> bf16 round-to-nearest-even for 8 values.
+__device__ __forceinline__ bf16x8 to_bf16x8(const float* x) {
+  bf16x8 r;
+#pragma unroll
+  for (int i = 0; i < 8; ++i) r[i] = (bf16)x[i];
+  return r;
+}
+
+// Two-term bf16 split of fp32 values: x ~= hi + lo with |x - hi - lo| <= 2^-16 |x|.
+// The post-score products (P V, P^T dO, dS^T Q, dS K) run as two MFMAs, one per
+// term, so the probabilities keep ~16 significant bits instead of bf16's 8.
+__device__ __forceinline__ void split_bf16x8(const float* x, bf16x8& hi, bf16x8& lo) {
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    const bf16 t = (bf16)x[i];
+    hi[i] = t;
+    lo[i] = (bf16)(x[i] - (float)t);
+  }
+}
+
+}  // namespace mala

@@ -1,0 +1,199 @@
+// MALA forward (Algorithm 1) for gfx950.
+//
+// One workgroup = 4 wavefronts = 128 consecutive query rows of one (batch, query
+// head); each wavefront owns 32 rows, which is the decision tile's B_q.  K and V
+// are staged through LDS 64 keys at a time, from the workgroup's highest legal
+// key down to key 0 (the diagonal-first traversal of the Online Sparse Softmax
+// paragraph); inside a stage each wavefront visits its two 32-key decision tiles
+// high half first, so every wavefront sees its tiles in strictly descending order.
+//
+// Per decision tile (32 keys x the wavefront's 32 rows):
+//   S^T = K_j Q_i^T       8 (D = 128) bf16 MFMAs 32x32x16, fp32 accumulate; each
+//                         lane holds one query row and 16 of the 32 keys, so the
+//                         row max is 15 in-lane max + one permlane32 swap;
+//   online test           skip iff every row with a legal key has
+//                         rowmax - m - log2(l) < log2(tau) - log2(L_q) (base-2 units,
+//                         equivalent to the natural-log test), rows with l == 0
+//                         always retain; one ballot makes the branch wave-uniform;
+//   retained path         m, l, rescale of O (only if some row's max moved),
+//                         P = exp2(S - m) split into two bf16 terms in place,
+//                         O^T += V^T P^T (2 x 8 MFMAs, V^T operand through
+//                         ds_read_b64_tr_b16).
+// A skipped tile costs its QK MFMAs, one max reduction and one compare.
+#include "mala_device.h"
+#include "mala_kernels.h"
+
+namespace mala {
+
+template <int D>
+__global__ __launch_bounds__(256) void mala_fwd_kernel(FwdParams p) {
+  constexpr int KS = D / 16;    // k-steps of the QK product
+  constexpr int DB = D / 32;    // 32-wide output column blocks
+  constexpr int LD = D + 8;     // LDS row stride in bf16 (16-byte pad)
+  __shared__ bf16 Ks[kFwdStage * LD];
+  __shared__ bf16 Vs[kFwdStage * LD];
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int h = lane >> 5, c = lane & 31, G = lane >> 4, t16 = lane & 15;
+  const int BH = p.B * p.Hq;
+  const int bh = blockIdx.x % BH;
+  const int qblk = p.nqblk - 1 - (int)(blockIdx.x / BH);   // longest rows first
+  const int b = bh / p.Hq, hq = bh % p.Hq, hkv = hq / (p.Hq / p.Hkv);
+  const long off = (long)p.Nk - p.Nq;
+  const int q0w = qblk * kFwdRows + wave * kBq;
+  const int qrow = q0w + c;
+  const bool row_valid = qrow < p.Nq;
+
+  const bf16* Qp = p.q + (long)bh * p.Nq * D;
+  const bf16* Kp = p.k + (long)(b * p.Hkv + hkv) * p.Nk * D;
+  const bf16* Vp = p.v + (long)(b * p.Hkv + hkv) * p.Nk * D;
+
+  // Q^T as the B operand: lane (h, c) holds Q[qrow][16kk + 8h .. +7]
+  bf16x8 qreg[KS];
+#pragma unroll
+  for (int kk = 0; kk < KS; ++kk)
+    qreg[kk] = row_valid ? load8(Qp + (long)qrow * D + 16 * kk + 8 * h) : zero8();
+
+  float m = kNegInf, l = 0.f;
+  f32x16 acc[DB];
+#pragma unroll
+  for (int db = 0; db < DB; ++db)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) acc[db][r] = 0.f;
+  int cnt = 0;
+  const float thr = p.log2tau - log2f((float)(qrow + 1 + off));   // log2(tau / L_q)
+
+  const int qlast_w = min(q0w + kBq - 1, p.Nq - 1);
+  const int jdiag = (q0w < p.Nq) ? (int)((qlast_w + off) / kBk) : -1;
+  const int nvalid = max(0, min(kBq, p.Nq - q0w));
+  const int qlast_g = min(qblk * kFwdRows + kFwdRows - 1, p.Nq - 1);
+  const int ttop = (int)((qlast_g + off) / kFwdStage);
+  unsigned n_legal = 0, n_ret = 0;
+
+  for (int t = ttop; t >= 0; --t) {
+    __syncthreads();
+    constexpr int CH = kFwdStage * D / 8;
+#pragma unroll
+    for (int ch = tid; ch < CH; ch += 256) {
+      const int row = ch / (D / 8), col = (ch % (D / 8)) * 8;
+      const long key = (long)t * kFwdStage + row;
+      bf16x8 kv = zero8(), vv = zero8();
+      if (key < p.Nk) {
+        kv = load8(Kp + key * D + col);
+        vv = load8(Vp + key * D + col);
+      }
+      store8(Ks + row * LD + col, kv);
+      store8(Vs + row * LD + col, vv);
+    }
+    __syncthreads();
+
+#pragma unroll
+    for (int sub = 1; sub >= 0; --sub) {
+      const int j = 2 * t + sub;
+      if (j > jdiag) continue;            // above this wavefront's diagonal
+      const long kb = (long)j * kBk;
+      ++n_legal;
+
+      // S^T[key][q] = K_j Q^T
+      f32x16 s;
+#pragma unroll
+      for (int r = 0; r < 16; ++r) s[r] = 0.f;
+      const bf16* kr = Ks + (sub * kBk + c) * LD + 8 * h;
+#pragma unroll
+      for (int kk = 0; kk < KS; ++kk) s = mfma32(load8(kr + 16 * kk), qreg[kk], s);
+
+      const bool need_mask = (kb + kBk - 1 > (long)q0w + off) || (q0w + kBq > p.Nq);
+      float sv[16];
+      float mt = kNegInf;
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        float x = s[r] * p.scale2;
+        if (need_mask) {
+          const long key = kb + 8 * (r >> 2) + 4 * h + (r & 3);
+          if (!row_valid || key > qrow + off) x = kNegInf;
+        }
+        sv[r] = x;
+        mt = fmaxf(mt, x);
+      }
+      mt = halves_max(mt);
+
+      // the online test (rows with no legal key in the tile do not vote)
+      const bool voter = row_valid && (kb <= qrow + off);
+      const bool demand = voter && (l == 0.f || (mt - m - log2f(l) >= thr));
+      if (!wave_any(demand)) continue;    // skipped: m, l and O unchanged
+      ++n_ret;
+      cnt += voter ? 1 : 0;
+
+      const float m_new = fmaxf(m, mt);
+      const float alpha = (m_new == kNegInf) ? 1.f : exp2f(m - m_new);
+      float ps = 0.f;
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const float e = (sv[r] == kNegInf) ? 0.f : exp2f(sv[r] - m_new);
+        sv[r] = e;
+        ps += e;
+      }
+      ps = halves_sum(ps);
+      l = alpha * l + ps;
+      m = m_new;
+      if (wave_any(alpha != 1.f)) {
+#pragma unroll
+        for (int db = 0; db < DB; ++db)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) acc[db][r] *= alpha;
+      }
+      bf16x8 ph[2], pl[2];
+      split_bf16x8(sv, ph[0], pl[0]);
+      split_bf16x8(sv + 8, ph[1], pl[1]);
+      // O^T[d][q] += V^T[d][key] P^T[key][q]; V^T rows through transposed LDS reads
+#pragma unroll
+      for (int db = 0; db < DB; ++db) {
+#pragma unroll
+        for (int ks = 0; ks < 2; ++ks) {
+          const bf16* vr = Vs + (sub * kBk + 16 * ks + 4 * h + (t16 >> 2)) * LD + 32 * db +
+                           16 * (G & 1) + 4 * (t16 & 3);
+          const bf16x8 a = cat(lds_read_tr(vr), lds_read_tr(vr + 8 * LD));
+          acc[db] = mfma32(a, ph[ks], acc[db]);
+          acc[db] = mfma32(a, pl[ks], acc[db]);
+        }
+      }
+    }
+  }
+
+  // epilogue: O <- O / l, LSE = (m + log2 l) * ln 2
+  if (row_valid) {
+    const float inv = 1.f / l;
+    float* op = p.o + ((long)bh * p.Nq + qrow) * D;
+#pragma unroll
+    for (int db = 0; db < DB; ++db)
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        f32x4 v4 = {acc[db][4 * g] * inv, acc[db][4 * g + 1] * inv, acc[db][4 * g + 2] * inv,
+                    acc[db][4 * g + 3] * inv};
+        *reinterpret_cast<f32x4*>(op + 32 * db + 8 * g + 4 * h) = v4;
+      }
+    if (h == 0) {
+      p.lse[(long)bh * p.Nq + qrow] = (m + log2f(l)) * kLn2;
+      if (p.row_tiles) p.row_tiles[(long)bh * p.Nq + qrow] = cnt;
+    }
+  }
+  if (p.counters) {
+    if (lane == 0 && n_legal) {
+      atomicAdd(&p.counters[0], (unsigned long long)n_legal);
+      atomicAdd(&p.counters[1], (unsigned long long)n_ret);
+      atomicAdd(&p.counters[3], (unsigned long long)n_ret * kBk * nvalid);
+    }
+    if (tid == 0) atomicAdd(&p.counters[2], (unsigned long long)(ttop + 1) * (kFwdStage / kBk));
+  }
+}
+
+hipError_t launch_fwd(const FwdParams& p, int D, hipStream_t st) {
+  dim3 grid((unsigned)p.nqblk * p.B * p.Hq), block(256);
+  if (D == 128)
+    hipLaunchKernelGGL(mala_fwd_kernel<128>, grid, block, 0, st, p);
+  else
+    hipLaunchKernelGGL(mala_fwd_kernel<64>, grid, block, 0, st, p);
+  return hipGetLastError();
+}
+
+}  // namespace mala

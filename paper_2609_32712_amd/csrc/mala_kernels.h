@@ -1,0 +1,71 @@
+// Kernel parameter blocks and host-side launchers of the MALA kernels.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace mala {
+
+// Decision geometry (shared by forward and backward so that the backward
+// support nests inside the forward support; decode uses 1 x kDecBk).
+constexpr int kBq = 32;      // query rows per decision tile = rows of one wavefront
+constexpr int kBk = 32;      // keys per decision tile
+constexpr int kDecBk = 32;   // keys per decode decision tile
+
+constexpr int kFwdWaves = 4;                 // wavefronts per forward workgroup
+constexpr int kFwdRows = kFwdWaves * kBq;    // 128 query rows per workgroup
+constexpr int kFwdStage = 64;                // keys per K/V stage in LDS
+constexpr int kBwdKeys = 128;                // keys per backward workgroup (4 waves x kBk)
+constexpr int kDecStride = 4;                // extra floats per decode partial (lse, count, pad)
+
+struct FwdParams {
+  const __bf16* q;
+  const __bf16* k;
+  const __bf16* v;
+  float* o;
+  float* lse;
+  int32_t* row_tiles;
+  unsigned long long* counters;
+  int B, Hq, Hkv, Nq, Nk;
+  float scale2;    // softmax scale * log2(e): scores are kept in base-2 units
+  float log2tau;   // log2(tau); -inf for tau == 0
+  int nqblk;       // ceil(Nq / kFwdRows)
+};
+
+struct BwdParams {
+  const __bf16* q;
+  const __bf16* k;
+  const __bf16* v;
+  const __bf16* dout;
+  const float* lse;
+  const float* dvec;   // D_q = rowsum(O_q * dO_q)
+  float* dq;
+  float* dk;
+  float* dv;
+  int32_t* row_tiles;
+  unsigned long long* counters;
+  int B, Hq, Hkv, Nq, Nk;
+  float scale, scale2, log2tau;
+  int nkblk;           // ceil(Nk / kBwdKeys)
+};
+
+struct DecParams {
+  const __bf16* q;
+  const __bf16* k;
+  const __bf16* v;
+  float* part;         // [B, Hq, S, D + kDecStride]
+  unsigned long long* counters;
+  int B, Hq, Hkv, Nk, S, T, tps;
+  float scale2, thr2;  // thr2 = log2(tau) - log2(Nk)
+};
+
+hipError_t launch_fill_zero(void* ptr, size_t bytes, hipStream_t st);
+hipError_t launch_fwd(const FwdParams& p, int D, hipStream_t st);
+hipError_t launch_bwd_preprocess(const float* o, const __bf16* dout, float* dvec, long rows, int D,
+                                 hipStream_t st);
+hipError_t launch_bwd(const BwdParams& p, int D, hipStream_t st);
+hipError_t launch_decode(const DecParams& p, int D, hipStream_t st);
+hipError_t launch_decode_combine(const float* part, float* o, float* lse, int32_t* head_tiles,
+                                 unsigned long long* counters, int BH, int S, int D,
+                                 hipStream_t st);
+
+}  // namespace mala

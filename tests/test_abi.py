@@ -1,0 +1,109 @@
+"""The C ABI without a GPU: the library loads, exports every function that
+include/mala.h declares, reports its geometry and workspace sizes, and rejects
+invalid arguments synchronously (before any HIP call)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+import paper_2609_32712_amd as mala
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "mala.h")
+
+
+def declared_functions():
+    src = open(HEADER).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"^\s*(?:const\s+)?[\w]+\*?\s+\**(mala_\w+)\s*\(", src, flags=re.M)))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(mala.LIB_PATH):
+        pytest.fail("libmala.so is not built (run __graft_entry__.build())")
+    return mala.load_library()
+
+
+def test_header_declares_the_boundary():
+    names = declared_functions()
+    for n in ("mala_fwd", "mala_bwd", "mala_decode", "mala_geometry", "mala_strerror",
+              "mala_last_error", "mala_bwd_workspace_size", "mala_decode_workspace_size"):
+        assert n in names
+    assert set(names) == set(mala.EXPORTS)
+
+
+def test_library_exports_every_declared_symbol(lib):
+    for n in declared_functions():
+        assert hasattr(lib, n), n
+
+
+def test_geometry(lib):
+    for d in (64, 128):
+        assert mala.mala_geometry(d, mala.PASS_FWD) == mala.mala_geometry(d, mala.PASS_BWD)
+        bq, bk = mala.mala_geometry(d, mala.PASS_FWD)
+        assert bq > 0 and bk > 0 and bk % bq == 0
+        assert mala.mala_geometry(d, mala.PASS_DECODE)[0] == 1
+    assert mala.mala_geometry(96, mala.PASS_FWD) == (0, 0)
+    assert mala.mala_geometry(128, 7) == (0, 0)
+
+
+def test_workspace_sizes(lib):
+    assert mala.mala_bwd_workspace_size(1, 8, 2, 1000, 1000, 128) >= 4 * 8 * 1000
+    assert mala.mala_bwd_workspace_size(0, 8, 2, 1000, 1000, 128) == 0
+    assert mala.mala_decode_workspace_size(16, 32, 128, 8) >= 16 * 32 * 8 * 130 * 4
+    assert mala.mala_decode_workspace_size(16, 32, 96, 8) == 0
+
+
+def _fwd(lib, **kw):
+    a = dict(q=16, k=16, v=16, o=16, lse=16, B=1, Hq=2, Hkv=1, Nq=64, Nk=64, D=128, causal=1,
+             scale=0.1, tau=1e-3)
+    a.update(kw)
+    P = lambda x: None if x is None else ctypes.c_void_p(x)
+    return lib.mala_fwd(P(a["q"]), P(a["k"]), P(a["v"]), P(a["o"]), P(a["lse"]), None, None,
+                        a["B"], a["Hq"], a["Hkv"], a["Nq"], a["Nk"], a["D"], a["causal"],
+                        a["scale"], a["tau"], None)
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(q=None), mala.MALA_ERR_INVALID_ARG),
+    (dict(lse=None), mala.MALA_ERR_INVALID_ARG),
+    (dict(B=0), mala.MALA_ERR_INVALID_ARG),
+    (dict(Hq=3, Hkv=2), mala.MALA_ERR_INVALID_ARG),
+    (dict(Nq=65), mala.MALA_ERR_INVALID_ARG),
+    (dict(tau=-1e-3), mala.MALA_ERR_INVALID_ARG),
+    (dict(tau=float("nan")), mala.MALA_ERR_INVALID_ARG),
+    (dict(tau=float("inf")), mala.MALA_ERR_INVALID_ARG),
+    (dict(scale=0.0), mala.MALA_ERR_INVALID_ARG),
+    (dict(scale=float("inf")), mala.MALA_ERR_INVALID_ARG),
+    (dict(D=96), mala.MALA_ERR_UNSUPPORTED),
+    (dict(causal=0), mala.MALA_ERR_UNSUPPORTED),
+])
+def test_fwd_rejects_invalid_arguments(lib, kw, status):
+    assert _fwd(lib, **kw) == status
+    assert lib.mala_last_error().decode() != ""
+    assert lib.mala_strerror(status).decode() not in ("", "unknown status")
+
+
+def test_bwd_and_decode_reject_missing_workspace(lib):
+    P = ctypes.c_void_p
+    st = lib.mala_bwd(*([P(16)] * 9), None, None, None, 0, 1, 2, 1, 64, 64, 128, 1, 0.1, 0.0, None)
+    assert st == mala.MALA_ERR_WORKSPACE
+    st = lib.mala_bwd(*([P(16)] * 9), None, None, P(16), 8, 1, 2, 1, 64, 64, 128, 1, 0.1, 0.0, None)
+    assert st == mala.MALA_ERR_WORKSPACE
+    st = lib.mala_decode(*([P(16)] * 5), None, None, 4, None, 0, 1, 2, 1, 64, 128, 0.1, 0.0, None)
+    assert st == mala.MALA_ERR_WORKSPACE
+    st = lib.mala_decode(*([P(16)] * 5), None, None, 0, P(16), 1 << 20, 1, 2, 1, 64, 128, 0.1, 0.0,
+                         None)
+    assert st == mala.MALA_ERR_INVALID_ARG
+    st = lib.mala_decode(*([P(16)] * 5), None, None, 2, P(16), 1 << 20, 1, 32, 1, 64, 128, 0.1, 0.0,
+                         None)
+    assert st == mala.MALA_ERR_UNSUPPORTED
+
+
+def test_python_binding_requires_device_tensors():
+    import torch
+    x = torch.zeros(1, 1, 8, 64, dtype=torch.bfloat16)
+    with pytest.raises(TypeError):
+        mala.fwd(x, x, x, 0.125, 0.0)

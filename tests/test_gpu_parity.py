@@ -1,0 +1,275 @@
+"""GPU parity: the HIP path (through the C ABI) against the fp64 oracle on the same
+seeded inputs.  Small cases compare every element; the full-size workloads compare
+sampled query blocks, the last key blocks and sampled decode heads (those the
+oracle can compute one by one), in the launch configuration the benchmark uses.
+"""
+import math
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2609_32712_amd as mala
+from parity_util import (LSE_DIAG, assert_close, assert_counts, dev, exempt_rows, host)
+from workloads import Workload, bf16_to_f64
+
+pytestmark = pytest.mark.gpu
+
+
+def f32(x):
+    return float(np.float32(x))
+
+
+def legal_tiles(B, Hq, Nq, Nk, bq, bk):
+    off = Nk - Nq
+    n = 0
+    for i in range(-(-Nq // bq)):
+        n += (min(i * bq + bq - 1, Nq - 1) + off) // bk + 1
+    return n * B * Hq
+
+
+# --------------------------------------------------------------------------
+# small cases: every element
+# --------------------------------------------------------------------------
+TRAIN_CASES = {
+    "cfg1": dict(spec=1, over={}),
+    "local_d64_ragged": dict(spec=dict(kind="train", B=1, Hq=2, Hkv=1, N=1000, D=64, beta=3.0,
+                                       local=4.0), over={}),
+    "gqa_d128_ragged": dict(spec=dict(kind="train", B=2, Hq=4, Hkv=2, N=700, D=128, beta=2.5,
+                                      local=2.0), over={}),
+    "tiny_d128": dict(spec=dict(kind="train", B=1, Hq=2, Hkv=2, N=37, D=128, beta=2.0, local=1.0),
+                      over={}),
+    "single_row_d64": dict(spec=dict(kind="train", B=1, Hq=1, Hkv=1, N=1, D=64, beta=1.0), over={}),
+}
+TRAIN_TAUS = {
+    "cfg1": (0.0, 1e-4, 1e-3),
+    "local_d64_ragged": (0.0, 1e-2, 0.3, 1.0),
+    "gqa_d128_ragged": (0.0, 1e-3, 0.1, 1.0),
+    "tiny_d128": (0.0, 0.5),
+    "single_row_d64": (0.0, 1.0),
+}
+
+
+def _train_case(name, tau, Nq=None, seed=0):
+    c = TRAIN_CASES[name]
+    w = Workload(c["spec"], seed=seed, **c["over"])
+    t = w.tensors()
+    q, k, v, do = t["q"], t["k"], t["v"], t["do"]
+    if Nq is not None:   # prefill of the last Nq tokens against the whole cache
+        q, do = np.ascontiguousarray(q[:, :, -Nq:]), np.ascontiguousarray(do[:, :, -Nq:])
+    return w, q, k, v, do
+
+
+def _check_train(w, q, k, v, do, tau):
+    scale = f32(w.scale)
+    bq, bk = mala.mala_geometry(w.D, mala.PASS_FWD)
+    assert (bq, bk) == mala.mala_geometry(w.D, mala.PASS_BWD)
+    qf, kf, vf, dof = map(bf16_to_f64, (q, k, v, do))
+    of = oracle.mala_fwd(qf, kf, vf, scale, f32(tau), bq, bk, want_tiles=True)
+    ob = oracle.mala_bwd(qf, kf, vf, of["o"], of["lse"], dof, scale, f32(tau), bq, bk)
+    Q, K, V, DO = map(dev, (q, k, v, do))
+    g = mala.fwd(Q, K, V, scale, tau)
+    gb = mala.bwd(Q, K, V, g["o"], g["lse"], DO, scale, tau)
+    torch.cuda.synchronize()
+    assert_close("O", host(g["o"]), of["o"])
+    lse_err = np.abs(host(g["lse"]) - of["lse"]).max()
+    assert lse_err <= LSE_DIAG, lse_err
+    ex_f = exempt_rows(tau, of["tie_abs"])
+    assert_counts("fwd row tiles", host(g["row_tiles"]), of["row_tiles"], ex_f)
+    ex_b = ex_f | exempt_rows(tau, ob["tie_abs"])
+    assert_counts("bwd row tiles", host(gb["row_tiles"]), ob["row_tiles"], ex_b)
+    assert_close("dQ", host(gb["dq"]), ob["dq"])
+    assert_close("dK", host(gb["dk"]), ob["dk"])
+    assert_close("dV", host(gb["dv"]), ob["dv"])
+    B, Hq, Nq, D = q.shape
+    Nk = k.shape[2]
+    cf = host(g["counters"]).astype(np.int64)
+    assert cf[0] == legal_tiles(B, Hq, Nq, Nk, bq, bk)
+    assert cf[1] <= cf[0] and (tau > 0 or cf[1] == cf[0])
+    if not ex_f.any():
+        assert cf[1] == int((of["tile_keep"] == 1).sum())
+    cb = host(gb["counters"]).astype(np.int64)
+    assert cb[0] == cf[0] and cb[1] <= cb[0]
+    return ex_f.mean(), ex_b.mean()
+
+
+@pytest.mark.parametrize("name,tau", [(n, t) for n in TRAIN_CASES for t in TRAIN_TAUS[n]])
+def test_train_parity_small(name, tau):
+    w, q, k, v, do = _train_case(name, tau)
+    _check_train(w, q, k, v, do, tau)
+
+
+@pytest.mark.parametrize("Nq,tau", [(200, 0.0), (200, 0.05), (77, 1.0)])
+def test_prefill_against_longer_cache(Nq, tau):
+    w, q, k, v, do = _train_case("gqa_d128_ragged", tau, Nq=Nq)
+    _check_train(w, q, k, v, do, tau)
+
+
+def test_forward_skips_are_exercised():
+    # the skip-heavy case must really skip in forward and more in backward
+    w, q, k, v, do = _train_case("local_d64_ragged", 1.0)
+    Q, K, V, DO = map(dev, (q, k, v, do))
+    g = mala.fwd(Q, K, V, f32(w.scale), 1.0)
+    gb = mala.bwd(Q, K, V, g["o"], g["lse"], DO, f32(w.scale), 1.0)
+    cf, cb = host(g["counters"]), host(gb["counters"])
+    assert cf[1] < 0.9 * cf[0]
+    assert cb[1] <= cf[1]
+
+
+DECODE_CASES = [
+    (dict(kind="decode", B=2, Hq=8, Hkv=2, N=3001, D=128, beta=3.0, needles=4), 1, 0.0),
+    (dict(kind="decode", B=2, Hq=8, Hkv=2, N=3001, D=128, beta=3.0, needles=4), 4, 1e-4),
+    (dict(kind="decode", B=2, Hq=8, Hkv=2, N=3001, D=128, beta=3.0, needles=4), 7, 1e-2),
+    (dict(kind="decode", B=1, Hq=2, Hkv=2, N=999, D=64, beta=3.0, needles=4), 3, 0.1),
+    (dict(kind="decode", B=3, Hq=16, Hkv=1, N=64, D=128, beta=2.0, needles=2), 2, 1e-3),
+    (dict(kind="decode", B=1, Hq=4, Hkv=4, N=5, D=64, beta=2.0, needles=1), 1, 1.0),
+]
+
+
+@pytest.mark.parametrize("spec,splits,tau", DECODE_CASES)
+def test_decode_parity_small(spec, splits, tau):
+    w = Workload(spec)
+    t = w.tensors()
+    scale = f32(w.scale)
+    bk = mala.mala_geometry(w.D, mala.PASS_DECODE)[1]
+    qf, kf, vf = map(bf16_to_f64, (t["q"], t["k"], t["v"]))
+    od = oracle.mala_decode(qf, kf, vf, scale, f32(tau), bk, splits)
+    g = mala.decode(dev(t["q"]), dev(t["k"]), dev(t["v"]), scale, tau, splits)
+    torch.cuda.synchronize()
+    assert_close("decode O", host(g["o"]), od["o"])
+    assert np.abs(host(g["lse"]) - od["lse"]).max() <= LSE_DIAG
+    assert_counts("decode head tiles", host(g["head_tiles"]), od["tiles"],
+                  exempt_rows(tau, od["tie_abs"]))
+
+
+def test_decode_splits_cover_dense_at_tau0():
+    spec = dict(kind="decode", B=1, Hq=4, Hkv=1, N=2048, D=128, beta=3.0, needles=4)
+    w = Workload(spec)
+    t = w.tensors()
+    outs = [mala.decode(dev(t["q"]), dev(t["k"]), dev(t["v"]), f32(w.scale), 0.0, s) for s in (1, 5, 64)]
+    torch.cuda.synchronize()
+    for o in outs[1:]:
+        np.testing.assert_allclose(host(o["o"]), host(outs[0]["o"]), atol=1e-5)
+        assert (host(o["head_tiles"]) == 64).all()
+
+
+# --------------------------------------------------------------------------
+# full-size workloads: sampled outputs in the benchmark's launch configuration
+# --------------------------------------------------------------------------
+def _full_train(cfg_id, tau, sample_blocks, heads, kv_head_tail, seed=0):
+    w = Workload(cfg_id, seed=seed)
+    print("[full cfg%d tau=%g] generating inputs" % (cfg_id, tau), flush=True)
+    t = w.tensors(threads=16)
+    scale = f32(w.scale)
+    bq, bk = mala.mala_geometry(w.D, mala.PASS_FWD)
+    N, D = w.N, w.D
+    Q, K, V, DO = map(dev, (t["q"], t["k"], t["v"], t["do"]))
+    print("[full cfg%d] gpu fwd+bwd" % cfg_id, flush=True)
+    g = mala.fwd(Q, K, V, scale, tau)
+    gb = mala.bwd(Q, K, V, g["o"], g["lse"], DO, scale, tau)
+    torch.cuda.synchronize()
+    o_gpu, lse_gpu, rt_gpu = host(g["o"]), host(g["lse"]), host(g["row_tiles"])
+    dq_gpu, rtb_gpu = host(gb["dq"]), host(gb["row_tiles"])
+    dk_gpu, dv_gpu = host(gb["dk"]), host(gb["dv"])
+    del Q, K, V, DO, g, gb
+    Tr = -(-N // bq)
+    grp = w.g
+    # sampled query blocks of sampled heads: forward, dQ and counts
+    for (b, h) in heads:
+        hk = h // grp
+        qf = bf16_to_f64(t["q"][b:b + 1, h:h + 1])
+        kf = bf16_to_f64(t["k"][b:b + 1, hk:hk + 1])
+        vf = bf16_to_f64(t["v"][b:b + 1, hk:hk + 1])
+        dof = bf16_to_f64(t["do"][b:b + 1, h:h + 1])
+        for i in sample_blocks(Tr):
+            print("[full cfg%d] oracle head %d block %d" % (cfg_id, h, i), flush=True)
+            rows = slice(i * bq, min(N, (i + 1) * bq))
+            of = oracle.mala_fwd(qf, kf, vf, scale, f32(tau), bq, bk, blocks=(i, i + 1))
+            ob = oracle.mala_bwd(qf, kf, vf, of["o"], of["lse"], dof, scale, f32(tau), bq, bk,
+                                 qblocks=(i, i + 1), kblocks=(0, 0))
+            assert_close("O blk %d" % i, o_gpu[b, h, rows], of["o"][0, 0, rows])
+            assert np.abs(lse_gpu[b, h, rows] - of["lse"][0, 0, rows]).max() <= LSE_DIAG
+            ex_f = exempt_rows(tau, of["tie_abs"][0, 0, rows])
+            assert_counts("fwd tiles", rt_gpu[b, h, rows], of["row_tiles"][0, 0, rows], ex_f)
+            ex_b = ex_f | exempt_rows(tau, ob["tie_abs"][0, 0, rows])
+            assert_counts("bwd tiles", rtb_gpu[b, h, rows], ob["row_tiles"][0, 0, rows], ex_b)
+            assert_close("dQ blk %d" % i, dq_gpu[b, h, rows], ob["dq"][0, 0, rows])
+    # dK, dV of the last key blocks of one KV head: they see only the last rows
+    b, hk = kv_head_tail
+    Tc = -(-N // bk)
+    last = 2
+    r0 = (Tc - last) * bk
+    qf = bf16_to_f64(t["q"][b:b + 1, hk * grp:(hk + 1) * grp])
+    kf = bf16_to_f64(t["k"][b:b + 1, hk:hk + 1])
+    vf = bf16_to_f64(t["v"][b:b + 1, hk:hk + 1])
+    dof = bf16_to_f64(t["do"][b:b + 1, hk * grp:(hk + 1) * grp])
+    print("[full cfg%d] oracle dK/dV of the last %d key blocks of kv head %d" % (cfg_id, last, hk),
+          flush=True)
+    of = oracle.mala_fwd(qf, kf, vf, scale, f32(tau), bq, bk, blocks=(r0 // bq, Tr))
+    o_in = np.nan_to_num(of["o"])
+    lse_in = np.nan_to_num(of["lse"])
+    ob = oracle.mala_bwd(qf, kf, vf, o_in, lse_in, dof, scale, f32(tau), bq, bk,
+                         qblocks=(0, 0), kblocks=(Tc - last, Tc))
+    assert_close("dK tail", dk_gpu[b, hk, r0:], ob["dk"][0, 0, r0:])
+    assert_close("dV tail", dv_gpu[b, hk, r0:], ob["dv"][0, 0, r0:])
+
+
+def _blocks(*fracs):
+    return lambda Tr: sorted({min(Tr - 1, int(f * Tr)) for f in fracs})
+
+
+@pytest.mark.parametrize("tau", [0.0, 1e-4, 1e-3])
+def test_full_config2_sampled(tau):
+    _full_train(2, tau, _blocks(0.0, 0.37, 0.999), heads=[(0, 3), (0, 12)], kv_head_tail=(0, 5))
+
+
+@pytest.mark.parametrize("tau", [0.0, 1e-4])
+def test_full_config3_sampled(tau):
+    _full_train(3, tau, _blocks(0.5, 0.999), heads=[(0, 1), (0, 30)], kv_head_tail=(0, 7))
+
+
+@pytest.mark.parametrize("tau", [1e-4])
+def test_full_config4_sampled(tau):
+    _full_train(4, tau, _blocks(0.25, 0.999), heads=[(0, 6)], kv_head_tail=(0, 1))
+
+
+@pytest.mark.parametrize("tau", [0.0, 1e-4])
+def test_full_config5_decode_sampled(tau):
+    w = Workload(5)
+    print("[full cfg5 tau=%g] generating inputs" % tau, flush=True)
+    t = w.tensors(threads=16)
+    scale = f32(w.scale)
+    bk = mala.mala_geometry(w.D, mala.PASS_DECODE)[1]
+    S = mala.default_num_splits(w.B, w.Hkv, w.N)
+    g = mala.decode(dev(t["q"]), dev(t["k"]), dev(t["v"]), scale, tau, S)
+    torch.cuda.synchronize()
+    o, lse, ht = host(g["o"]), host(g["lse"]), host(g["head_tiles"])
+    rng = np.random.default_rng(5)
+    pairs = [(int(rng.integers(w.B)), int(rng.integers(w.Hq))) for _ in range(6)]
+    print("[full cfg5] oracle on", pairs, "splits", S, flush=True)
+    qf = bf16_to_f64(t["q"])
+    for b, h in pairs:
+        hk = h // w.g
+        od = oracle.mala_decode(qf[b:b + 1, h:h + 1], bf16_to_f64(t["k"][b:b + 1, hk:hk + 1]),
+                                bf16_to_f64(t["v"][b:b + 1, hk:hk + 1]), scale, f32(tau), bk, S)
+        assert_close("decode O", o[b, h], od["o"][0, 0])
+        assert abs(lse[b, h] - od["lse"][0, 0]) <= LSE_DIAG
+        assert_counts("decode tiles", ht[b:b + 1, h:h + 1], od["tiles"],
+                      exempt_rows(tau, od["tie_abs"]))
+
+
+# --------------------------------------------------------------------------
+# reproducibility
+# --------------------------------------------------------------------------
+def test_repeat_runs_bitwise_forward_dk_dv():
+    w, q, k, v, do = _train_case("gqa_d128_ragged", 0.1)
+    Q, K, V, DO = map(dev, (q, k, v, do))
+    r1 = mala.fwd(Q, K, V, f32(w.scale), 0.1)
+    r2 = mala.fwd(Q, K, V, f32(w.scale), 0.1)
+    b1 = mala.bwd(Q, K, V, r1["o"], r1["lse"], DO, f32(w.scale), 0.1)
+    b2 = mala.bwd(Q, K, V, r1["o"], r1["lse"], DO, f32(w.scale), 0.1)
+    torch.cuda.synchronize()
+    assert torch.equal(r1["o"], r2["o"]) and torch.equal(r1["lse"], r2["lse"])
+    assert torch.equal(b1["dk"], b2["dk"]) and torch.equal(b1["dv"], b2["dv"])
+    assert torch.allclose(b1["dq"], b2["dq"], atol=1e-5)

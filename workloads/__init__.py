@@ -9,7 +9,8 @@ stand in for both.  Recipe (identical for every configuration):
   * one independent PCG64 stream per (tensor, batch, head), seeded with
     ``numpy.random.default_rng([seed, config_id, tensor_id, b, h])``, so any
     single head can be regenerated without drawing the others;
-  * values drawn in float64 and rounded to bf16 with round-to-nearest-even;
+  * standard normals drawn as float32 (PCG64 + ziggurat), combined in float64,
+    and rounded to bf16 with round-to-nearest-even;
   * K and V ~ N(0, 1); dO ~ N(0, 1);
   * planted-needle queries: Q_i = g_i + beta * K_{r(i)} with g ~ N(0, 1) and
     r(i) uniform on {0..i}, built from the ROUNDED K of the head's KV head and
@@ -24,6 +25,7 @@ import math
 from concurrent.futures import ThreadPoolExecutor
 
 import numpy as np
+import torch
 
 # tensor ids of the per-slice streams
 _T_K, _T_V, _T_Q, _T_DO, _T_BETA, _T_POS = 1, 2, 3, 4, 5, 6
@@ -44,13 +46,29 @@ CONFIGS = {
 
 
 def bf16_round(x: np.ndarray) -> np.ndarray:
-    """Round float64 values to bf16 (round-to-nearest-even); return uint16 bits."""
-    x = np.asarray(x, dtype=np.float64)
-    m, e = np.frexp(x)                      # x = m * 2**e, 0.5 <= |m| < 1
-    # bf16 keeps 8 significant bits: quantum 2**(e - 8) for |x| in [2**(e-1), 2**e)
-    r = np.ldexp(np.round(np.ldexp(m, 8)), e - 8)   # np.round: half to even, exact scaling
-    bits = r.astype(np.float32).view(np.uint32)     # exact: r has <= 8 significant bits
-    return (bits >> 16).astype(np.uint16)
+    """Round float64 values to bf16 (round-to-nearest-even); return uint16 bits.
+
+    Rounds the float64 bit pattern directly at bf16's last mantissa bit (no
+    intermediate float32 rounding, hence no double rounding): add 2^44 - 1 plus the
+    bit that will become the last kept one, then clear the 45 dropped bits.  The
+    bit arithmetic runs in torch (CPU, multi-threaded).  Magnitudes outside the
+    normal bf16 range take an exact slower path."""
+    x = np.ascontiguousarray(x, dtype=np.float64)
+    xt = torch.from_numpy(x)
+    u = xt.view(torch.int64)
+    r = ((u + (((u >> 45) & 1) + ((1 << 44) - 1))) >> 45) << 45
+    bits = (r.view(torch.float64).to(torch.float32).view(torch.int32) >> 16) & 0xFFFF
+    out = bits.to(torch.int16).numpy().view(np.uint16)
+    ax = xt.abs()
+    odd_t = (ax < 2.0 ** -126) | (ax >= 2.0 ** 127) | ~torch.isfinite(xt)
+    if bool(odd_t.any()):
+        odd = odd_t.numpy()
+        xs = x[odd]
+        m, e = np.frexp(xs)
+        rs = np.ldexp(np.round(np.ldexp(m, 8)), e - 8)
+        with np.errstate(over="ignore", invalid="ignore"):
+            out[odd] = (rs.astype(np.float32).view(np.uint32) >> 16).astype(np.uint16)
+    return out
 
 
 def bf16_to_f64(bits: np.ndarray) -> np.ndarray:
@@ -63,8 +81,12 @@ def _rng(seed, cfg_id, tensor, b, h):
     return np.random.default_rng([int(seed), int(cfg_id), tensor, int(b), int(h)])
 
 
+def _normal(seed, cfg_id, tensor, b, h, shape):
+    return _rng(seed, cfg_id, tensor, b, h).standard_normal(shape, dtype=np.float32)
+
+
 def _normal_bits(seed, cfg_id, tensor, b, h, shape):
-    return bf16_round(_rng(seed, cfg_id, tensor, b, h).standard_normal(shape))
+    return bf16_round(_normal(seed, cfg_id, tensor, b, h, shape))
 
 
 class Workload:
@@ -113,12 +135,12 @@ class Workload:
         rng = _rng(self.seed, self.cfg_id, _T_Q, b, h)
         beta = self.beta(h)
         if self.kind == "decode":
-            g = rng.standard_normal(self.D)
+            g = rng.standard_normal(self.D, dtype=np.float32).astype(np.float64)
             n = self.spec.get("needles", 4)
             pos = rng.choice(self.N, size=n, replace=False)
             return bf16_round(g + beta * kf[pos].sum(axis=0))
         N = self.N
-        g = rng.standard_normal((N, self.D))
+        g = rng.standard_normal((N, self.D), dtype=np.float32).astype(np.float64)
         r = rng.integers(0, np.arange(1, N + 1))        # r(i) uniform on {0..i}
         q = g + beta * kf[r]
         alpha = float(self.spec.get("local", 0.0))
@@ -129,7 +151,7 @@ class Workload:
     def needle_positions(self, b, h):
         """Decode only: the planted positions of query head (b, h)."""
         rng = _rng(self.seed, self.cfg_id, _T_Q, b, h)
-        rng.standard_normal(self.D)
+        rng.standard_normal(self.D, dtype=np.float32)
         return np.sort(rng.choice(self.N, size=self.spec.get("needles", 4), replace=False))
 
     # ---- whole tensors ---------------------------------------------------
