@@ -1,0 +1,364 @@
+"""Benchmark of the MALA hot path on one MI355X.
+
+A step is one pass of the whole path over one batch of synthetic input:
+  mala_fwd + mala_bwd on the 131072-token causal workload (one tensor-parallel
+  share: batch 1, 8 query heads, 2 KV heads, head_dim 128, tau = 1e-4), then
+  mala_decode of 16 one-token queries over 131072-token KV caches (32 query
+  heads, 8 KV heads, tau = 1e-4).
+Inputs are resident in HBM before the timed region; outputs and workspaces are
+preallocated.  The same kernels at tau = 0 (dense attention) and the
+32768-token GQA 32/8 workload are timed as well, because the metric asks for
+the speed-up over dense at 32K and 128K.
+
+Prints ONE JSON line (rank 0, N = 1).  More than one GPU is not supported.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import math
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "MALA fwd/bwd ms + speedup vs dense at 32K/128K; decode ms; retained-tile %"
+PEAK_BF16_TFLOPS = 2500.0      # MI355X dense bf16 MFMA
+PEAK_HBM_GBS = 8000.0          # MI355X HBM3E
+
+
+def log(*a):
+    print("[bench]", *a, file=sys.stderr, flush=True)
+
+
+class Train:
+    """Device-resident inputs, outputs and workspace of one fwd+bwd workload."""
+
+    def __init__(self, cfg_id, tau):
+        import torch
+        import paper_2609_32712_amd as mala
+        from workloads import Workload
+        self.w = Workload(cfg_id)
+        self.tau = tau
+        t0 = time.time()
+        t = self.w.tensors(threads=16)
+        log("cfg%d inputs generated in %.1fs" % (cfg_id, time.time() - t0))
+        dev = lambda b: torch.from_numpy(b.view(np.int16)).to("cuda").view(torch.bfloat16)
+        self.q, self.k, self.v, self.do = (dev(t[x]) for x in ("q", "k", "v", "do"))
+        del t
+        w = self.w
+        f = dict(dtype=torch.float32, device="cuda")
+        self.o = torch.empty((w.B, w.Hq, w.N, w.D), **f)
+        self.lse = torch.empty((w.B, w.Hq, w.N), **f)
+        self.dq = torch.empty((w.B, w.Hq, w.N, w.D), **f)
+        self.dk = torch.empty((w.B, w.Hkv, w.N, w.D), **f)
+        self.dv = torch.empty((w.B, w.Hkv, w.N, w.D), **f)
+        i32 = dict(dtype=torch.int32, device="cuda")
+        self.rt_f = torch.empty((w.B, w.Hq, w.N), **i32)
+        self.rt_b = torch.empty((w.B, w.Hq, w.N), **i32)
+        self.cnt_f = torch.empty(4, dtype=torch.int64, device="cuda")
+        self.cnt_b = torch.empty(4, dtype=torch.int64, device="cuda")
+        n = mala.mala_bwd_workspace_size(w.B, w.Hq, w.Hkv, w.N, w.N, w.D)
+        self.ws = torch.empty(n, dtype=torch.uint8, device="cuda")
+        self.scale = float(np.float32(w.scale))
+        self.mala = mala
+
+    def fwd(self, tau):
+        self.mala.mala_fwd(self.q, self.k, self.v, self.o, self.lse, self.rt_f, self.cnt_f,
+                           self.scale, tau)
+
+    def bwd(self, tau):
+        self.mala.mala_bwd(self.q, self.k, self.v, self.o, self.lse, self.do, self.dq, self.dk,
+                           self.dv, self.rt_b, self.cnt_b, self.ws, self.scale, tau)
+
+    def counters(self):
+        return self.cnt_f.cpu().numpy(), self.cnt_b.cpu().numpy()
+
+
+class Decode:
+    def __init__(self, cfg_id, tau, splits=None):
+        import torch
+        import paper_2609_32712_amd as mala
+        from workloads import Workload
+        self.w = Workload(cfg_id)
+        t0 = time.time()
+        t = self.w.tensors(threads=16)
+        log("cfg%d inputs generated in %.1fs" % (cfg_id, time.time() - t0))
+        dev = lambda b: torch.from_numpy(b.view(np.int16)).to("cuda").view(torch.bfloat16)
+        self.q, self.k, self.v = (dev(t[x]) for x in ("q", "k", "v"))
+        del t
+        w = self.w
+        self.splits = splits or mala.default_num_splits(w.B, w.Hkv, w.N)
+        self.o = torch.empty((w.B, w.Hq, w.D), dtype=torch.float32, device="cuda")
+        self.lse = torch.empty((w.B, w.Hq), dtype=torch.float32, device="cuda")
+        self.ht = torch.empty((w.B, w.Hq), dtype=torch.int32, device="cuda")
+        self.cnt = torch.empty(4, dtype=torch.int64, device="cuda")
+        n = mala.mala_decode_workspace_size(w.B, w.Hq, w.D, self.splits)
+        self.ws = torch.empty(n, dtype=torch.uint8, device="cuda")
+        self.scale = float(np.float32(w.scale))
+        self.mala = mala
+
+    def run(self, tau):
+        self.mala.mala_decode(self.q, self.k, self.v, self.o, self.lse, self.ht, self.cnt,
+                              self.splits, self.ws, self.scale, tau)
+
+
+def time_calls(fn, reps, warmup):
+    """Mean and median per-call device time (ms) from HIP events on the current stream."""
+    import torch
+    for _ in range(warmup):
+        fn()
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+          for _ in range(reps)]
+    for a, b in ev:
+        a.record()
+        fn()
+        b.record()
+    torch.cuda.synchronize()
+    ts = [a.elapsed_time(b) for a, b in ev]
+    return float(np.mean(ts)), float(np.median(ts))
+
+
+def train_flops(cnt_f, cnt_b, D, bq, bk):
+    """Algorithmic flops of one fwd and one bwd launch at tile granularity:
+    2*d per legal QK slot (score discovery), plus 2*d (fwd PV) or 8*d (bwd dP, dV,
+    dK, dQ) per retained slot."""
+    slots = bq * bk
+    fwd = (cnt_f[0] + cnt_f[1]) * slots * 2 * D
+    bwd = (cnt_b[0] * 2 + cnt_b[1] * 8) * slots * D
+    return float(fwd), float(bwd)
+
+
+def dense_equivalent_flops(B, Hq, N, D):
+    pairs = B * Hq * N * (N + 1) / 2
+    return pairs * 4 * D, pairs * 10 * D
+
+
+def source_sha(path):
+    with open(path, "rb") as fh:
+        return hashlib.sha256(fh.read()).hexdigest()[:16]
+
+
+def traffic_from_profiles(kernel_src, launches_per_step=1):
+    """HBM bytes per launch from committed rocprofv3 counter summaries, or None if
+    the kernel source changed since they were taken."""
+    p = os.path.join(ROOT, "profiles", "mala_bwd_kernel_traffic.json")
+    if not os.path.exists(p):
+        return None
+    with open(p) as fh:
+        d = json.load(fh)
+    if d.get("source_sha") != source_sha(kernel_src):
+        return None
+    return float(d["bytes_per_launch"])
+
+
+def cpu_baseline(step_ms_model):
+    """Time the fp64 oracle on a bounded sample of the same step and scale it up."""
+    import oracle
+    from workloads import Workload, bf16_to_f64
+    import paper_2609_32712_amd as mala
+    oracle.build()
+    cores = int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1))
+    w = Workload(4)
+    bq, bk = mala.mala_geometry(w.D, mala.PASS_FWD)
+    Tr = -(-w.N // bq)
+    nb = 2 * cores
+    i0 = Tr // 2 - nb // 2
+    qf = bf16_to_f64(w.q_head(0, 0))[None, None]
+    kf = bf16_to_f64(w.k_head(0, 0))[None, None]
+    vf = bf16_to_f64(w.v_head(0, 0))[None, None]
+    dof = bf16_to_f64(w.do_head(0, 0))[None, None]
+    scale = float(np.float32(w.scale))
+    t0 = time.time()
+    of = oracle.mala_fwd(qf, kf, vf, scale, float(np.float32(1e-4)), bq, bk, blocks=(i0, i0 + nb),
+                         heads=[(0, 0)])
+    t_f = time.time() - t0
+    t0 = time.time()
+    oracle.mala_bwd(qf, kf, vf, np.nan_to_num(of["o"]), np.nan_to_num(of["lse"]), dof, scale,
+                    float(np.float32(1e-4)), bq, bk, qblocks=(i0, i0 + nb), kblocks=(0, 0))
+    t_b = time.time() - t0
+    # sampled tiles: blocks i0..i0+nb-1 each see (i + 1) key tiles; the whole step
+    # has Hq * Tr (Tr + 1) / 2 tiles; the dQ-only sweep is half of the backward work
+    sample_tiles = sum(i + 1 for i in range(i0, i0 + nb))
+    total_tiles = w.Hq * Tr * (Tr + 1) / 2
+    ms_fwd = t_f * 1e3 * total_tiles / sample_tiles
+    ms_bwd = 2 * t_b * 1e3 * total_tiles / sample_tiles
+    wd = Workload(5)
+    sd = mala.default_num_splits(wd.B, wd.Hkv, wd.N)
+    qd = bf16_to_f64(wd.q_head(0, 0))[None, None]
+    kd = bf16_to_f64(wd.k_head(0, 0))[None, None]
+    vd = bf16_to_f64(wd.v_head(0, 0))[None, None]
+    t0 = time.time()
+    nh = 4
+    for h in range(nh):
+        oracle.mala_decode(qd, kd, vd, scale, float(np.float32(1e-4)),
+                           mala.mala_geometry(wd.D, mala.PASS_DECODE)[1], sd)
+    t_d = (time.time() - t0) / nh
+    ms_dec = t_d * 1e3 * wd.B * wd.Hq
+    total = ms_fwd + ms_bwd + ms_dec
+    return {"value": round(total, 1), "unit": "ms", "cores": cores, "kind": "oracle",
+            "sample": ("fp64 C oracle (OpenMP over query blocks) on %d consecutive query blocks "
+                       "of head 0 of the 131072-token workload (fwd %.1fs, dQ sweep %.1fs, scaled "
+                       "by total/sampled tiles, x2 for the dK/dV sweep) plus %d decode heads "
+                       "(%.2fs each, x%d heads); extrapolated to one full step"
+                       % (nb, t_f, t_b, nh, t_d, wd.B * wd.Hq)),
+            "fwd_ms": round(ms_fwd, 1), "bwd_ms": round(ms_bwd, 1), "decode_ms": round(ms_dec, 1)}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=5)
+    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--tau", type=float, default=1e-4)
+    ap.add_argument("--reps", type=int, default=5, help="event-timed calls per kernel and tau")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-32k", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU only: the MALA operator is built and measured on a "
+              "single MI355X (heads and batch shard with no exchange; see the design notes).",
+              file=sys.stderr)
+        sys.exit(2)
+    import torch
+    import paper_2609_32712_amd as mala
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    mala.load_library()
+    tau = args.tau
+
+    tr = Train(4, tau)
+    dec = Decode(5, tau)
+    w = tr.w
+    bq, bk = mala.mala_geometry(w.D, mala.PASS_FWD)
+
+    def step():
+        tr.fwd(tau)
+        tr.bwd(tau)
+        dec.run(tau)
+
+    log("warmup")
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    log("timed region: %d steps" % args.steps)
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        step()
+    torch.cuda.synchronize()
+    ms_per_step = (time.perf_counter() - t0) * 1e3 / args.steps
+
+    # per-kernel event timings at tau and at tau = 0 (dense through the same kernels)
+    res = {}
+    for name, t_ in (("tau", tau), ("dense", 0.0)):
+        f = time_calls(lambda: tr.fwd(t_), args.reps, 1)
+        b = time_calls(lambda: tr.bwd(t_), args.reps, 1)
+        d = time_calls(lambda: dec.run(t_), args.reps, 1)
+        cf, cb = tr.counters()
+        cd = dec.cnt.cpu().numpy()
+        res[name] = dict(fwd=f, bwd=b, dec=d, cf=cf, cb=cb, cd=cd)
+        log(name, "fwd %.2f bwd %.2f decode %.3f ms" % (f[0], b[0], d[0]))
+    rt, rd = res["tau"], res["dense"]
+    fl_f, fl_b = train_flops(rt["cf"], rt["cb"], w.D, bq, bk)
+    de_f, de_b = dense_equivalent_flops(w.B, w.Hq, w.N, w.D)
+    bwd_ms = rt["bwd"][0]
+    achieved = fl_b / (bwd_ms * 1e-3) / 1e12
+    kv_bytes = dec.w.B * dec.w.Hkv * dec.w.N * dec.w.D * 2
+    cd = rt["cd"]
+    dec_bytes = kv_bytes + kv_bytes * cd[2] / max(1, cd[0] / dec.w.g)
+    pct = lambda a, b_: round(100.0 * float(a) / max(1.0, float(b_)), 3)
+
+    detail = {
+        "128k": {
+            "fwd_ms": round(rt["fwd"][0], 3), "fwd_ms_median": round(rt["fwd"][1], 3),
+            "bwd_ms": round(rt["bwd"][0], 3), "bwd_ms_median": round(rt["bwd"][1], 3),
+            "dense_fwd_ms": round(rd["fwd"][0], 3), "dense_bwd_ms": round(rd["bwd"][0], 3),
+            "speedup_fwd": round(rd["fwd"][0] / rt["fwd"][0], 4),
+            "speedup_bwd": round(rd["bwd"][0] / rt["bwd"][0], 4),
+            "retained_tiles_pct_fwd": pct(rt["cf"][1], rt["cf"][0]),
+            "retained_tiles_pct_bwd": pct(rt["cb"][1], rt["cb"][0]),
+            "mean_slots_per_query_fwd": round(float(rt["cf"][3]) / (w.B * w.Hq * w.N), 1),
+            "mean_slots_per_query_bwd": round(float(rt["cb"][3]) / (w.B * w.Hq * w.N), 1),
+            "executed_tflops_fwd": round(fl_f / (rt["fwd"][0] * 1e-3) / 1e12, 1),
+            "executed_tflops_bwd": round(achieved, 1),
+            "dense_equiv_tflops_fwd": round(de_f / (rt["fwd"][0] * 1e-3) / 1e12, 1),
+            "dense_equiv_tflops_bwd": round(de_b / (rt["bwd"][0] * 1e-3) / 1e12, 1),
+        },
+        "decode": {
+            "ms": round(rt["dec"][0], 4), "ms_median": round(rt["dec"][1], 4),
+            "dense_ms": round(rd["dec"][0], 4),
+            "speedup": round(rd["dec"][0] / rt["dec"][0], 4),
+            "num_splits": dec.splits,
+            "retained_head_tiles_pct": pct(cd[1], cd[0]),
+            "v_tiles_loaded_pct": pct(cd[2], cd[0] / dec.w.g),
+            "hbm_gbs_algorithmic": round(dec_bytes / (rt["dec"][0] * 1e-3) / 1e9, 1),
+            "hbm_frac": round(dec_bytes / (rt["dec"][0] * 1e-3) / 1e9 / PEAK_HBM_GBS, 4),
+        },
+        "decision_tile": [bq, bk],
+    }
+    del tr
+    torch.cuda.empty_cache()
+    if not args.no_32k:
+        t3 = Train(3, tau)
+        r3 = {}
+        for name, t_ in (("tau", tau), ("dense", 0.0)):
+            r3[name] = (time_calls(lambda: t3.fwd(t_), args.reps, 1),
+                        time_calls(lambda: t3.bwd(t_), args.reps, 1), t3.counters())
+        (f3, b3, (cf3, cb3)), (f3d, b3d, _) = r3["tau"], r3["dense"]
+        detail["32k"] = {
+            "fwd_ms": round(f3[0], 3), "bwd_ms": round(b3[0], 3),
+            "dense_fwd_ms": round(f3d[0], 3), "dense_bwd_ms": round(b3d[0], 3),
+            "speedup_fwd": round(f3d[0] / f3[0], 4), "speedup_bwd": round(b3d[0] / b3[0], 4),
+            "retained_tiles_pct_fwd": pct(cf3[1], cf3[0]),
+            "retained_tiles_pct_bwd": pct(cb3[1], cb3[0]),
+        }
+        del t3
+        torch.cuda.empty_cache()
+
+    line = {
+        "metric": METRIC,
+        "value": round(ms_per_step, 3),
+        "unit": "ms",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 3),
+        "higher_is_better": False,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {
+            "workload": ("mala_fwd + mala_bwd, causal, batch 1, 8 query / 2 KV heads, 131072 "
+                         "tokens, head_dim 128 (one TP=8 share), planted needles beta=2; then "
+                         "mala_decode, batch 16, 32 query / 8 KV heads, 131072-token caches, "
+                         "4 needles beta=3"),
+            "tau": tau, "seq_len": w.N, "head_dim": w.D, "q_heads": w.Hq, "kv_heads": w.Hkv,
+            "decode_batch": dec.w.B, "decode_splits": dec.splits,
+        },
+        "roofline": {
+            "kernel": "mala_bwd_kernel",
+            "bound": "mfma",
+            "achieved": round(achieved, 1),
+            "peak": PEAK_BF16_TFLOPS,
+            "unit": "TFLOP/s",
+            "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
+            "traffic": traffic_from_profiles(
+                os.path.join(ROOT, "paper_2609_32712_amd", "csrc", "mala_bwd.hip")),
+            "flops_per_launch": fl_b,
+            "launch_ms": round(bwd_ms, 3),
+        },
+        "detail": detail,
+    }
+    if not args.no_cpu_baseline:
+        log("cpu baseline (oracle)")
+        line["cpu_baseline"] = cpu_baseline(ms_per_step)
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()
