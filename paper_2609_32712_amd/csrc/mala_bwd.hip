@@ -6,8 +6,9 @@
 // diagonal to the end.  Wavefront w owns keys [32w, 32w + 32) of the block, so a
 // wavefront's work on one query tile is exactly one 32 x 32 decision tile.
 //
-// Per query tile (32 rows), staged once per workgroup in LDS (Q, dO, and the
-// per-row base-2 LSE, test threshold and D_q = rowsum(O * dO)):
+// Per query tile (32 rows), staged once per workgroup in double-buffered LDS (Q,
+// dO, and the per-row base-2 LSE, test threshold and D_q = rowsum(O * dO)); the
+// next tile is fetched into registers while the current one is processed:
 //   S = Q_i K_w^T         8 MFMAs (lane = one key column, 16 query rows)
 //   offline test          retain iff some valid entry has
 //                         s - lse_q >= log2(tau) - log2(L_q) (base-2 units); ballot
@@ -87,14 +88,18 @@ __global__ __launch_bounds__(256) void mala_bwd_kernel(BwdParams p) {
   constexpr int DSS = kBq + 8;     // dS row stride: [key][q]
   constexpr int WPB = 4 / DB;      // wavefronts per dQ column block
   constexpr int QK = kBwdKeys / WPB;   // keys one wavefront sums for its dQ slice
+  constexpr int TILE = kBq * LD;       // one Q or dO tile in LDS
+  constexpr int CPT = kBq * D / 8 / 256;   // 16-byte chunks per thread per tile
   // K_j (row-major) is only needed until the dQ operands are in registers; its LDS
   // is then reused for the two bf16 planes (hi, lo) of dS stored as [key][q].
   constexpr int KT_ELEMS = kBwdKeys * LD;
   constexpr int DS_ELEMS = 2 * kBwdKeys * DSS;
   __shared__ __attribute__((aligned(16))) bf16 shared_kt_ds[KT_ELEMS > DS_ELEMS ? KT_ELEMS : DS_ELEMS];
-  __shared__ __attribute__((aligned(16))) bf16 Qs[kBq * LD];
-  __shared__ __attribute__((aligned(16))) bf16 dOs[kBq * LD];
-  __shared__ __attribute__((aligned(16))) float lse2s[kBq], thrs[kBq], Dsv[kBq];
+  // double-buffered query tiles: the next tile is fetched into registers while the
+  // current one is processed, then written to the other buffer
+  __shared__ __attribute__((aligned(16))) bf16 Qs[2 * TILE];
+  __shared__ __attribute__((aligned(16))) bf16 dOs[2 * TILE];
+  __shared__ __attribute__((aligned(16))) float rowv[2][3][kBq];   // base-2 lse, threshold, D_q
   __shared__ int flags[4];
   bf16* const Kt = shared_kt_ds;
   bf16* const dSh = shared_kt_ds;
@@ -139,173 +144,204 @@ __global__ __launch_bounds__(256) void mala_bwd_kernel(BwdParams p) {
     ktreg[ks] = cat(lds_read_tr(kr), lds_read_tr(kr + 8 * LD));
   }
 
-  __syncthreads();   // every wavefront holds its dQ operands: K_j's LDS becomes the dS planes
-
   f32x16 dvacc[DB], dkacc[DB];
 #pragma unroll
   for (int db = 0; db < DB; ++db)
 #pragma unroll
     for (int r = 0; r < 16; ++r) dvacc[db][r] = dkacc[db][r] = 0.f;
 
-  unsigned n_legal = 0, n_ret = 0, n_tiles = 0;
+  unsigned n_legal = 0, n_ret = 0;
   unsigned long long slots = 0;
   const long first_q = (long)kb0 - off;
   const int qi_start = first_q <= 0 ? 0 : (int)(first_q / kBq);
   const int nqt = (p.Nq + kBq - 1) / kBq;
+  const int per_head = nqt - qi_start;     // >= 1: key kb0 < Nk is visible to row Nq - 1
+  const int total = grp * per_head;
 
-  for (int hh = 0; hh < grp; ++hh) {
-    const int hq = hkv * grp + hh;
-    const long bhq = (long)b * p.Hq + hq;
-    const bf16* Qp = p.q + bhq * p.Nq * D;
-    const bf16* dOp = p.dout + bhq * p.Nq * D;
-    const float* lsep = p.lse + bhq * p.Nq;
-    const float* dvp = p.dvec + bhq * p.Nq;
-    for (int qi = qi_start; qi < nqt; ++qi) {
-      const int q0 = qi * kBq;
-      __syncthreads();
-      for (int ch = tid; ch < kBq * D / 8; ch += 256) {
-        const int row = ch / (D / 8), col = (ch % (D / 8)) * 8;
-        const long qq = (long)q0 + row;
-        const bool ok = qq < p.Nq;
-        store8(Qs + row * LD + col, ok ? load8(Qp + qq * D + col) : zero8());
-        store8(dOs + row * LD + col, ok ? load8(dOp + qq * D + col) : zero8());
+  // prefetch registers of the next query tile
+  bf16x8 pq[CPT], pdo[CPT];
+  float plse = 0.f, pdv = 0.f;
+  auto fetch = [&](int it) {
+    const long bhq = (long)b * p.Hq + hkv * grp + it / per_head;
+    const int q0 = (qi_start + it % per_head) * kBq;
+#pragma unroll
+    for (int e = 0; e < CPT; ++e) {
+      const int ch = tid + 256 * e;
+      const int row = ch / (D / 8), col = (ch % (D / 8)) * 8;
+      const long qq = (long)q0 + row;
+      const bool ok = qq < p.Nq;
+      pq[e] = ok ? load8(p.q + (bhq * p.Nq + qq) * D + col) : zero8();
+      pdo[e] = ok ? load8(p.dout + (bhq * p.Nq + qq) * D + col) : zero8();
+    }
+    if (tid < kBq) {
+      const long qq = (long)q0 + tid;
+      if (qq < p.Nq) {
+        plse = p.lse[bhq * p.Nq + qq];
+        pdv = p.dvec[bhq * p.Nq + qq];
       }
-      if (tid < kBq) {
-        const long qq = (long)q0 + tid;
-        if (qq < p.Nq) {
-          const float l2 = lsep[qq] * kLog2e;
-          lse2s[tid] = l2;
-          thrs[tid] = l2 + p.log2tau - log2f((float)(qq + 1 + off));
-          Dsv[tid] = dvp[qq];
-        } else {
-          lse2s[tid] = 0.f;
-          thrs[tid] = __builtin_huge_valf();
-          Dsv[tid] = 0.f;
+    }
+  };
+  auto stash = [&](int it, int buf) {
+    const int q0 = (qi_start + it % per_head) * kBq;
+#pragma unroll
+    for (int e = 0; e < CPT; ++e) {
+      const int ch = tid + 256 * e;
+      const int row = ch / (D / 8), col = (ch % (D / 8)) * 8;
+      store8(Qs + buf * TILE + row * LD + col, pq[e]);
+      store8(dOs + buf * TILE + row * LD + col, pdo[e]);
+    }
+    if (tid < kBq) {
+      const long qq = (long)q0 + tid;
+      if (qq < p.Nq) {
+        const float l2 = plse * kLog2e;
+        rowv[buf][0][tid] = l2;
+        rowv[buf][1][tid] = l2 + p.log2tau - log2f((float)(qq + 1 + off));
+        rowv[buf][2][tid] = pdv;
+      } else {
+        rowv[buf][0][tid] = 0.f;
+        rowv[buf][1][tid] = __builtin_huge_valf();   // padded rows never retain
+        rowv[buf][2][tid] = 0.f;
+      }
+    }
+  };
+
+  fetch(0);
+  __syncthreads();   // every wavefront holds its dQ operands: K_j's LDS becomes the dS planes
+  stash(0, 0);
+  __syncthreads();
+
+  for (int it = 0; it < total; ++it) {
+    const int buf = it & 1;
+    const long bhq = (long)b * p.Hq + hkv * grp + it / per_head;
+    const int q0 = (qi_start + it % per_head) * kBq;
+    if (it + 1 < total) fetch(it + 1);
+    const bf16* Qb = Qs + buf * TILE;
+    const bf16* dOb = dOs + buf * TILE;
+    const float* lse2s = rowv[buf][0];
+    const float* thrs = rowv[buf][1];
+    const float* Dsv = rowv[buf][2];
+
+    const int qlast = min(q0 + kBq - 1, p.Nq - 1);
+    const bool legal_tile = (kw < p.Nk) && ((long)kw <= (long)qlast + off);
+    bool ret = false;
+    if (legal_tile) {
+      ++n_legal;
+      f32x16 s;
+#pragma unroll
+      for (int r = 0; r < 16; ++r) s[r] = 0.f;
+#pragma unroll
+      for (int kk = 0; kk < KS; ++kk) s = mfma32(load8(Qb + c * LD + 16 * kk + 8 * h), kreg[kk], s);
+      const bool need_mask =
+          ((long)kw + kBk - 1 > (long)q0 + off) || (q0 + kBq > p.Nq) || (kw + kBk > p.Nk);
+      float sv[16];
+      bool dem = false;
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        const f32x4 th = *reinterpret_cast<const f32x4*>(thrs + 8 * g + 4 * h);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const int r = 4 * g + e;
+          float x = s[r] * p.scale2;
+          if (need_mask) {
+            const long qq = (long)q0 + 8 * g + 4 * h + e;
+            if (qq >= p.Nq || key >= p.Nk || key > qq + off) x = kNegInf;
+          }
+          sv[r] = x;
+          dem |= (x != kNegInf) && (x >= th[e]);
         }
       }
-      ++n_tiles;
-      __syncthreads();
-
-      const int qlast = min(q0 + kBq - 1, p.Nq - 1);
-      const bool legal_tile = (kw < p.Nk) && ((long)kw <= (long)qlast + off);
-      bool ret = false;
-      if (legal_tile) {
-        ++n_legal;
-        f32x16 s;
-#pragma unroll
-        for (int r = 0; r < 16; ++r) s[r] = 0.f;
-#pragma unroll
-        for (int kk = 0; kk < KS; ++kk) s = mfma32(load8(Qs + c * LD + 16 * kk + 8 * h), kreg[kk], s);
-        const bool need_mask =
-            ((long)kw + kBk - 1 > (long)q0 + off) || (q0 + kBq > p.Nq) || (kw + kBk > p.Nk);
-        float sv[16];
-        bool dem = false;
+      ret = wave_any(dem);
+      if (ret) {
+        ++n_ret;
+        slots += (unsigned long long)kBk * (unsigned)(qlast - q0 + 1);
+        // P = exp2(S - lse)
 #pragma unroll
         for (int g = 0; g < 4; ++g) {
-          const f32x4 th = *reinterpret_cast<const f32x4*>(thrs + 8 * g + 4 * h);
+          const f32x4 l4 = *reinterpret_cast<const f32x4*>(lse2s + 8 * g + 4 * h);
 #pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            const int r = 4 * g + e;
-            float x = s[r] * p.scale2;
-            if (need_mask) {
-              const long qq = (long)q0 + 8 * g + 4 * h + e;
-              if (qq >= p.Nq || key >= p.Nk || key > qq + off) x = kNegInf;
-            }
-            sv[r] = x;
-            dem |= (x != kNegInf) && (x >= th[e]);
+          for (int e = 0; e < 4; ++e) sv[4 * g + e] = exp2f(sv[4 * g + e] - l4[e]);
+        }
+        // dP = dO_i V_w^T
+        f32x16 dp;
+#pragma unroll
+        for (int r = 0; r < 16; ++r) dp[r] = 0.f;
+#pragma unroll
+        for (int kk = 0; kk < KS; ++kk)
+          dp = mfma32(load8(dOb + c * LD + 16 * kk + 8 * h), vreg[kk], dp);
+        float dsv[16];
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+          const f32x4 d4 = *reinterpret_cast<const f32x4*>(Dsv + 8 * g + 4 * h);
+#pragma unroll
+          for (int e = 0; e < 4; ++e) dsv[4 * g + e] = sv[4 * g + e] * (dp[4 * g + e] - d4[e]);
+        }
+        bf16x8 ph[2], pl[2], dh[2], dl[2];
+        split_bf16x8(sv, ph[0], pl[0]);
+        split_bf16x8(sv + 8, ph[1], pl[1]);
+        split_bf16x8(dsv, dh[0], dl[0]);
+        split_bf16x8(dsv + 8, dh[1], dl[1]);
+        // dV^T[d][key] += dO^T[d][q] P[q][key];  dK^T[d][key] += Q^T[d][q] dS[q][key]
+#pragma unroll
+        for (int db = 0; db < DB; ++db) {
+#pragma unroll
+          for (int ks = 0; ks < 2; ++ks) {
+            const int ro = (16 * ks + 4 * h + (t16 >> 2)) * LD + 32 * db + 16 * (G & 1) + 4 * (t16 & 3);
+            const bf16x8 ao = cat(lds_read_tr(dOb + ro), lds_read_tr(dOb + ro + 8 * LD));
+            dvacc[db] = mfma32(ao, ph[ks], dvacc[db]);
+            dvacc[db] = mfma32(ao, pl[ks], dvacc[db]);
+            const bf16x8 aq = cat(lds_read_tr(Qb + ro), lds_read_tr(Qb + ro + 8 * LD));
+            dkacc[db] = mfma32(aq, dh[ks], dkacc[db]);
+            dkacc[db] = mfma32(aq, dl[ks], dkacc[db]);
           }
         }
-        ret = wave_any(dem);
-        if (ret) {
-          ++n_ret;
-          slots += (unsigned long long)kBk * (unsigned)(qlast - q0 + 1);
-          // P = exp2(S - lse)
+        // dS (hi and lo planes) -> LDS as [key][q] for the dQ product
 #pragma unroll
-          for (int g = 0; g < 4; ++g) {
-            const f32x4 l4 = *reinterpret_cast<const f32x4*>(lse2s + 8 * g + 4 * h);
-#pragma unroll
-            for (int e = 0; e < 4; ++e) sv[4 * g + e] = exp2f(sv[4 * g + e] - l4[e]);
-          }
-          // dP = dO_i V_w^T
-          f32x16 dp;
-#pragma unroll
-          for (int r = 0; r < 16; ++r) dp[r] = 0.f;
-#pragma unroll
-          for (int kk = 0; kk < KS; ++kk)
-            dp = mfma32(load8(dOs + c * LD + 16 * kk + 8 * h), vreg[kk], dp);
-          float dsv[16];
-#pragma unroll
-          for (int g = 0; g < 4; ++g) {
-            const f32x4 d4 = *reinterpret_cast<const f32x4*>(Dsv + 8 * g + 4 * h);
-#pragma unroll
-            for (int e = 0; e < 4; ++e) dsv[4 * g + e] = sv[4 * g + e] * (dp[4 * g + e] - d4[e]);
-          }
-          bf16x8 ph[2], pl[2], dh[2], dl[2];
-          split_bf16x8(sv, ph[0], pl[0]);
-          split_bf16x8(sv + 8, ph[1], pl[1]);
-          split_bf16x8(dsv, dh[0], dl[0]);
-          split_bf16x8(dsv + 8, dh[1], dl[1]);
-          // dV^T[d][key] += dO^T[d][q] P[q][key];  dK^T[d][key] += Q^T[d][q] dS[q][key]
-#pragma unroll
-          for (int db = 0; db < DB; ++db) {
-#pragma unroll
-            for (int ks = 0; ks < 2; ++ks) {
-              const int ro = (16 * ks + 4 * h + (t16 >> 2)) * LD + 32 * db + 16 * (G & 1) + 4 * (t16 & 3);
-              const bf16x8 ao = cat(lds_read_tr(dOs + ro), lds_read_tr(dOs + ro + 8 * LD));
-              dvacc[db] = mfma32(ao, ph[ks], dvacc[db]);
-              dvacc[db] = mfma32(ao, pl[ks], dvacc[db]);
-              const bf16x8 aq = cat(lds_read_tr(Qs + ro), lds_read_tr(Qs + ro + 8 * LD));
-              dkacc[db] = mfma32(aq, dh[ks], dkacc[db]);
-              dkacc[db] = mfma32(aq, dl[ks], dkacc[db]);
-            }
-          }
-          // dS (hi and lo planes) -> LDS as [key][q] for the dQ product
-#pragma unroll
-          for (int g = 0; g < 4; ++g) {
-            const bf16x8& hs = dh[g >> 1];
-            const bf16x8& ls = dl[g >> 1];
-            const int o4 = 4 * (g & 1);
-            bf16x4 wh = {hs[o4], hs[o4 + 1], hs[o4 + 2], hs[o4 + 3]};
-            bf16x4 wl = {ls[o4], ls[o4 + 1], ls[o4 + 2], ls[o4 + 3]};
-            *reinterpret_cast<bf16x4*>(dSh + (wave * kBk + c) * DSS + 8 * g + 4 * h) = wh;
-            *reinterpret_cast<bf16x4*>(dSl + (wave * kBk + c) * DSS + 8 * g + 4 * h) = wl;
-          }
-          if (p.row_tiles && c == 0) {
-#pragma unroll
-            for (int r = 0; r < 16; ++r) {
-              const long qq = (long)q0 + 8 * (r >> 2) + 4 * h + (r & 3);
-              if (qq < p.Nq && (long)kw <= qq + off) atomicAdd(p.row_tiles + bhq * p.Nq + qq, 1);
-            }
-          }
+        for (int g = 0; g < 4; ++g) {
+          const bf16x8& hs = dh[g >> 1];
+          const bf16x8& ls = dl[g >> 1];
+          const int o4 = 4 * (g & 1);
+          bf16x4 wh = {hs[o4], hs[o4 + 1], hs[o4 + 2], hs[o4 + 3]};
+          bf16x4 wl = {ls[o4], ls[o4 + 1], ls[o4 + 2], ls[o4 + 3]};
+          *reinterpret_cast<bf16x4*>(dSh + (wave * kBk + c) * DSS + 8 * g + 4 * h) = wh;
+          *reinterpret_cast<bf16x4*>(dSl + (wave * kBk + c) * DSS + 8 * g + 4 * h) = wl;
         }
-      }
-      if (lane == 0) flags[wave] = ret ? 1 : 0;
-      __syncthreads();
-
-      // dQ_i[:, 32 dqb .. +32] = sum over retained tiles of dS K  (fp32 atomics)
-      f32x16 dqacc;
+        if (p.row_tiles && c == 0) {
 #pragma unroll
-      for (int r = 0; r < 16; ++r) dqacc[r] = 0.f;
-      bool any = false;
-#pragma unroll
-      for (int ks = 0; ks < QK / 16; ++ks) {
-        if (!flags[(kq0 + 16 * ks) / kBk]) continue;
-        any = true;
-        const int ao = (kq0 + 16 * ks + 4 * h + (t16 >> 2)) * DSS + 16 * (G & 1) + 4 * (t16 & 3);
-        const bf16x8 ah = cat(lds_read_tr(dSh + ao), lds_read_tr(dSh + ao + 8 * DSS));
-        const bf16x8 al = cat(lds_read_tr(dSl + ao), lds_read_tr(dSl + ao + 8 * DSS));
-        dqacc = mfma32(ah, ktreg[ks], dqacc);
-        dqacc = mfma32(al, ktreg[ks], dqacc);
-      }
-      if (any) {
-        float* dqp = p.dq + (bhq * p.Nq) * D + 32 * dqb + c;
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const long qq = (long)q0 + 8 * (r >> 2) + 4 * h + (r & 3);
-          if (qq < p.Nq) atomicAdd(dqp + qq * D, dqacc[r] * p.scale);
+          for (int r = 0; r < 16; ++r) {
+            const long qq = (long)q0 + 8 * (r >> 2) + 4 * h + (r & 3);
+            if (qq < p.Nq && (long)kw <= qq + off) atomicAdd(p.row_tiles + bhq * p.Nq + qq, 1);
+          }
         }
       }
     }
+    if (lane == 0) flags[wave] = ret ? 1 : 0;
+    __syncthreads();
+
+    // dQ_i[:, 32 dqb .. +32] = sum over retained tiles of dS K  (fp32 atomics)
+    f32x16 dqacc;
+#pragma unroll
+    for (int r = 0; r < 16; ++r) dqacc[r] = 0.f;
+    bool any = false;
+#pragma unroll
+    for (int ks = 0; ks < QK / 16; ++ks) {
+      if (!flags[(kq0 + 16 * ks) / kBk]) continue;
+      any = true;
+      const int ao = (kq0 + 16 * ks + 4 * h + (t16 >> 2)) * DSS + 16 * (G & 1) + 4 * (t16 & 3);
+      const bf16x8 ah = cat(lds_read_tr(dSh + ao), lds_read_tr(dSh + ao + 8 * DSS));
+      const bf16x8 al = cat(lds_read_tr(dSl + ao), lds_read_tr(dSl + ao + 8 * DSS));
+      dqacc = mfma32(ah, ktreg[ks], dqacc);
+      dqacc = mfma32(al, ktreg[ks], dqacc);
+    }
+    if (any) {
+      float* dqp = p.dq + (bhq * p.Nq) * D + 32 * dqb + c;
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const long qq = (long)q0 + 8 * (r >> 2) + 4 * h + (r & 3);
+        if (qq < p.Nq) atomicAdd(dqp + qq * D, dqacc[r] * p.scale);
+      }
+    }
+    if (it + 1 < total) stash(it + 1, buf ^ 1);
+    __syncthreads();
   }
 
   // dK = scale * sum dS^T Q, dV = sum P^T dO; lane (h, c) holds key kw + c
@@ -330,7 +366,7 @@ __global__ __launch_bounds__(256) void mala_bwd_kernel(BwdParams p) {
       atomicAdd(&p.counters[1], (unsigned long long)n_ret);
       atomicAdd(&p.counters[3], slots);
     }
-    if (tid == 0) atomicAdd(&p.counters[2], (unsigned long long)n_tiles);
+    if (tid == 0) atomicAdd(&p.counters[2], (unsigned long long)total);
   }
 }
 

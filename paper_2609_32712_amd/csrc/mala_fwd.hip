@@ -1,11 +1,13 @@
 // MALA forward (Algorithm 1) for gfx950.
 //
-// One workgroup = 4 wavefronts = 128 consecutive query rows of one (batch, query
+// One workgroup = 8 wavefronts = 256 consecutive query rows of one (batch, query
 // head); each wavefront owns 32 rows, which is the decision tile's B_q.  K and V
-// are staged through LDS 64 keys at a time, from the workgroup's highest legal
-// key down to key 0 (the diagonal-first traversal of the Online Sparse Softmax
-// paragraph); inside a stage each wavefront visits its two 32-key decision tiles
-// high half first, so every wavefront sees its tiles in strictly descending order.
+// are staged through double-buffered LDS 64 keys at a time, from the workgroup's
+// highest legal key down to key 0 (the diagonal-first traversal of the Online
+// Sparse Softmax paragraph); the next stage is fetched into registers while the
+// current one is processed.  Inside a stage each wavefront visits its two 32-key
+// decision tiles high half first, so every wavefront sees its tiles in strictly
+// descending order.
 //
 // Per decision tile (32 keys x the wavefront's 32 rows):
 //   S^T = K_j Q_i^T       8 (D = 128) bf16 MFMAs 32x32x16, fp32 accumulate; each
@@ -26,12 +28,18 @@
 namespace mala {
 
 template <int D>
-__global__ __launch_bounds__(256) void mala_fwd_kernel(FwdParams p) {
-  constexpr int KS = D / 16;    // k-steps of the QK product
-  constexpr int DB = D / 32;    // 32-wide output column blocks
-  constexpr int LD = D + 8;     // LDS row stride in bf16 (16-byte pad)
-  __shared__ bf16 Ks[kFwdStage * LD];
-  __shared__ bf16 Vs[kFwdStage * LD];
+__global__ __launch_bounds__(kFwdWaves * 64) void mala_fwd_kernel(FwdParams p) {
+  constexpr int NT = kFwdWaves * 64;     // threads per workgroup
+  constexpr int KS = D / 16;             // k-steps of the QK product
+  constexpr int DB = D / 32;             // 32-wide output column blocks
+  constexpr int LD = D + 8;              // LDS row stride in bf16 (16-byte pad)
+  constexpr int STAGE = kFwdStage * LD;
+  constexpr int CPT = kFwdStage * D / 8 / NT;   // 16-byte chunks per thread per stage
+  static_assert(CPT >= 1 && CPT * NT == kFwdStage * D / 8, "stage must split evenly");
+  // double-buffered K and V stages: the next stage is fetched into registers while
+  // the current one is processed
+  __shared__ __attribute__((aligned(16))) bf16 Ks[2 * STAGE];
+  __shared__ __attribute__((aligned(16))) bf16 Vs[2 * STAGE];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int h = lane >> 5, c = lane & 31, G = lane >> 4, t16 = lane & 15;
@@ -70,24 +78,39 @@ __global__ __launch_bounds__(256) void mala_fwd_kernel(FwdParams p) {
   const int ttop = (int)((qlast_g + off) / kFwdStage);
   unsigned n_legal = 0, n_ret = 0;
 
-  for (int t = ttop; t >= 0; --t) {
-    __syncthreads();
-    constexpr int CH = kFwdStage * D / 8;
+  bf16x8 pk[CPT], pv[CPT];
+  auto fetch = [&](int t) {
 #pragma unroll
-    for (int ch = tid; ch < CH; ch += 256) {
+    for (int e = 0; e < CPT; ++e) {
+      const int ch = tid + NT * e;
       const int row = ch / (D / 8), col = (ch % (D / 8)) * 8;
       const long key = (long)t * kFwdStage + row;
-      bf16x8 kv = zero8(), vv = zero8();
-      if (key < p.Nk) {
-        kv = load8(Kp + key * D + col);
-        vv = load8(Vp + key * D + col);
-      }
-      store8(Ks + row * LD + col, kv);
-      store8(Vs + row * LD + col, vv);
+      const bool ok = key < p.Nk;
+      pk[e] = ok ? load8(Kp + key * D + col) : zero8();
+      pv[e] = ok ? load8(Vp + key * D + col) : zero8();
     }
-    __syncthreads();
-
+  };
+  auto stash = [&](int buf) {
 #pragma unroll
+    for (int e = 0; e < CPT; ++e) {
+      const int ch = tid + NT * e;
+      const int row = ch / (D / 8), col = (ch % (D / 8)) * 8;
+      store8(Ks + buf * STAGE + row * LD + col, pk[e]);
+      store8(Vs + buf * STAGE + row * LD + col, pv[e]);
+    }
+  };
+
+  fetch(ttop);
+  stash(0);
+  __syncthreads();
+
+  for (int t = ttop; t >= 0; --t) {
+    const int buf = (ttop - t) & 1;
+    if (t > 0) fetch(t - 1);
+    const bf16* Kb = Ks + buf * STAGE;
+    const bf16* Vb = Vs + buf * STAGE;
+
+#pragma unroll 1
     for (int sub = 1; sub >= 0; --sub) {
       const int j = 2 * t + sub;
       if (j > jdiag) continue;            // above this wavefront's diagonal
@@ -98,7 +121,7 @@ __global__ __launch_bounds__(256) void mala_fwd_kernel(FwdParams p) {
       f32x16 s;
 #pragma unroll
       for (int r = 0; r < 16; ++r) s[r] = 0.f;
-      const bf16* kr = Ks + (sub * kBk + c) * LD + 8 * h;
+      const bf16* kr = Kb + (sub * kBk + c) * LD + 8 * h;
 #pragma unroll
       for (int kk = 0; kk < KS; ++kk) s = mfma32(load8(kr + 16 * kk), qreg[kk], s);
 
@@ -150,7 +173,7 @@ __global__ __launch_bounds__(256) void mala_fwd_kernel(FwdParams p) {
       for (int db = 0; db < DB; ++db) {
 #pragma unroll
         for (int ks = 0; ks < 2; ++ks) {
-          const bf16* vr = Vs + (sub * kBk + 16 * ks + 4 * h + (t16 >> 2)) * LD + 32 * db +
+          const bf16* vr = Vb + (sub * kBk + 16 * ks + 4 * h + (t16 >> 2)) * LD + 32 * db +
                            16 * (G & 1) + 4 * (t16 & 3);
           const bf16x8 a = cat(lds_read_tr(vr), lds_read_tr(vr + 8 * LD));
           acc[db] = mfma32(a, ph[ks], acc[db]);
@@ -158,6 +181,8 @@ __global__ __launch_bounds__(256) void mala_fwd_kernel(FwdParams p) {
         }
       }
     }
+    if (t > 0) stash(buf ^ 1);
+    __syncthreads();
   }
 
   // epilogue: O <- O / l, LSE = (m + log2 l) * ln 2
@@ -188,7 +213,7 @@ __global__ __launch_bounds__(256) void mala_fwd_kernel(FwdParams p) {
 }
 
 hipError_t launch_fwd(const FwdParams& p, int D, hipStream_t st) {
-  dim3 grid((unsigned)p.nqblk * p.B * p.Hq), block(256);
+  dim3 grid((unsigned)p.nqblk * p.B * p.Hq), block(kFwdWaves * 64);
   if (D == 128)
     hipLaunchKernelGGL(mala_fwd_kernel<128>, grid, block, 0, st, p);
   else

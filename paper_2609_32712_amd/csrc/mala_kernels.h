@@ -11,8 +11,8 @@ constexpr int kBq = 32;      // query rows per decision tile = rows of one wavef
 constexpr int kBk = 32;      // keys per decision tile
 constexpr int kDecBk = 32;   // keys per decode decision tile
 
-constexpr int kFwdWaves = 4;                 // wavefronts per forward workgroup
-constexpr int kFwdRows = kFwdWaves * kBq;    // 128 query rows per workgroup
+constexpr int kFwdWaves = 8;                 // wavefronts per forward workgroup
+constexpr int kFwdRows = kFwdWaves * kBq;    // 256 query rows per workgroup
 constexpr int kFwdStage = 64;                // keys per K/V stage in LDS
 constexpr int kBwdKeys = 128;                // keys per backward workgroup (4 waves x kBk)
 constexpr int kDecStride = 4;                // extra floats per decode partial (lse, count, pad)
