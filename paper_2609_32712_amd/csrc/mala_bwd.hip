@@ -84,15 +84,14 @@ template <int D>
 __global__ __launch_bounds__(256) void mala_bwd_kernel(BwdParams p) {
   constexpr int KS = D / 16;       // k-steps over head_dim
   constexpr int DB = D / 32;       // 32-wide column blocks
-  constexpr int LD = D + 8;        // LDS row stride (bf16)
-  constexpr int DSS = kBq + 8;     // dS row stride: [key][q]
+  constexpr int DSS = kBq + 16;    // dS row stride [key][q]: 24 dwords, conflict-free tr reads
   constexpr int WPB = 4 / DB;      // wavefronts per dQ column block
   constexpr int QK = kBwdKeys / WPB;   // keys one wavefront sums for its dQ slice
-  constexpr int TILE = kBq * LD;       // one Q or dO tile in LDS
+  constexpr int TILE = tile_elems<D>(kBq);   // one Q or dO tile in LDS
   constexpr int CPT = kBq * D / 8 / 256;   // 16-byte chunks per thread per tile
   // K_j (row-major) is only needed until the dQ operands are in registers; its LDS
   // is then reused for the two bf16 planes (hi, lo) of dS stored as [key][q].
-  constexpr int KT_ELEMS = kBwdKeys * LD;
+  constexpr int KT_ELEMS = tile_elems<D>(kBwdKeys);
   constexpr int DS_ELEMS = 2 * kBwdKeys * DSS;
   __shared__ __attribute__((aligned(16))) bf16 shared_kt_ds[KT_ELEMS > DS_ELEMS ? KT_ELEMS : DS_ELEMS];
   // double-buffered query tiles: the next tile is fetched into registers while the
@@ -123,7 +122,7 @@ __global__ __launch_bounds__(256) void mala_bwd_kernel(BwdParams p) {
   for (int ch = tid; ch < kBwdKeys * D / 8; ch += 256) {
     const int row = ch / (D / 8), col = (ch % (D / 8)) * 8;
     const long kk = (long)kb0 + row;
-    store8(Kt + row * LD + col, kk < p.Nk ? load8(Kp + kk * D + col) : zero8());
+    store8(Kt + tile_off<D>(row, col), kk < p.Nk ? load8(Kp + kk * D + col) : zero8());
   }
   // K_w, V_w rows as B operands of S = Q K^T and dP = dO V^T
   bf16x8 kreg[KS], vreg[KS];
@@ -139,9 +138,9 @@ __global__ __launch_bounds__(256) void mala_bwd_kernel(BwdParams p) {
   bf16x8 ktreg[QK / 16];
 #pragma unroll
   for (int ks = 0; ks < QK / 16; ++ks) {
-    const bf16* kr = Kt + (kq0 + 16 * ks + 4 * h + (t16 >> 2)) * LD + 32 * dqb + 16 * (G & 1) +
-                     4 * (t16 & 3);
-    ktreg[ks] = cat(lds_read_tr(kr), lds_read_tr(kr + 8 * LD));
+    const int krow = kq0 + 16 * ks + 4 * h + (t16 >> 2);
+    const int kcol = 32 * dqb + 16 * (G & 1) + 4 * (t16 & 3);
+    ktreg[ks] = cat(lds_read_tr(Kt + tile_off<D>(krow, kcol)), lds_read_tr(Kt + tile_off<D>(krow + 8, kcol)));
   }
 
   f32x16 dvacc[DB], dkacc[DB];
@@ -187,8 +186,8 @@ __global__ __launch_bounds__(256) void mala_bwd_kernel(BwdParams p) {
     for (int e = 0; e < CPT; ++e) {
       const int ch = tid + 256 * e;
       const int row = ch / (D / 8), col = (ch % (D / 8)) * 8;
-      store8(Qs + buf * TILE + row * LD + col, pq[e]);
-      store8(dOs + buf * TILE + row * LD + col, pdo[e]);
+      store8(Qs + buf * TILE + tile_off<D>(row, col), pq[e]);
+      store8(dOs + buf * TILE + tile_off<D>(row, col), pdo[e]);
     }
     if (tid < kBq) {
       const long qq = (long)q0 + tid;
@@ -226,15 +225,29 @@ __global__ __launch_bounds__(256) void mala_bwd_kernel(BwdParams p) {
     bool ret = false;
     if (legal_tile) {
       ++n_legal;
-      f32x16 s;
+      // S = Q_i K_w^T as two independent chains (even / odd k-steps), operands read first
+      f32x16 s, s_odd;
 #pragma unroll
-      for (int r = 0; r < 16; ++r) s[r] = 0.f;
+      for (int r = 0; r < 16; ++r) s[r] = s_odd[r] = 0.f;
+      {
+        bf16x8 qa[KS];
 #pragma unroll
-      for (int kk = 0; kk < KS; ++kk) s = mfma32(load8(Qb + c * LD + 16 * kk + 8 * h), kreg[kk], s);
+        for (int kk = 0; kk < KS; ++kk) qa[kk] = load8(Qb + tile_off<D>(c, 16 * kk + 8 * h));
+#pragma unroll
+        for (int kk = 0; kk < KS; kk += 2) {
+          s = mfma32(qa[kk], kreg[kk], s);
+          s_odd = mfma32(qa[kk + 1], kreg[kk + 1], s_odd);
+        }
+      }
+      s += s_odd;
       const bool need_mask =
           ((long)kw + kBk - 1 > (long)q0 + off) || (q0 + kBq > p.Nq) || (kw + kBk > p.Nk);
       float sv[16];
       bool dem = false;
+      // rows of this lane: q0 + 8 g + 4 h + e; entry legal iff row < Nq, key < Nk and
+      // key <= row + off, i.e. 8 g + e in [klo, qlim)
+      const int klo = key < p.Nk ? (int)((long)key - off - q0) - 4 * h : 1000000;
+      const int qlim = p.Nq - q0 - 4 * h;
 #pragma unroll
       for (int g = 0; g < 4; ++g) {
         const f32x4 th = *reinterpret_cast<const f32x4*>(thrs + 8 * g + 4 * h);
@@ -242,10 +255,7 @@ __global__ __launch_bounds__(256) void mala_bwd_kernel(BwdParams p) {
         for (int e = 0; e < 4; ++e) {
           const int r = 4 * g + e;
           float x = s[r] * p.scale2;
-          if (need_mask) {
-            const long qq = (long)q0 + 8 * g + 4 * h + e;
-            if (qq >= p.Nq || key >= p.Nk || key > qq + off) x = kNegInf;
-          }
+          if (need_mask && (8 * g + e < klo || 8 * g + e >= qlim)) x = kNegInf;
           sv[r] = x;
           dem |= (x != kNegInf) && (x >= th[e]);
         }
@@ -259,15 +269,23 @@ __global__ __launch_bounds__(256) void mala_bwd_kernel(BwdParams p) {
         for (int g = 0; g < 4; ++g) {
           const f32x4 l4 = *reinterpret_cast<const f32x4*>(lse2s + 8 * g + 4 * h);
 #pragma unroll
-          for (int e = 0; e < 4; ++e) sv[4 * g + e] = exp2f(sv[4 * g + e] - l4[e]);
+          for (int e = 0; e < 4; ++e) sv[4 * g + e] = fast_exp2(sv[4 * g + e] - l4[e]);
         }
         // dP = dO_i V_w^T
-        f32x16 dp;
+        f32x16 dp, dp_odd;
 #pragma unroll
-        for (int r = 0; r < 16; ++r) dp[r] = 0.f;
+        for (int r = 0; r < 16; ++r) dp[r] = dp_odd[r] = 0.f;
+        {
+          bf16x8 oa[KS];
 #pragma unroll
-        for (int kk = 0; kk < KS; ++kk)
-          dp = mfma32(load8(dOb + c * LD + 16 * kk + 8 * h), vreg[kk], dp);
+          for (int kk = 0; kk < KS; ++kk) oa[kk] = load8(dOb + tile_off<D>(c, 16 * kk + 8 * h));
+#pragma unroll
+          for (int kk = 0; kk < KS; kk += 2) {
+            dp = mfma32(oa[kk], vreg[kk], dp);
+            dp_odd = mfma32(oa[kk + 1], vreg[kk + 1], dp_odd);
+          }
+        }
+        dp += dp_odd;
         float dsv[16];
 #pragma unroll
         for (int g = 0; g < 4; ++g) {
@@ -285,11 +303,13 @@ __global__ __launch_bounds__(256) void mala_bwd_kernel(BwdParams p) {
         for (int db = 0; db < DB; ++db) {
 #pragma unroll
           for (int ks = 0; ks < 2; ++ks) {
-            const int ro = (16 * ks + 4 * h + (t16 >> 2)) * LD + 32 * db + 16 * (G & 1) + 4 * (t16 & 3);
-            const bf16x8 ao = cat(lds_read_tr(dOb + ro), lds_read_tr(dOb + ro + 8 * LD));
+            const int trow = 16 * ks + 4 * h + (t16 >> 2);
+            const int tcol = 32 * db + 16 * (G & 1) + 4 * (t16 & 3);
+            const int ro = tile_off<D>(trow, tcol), ro8 = tile_off<D>(trow + 8, tcol);
+            const bf16x8 ao = cat(lds_read_tr(dOb + ro), lds_read_tr(dOb + ro8));
             dvacc[db] = mfma32(ao, ph[ks], dvacc[db]);
             dvacc[db] = mfma32(ao, pl[ks], dvacc[db]);
-            const bf16x8 aq = cat(lds_read_tr(Qb + ro), lds_read_tr(Qb + ro + 8 * LD));
+            const bf16x8 aq = cat(lds_read_tr(Qb + ro), lds_read_tr(Qb + ro8));
             dkacc[db] = mfma32(aq, dh[ks], dkacc[db]);
             dkacc[db] = mfma32(aq, dl[ks], dkacc[db]);
           }
@@ -305,22 +325,30 @@ __global__ __launch_bounds__(256) void mala_bwd_kernel(BwdParams p) {
           *reinterpret_cast<bf16x4*>(dSh + (wave * kBk + c) * DSS + 8 * g + 4 * h) = wh;
           *reinterpret_cast<bf16x4*>(dSl + (wave * kBk + c) * DSS + 8 * g + 4 * h) = wl;
         }
-        if (p.row_tiles && c == 0) {
-#pragma unroll
-          for (int r = 0; r < 16; ++r) {
-            const long qq = (long)q0 + 8 * (r >> 2) + 4 * h + (r & 3);
-            if (qq < p.Nq && (long)kw <= qq + off) atomicAdd(p.row_tiles + bhq * p.Nq + qq, 1);
-          }
-        }
       }
     }
     if (lane == 0) flags[wave] = ret ? 1 : 0;
     __syncthreads();
 
-    // dQ_i[:, 32 dqb .. +32] = sum over retained tiles of dS K  (fp32 atomics)
-    f32x16 dqacc;
+    // per-row statistics: retained tiles of this workgroup in which the row has a key
+    if (p.row_tiles && wave == 0 && lane < kBq) {
+      const long qq = (long)q0 + lane;
+      if (qq < p.Nq) {
+        int n = 0;
 #pragma unroll
-    for (int r = 0; r < 16; ++r) dqacc[r] = 0.f;
+        for (int w = 0; w < 4; ++w) {
+          const long kww = (long)kb0 + w * kBk;
+          n += (flags[w] && kww < p.Nk && kww <= qq + off) ? 1 : 0;
+        }
+        if (n) atomicAdd(p.row_tiles + bhq * p.Nq + qq, n);
+      }
+    }
+
+    // dQ_i[:, 32 dqb .. +32] = sum over retained tiles of dS K  (fp32 atomics)
+    // hi and lo planes accumulate in separate chains
+    f32x16 dqacc, dqlo;
+#pragma unroll
+    for (int r = 0; r < 16; ++r) dqacc[r] = dqlo[r] = 0.f;
     bool any = false;
 #pragma unroll
     for (int ks = 0; ks < QK / 16; ++ks) {
@@ -330,8 +358,9 @@ __global__ __launch_bounds__(256) void mala_bwd_kernel(BwdParams p) {
       const bf16x8 ah = cat(lds_read_tr(dSh + ao), lds_read_tr(dSh + ao + 8 * DSS));
       const bf16x8 al = cat(lds_read_tr(dSl + ao), lds_read_tr(dSl + ao + 8 * DSS));
       dqacc = mfma32(ah, ktreg[ks], dqacc);
-      dqacc = mfma32(al, ktreg[ks], dqacc);
+      dqlo = mfma32(al, ktreg[ks], dqlo);
     }
+    dqacc += dqlo;
     if (any) {
       float* dqp = p.dq + (bhq * p.Nq) * D + 32 * dqb + c;
 #pragma unroll

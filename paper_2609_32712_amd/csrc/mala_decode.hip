@@ -85,7 +85,7 @@ __global__ __launch_bounds__(64) void mala_decode_split_kernel(DecParams p) {
     }
     mt = fmaxf(mt, __shfl_xor(mt, 16));
     mt = fmaxf(mt, __shfl_xor(mt, 32));
-    const bool demand = head_valid && (l == 0.f || (mt - m - log2f(l) >= p.thr2));
+    const bool demand = head_valid && (l == 0.f || (mt - m - fast_log2(l) >= p.thr2));
     if (!wave_any(demand)) continue;
 
     // V tile -> LDS (rows beyond Nk are zero)
@@ -101,12 +101,12 @@ __global__ __launch_bounds__(64) void mala_decode_split_kernel(DecParams p) {
     float alpha = 1.f, m_new = m;
     if (demand) {
       m_new = fmaxf(m, mt);
-      alpha = exp2f(m - m_new);
+      alpha = fast_exp2(m - m_new);
     }
     float ps = 0.f;
 #pragma unroll
     for (int r = 0; r < 8; ++r) {
-      const float e = demand ? exp2f(sv[r] - m_new) : 0.f;
+      const float e = demand ? fast_exp2(sv[r] - m_new) : 0.f;
       sv[r] = e;
       ps += e;
     }
@@ -136,7 +136,7 @@ __global__ __launch_bounds__(64) void mala_decode_split_kernel(DecParams p) {
     for (int db = 0; db < NDB; ++db)
       *reinterpret_cast<f32x4*>(pp + 16 * db + 4 * g) = acc[db] * inv;
     if (g == 0) {
-      pp[D] = l > 0.f ? (m + log2f(l)) * kLn2 : kNegInf;
+      pp[D] = l > 0.f ? (m + fast_log2(l)) * kLn2 : kNegInf;
       pp[D + 1] = __int_as_float(cnt);
     }
   }

@@ -61,6 +61,32 @@ __device__ __forceinline__ float halves_sum(float x) {
   return __uint_as_float(r[0]) + __uint_as_float(r[1]);
 }
 
+// Offset (in bf16 elements) of element (row, col) of a row-major [rows][D] bf16 tile
+// in LDS.  D = 128 rows are 256 bytes with their 16-byte chunks XOR-swizzled by
+// f(row) = 2 * (row % 8) + (row / 8) % 2, which keeps both access patterns of the
+// kernels free of bank conflicts: 16 lanes reading one chunk of 16 consecutive
+// rows (ds_read_b128) and 16 lanes reading two adjacent chunks of 4 consecutive
+// rows (ds_read_b64_tr_b16).  D = 64 rows are padded to 72 elements.
+template <int D>
+__device__ __forceinline__ int tile_off(int row, int col) {
+  if constexpr (D == 128) {
+    const int f = ((row & 7) << 1) | ((row >> 3) & 1);
+    return row * 128 + ((((col >> 3) ^ f)) << 3) + (col & 7);
+  } else {
+    return row * (D + 8) + col;
+  }
+}
+template <int D>
+constexpr int tile_elems(int rows) {
+  return D == 128 ? rows * 128 : rows * (D + 8);
+}
+
+// Hardware base-2 exponential / logarithm (v_exp_f32 / v_log_f32, ~1 ulp on normal
+// results).  The softmax arguments are <= 0, so the results lie in [0, 1]; values
+// below 2^-126 may flush to zero, which no tolerance here can see.
+__device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
+__device__ __forceinline__ float fast_log2(float x) { return __builtin_amdgcn_logf(x); }
+
 __device__ __forceinline__ bool wave_any(bool p) { return __builtin_amdgcn_ballot_w64(p) != 0; }
 
 __device__ __forceinline__ bf16x8 zero8() {

@@ -17,8 +17,8 @@
 //                         rowmax - m - log2(l) < log2(tau) - log2(L_q) (base-2 units,
 //                         equivalent to the natural-log test), rows with l == 0
 //                         always retain; one ballot makes the branch wave-uniform;
-//   retained path         m, l, rescale of O (only if some row's max moved),
-//                         P = exp2(S - m) split into two bf16 terms in place,
+//   retained path         lazy rescale of O and l (only when some row's max grew by
+//                         more than 2^8), P = exp2(S - m) split into two bf16 terms,
 //                         O^T += V^T P^T (2 x 8 MFMAs, V^T operand through
 //                         ds_read_b64_tr_b16).
 // A skipped tile costs its QK MFMAs, one max reduction and one compare.
@@ -32,8 +32,7 @@ __global__ __launch_bounds__(kFwdWaves * 64) void mala_fwd_kernel(FwdParams p) {
   constexpr int NT = kFwdWaves * 64;     // threads per workgroup
   constexpr int KS = D / 16;             // k-steps of the QK product
   constexpr int DB = D / 32;             // 32-wide output column blocks
-  constexpr int LD = D + 8;              // LDS row stride in bf16 (16-byte pad)
-  constexpr int STAGE = kFwdStage * LD;
+  constexpr int STAGE = tile_elems<D>(kFwdStage);
   constexpr int CPT = kFwdStage * D / 8 / NT;   // 16-byte chunks per thread per stage
   static_assert(CPT >= 1 && CPT * NT == kFwdStage * D / 8, "stage must split evenly");
   // double-buffered K and V stages: the next stage is fetched into registers while
@@ -95,8 +94,8 @@ __global__ __launch_bounds__(kFwdWaves * 64) void mala_fwd_kernel(FwdParams p) {
     for (int e = 0; e < CPT; ++e) {
       const int ch = tid + NT * e;
       const int row = ch / (D / 8), col = (ch % (D / 8)) * 8;
-      store8(Ks + buf * STAGE + row * LD + col, pk[e]);
-      store8(Vs + buf * STAGE + row * LD + col, pv[e]);
+      store8(Ks + buf * STAGE + tile_off<D>(row, col), pk[e]);
+      store8(Vs + buf * STAGE + tile_off<D>(row, col), pv[e]);
     }
   };
 
@@ -110,75 +109,111 @@ __global__ __launch_bounds__(kFwdWaves * 64) void mala_fwd_kernel(FwdParams p) {
     const bf16* Kb = Ks + buf * STAGE;
     const bf16* Vb = Vs + buf * STAGE;
 
-#pragma unroll 1
-    for (int sub = 1; sub >= 0; --sub) {
-      const int j = 2 * t + sub;
-      if (j > jdiag) continue;            // above this wavefront's diagonal
-      const long kb = (long)j * kBk;
-      ++n_legal;
-
-      // S^T[key][q] = K_j Q^T
-      f32x16 s;
+    // Score discovery for both 32-key decision tiles of the stage at once (two
+    // independent accumulators; all K operands are read from LDS first).
+    if (2 * t <= jdiag) {
+      f32x16 s2[2];
 #pragma unroll
-      for (int r = 0; r < 16; ++r) s[r] = 0.f;
-      const bf16* kr = Kb + (sub * kBk + c) * LD + 8 * h;
+      for (int u = 0; u < 2; ++u)
 #pragma unroll
-      for (int kk = 0; kk < KS; ++kk) s = mfma32(load8(kr + 16 * kk), qreg[kk], s);
-
-      const bool need_mask = (kb + kBk - 1 > (long)q0w + off) || (q0w + kBq > p.Nq);
-      float sv[16];
-      float mt = kNegInf;
+        for (int r = 0; r < 16; ++r) s2[u][r] = 0.f;
+      {
+        bf16x8 ka[2][KS];
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        float x = s[r] * p.scale2;
-        if (need_mask) {
-          const long key = kb + 8 * (r >> 2) + 4 * h + (r & 3);
-          if (!row_valid || key > qrow + off) x = kNegInf;
+        for (int kk = 0; kk < KS; ++kk) {
+          ka[1][kk] = load8(Kb + tile_off<D>(kBk + c, 16 * kk + 8 * h));
+          ka[0][kk] = load8(Kb + tile_off<D>(c, 16 * kk + 8 * h));
         }
-        sv[r] = x;
-        mt = fmaxf(mt, x);
-      }
-      mt = halves_max(mt);
-
-      // the online test (rows with no legal key in the tile do not vote)
-      const bool voter = row_valid && (kb <= qrow + off);
-      const bool demand = voter && (l == 0.f || (mt - m - log2f(l) >= thr));
-      if (!wave_any(demand)) continue;    // skipped: m, l and O unchanged
-      ++n_ret;
-      cnt += voter ? 1 : 0;
-
-      const float m_new = fmaxf(m, mt);
-      const float alpha = (m_new == kNegInf) ? 1.f : exp2f(m - m_new);
-      float ps = 0.f;
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const float e = (sv[r] == kNegInf) ? 0.f : exp2f(sv[r] - m_new);
-        sv[r] = e;
-        ps += e;
+        for (int kk = 0; kk < KS; ++kk) {
+          s2[1] = mfma32(ka[1][kk], qreg[kk], s2[1]);
+          s2[0] = mfma32(ka[0][kk], qreg[kk], s2[0]);
+        }
       }
-      ps = halves_sum(ps);
-      l = alpha * l + ps;
-      m = m_new;
-      if (wave_any(alpha != 1.f)) {
+      // the two tiles in descending key order: the high half first
+#pragma unroll
+      for (int sub = 1; sub >= 0; --sub) {
+        const int j = 2 * t + sub;
+        if (j > jdiag) continue;            // above this wavefront's diagonal
+        const long kb = (long)j * kBk;
+        ++n_legal;
+        const f32x16& s = s2[sub];
+
+        const bool need_mask = (kb + kBk - 1 > (long)q0w + off) || (q0w + kBq > p.Nq);
+        float sv[16];
+        float mt = kNegInf;
+        if (need_mask) {
+          // keys of this lane: kb + 8 (r / 4) + 4 h + r % 4; legal iff key <= qrow + off
+          const int lim = row_valid ? (int)((long)qrow + off - kb) - 4 * h : -1000000;
+#pragma unroll
+          for (int r = 0; r < 16; ++r) {
+            const float x = (8 * (r >> 2) + (r & 3) <= lim) ? s[r] * p.scale2 : kNegInf;
+            sv[r] = x;
+            mt = fmaxf(mt, x);
+          }
+        } else {
+#pragma unroll
+          for (int r = 0; r < 16; ++r) {
+            sv[r] = s[r] * p.scale2;
+            mt = fmaxf(mt, sv[r]);
+          }
+        }
+        mt = halves_max(mt);
+
+        // the online test (rows with no legal key in the tile do not vote); m + log2(l)
+        // is log2 of the retained normalizer whichever reference m the row uses
+        const bool voter = row_valid && (kb <= qrow + off);
+        const bool demand = voter && (l == 0.f || (mt - m - fast_log2(l) >= thr));
+        if (!wave_any(demand)) continue;    // skipped: m, l and O unchanged
+        ++n_ret;
+        cnt += voter ? 1 : 0;
+
+        // Lazy rescaling: a row's reference m moves only when some row of the
+        // wavefront would otherwise see P = exp2(s - m) above 2^8; O and l are then
+        // rescaled.  The result is the same softmax; P stays in [0, 2^8].
+        if (wave_any(mt > m + 8.f)) {
+          const float m_new = fmaxf(m, mt);
+          const float alpha = (m_new == kNegInf) ? 1.f : fast_exp2(m - m_new);
+          l *= alpha;
+          m = m_new;
+#pragma unroll
+          for (int db = 0; db < DB; ++db)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) acc[db][r] *= alpha;
+        }
+        // a row with no legal key so far keeps m = -inf: shift by 0 so exp2(-inf) = 0
+        const float shift = (m == kNegInf) ? 0.f : m;
+        float ps = 0.f;
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          sv[r] = fast_exp2(sv[r] - shift);
+          ps += sv[r];
+        }
+        l += halves_sum(ps);
+        // P as two bf16 terms: the backward's D = rowsum(O * dO) cancels against
+        // dP for dominant keys, so O must be accurate well beyond one bf16 rounding
+        bf16x8 ph[2], pl[2];
+        split_bf16x8(sv, ph[0], pl[0]);
+        split_bf16x8(sv + 8, ph[1], pl[1]);
+        // O^T[d][q] += V^T[d][key] P^T[key][q]; V^T rows through transposed LDS reads
+        bf16x8 va[DB][2];
 #pragma unroll
         for (int db = 0; db < DB; ++db)
 #pragma unroll
-          for (int r = 0; r < 16; ++r) acc[db][r] *= alpha;
-      }
-      bf16x8 ph[2], pl[2];
-      split_bf16x8(sv, ph[0], pl[0]);
-      split_bf16x8(sv + 8, ph[1], pl[1]);
-      // O^T[d][q] += V^T[d][key] P^T[key][q]; V^T rows through transposed LDS reads
+          for (int ks = 0; ks < 2; ++ks) {
+            const int vrow = sub * kBk + 16 * ks + 4 * h + (t16 >> 2);
+            const int vcol = 32 * db + 16 * (G & 1) + 4 * (t16 & 3);
+            va[db][ks] = cat(lds_read_tr(Vb + tile_off<D>(vrow, vcol)),
+                             lds_read_tr(Vb + tile_off<D>(vrow + 8, vcol)));
+          }
 #pragma unroll
-      for (int db = 0; db < DB; ++db) {
+        for (int ks = 0; ks < 2; ++ks)
 #pragma unroll
-        for (int ks = 0; ks < 2; ++ks) {
-          const bf16* vr = Vb + (sub * kBk + 16 * ks + 4 * h + (t16 >> 2)) * LD + 32 * db +
-                           16 * (G & 1) + 4 * (t16 & 3);
-          const bf16x8 a = cat(lds_read_tr(vr), lds_read_tr(vr + 8 * LD));
-          acc[db] = mfma32(a, ph[ks], acc[db]);
-          acc[db] = mfma32(a, pl[ks], acc[db]);
-        }
+          for (int db = 0; db < DB; ++db) acc[db] = mfma32(va[db][ks], ph[ks], acc[db]);
+#pragma unroll
+        for (int ks = 0; ks < 2; ++ks)
+#pragma unroll
+          for (int db = 0; db < DB; ++db) acc[db] = mfma32(va[db][ks], pl[ks], acc[db]);
       }
     }
     if (t > 0) stash(buf ^ 1);
@@ -198,7 +233,7 @@ __global__ __launch_bounds__(kFwdWaves * 64) void mala_fwd_kernel(FwdParams p) {
         *reinterpret_cast<f32x4*>(op + 32 * db + 8 * g + 4 * h) = v4;
       }
     if (h == 0) {
-      p.lse[(long)bh * p.Nq + qrow] = (m + log2f(l)) * kLn2;
+      p.lse[(long)bh * p.Nq + qrow] = (m + fast_log2(l)) * kLn2;
       if (p.row_tiles) p.row_tiles[(long)bh * p.Nq + qrow] = cnt;
     }
   }
