@@ -117,10 +117,11 @@ size_t mala_bwd_workspace_size(int B, int Hq, int Hkv, int Nq, int Nk, int D);
  * pass the offline test against the saved lse.
  *   q: bf16 [B, Hq, Nq, D]; k, v: bf16 [B, Hkv, Nk, D]; o: fp32 [B, Hq, Nq, D] and
  *   lse: fp32 [B, Hq, Nq] as returned by mala_fwd; dout: bf16 [B, Hq, Nq, D].
- *   dq: fp32 [B, Hq, Nq, D] out (accumulated with fp32 atomics after the library
- *       clears it; summation order, and so the last bits, may vary run to run);
- *   dk, dv: fp32 [B, Hkv, Nk, D] out (summed over the GQA group inside one
- *       workgroup, no atomics: bitwise reproducible);
+ *   dq: fp32 [B, Hq, Nq, D] out; dk, dv: fp32 [B, Hkv, Nk, D] out (dK and dV of a
+ *       KV head summed over its GQA group).  No atomics: all three are bitwise
+ *       reproducible.  dQ comes from a query-major pass that recomputes the
+ *       tile scores with the same arithmetic, so it uses exactly the tiles the
+ *       key-major dK/dV pass retains;
  *   row_tiles: int32 [B, Hq, Nq] or NULL out; counters: int64 [4] or NULL out.
  *   workspace: device memory of at least mala_bwd_workspace_size(...) bytes,
  *   16-byte aligned, owned by the caller, not read by the caller afterwards.

@@ -123,10 +123,6 @@ int mala_bwd(const void* q, const void* k, const void* v, const float* o, const 
   hipStream_t s = (hipStream_t)stream;
   hipError_t e;
   const long rows = (long)B * Hq * Nq;
-  if ((e = mala::launch_fill_zero(dq, (size_t)rows * D * sizeof(float), s)) != hipSuccess)
-    return hip_fail(e, "mala_bwd: clearing dq");
-  if (row_tiles && (e = mala::launch_fill_zero(row_tiles, (size_t)rows * sizeof(int32_t), s)) != hipSuccess)
-    return hip_fail(e, "mala_bwd: clearing row_tiles");
   if (counters && (e = mala::launch_fill_zero(counters, 4 * sizeof(int64_t), s)) != hipSuccess)
     return hip_fail(e, "mala_bwd: clearing counters");
   float* dvec = (float*)workspace;
