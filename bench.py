@@ -144,10 +144,11 @@ def source_sha(path):
         return hashlib.sha256(fh.read()).hexdigest()[:16]
 
 
-def traffic_from_profiles(kernel_src, launches_per_step=1):
-    """HBM bytes per launch from committed rocprofv3 counter summaries, or None if
-    the kernel source changed since they were taken."""
-    p = os.path.join(ROOT, "profiles", "mala_bwd_kernel_traffic.json")
+def traffic_from_profiles(kernel_src):
+    """HBM bytes per launch of the backward operator from the committed rocprofv3
+    counter summary (FETCH_SIZE x 2.0 + WRITE_SIZE x 1.0, calibrated on a plain
+    copy), or None if the kernel source changed since the counters were taken."""
+    p = os.path.join(ROOT, "profiles", "mala_bwd_traffic_128k.json")
     if not os.path.exists(p):
         return None
     with open(p) as fh:
@@ -341,7 +342,7 @@ def main():
             "decode_batch": dec.w.B, "decode_splits": dec.splits,
         },
         "roofline": {
-            "kernel": "mala_bwd_kernel",
+            "kernel": "mala_bwd (preprocess + dK/dV + dQ kernels)",
             "bound": "mfma",
             "achieved": round(achieved, 1),
             "peak": PEAK_BF16_TFLOPS,

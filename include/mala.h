@@ -132,7 +132,7 @@ int mala_bwd(const void* q, const void* k, const void* v, const float* o, const 
              int Nq, int Nk, int D, int causal, float scale, float tau, void* stream);
 
 /* Bytes of device workspace mala_decode needs: fp32 split partials
- * [B, Hq, num_splits, D + 2]. */
+ * [B, Hq, num_splits, D + 4] (O_s / l_s, lse_s, retained count, pad). */
 size_t mala_decode_workspace_size(int B, int Hq, int D, int num_splits);
 
 /*

@@ -5,7 +5,7 @@
 // keys of one (batch, KV head), with their K and V rows in LDS, and keeps their dK
 // and dV in registers for the whole kernel (no atomics, bitwise reproducible); it
 // loops over every query head of the GQA group and over the query tiles from the
-// diagonal to the end.  Eight wavefronts in two roles: wavefront w accumulates dV
+// end down to the diagonal.  Eight wavefronts in two roles: wavefront w accumulates dV
 // (w < 4) or dK (w >= 4) of keys [32 (w % 4), +32), so each wavefront's work on one
 // query tile is exactly one 32 x 32 decision tile, with a 64-register accumulator
 // (two wavefronts per SIMD).  Query tiles (Q, dO and the per-row base-2 LSE,
@@ -104,30 +104,48 @@ __device__ __forceinline__ f32x16 qk_tile(const bf16x8 (&a)[KS], const bf16x8 (&
 
 // Offline test of one tile in the C layout of qk_tile (lane = key column, rows
 // 8 g + 4 h + e of the query tile): base-2 masked scores into sv; returns whether
-// some legal entry of this lane reaches its row's threshold (lse2 + log2(tau / L)).
-// klo / qlim bound the legal rows: 8 g + e in [klo, qlim).
+// some legal entry of this lane reaches its row's threshold (lse2 + log2(tau / L)),
+// evaluated as max(x - thr) >= 0 (for finite x this is exactly x >= thr; padded
+// rows have thr = +inf, tau = 0 gives thr = -inf).  klo / qlim bound the legal
+// rows: 8 g + e in [klo, qlim); the bounds are only consulted on tiles that cross
+// the diagonal or the end of the sequence (need_mask, uniform over the wavefront).
 __device__ __forceinline__ bool offline_entries(const f32x16& s, float scale2, bool need_mask,
                                                 int klo, int qlim, const float* thrs, int h,
                                                 float (&sv)[16]) {
-  bool dem = false;
+  // no FMA contraction: both backward kernels must round identically
+#pragma clang fp contract(off)
+  float dm = kNegInf;
+  if (need_mask) {
 #pragma unroll
-  for (int g = 0; g < 4; ++g) {
-    const f32x4 th = *reinterpret_cast<const f32x4*>(thrs + 8 * g + 4 * h);
+    for (int g = 0; g < 4; ++g) {
+      const f32x4 th = *reinterpret_cast<const f32x4*>(thrs + 8 * g + 4 * h);
 #pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      const int r = 4 * g + e;
-      float x = s[r] * scale2;
-      if (need_mask && (8 * g + e < klo || 8 * g + e >= qlim)) x = kNegInf;
-      sv[r] = x;
-      dem |= (x != kNegInf) && (x >= th[e]);
+      for (int e = 0; e < 4; ++e) {
+        const bool legal = (8 * g + e >= klo) && (8 * g + e < qlim);
+        const float x = s[4 * g + e] * scale2;
+        sv[4 * g + e] = legal ? x : kNegInf;
+        dm = fmaxf(dm, legal ? x - th[e] : kNegInf);
+      }
+    }
+  } else {
+#pragma unroll
+    for (int g = 0; g < 4; ++g) {
+      const f32x4 th = *reinterpret_cast<const f32x4*>(thrs + 8 * g + 4 * h);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const float x = s[4 * g + e] * scale2;
+        sv[4 * g + e] = x;
+        dm = fmaxf(dm, x - th[e]);
+      }
     }
   }
-  return dem;
+  return dm >= 0.f;
 }
 
 // Per-row vectors of a query tile: base-2 lse, test threshold, D_q.
 __device__ __forceinline__ void row_vectors(const BwdParams& p, long bhq, long qq, long off,
                                             float* lse2, float* thr, float* dv) {
+#pragma clang fp contract(off)
   if (qq < p.Nq) {
     const float l2 = p.lse[bhq * p.Nq + qq] * kLog2e;
     *lse2 = l2;
@@ -196,9 +214,14 @@ __global__ __launch_bounds__(512) void mala_bwd_dkdv_kernel(BwdParams p) {
   // prefetch registers of the next query tile
   bf16x8 pq = zero8(), pdo = zero8();
   float plse = 0.f, pthr = 0.f, pdv = 0.f;
+  // Query tiles are swept from the last one down to the block's diagonal: the
+  // offline test does not depend on the order, and co-resident workgroups of the
+  // same KV head (one per CU of an XCD) then read the same Q / dO tiles at about the
+  // same time, so those come from L2 instead of HBM.
+  auto tile_q0 = [&](int it) { return (nqt - 1 - it % per_head) * kBq; };
   auto fetch = [&](int it) {
     const long bhq = (long)b * p.Hq + hkv * grp + it / per_head;
-    const int q0 = (qi_start + it % per_head) * kBq;
+    const int q0 = tile_q0(it);
     if (tid < NCH) {
       const int row = tid / (D / 8), col = (tid % (D / 8)) * 8;
       const long qq = (long)q0 + row;
@@ -227,7 +250,7 @@ __global__ __launch_bounds__(512) void mala_bwd_dkdv_kernel(BwdParams p) {
 
   for (int it = 0; it < total; ++it) {
     const int buf = it & 1;
-    const int q0 = (qi_start + it % per_head) * kBq;
+    const int q0 = tile_q0(it);
     if (it + 1 < total) fetch(it + 1);
     const bf16* Qb = Qs + buf * TILE;
     const bf16* dOb = dOs + buf * TILE;

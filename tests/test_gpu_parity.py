@@ -47,7 +47,9 @@ TRAIN_TAUS = {
     "local_d64_ragged": (0.0, 1e-2, 0.3, 1.0),
     "gqa_d128_ragged": (0.0, 1e-3, 0.1, 1.0),
     "tiny_d128": (0.0, 0.5),
-    "single_row_d64": (0.0, 1.0),
+    # tau = 1 would put the only tile exactly on the threshold (P = 1 = tau / L):
+    # 0.5 retains and 1.5 skips it in the backward, both unambiguously
+    "single_row_d64": (0.0, 0.5, 1.5),
 }
 
 
