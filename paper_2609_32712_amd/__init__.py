@@ -197,9 +197,10 @@ def decode(q, k_cache, v_cache, scale, tau, num_splits, stats=True, workspace=No
     return dict(o=o, lse=lse, head_tiles=ht, counters=cnt)
 
 
-def default_num_splits(B, Hkv, Nk, num_cus=256, waves_per_cu=8):
-    """Splits that give about num_cus * waves_per_cu decode wavefronts, capped so
-    that each split keeps at least 16 tiles of 32 keys."""
+def default_num_splits(B, Hkv, Nk, num_cus=256, waves_per_simd=2):
+    """Splits that give about num_cus * 4 * waves_per_simd decode wavefronts (one
+    wavefront per batch x KV head x split), capped so that each split keeps at
+    least 16 tiles of 32 keys."""
     tiles = -(-Nk // 32)
-    want = max(1, (num_cus * waves_per_cu) // max(1, B * Hkv))
+    want = max(1, (num_cus * 4 * waves_per_simd) // max(1, B * Hkv))
     return int(max(1, min(want, tiles // 16 if tiles >= 16 else 1)))

@@ -9,10 +9,12 @@
 // Per 32-key tile, in descending order inside the split:
 //   S^T = K_t Q^T     2 x 4 (D = 128) MFMAs 16x16x32, K loaded straight from HBM
 //                     into the A operand; lane (g, col) holds query head col and
-//                     8 of the 32 keys; the next tile's K is prefetched meanwhile
+//                     8 of the 32 keys; K is prefetched two tiles ahead
 //   test              per head against that head's running (m, l) of the split
-//   retained (any)    V tile -> LDS; per head P = exp2(S - m_new) (0 for heads that
-//                     skip); O^T += V^T P^T with V^T through ds_read_b64_tr_b16.
+//   retained (any)    V tile (fetched one tile ahead when a look-ahead test says
+//                     it may be needed) -> LDS; per head P = exp2(S - m_new) (0 for
+//                     heads that skip); O^T += V^T P^T with V^T through
+//                     ds_read_b64_tr_b16.
 // Partials (O / l, lse, count) go to the workspace; a second kernel merges the
 // splits with the normalizer-aware (log-sum-exp weighted) reduction.
 #include "mala_device.h"
@@ -25,7 +27,8 @@ __global__ __launch_bounds__(64) void mala_decode_split_kernel(DecParams p) {
   constexpr int KS = D / 32;   // k-steps of 32 over head_dim
   constexpr int NDB = D / 16;  // 16-row blocks of O^T
   constexpr int LD = D + 8;
-  __shared__ bf16 Vs[kDecBk * LD];
+  constexpr int VCH = kDecBk * D / 8 / 64;   // 16-byte V chunks per lane per tile
+  __shared__ __attribute__((aligned(16))) bf16 Vs[kDecBk * LD];
 
   const int lane = threadIdx.x, g = lane >> 4, col = lane & 15;
   const int s = blockIdx.x % p.S;
@@ -50,7 +53,7 @@ __global__ __launch_bounds__(64) void mala_decode_split_kernel(DecParams p) {
   int cnt = 0;
   unsigned vloads = 0;
 
-  // K operand of tile t: rows kb + col (block 0) and kb + 16 + col (block 1)
+  // K of a tile as A operands: rows kb + col (block 0) and kb + 16 + col (block 1)
   bf16x8 ka[KS], kb1[KS];
   auto load_k = [&](int t) {
     const long k0 = (long)t * kDecBk + col, k1 = k0 + 16;
@@ -60,19 +63,26 @@ __global__ __launch_bounds__(64) void mala_decode_split_kernel(DecParams p) {
       kb1[kk] = k1 < p.Nk ? load8(Kp + k1 * D + 32 * kk + 8 * g) : zero8();
     }
   };
-  if (t_hi > t_lo) load_k(t_hi - 1);
-
-  for (int t = t_hi - 1; t >= t_lo; --t) {
+  // V of a tile into registers (row-major chunks); written to LDS when needed
+  bf16x8 vr[VCH];
+  auto load_v = [&](int t) {
+    const long kb = (long)t * kDecBk;
+#pragma unroll
+    for (int e = 0; e < VCH; ++e) {
+      const int ch = lane + 64 * e;
+      const int row = ch / (D / 8), c8 = (ch % (D / 8)) * 8;
+      vr[e] = kb + row < p.Nk ? load8(Vp + (kb + row) * D + c8) : zero8();
+    }
+  };
+  // base-2 scores of tile t for this lane's head (8 keys) and their max over the tile
+  auto scores = [&](int t, float (&sv)[8]) {
     f32x4 s0 = {0.f, 0.f, 0.f, 0.f}, s1 = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int kk = 0; kk < KS; ++kk) {
       s0 = mfma16(ka[kk], qreg[kk], s0);
       s1 = mfma16(kb1[kk], qreg[kk], s1);
     }
-    if (t > t_lo) load_k(t - 1);   // prefetch the next (lower) tile's K
-
     const long kb = (long)t * kDecBk;
-    float sv[8];
     float mt = kNegInf;
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
@@ -84,48 +94,76 @@ __global__ __launch_bounds__(64) void mala_decode_split_kernel(DecParams p) {
       mt = fmaxf(mt, fmaxf(x0, x1));
     }
     mt = fmaxf(mt, __shfl_xor(mt, 16));
-    mt = fmaxf(mt, __shfl_xor(mt, 32));
-    const bool demand = head_valid && (l == 0.f || (mt - m - fast_log2(l) >= p.thr2));
-    if (!wave_any(demand)) continue;
+    return fmaxf(mt, __shfl_xor(mt, 32));
+  };
 
-    // V tile -> LDS (rows beyond Nk are zero)
-    __syncthreads();
-    for (int ch = lane; ch < kDecBk * D / 8; ch += 64) {
-      const int row = ch / (D / 8), c8 = (ch % (D / 8)) * 8;
-      const long kk = kb + row;
-      store8(Vs + row * LD + c8, kk < p.Nk ? load8(Vp + kk * D + c8) : zero8());
+  // Pipeline: while tile t is decided and processed, K of tile t - 1 is already in
+  // registers (its scores are computed first) and K of t - 2 is loading.  Whether
+  // tile t - 1 can still be retained is checked against the state BEFORE tile t's
+  // update; since the retained normalizer only grows, a tile that fails this check
+  // fails the real test too, so V of t - 1 is fetched early exactly when it may be
+  // needed (with a small margin against fp32 rounding of the normalizer).
+  constexpr float kHintMargin = 1e-2f;
+  float sv[8], sn[8];
+  float mt = kNegInf, mtn = kNegInf;
+  if (t_hi > t_lo) {
+    load_k(t_hi - 1);
+    mt = scores(t_hi - 1, sv);
+    load_v(t_hi - 1);     // the first tile of a split is always retained (l = 0)
+    if (t_hi - 2 >= t_lo) load_k(t_hi - 2);
+  }
+  for (int t = t_hi - 1; t >= t_lo; --t) {
+    const bool has_next = t - 1 >= t_lo;
+    if (has_next) {
+      mtn = scores(t - 1, sn);
+      if (t - 2 >= t_lo) load_k(t - 2);
     }
-    __syncthreads();
-    ++vloads;
-
-    float alpha = 1.f, m_new = m;
-    if (demand) {
-      m_new = fmaxf(m, mt);
-      alpha = fast_exp2(m - m_new);
-    }
-    float ps = 0.f;
+    const float lse_run = m + fast_log2(l);
+    const bool demand = head_valid && (l == 0.f || (mt - lse_run >= p.thr2));
+    const bool hint = has_next && wave_any(head_valid && (l == 0.f || (mtn - lse_run >= p.thr2 - kHintMargin)));
+    if (wave_any(demand)) {
+      __syncthreads();   // the previous tile's transposed reads are done
 #pragma unroll
-    for (int r = 0; r < 8; ++r) {
-      const float e = demand ? fast_exp2(sv[r] - m_new) : 0.f;
-      sv[r] = e;
-      ps += e;
-    }
-    ps += __shfl_xor(ps, 16);
-    ps += __shfl_xor(ps, 32);
-    if (demand) {
-      l = alpha * l + ps;
-      m = m_new;
-      ++cnt;
-    }
-    bf16x8 ph, pl;
-    split_bf16x8(sv, ph, pl);
+      for (int e = 0; e < VCH; ++e) {
+        const int ch = lane + 64 * e;
+        const int row = ch / (D / 8), c8 = (ch % (D / 8)) * 8;
+        store8(Vs + row * LD + c8, vr[e]);
+      }
+      __syncthreads();
+      ++vloads;
+      float alpha = 1.f, m_new = m;
+      if (demand) {
+        m_new = fmaxf(m, mt);
+        alpha = fast_exp2(m - m_new);
+      }
+      float ps = 0.f;
 #pragma unroll
-    for (int db = 0; db < NDB; ++db) {
-      const bf16* vr = Vs + (4 * g + (col >> 2)) * LD + 16 * db + 4 * (col & 3);
-      const bf16x8 a = cat(lds_read_tr(vr), lds_read_tr(vr + 16 * LD));
-      acc[db] = mfma16(a, ph, acc[db] * alpha);
-      acc[db] = mfma16(a, pl, acc[db]);
+      for (int r = 0; r < 8; ++r) {
+        const float e = demand ? fast_exp2(sv[r] - m_new) : 0.f;
+        sv[r] = e;
+        ps += e;
+      }
+      ps += __shfl_xor(ps, 16);
+      ps += __shfl_xor(ps, 32);
+      if (demand) {
+        l = alpha * l + ps;
+        m = m_new;
+        ++cnt;
+      }
+      bf16x8 ph, pl;
+      split_bf16x8(sv, ph, pl);
+#pragma unroll
+      for (int db = 0; db < NDB; ++db) {
+        const bf16* vrow = Vs + (4 * g + (col >> 2)) * LD + 16 * db + 4 * (col & 3);
+        const bf16x8 a = cat(lds_read_tr(vrow), lds_read_tr(vrow + 16 * LD));
+        acc[db] = mfma16(a, ph, acc[db] * alpha);
+        acc[db] = mfma16(a, pl, acc[db]);
+      }
     }
+    if (hint) load_v(t - 1);
+#pragma unroll
+    for (int r = 0; r < 8; ++r) sv[r] = sn[r];
+    mt = mtn;
   }
 
   // partial of this split: O / l, lse (natural log) and the retained-tile count
