@@ -263,6 +263,13 @@ def main():
         cd = dec.cnt.cpu().numpy()
         res[name] = dict(fwd=f, bwd=b, dec=d, cf=cf, cb=cb, cd=cd)
         log(name, "fwd %.2f bwd %.2f decode %.3f ms" % (f[0], b[0], d[0]))
+    # supplementary: the paper's canonical tolerance tau = 1 on the same inputs
+    f1 = time_calls(lambda: tr.fwd(1.0), args.reps, 1)
+    b1 = time_calls(lambda: tr.bwd(1.0), args.reps, 1)
+    d1 = time_calls(lambda: dec.run(1.0), args.reps, 1)
+    cf1, cb1 = tr.counters()
+    cd1 = dec.cnt.cpu().numpy()
+    log("tau=1 fwd %.2f bwd %.2f decode %.3f ms" % (f1[0], b1[0], d1[0]))
     rt, rd = res["tau"], res["dense"]
     fl_f, fl_b = train_flops(rt["cf"], rt["cb"], w.D, bq, bk)
     de_f, de_b = dense_equivalent_flops(w.B, w.Hq, w.N, w.D)
@@ -300,6 +307,18 @@ def main():
             "hbm_frac": round(dec_bytes / (rt["dec"][0] * 1e-3) / 1e9 / PEAK_HBM_GBS, 4),
         },
         "decision_tile": [bq, bk],
+        "tau1_supplementary": {
+            "fwd_ms": round(f1[0], 3), "bwd_ms": round(b1[0], 3), "decode_ms": round(d1[0], 4),
+            "speedup_fwd": round(rd["fwd"][0] / f1[0], 4),
+            "speedup_bwd": round(rd["bwd"][0] / b1[0], 4),
+            "speedup_decode": round(rd["dec"][0] / d1[0], 4),
+            "retained_tiles_pct_fwd": pct(cf1[1], cf1[0]),
+            "retained_tiles_pct_bwd": pct(cb1[1], cb1[0]),
+            "retained_head_tiles_pct_decode": pct(cd1[1], cd1[0]),
+            "v_tiles_loaded_pct_decode": pct(cd1[2], cd1[0] / dec.w.g),
+            "mean_slots_per_query_fwd": round(float(cf1[3]) / (w.B * w.Hq * w.N), 1),
+            "mean_slots_per_query_bwd": round(float(cb1[3]) / (w.B * w.Hq * w.N), 1),
+        },
     }
     del tr
     torch.cuda.empty_cache()

@@ -231,12 +231,12 @@ def test_full_config3_sampled(tau):
     _full_train(3, tau, _blocks(0.5, 0.999), heads=[(0, 1), (0, 30)], kv_head_tail=(0, 7))
 
 
-@pytest.mark.parametrize("tau", [1e-4])
+@pytest.mark.parametrize("tau", [1e-4, 1.0])
 def test_full_config4_sampled(tau):
     _full_train(4, tau, _blocks(0.25, 0.999), heads=[(0, 6)], kv_head_tail=(0, 1))
 
 
-@pytest.mark.parametrize("tau", [0.0, 1e-4])
+@pytest.mark.parametrize("tau", [0.0, 1e-4, 1.0])
 def test_full_config5_decode_sampled(tau):
     w = Workload(5)
     print("[full cfg5 tau=%g] generating inputs" % tau, flush=True)
