@@ -5,19 +5,21 @@
 // keys of one (batch, KV head), with their K and V rows in LDS, and keeps their dK
 // and dV in registers for the whole kernel (no atomics, bitwise reproducible); it
 // loops over every query head of the GQA group and over the query tiles from the
-// end down to the diagonal.  Eight wavefronts in two roles: wavefront w accumulates dV
-// (w < 4) or dK (w >= 4) of keys [32 (w % 4), +32), so each wavefront's work on one
-// query tile is exactly one 32 x 32 decision tile, with a 64-register accumulator
-// (two wavefronts per SIMD).  Query tiles (Q, dO and the per-row base-2 LSE,
+// end down to the diagonal.  Eight wavefronts in two pipelined roles over keys
+// [32 (w % 4), +32): wavefronts 4-7 take the tile decisions, form P and accumulate
+// dK; wavefronts 0-3 accumulate dV and form dP and dS; P and dS pass between the
+// two through LDS.  Each wavefront holds a 64-register accumulator (two
+// wavefronts per SIMD) and runs 24 MFMAs per retained tile.  Query tiles (Q, dO and the per-row base-2 LSE,
 // threshold and D_q = rowsum(O * dO)) are double-buffered in LDS; the next tile is
 // fetched into registers while the current one is processed.
 //   S = Q_i K_w^T         8 MFMAs (lane = one key column, 16 query rows)
 //   offline test          retain iff some valid entry has
 //                         s - lse_q >= log2(tau) - log2(L_q) (base-2 units); ballot
-//   retained path         P = exp2(S - lse); dV role: dV^T += dO_i^T P;
-//                         dK role: dP = dO_i V_w^T, dS = P (dP - D_q), dK^T += Q_i^T dS;
-//                         P and dS enter as two bf16 terms (hi + lo), the A operands
-//                         come through ds_read_b64_tr_b16.
+//   retained path         P = exp2(S - lse) (handed on as bf16 hi + lo operands);
+//                         one tile later: dV^T += dO_i^T P, dP = dO_i V_w^T,
+//                         dS = P (dP - D_q) (handed back); two tiles later:
+//                         dK^T += Q_i^T dS; the A operands come through
+//                         ds_read_b64_tr_b16.
 // mala_bwd_dq_kernel (query-major, like the forward): one workgroup = 8 wavefronts
 // = 256 query rows; K and V stream through double-buffered LDS.  Per decision
 // tile it recomputes S and dP with the same MFMA operand roles and accumulation
@@ -164,21 +166,27 @@ __global__ __launch_bounds__(512) void mala_bwd_dkdv_kernel(BwdParams p) {
   constexpr int KS = D / 16;       // k-steps over head_dim
   constexpr int DB = D / 32;       // 32-wide column blocks
   constexpr int TILE = tile_elems<D>(kBq);          // one Q or dO tile in LDS
-  constexpr int KVT = tile_elems<D>(kBwdKeys);      // the workgroup's K (or V) block
   constexpr int NCH = kBq * D / 8;                  // 16-byte chunks of one query tile
   static_assert(NCH <= NT, "one chunk per thread");
-  __shared__ __attribute__((aligned(16))) bf16 Kblk[KVT];
-  __shared__ __attribute__((aligned(16))) bf16 Vblk[KVT];
-  __shared__ __attribute__((aligned(16))) bf16 Qs[2 * TILE];
-  __shared__ __attribute__((aligned(16))) bf16 dOs[2 * TILE];
-  __shared__ __attribute__((aligned(16))) float rowv[2][3][kBq];   // lse2, threshold, D_q
+  // rings: Q is read at iterations t and t + 2, dO and the row vectors at t and t + 1
+  __shared__ __attribute__((aligned(16))) bf16 Qs[4 * TILE];
+  __shared__ __attribute__((aligned(16))) bf16 dOs[3 * TILE];
+  __shared__ __attribute__((aligned(16))) float rowv[3][3][kBq];   // lse2, threshold, D_q
+  // hand-off operands, [buf][key wave][operand hi0, hi1, lo0, lo1][lane]
+  __shared__ __attribute__((aligned(16))) bf16x8 Pop[2][4][4][64];
+  __shared__ __attribute__((aligned(16))) bf16x8 dSop[2][4][4][64];
+  __shared__ int Pflag[3][4];
 
-  // Two roles per 32-key decision tile: waves 0-3 accumulate dV, waves 4-7 dK, each
-  // over keys [32 (w % 4), +32) of the block.  Both roles evaluate the same tile
-  // test; the dK role also forms dP and dS.
+  // Two wavefronts per 32 keys [32 (w % 4), +32), on the same SIMD, in a pipeline:
+  //   producer (w >= 4), iteration t:    S_t, offline test, P_t -> LDS; dK += Q_{t-2}^T dS_{t-2}
+  //   consumer (w < 4),  iteration t+1:  dV += dO_t^T P_t; dP_t = dO_t V^T,
+  //                                      dS_t = P_t (dP_t - D) -> LDS
+  // Each wavefront runs 24 MFMAs per retained tile; P and dS travel as the exact
+  // bf16 hi / lo B operands of the receiving lane (same lane, same layout).
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const bool role_dk = wave >= 4;
-  const int kw_local = (wave & 3) * kBk;
+  const bool producer = wave >= 4;
+  const int kwave = wave & 3;
+  const int kw_local = kwave * kBk;
   const int h = lane >> 5, c = lane & 31, G = lane >> 4, t16 = lane & 15;
   const int BHk = p.B * p.Hkv;
   const int bhk = blockIdx.x % BHk;
@@ -189,15 +197,15 @@ __global__ __launch_bounds__(512) void mala_bwd_dkdv_kernel(BwdParams p) {
   const int kw = kb0 + kw_local;           // first key of this wavefront's decision tile
   const int key = kw + c;                  // this lane's key (C-layout column)
 
-  const bf16* Kp = p.k + (long)bhk * p.Nk * D;
-  const bf16* Vp = p.v + (long)bhk * p.Nk * D;
-  for (int ch = tid; ch < kBwdKeys * D / 8; ch += NT) {
-    const int row = ch / (D / 8), col = (ch % (D / 8)) * 8;
-    const long kk = (long)kb0 + row;
-    const bool ok = kk < p.Nk;
-    store8(Kblk + tile_off<D>(row, col), ok ? load8(Kp + kk * D + col) : zero8());
-    store8(Vblk + tile_off<D>(row, col), ok ? load8(Vp + kk * D + col) : zero8());
+  // producer: K rows (B operand of S = Q K^T); consumer: V rows (of dP = dO V^T)
+  bf16x8 kv[KS];
+  {
+    const bf16* src = (producer ? p.k : p.v) + (long)bhk * p.Nk * D;
+#pragma unroll
+    for (int kk = 0; kk < KS; ++kk)
+      kv[kk] = key < p.Nk ? load8(src + (long)key * D + 16 * kk + 8 * h) : zero8();
   }
+  if (tid < 12) Pflag[tid >> 2][tid & 3] = 0;
 
   f32x16 acc[DB];
 #pragma unroll
@@ -211,14 +219,13 @@ __global__ __launch_bounds__(512) void mala_bwd_dkdv_kernel(BwdParams p) {
   const int per_head = nqt - qi_start;     // >= 1: key kb0 < Nk is visible to row Nq - 1
   const int total = grp * per_head;
 
-  // prefetch registers of the next query tile
-  bf16x8 pq = zero8(), pdo = zero8();
-  float plse = 0.f, pthr = 0.f, pdv = 0.f;
   // Query tiles are swept from the last one down to the block's diagonal: the
   // offline test does not depend on the order, and co-resident workgroups of the
   // same KV head (one per CU of an XCD) then read the same Q / dO tiles at about the
   // same time, so those come from L2 instead of HBM.
   auto tile_q0 = [&](int it) { return (nqt - 1 - it % per_head) * kBq; };
+  bf16x8 pq = zero8(), pdo = zero8();
+  float plse = 0.f, pthr = 0.f, pdv = 0.f;
   auto fetch = [&](int it) {
     const long bhq = (long)b * p.Hq + hkv * grp + it / per_head;
     const int q0 = tile_q0(it);
@@ -231,16 +238,16 @@ __global__ __launch_bounds__(512) void mala_bwd_dkdv_kernel(BwdParams p) {
     }
     if (tid < kBq) row_vectors(p, bhq, (long)q0 + tid, off, &plse, &pthr, &pdv);
   };
-  auto stash = [&](int buf) {
+  auto stash = [&](int it) {
     if (tid < NCH) {
       const int row = tid / (D / 8), col = (tid % (D / 8)) * 8;
-      store8(Qs + buf * TILE + tile_off<D>(row, col), pq);
-      store8(dOs + buf * TILE + tile_off<D>(row, col), pdo);
+      store8(Qs + (it & 3) * TILE + tile_off<D>(row, col), pq);
+      store8(dOs + (it % 3) * TILE + tile_off<D>(row, col), pdo);
     }
     if (tid < kBq) {
-      rowv[buf][0][tid] = plse;
-      rowv[buf][1][tid] = pthr;
-      rowv[buf][2][tid] = pdv;
+      rowv[it % 3][0][tid] = plse;
+      rowv[it % 3][1][tid] = pthr;
+      rowv[it % 3][2][tid] = pdv;
     }
   };
 
@@ -248,82 +255,118 @@ __global__ __launch_bounds__(512) void mala_bwd_dkdv_kernel(BwdParams p) {
   stash(0);
   __syncthreads();
 
-  for (int it = 0; it < total; ++it) {
-    const int buf = it & 1;
-    const int q0 = tile_q0(it);
+  for (int it = 0; it <= total + 1; ++it) {
     if (it + 1 < total) fetch(it + 1);
-    const bf16* Qb = Qs + buf * TILE;
-    const bf16* dOb = dOs + buf * TILE;
-
-    const int qlast = min(q0 + kBq - 1, p.Nq - 1);
-    if (kw < p.Nk && (long)kw <= (long)qlast + off) {
-      bf16x8 qa[KS], kop[KS];
+    if (producer) {
+      if (it < total) {
+        // tile it: score discovery, test, P
+        const int q0 = tile_q0(it);
+        const bf16* Qb = Qs + (it & 3) * TILE;
+        const float* rv = &rowv[it % 3][0][0];
+        const int qlast = min(q0 + kBq - 1, p.Nq - 1);
+        bool ret = false;
+        if (kw < p.Nk && (long)kw <= (long)qlast + off) {
+          bf16x8 qa[KS];
 #pragma unroll
-      for (int kk = 0; kk < KS; ++kk) {
-        qa[kk] = load8(Qb + tile_off<D>(c, 16 * kk + 8 * h));
-        kop[kk] = load8(Kblk + tile_off<D>(kw_local + c, 16 * kk + 8 * h));
+          for (int kk = 0; kk < KS; ++kk) qa[kk] = load8(Qb + tile_off<D>(c, 16 * kk + 8 * h));
+          const f32x16 s = qk_tile<KS>(qa, kv);
+          const bool need_mask =
+              ((long)kw + kBk - 1 > (long)q0 + off) || (q0 + kBq > p.Nq) || (kw + kBk > p.Nk);
+          const int klo = key < p.Nk ? (int)((long)key - off - q0) - 4 * h : 1000000;
+          float sv[16];
+          const bool dem =
+              offline_entries(s, p.scale2, need_mask, klo, p.Nq - q0 - 4 * h, rv + kBq, h, sv);
+          ret = wave_any(dem);
+          if (ret) {
+#pragma unroll
+            for (int g = 0; g < 4; ++g) {
+              const f32x4 l4 = *reinterpret_cast<const f32x4*>(rv + 8 * g + 4 * h);
+#pragma unroll
+              for (int e = 0; e < 4; ++e) sv[4 * g + e] = fast_exp2(sv[4 * g + e] - l4[e]);
+            }
+            bf16x8 xh[2], xl[2];
+            split_bf16x8(sv, xh[0], xl[0]);
+            split_bf16x8(sv + 8, xh[1], xl[1]);
+            Pop[it & 1][kwave][0][lane] = xh[0];
+            Pop[it & 1][kwave][1][lane] = xh[1];
+            Pop[it & 1][kwave][2][lane] = xl[0];
+            Pop[it & 1][kwave][3][lane] = xl[1];
+          }
+        }
+        if (lane == 0) Pflag[it % 3][kwave] = ret ? 1 : 0;
       }
-      const f32x16 s = qk_tile<KS>(qa, kop);
-      const bool need_mask =
-          ((long)kw + kBk - 1 > (long)q0 + off) || (q0 + kBq > p.Nq) || (kw + kBk > p.Nk);
-      const int klo = key < p.Nk ? (int)((long)key - off - q0) - 4 * h : 1000000;
-      float sv[16];
-      const bool dem =
-          offline_entries(s, p.scale2, need_mask, klo, p.Nq - q0 - 4 * h, rowv[buf][1], h, sv);
-      if (wave_any(dem)) {
-        // P = exp2(S - lse)
-#pragma unroll
-        for (int g = 0; g < 4; ++g) {
-          const f32x4 l4 = *reinterpret_cast<const f32x4*>(rowv[buf][0] + 8 * g + 4 * h);
-#pragma unroll
-          for (int e = 0; e < 4; ++e) sv[4 * g + e] = fast_exp2(sv[4 * g + e] - l4[e]);
-        }
-        const bf16* Ab;   // the A operand source: dO^T for dV, Q^T for dK
-        if (role_dk) {
-          // dP = dO_i V_w^T, dS = P (dP - D_q); the B operand of dK^T += Q^T dS is dS
-          bf16x8 oa[KS], vop[KS];
-#pragma unroll
-          for (int kk = 0; kk < KS; ++kk) {
-            oa[kk] = load8(dOb + tile_off<D>(c, 16 * kk + 8 * h));
-            vop[kk] = load8(Vblk + tile_off<D>(kw_local + c, 16 * kk + 8 * h));
-          }
-          const f32x16 dp = qk_tile<KS>(oa, vop);
-#pragma unroll
-          for (int g = 0; g < 4; ++g) {
-            const f32x4 d4 = *reinterpret_cast<const f32x4*>(rowv[buf][2] + 8 * g + 4 * h);
-#pragma unroll
-            for (int e = 0; e < 4; ++e) sv[4 * g + e] = sv[4 * g + e] * (dp[4 * g + e] - d4[e]);
-          }
-          Ab = Qb;
-        } else {
-          Ab = dOb;   // dV^T += dO^T P
-        }
-        bf16x8 xh[2], xl[2];
-        split_bf16x8(sv, xh[0], xl[0]);
-        split_bf16x8(sv + 8, xh[1], xl[1]);
+      if (it >= 2 && it - 2 < total && Pflag[(it - 2) % 3][kwave]) {
+        // dK^T += Q^T dS for tile it - 2
+        const bf16* Qb = Qs + ((it - 2) & 3) * TILE;
+        const int sb = (it - 2) & 1;
+        const bf16x8 dh0 = dSop[sb][kwave][0][lane], dh1 = dSop[sb][kwave][1][lane];
+        const bf16x8 dl0 = dSop[sb][kwave][2][lane], dl1 = dSop[sb][kwave][3][lane];
 #pragma unroll
         for (int db = 0; db < DB; ++db) {
 #pragma unroll
           for (int ks = 0; ks < 2; ++ks) {
             const int trow = 16 * ks + 4 * h + (t16 >> 2);
             const int tcol = 32 * db + 16 * (G & 1) + 4 * (t16 & 3);
-            const bf16x8 a = cat(lds_read_tr(Ab + tile_off<D>(trow, tcol)),
-                                 lds_read_tr(Ab + tile_off<D>(trow + 8, tcol)));
-            acc[db] = mfma32(a, xh[ks], acc[db]);
-            acc[db] = mfma32(a, xl[ks], acc[db]);
+            const bf16x8 a = cat(lds_read_tr(Qb + tile_off<D>(trow, tcol)),
+                                 lds_read_tr(Qb + tile_off<D>(trow + 8, tcol)));
+            acc[db] = mfma32(a, ks ? dh1 : dh0, acc[db]);
+            acc[db] = mfma32(a, ks ? dl1 : dl0, acc[db]);
           }
         }
       }
+    } else if (it >= 1 && it - 1 < total && Pflag[(it - 1) % 3][kwave]) {
+      // consumer, tile t = it - 1: dV^T += dO^T P; dP = dO V^T; dS = P (dP - D)
+      const int t = it - 1;
+      const bf16* dOb = dOs + (t % 3) * TILE;
+      const float* rv = &rowv[t % 3][0][0];
+      const bf16x8 ph0 = Pop[t & 1][kwave][0][lane], ph1 = Pop[t & 1][kwave][1][lane];
+      const bf16x8 pl0 = Pop[t & 1][kwave][2][lane], pl1 = Pop[t & 1][kwave][3][lane];
+#pragma unroll
+      for (int db = 0; db < DB; ++db) {
+#pragma unroll
+        for (int ks = 0; ks < 2; ++ks) {
+          const int trow = 16 * ks + 4 * h + (t16 >> 2);
+          const int tcol = 32 * db + 16 * (G & 1) + 4 * (t16 & 3);
+          const bf16x8 a = cat(lds_read_tr(dOb + tile_off<D>(trow, tcol)),
+                               lds_read_tr(dOb + tile_off<D>(trow + 8, tcol)));
+          acc[db] = mfma32(a, ks ? ph1 : ph0, acc[db]);
+          acc[db] = mfma32(a, ks ? pl1 : pl0, acc[db]);
+        }
+      }
+      bf16x8 oa[KS];
+#pragma unroll
+      for (int kk = 0; kk < KS; ++kk) oa[kk] = load8(dOb + tile_off<D>(c, 16 * kk + 8 * h));
+      const f32x16 dp = qk_tile<KS>(oa, kv);
+      // P back to fp32 (hi + lo), then dS in the C layout of dP
+      float ds[16];
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        ds[i] = (float)ph0[i] + (float)pl0[i];
+        ds[8 + i] = (float)ph1[i] + (float)pl1[i];
+      }
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        const f32x4 d4 = *reinterpret_cast<const f32x4*>(rv + 2 * kBq + 8 * g + 4 * h);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) ds[4 * g + e] = ds[4 * g + e] * (dp[4 * g + e] - d4[e]);
+      }
+      bf16x8 xh[2], xl[2];
+      split_bf16x8(ds, xh[0], xl[0]);
+      split_bf16x8(ds + 8, xh[1], xl[1]);
+      dSop[t & 1][kwave][0][lane] = xh[0];
+      dSop[t & 1][kwave][1][lane] = xh[1];
+      dSop[t & 1][kwave][2][lane] = xl[0];
+      dSop[t & 1][kwave][3][lane] = xl[1];
     }
-    if (it + 1 < total) stash(buf ^ 1);
+    if (it + 1 < total) stash(it + 1);
     __syncthreads();
   }
 
-  // dV = sum P^T dO (waves 0-3), dK = scale * sum dS^T Q (waves 4-7); lane (h, c)
+  // dV = sum P^T dO (consumers), dK = scale * sum dS^T Q (producers); lane (h, c)
   // holds key kw + c
   if (key < p.Nk) {
-    const float f = role_dk ? p.scale : 1.f;
-    float* dst = (role_dk ? p.dk : p.dv) + ((long)bhk * p.Nk + key) * D;
+    const float f = producer ? p.scale : 1.f;
+    float* dst = (producer ? p.dk : p.dv) + ((long)bhk * p.Nk + key) * D;
 #pragma unroll
     for (int db = 0; db < DB; ++db)
 #pragma unroll
