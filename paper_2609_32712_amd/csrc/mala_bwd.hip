@@ -93,28 +93,28 @@ hipError_t launch_bwd_preprocess(const float* o, const bf16* dout, float* dvec, 
 // Both backward kernels use exactly this sequence, so their scores are identical.
 template <int KS>
 __device__ __forceinline__ f32x16 qk_tile(const bf16x8 (&a)[KS], const bf16x8 (&b)[KS]) {
-  f32x16 s, s_odd;
+  f32x16 s;
 #pragma unroll
-  for (int r = 0; r < 16; ++r) s[r] = s_odd[r] = 0.f;
+  for (int r = 0; r < 16; ++r) s[r] = 0.f;
 #pragma unroll
-  for (int kk = 0; kk < KS; kk += 2) {
-    s = mfma32(a[kk], b[kk], s);
-    s_odd = mfma32(a[kk + 1], b[kk + 1], s_odd);
-  }
-  return s + s_odd;
+  for (int kk = 0; kk < KS; ++kk) s = mfma32(a[kk], b[kk], s);
+  return s;
 }
 
 // Offline test of one tile in the C layout of qk_tile (lane = key column, rows
-// 8 g + 4 h + e of the query tile): base-2 masked scores into sv; returns whether
-// some legal entry of this lane reaches its row's threshold (lse2 + log2(tau / L)),
-// evaluated as max(x - thr) >= 0 (for finite x this is exactly x >= thr; padded
-// rows have thr = +inf, tau = 0 gives thr = -inf).  klo / qlim bound the legal
-// rows: 8 g + e in [klo, qlim); the bounds are only consulted on tiles that cross
-// the diagonal or the end of the sequence (need_mask, uniform over the wavefront).
+// 8 g + 4 h + e of the query tile).  Copies the raw scores into sv (-inf where
+// masked) and returns whether some legal entry of this lane reaches its row's
+// threshold (lse2 + log2(tau / L), base 2): max(s * scale2 - thr) >= 0 with one
+// rounding (fma).  For finite values this is exactly the comparison of the
+// rounded base-2 score with thr; padded rows have thr = +inf, tau = 0 gives
+// thr = -inf.  klo / qlim bound the legal rows: 8 g + e in [klo, qlim); the bounds
+// are only consulted on tiles that cross the diagonal or the end of the sequence
+// (need_mask, uniform over the wavefront).  The probability of an entry is then
+// exp2(fma(s, scale2, -lse2)).
 __device__ __forceinline__ bool offline_entries(const f32x16& s, float scale2, bool need_mask,
                                                 int klo, int qlim, const float* thrs, int h,
                                                 float (&sv)[16]) {
-  // no FMA contraction: both backward kernels must round identically
+  // both backward kernels must round identically: explicit fma, no contraction
 #pragma clang fp contract(off)
   float dm = kNegInf;
   if (need_mask) {
@@ -124,9 +124,9 @@ __device__ __forceinline__ bool offline_entries(const f32x16& s, float scale2, b
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
         const bool legal = (8 * g + e >= klo) && (8 * g + e < qlim);
-        const float x = s[4 * g + e] * scale2;
+        const float x = s[4 * g + e];
         sv[4 * g + e] = legal ? x : kNegInf;
-        dm = fmaxf(dm, legal ? x - th[e] : kNegInf);
+        dm = fmaxf(dm, legal ? __builtin_fmaf(x, scale2, -th[e]) : kNegInf);
       }
     }
   } else {
@@ -135,13 +135,25 @@ __device__ __forceinline__ bool offline_entries(const f32x16& s, float scale2, b
       const f32x4 th = *reinterpret_cast<const f32x4*>(thrs + 8 * g + 4 * h);
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
-        const float x = s[4 * g + e] * scale2;
+        const float x = s[4 * g + e];
         sv[4 * g + e] = x;
-        dm = fmaxf(dm, x - th[e]);
+        dm = fmaxf(dm, __builtin_fmaf(x, scale2, -th[e]));
       }
     }
   }
   return dm >= 0.f;
+}
+
+// P = exp2(s * scale2 - lse2) in place, for the C layout of qk_tile.
+__device__ __forceinline__ void probabilities(float (&sv)[16], float scale2, const float* lse2,
+                                              int h) {
+#pragma unroll
+  for (int g = 0; g < 4; ++g) {
+    const f32x4 l4 = *reinterpret_cast<const f32x4*>(lse2 + 8 * g + 4 * h);
+#pragma unroll
+    for (int e = 0; e < 4; ++e)
+      sv[4 * g + e] = fast_exp2(__builtin_fmaf(sv[4 * g + e], scale2, -l4[e]));
+  }
 }
 
 // Per-row vectors of a query tile: base-2 lse, test threshold, D_q.
@@ -172,8 +184,9 @@ __global__ __launch_bounds__(512) void mala_bwd_dkdv_kernel(BwdParams p) {
   __shared__ __attribute__((aligned(16))) bf16 Qs[4 * TILE];
   __shared__ __attribute__((aligned(16))) bf16 dOs[3 * TILE];
   __shared__ __attribute__((aligned(16))) float rowv[3][3][kBq];   // lse2, threshold, D_q
-  // hand-off operands, [buf][key wave][operand hi0, hi1, lo0, lo1][lane]
-  __shared__ __attribute__((aligned(16))) bf16x8 Pop[2][4][4][64];
+  // hand-off: P in fp32 as [buf][key wave][C registers 4g .. 4g+3][lane]; dS as the
+  // B operands [buf][key wave][hi0, hi1, lo0, lo1][lane]
+  __shared__ __attribute__((aligned(16))) f32x4 Pf[2][4][4][64];
   __shared__ __attribute__((aligned(16))) bf16x8 dSop[2][4][4][64];
   __shared__ int Pflag[3][4];
 
@@ -188,6 +201,8 @@ __global__ __launch_bounds__(512) void mala_bwd_dkdv_kernel(BwdParams p) {
   const int kwave = wave & 3;
   const int kw_local = kwave * kBk;
   const int h = lane >> 5, c = lane & 31, G = lane >> 4, t16 = lane & 15;
+  // lane bases of the LDS tile reads: operand rows (row c) and transposed rows
+  const int rdo = rd_base<D>(c, h), tro = tr_base<D>(4 * h + (t16 >> 2), G & 1, t16);
   const int BHk = p.B * p.Hkv;
   const int bhk = blockIdx.x % BHk;
   const int kblk = blockIdx.x / BHk;       // ascending: the longest key blocks first
@@ -267,8 +282,9 @@ __global__ __launch_bounds__(512) void mala_bwd_dkdv_kernel(BwdParams p) {
         bool ret = false;
         if (kw < p.Nk && (long)kw <= (long)qlast + off) {
           bf16x8 qa[KS];
+          const bf16* qr = lds_pin(Qb + rdo);
 #pragma unroll
-          for (int kk = 0; kk < KS; ++kk) qa[kk] = load8(Qb + tile_off<D>(c, 16 * kk + 8 * h));
+          for (int kk = 0; kk < KS; ++kk) qa[kk] = load8(qr + rd_step<D>(kk));
           const f32x16 s = qk_tile<KS>(qa, kv);
           const bool need_mask =
               ((long)kw + kBk - 1 > (long)q0 + off) || (q0 + kBq > p.Nq) || (kw + kBk > p.Nk);
@@ -278,26 +294,18 @@ __global__ __launch_bounds__(512) void mala_bwd_dkdv_kernel(BwdParams p) {
               offline_entries(s, p.scale2, need_mask, klo, p.Nq - q0 - 4 * h, rv + kBq, h, sv);
           ret = wave_any(dem);
           if (ret) {
+            probabilities(sv, p.scale2, rv, h);
 #pragma unroll
-            for (int g = 0; g < 4; ++g) {
-              const f32x4 l4 = *reinterpret_cast<const f32x4*>(rv + 8 * g + 4 * h);
-#pragma unroll
-              for (int e = 0; e < 4; ++e) sv[4 * g + e] = fast_exp2(sv[4 * g + e] - l4[e]);
-            }
-            bf16x8 xh[2], xl[2];
-            split_bf16x8(sv, xh[0], xl[0]);
-            split_bf16x8(sv + 8, xh[1], xl[1]);
-            Pop[it & 1][kwave][0][lane] = xh[0];
-            Pop[it & 1][kwave][1][lane] = xh[1];
-            Pop[it & 1][kwave][2][lane] = xl[0];
-            Pop[it & 1][kwave][3][lane] = xl[1];
+            for (int g = 0; g < 4; ++g)
+              Pf[it & 1][kwave][g][lane] =
+                  f32x4{sv[4 * g], sv[4 * g + 1], sv[4 * g + 2], sv[4 * g + 3]};
           }
         }
         if (lane == 0) Pflag[it % 3][kwave] = ret ? 1 : 0;
       }
       if (it >= 2 && it - 2 < total && Pflag[(it - 2) % 3][kwave]) {
         // dK^T += Q^T dS for tile it - 2
-        const bf16* Qb = Qs + ((it - 2) & 3) * TILE;
+        const bf16* qtb = lds_pin(Qs + ((it - 2) & 3) * TILE + tro);
         const int sb = (it - 2) & 1;
         const bf16x8 dh0 = dSop[sb][kwave][0][lane], dh1 = dSop[sb][kwave][1][lane];
         const bf16x8 dl0 = dSop[sb][kwave][2][lane], dl1 = dSop[sb][kwave][3][lane];
@@ -305,10 +313,8 @@ __global__ __launch_bounds__(512) void mala_bwd_dkdv_kernel(BwdParams p) {
         for (int db = 0; db < DB; ++db) {
 #pragma unroll
           for (int ks = 0; ks < 2; ++ks) {
-            const int trow = 16 * ks + 4 * h + (t16 >> 2);
-            const int tcol = 32 * db + 16 * (G & 1) + 4 * (t16 & 3);
-            const bf16x8 a = cat(lds_read_tr(Qb + tile_off<D>(trow, tcol)),
-                                 lds_read_tr(Qb + tile_off<D>(trow + 8, tcol)));
+            const bf16* qt = qtb + 16 * ks * (D + 8) + tr_step<D>(db);
+            const bf16x8 a = cat(lds_read_tr(qt), lds_read_tr(qt + 8 * (D + 8)));
             acc[db] = mfma32(a, ks ? dh1 : dh0, acc[db]);
             acc[db] = mfma32(a, ks ? dl1 : dl0, acc[db]);
           }
@@ -318,32 +324,34 @@ __global__ __launch_bounds__(512) void mala_bwd_dkdv_kernel(BwdParams p) {
       // consumer, tile t = it - 1: dV^T += dO^T P; dP = dO V^T; dS = P (dP - D)
       const int t = it - 1;
       const bf16* dOb = dOs + (t % 3) * TILE;
+      const bf16* otb = lds_pin(dOb + tro);
       const float* rv = &rowv[t % 3][0][0];
-      const bf16x8 ph0 = Pop[t & 1][kwave][0][lane], ph1 = Pop[t & 1][kwave][1][lane];
-      const bf16x8 pl0 = Pop[t & 1][kwave][2][lane], pl1 = Pop[t & 1][kwave][3][lane];
+      float ds[16];
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        const f32x4 p4 = Pf[t & 1][kwave][g][lane];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) ds[4 * g + e] = p4[e];
+      }
+      bf16x8 ph0, ph1, pl0, pl1;
+      split_bf16x8(ds, ph0, pl0);
+      split_bf16x8(ds + 8, ph1, pl1);
 #pragma unroll
       for (int db = 0; db < DB; ++db) {
 #pragma unroll
         for (int ks = 0; ks < 2; ++ks) {
-          const int trow = 16 * ks + 4 * h + (t16 >> 2);
-          const int tcol = 32 * db + 16 * (G & 1) + 4 * (t16 & 3);
-          const bf16x8 a = cat(lds_read_tr(dOb + tile_off<D>(trow, tcol)),
-                               lds_read_tr(dOb + tile_off<D>(trow + 8, tcol)));
+          const bf16* ot = otb + 16 * ks * (D + 8) + tr_step<D>(db);
+          const bf16x8 a = cat(lds_read_tr(ot), lds_read_tr(ot + 8 * (D + 8)));
           acc[db] = mfma32(a, ks ? ph1 : ph0, acc[db]);
           acc[db] = mfma32(a, ks ? pl1 : pl0, acc[db]);
         }
       }
       bf16x8 oa[KS];
+      const bf16* orr = lds_pin(dOb + rdo);
 #pragma unroll
-      for (int kk = 0; kk < KS; ++kk) oa[kk] = load8(dOb + tile_off<D>(c, 16 * kk + 8 * h));
+      for (int kk = 0; kk < KS; ++kk) oa[kk] = load8(orr + rd_step<D>(kk));
       const f32x16 dp = qk_tile<KS>(oa, kv);
-      // P back to fp32 (hi + lo), then dS in the C layout of dP
-      float ds[16];
-#pragma unroll
-      for (int i = 0; i < 8; ++i) {
-        ds[i] = (float)ph0[i] + (float)pl0[i];
-        ds[8 + i] = (float)ph1[i] + (float)pl1[i];
-      }
+      // dS = P (dP - D) in the C layout of dP
 #pragma unroll
       for (int g = 0; g < 4; ++g) {
         const f32x4 d4 = *reinterpret_cast<const f32x4*>(rv + 2 * kBq + 8 * g + 4 * h);
@@ -395,6 +403,8 @@ __global__ __launch_bounds__(kFwdWaves * 64) void mala_bwd_dq_kernel(BwdParams p
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int h = lane >> 5, c = lane & 31, G = lane >> 4, t16 = lane & 15;
+  // lane bases of the LDS tile reads: operand rows (row c) and transposed rows
+  const int rdo = rd_base<D>(c, h), tro = tr_base<D>(4 * h + (t16 >> 2), G & 1, t16);
   const int BH = p.B * p.Hq;
   const int bh = blockIdx.x % BH;
   const int qblk = (p.Nq + kFwdRows - 1) / kFwdRows - 1 - (int)(blockIdx.x / BH);
@@ -463,6 +473,9 @@ __global__ __launch_bounds__(kFwdWaves * 64) void mala_bwd_dq_kernel(BwdParams p
     if (t > 0) fetch(t - 1);
     const bf16* Kb = Ks + buf * STAGE;
     const bf16* Vb = Vs + buf * STAGE;
+    const bf16* kr = lds_pin(Kb + rdo);
+    const bf16* vr = lds_pin(Vb + rdo);
+    const bf16* ktb = lds_pin(Kb + tro);
 #pragma unroll 1
     for (int sub = 1; sub >= 0; --sub) {
       const int j = 2 * t + sub;
@@ -472,7 +485,7 @@ __global__ __launch_bounds__(kFwdWaves * 64) void mala_bwd_dq_kernel(BwdParams p
       ++n_legal;
       bf16x8 kop[KS];
 #pragma unroll
-      for (int kk = 0; kk < KS; ++kk) kop[kk] = load8(Kb + tile_off<D>(sub * kBk + c, 16 * kk + 8 * h));
+      for (int kk = 0; kk < KS; ++kk) kop[kk] = load8(kr + sub * kBk * (D + 8) + rd_step<D>(kk));
       const f32x16 s = qk_tile<KS>(qa, kop);
       const bool need_mask =
           (kb + kBk - 1 > (long)q0w + off) || (q0w + kBq > p.Nq) || (kb + kBk > p.Nk);
@@ -483,15 +496,10 @@ __global__ __launch_bounds__(kFwdWaves * 64) void mala_bwd_dq_kernel(BwdParams p
       if (!wave_any(dem)) continue;
       ++n_ret;
       cnt_row += (row_valid && kb <= (long)q0w + c + off) ? 1 : 0;
-#pragma unroll
-      for (int g = 0; g < 4; ++g) {
-        const f32x4 l4 = *reinterpret_cast<const f32x4*>(rowv[wave][0] + 8 * g + 4 * h);
-#pragma unroll
-        for (int e = 0; e < 4; ++e) sv[4 * g + e] = fast_exp2(sv[4 * g + e] - l4[e]);
-      }
+      probabilities(sv, p.scale2, rowv[wave][0], h);
       bf16x8 vop[KS];
 #pragma unroll
-      for (int kk = 0; kk < KS; ++kk) vop[kk] = load8(Vb + tile_off<D>(sub * kBk + c, 16 * kk + 8 * h));
+      for (int kk = 0; kk < KS; ++kk) vop[kk] = load8(vr + sub * kBk * (D + 8) + rd_step<D>(kk));
       const f32x16 dp = qk_tile<KS>(oa, vop);
       float dsv[16];
 #pragma unroll
@@ -524,9 +532,8 @@ __global__ __launch_bounds__(kFwdWaves * 64) void mala_bwd_dq_kernel(BwdParams p
         const bf16x8 al = cat(lds_read_tr(dSl + ao), lds_read_tr(dSl + ao + 8 * DSS));
 #pragma unroll
         for (int db = 0; db < DB; ++db) {
-          const int kcol = 32 * db + 16 * (G & 1) + 4 * (t16 & 3);
-          const bf16x8 kbop = cat(lds_read_tr(Kb + tile_off<D>(sub * kBk + arow, kcol)),
-                                  lds_read_tr(Kb + tile_off<D>(sub * kBk + arow + 8, kcol)));
+          const bf16* kt = ktb + (sub * kBk + 16 * ks) * (D + 8) + tr_step<D>(db);
+          const bf16x8 kbop = cat(lds_read_tr(kt), lds_read_tr(kt + 8 * (D + 8)));
           acc[db] = mfma32(ah, kbop, acc[db]);
           acc[db] = mfma32(al, kbop, acc[db]);
         }

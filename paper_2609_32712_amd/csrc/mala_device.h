@@ -27,6 +27,7 @@ namespace mala {
 typedef __bf16 bf16;
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef float f32x2 __attribute__((ext_vector_type(2)));
@@ -61,24 +62,59 @@ __device__ __forceinline__ float halves_sum(float x) {
   return __uint_as_float(r[0]) + __uint_as_float(r[1]);
 }
 
-// Offset (in bf16 elements) of element (row, col) of a row-major [rows][D] bf16 tile
-// in LDS.  D = 128 rows are 256 bytes with their 16-byte chunks XOR-swizzled by
-// f(row) = 2 * (row % 8) + (row / 8) % 2, which keeps both access patterns of the
-// kernels free of bank conflicts: 16 lanes reading one chunk of 16 consecutive
-// rows (ds_read_b128) and 16 lanes reading two adjacent chunks of 4 consecutive
-// rows (ds_read_b64_tr_b16).  D = 64 rows are padded to 72 elements.
+// LDS layout of a row-major [rows][D] bf16 tile.  Rows are D + 8 elements apart
+// (272 bytes at D = 128: consecutive rows start 4 banks apart), and within a row
+// the 16-byte chunk L (columns 8L .. 8L+7) is stored at chunk position
+// (D / 32) * (L % 4) + L / 4.  With the 64 banks of 4 bytes and the access phases
+// of gfx950 (16 lanes per phase for ds_read_b128, 32 for ds_read_b64_tr_b16),
+// both access patterns of the kernels are then free of bank conflicts at D = 128:
+//   * A / B operand reads: 16 lanes read the same chunk of 16 consecutive rows
+//     (row offsets 17 chunks apart cover all 16 positions mod 256 bytes);
+//   * transposed reads: 32 lanes read 4 consecutive rows x 32 columns, i.e. chunks
+//     {4 db + x, x = 0..3}, stored at positions {4 x + db}, which the 4 rows shift
+//     onto 16 distinct positions.
+// Both patterns are also affine in the unrolled loop indices (k-step, column block,
+// row block), so one base address per lane serves all reads of a tile with
+// immediate offsets: rd_base / rd_step and tr_base / tr_step below.
 template <int D>
 __device__ __forceinline__ int tile_off(int row, int col) {
-  if constexpr (D == 128) {
-    const int f = ((row & 7) << 1) | ((row >> 3) & 1);
-    return row * 128 + ((((col >> 3) ^ f)) << 3) + (col & 7);
-  } else {
-    return row * (D + 8) + col;
-  }
+  const int ch = col >> 3;
+  return row * (D + 8) + 8 * ((D / 32) * (ch & 3) + (ch >> 2)) + (col & 7);
 }
 template <int D>
 constexpr int tile_elems(int rows) {
-  return D == 128 ? rows * 128 : rows * (D + 8);
+  return rows * (D + 8);
+}
+// Element (row, 16 kk + 8 h .. +7), the k-step kk operand of an MFMA lane in half h:
+// tile_off(row, 16 kk + 8 h) == rd_base(row, h) + rd_step(kk).
+template <int D>
+__device__ __forceinline__ int rd_base(int row, int h) {
+  return row * (D + 8) + (D / 4) * h;
+}
+template <int D>
+constexpr int rd_step(int kk) {
+  return (D / 4) * 2 * (kk & 1) + 8 * (kk >> 1);
+}
+// Transposed read of rows row .. row+3 at columns 32 db + 16 g1 + 4 (t16 % 4) .. +3
+// (lane t16 of a 16-lane group, g1 = group % 2):
+// tile_off(row + t16 / 4, 32 db + 16 g1 + 4 (t16 % 4)) == tr_base(row + t16 / 4, g1, t16) + tr_step(db).
+template <int D>
+__device__ __forceinline__ int tr_base(int row, int g1, int t16) {
+  return row * (D + 8) + (D / 4) * (2 * g1 + ((t16 >> 1) & 1)) + 4 * (t16 & 1);
+}
+template <int D>
+constexpr int tr_step(int db) {
+  return 8 * db;
+}
+
+// The LDS address p (a lane base plus a uniform buffer offset), opaque to the
+// compiler's reassociation: reads at p + constant then take the constant in the
+// instruction's offset field, instead of the compiler keeping one precomputed
+// register per read and re-adding the buffer offset to each.
+__device__ __forceinline__ const bf16* lds_pin(const bf16* p) {
+  auto q = (const __attribute__((address_space(3))) bf16*)p;
+  asm volatile("" : "+v"(q));
+  return (const bf16*)q;
 }
 
 // Hardware base-2 exponential / logarithm (v_exp_f32 / v_log_f32, ~1 ulp on normal
@@ -115,11 +151,18 @@ __device__ __forceinline__ bf16x8 to_bf16x8(const float* x) {
 // The post-score products (P V, P^T dO, dS^T Q, dS K) run as two MFMAs, one per
 // term, so the probabilities keep ~16 significant bits instead of bf16's 8.
 __device__ __forceinline__ void split_bf16x8(const float* x, bf16x8& hi, bf16x8& lo) {
+  // one packed conversion per pair; the high parts come back to fp32 by bit moves
+  // (a bf16 is the upper half of an fp32), so x - hi is exact
 #pragma unroll
-  for (int i = 0; i < 8; ++i) {
-    const bf16 t = (bf16)x[i];
-    hi[i] = t;
-    lo[i] = (bf16)(x[i] - (float)t);
+  for (int i = 0; i < 8; i += 2) {
+    const bf16x2 h2 = __builtin_convertvector((f32x2{x[i], x[i + 1]}), bf16x2);
+    const uint32_t u = __builtin_bit_cast(uint32_t, h2);
+    const float h0 = __uint_as_float(u << 16), h1 = __uint_as_float(u & 0xffff0000u);
+    const bf16x2 l2 = __builtin_convertvector((f32x2{x[i] - h0, x[i + 1] - h1}), bf16x2);
+    hi[i] = h2[0];
+    hi[i + 1] = h2[1];
+    lo[i] = l2[0];
+    lo[i + 1] = l2[1];
   }
 }
 

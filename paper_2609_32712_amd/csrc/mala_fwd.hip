@@ -42,6 +42,8 @@ __global__ __launch_bounds__(kFwdWaves * 64) void mala_fwd_kernel(FwdParams p) {
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int h = lane >> 5, c = lane & 31, G = lane >> 4, t16 = lane & 15;
+  // lane bases of the LDS tile reads: operand rows (row c) and transposed rows
+  const int rdo = rd_base<D>(c, h), tro = tr_base<D>(4 * h + (t16 >> 2), G & 1, t16);
   const int BH = p.B * p.Hq;
   const int bh = blockIdx.x % BH;
   const int qblk = p.nqblk - 1 - (int)(blockIdx.x / BH);   // longest rows first
@@ -106,8 +108,8 @@ __global__ __launch_bounds__(kFwdWaves * 64) void mala_fwd_kernel(FwdParams p) {
   for (int t = ttop; t >= 0; --t) {
     const int buf = (ttop - t) & 1;
     if (t > 0) fetch(t - 1);
-    const bf16* Kb = Ks + buf * STAGE;
-    const bf16* Vb = Vs + buf * STAGE;
+    const bf16* kr = lds_pin(Ks + buf * STAGE + rdo);
+    const bf16* vtb = lds_pin(Vs + buf * STAGE + tro);
 
     // Score discovery for both 32-key decision tiles of the stage at once (two
     // independent accumulators; all K operands are read from LDS first).
@@ -121,8 +123,8 @@ __global__ __launch_bounds__(kFwdWaves * 64) void mala_fwd_kernel(FwdParams p) {
         bf16x8 ka[2][KS];
 #pragma unroll
         for (int kk = 0; kk < KS; ++kk) {
-          ka[1][kk] = load8(Kb + tile_off<D>(kBk + c, 16 * kk + 8 * h));
-          ka[0][kk] = load8(Kb + tile_off<D>(c, 16 * kk + 8 * h));
+          ka[1][kk] = load8(kr + kBk * (D + 8) + rd_step<D>(kk));
+          ka[0][kk] = load8(kr + rd_step<D>(kk));
         }
 #pragma unroll
         for (int kk = 0; kk < KS; ++kk) {
@@ -201,10 +203,8 @@ __global__ __launch_bounds__(kFwdWaves * 64) void mala_fwd_kernel(FwdParams p) {
         for (int db = 0; db < DB; ++db)
 #pragma unroll
           for (int ks = 0; ks < 2; ++ks) {
-            const int vrow = sub * kBk + 16 * ks + 4 * h + (t16 >> 2);
-            const int vcol = 32 * db + 16 * (G & 1) + 4 * (t16 & 3);
-            va[db][ks] = cat(lds_read_tr(Vb + tile_off<D>(vrow, vcol)),
-                             lds_read_tr(Vb + tile_off<D>(vrow + 8, vcol)));
+            const bf16* vt = vtb + (sub * kBk + 16 * ks) * (D + 8) + tr_step<D>(db);
+            va[db][ks] = cat(lds_read_tr(vt), lds_read_tr(vt + 8 * (D + 8)));
           }
 #pragma unroll
         for (int ks = 0; ks < 2; ++ks)
