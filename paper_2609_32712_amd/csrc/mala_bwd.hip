@@ -111,37 +111,35 @@ __device__ __forceinline__ f32x16 qk_tile(const bf16x8 (&a)[KS], const bf16x8 (&
 // are only consulted on tiles that cross the diagonal or the end of the sequence
 // (need_mask, uniform over the wavefront).  The probability of an entry is then
 // exp2(fma(s, scale2, -lse2)).
-__device__ __forceinline__ bool offline_entries(const f32x16& s, float scale2, bool need_mask,
-                                                int klo, int qlim, const float* thrs, int h,
-                                                float (&sv)[16]) {
+template <bool MASK>
+__device__ __forceinline__ bool offline_test(const f32x16& s, float scale2, int klo, int qlim,
+                                             const float* thrs, int h, float (&sv)[16]) {
   // both backward kernels must round identically: explicit fma, no contraction
 #pragma clang fp contract(off)
   float dm = kNegInf;
-  if (need_mask) {
 #pragma unroll
-    for (int g = 0; g < 4; ++g) {
-      const f32x4 th = *reinterpret_cast<const f32x4*>(thrs + 8 * g + 4 * h);
+  for (int g = 0; g < 4; ++g) {
+    const f32x4 th = *reinterpret_cast<const f32x4*>(thrs + 8 * g + 4 * h);
 #pragma unroll
-      for (int e = 0; e < 4; ++e) {
+    for (int e = 0; e < 4; ++e) {
+      const float x = s[4 * g + e];
+      if (MASK) {
         const bool legal = (8 * g + e >= klo) && (8 * g + e < qlim);
-        const float x = s[4 * g + e];
         sv[4 * g + e] = legal ? x : kNegInf;
         dm = fmaxf(dm, legal ? __builtin_fmaf(x, scale2, -th[e]) : kNegInf);
-      }
-    }
-  } else {
-#pragma unroll
-    for (int g = 0; g < 4; ++g) {
-      const f32x4 th = *reinterpret_cast<const f32x4*>(thrs + 8 * g + 4 * h);
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const float x = s[4 * g + e];
+      } else {
         sv[4 * g + e] = x;
         dm = fmaxf(dm, __builtin_fmaf(x, scale2, -th[e]));
       }
     }
   }
   return dm >= 0.f;
+}
+__device__ __forceinline__ bool offline_entries(const f32x16& s, float scale2, bool need_mask,
+                                                int klo, int qlim, const float* thrs, int h,
+                                                float (&sv)[16]) {
+  return need_mask ? offline_test<true>(s, scale2, klo, qlim, thrs, h, sv)
+                   : offline_test<false>(s, scale2, klo, qlim, thrs, h, sv);
 }
 
 // P = exp2(s * scale2 - lse2) in place, for the C layout of qk_tile.
@@ -326,6 +324,13 @@ __global__ __launch_bounds__(512) void mala_bwd_dkdv_kernel(BwdParams p) {
       const bf16* dOb = dOs + (t % 3) * TILE;
       const bf16* otb = lds_pin(dOb + tro);
       const float* rv = &rowv[t % 3][0][0];
+      // dP first: its MFMA chain runs while P is split, and the dS arithmetic can
+      // then interleave with the dV MFMAs
+      bf16x8 oa[KS];
+      const bf16* orr = lds_pin(dOb + rdo);
+#pragma unroll
+      for (int kk = 0; kk < KS; ++kk) oa[kk] = load8(orr + rd_step<D>(kk));
+      const f32x16 dp = qk_tile<KS>(oa, kv);
       float ds[16];
 #pragma unroll
       for (int g = 0; g < 4; ++g) {
@@ -346,11 +351,6 @@ __global__ __launch_bounds__(512) void mala_bwd_dkdv_kernel(BwdParams p) {
           acc[db] = mfma32(a, ks ? pl1 : pl0, acc[db]);
         }
       }
-      bf16x8 oa[KS];
-      const bf16* orr = lds_pin(dOb + rdo);
-#pragma unroll
-      for (int kk = 0; kk < KS; ++kk) oa[kk] = load8(orr + rd_step<D>(kk));
-      const f32x16 dp = qk_tile<KS>(oa, kv);
       // dS = P (dP - D) in the C layout of dP
 #pragma unroll
       for (int g = 0; g < 4; ++g) {
@@ -387,6 +387,17 @@ __global__ __launch_bounds__(512) void mala_bwd_dkdv_kernel(BwdParams p) {
   if (p.counters && tid == 0) atomicAdd(&p.counters[2], (unsigned long long)total);
 }
 
+// Staging tile of dS in the query-major kernel: [32 keys][32 query positions] bf16
+// without padding.  The 16-byte chunk j (positions 8 j .. 8 j + 7) of key row r is
+// stored at chunk 16 (r / 4) + r % 4 + 4 ((j + r / 4) % 4).  Query 8 g + 4 h + e of a
+// lane's C registers goes to position 16 (g / 2) + 8 h + 4 (g % 2) + e, so each lane
+// writes its values as two whole chunks; the chunk writes (16 lanes: 16 rows, one
+// chunk) and the transposed reads (32 lanes: 4 rows, 4 chunks) are both free of
+// bank conflicts, and 16 rows further on is always 64 chunks further on.
+__device__ __forceinline__ int ds_chunk(int r, int j) {
+  return 16 * (r >> 2) + (r & 3) + 4 * ((j + (r >> 2)) & 3);
+}
+
 template <int D>
 __global__ __launch_bounds__(kFwdWaves * 64) void mala_bwd_dq_kernel(BwdParams p) {
   constexpr int NT = kFwdWaves * 64;
@@ -394,8 +405,8 @@ __global__ __launch_bounds__(kFwdWaves * 64) void mala_bwd_dq_kernel(BwdParams p
   constexpr int DB = D / 32;
   constexpr int STAGE = tile_elems<D>(kFwdStage);
   constexpr int CPT = kFwdStage * D / 8 / NT;
-  constexpr int DSS = kBq + 16;              // dS row stride [key][q]: 24 dwords
-  constexpr int DSW = 2 * kBk * DSS;         // one wavefront's dS planes (hi, lo)
+  constexpr int DSP = kBk * kBq;             // one dS plane [key][query position]
+  constexpr int DSW = 2 * DSP;               // one wavefront's dS planes (hi, lo)
   __shared__ __attribute__((aligned(16))) bf16 Ks[2 * STAGE];
   __shared__ __attribute__((aligned(16))) bf16 Vs[2 * STAGE];
   __shared__ __attribute__((aligned(16))) bf16 dSw[kFwdWaves * DSW];
@@ -440,7 +451,13 @@ __global__ __launch_bounds__(kFwdWaves * 64) void mala_bwd_dq_kernel(BwdParams p
   unsigned n_legal = 0, n_ret = 0;
   int cnt_row = 0;   // retained tiles in which row q0w + c has a legal key
   bf16* const dSh = dSw + wave * DSW;
-  bf16* const dSl = dSh + kBk * DSS;
+  bf16* const dSl = dSh + DSP;
+  // dS plane offsets: this lane's two chunk writes (key c, chunks h and 2 + h) and
+  // the bases of its transposed reads (key rows 4 h + t16 / 4 and 8 more)
+  const int dsw0 = 8 * ds_chunk(c, h), dsw1 = 8 * ds_chunk(c, 2 + h);
+  const int dsj = 2 * (G & 1) + ((t16 >> 1) & 1);
+  const int dsr0 = 8 * ds_chunk(4 * h + (t16 >> 2), dsj) + 4 * (t16 & 1);
+  const int dsr1 = 8 * ds_chunk(8 + 4 * h + (t16 >> 2), dsj) + 4 * (t16 & 1);
 
   bf16x8 pk[CPT], pv[CPT];
   auto fetch = [&](int t) {
@@ -511,25 +528,17 @@ __global__ __launch_bounds__(kFwdWaves * 64) void mala_bwd_dq_kernel(BwdParams p
       bf16x8 dh[2], dl[2];
       split_bf16x8(dsv, dh[0], dl[0]);
       split_bf16x8(dsv + 8, dh[1], dl[1]);
-      // dS^T -> this wavefront's LDS planes as [key][q]
-#pragma unroll
-      for (int g = 0; g < 4; ++g) {
-        const int o4 = 4 * (g & 1);
-        const bf16x8& hs = dh[g >> 1];
-        const bf16x8& ls = dl[g >> 1];
-        bf16x4 wh = {hs[o4], hs[o4 + 1], hs[o4 + 2], hs[o4 + 3]};
-        bf16x4 wl = {ls[o4], ls[o4 + 1], ls[o4 + 2], ls[o4 + 3]};
-        *reinterpret_cast<bf16x4*>(dSh + c * DSS + 8 * g + 4 * h) = wh;
-        *reinterpret_cast<bf16x4*>(dSl + c * DSS + 8 * g + 4 * h) = wl;
-      }
+      // dS^T -> this wavefront's LDS planes as [key][query position]
+      store8(dSh + dsw0, dh[0]);
+      store8(dSh + dsw1, dh[1]);
+      store8(dSl + dsw0, dl[0]);
+      store8(dSl + dsw1, dl[1]);
       wave_lds_sync();
-      // dQ[q][d] += dS[q][key] K[key][d]
+      // dQ[q][d] += dS[q][key] K[key][d]; MFMA row m holds query position m
 #pragma unroll
       for (int ks = 0; ks < 2; ++ks) {
-        const int arow = 16 * ks + 4 * h + (t16 >> 2);
-        const int ao = arow * DSS + 16 * (G & 1) + 4 * (t16 & 3);
-        const bf16x8 ah = cat(lds_read_tr(dSh + ao), lds_read_tr(dSh + ao + 8 * DSS));
-        const bf16x8 al = cat(lds_read_tr(dSl + ao), lds_read_tr(dSl + ao + 8 * DSS));
+        const bf16x8 ah = cat(lds_read_tr(dSh + dsr0 + 512 * ks), lds_read_tr(dSh + dsr1 + 512 * ks));
+        const bf16x8 al = cat(lds_read_tr(dSl + dsr0 + 512 * ks), lds_read_tr(dSl + dsr1 + 512 * ks));
 #pragma unroll
         for (int db = 0; db < DB; ++db) {
           const bf16* kt = ktb + (sub * kBk + 16 * ks) * (D + 8) + tr_step<D>(db);
@@ -544,12 +553,14 @@ __global__ __launch_bounds__(kFwdWaves * 64) void mala_bwd_dq_kernel(BwdParams p
     __syncthreads();
   }
 
-  // dQ = scale * sum dS K; lane (h, c) holds column 32 db + c of rows 8 (r / 4) + 4 h + r % 4
+  // dQ = scale * sum dS K; lane (h, c) holds column 32 db + c of the query positions
+  // m = 8 (r / 4) + 4 h + r % 4, i.e. of queries m with bits 2 and 3 swapped
 #pragma unroll
   for (int db = 0; db < DB; ++db)
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
-      const long qq = (long)q0w + 8 * (r >> 2) + 4 * h + (r & 3);
+      const int m = 8 * (r >> 2) + 4 * h + (r & 3);
+      const long qq = (long)q0w + ((m & ~12) | ((m & 4) << 1) | ((m & 8) >> 1));
       if (qq < p.Nq) p.dq[((long)bh * p.Nq + qq) * D + 32 * db + c] = acc[db][r] * p.scale;
     }
   if (p.row_tiles && h == 0 && row_valid) p.row_tiles[(long)bh * p.Nq + q0w + c] = cnt_row;
