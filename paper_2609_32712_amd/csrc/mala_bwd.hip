@@ -2,23 +2,24 @@
 // tile decisions.
 //
 // mala_bwd_dkdv_kernel (key-major, Algorithm 2's traversal): one workgroup owns 128
-// keys of one (batch, KV head), with their K and V rows in LDS, and keeps their dK
-// and dV in registers for the whole kernel (no atomics, bitwise reproducible); it
+// keys of one (batch, KV head), with their K and V rows in registers, and keeps their
+// dK and dV in registers for the whole kernel (no atomics, bitwise reproducible); it
 // loops over every query head of the GQA group and over the query tiles from the
 // end down to the diagonal.  Eight wavefronts in two pipelined roles over keys
 // [32 (w % 4), +32): wavefronts 4-7 take the tile decisions, form P and accumulate
-// dK; wavefronts 0-3 accumulate dV and form dP and dS; P and dS pass between the
-// two through LDS.  Each wavefront holds a 64-register accumulator (two
-// wavefronts per SIMD) and runs 24 MFMAs per retained tile.  Query tiles (Q, dO and the per-row base-2 LSE,
-// threshold and D_q = rowsum(O * dO)) are double-buffered in LDS; the next tile is
-// fetched into registers while the current one is processed.
+// dV; one tile later wavefronts 0-3 form dP and dS and accumulate dK; P passes
+// between the two through LDS.  Each wavefront holds a 64-register accumulator
+// (two wavefronts per SIMD) and runs 24 MFMAs per retained tile.  Query tiles (Q,
+// dO and the per-row base-2 LSE, threshold and D_q = rowsum(O * dO)) rotate
+// through three LDS buffers; the next tile is fetched into registers while the
+// current one is processed.
 //   S = Q_i K_w^T         8 MFMAs (lane = one key column, 16 query rows)
 //   offline test          retain iff some valid entry has
 //                         s - lse_q >= log2(tau) - log2(L_q) (base-2 units); ballot
-//   retained path         P = exp2(S - lse) (handed on as bf16 hi + lo operands);
-//                         one tile later: dV^T += dO_i^T P, dP = dO_i V_w^T,
-//                         dS = P (dP - D_q) (handed back); two tiles later:
-//                         dK^T += Q_i^T dS; the A operands come through
+//   retained path         P = exp2(S - lse) (handed on in fp32), dV^T += dO_i^T P;
+//                         one tile later: dP = dO_i V_w^T, dS = P (dP - D_q),
+//                         dK^T += Q_i^T dS.  P and dS enter the MFMAs as two bf16
+//                         terms (hi + lo); the A operands come through
 //                         ds_read_b64_tr_b16.
 // mala_bwd_dq_kernel (query-major, like the forward): one workgroup = 8 wavefronts
 // = 256 query rows; K and V stream through double-buffered LDS.  Per decision
@@ -178,23 +179,23 @@ __global__ __launch_bounds__(512) void mala_bwd_dkdv_kernel(BwdParams p) {
   constexpr int TILE = tile_elems<D>(kBq);          // one Q or dO tile in LDS
   constexpr int NCH = kBq * D / 8;                  // 16-byte chunks of one query tile
   static_assert(NCH <= NT, "one chunk per thread");
-  // rings: Q is read at iterations t and t + 2, dO and the row vectors at t and t + 1
-  __shared__ __attribute__((aligned(16))) bf16 Qs[4 * TILE];
+  // rings of query tiles: tile t is read at iterations t and t + 1
+  __shared__ __attribute__((aligned(16))) bf16 Qs[3 * TILE];
   __shared__ __attribute__((aligned(16))) bf16 dOs[3 * TILE];
   __shared__ __attribute__((aligned(16))) float rowv[3][3][kBq];   // lse2, threshold, D_q
-  // hand-off: P in fp32 as [buf][key wave][C registers 4g .. 4g+3][lane]; dS as the
-  // B operands [buf][key wave][hi0, hi1, lo0, lo1][lane]
+  // hand-off: P in fp32 as [buf][key wave][C registers 4g .. 4g+3][lane]
   __shared__ __attribute__((aligned(16))) f32x4 Pf[2][4][4][64];
-  __shared__ __attribute__((aligned(16))) bf16x8 dSop[2][4][4][64];
-  __shared__ int Pflag[3][4];
+  __shared__ int Pflag[2][4];
 
   // Two wavefronts per 32 keys [32 (w % 4), +32), on the same SIMD, in a pipeline:
-  //   producer (w >= 4), iteration t:    S_t, offline test, P_t -> LDS; dK += Q_{t-2}^T dS_{t-2}
-  //   consumer (w < 4),  iteration t+1:  dV += dO_t^T P_t; dP_t = dO_t V^T,
-  //                                      dS_t = P_t (dP_t - D) -> LDS
-  // Each wavefront runs 24 MFMAs per retained tile; P and dS travel as the exact
-  // bf16 hi / lo B operands of the receiving lane (same lane, same layout).
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  //   producer (w >= 4), iteration t:    S_t = Q_t K^T, offline test, P_t -> LDS,
+  //                                      dV += dO_t^T P_t
+  //   consumer (w < 4),  iteration t+1:  dP_t = dO_t V^T, dS_t = P_t (dP_t - D),
+  //                                      dK += Q_t^T dS_t
+  // Each wavefront runs 24 MFMAs per retained tile; P travels through LDS in fp32,
+  // in the C layout that both wavefronts share.
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const bool producer = wave >= 4;
   const int kwave = wave & 3;
   const int kw_local = kwave * kBk;
@@ -218,9 +219,8 @@ __global__ __launch_bounds__(512) void mala_bwd_dkdv_kernel(BwdParams p) {
     for (int kk = 0; kk < KS; ++kk)
       kv[kk] = key < p.Nk ? load8(src + (long)key * D + 16 * kk + 8 * h) : zero8();
   }
-  if (tid < 12) Pflag[tid >> 2][tid & 3] = 0;
 
-  f32x16 acc[DB];
+  f32x16 acc[DB];    // producer: dV^T, consumer: dK^T (unscaled)
 #pragma unroll
   for (int db = 0; db < DB; ++db)
 #pragma unroll
@@ -235,32 +235,46 @@ __global__ __launch_bounds__(512) void mala_bwd_dkdv_kernel(BwdParams p) {
   // Query tiles are swept from the last one down to the block's diagonal: the
   // offline test does not depend on the order, and co-resident workgroups of the
   // same KV head (one per CU of an XCD) then read the same Q / dO tiles at about the
-  // same time, so those come from L2 instead of HBM.
+  // same time, so those come from L2 instead of HBM.  The next tile is fetched into
+  // registers while the current one is processed; the arithmetic on the fetched
+  // row values waits until the store to LDS, so that no wavefront stalls on the
+  // loads inside the iteration.
   auto tile_q0 = [&](int it) { return (nqt - 1 - it % per_head) * kBq; };
-  bf16x8 pq = zero8(), pdo = zero8();
-  float plse = 0.f, pthr = 0.f, pdv = 0.f;
+  // tiles come through buffer loads: rows past the end of the sequence read as zeros
+  const uint32_t voff = (uint32_t)((tid / (D / 8)) * D + (tid % (D / 8)) * 8) * 2;
+  bf16x8 pq, pdo;
+  float plse = 0.f, pdv = 0.f, plg = 0.f;
+  bool prow = false;
   auto fetch = [&](int it) {
     const long bhq = (long)b * p.Hq + hkv * grp + it / per_head;
     const int q0 = tile_q0(it);
-    if (tid < NCH) {
-      const int row = tid / (D / 8), col = (tid % (D / 8)) * 8;
-      const long qq = (long)q0 + row;
-      const bool ok = qq < p.Nq;
-      pq = ok ? load8(p.q + (bhq * p.Nq + qq) * D + col) : zero8();
-      pdo = ok ? load8(p.dout + (bhq * p.Nq + qq) * D + col) : zero8();
+    const long r0 = bhq * p.Nq + q0;
+    if (tid < kBq) {
+      const uint32_t nr = (uint32_t)(p.Nq - q0) * 4u;
+      plse = buf_load1(make_rsrc(p.lse + r0, nr), tid * 4u);
+      pdv = buf_load1(make_rsrc(p.dvec + r0, nr), tid * 4u);
+      prow = q0 + tid < p.Nq;
+      plg = log2f((float)((long)q0 + tid + 1 + off));
     }
-    if (tid < kBq) row_vectors(p, bhq, (long)q0 + tid, off, &plse, &pthr, &pdv);
+    if (tid < NCH) {
+      const uint32_t nb = (uint32_t)(p.Nq - q0) * (uint32_t)D * 2u;
+      pq = buf_load8(make_rsrc(p.q + r0 * D, nb), voff);
+      pdo = buf_load8(make_rsrc(p.dout + r0 * D, nb), voff);
+    }
   };
   auto stash = [&](int it) {
     if (tid < NCH) {
       const int row = tid / (D / 8), col = (tid % (D / 8)) * 8;
-      store8(Qs + (it & 3) * TILE + tile_off<D>(row, col), pq);
+      store8(Qs + (it % 3) * TILE + tile_off<D>(row, col), pq);
       store8(dOs + (it % 3) * TILE + tile_off<D>(row, col), pdo);
     }
     if (tid < kBq) {
-      rowv[it % 3][0][tid] = plse;
-      rowv[it % 3][1][tid] = pthr;
-      rowv[it % 3][2][tid] = pdv;
+      // the same arithmetic as row_vectors (the query-major kernel must agree bitwise)
+#pragma clang fp contract(off)
+      const float l2 = plse * kLog2e;
+      rowv[it % 3][0][tid] = prow ? l2 : 0.f;
+      rowv[it % 3][1][tid] = prow ? l2 + p.log2tau - plg : __builtin_huge_valf();
+      rowv[it % 3][2][tid] = prow ? pdv : 0.f;
     }
   };
 
@@ -268,66 +282,57 @@ __global__ __launch_bounds__(512) void mala_bwd_dkdv_kernel(BwdParams p) {
   stash(0);
   __syncthreads();
 
-  for (int it = 0; it <= total + 1; ++it) {
+  for (int it = 0; it <= total; ++it) {
     if (it + 1 < total) fetch(it + 1);
+    // each role prepares the B operands (hi, lo per k-step) and the transposed A tile
+    // of its accumulator update; the update itself is one piece of code for both
+    // roles, so that the accumulator stays in the same registers
+    bool upd = false;
+    bf16x8 bh0, bh1, bl0, bl1;
+    const bf16* atb = nullptr;
     if (producer) {
       if (it < total) {
-        // tile it: score discovery, test, P
+        // tile it: score discovery, test, P; then dV^T += dO^T P
         const int q0 = tile_q0(it);
-        const bf16* Qb = Qs + (it & 3) * TILE;
-        const float* rv = &rowv[it % 3][0][0];
-        const int qlast = min(q0 + kBq - 1, p.Nq - 1);
-        bool ret = false;
-        if (kw < p.Nk && (long)kw <= (long)qlast + off) {
-          bf16x8 qa[KS];
-          const bf16* qr = lds_pin(Qb + rdo);
+        const int slot = it % 3;
+        const float* rv = &rowv[slot][0][0];
+        // the tile decision and P are the critical path of the pipeline: raise this
+        // wavefront's issue priority over its partner's MFMAs until P is out
+        __builtin_amdgcn_s_setprio(3);
+        bf16x8 qa[KS];
+        const bf16* qr = lds_pin(Qs + slot * TILE + rdo);
 #pragma unroll
-          for (int kk = 0; kk < KS; ++kk) qa[kk] = load8(qr + rd_step<D>(kk));
-          const f32x16 s = qk_tile<KS>(qa, kv);
-          const bool need_mask =
-              ((long)kw + kBk - 1 > (long)q0 + off) || (q0 + kBq > p.Nq) || (kw + kBk > p.Nk);
-          const int klo = key < p.Nk ? (int)((long)key - off - q0) - 4 * h : 1000000;
-          float sv[16];
-          const bool dem =
-              offline_entries(s, p.scale2, need_mask, klo, p.Nq - q0 - 4 * h, rv + kBq, h, sv);
-          ret = wave_any(dem);
-          if (ret) {
-            probabilities(sv, p.scale2, rv, h);
+        for (int kk = 0; kk < KS; ++kk) qa[kk] = load8(qr + rd_step<D>(kk));
+        const f32x16 sc = qk_tile<KS>(qa, kv);
+        // tiles that cross the diagonal or the end of the sequence (or whose keys all
+        // lie beyond this tile's rows) take the masked test
+        const bool need_mask =
+            ((long)kw + kBk - 1 > (long)q0 + off) || (q0 + kBq > p.Nq) || (kw + kBk > p.Nk);
+        const int klo = key < p.Nk ? (int)((long)key - off - q0) - 4 * h : 1000000;
+        float sv[16];
+        const bool dem =
+            offline_entries(sc, p.scale2, need_mask, klo, p.Nq - q0 - 4 * h, rv + kBq, h, sv);
+        const bool ret = wave_any(dem);
+        if (ret) {
+          probabilities(sv, p.scale2, rv, h);
 #pragma unroll
-            for (int g = 0; g < 4; ++g)
-              Pf[it & 1][kwave][g][lane] =
-                  f32x4{sv[4 * g], sv[4 * g + 1], sv[4 * g + 2], sv[4 * g + 3]};
-          }
+          for (int g = 0; g < 4; ++g)
+            Pf[it & 1][kwave][g][lane] = f32x4{sv[4 * g], sv[4 * g + 1], sv[4 * g + 2], sv[4 * g + 3]};
+          split_bf16x8(sv, bh0, bl0);
+          split_bf16x8(sv + 8, bh1, bl1);
+          atb = dOs + slot * TILE + tro;
+          upd = true;
         }
-        if (lane == 0) Pflag[it % 3][kwave] = ret ? 1 : 0;
+        if (lane == 0) Pflag[it & 1][kwave] = ret ? 1 : 0;
+        __builtin_amdgcn_s_setprio(0);
       }
-      if (it >= 2 && it - 2 < total && Pflag[(it - 2) % 3][kwave]) {
-        // dK^T += Q^T dS for tile it - 2
-        const bf16* qtb = lds_pin(Qs + ((it - 2) & 3) * TILE + tro);
-        const int sb = (it - 2) & 1;
-        const bf16x8 dh0 = dSop[sb][kwave][0][lane], dh1 = dSop[sb][kwave][1][lane];
-        const bf16x8 dl0 = dSop[sb][kwave][2][lane], dl1 = dSop[sb][kwave][3][lane];
-#pragma unroll
-        for (int db = 0; db < DB; ++db) {
-#pragma unroll
-          for (int ks = 0; ks < 2; ++ks) {
-            const bf16* qt = qtb + 16 * ks * (D + 8) + tr_step<D>(db);
-            const bf16x8 a = cat(lds_read_tr(qt), lds_read_tr(qt + 8 * (D + 8)));
-            acc[db] = mfma32(a, ks ? dh1 : dh0, acc[db]);
-            acc[db] = mfma32(a, ks ? dl1 : dl0, acc[db]);
-          }
-        }
-      }
-    } else if (it >= 1 && it - 1 < total && Pflag[(it - 1) % 3][kwave]) {
-      // consumer, tile t = it - 1: dV^T += dO^T P; dP = dO V^T; dS = P (dP - D)
+    } else if (it >= 1 && Pflag[(it - 1) & 1][kwave]) {
+      // consumer, tile t = it - 1: dP = dO V^T; dS = P (dP - D); then dK^T += Q^T dS
       const int t = it - 1;
-      const bf16* dOb = dOs + (t % 3) * TILE;
-      const bf16* otb = lds_pin(dOb + tro);
-      const float* rv = &rowv[t % 3][0][0];
-      // dP first: its MFMA chain runs while P is split, and the dS arithmetic can
-      // then interleave with the dV MFMAs
+      const int slot = t % 3;
+      const float* rv = &rowv[slot][0][0];
       bf16x8 oa[KS];
-      const bf16* orr = lds_pin(dOb + rdo);
+      const bf16* orr = lds_pin(dOs + slot * TILE + rdo);
 #pragma unroll
       for (int kk = 0; kk < KS; ++kk) oa[kk] = load8(orr + rd_step<D>(kk));
       const f32x16 dp = qk_tile<KS>(oa, kv);
@@ -335,46 +340,37 @@ __global__ __launch_bounds__(512) void mala_bwd_dkdv_kernel(BwdParams p) {
 #pragma unroll
       for (int g = 0; g < 4; ++g) {
         const f32x4 p4 = Pf[t & 1][kwave][g][lane];
+        const f32x4 d4 = *reinterpret_cast<const f32x4*>(rv + 2 * kBq + 8 * g + 4 * h);
 #pragma unroll
-        for (int e = 0; e < 4; ++e) ds[4 * g + e] = p4[e];
+        for (int e = 0; e < 4; ++e) ds[4 * g + e] = p4[e] * (dp[4 * g + e] - d4[e]);
       }
-      bf16x8 ph0, ph1, pl0, pl1;
-      split_bf16x8(ds, ph0, pl0);
-      split_bf16x8(ds + 8, ph1, pl1);
+      split_bf16x8(ds, bh0, bl0);
+      split_bf16x8(ds + 8, bh1, bl1);
+      atb = Qs + slot * TILE + tro;
+      upd = true;
+    }
+    if (upd) {
+      const bf16* ab = lds_pin(atb);
 #pragma unroll
       for (int db = 0; db < DB; ++db) {
 #pragma unroll
         for (int ks = 0; ks < 2; ++ks) {
-          const bf16* ot = otb + 16 * ks * (D + 8) + tr_step<D>(db);
-          const bf16x8 a = cat(lds_read_tr(ot), lds_read_tr(ot + 8 * (D + 8)));
-          acc[db] = mfma32(a, ks ? ph1 : ph0, acc[db]);
-          acc[db] = mfma32(a, ks ? pl1 : pl0, acc[db]);
+          const bf16* at = ab + 16 * ks * (D + 8) + tr_step<D>(db);
+          const bf16x8 a = cat(lds_read_tr(at), lds_read_tr(at + 8 * (D + 8)));
+          acc[db] = mfma32(a, ks ? bh1 : bh0, acc[db]);
+          acc[db] = mfma32(a, ks ? bl1 : bl0, acc[db]);
         }
       }
-      // dS = P (dP - D) in the C layout of dP
-#pragma unroll
-      for (int g = 0; g < 4; ++g) {
-        const f32x4 d4 = *reinterpret_cast<const f32x4*>(rv + 2 * kBq + 8 * g + 4 * h);
-#pragma unroll
-        for (int e = 0; e < 4; ++e) ds[4 * g + e] = ds[4 * g + e] * (dp[4 * g + e] - d4[e]);
-      }
-      bf16x8 xh[2], xl[2];
-      split_bf16x8(ds, xh[0], xl[0]);
-      split_bf16x8(ds + 8, xh[1], xl[1]);
-      dSop[t & 1][kwave][0][lane] = xh[0];
-      dSop[t & 1][kwave][1][lane] = xh[1];
-      dSop[t & 1][kwave][2][lane] = xl[0];
-      dSop[t & 1][kwave][3][lane] = xl[1];
     }
     if (it + 1 < total) stash(it + 1);
     __syncthreads();
   }
 
-  // dV = sum P^T dO (consumers), dK = scale * sum dS^T Q (producers); lane (h, c)
+  // dV = sum P^T dO (producers), dK = scale * sum dS^T Q (consumers); lane (h, c)
   // holds key kw + c
   if (key < p.Nk) {
-    const float f = producer ? p.scale : 1.f;
-    float* dst = (producer ? p.dk : p.dv) + ((long)bhk * p.Nk + key) * D;
+    const float f = producer ? 1.f : p.scale;
+    float* dst = (producer ? p.dv : p.dk) + ((long)bhk * p.Nk + key) * D;
 #pragma unroll
     for (int db = 0; db < DB; ++db)
 #pragma unroll

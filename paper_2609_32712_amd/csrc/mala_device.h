@@ -117,6 +117,22 @@ __device__ __forceinline__ const bf16* lds_pin(const bf16* p) {
   return (const bf16*)q;
 }
 
+// Loads through a buffer resource (base address, size in bytes): each lane gives a
+// byte offset, and offsets at or past the size read as zeros, which covers the
+// ragged end of a sequence without a compare or a clamp.  The address arithmetic
+// is then one 32-bit lane offset plus scalar registers.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes,
+                                           0x00020000);
+}
+__device__ __forceinline__ bf16x8 buf_load8(__amdgpu_buffer_rsrc_t r, uint32_t byte_off) {
+  typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
+  return __builtin_bit_cast(bf16x8, __builtin_amdgcn_raw_buffer_load_b128(r, byte_off, 0, 0));
+}
+__device__ __forceinline__ float buf_load1(__amdgpu_buffer_rsrc_t r, uint32_t byte_off) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(r, byte_off, 0, 0));
+}
+
 // Hardware base-2 exponential / logarithm (v_exp_f32 / v_log_f32, ~1 ulp on normal
 // results).  The softmax arguments are <= 0, so the results lie in [0, 1]; values
 // below 2^-126 may flush to zero, which no tolerance here can see.
