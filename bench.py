@@ -211,6 +211,127 @@ def cpu_baseline(step_ms_model):
             "fwd_ms": round(ms_fwd, 1), "bwd_ms": round(ms_bwd, 1), "decode_ms": round(ms_dec, 1)}
 
 
+COUNTER_CMD = ("cd /tmp && export TMPDIR=/tmp && timeout -s KILL 180 rocprofv3 --pmc {c} "
+               "--output-format csv -d $REPO/gpurun_out/pmc_{d} -o run -- "
+               "python $REPO/bench.py --counter-pass")
+TRACE_CMD = ("cd /tmp && export TMPDIR=/tmp && timeout -k 10 600 rocprofv3 --kernel-trace --stats "
+             "--output-format csv -d $REPO/gpurun_out/trace_bench -o bench -- "
+             "python $REPO/bench.py --steps 2 --warmup 1 --reps 2 --no-cpu-baseline --no-32k")
+
+
+def counter_pass():
+    """The program the traffic counters are taken on: a plain 512 MiB device copy
+    (the calibration kernel), then two mala_fwd + mala_bwd calls of the
+    131072-token workload."""
+    import torch
+    import paper_2609_32712_amd as mala
+    mala.load_library()
+    x = torch.empty(512 << 20, dtype=torch.uint8, device="cuda")
+    x.fill_(1)
+    y = torch.empty_like(x)
+    y.copy_(x)
+    torch.cuda.synchronize()
+    del x, y
+    tr = Train(4, 1e-4)
+    for _ in range(2):
+        tr.fwd(1e-4)
+        tr.bwd(1e-4)
+    torch.cuda.synchronize()
+    log("counter pass done")
+
+
+def _counter_means(path):
+    """Per-kernel mean over dispatches of a rocprofv3 counter CSV (KiB for the
+    *_SIZE counters); values of one dispatch are summed first."""
+    import csv
+    import collections
+    per = collections.defaultdict(float)
+    names = {}
+    with open(path) as fh:
+        for r in csv.DictReader(fh):
+            per[r["Dispatch_Id"]] += float(r["Counter_Value"])
+            names[r["Dispatch_Id"]] = r["Kernel_Name"]
+    by = collections.defaultdict(list)
+    for d, v in per.items():
+        by[names[d]].append(v)
+    return {k: sum(v) / len(v) for k, v in by.items()}
+
+
+def summarize_counters(fetch_csv, write_csv):
+    """profiles/mala_bwd_traffic_128k.json: HBM bytes per mala_bwd launch from the
+    FETCH_SIZE and WRITE_SIZE passes, each scaled by what the counter reads for the
+    512 MiB copy of the same run."""
+    f, w = _counter_means(fetch_csv), _counter_means(write_csv)
+    copy = [k for k in f if "copy" in k.lower()]
+    if not copy:
+        raise SystemExit("no copy kernel in %s" % fetch_csv)
+    copy = copy[0]
+    kib = 512 * 1024
+    fscale, wscale = round(kib / f[copy], 1), round(kib / w[copy], 1)
+    kernels, total = {}, 0.0
+    for k in sorted(f):
+        if "mala_bwd" in k or "mala_fill_zero" in k:
+            b = (f[k] * fscale + w.get(k, 0.0) * wscale) * 1024
+            if "mala_bwd" in k:
+                total += b
+            kernels[k] = {"fetch_kib": f[k], "write_kib": w.get(k, 0.0), "bytes": b}
+    out = {"source_sha": source_sha(os.path.join(ROOT, "paper_2609_32712_amd", "csrc",
+                                                 "mala_bwd.hip")),
+           "bytes_per_launch": total, "fetch_scale": fscale, "write_scale": wscale,
+           "kernels": kernels,
+           "calibration": {"copy_kernel": copy, "copy_bytes": 512 << 20,
+                           "copy_fetch_kib": f[copy], "copy_write_kib": w[copy]},
+           "workload": "mala_bwd on the 131072-token share (8 q / 2 kv heads, d 128), tau 1e-4",
+           "commands": [COUNTER_CMD.format(c="FETCH_SIZE", d="fetch"),
+                        COUNTER_CMD.format(c="WRITE_SIZE", d="write"),
+                        "python bench.py --summarize-counters "
+                        "gpurun_out/pmc_fetch/run_counter_collection.csv "
+                        "gpurun_out/pmc_write/run_counter_collection.csv"]}
+    with open(os.path.join(ROOT, "profiles", "mala_bwd_traffic_128k.json"), "w") as fh:
+        json.dump(out, fh, indent=1)
+    print("mala_bwd HBM bytes per launch %.3f GB (fetch x%.1f, write x%.1f)"
+          % (total / 1e9, fscale, wscale))
+
+
+def summarize_trace(trace_csv):
+    """profiles/kernels_128k_train_and_decode.md from the rocprofv3 kernel trace of
+    TRACE_CMD.  That run calls each operator 3 times at tau = 1e-4 (1 warm-up + 2
+    timed steps), then 3 times at each of tau = 1e-4, 0 and 1 (1 warm-up + 2 event-
+    timed calls), so every kernel has 12 dispatches in that order."""
+    import csv
+    import collections
+    with open(trace_csv) as fh:
+        rows = list(csv.DictReader(fh))
+    rows.sort(key=lambda r: int(r["Start_Timestamp"]))
+    dur = collections.defaultdict(list)
+    for r in rows:
+        dur[r["Kernel_Name"]].append((int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e6)
+    ms = lambda v: sum(v) / len(v) if v else float("nan")
+    lines = ["# Kernel time of one bench run: 131072-token fwd + bwd and decode", "",
+             "Command (run from the repository root on one MI355X; `$REPO` is that root):", "",
+             "```", TRACE_CMD, "python bench.py --summarize-trace "
+             "gpurun_out/trace_bench/bench_kernel_trace.csv", "```", "",
+             "Durations in milliseconds from the rocprofv3 kernel trace.  Each operator is "
+             "called 12 times: dispatches 1-6 at tau = 1e-4 (the bench step and its "
+             "event-timed calls), 7-9 at tau = 0 (dense through the same kernels), 10-12 at "
+             "tau = 1.", "",
+             "| kernel | calls | mean ms, tau 1e-4 | mean ms, tau 0 | mean ms, tau 1 | total ms |",
+             "|---|---|---|---|---|---|"]
+    for k, v in sorted(dur.items(), key=lambda kv: -sum(kv[1])):
+        n = len(v)
+        if n % 12 == 0:
+            m = n // 12
+            cells = (ms(v[:6 * m]), ms(v[6 * m:9 * m]), ms(v[9 * m:]))
+            lines.append("| `%s` | %d | %.3f | %.3f | %.3f | %.3f |"
+                         % ((k.replace("|", "/"), n) + cells + (sum(v),)))
+        else:
+            lines.append("| `%s` | %d | %.3f (all) | | | %.3f |" % (k.replace("|", "/"), n, ms(v),
+                                                                  sum(v)))
+    with open(os.path.join(ROOT, "profiles", "kernels_128k_train_and_decode.md"), "w") as fh:
+        fh.write("\n".join(lines) + "\n")
+    print("\n".join(lines))
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -220,12 +341,25 @@ def main():
     ap.add_argument("--reps", type=int, default=5, help="event-timed calls per kernel and tau")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-32k", action="store_true")
+    ap.add_argument("--counter-pass", action="store_true",
+                    help="run only the program profiled for the traffic counters")
+    ap.add_argument("--summarize-counters", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"))
+    ap.add_argument("--summarize-trace", metavar="KERNEL_TRACE_CSV")
     args = ap.parse_args()
+    if args.summarize_counters:
+        summarize_counters(*args.summarize_counters)
+        return
+    if args.summarize_trace:
+        summarize_trace(args.summarize_trace)
+        return
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU only: the MALA operator is built and measured on a "
               "single MI355X (heads and batch shard with no exchange; see the design notes).",
               file=sys.stderr)
         sys.exit(2)
+    if args.counter_pass:
+        counter_pass()
+        return
     import torch
     import paper_2609_32712_amd as mala
     assert torch.cuda.is_available(), "bench.py needs a GPU"
