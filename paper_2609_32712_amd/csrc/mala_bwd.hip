@@ -455,16 +455,18 @@ __global__ __launch_bounds__(kFwdWaves * 64) void mala_bwd_dq_kernel(BwdParams p
   const int dsr0 = 8 * ds_chunk(4 * h + (t16 >> 2), dsj) + 4 * (t16 & 1);
   const int dsr1 = 8 * ds_chunk(8 + 4 * h + (t16 >> 2), dsj) + 4 * (t16 & 1);
 
+  // K / V stages come through buffer loads: keys past the end read as zeros
   bf16x8 pk[CPT], pv[CPT];
   auto fetch = [&](int t) {
+    const long k0 = (long)t * kFwdStage;
+    const uint32_t nb = (uint32_t)(p.Nk - k0) * (uint32_t)D * 2u;
+    const auto rk = make_rsrc(Kp + k0 * D, nb), rvv = make_rsrc(Vp + k0 * D, nb);
 #pragma unroll
     for (int e = 0; e < CPT; ++e) {
       const int ch = tid + NT * e;
-      const int row = ch / (D / 8), col = (ch % (D / 8)) * 8;
-      const long key = (long)t * kFwdStage + row;
-      const bool ok = key < p.Nk;
-      pk[e] = ok ? load8(Kp + key * D + col) : zero8();
-      pv[e] = ok ? load8(Vp + key * D + col) : zero8();
+      const uint32_t off_b = (uint32_t)((ch / (D / 8)) * D + (ch % (D / 8)) * 8) * 2u;
+      pk[e] = buf_load8(rk, off_b);
+      pv[e] = buf_load8(rvv, off_b);
     }
   };
   auto stash = [&](int buf) {
