@@ -332,6 +332,42 @@ def summarize_trace(trace_csv):
     print("\n".join(lines))
 
 
+def summarize_mfma(csv_path):
+    """profiles/mfma_util_128k.md from a `rocprofv3 --pmc MfmaUtil MfmaFlopsBF16` pass
+    over --counter-pass (rocprofv3's derived counters: MFMA-busy SIMD cycles over
+    active cycles x SIMDs, and executed bf16 MFMA flops)."""
+    import csv
+    import collections
+    per = collections.defaultdict(dict)
+    names = {}
+    with open(csv_path) as fh:
+        for r in csv.DictReader(fh):
+            d = r["Dispatch_Id"]
+            per[d][r["Counter_Name"]] = per[d].get(r["Counter_Name"], 0.0) + float(r["Counter_Value"])
+            names[d] = r["Kernel_Name"]
+    by = collections.defaultdict(list)
+    for d, v in per.items():
+        if "mala" in names[d]:
+            by[names[d]].append(v)
+    cmd = COUNTER_CMD.format(c="MfmaUtil MfmaFlopsBF16", d="mfma")
+    lines = ["# MFMA utilisation of the 131072-token fwd + bwd kernels", "",
+             "Command (from the repository root on one MI355X; `$REPO` is that root):", "",
+             "```", cmd, "python bench.py --summarize-mfma gpurun_out/pmc_mfma/run_counter_collection.csv",
+             "```", "",
+             "`MfmaUtil` = MFMA-busy cycles summed over SIMDs / (active cycles x SIMDs), %; "
+             "`MfmaFlopsBF16` = executed bf16 MFMA flops per dispatch (the hi/lo split and "
+             "the dQ pass's recomputation included).  Mean over the dispatches of the run.", "",
+             "| kernel | dispatches | MfmaUtil % | executed bf16 MFMA TFLOP per dispatch |",
+             "|---|---|---|---|"]
+    for k, vs in sorted(by.items()):
+        u = sum(v.get("MfmaUtil", 0.0) for v in vs) / len(vs)
+        f = sum(v.get("MfmaFlopsBF16", 0.0) for v in vs) / len(vs)
+        lines.append("| `%s` | %d | %.1f | %.2f |" % (k.replace("|", "/"), len(vs), u, f / 1e12))
+    with open(os.path.join(ROOT, "profiles", "mfma_util_128k.md"), "w") as fh:
+        fh.write("\n".join(lines) + "\n")
+    print("\n".join(lines))
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -345,12 +381,16 @@ def main():
                     help="run only the program profiled for the traffic counters")
     ap.add_argument("--summarize-counters", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"))
     ap.add_argument("--summarize-trace", metavar="KERNEL_TRACE_CSV")
+    ap.add_argument("--summarize-mfma", metavar="COUNTER_CSV")
     args = ap.parse_args()
     if args.summarize_counters:
         summarize_counters(*args.summarize_counters)
         return
     if args.summarize_trace:
         summarize_trace(args.summarize_trace)
+        return
+    if args.summarize_mfma:
+        summarize_mfma(args.summarize_mfma)
         return
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU only: the MALA operator is built and measured on a "
