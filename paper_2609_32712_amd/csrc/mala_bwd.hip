@@ -172,33 +172,37 @@ __device__ __forceinline__ void row_vectors(const BwdParams& p, long bhq, long q
 }
 
 template <int D>
-__global__ __launch_bounds__(512) void mala_bwd_dkdv_kernel(BwdParams p) {
-  constexpr int NT = 512;
+__global__ __launch_bounds__(1024) void mala_bwd_dkdv_kernel(BwdParams p) {
   constexpr int KS = D / 16;       // k-steps over head_dim
   constexpr int DB = D / 32;       // 32-wide column blocks
   constexpr int TILE = tile_elems<D>(kBq);          // one Q or dO tile in LDS
-  constexpr int NCH = kBq * D / 8;                  // 16-byte chunks of one query tile
-  static_assert(NCH <= NT, "one chunk per thread");
-  // rings of query tiles: tile t is read at iterations t and t + 1
-  __shared__ __attribute__((aligned(16))) bf16 Qs[3 * TILE];
-  __shared__ __attribute__((aligned(16))) bf16 dOs[3 * TILE];
+  constexpr int RC = D / 8 + 1;                     // 16-byte chunk positions per LDS row
+  constexpr int NI = (kBq * RC + 63) / 64;          // 64-chunk LDS-DMA loads per tile
+  constexpr int TS = NI * 64 * 8;                   // tile slot stride (elements)
+  static_assert(TS >= TILE, "slot holds the tile");
+  // rings of query tiles: Q_t is read at iterations t and t + 2, dO_t and the row
+  // vectors at iterations t + 1
+  __shared__ __attribute__((aligned(16))) bf16 Qs[4 * TS];
+  __shared__ __attribute__((aligned(16))) bf16 dOs[3 * TS];
   __shared__ __attribute__((aligned(16))) float rowv[3][3][kBq];   // lse2, threshold, D_q
-  // hand-off: P in fp32 as [buf][key wave][C registers 4g .. 4g+3][lane]
+  // hand-offs per key group: P in fp32 as [buf][group][C registers 4g .. 4g+3][lane];
+  // dS as the B operands [buf][group][hi0, hi1, lo0, lo1][lane]
   __shared__ __attribute__((aligned(16))) f32x4 Pf[2][4][4][64];
-  __shared__ int Pflag[2][4];
+  __shared__ __attribute__((aligned(16))) bf16x8 dSop[2][4][4][64];
+  __shared__ int Pflag[3][4];
 
-  // Two wavefronts per 32 keys [32 (w % 4), +32), on the same SIMD, in a pipeline:
-  //   producer (w >= 4), iteration t:    S_t = Q_t K^T, offline test, P_t -> LDS,
-  //                                      dV += dO_t^T P_t
-  //   consumer (w < 4),  iteration t+1:  dP_t = dO_t V^T, dS_t = P_t (dP_t - D),
-  //                                      dK += Q_t^T dS_t
-  // Each wavefront runs 24 MFMAs per retained tile; P travels through LDS in fp32,
-  // in the C layout that both wavefronts share.
+  // Sixteen wavefronts, four per 32 keys [32 g, +32) of the block (g = w % 4, so a
+  // key group's four wavefronts share one SIMD), in a pipeline over query tiles:
+  //   role 0, iteration t:  S_t = Q_t K^T, offline test, P_t (fp32) -> LDS
+  //   role 1, iteration t+1: dV^T += dO_t^T P_t (16 MFMAs)
+  //   role 2, iteration t+1: dP_t = dO_t V^T, dS_t = P_t (dP_t - D) -> LDS
+  //   role 3, iteration t+2: dK^T += Q_t^T dS_t (16 MFMAs)
+  // Each role runs its own loop (one barrier per iteration, the same count in all
+  // roles), so that the register allocation of one role carries no values of
+  // another: no wavefront needs more than 128 registers and four share a SIMD.
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const bool producer = wave >= 4;
-  const int kwave = wave & 3;
-  const int kw_local = kwave * kBk;
+  const int role = wave >> 2, grp_k = wave & 3;
   const int h = lane >> 5, c = lane & 31, G = lane >> 4, t16 = lane & 15;
   // lane bases of the LDS tile reads: operand rows (row c) and transposed rows
   const int rdo = rd_base<D>(c, h), tro = tr_base<D>(4 * h + (t16 >> 2), G & 1, t16);
@@ -208,23 +212,8 @@ __global__ __launch_bounds__(512) void mala_bwd_dkdv_kernel(BwdParams p) {
   const int b = bhk / p.Hkv, hkv = bhk % p.Hkv, grp = p.Hq / p.Hkv;
   const long off = (long)p.Nk - p.Nq;
   const int kb0 = kblk * kBwdKeys;
-  const int kw = kb0 + kw_local;           // first key of this wavefront's decision tile
+  const int kw = kb0 + grp_k * kBk;        // first key of this wavefront's decision tile
   const int key = kw + c;                  // this lane's key (C-layout column)
-
-  // producer: K rows (B operand of S = Q K^T); consumer: V rows (of dP = dO V^T)
-  bf16x8 kv[KS];
-  {
-    const bf16* src = (producer ? p.k : p.v) + (long)bhk * p.Nk * D;
-#pragma unroll
-    for (int kk = 0; kk < KS; ++kk)
-      kv[kk] = key < p.Nk ? load8(src + (long)key * D + 16 * kk + 8 * h) : zero8();
-  }
-
-  f32x16 acc[DB];    // producer: dV^T, consumer: dK^T (unscaled)
-#pragma unroll
-  for (int db = 0; db < DB; ++db)
-#pragma unroll
-    for (int r = 0; r < 16; ++r) acc[db][r] = 0.f;
 
   const long first_q = (long)kb0 - off;
   const int qi_start = first_q <= 0 ? 0 : (int)(first_q / kBq);
@@ -234,151 +223,213 @@ __global__ __launch_bounds__(512) void mala_bwd_dkdv_kernel(BwdParams p) {
 
   // Query tiles are swept from the last one down to the block's diagonal: the
   // offline test does not depend on the order, and co-resident workgroups of the
-  // same KV head (one per CU of an XCD) then read the same Q / dO tiles at about the
-  // same time, so those come from L2 instead of HBM.  The next tile is fetched into
-  // registers while the current one is processed; the arithmetic on the fetched
-  // row values waits until the store to LDS, so that no wavefront stalls on the
-  // loads inside the iteration.
+  // same KV head then read the same Q / dO tiles at about the same time, so those
+  // come from L2.  The dV wavefronts (role 1, which wait longest at the barrier)
+  // move them with buffer loads straight into LDS: the 64 lanes of one load fill
+  // 64 consecutive 16-byte positions of the tile's slot, each lane fetching the
+  // chunk that the LDS layout keeps there (row padding positions and the slack at
+  // the slot's end receive harmless data); the range check reads rows past the end
+  // of the sequence as zeros.  Loads for tile t + 1 are issued at the start of
+  // iteration t and waited for just before its closing barrier.
   auto tile_q0 = [&](int it) { return (nqt - 1 - it % per_head) * kBq; };
-  // tiles come through buffer loads: rows past the end of the sequence read as zeros
-  const uint32_t voff = (uint32_t)((tid / (D / 8)) * D + (tid % (D / 8)) * 8) * 2;
-  bf16x8 pq, pdo;
+  const bool mover = role == 1;
+  const int mt = tid & 255;                  // thread index within the moving role
+  const int mw = grp_k;                      // moving wavefront 0..3: loads mw, mw + 4, ...
+  constexpr int NJ = (NI + 3) / 4;           // loads per moving wavefront and tile
+  uint32_t dma_off[NJ];
+#pragma unroll
+  for (int u = 0; u < NJ; ++u) {
+    const int pos = 64 * (mw + 4 * u) + lane;          // chunk position in the slot
+    const int row = pos / RC, pc = pos % RC;
+    const int L = pc < D / 8 ? pc / (D / 32) + 4 * (pc % (D / 32)) : 0;   // logical chunk
+    dma_off[u] = (uint32_t)(row * D + 8 * L) * 2u;
+  }
   float plse = 0.f, pdv = 0.f, plg = 0.f;
   bool prow = false;
   auto fetch = [&](int it) {
     const long bhq = (long)b * p.Hq + hkv * grp + it / per_head;
     const int q0 = tile_q0(it);
     const long r0 = bhq * p.Nq + q0;
-    if (tid < kBq) {
+    if (mt < kBq) {
       const uint32_t nr = (uint32_t)(p.Nq - q0) * 4u;
-      plse = buf_load1(make_rsrc(p.lse + r0, nr), tid * 4u);
-      pdv = buf_load1(make_rsrc(p.dvec + r0, nr), tid * 4u);
-      prow = q0 + tid < p.Nq;
-      plg = log2f((float)((long)q0 + tid + 1 + off));
+      plse = buf_load1(make_rsrc(p.lse + r0, nr), mt * 4u);
+      pdv = buf_load1(make_rsrc(p.dvec + r0, nr), mt * 4u);
+      prow = q0 + mt < p.Nq;
+      plg = log2f((float)((long)q0 + mt + 1 + off));
     }
-    if (tid < NCH) {
-      const uint32_t nb = (uint32_t)(p.Nq - q0) * (uint32_t)D * 2u;
-      pq = buf_load8(make_rsrc(p.q + r0 * D, nb), voff);
-      pdo = buf_load8(make_rsrc(p.dout + r0 * D, nb), voff);
+    const uint32_t nb = (uint32_t)(p.Nq - q0) * (uint32_t)D * 2u;
+    const auto rq = make_rsrc(p.q + r0 * D, nb), ro = make_rsrc(p.dout + r0 * D, nb);
+#pragma unroll
+    for (int u = 0; u < NJ; ++u) {
+      const int j = mw + 4 * u;
+      if (j < NI) {
+        buf_load_lds16(rq, dma_off[u], Qs + (it & 3) * TS + 512 * j);
+        buf_load_lds16(ro, dma_off[u], dOs + (it % 3) * TS + 512 * j);
+      }
     }
   };
   auto stash = [&](int it) {
-    if (tid < NCH) {
-      const int row = tid / (D / 8), col = (tid % (D / 8)) * 8;
-      store8(Qs + (it % 3) * TILE + tile_off<D>(row, col), pq);
-      store8(dOs + (it % 3) * TILE + tile_off<D>(row, col), pdo);
-    }
-    if (tid < kBq) {
+    if (mt < kBq) {
       // the same arithmetic as row_vectors (the query-major kernel must agree bitwise)
 #pragma clang fp contract(off)
       const float l2 = plse * kLog2e;
-      rowv[it % 3][0][tid] = prow ? l2 : 0.f;
-      rowv[it % 3][1][tid] = prow ? l2 + p.log2tau - plg : __builtin_huge_valf();
-      rowv[it % 3][2][tid] = prow ? pdv : 0.f;
+      rowv[it % 3][0][mt] = prow ? l2 : 0.f;
+      rowv[it % 3][1][mt] = prow ? l2 + p.log2tau - plg : __builtin_huge_valf();
+      rowv[it % 3][2][mt] = prow ? pdv : 0.f;
     }
+    wait_vm();
   };
+  // the iteration's end: stage the next tile, then the barrier (every role passes
+  // the same number of barriers)
+  auto iteration_end = [&](int) { __syncthreads(); };
 
-  fetch(0);
-  stash(0);
-  __syncthreads();
-
-  for (int it = 0; it <= total; ++it) {
-    if (it + 1 < total) fetch(it + 1);
-    // each role prepares the B operands (hi, lo per k-step) and the transposed A tile
-    // of its accumulator update; the update itself is one piece of code for both
-    // roles, so that the accumulator stays in the same registers
-    bool upd = false;
-    bf16x8 bh0, bh1, bl0, bl1;
-    const bf16* atb = nullptr;
-    if (producer) {
-      if (it < total) {
-        // tile it: score discovery, test, P; then dV^T += dO^T P
-        const int q0 = tile_q0(it);
-        const int slot = it % 3;
-        const float* rv = &rowv[slot][0][0];
-        // the tile decision and P are the critical path of the pipeline: raise this
-        // wavefront's issue priority over its partner's MFMAs until P is out
-        __builtin_amdgcn_s_setprio(3);
-        bf16x8 qa[KS];
-        const bf16* qr = lds_pin(Qs + slot * TILE + rdo);
-#pragma unroll
-        for (int kk = 0; kk < KS; ++kk) qa[kk] = load8(qr + rd_step<D>(kk));
-        const f32x16 sc = qk_tile<KS>(qa, kv);
-        // tiles that cross the diagonal or the end of the sequence (or whose keys all
-        // lie beyond this tile's rows) take the masked test
-        const bool need_mask =
-            ((long)kw + kBk - 1 > (long)q0 + off) || (q0 + kBq > p.Nq) || (kw + kBk > p.Nk);
-        const int klo = key < p.Nk ? (int)((long)key - off - q0) - 4 * h : 1000000;
-        float sv[16];
-        const bool dem =
-            offline_entries(sc, p.scale2, need_mask, klo, p.Nq - q0 - 4 * h, rv + kBq, h, sv);
-        const bool ret = wave_any(dem);
-        if (ret) {
-          probabilities(sv, p.scale2, rv, h);
-#pragma unroll
-          for (int g = 0; g < 4; ++g)
-            Pf[it & 1][kwave][g][lane] = f32x4{sv[4 * g], sv[4 * g + 1], sv[4 * g + 2], sv[4 * g + 3]};
-          split_bf16x8(sv, bh0, bl0);
-          split_bf16x8(sv + 8, bh1, bl1);
-          atb = dOs + slot * TILE + tro;
-          upd = true;
-        }
-        if (lane == 0) Pflag[it & 1][kwave] = ret ? 1 : 0;
-        __builtin_amdgcn_s_setprio(0);
-      }
-    } else if (it >= 1 && Pflag[(it - 1) & 1][kwave]) {
-      // consumer, tile t = it - 1: dP = dO V^T; dS = P (dP - D); then dK^T += Q^T dS
-      const int t = it - 1;
-      const int slot = t % 3;
-      const float* rv = &rowv[slot][0][0];
-      bf16x8 oa[KS];
-      const bf16* orr = lds_pin(dOs + slot * TILE + rdo);
-#pragma unroll
-      for (int kk = 0; kk < KS; ++kk) oa[kk] = load8(orr + rd_step<D>(kk));
-      const f32x16 dp = qk_tile<KS>(oa, kv);
-      float ds[16];
-#pragma unroll
-      for (int g = 0; g < 4; ++g) {
-        const f32x4 p4 = Pf[t & 1][kwave][g][lane];
-        const f32x4 d4 = *reinterpret_cast<const f32x4*>(rv + 2 * kBq + 8 * g + 4 * h);
-#pragma unroll
-        for (int e = 0; e < 4; ++e) ds[4 * g + e] = p4[e] * (dp[4 * g + e] - d4[e]);
-      }
-      split_bf16x8(ds, bh0, bl0);
-      split_bf16x8(ds + 8, bh1, bl1);
-      atb = Qs + slot * TILE + tro;
-      upd = true;
-    }
-    if (upd) {
-      const bf16* ab = lds_pin(atb);
-#pragma unroll
-      for (int db = 0; db < DB; ++db) {
-#pragma unroll
-        for (int ks = 0; ks < 2; ++ks) {
-          const bf16* at = ab + 16 * ks * (D + 8) + tr_step<D>(db);
-          const bf16x8 a = cat(lds_read_tr(at), lds_read_tr(at + 8 * (D + 8)));
-          acc[db] = mfma32(a, ks ? bh1 : bh0, acc[db]);
-          acc[db] = mfma32(a, ks ? bl1 : bl0, acc[db]);
-        }
-      }
-    }
-    if (it + 1 < total) stash(it + 1);
-    __syncthreads();
+  if (mover) {
+    fetch(0);
+    stash(0);
   }
+  __syncthreads();
+  (void)mover;
 
-  // dV = sum P^T dO (producers), dK = scale * sum dS^T Q (consumers); lane (h, c)
-  // holds key kw + c
-  if (key < p.Nk) {
-    const float f = producer ? 1.f : p.scale;
-    float* dst = (producer ? p.dv : p.dk) + ((long)bhk * p.Nk + key) * D;
+  const int n_it = total + 2;
+  if (role == 0 || role == 2) {
+    // K rows (role 0, B operand of S = Q K^T) or V rows (role 2, of dP = dO V^T)
+    bf16x8 kv[KS];
+    {
+      const bf16* src = (role == 0 ? p.k : p.v) + (long)bhk * p.Nk * D;
+#pragma unroll
+      for (int kk = 0; kk < KS; ++kk)
+        kv[kk] = key < p.Nk ? load8(src + (long)key * D + 16 * kk + 8 * h) : zero8();
+    }
+    if (role == 0) {
+      for (int it = 0; it < n_it; ++it) {
+        if (it < total) {
+          // tile it: score discovery, offline test, P
+          const int q0 = tile_q0(it);
+          const float* rv = &rowv[it % 3][0][0];
+          bf16x8 qa[KS];
+          const bf16* qr = lds_pin(Qs + (it & 3) * TS + rdo);
+#pragma unroll
+          for (int kk = 0; kk < KS; ++kk) qa[kk] = load8(qr + rd_step<D>(kk));
+          const f32x16 sc = qk_tile<KS>(qa, kv);
+          // tiles that cross the diagonal or the end of the sequence (or whose keys
+          // all lie beyond this tile's rows) take the masked test
+          const bool need_mask =
+              ((long)kw + kBk - 1 > (long)q0 + off) || (q0 + kBq > p.Nq) || (kw + kBk > p.Nk);
+          const int klo = key < p.Nk ? (int)((long)key - off - q0) - 4 * h : 1000000;
+          float sv[16];
+          const bool dem =
+              offline_entries(sc, p.scale2, need_mask, klo, p.Nq - q0 - 4 * h, rv + kBq, h, sv);
+          const bool ret = wave_any(dem);
+          if (ret) {
+            probabilities(sv, p.scale2, rv, h);
+#pragma unroll
+            for (int g = 0; g < 4; ++g)
+              Pf[it & 1][grp_k][g][lane] =
+                  f32x4{sv[4 * g], sv[4 * g + 1], sv[4 * g + 2], sv[4 * g + 3]};
+          }
+          if (lane == 0) Pflag[it % 3][grp_k] = ret ? 1 : 0;
+        }
+        iteration_end(it);
+      }
+    } else {
+      for (int it = 0; it < n_it; ++it) {
+        const int t = it - 1;
+        if (t >= 0 && t < total && Pflag[t % 3][grp_k]) {
+          // tile t: dP = dO V^T; dS = P (dP - D) -> LDS as hi / lo B operands
+          const float* rv = &rowv[t % 3][0][0];
+          bf16x8 oa[KS];
+          const bf16* orr = lds_pin(dOs + (t % 3) * TS + rdo);
+#pragma unroll
+          for (int kk = 0; kk < KS; ++kk) oa[kk] = load8(orr + rd_step<D>(kk));
+          const f32x16 dp = qk_tile<KS>(oa, kv);
+          float ds[16];
+#pragma unroll
+          for (int g = 0; g < 4; ++g) {
+            const f32x4 p4 = Pf[t & 1][grp_k][g][lane];
+            const f32x4 d4 = *reinterpret_cast<const f32x4*>(rv + 2 * kBq + 8 * g + 4 * h);
+#pragma unroll
+            for (int e = 0; e < 4; ++e) ds[4 * g + e] = p4[e] * (dp[4 * g + e] - d4[e]);
+          }
+          bf16x8 xh[2], xl[2];
+          split_bf16x8(ds, xh[0], xl[0]);
+          split_bf16x8(ds + 8, xh[1], xl[1]);
+          dSop[t & 1][grp_k][0][lane] = xh[0];
+          dSop[t & 1][grp_k][1][lane] = xh[1];
+          dSop[t & 1][grp_k][2][lane] = xl[0];
+          dSop[t & 1][grp_k][3][lane] = xl[1];
+        }
+        iteration_end(it);
+      }
+    }
+  } else {
+    // roles 1 (dV^T += dO^T P, one tile behind) and 3 (dK^T += Q^T dS, two behind)
+    f32x16 acc[DB];
 #pragma unroll
     for (int db = 0; db < DB; ++db)
 #pragma unroll
-      for (int g = 0; g < 4; ++g) {
-        f32x4 v4 = {acc[db][4 * g] * f, acc[db][4 * g + 1] * f, acc[db][4 * g + 2] * f,
-                    acc[db][4 * g + 3] * f};
-        *reinterpret_cast<f32x4*>(dst + 32 * db + 8 * g + 4 * h) = v4;
+      for (int r = 0; r < 16; ++r) acc[db][r] = 0.f;
+    const int lag = role == 1 ? 1 : 2;
+    // the decision of tile it - 2 is known since the end of iteration it - 2: role
+    // 3 reads it one iteration early, off its critical path
+    int fl3 = 0;
+    for (int it = 0; it < n_it; ++it) {
+      if (role == 1 && it + 1 < total) fetch(it + 1);
+      const int t = it - lag;
+      const bool fl = role == 1 ? (t >= 0 && t < total && Pflag[t % 3][grp_k]) : fl3 != 0;
+      if (fl) {
+        bf16x8 bh0, bh1, bl0, bl1;
+        const bf16* atb;
+        if (role == 1) {
+          float pv[16];
+#pragma unroll
+          for (int g = 0; g < 4; ++g) {
+            const f32x4 p4 = Pf[t & 1][grp_k][g][lane];
+#pragma unroll
+            for (int e = 0; e < 4; ++e) pv[4 * g + e] = p4[e];
+          }
+          split_bf16x8(pv, bh0, bl0);
+          split_bf16x8(pv + 8, bh1, bl1);
+          atb = dOs + (t % 3) * TS + tro;
+        } else {
+          bh0 = dSop[t & 1][grp_k][0][lane];
+          bh1 = dSop[t & 1][grp_k][1][lane];
+          bl0 = dSop[t & 1][grp_k][2][lane];
+          bl1 = dSop[t & 1][grp_k][3][lane];
+          atb = Qs + (t & 3) * TS + tro;
+        }
+        const bf16* ab = lds_pin(atb);
+#pragma unroll
+        for (int db = 0; db < DB; ++db) {
+#pragma unroll
+          for (int ks = 0; ks < 2; ++ks) {
+            const bf16* at = ab + 16 * ks * (D + 8) + tr_step<D>(db);
+            const bf16x8 a = cat(lds_read_tr(at), lds_read_tr(at + 8 * (D + 8)));
+            acc[db] = mfma32(a, ks ? bh1 : bh0, acc[db]);
+            acc[db] = mfma32(a, ks ? bl1 : bl0, acc[db]);
+          }
+        }
       }
+      if (role == 3) {
+        const int tn = it - 1;   // the tile of the next iteration
+        fl3 = (tn >= 0 && tn < total) ? Pflag[tn % 3][grp_k] : 0;
+      }
+      if (role == 1 && it + 1 < total) stash(it + 1);
+      __syncthreads();
+    }
+    // dV = sum P^T dO (role 1), dK = scale * sum dS^T Q (role 3); lane (h, c)
+    // holds key kw + c
+    if (key < p.Nk) {
+      const float f = role == 1 ? 1.f : p.scale;
+      float* dst = (role == 1 ? p.dv : p.dk) + ((long)bhk * p.Nk + key) * D;
+#pragma unroll
+      for (int db = 0; db < DB; ++db)
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+          f32x4 v4 = {acc[db][4 * g] * f, acc[db][4 * g + 1] * f, acc[db][4 * g + 2] * f,
+                      acc[db][4 * g + 3] * f};
+          *reinterpret_cast<f32x4*>(dst + 32 * db + 8 * g + 4 * h) = v4;
+        }
+    }
   }
   if (p.counters && tid == 0) atomicAdd(&p.counters[2], (unsigned long long)total);
 }
@@ -570,7 +621,7 @@ __global__ __launch_bounds__(kFwdWaves * 64) void mala_bwd_dq_kernel(BwdParams p
 }
 
 hipError_t launch_bwd(const BwdParams& p, int D, hipStream_t st) {
-  dim3 grid_kv((unsigned)p.nkblk * p.B * p.Hkv), block_kv(512);
+  dim3 grid_kv((unsigned)p.nkblk * p.B * p.Hkv), block_kv(1024);
   dim3 grid_q((unsigned)((p.Nq + kFwdRows - 1) / kFwdRows) * p.B * p.Hq), block_q(kFwdWaves * 64);
   if (D == 128) {
     hipLaunchKernelGGL(mala_bwd_dkdv_kernel<128>, grid_kv, block_kv, 0, st, p);

@@ -133,6 +133,16 @@ __device__ __forceinline__ float buf_load1(__amdgpu_buffer_rsrc_t r, uint32_t by
   return __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(r, byte_off, 0, 0));
 }
 
+// Buffer load straight into LDS (buffer_load_dwordx4 ... lds): lane i's 16 bytes
+// land at lds_base + 16 i (lds_base uniform over the wavefront; checked by a
+// lane-layout probe on gfx950).  Completion is counted by vmcnt.
+__device__ __forceinline__ void buf_load_lds16(__amdgpu_buffer_rsrc_t r, uint32_t byte_off,
+                                               bf16* lds_base) {
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (__attribute__((address_space(3))) void*)lds_base,
+                                           16, byte_off, 0, 0, 0);
+}
+__device__ __forceinline__ void wait_vm() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
+
 // Hardware base-2 exponential / logarithm (v_exp_f32 / v_log_f32, ~1 ulp on normal
 // results).  The softmax arguments are <= 0, so the results lie in [0, 1]; values
 // below 2^-126 may flush to zero, which no tolerance here can see.
