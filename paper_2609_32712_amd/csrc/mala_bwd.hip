@@ -542,8 +542,11 @@ __global__ __launch_bounds__(kFwdWaves * 64) void mala_bwd_dq_kernel(BwdParams p
     const bf16* kr = lds_pin(Kb + rdo);
     const bf16* vr = lds_pin(Vb + rdo);
     const bf16* ktb = lds_pin(Kb + tro);
+    // the two wavefronts of a SIMD keep pace: the one with more of the stage left
+    // issues first (priority 2, then 1 for the second tile, 0 at the barrier)
 #pragma unroll 1
     for (int sub = 1; sub >= 0; --sub) {
+      if (sub) __builtin_amdgcn_s_setprio(2); else __builtin_amdgcn_s_setprio(1);
       const int j = 2 * t + sub;
       if (j > jdiag) continue;
       const long kb = (long)j * kBk;
@@ -598,6 +601,7 @@ __global__ __launch_bounds__(kFwdWaves * 64) void mala_bwd_dq_kernel(BwdParams p
       }
       wave_lds_sync();   // the planes are rewritten by the next retained tile
     }
+    __builtin_amdgcn_s_setprio(0);
     if (t > 0) stash(buf ^ 1);
     __syncthreads();
   }
