@@ -447,11 +447,9 @@ __device__ __forceinline__ int ds_chunk(int r, int j) {
 
 template <int D>
 __global__ __launch_bounds__(kFwdWaves * 64) void mala_bwd_dq_kernel(BwdParams p) {
-  constexpr int NT = kFwdWaves * 64;
   constexpr int KS = D / 16;
   constexpr int DB = D / 32;
   constexpr int STAGE = tile_elems<D>(kFwdStage);
-  constexpr int CPT = kFwdStage * D / 8 / NT;
   constexpr int DSP = kBk * kBq;             // one dS plane [key][query position]
   constexpr int DSW = 2 * DSP;               // one wavefront's dS planes (hi, lo)
   __shared__ __attribute__((aligned(16))) bf16 Ks[2 * STAGE];
@@ -459,7 +457,8 @@ __global__ __launch_bounds__(kFwdWaves * 64) void mala_bwd_dq_kernel(BwdParams p
   __shared__ __attribute__((aligned(16))) bf16 dSw[kFwdWaves * DSW];
   __shared__ __attribute__((aligned(16))) float rowv[kFwdWaves][3][kBq];
 
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int h = lane >> 5, c = lane & 31, G = lane >> 4, t16 = lane & 15;
   // lane bases of the LDS tile reads: operand rows (row c) and transposed rows
   const int rdo = rd_base<D>(c, h), tro = tr_base<D>(4 * h + (t16 >> 2), G & 1, t16);
@@ -506,37 +505,35 @@ __global__ __launch_bounds__(kFwdWaves * 64) void mala_bwd_dq_kernel(BwdParams p
   const int dsr0 = 8 * ds_chunk(4 * h + (t16 >> 2), dsj) + 4 * (t16 & 1);
   const int dsr1 = 8 * ds_chunk(8 + 4 * h + (t16 >> 2), dsj) + 4 * (t16 & 1);
 
-  // K / V stages come through buffer loads: keys past the end read as zeros
-  bf16x8 pk[CPT], pv[CPT];
-  auto fetch = [&](int t) {
+  // K / V stages move with buffer loads straight into LDS (keys past the end read
+  // as zeros): wavefront w issues the 64-position loads w, w + 8, ... of each slot
+  constexpr int NIS = STAGE / 512;           // 64-position loads per stage slot
+  static_assert(NIS * 512 == STAGE, "whole loads per slot");
+  constexpr int NJS = (NIS + kFwdWaves - 1) / kFwdWaves;
+  uint32_t dma_off[NJS];
+#pragma unroll
+  for (int u = 0; u < NJS; ++u) dma_off[u] = dma_lane_offset<D>(64 * (wave + kFwdWaves * u) + lane);
+  auto fetch = [&](int t, int buf) {
     const long k0 = (long)t * kFwdStage;
     const uint32_t nb = (uint32_t)(p.Nk - k0) * (uint32_t)D * 2u;
     const auto rk = make_rsrc(Kp + k0 * D, nb), rvv = make_rsrc(Vp + k0 * D, nb);
 #pragma unroll
-    for (int e = 0; e < CPT; ++e) {
-      const int ch = tid + NT * e;
-      const uint32_t off_b = (uint32_t)((ch / (D / 8)) * D + (ch % (D / 8)) * 8) * 2u;
-      pk[e] = buf_load8(rk, off_b);
-      pv[e] = buf_load8(rvv, off_b);
-    }
-  };
-  auto stash = [&](int buf) {
-#pragma unroll
-    for (int e = 0; e < CPT; ++e) {
-      const int ch = tid + NT * e;
-      const int row = ch / (D / 8), col = (ch % (D / 8)) * 8;
-      store8(Ks + buf * STAGE + tile_off<D>(row, col), pk[e]);
-      store8(Vs + buf * STAGE + tile_off<D>(row, col), pv[e]);
+    for (int u = 0; u < NJS; ++u) {
+      const int j = wave + kFwdWaves * u;
+      if (j < NIS) {
+        buf_load_lds16(rk, dma_off[u], Ks + buf * STAGE + 512 * j);
+        buf_load_lds16(rvv, dma_off[u], Vs + buf * STAGE + 512 * j);
+      }
     }
   };
 
-  fetch(ttop);
-  stash(0);
+  fetch(ttop, 0);
+  wait_vm();
   __syncthreads();
 
   for (int t = ttop; t >= 0; --t) {
     const int buf = (ttop - t) & 1;
-    if (t > 0) fetch(t - 1);
+    if (t > 0) fetch(t - 1, buf ^ 1);
     const bf16* Kb = Ks + buf * STAGE;
     const bf16* Vb = Vs + buf * STAGE;
     const bf16* kr = lds_pin(Kb + rdo);
@@ -602,7 +599,7 @@ __global__ __launch_bounds__(kFwdWaves * 64) void mala_bwd_dq_kernel(BwdParams p
       wave_lds_sync();   // the planes are rewritten by the next retained tile
     }
     __builtin_amdgcn_s_setprio(0);
-    if (t > 0) stash(buf ^ 1);
+    wait_vm();
     __syncthreads();
   }
 

@@ -141,6 +141,17 @@ __device__ __forceinline__ void buf_load_lds16(__amdgpu_buffer_rsrc_t r, uint32_
   __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (__attribute__((address_space(3))) void*)lds_base,
                                            16, byte_off, 0, 0, 0);
 }
+// Byte offset, within a row-major [*][D] bf16 matrix, of the chunk that an
+// LDS-DMA lane must fetch so that chunk position pos of a tile slot laid out by
+// tile_off holds the right data: rows of D/8 + 1 positions, position
+// (D/32)(L % 4) + L / 4 holding logical chunk L; the padding position takes chunk 0.
+template <int D>
+__device__ __forceinline__ uint32_t dma_lane_offset(int pos) {
+  constexpr int RC = D / 8 + 1;
+  const int row = pos / RC, pc = pos % RC;
+  const int L = pc < D / 8 ? pc / (D / 32) + 4 * (pc % (D / 32)) : 0;
+  return (uint32_t)(row * D + 8 * L) * 2u;
+}
 __device__ __forceinline__ void wait_vm() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
 
 // Hardware base-2 exponential / logarithm (v_exp_f32 / v_log_f32, ~1 ulp on normal

@@ -40,7 +40,8 @@ __global__ __launch_bounds__(kFwdWaves * 64) void mala_fwd_kernel(FwdParams p) {
   __shared__ __attribute__((aligned(16))) bf16 Ks[2 * STAGE];
   __shared__ __attribute__((aligned(16))) bf16 Vs[2 * STAGE];
 
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int h = lane >> 5, c = lane & 31, G = lane >> 4, t16 = lane & 15;
   // lane bases of the LDS tile reads: operand rows (row c) and transposed rows
   const int rdo = rd_base<D>(c, h), tro = tr_base<D>(4 * h + (t16 >> 2), G & 1, t16);
