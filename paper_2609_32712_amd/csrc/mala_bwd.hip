@@ -189,7 +189,8 @@ __global__ __launch_bounds__(1024) void mala_bwd_dkdv_kernel(BwdParams p) {
   // dS as the B operands [buf][group][hi0, hi1, lo0, lo1][lane]
   __shared__ __attribute__((aligned(16))) f32x4 Pf[2][4][4][64];
   __shared__ __attribute__((aligned(16))) bf16x8 dSop[2][4][4][64];
-  __shared__ int Pflag[3][4];
+  __shared__ int Pflag[3][4];    // 0 skipped, 1 retained, 3 retained with P's lo term
+  __shared__ int dSlo[2][4];     // dS of the tile needs its lo term
 
   // Sixteen wavefronts, four per 32 keys [32 g, +32) of the block (g = w % 4, so a
   // key group's four wavefronts share one SIMD), in a pipeline over query tiles:
@@ -301,6 +302,7 @@ __global__ __launch_bounds__(1024) void mala_bwd_dkdv_kernel(BwdParams p) {
         kv[kk] = key < p.Nk ? load8(src + (long)key * D + 16 * kk + 8 * h) : zero8();
     }
     if (role == 0) {
+      float fdv = 0.f;   // P mass of this lane's key in tiles run without the lo term
       for (int it = 0; it < n_it; ++it) {
         if (it < total) {
           // tile it: score discovery, offline test, P
@@ -320,18 +322,28 @@ __global__ __launch_bounds__(1024) void mala_bwd_dkdv_kernel(BwdParams p) {
           const bool dem =
               offline_entries(sc, p.scale2, need_mask, klo, p.Nq - q0 - 4 * h, rv + kBq, h, sv);
           const bool ret = wave_any(dem);
+          bool with_lo = false;
           if (ret) {
             probabilities(sv, p.scale2, rv, h);
 #pragma unroll
             for (int g = 0; g < 4; ++g)
               Pf[it & 1][grp_k][g][lane] =
                   f32x4{sv[4 * g], sv[4 * g + 1], sv[4 * g + 2], sv[4 * g + 3]};
+            // dV runs this tile without P's lo term while the key's P mass in such
+            // tiles stays within kLoMassDv (for every key of the tile)
+            float ps = 0.f;
+#pragma unroll
+            for (int r = 0; r < 16; ++r) ps += sv[r];
+            const float fv_new = fdv + halves_sum(ps);
+            with_lo = wave_any(fv_new > kLoMassDv);
+            if (!with_lo) fdv = fv_new;
           }
-          if (lane == 0) Pflag[it % 3][grp_k] = ret ? 1 : 0;
+          if (lane == 0) Pflag[it % 3][grp_k] = ret ? (with_lo ? 3 : 1) : 0;
         }
         iteration_end(it);
       }
     } else {
+      float fdk = 0.f;   // sum of |dS| of this lane's key in tiles run without the lo term
       for (int it = 0; it < n_it; ++it) {
         const int t = it - 1;
         if (t >= 0 && t < total && Pflag[t % 3][grp_k]) {
@@ -350,13 +362,27 @@ __global__ __launch_bounds__(1024) void mala_bwd_dkdv_kernel(BwdParams p) {
 #pragma unroll
             for (int e = 0; e < 4; ++e) ds[4 * g + e] = p4[e] * (dp[4 * g + e] - d4[e]);
           }
+          // dK runs this tile without dS's lo term while the key's sum of |dS| in
+          // such tiles stays within kLoMassDk (for every key of the tile)
+          float as = 0.f;
+#pragma unroll
+          for (int r = 0; r < 16; ++r) as += fabsf(ds[r]);
+          const float fk_new = fdk + halves_sum(as);
+          const bool with_lo = wave_any(fk_new > kLoMassDk);
+          if (!with_lo) fdk = fk_new;
           bf16x8 xh[2], xl[2];
-          split_bf16x8(ds, xh[0], xl[0]);
-          split_bf16x8(ds + 8, xh[1], xl[1]);
+          if (with_lo) {
+            split_bf16x8(ds, xh[0], xl[0]);
+            split_bf16x8(ds + 8, xh[1], xl[1]);
+            dSop[t & 1][grp_k][2][lane] = xl[0];
+            dSop[t & 1][grp_k][3][lane] = xl[1];
+          } else {
+            xh[0] = hi_bf16x8(ds);
+            xh[1] = hi_bf16x8(ds + 8);
+          }
           dSop[t & 1][grp_k][0][lane] = xh[0];
           dSop[t & 1][grp_k][1][lane] = xh[1];
-          dSop[t & 1][grp_k][2][lane] = xl[0];
-          dSop[t & 1][grp_k][3][lane] = xl[1];
+          if (lane == 0) dSlo[t & 1][grp_k] = with_lo ? 1 : 0;
         }
         iteration_end(it);
       }
@@ -375,8 +401,9 @@ __global__ __launch_bounds__(1024) void mala_bwd_dkdv_kernel(BwdParams p) {
     for (int it = 0; it < n_it; ++it) {
       if (role == 1 && it + 1 < total) fetch(it + 1);
       const int t = it - lag;
-      const bool fl = role == 1 ? (t >= 0 && t < total && Pflag[t % 3][grp_k]) : fl3 != 0;
-      if (fl) {
+      const int pf = role == 1 ? ((t >= 0 && t < total) ? Pflag[t % 3][grp_k] : 0) : fl3;
+      if (pf) {
+        const bool with_lo = role == 1 ? (pf & 2) != 0 : dSlo[t & 1][grp_k] != 0;
         bf16x8 bh0, bh1, bl0, bl1;
         const bf16* atb;
         if (role == 1) {
@@ -405,7 +432,7 @@ __global__ __launch_bounds__(1024) void mala_bwd_dkdv_kernel(BwdParams p) {
             const bf16* at = ab + 16 * ks * (D + 8) + tr_step<D>(db);
             const bf16x8 a = cat(lds_read_tr(at), lds_read_tr(at + 8 * (D + 8)));
             acc[db] = mfma32(a, ks ? bh1 : bh0, acc[db]);
-            acc[db] = mfma32(a, ks ? bl1 : bl0, acc[db]);
+            if (with_lo) acc[db] = mfma32(a, ks ? bl1 : bl0, acc[db]);
           }
         }
       }

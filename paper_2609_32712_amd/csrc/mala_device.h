@@ -203,4 +203,16 @@ __device__ __forceinline__ void split_bf16x8(const float* x, bf16x8& hi, bf16x8&
   }
 }
 
+// The high bf16 terms only (see split_bf16x8).
+__device__ __forceinline__ bf16x8 hi_bf16x8(const float* x) {
+  bf16x8 hi;
+#pragma unroll
+  for (int i = 0; i < 8; i += 2) {
+    const bf16x2 h2 = __builtin_convertvector((f32x2{x[i], x[i + 1]}), bf16x2);
+    hi[i] = h2[0];
+    hi[i + 1] = h2[1];
+  }
+  return hi;
+}
+
 }  // namespace mala

@@ -34,6 +34,7 @@ def assert_close(name, got, ref, where=None):
     assert np.isfinite(got).all(), "%s: non-finite values" % name
     err = np.abs(got - ref)
     mx, mean = float(err.max()), float(err.mean())
+    print("[parity] %-12s max-abs %.3e mean-abs %.3e" % (name, mx, mean), flush=True)
     assert mx <= TOL_MAX and mean <= TOL_MEAN, "%s: max-abs %.3e mean-abs %.3e" % (name, mx, mean)
     return mx, mean
 
