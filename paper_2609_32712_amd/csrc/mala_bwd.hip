@@ -222,17 +222,18 @@ __global__ __launch_bounds__(1024) void mala_bwd_dkdv_kernel(BwdParams p) {
   const int per_head = nqt - qi_start;     // >= 1: key kb0 < Nk is visible to row Nq - 1
   const int total = grp * per_head;
 
-  // Query tiles are swept from the last one down to the block's diagonal: the
-  // offline test does not depend on the order, and co-resident workgroups of the
-  // same KV head then read the same Q / dO tiles at about the same time, so those
-  // come from L2.  The dV wavefronts (role 1, which wait longest at the barrier)
+  // Query tiles are swept from the last one down to the block's diagonal, the
+  // heads of the group innermost (iteration it: tile nqt - 1 - it / grp, head
+  // it % grp): the offline test does not depend on the order, and all co-resident
+  // workgroups of the same KV head then step through the same Q / dO tiles in
+  // lockstep, so that one fetch from HBM serves the whole XCD through its L2.  The dV wavefronts (role 1, which wait longest at the barrier)
   // move them with buffer loads straight into LDS: the 64 lanes of one load fill
   // 64 consecutive 16-byte positions of the tile's slot, each lane fetching the
   // chunk that the LDS layout keeps there (row padding positions and the slack at
   // the slot's end receive harmless data); the range check reads rows past the end
   // of the sequence as zeros.  Loads for tile t + 1 are issued at the start of
   // iteration t and waited for just before its closing barrier.
-  auto tile_q0 = [&](int it) { return (nqt - 1 - it % per_head) * kBq; };
+  auto tile_q0 = [&](int it) { return (nqt - 1 - it / grp) * kBq; };
   const bool mover = role == 1;
   const int mt = tid & 255;                  // thread index within the moving role
   const int mw = grp_k;                      // moving wavefront 0..3: loads mw, mw + 4, ...
@@ -248,7 +249,7 @@ __global__ __launch_bounds__(1024) void mala_bwd_dkdv_kernel(BwdParams p) {
   float plse = 0.f, pdv = 0.f, plg = 0.f;
   bool prow = false;
   auto fetch = [&](int it) {
-    const long bhq = (long)b * p.Hq + hkv * grp + it / per_head;
+    const long bhq = (long)b * p.Hq + hkv * grp + it % grp;
     const int q0 = tile_q0(it);
     const long r0 = bhq * p.Nq + q0;
     if (mt < kBq) {
@@ -523,6 +524,7 @@ __global__ __launch_bounds__(kFwdWaves * 64) void mala_bwd_dq_kernel(BwdParams p
   const int ttop = (int)((qlast_g + off) / kFwdStage);
   unsigned n_legal = 0, n_ret = 0;
   int cnt_row = 0;   // retained tiles in which row q0w + c has a legal key
+  float fdq = 0.f;   // sum of this lane's largest |dS| in tiles run without the lo term
   bf16* const dSh = dSw + wave * DSW;
   bf16* const dSl = dSh + DSP;
   // dS plane offsets: this lane's two chunk writes (key c, chunks h and 2 + h) and
@@ -601,26 +603,42 @@ __global__ __launch_bounds__(kFwdWaves * 64) void mala_bwd_dq_kernel(BwdParams p
 #pragma unroll
         for (int e = 0; e < 4; ++e) dsv[4 * g + e] = sv[4 * g + e] * (dp[4 * g + e] - d4[e]);
       }
+      // dQ runs this tile without dS's lo term while, for every lane, the sum over
+      // such tiles of the lane's largest |dS| stays within kLoMassDq / 32: a query
+      // row's 32 keys of a tile sit in 32 lanes, so its sum of |dS| over those
+      // tiles stays within kLoMassDq
+      float mx = 0.f;
+#pragma unroll
+      for (int r = 0; r < 16; ++r) mx = fmaxf(mx, fabsf(dsv[r]));
+      const float fq_new = fdq + mx;
+      const bool with_lo = wave_any(fq_new > kLoMassDq * (1.f / kBk));
+      if (!with_lo) fdq = fq_new;
       bf16x8 dh[2], dl[2];
-      split_bf16x8(dsv, dh[0], dl[0]);
-      split_bf16x8(dsv + 8, dh[1], dl[1]);
       // dS^T -> this wavefront's LDS planes as [key][query position]
+      if (with_lo) {
+        split_bf16x8(dsv, dh[0], dl[0]);
+        split_bf16x8(dsv + 8, dh[1], dl[1]);
+        store8(dSl + dsw0, dl[0]);
+        store8(dSl + dsw1, dl[1]);
+      } else {
+        dh[0] = hi_bf16x8(dsv);
+        dh[1] = hi_bf16x8(dsv + 8);
+      }
       store8(dSh + dsw0, dh[0]);
       store8(dSh + dsw1, dh[1]);
-      store8(dSl + dsw0, dl[0]);
-      store8(dSl + dsw1, dl[1]);
       wave_lds_sync();
       // dQ[q][d] += dS[q][key] K[key][d]; MFMA row m holds query position m
 #pragma unroll
       for (int ks = 0; ks < 2; ++ks) {
         const bf16x8 ah = cat(lds_read_tr(dSh + dsr0 + 512 * ks), lds_read_tr(dSh + dsr1 + 512 * ks));
-        const bf16x8 al = cat(lds_read_tr(dSl + dsr0 + 512 * ks), lds_read_tr(dSl + dsr1 + 512 * ks));
+        bf16x8 al = ah;
+        if (with_lo) al = cat(lds_read_tr(dSl + dsr0 + 512 * ks), lds_read_tr(dSl + dsr1 + 512 * ks));
 #pragma unroll
         for (int db = 0; db < DB; ++db) {
           const bf16* kt = ktb + (sub * kBk + 16 * ks) * (D + 8) + tr_step<D>(db);
           const bf16x8 kbop = cat(lds_read_tr(kt), lds_read_tr(kt + 8 * (D + 8)));
           acc[db] = mfma32(ah, kbop, acc[db]);
-          acc[db] = mfma32(al, kbop, acc[db]);
+          if (with_lo) acc[db] = mfma32(al, kbop, acc[db]);
         }
       }
       wave_lds_sync();   // the planes are rewritten by the next retained tile

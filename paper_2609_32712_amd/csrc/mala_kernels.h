@@ -15,14 +15,16 @@ constexpr int kFwdWaves = 8;                 // wavefronts per forward workgroup
 constexpr int kFwdRows = kFwdWaves * kBq;    // 256 query rows per workgroup
 constexpr int kFwdStage = 64;                // keys per K/V stage in LDS
 constexpr int kBwdKeys = 128;                // keys per backward workgroup (4 waves x kBk)
-// Budgets of the low bf16 term in the key-major backward.  P and dS enter the
-// MFMAs as hi + lo (two bf16 terms, 2^-16 relative).  The lo term of a tile is
-// left out of dV (P) or dK (dS) while, for every key of the tile, the P mass or the
-// sum of |dS| of the tiles run without it stays within a budget.  Since |lo| <=
-// 2^-8 |hi + lo|, the added error of a dV (dK) element is at most 2^-8 x budget x
-// the largest |dO| (|Q|, times the softmax scale).
+// Budgets of the low bf16 term in the backward.  P and dS enter the MFMAs as
+// hi + lo (two bf16 terms, 2^-16 relative).  The lo term of a tile is left out of
+// dV (P) or dK (dS) while, for every key of the tile, the P mass or the sum of |dS|
+// of the tiles run without it stays within a budget, and out of dQ (dS) while the
+// same holds for every query row.  Since |lo| <= 2^-8 |hi + lo|, the added error
+// of a dV (dK, dQ) element is at most 2^-8 x budget x the largest |dO| (|Q|, |K|,
+// times the softmax scale).
 constexpr float kLoMassDv = 1.0f / 16;      // dV: P mass per key
 constexpr float kLoMassDk = 0.25f;          // dK: sum of |dS| per key
+constexpr float kLoMassDq = 0.25f;          // dQ: sum of |dS| per query row
 constexpr int kDecStride = 4;                // extra floats per decode partial (lse, count, pad)
 
 struct FwdParams {
