@@ -232,7 +232,10 @@ __global__ __launch_bounds__(1024) void mala_bwd_dkdv_kernel(BwdParams p) {
   // chunk that the LDS layout keeps there (row padding positions and the slack at
   // the slot's end receive harmless data); the range check reads rows past the end
   // of the sequence as zeros.  Loads for tile t + 1 are issued at the start of
-  // iteration t and waited for just before its closing barrier.
+  // iteration t in the compiler-tracked form, so the dV wavefront waits for them at
+  // its first read of the dO tile (after reading and splitting P): that also holds
+  // its MFMAs back until the S wavefronts' dependent chains are under way, which
+  // measured faster than the untracked form with the wait at the barrier.
   auto tile_q0 = [&](int it) { return (nqt - 1 - it / grp) * kBq; };
   const bool mover = role == 1;
   const int mt = tid & 255;                  // thread index within the moving role
@@ -265,8 +268,8 @@ __global__ __launch_bounds__(1024) void mala_bwd_dkdv_kernel(BwdParams p) {
     for (int u = 0; u < NJ; ++u) {
       const int j = mw + 4 * u;
       if (j < NI) {
-        buf_load_lds16(rq, dma_off[u], Qs + (it & 3) * TS + 512 * j);
-        buf_load_lds16(ro, dma_off[u], dOs + (it % 3) * TS + 512 * j);
+        buf_load_lds16_tracked(rq, dma_off[u], Qs + (it & 3) * TS + 512 * j);
+        buf_load_lds16_tracked(ro, dma_off[u], dOs + (it % 3) * TS + 512 * j);
       }
     }
   };
@@ -535,7 +538,9 @@ __global__ __launch_bounds__(kFwdWaves * 64) void mala_bwd_dq_kernel(BwdParams p
   const int dsr1 = 8 * ds_chunk(8 + 4 * h + (t16 >> 2), dsj) + 4 * (t16 & 1);
 
   // K / V stages move with buffer loads straight into LDS (keys past the end read
-  // as zeros): wavefront w issues the 64-position loads w, w + 8, ... of each slot
+  // as zeros): wavefront w issues the 64-position loads w, w + 8, ... of each slot.
+  // The loads of stage t - 1 overlap the compute of stage t (untracked form) and
+  // are waited for just before the stage's closing barrier.
   constexpr int NIS = STAGE / 512;           // 64-position loads per stage slot
   static_assert(NIS * 512 == STAGE, "whole loads per slot");
   constexpr int NJS = (NIS + kFwdWaves - 1) / kFwdWaves;
@@ -545,7 +550,7 @@ __global__ __launch_bounds__(kFwdWaves * 64) void mala_bwd_dq_kernel(BwdParams p
   auto fetch = [&](int t, int buf) {
     const long k0 = (long)t * kFwdStage;
     const uint32_t nb = (uint32_t)(p.Nk - k0) * (uint32_t)D * 2u;
-    const auto rk = make_rsrc(Kp + k0 * D, nb), rvv = make_rsrc(Vp + k0 * D, nb);
+    const i32x4 rk = rsrc_words(Kp + k0 * D, nb), rvv = rsrc_words(Vp + k0 * D, nb);
 #pragma unroll
     for (int u = 0; u < NJS; ++u) {
       const int j = wave + kFwdWaves * u;

@@ -133,13 +133,42 @@ __device__ __forceinline__ float buf_load1(__amdgpu_buffer_rsrc_t r, uint32_t by
   return __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(r, byte_off, 0, 0));
 }
 
-// Buffer load straight into LDS (buffer_load_dwordx4 ... lds): lane i's 16 bytes
+// Buffer loads straight into LDS (buffer_load_dwordx4 ... lds): lane i's 16 bytes
 // land at lds_base + 16 i (lds_base uniform over the wavefront; checked by a
-// lane-layout probe on gfx950).  Completion is counted by vmcnt.
-__device__ __forceinline__ void buf_load_lds16(__amdgpu_buffer_rsrc_t r, uint32_t byte_off,
-                                               bf16* lds_base) {
+// lane-layout probe on gfx950).  Completion is counted by vmcnt.  Two forms:
+//  * buf_load_lds16_tracked, the compiler's builtin: the compiler orders every
+//    later LDS access of the wavefront after all of its outstanding loads (it
+//    cannot tell ring slots apart), i.e. the wavefront waits for the load at its
+//    next LDS access;
+//  * buf_load_lds16, in assembly: the compiler does not see the LDS write and adds
+//    no wait, so the load overlaps the wavefront's compute; the caller waits with
+//    wait_vm / wait_vm_keep before the data is read.  M0 (the LDS base) is saved and
+//    restored inside the statement, and one wait state separates its write from
+//    the load.
+__device__ __forceinline__ void buf_load_lds16_tracked(__amdgpu_buffer_rsrc_t r, uint32_t byte_off,
+                                                       bf16* lds_base) {
   __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (__attribute__((address_space(3))) void*)lds_base,
                                            16, byte_off, 0, 0, 0);
+}
+typedef int i32x4 __attribute__((ext_vector_type(4)));
+// The words of a buffer resource (base, size in bytes, reads past the size return
+// zeros), as make_rsrc builds it, for the assembly form.
+__device__ __forceinline__ i32x4 rsrc_words(const void* base, uint32_t bytes) {
+  const uint64_t a = (uint64_t)(uintptr_t)base;
+  return i32x4{(int)(uint32_t)a, (int)((uint32_t)(a >> 32) & 0xffffu), (int)bytes, 0x00020000};
+}
+__device__ __forceinline__ void buf_load_lds16(i32x4 rsrc, uint32_t byte_off, bf16* lds_base) {
+  const uint32_t lds = (uint32_t)(uintptr_t)((__attribute__((address_space(3))) bf16*)lds_base);
+  uint32_t saved;
+  asm volatile(
+      "s_mov_b32 %0, m0\n\t"
+      "s_mov_b32 m0, %3\n\t"
+      "s_nop 0\n\t"
+      "buffer_load_dwordx4 %1, %2, 0 offen lds\n\t"
+      "s_mov_b32 m0, %0"
+      : "=&s"(saved)
+      : "v"(byte_off), "s"(rsrc), "s"(lds)
+      : "memory");
 }
 // Byte offset, within a row-major [*][D] bf16 matrix, of the chunk that an
 // LDS-DMA lane must fetch so that chunk position pos of a tile slot laid out by
@@ -152,7 +181,19 @@ __device__ __forceinline__ uint32_t dma_lane_offset(int pos) {
   const int L = pc < D / 8 ? pc / (D / 32) + 4 * (pc % (D / 32)) : 0;
   return (uint32_t)(row * D + 8 * L) * 2u;
 }
-__device__ __forceinline__ void wait_vm() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
+// Waits until at most N vector-memory loads of this wavefront are outstanding
+// (loads, LDS-DMA included, complete in the order they were issued, so this waits
+// for all but the N most recent).  Written with the builtin, which the compiler's
+// own wait insertion takes into account, so that it adds no later wait for loads
+// this one already covered.  The encoding is gfx9's: vmcnt in bits 3:0 and 15:14,
+// expcnt (7) and lgkmcnt (15) left at their maxima.
+template <int N>
+__device__ __forceinline__ void wait_vm_keep() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt(0x0F70 | (N & 15) | ((N >> 4) << 14));
+  asm volatile("" ::: "memory");
+}
+__device__ __forceinline__ void wait_vm() { wait_vm_keep<0>(); }
 
 // Hardware base-2 exponential / logarithm (v_exp_f32 / v_log_f32, ~1 ulp on normal
 // results).  The softmax arguments are <= 0, so the results lie in [0, 1]; values
