@@ -408,36 +408,58 @@ __global__ __launch_bounds__(1024) void mala_bwd_dkdv_kernel(BwdParams p) {
       const int pf = role == 1 ? ((t >= 0 && t < total) ? Pflag[t % 3][grp_k] : 0) : fl3;
       if (pf) {
         const bool with_lo = role == 1 ? (pf & 2) != 0 : dSlo[t & 1][grp_k] != 0;
-        bf16x8 bh0, bh1, bl0, bl1;
-        const bf16* atb;
-        if (role == 1) {
-          float pv[16];
+        // B operands: P^T (role 1, from P in fp32) or dS (role 3, already split)
+        auto p_values = [&](float (&pv)[16]) {
 #pragma unroll
           for (int g = 0; g < 4; ++g) {
             const f32x4 p4 = Pf[t & 1][grp_k][g][lane];
 #pragma unroll
             for (int e = 0; e < 4; ++e) pv[4 * g + e] = p4[e];
           }
-          split_bf16x8(pv, bh0, bl0);
-          split_bf16x8(pv + 8, bh1, bl1);
+        };
+        bf16x8 bh0, bh1;
+        const bf16* atb;
+        if (role == 1) {
+          float pv[16];
+          p_values(pv);
+          bh0 = hi_bf16x8(pv);
+          bh1 = hi_bf16x8(pv + 8);
           atb = dOs + (t % 3) * TS + tro;
         } else {
           bh0 = dSop[t & 1][grp_k][0][lane];
           bh1 = dSop[t & 1][grp_k][1][lane];
-          bl0 = dSop[t & 1][grp_k][2][lane];
-          bl1 = dSop[t & 1][grp_k][3][lane];
           atb = Qs + (t & 3) * TS + tro;
         }
         const bf16* ab = lds_pin(atb);
+        auto a_operand = [&](int db, int ks) {
+          const bf16* at = ab + 16 * ks * (D + 8) + tr_step<D>(db);
+          return cat(lds_read_tr(at), lds_read_tr(at + 8 * (D + 8)));
+        };
+        // the hi MFMAs with no branch among them (a branch per MFMA kept each A
+        // read from being issued before the previous MFMA), then, when needed, a
+        // second pass with the lo B operands that reads the A operands again; the
+        // lo operands are formed only there, so they and the hi ones are never
+        // live together
 #pragma unroll
-        for (int db = 0; db < DB; ++db) {
+        for (int db = 0; db < DB; ++db)
 #pragma unroll
-          for (int ks = 0; ks < 2; ++ks) {
-            const bf16* at = ab + 16 * ks * (D + 8) + tr_step<D>(db);
-            const bf16x8 a = cat(lds_read_tr(at), lds_read_tr(at + 8 * (D + 8)));
-            acc[db] = mfma32(a, ks ? bh1 : bh0, acc[db]);
-            if (with_lo) acc[db] = mfma32(a, ks ? bl1 : bl0, acc[db]);
+          for (int ks = 0; ks < 2; ++ks) acc[db] = mfma32(a_operand(db, ks), ks ? bh1 : bh0, acc[db]);
+        if (with_lo) {
+          bf16x8 bl0, bl1;
+          if (role == 1) {
+            float pv[16];
+            p_values(pv);
+            bf16x8 h0, h1;
+            split_bf16x8(pv, h0, bl0);
+            split_bf16x8(pv + 8, h1, bl1);
+          } else {
+            bl0 = dSop[t & 1][grp_k][2][lane];
+            bl1 = dSop[t & 1][grp_k][3][lane];
           }
+#pragma unroll
+          for (int db = 0; db < DB; ++db)
+#pragma unroll
+            for (int ks = 0; ks < 2; ++ks) acc[db] = mfma32(a_operand(db, ks), ks ? bl1 : bl0, acc[db]);
         }
       }
       if (role == 3) {
@@ -632,18 +654,25 @@ __global__ __launch_bounds__(kFwdWaves * 64) void mala_bwd_dq_kernel(BwdParams p
       store8(dSh + dsw0, dh[0]);
       store8(dSh + dsw1, dh[1]);
       wave_lds_sync();
-      // dQ[q][d] += dS[q][key] K[key][d]; MFMA row m holds query position m
+      // dQ[q][d] += dS[q][key] K[key][d]; MFMA row m holds query position m.  The
+      // hi MFMAs run with no branch among them; the lo ones, when needed, in a
+      // second pass that reads the K operands again
+      auto k_operand = [&](int ks, int db) {
+        const bf16* kt = ktb + (sub * kBk + 16 * ks) * (D + 8) + tr_step<D>(db);
+        return cat(lds_read_tr(kt), lds_read_tr(kt + 8 * (D + 8)));
+      };
 #pragma unroll
       for (int ks = 0; ks < 2; ++ks) {
         const bf16x8 ah = cat(lds_read_tr(dSh + dsr0 + 512 * ks), lds_read_tr(dSh + dsr1 + 512 * ks));
-        bf16x8 al = ah;
-        if (with_lo) al = cat(lds_read_tr(dSl + dsr0 + 512 * ks), lds_read_tr(dSl + dsr1 + 512 * ks));
 #pragma unroll
-        for (int db = 0; db < DB; ++db) {
-          const bf16* kt = ktb + (sub * kBk + 16 * ks) * (D + 8) + tr_step<D>(db);
-          const bf16x8 kbop = cat(lds_read_tr(kt), lds_read_tr(kt + 8 * (D + 8)));
-          acc[db] = mfma32(ah, kbop, acc[db]);
-          if (with_lo) acc[db] = mfma32(al, kbop, acc[db]);
+        for (int db = 0; db < DB; ++db) acc[db] = mfma32(ah, k_operand(ks, db), acc[db]);
+      }
+      if (with_lo) {
+#pragma unroll
+        for (int ks = 0; ks < 2; ++ks) {
+          const bf16x8 al = cat(lds_read_tr(dSl + dsr0 + 512 * ks), lds_read_tr(dSl + dsr1 + 512 * ks));
+#pragma unroll
+          for (int db = 0; db < DB; ++db) acc[db] = mfma32(al, k_operand(ks, db), acc[db]);
         }
       }
       wave_lds_sync();   // the planes are rewritten by the next retained tile
