@@ -90,8 +90,8 @@ hipError_t launch_bwd_preprocess(const float* o, const bf16* dout, float* dvec, 
 
 
 // S = Q K^T for one 32 x 32 tile: A = Q rows (lane row q, 8 of d), B = K rows
-// (lane column key, 8 of d); even and odd k-steps in two chains, then summed.
-// Both backward kernels use exactly this sequence, so their scores are identical.
+// (lane column key, 8 of d); the k-steps accumulate in order in one chain.  Both
+// backward kernels use exactly this sequence, so their scores are identical.
 template <int KS>
 __device__ __forceinline__ f32x16 qk_tile(const bf16x8 (&a)[KS], const bf16x8 (&b)[KS]) {
   f32x16 s;
@@ -499,7 +499,7 @@ __device__ __forceinline__ int ds_chunk(int r, int j) {
 }
 
 template <int D>
-__global__ __launch_bounds__(kFwdWaves * 64) void mala_bwd_dq_kernel(BwdParams p) {
+__global__ __launch_bounds__(kDqWaves * 64) void mala_bwd_dq_kernel(BwdParams p) {
   constexpr int KS = D / 16;
   constexpr int DB = D / 32;
   constexpr int STAGE = tile_elems<D>(kFwdStage);
@@ -507,8 +507,8 @@ __global__ __launch_bounds__(kFwdWaves * 64) void mala_bwd_dq_kernel(BwdParams p
   constexpr int DSW = 2 * DSP;               // one wavefront's dS planes (hi, lo)
   __shared__ __attribute__((aligned(16))) bf16 Ks[2 * STAGE];
   __shared__ __attribute__((aligned(16))) bf16 Vs[2 * STAGE];
-  __shared__ __attribute__((aligned(16))) bf16 dSw[kFwdWaves * DSW];
-  __shared__ __attribute__((aligned(16))) float rowv[kFwdWaves][3][kBq];
+  __shared__ __attribute__((aligned(16))) bf16 dSw[kDqWaves * DSW];
+  __shared__ __attribute__((aligned(16))) float rowv[kDqWaves][3][kBq];
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -517,10 +517,10 @@ __global__ __launch_bounds__(kFwdWaves * 64) void mala_bwd_dq_kernel(BwdParams p
   const int rdo = rd_base<D>(c, h), tro = tr_base<D>(4 * h + (t16 >> 2), G & 1, t16);
   const int BH = p.B * p.Hq;
   const int bh = blockIdx.x % BH;
-  const int qblk = (p.Nq + kFwdRows - 1) / kFwdRows - 1 - (int)(blockIdx.x / BH);
+  const int qblk = (p.Nq + kDqRows - 1) / kDqRows - 1 - (int)(blockIdx.x / BH);
   const int b = bh / p.Hq, hq = bh % p.Hq, hkv = hq / (p.Hq / p.Hkv);
   const long off = (long)p.Nk - p.Nq;
-  const int q0w = qblk * kFwdRows + wave * kBq;
+  const int q0w = qblk * kDqRows + wave * kBq;
   const bool row_valid = q0w + c < p.Nq;
   const bf16* Kp = p.k + (long)(b * p.Hkv + hkv) * p.Nk * D;
   const bf16* Vp = p.v + (long)(b * p.Hkv + hkv) * p.Nk * D;
@@ -545,7 +545,7 @@ __global__ __launch_bounds__(kFwdWaves * 64) void mala_bwd_dq_kernel(BwdParams p
   const int qlast_w = min(q0w + kBq - 1, p.Nq - 1);
   const int jdiag = (q0w < p.Nq) ? (int)((qlast_w + off) / kBk) : -1;
   const int nvalid = max(0, min(kBq, p.Nq - q0w));
-  const int qlast_g = min(qblk * kFwdRows + kFwdRows - 1, p.Nq - 1);
+  const int qlast_g = min(qblk * kDqRows + kDqRows - 1, p.Nq - 1);
   const int ttop = (int)((qlast_g + off) / kFwdStage);
   unsigned n_legal = 0, n_ret = 0;
   int cnt_row = 0;   // retained tiles in which row q0w + c has a legal key
@@ -565,17 +565,17 @@ __global__ __launch_bounds__(kFwdWaves * 64) void mala_bwd_dq_kernel(BwdParams p
   // are waited for just before the stage's closing barrier.
   constexpr int NIS = STAGE / 512;           // 64-position loads per stage slot
   static_assert(NIS * 512 == STAGE, "whole loads per slot");
-  constexpr int NJS = (NIS + kFwdWaves - 1) / kFwdWaves;
+  constexpr int NJS = (NIS + kDqWaves - 1) / kDqWaves;
   uint32_t dma_off[NJS];
 #pragma unroll
-  for (int u = 0; u < NJS; ++u) dma_off[u] = dma_lane_offset<D>(64 * (wave + kFwdWaves * u) + lane);
+  for (int u = 0; u < NJS; ++u) dma_off[u] = dma_lane_offset<D>(64 * (wave + kDqWaves * u) + lane);
   auto fetch = [&](int t, int buf) {
     const long k0 = (long)t * kFwdStage;
     const uint32_t nb = (uint32_t)(p.Nk - k0) * (uint32_t)D * 2u;
     const i32x4 rk = rsrc_words(Kp + k0 * D, nb), rvv = rsrc_words(Vp + k0 * D, nb);
 #pragma unroll
     for (int u = 0; u < NJS; ++u) {
-      const int j = wave + kFwdWaves * u;
+      const int j = wave + kDqWaves * u;
       if (j < NIS) {
         buf_load_lds16(rk, dma_off[u], Ks + buf * STAGE + 512 * j);
         buf_load_lds16(rvv, dma_off[u], Vs + buf * STAGE + 512 * j);
@@ -702,7 +702,7 @@ __global__ __launch_bounds__(kFwdWaves * 64) void mala_bwd_dq_kernel(BwdParams p
 
 hipError_t launch_bwd(const BwdParams& p, int D, hipStream_t st) {
   dim3 grid_kv((unsigned)p.nkblk * p.B * p.Hkv), block_kv(1024);
-  dim3 grid_q((unsigned)((p.Nq + kFwdRows - 1) / kFwdRows) * p.B * p.Hq), block_q(kFwdWaves * 64);
+  dim3 grid_q((unsigned)((p.Nq + kDqRows - 1) / kDqRows) * p.B * p.Hq), block_q(kDqWaves * 64);
   if (D == 128) {
     hipLaunchKernelGGL(mala_bwd_dkdv_kernel<128>, grid_kv, block_kv, 0, st, p);
     hipLaunchKernelGGL(mala_bwd_dq_kernel<128>, grid_q, block_q, 0, st, p);

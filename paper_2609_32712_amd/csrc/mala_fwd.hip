@@ -4,10 +4,10 @@
 // head); each wavefront owns 32 rows, which is the decision tile's B_q.  K and V
 // are staged through double-buffered LDS 64 keys at a time, from the workgroup's
 // highest legal key down to key 0 (the diagonal-first traversal of the Online
-// Sparse Softmax paragraph); the next stage is fetched into registers while the
-// current one is processed.  Inside a stage each wavefront visits its two 32-key
-// decision tiles high half first, so every wavefront sees its tiles in strictly
-// descending order.
+// Sparse Softmax paragraph); the next stage moves straight into LDS (buffer loads
+// with the LDS flag) while the current one is processed.  Inside a stage each
+// wavefront visits its two 32-key decision tiles high half first, so every
+// wavefront sees its tiles in strictly descending order.
 //
 // Per decision tile (32 keys x the wavefront's 32 rows):
 //   S^T = K_j Q_i^T       8 (D = 128) bf16 MFMAs 32x32x16, fp32 accumulate; each
@@ -33,10 +33,8 @@ __global__ __launch_bounds__(kFwdWaves * 64) void mala_fwd_kernel(FwdParams p) {
   constexpr int KS = D / 16;             // k-steps of the QK product
   constexpr int DB = D / 32;             // 32-wide output column blocks
   constexpr int STAGE = tile_elems<D>(kFwdStage);
-  constexpr int CPT = kFwdStage * D / 8 / NT;   // 16-byte chunks per thread per stage
-  static_assert(CPT >= 1 && CPT * NT == kFwdStage * D / 8, "stage must split evenly");
-  // double-buffered K and V stages: the next stage is fetched into registers while
-  // the current one is processed
+  // double-buffered K and V stages: the next stage is fetched while the current one
+  // is processed
   __shared__ __attribute__((aligned(16))) bf16 Ks[2 * STAGE];
   __shared__ __attribute__((aligned(16))) bf16 Vs[2 * STAGE];
 
@@ -80,61 +78,41 @@ __global__ __launch_bounds__(kFwdWaves * 64) void mala_fwd_kernel(FwdParams p) {
   const int ttop = (int)((qlast_g + off) / kFwdStage);
   unsigned n_legal = 0, n_ret = 0;
 
-  bf16x8 pk[CPT], pv[CPT];
-  // K / V stages come through buffer loads: keys past the end read as zeros
-  auto fetch = [&](int t) {
+  // K / V stages move with buffer loads straight into LDS (keys past the end read
+  // as zeros): wavefront w issues the 64-position loads w, w + 8, ... of each slot.
+  // The loads of stage t - 1 overlap the compute of stage t and are waited for just
+  // before the stage's closing barrier.
+  constexpr int NIS = STAGE / 512;           // 64-position loads per stage slot
+  static_assert(NIS * 512 == STAGE, "whole loads per slot");
+  constexpr int NJS = (NIS + kFwdWaves - 1) / kFwdWaves;
+  uint32_t dma_off[NJS];
+#pragma unroll
+  for (int u = 0; u < NJS; ++u) dma_off[u] = dma_lane_offset<D>(64 * (wave + kFwdWaves * u) + lane);
+  auto fetch = [&](int t, int buf) {
     const long k0 = (long)t * kFwdStage;
     const uint32_t nb = (uint32_t)(p.Nk - k0) * (uint32_t)D * 2u;
-    const auto rk = make_rsrc(Kp + k0 * D, nb), rvv = make_rsrc(Vp + k0 * D, nb);
+    const i32x4 rk = rsrc_words(Kp + k0 * D, nb), rvv = rsrc_words(Vp + k0 * D, nb);
 #pragma unroll
-    for (int e = 0; e < CPT; ++e) {
-      const int ch = tid + NT * e;
-      const uint32_t off_b = (uint32_t)((ch / (D / 8)) * D + (ch % (D / 8)) * 8) * 2u;
-      pk[e] = buf_load8(rk, off_b);
-      pv[e] = buf_load8(rvv, off_b);
-    }
-  };
-  auto stash = [&](int buf) {
-#pragma unroll
-    for (int e = 0; e < CPT; ++e) {
-      const int ch = tid + NT * e;
-      const int row = ch / (D / 8), col = (ch % (D / 8)) * 8;
-      store8(Ks + buf * STAGE + tile_off<D>(row, col), pk[e]);
-      store8(Vs + buf * STAGE + tile_off<D>(row, col), pv[e]);
+    for (int u = 0; u < NJS; ++u) {
+      const int j = wave + kFwdWaves * u;
+      if (j < NIS) {
+        buf_load_lds16(rk, dma_off[u], Ks + buf * STAGE + 512 * j);
+        buf_load_lds16(rvv, dma_off[u], Vs + buf * STAGE + 512 * j);
+      }
     }
   };
 
-  fetch(ttop);
-  stash(0);
+  fetch(ttop, 0);
+  wait_vm();   // (also the Q loads above, so that no wait for them lands in the loop)
   __syncthreads();
 
   for (int t = ttop; t >= 0; --t) {
     const int buf = (ttop - t) & 1;
-    if (t > 0) fetch(t - 1);
+    if (t > 0) fetch(t - 1, buf ^ 1);
     const bf16* kr = lds_pin(Ks + buf * STAGE + rdo);
     const bf16* vtb = lds_pin(Vs + buf * STAGE + tro);
 
-    // Score discovery for both 32-key decision tiles of the stage at once (two
-    // independent accumulators; all K operands are read from LDS first).
     if (2 * t <= jdiag) {
-      f32x16 s2[2];
-#pragma unroll
-      for (int u = 0; u < 2; ++u)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) s2[u][r] = 0.f;
-      {
-        bf16x8 ka[2][KS];
-#pragma unroll
-        for (int kk = 0; kk < KS; ++kk) {
-          ka[1][kk] = load8(kr + kBk * (D + 8) + rd_step<D>(kk));
-          ka[0][kk] = load8(kr + rd_step<D>(kk));
-        }
-#pragma unroll
-        for (int kk = 0; kk < KS; ++kk) {
-          s2[1] = mfma32(ka[1][kk], qreg[kk], s2[1]);
-          s2[0] = mfma32(ka[0][kk], qreg[kk], s2[0]);
-        }
-      }
       // the two tiles in descending key order: the high half first
 #pragma unroll
       for (int sub = 1; sub >= 0; --sub) {
@@ -142,7 +120,17 @@ __global__ __launch_bounds__(kFwdWaves * 64) void mala_fwd_kernel(FwdParams p) {
         if (j > jdiag) continue;            // above this wavefront's diagonal
         const long kb = (long)j * kBk;
         ++n_legal;
-        const f32x16& s = s2[sub];
+        // score discovery (all K operands are read from LDS first)
+        f32x16 s;
+#pragma unroll
+        for (int r = 0; r < 16; ++r) s[r] = 0.f;
+        {
+          bf16x8 ka[KS];
+#pragma unroll
+          for (int kk = 0; kk < KS; ++kk) ka[kk] = load8(kr + sub * kBk * (D + 8) + rd_step<D>(kk));
+#pragma unroll
+          for (int kk = 0; kk < KS; ++kk) s = mfma32(ka[kk], qreg[kk], s);
+        }
 
         const bool need_mask = (kb + kBk - 1 > (long)q0w + off) || (q0w + kBq > p.Nq);
         float sv[16];
@@ -219,7 +207,7 @@ __global__ __launch_bounds__(kFwdWaves * 64) void mala_fwd_kernel(FwdParams p) {
           for (int db = 0; db < DB; ++db) acc[db] = mfma32(va[db][ks], pl[ks], acc[db]);
       }
     }
-    if (t > 0) stash(buf ^ 1);
+    wait_vm();
     __syncthreads();
   }
 

@@ -11,9 +11,11 @@ constexpr int kBq = 32;      // query rows per decision tile = rows of one wavef
 constexpr int kBk = 32;      // keys per decision tile
 constexpr int kDecBk = 32;   // keys per decode decision tile
 
-constexpr int kFwdWaves = 8;                 // wavefronts per forward workgroup
+constexpr int kFwdWaves = 8;                 // wavefronts per forward workgroup (2 per SIMD)
 constexpr int kFwdRows = kFwdWaves * kBq;    // 256 query rows per workgroup
-constexpr int kFwdStage = 64;                // keys per K/V stage in LDS
+constexpr int kDqWaves = 8;                  // wavefronts per dQ workgroup (2 per SIMD)
+constexpr int kDqRows = kDqWaves * kBq;      // 256 query rows per workgroup
+constexpr int kFwdStage = 64;                // keys per K/V stage in LDS (forward and dQ)
 constexpr int kBwdKeys = 128;                // keys per backward workgroup (4 waves x kBk)
 // Budgets of the low bf16 term in the backward.  P and dS enter the MFMAs as
 // hi + lo (two bf16 terms, 2^-16 relative).  The lo term of a tile is left out of
