@@ -487,28 +487,50 @@ __global__ __launch_bounds__(1024) void mala_bwd_dkdv_kernel(BwdParams p) {
   if (p.counters && tid == 0) atomicAdd(&p.counters[2], (unsigned long long)total);
 }
 
-// Staging tile of dS in the query-major kernel: [32 keys][32 query positions] bf16
-// without padding.  The 16-byte chunk j (positions 8 j .. 8 j + 7) of key row r is
-// stored at chunk 16 (r / 4) + r % 4 + 4 ((j + r / 4) % 4).  Query 8 g + 4 h + e of a
-// lane's C registers goes to position 16 (g / 2) + 8 h + 4 (g % 2) + e, so each lane
-// writes its values as two whole chunks; the chunk writes (16 lanes: 16 rows, one
-// chunk) and the transposed reads (32 lanes: 4 rows, 4 chunks) are both free of
-// bank conflicts, and 16 rows further on is always 64 chunks further on.
-__device__ __forceinline__ int ds_chunk(int r, int j) {
-  return 16 * (r >> 2) + (r & 3) + 4 * ((j + (r >> 2)) & 3);
+// Offline test of one tile in the transposed C layout of the dQ pass: the lane
+// holds one query row (threshold thr) and its 16 keys kb + 8 (r / 4) + 4 h + r % 4.
+// The same per-entry arithmetic as offline_test: fma(s, scale2, -thr) >= 0 with one
+// rounding.  Keys with 8 (r / 4) + r % 4 > kmax lie beyond the row's causal limit,
+// those with 8 (r / 4) + r % 4 >= klim beyond the sequence; both are only consulted
+// on tiles that cross the diagonal or an end (need_mask, uniform over the wavefront).
+// Rows past the end have thr = +inf and never retain.
+template <bool MASK>
+__device__ __forceinline__ bool offline_test_t(const f32x16& s, float scale2, int kmax, int klim,
+                                               float thr, float (&sv)[16]) {
+#pragma clang fp contract(off)
+  float dm = kNegInf;
+#pragma unroll
+  for (int r = 0; r < 16; ++r) {
+    const int kr = 8 * (r >> 2) + (r & 3);
+    const float x = s[r];
+    if (MASK) {
+      const bool legal = kr <= kmax && kr < klim;
+      sv[r] = legal ? x : kNegInf;
+      dm = fmaxf(dm, legal ? __builtin_fmaf(x, scale2, -thr) : kNegInf);
+    } else {
+      sv[r] = x;
+      dm = fmaxf(dm, __builtin_fmaf(x, scale2, -thr));
+    }
+  }
+  return dm >= 0.f;
 }
 
+// dQ pass (query-major).  Each wavefront owns 32 query rows and computes the
+// transposed products, so that every lane holds one query row: S^T = K Q^T and
+// dP^T = V dO^T (A = K / V rows from the LDS stage, B = the wavefront's Q / dO rows
+// in registers), then dQ^T += K^T dS^T with dS^T fed straight back from the C
+// registers as the B operand (the contraction index permuted as in the forward's
+// P.V) and K^T through transposed LDS reads.  An MFMA with its two operands
+// exchanged gives the transposed result bit for bit (checked by a probe on gfx950),
+// so the scores, and with them the retention decisions, equal those of the
+// key-major kernel (same operand values, k-step order and threshold arithmetic).
 template <int D>
 __global__ __launch_bounds__(kDqWaves * 64) void mala_bwd_dq_kernel(BwdParams p) {
   constexpr int KS = D / 16;
   constexpr int DB = D / 32;
   constexpr int STAGE = tile_elems<D>(kFwdStage);
-  constexpr int DSP = kBk * kBq;             // one dS plane [key][query position]
-  constexpr int DSW = 2 * DSP;               // one wavefront's dS planes (hi, lo)
   __shared__ __attribute__((aligned(16))) bf16 Ks[2 * STAGE];
   __shared__ __attribute__((aligned(16))) bf16 Vs[2 * STAGE];
-  __shared__ __attribute__((aligned(16))) bf16 dSw[kDqWaves * DSW];
-  __shared__ __attribute__((aligned(16))) float rowv[kDqWaves][3][kBq];
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -521,20 +543,22 @@ __global__ __launch_bounds__(kDqWaves * 64) void mala_bwd_dq_kernel(BwdParams p)
   const int b = bh / p.Hq, hq = bh % p.Hq, hkv = hq / (p.Hq / p.Hkv);
   const long off = (long)p.Nk - p.Nq;
   const int q0w = qblk * kDqRows + wave * kBq;
-  const bool row_valid = q0w + c < p.Nq;
+  const int qrow = q0w + c;
+  const bool row_valid = qrow < p.Nq;
   const bf16* Kp = p.k + (long)(b * p.Hkv + hkv) * p.Nk * D;
   const bf16* Vp = p.v + (long)(b * p.Hkv + hkv) * p.Nk * D;
 
-  // Q and dO rows of this wavefront as A operands (lane row q0w + c)
-  bf16x8 qa[KS], oa[KS];
+  // Q and dO rows of this wavefront as B operands (lane column qrow)
+  bf16x8 qb[KS], ob[KS];
 #pragma unroll
   for (int kk = 0; kk < KS; ++kk) {
-    const long off_e = ((long)bh * p.Nq + q0w + c) * D + 16 * kk + 8 * h;
-    qa[kk] = row_valid ? load8(p.q + off_e) : zero8();
-    oa[kk] = row_valid ? load8(p.dout + off_e) : zero8();
+    const long off_e = ((long)bh * p.Nq + qrow) * D + 16 * kk + 8 * h;
+    qb[kk] = row_valid ? load8(p.q + off_e) : zero8();
+    ob[kk] = row_valid ? load8(p.dout + off_e) : zero8();
   }
-  if (h == 0) row_vectors(p, bh, (long)q0w + c, off, &rowv[wave][0][c], &rowv[wave][1][c],
-                          &rowv[wave][2][c]);
+  // this lane's row vectors: base-2 lse, test threshold, D_q
+  float lse2, thr, dvq;
+  row_vectors(p, bh, (long)qrow, off, &lse2, &thr, &dvq);
 
   f32x16 acc[DB];
 #pragma unroll
@@ -548,16 +572,8 @@ __global__ __launch_bounds__(kDqWaves * 64) void mala_bwd_dq_kernel(BwdParams p)
   const int qlast_g = min(qblk * kDqRows + kDqRows - 1, p.Nq - 1);
   const int ttop = (int)((qlast_g + off) / kFwdStage);
   unsigned n_legal = 0, n_ret = 0;
-  int cnt_row = 0;   // retained tiles in which row q0w + c has a legal key
-  float fdq = 0.f;   // sum of this lane's largest |dS| in tiles run without the lo term
-  bf16* const dSh = dSw + wave * DSW;
-  bf16* const dSl = dSh + DSP;
-  // dS plane offsets: this lane's two chunk writes (key c, chunks h and 2 + h) and
-  // the bases of its transposed reads (key rows 4 h + t16 / 4 and 8 more)
-  const int dsw0 = 8 * ds_chunk(c, h), dsw1 = 8 * ds_chunk(c, 2 + h);
-  const int dsj = 2 * (G & 1) + ((t16 >> 1) & 1);
-  const int dsr0 = 8 * ds_chunk(4 * h + (t16 >> 2), dsj) + 4 * (t16 & 1);
-  const int dsr1 = 8 * ds_chunk(8 + 4 * h + (t16 >> 2), dsj) + 4 * (t16 & 1);
+  int cnt_row = 0;   // retained tiles in which row qrow has a legal key
+  float fdq = 0.f;   // this row's sum of |dS| in tiles run without the lo term
 
   // K / V stages move with buffer loads straight into LDS (keys past the end read
   // as zeros): wavefront w issues the 64-position loads w, w + 8, ... of each slot.
@@ -584,7 +600,7 @@ __global__ __launch_bounds__(kDqWaves * 64) void mala_bwd_dq_kernel(BwdParams p)
   };
 
   fetch(ttop, 0);
-  wait_vm();
+  wait_vm();   // (also the loads above, so that no wait for them lands in the loop)
   __syncthreads();
 
   for (int t = ttop; t >= 0; --t) {
@@ -603,96 +619,80 @@ __global__ __launch_bounds__(kDqWaves * 64) void mala_bwd_dq_kernel(BwdParams p)
       const int j = 2 * t + sub;
       if (j > jdiag) continue;
       const long kb = (long)j * kBk;
-      const int key = (int)kb + c;
       ++n_legal;
       bf16x8 kop[KS];
 #pragma unroll
       for (int kk = 0; kk < KS; ++kk) kop[kk] = load8(kr + sub * kBk * (D + 8) + rd_step<D>(kk));
-      const f32x16 s = qk_tile<KS>(qa, kop);
+      const f32x16 s = qk_tile<KS>(kop, qb);
       const bool need_mask =
           (kb + kBk - 1 > (long)q0w + off) || (q0w + kBq > p.Nq) || (kb + kBk > p.Nk);
-      const int klo = key < p.Nk ? (int)((long)key - off - q0w) - 4 * h : 1000000;
+      const int kmax = (int)((long)qrow + off - kb) - 4 * h;
+      const int klim = (int)min((long)p.Nk - kb, (long)kBk) - 4 * h;
       float sv[16];
-      const bool dem =
-          offline_entries(s, p.scale2, need_mask, klo, p.Nq - q0w - 4 * h, rowv[wave][1], h, sv);
+      const bool dem = need_mask ? offline_test_t<true>(s, p.scale2, kmax, klim, thr, sv)
+                                 : offline_test_t<false>(s, p.scale2, kmax, klim, thr, sv);
       if (!wave_any(dem)) continue;
       ++n_ret;
-      cnt_row += (row_valid && kb <= (long)q0w + c + off) ? 1 : 0;
-      probabilities(sv, p.scale2, rowv[wave][0], h);
+      cnt_row += (row_valid && kb <= (long)qrow + off) ? 1 : 0;
+      // P^T = exp2(s * scale2 - lse2), the key-major kernel's arithmetic
+#pragma unroll
+      for (int r = 0; r < 16; ++r) sv[r] = fast_exp2(__builtin_fmaf(sv[r], p.scale2, -lse2));
       bf16x8 vop[KS];
 #pragma unroll
       for (int kk = 0; kk < KS; ++kk) vop[kk] = load8(vr + sub * kBk * (D + 8) + rd_step<D>(kk));
-      const f32x16 dp = qk_tile<KS>(oa, vop);
+      const f32x16 dp = qk_tile<KS>(vop, ob);
       float dsv[16];
 #pragma unroll
-      for (int g = 0; g < 4; ++g) {
-        const f32x4 d4 = *reinterpret_cast<const f32x4*>(rowv[wave][2] + 8 * g + 4 * h);
+      for (int r = 0; r < 16; ++r) dsv[r] = sv[r] * (dp[r] - dvq);
+      // dQ runs this tile without dS's lo term while this row's sum of |dS| over
+      // such tiles stays within kLoMassDq (for every row of the wavefront)
+      float as = 0.f;
 #pragma unroll
-        for (int e = 0; e < 4; ++e) dsv[4 * g + e] = sv[4 * g + e] * (dp[4 * g + e] - d4[e]);
-      }
-      // dQ runs this tile without dS's lo term while, for every lane, the sum over
-      // such tiles of the lane's largest |dS| stays within kLoMassDq / 32: a query
-      // row's 32 keys of a tile sit in 32 lanes, so its sum of |dS| over those
-      // tiles stays within kLoMassDq
-      float mx = 0.f;
-#pragma unroll
-      for (int r = 0; r < 16; ++r) mx = fmaxf(mx, fabsf(dsv[r]));
-      const float fq_new = fdq + mx;
-      const bool with_lo = wave_any(fq_new > kLoMassDq * (1.f / kBk));
+      for (int r = 0; r < 16; ++r) as += fabsf(dsv[r]);
+      const float fq_new = fdq + halves_sum(as);
+      const bool with_lo = wave_any(fq_new > kLoMassDq);
       if (!with_lo) fdq = fq_new;
-      bf16x8 dh[2], dl[2];
-      // dS^T -> this wavefront's LDS planes as [key][query position]
-      if (with_lo) {
-        split_bf16x8(dsv, dh[0], dl[0]);
-        split_bf16x8(dsv + 8, dh[1], dl[1]);
-        store8(dSl + dsw0, dl[0]);
-        store8(dSl + dsw1, dl[1]);
-      } else {
-        dh[0] = hi_bf16x8(dsv);
-        dh[1] = hi_bf16x8(dsv + 8);
-      }
-      store8(dSh + dsw0, dh[0]);
-      store8(dSh + dsw1, dh[1]);
-      wave_lds_sync();
-      // dQ[q][d] += dS[q][key] K[key][d]; MFMA row m holds query position m.  The
-      // hi MFMAs run with no branch among them; the lo ones, when needed, in a
-      // second pass that reads the K operands again
+      // dQ^T[d][q] += K^T[d][key] dS^T[key][q]: k-step ks takes C registers
+      // 8 ks .. 8 ks + 7 as the B operand, K^T through transposed reads of the same
+      // key rows.  The hi MFMAs run with no branch among them; the lo ones, when
+      // needed, in a second pass that reads the K operands again.
       auto k_operand = [&](int ks, int db) {
         const bf16* kt = ktb + (sub * kBk + 16 * ks) * (D + 8) + tr_step<D>(db);
         return cat(lds_read_tr(kt), lds_read_tr(kt + 8 * (D + 8)));
       };
+      const bf16x8 dh[2] = {hi_bf16x8(dsv), hi_bf16x8(dsv + 8)};
 #pragma unroll
-      for (int ks = 0; ks < 2; ++ks) {
-        const bf16x8 ah = cat(lds_read_tr(dSh + dsr0 + 512 * ks), lds_read_tr(dSh + dsr1 + 512 * ks));
+      for (int ks = 0; ks < 2; ++ks)
 #pragma unroll
-        for (int db = 0; db < DB; ++db) acc[db] = mfma32(ah, k_operand(ks, db), acc[db]);
-      }
+        for (int db = 0; db < DB; ++db) acc[db] = mfma32(k_operand(ks, db), dh[ks], acc[db]);
       if (with_lo) {
+        bf16x8 dl[2], hh[2];
+        split_bf16x8(dsv, hh[0], dl[0]);
+        split_bf16x8(dsv + 8, hh[1], dl[1]);
 #pragma unroll
-        for (int ks = 0; ks < 2; ++ks) {
-          const bf16x8 al = cat(lds_read_tr(dSl + dsr0 + 512 * ks), lds_read_tr(dSl + dsr1 + 512 * ks));
+        for (int ks = 0; ks < 2; ++ks)
 #pragma unroll
-          for (int db = 0; db < DB; ++db) acc[db] = mfma32(al, k_operand(ks, db), acc[db]);
-        }
+          for (int db = 0; db < DB; ++db) acc[db] = mfma32(k_operand(ks, db), dl[ks], acc[db]);
       }
-      wave_lds_sync();   // the planes are rewritten by the next retained tile
     }
     __builtin_amdgcn_s_setprio(0);
     wait_vm();
     __syncthreads();
   }
 
-  // dQ = scale * sum dS K; lane (h, c) holds column 32 db + c of the query positions
-  // m = 8 (r / 4) + 4 h + r % 4, i.e. of queries m with bits 2 and 3 swapped
+  // dQ = scale * sum dS K; lane (h, c) holds row qrow, columns 32 db + 8 g + 4 h + e
+  if (row_valid) {
+    float* dst = p.dq + ((long)bh * p.Nq + qrow) * D;
 #pragma unroll
-  for (int db = 0; db < DB; ++db)
+    for (int db = 0; db < DB; ++db)
 #pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      const int m = 8 * (r >> 2) + 4 * h + (r & 3);
-      const long qq = (long)q0w + ((m & ~12) | ((m & 4) << 1) | ((m & 8) >> 1));
-      if (qq < p.Nq) p.dq[((long)bh * p.Nq + qq) * D + 32 * db + c] = acc[db][r] * p.scale;
-    }
-  if (p.row_tiles && h == 0 && row_valid) p.row_tiles[(long)bh * p.Nq + q0w + c] = cnt_row;
+      for (int g = 0; g < 4; ++g) {
+        const f32x4 v4 = {acc[db][4 * g] * p.scale, acc[db][4 * g + 1] * p.scale,
+                          acc[db][4 * g + 2] * p.scale, acc[db][4 * g + 3] * p.scale};
+        *reinterpret_cast<f32x4*>(dst + 32 * db + 8 * g + 4 * h) = v4;
+      }
+    if (p.row_tiles && h == 0) p.row_tiles[(long)bh * p.Nq + qrow] = cnt_row;
+  }
   if (p.counters && lane == 0 && n_legal) {
     atomicAdd(&p.counters[0], (unsigned long long)n_legal);
     atomicAdd(&p.counters[1], (unsigned long long)n_ret);
