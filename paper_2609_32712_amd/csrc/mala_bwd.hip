@@ -489,30 +489,26 @@ __global__ __launch_bounds__(1024) void mala_bwd_dkdv_kernel(BwdParams p) {
 
 // Offline test of one tile in the transposed C layout of the dQ pass: the lane
 // holds one query row (threshold thr) and its 16 keys kb + 8 (r / 4) + 4 h + r % 4.
-// The same per-entry arithmetic as offline_test: fma(s, scale2, -thr) >= 0 with one
-// rounding.  Keys with 8 (r / 4) + r % 4 > kmax lie beyond the row's causal limit,
+// The per-entry test of offline_test, fma(s, scale2, -thr) >= 0 with one rounding,
+// is monotonic in s (scale2 > 0), so with one threshold per lane it is taken once,
+// on the lane's largest legal score: the same decision with one fma instead of
+// sixteen.  Keys with 8 (r / 4) + r % 4 > kmax lie beyond the row's causal limit,
 // those with 8 (r / 4) + r % 4 >= klim beyond the sequence; both are only consulted
-// on tiles that cross the diagonal or an end (need_mask, uniform over the wavefront).
-// Rows past the end have thr = +inf and never retain.
+// on tiles that cross the diagonal or an end (need_mask, uniform over the
+// wavefront).  Rows past the end have thr = +inf and never retain.
 template <bool MASK>
 __device__ __forceinline__ bool offline_test_t(const f32x16& s, float scale2, int kmax, int klim,
                                                float thr, float (&sv)[16]) {
 #pragma clang fp contract(off)
-  float dm = kNegInf;
+  float mx = kNegInf;
 #pragma unroll
   for (int r = 0; r < 16; ++r) {
     const int kr = 8 * (r >> 2) + (r & 3);
-    const float x = s[r];
-    if (MASK) {
-      const bool legal = kr <= kmax && kr < klim;
-      sv[r] = legal ? x : kNegInf;
-      dm = fmaxf(dm, legal ? __builtin_fmaf(x, scale2, -thr) : kNegInf);
-    } else {
-      sv[r] = x;
-      dm = fmaxf(dm, __builtin_fmaf(x, scale2, -thr));
-    }
+    const float x = (!MASK || (kr <= kmax && kr < klim)) ? s[r] : kNegInf;
+    sv[r] = x;
+    mx = fmaxf(mx, x);
   }
-  return dm >= 0.f;
+  return __builtin_fmaf(mx, scale2, -thr) >= 0.f;
 }
 
 // dQ pass (query-major).  Each wavefront owns 32 query rows and computes the

@@ -140,18 +140,20 @@ __global__ __launch_bounds__(kFwdWaves * 64) void mala_fwd_kernel(FwdParams p) {
           const int lim = row_valid ? (int)((long)qrow + off - kb) - 4 * h : -1000000;
 #pragma unroll
           for (int r = 0; r < 16; ++r) {
-            const float x = (8 * (r >> 2) + (r & 3) <= lim) ? s[r] * p.scale2 : kNegInf;
+            const float x = (8 * (r >> 2) + (r & 3) <= lim) ? s[r] : kNegInf;
             sv[r] = x;
             mt = fmaxf(mt, x);
           }
         } else {
 #pragma unroll
           for (int r = 0; r < 16; ++r) {
-            sv[r] = s[r] * p.scale2;
+            sv[r] = s[r];
             mt = fmaxf(mt, sv[r]);
           }
         }
-        mt = halves_max(mt);
+        // the row max of the raw scores, then scaled (scale2 > 0 and rounding is
+        // monotonic, so this is the max of the scaled scores)
+        mt = halves_max(mt) * p.scale2;
 
         // the online test (rows with no legal key in the tile do not vote); m + log2(l)
         // is log2 of the retained normalizer whichever reference m the row uses
@@ -176,13 +178,13 @@ __global__ __launch_bounds__(kFwdWaves * 64) void mala_fwd_kernel(FwdParams p) {
         }
         // a row with no legal key so far keeps m = -inf: shift by 0 so exp2(-inf) = 0
         const float shift = (m == kNegInf) ? 0.f : m;
-        float ps = 0.f;
+        // P = exp2(s scale2 - shift) with one rounding; the row sum as a tree
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          sv[r] = fast_exp2(sv[r] - shift);
-          ps += sv[r];
-        }
-        l += halves_sum(ps);
+        for (int r = 0; r < 16; ++r) sv[r] = fast_exp2(__builtin_fmaf(sv[r], p.scale2, -shift));
+        float ps4[4];
+#pragma unroll
+        for (int g = 0; g < 4; ++g) ps4[g] = (sv[4 * g] + sv[4 * g + 1]) + (sv[4 * g + 2] + sv[4 * g + 3]);
+        l += halves_sum((ps4[0] + ps4[1]) + (ps4[2] + ps4[3]));
         // P as two bf16 terms: the backward's D = rowsum(O * dO) cancels against
         // dP for dominant keys, so O must be accurate well beyond one bf16 rounding
         bf16x8 ph[2], pl[2];
