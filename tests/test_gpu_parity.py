@@ -265,6 +265,8 @@ def test_full_config5_decode_sampled(tau):
 # reproducibility
 # --------------------------------------------------------------------------
 def test_repeat_runs_bitwise_forward_dk_dv():
+    # no kernel accumulates through atomics or in a launch-dependent order, so
+    # repeated calls give identical outputs and statistics
     w, q, k, v, do = _train_case("gqa_d128_ragged", 0.1)
     Q, K, V, DO = map(dev, (q, k, v, do))
     r1 = mala.fwd(Q, K, V, f32(w.scale), 0.1)
@@ -274,4 +276,5 @@ def test_repeat_runs_bitwise_forward_dk_dv():
     torch.cuda.synchronize()
     assert torch.equal(r1["o"], r2["o"]) and torch.equal(r1["lse"], r2["lse"])
     assert torch.equal(b1["dk"], b2["dk"]) and torch.equal(b1["dv"], b2["dv"])
-    assert torch.allclose(b1["dq"], b2["dq"], atol=1e-5)
+    assert torch.equal(b1["dq"], b2["dq"])
+    assert torch.equal(b1["row_tiles"], b2["row_tiles"]) and torch.equal(r1["row_tiles"], r2["row_tiles"])
