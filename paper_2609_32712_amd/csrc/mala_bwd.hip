@@ -2,31 +2,28 @@
 // tile decisions.
 //
 // mala_bwd_dkdv_kernel (key-major, Algorithm 2's traversal): one workgroup owns 128
-// keys of one (batch, KV head), with their K and V rows in registers, and keeps their
-// dK and dV in registers for the whole kernel (no atomics, bitwise reproducible); it
-// loops over every query head of the GQA group and over the query tiles from the
-// end down to the diagonal.  Eight wavefronts in two pipelined roles over keys
-// [32 (w % 4), +32): wavefronts 4-7 take the tile decisions, form P and accumulate
-// dV; one tile later wavefronts 0-3 form dP and dS and accumulate dK; P passes
-// between the two through LDS.  Each wavefront holds a 64-register accumulator
-// (two wavefronts per SIMD) and runs 24 MFMAs per retained tile.  Query tiles (Q,
-// dO and the per-row base-2 LSE, threshold and D_q = rowsum(O * dO)) rotate
-// through three LDS buffers; the next tile is fetched into registers while the
-// current one is processed.
+// keys of one (batch, KV head) and keeps their dK and dV in registers for the whole
+// kernel (no atomics, bitwise reproducible); it sweeps the query tiles of every
+// query head of the GQA group from the end down to the diagonal.  Sixteen
+// wavefronts, four roles per 32 keys on one SIMD, pipelined over the query tiles:
+// role 0 takes the tile decision and forms P (fp32, handed on through LDS), role 1
+// accumulates dV one tile later and moves the query tiles into LDS, role 2 forms
+// dP and dS, role 3 accumulates dK two tiles later (dS handed on as bf16 operands).
 //   S = Q_i K_w^T         8 MFMAs (lane = one key column, 16 query rows)
 //   offline test          retain iff some valid entry has
 //                         s - lse_q >= log2(tau) - log2(L_q) (base-2 units); ballot
-//   retained path         P = exp2(S - lse) (handed on in fp32), dV^T += dO_i^T P;
-//                         one tile later: dP = dO_i V_w^T, dS = P (dP - D_q),
-//                         dK^T += Q_i^T dS.  P and dS enter the MFMAs as two bf16
-//                         terms (hi + lo); the A operands come through
+//   retained path         P = exp2(S - lse), dV^T += dO_i^T P; dP = dO_i V_w^T,
+//                         dS = P (dP - D_q), dK^T += Q_i^T dS.  P and dS enter the
+//                         MFMAs as two bf16 terms (hi + lo) unless an error budget
+//                         allows the hi term alone; the A operands come through
 //                         ds_read_b64_tr_b16.
 // mala_bwd_dq_kernel (query-major, like the forward): one workgroup = 8 wavefronts
-// = 256 query rows; K and V stream through double-buffered LDS.  Per decision
-// tile it recomputes S and dP with the same MFMA operand roles and accumulation
-// order as the key-major kernel (so the offline test sees bitwise the same
-// scores), then dQ_i += dS K_j with dS transposed through a per-wavefront LDS
-// tile.  dQ needs no atomics and is bitwise reproducible.
+// = 256 query rows; K and V stream through double-buffered LDS.  It computes the
+// transposed products (S^T = K Q^T, dP^T = V dO^T, dQ^T += K^T dS^T), so that a
+// lane holds one query row and dS feeds the dQ MFMA straight from registers; an
+// MFMA with its operands exchanged gives the transposed scores bit for bit, so the
+// offline test sees the key-major kernel's scores.  dQ needs no atomics and is
+// bitwise reproducible.
 // A skipped tile costs its QK MFMAs and the test in both kernels.
 #include "mala_device.h"
 #include "mala_kernels.h"
@@ -226,8 +223,9 @@ __global__ __launch_bounds__(1024) void mala_bwd_dkdv_kernel(BwdParams p) {
   // heads of the group innermost (iteration it: tile nqt - 1 - it / grp, head
   // it % grp): the offline test does not depend on the order, and all co-resident
   // workgroups of the same KV head then step through the same Q / dO tiles in
-  // lockstep, so that one fetch from HBM serves the whole XCD through its L2.  The dV wavefronts (role 1, which wait longest at the barrier)
-  // move them with buffer loads straight into LDS: the 64 lanes of one load fill
+  // lockstep, so that one fetch from HBM serves the whole XCD through its L2.
+  // The dV wavefronts (role 1, which wait longest at the barrier) move the tiles
+  // with buffer loads straight into LDS: the 64 lanes of one load fill
   // 64 consecutive 16-byte positions of the tile's slot, each lane fetching the
   // chunk that the LDS layout keeps there (row padding positions and the slack at
   // the slot's end receive harmless data); the range check reads rows past the end
@@ -443,7 +441,8 @@ __global__ __launch_bounds__(1024) void mala_bwd_dkdv_kernel(BwdParams p) {
 #pragma unroll
         for (int db = 0; db < DB; ++db)
 #pragma unroll
-          for (int ks = 0; ks < 2; ++ks) acc[db] = mfma32(a_operand(db, ks), ks ? bh1 : bh0, acc[db]);
+          for (int ks = 0; ks < 2; ++ks)
+            acc[db] = mfma32(a_operand(db, ks), ks ? bh1 : bh0, acc[db]);
         if (with_lo) {
           bf16x8 bl0, bl1;
           if (role == 1) {
@@ -459,7 +458,8 @@ __global__ __launch_bounds__(1024) void mala_bwd_dkdv_kernel(BwdParams p) {
 #pragma unroll
           for (int db = 0; db < DB; ++db)
 #pragma unroll
-            for (int ks = 0; ks < 2; ++ks) acc[db] = mfma32(a_operand(db, ks), ks ? bl1 : bl0, acc[db]);
+            for (int ks = 0; ks < 2; ++ks)
+              acc[db] = mfma32(a_operand(db, ks), ks ? bl1 : bl0, acc[db]);
         }
       }
       if (role == 3) {

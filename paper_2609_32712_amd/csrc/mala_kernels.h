@@ -16,7 +16,7 @@ constexpr int kFwdRows = kFwdWaves * kBq;    // 256 query rows per workgroup
 constexpr int kDqWaves = 8;                  // wavefronts per dQ workgroup (2 per SIMD)
 constexpr int kDqRows = kDqWaves * kBq;      // 256 query rows per workgroup
 constexpr int kFwdStage = 64;                // keys per K/V stage in LDS (forward and dQ)
-constexpr int kBwdKeys = 128;                // keys per backward workgroup (4 waves x kBk)
+constexpr int kBwdKeys = 128;                // keys per dK/dV workgroup (4 key groups x kBk)
 // Budgets of the low bf16 term in the backward.  P and dS enter the MFMAs as
 // hi + lo (two bf16 terms, 2^-16 relative).  The lo term of a tile is left out of
 // dV (P) or dK (dS) while, for every key of the tile, the P mass or the sum of |dS|
