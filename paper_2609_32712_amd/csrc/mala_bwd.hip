@@ -390,84 +390,63 @@ __global__ __launch_bounds__(1024) void mala_bwd_dkdv_kernel(BwdParams p) {
       }
     }
   } else {
-    // roles 1 (dV^T += dO^T P, one tile behind) and 3 (dK^T += Q^T dS, two behind)
+    // roles 1 (dV^T += dO^T P, one tile behind) and 3 (dK^T += Q^T dS, two behind),
+    // each in its own loop
     f32x16 acc[DB];
 #pragma unroll
     for (int db = 0; db < DB; ++db)
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[db][r] = 0.f;
-    const int lag = role == 1 ? 1 : 2;
-    // the decision of tile it - 2 is known since the end of iteration it - 2: role
-    // 3 reads it one iteration early, off its critical path
-    int fl3 = 0;
-    for (int it = 0; it < n_it; ++it) {
-      if (role == 1 && it + 1 < total) fetch(it + 1);
-      const int t = it - lag;
-      const int pf = role == 1 ? ((t >= 0 && t < total) ? Pflag[t % 3][grp_k] : 0) : fl3;
-      if (pf) {
-        const bool with_lo = role == 1 ? (pf & 2) != 0 : dSlo[t & 1][grp_k] != 0;
-        // B operands: P^T (role 1, from P in fp32) or dS (role 3, already split)
-        auto p_values = [&](float (&pv)[16]) {
+    auto accumulate = [&](const bf16* atb, bf16x8 b0, bf16x8 b1) {
+      const bf16* ab = lds_pin(atb);
+#pragma unroll
+      for (int db = 0; db < DB; ++db)
+#pragma unroll
+        for (int ks = 0; ks < 2; ++ks) {
+          const bf16* at = ab + 16 * ks * (D + 8) + tr_step<D>(db);
+          acc[db] = mfma32(cat(lds_read_tr(at), lds_read_tr(at + 8 * (D + 8))), ks ? b1 : b0, acc[db]);
+        }
+    };
+    if (role == 1) {
+      for (int it = 0; it < n_it; ++it) {
+        if (it + 1 < total) fetch(it + 1);
+        const int t = it - 1;
+        const int pf = (t >= 0 && t < total) ? Pflag[t % 3][grp_k] : 0;
+        if (pf) {
+          float pv[16];
 #pragma unroll
           for (int g = 0; g < 4; ++g) {
             const f32x4 p4 = Pf[t & 1][grp_k][g][lane];
 #pragma unroll
             for (int e = 0; e < 4; ++e) pv[4 * g + e] = p4[e];
           }
-        };
-        bf16x8 bh0, bh1;
-        const bf16* atb;
-        if (role == 1) {
-          float pv[16];
-          p_values(pv);
-          bh0 = hi_bf16x8(pv);
-          bh1 = hi_bf16x8(pv + 8);
-          atb = dOs + (t % 3) * TS + tro;
-        } else {
-          bh0 = dSop[t & 1][grp_k][0][lane];
-          bh1 = dSop[t & 1][grp_k][1][lane];
-          atb = Qs + (t & 3) * TS + tro;
-        }
-        const bf16* ab = lds_pin(atb);
-        auto a_operand = [&](int db, int ks) {
-          const bf16* at = ab + 16 * ks * (D + 8) + tr_step<D>(db);
-          return cat(lds_read_tr(at), lds_read_tr(at + 8 * (D + 8)));
-        };
-        // the hi MFMAs with no branch among them (a branch per MFMA kept each A
-        // read from being issued before the previous MFMA), then, when needed, a
-        // second pass with the lo B operands that reads the A operands again; the
-        // lo operands are formed only there, so they and the hi ones are never
-        // live together
-#pragma unroll
-        for (int db = 0; db < DB; ++db)
-#pragma unroll
-          for (int ks = 0; ks < 2; ++ks)
-            acc[db] = mfma32(a_operand(db, ks), ks ? bh1 : bh0, acc[db]);
-        if (with_lo) {
-          bf16x8 bl0, bl1;
-          if (role == 1) {
-            float pv[16];
-            p_values(pv);
-            bf16x8 h0, h1;
-            split_bf16x8(pv, h0, bl0);
-            split_bf16x8(pv + 8, h1, bl1);
-          } else {
-            bl0 = dSop[t & 1][grp_k][2][lane];
-            bl1 = dSop[t & 1][grp_k][3][lane];
+          const bf16* atb = dOs + (t % 3) * TS + tro;
+          accumulate(atb, hi_bf16x8(pv), hi_bf16x8(pv + 8));
+          if (pf & 2) {
+            bf16x8 hh[2], bl[2];
+            split_bf16x8(pv, hh[0], bl[0]);
+            split_bf16x8(pv + 8, hh[1], bl[1]);
+            accumulate(atb, bl[0], bl[1]);
           }
-#pragma unroll
-          for (int db = 0; db < DB; ++db)
-#pragma unroll
-            for (int ks = 0; ks < 2; ++ks)
-              acc[db] = mfma32(a_operand(db, ks), ks ? bl1 : bl0, acc[db]);
         }
+        if (it + 1 < total) stash(it + 1);
+        __syncthreads();
       }
-      if (role == 3) {
+    } else {
+      // the decision of tile it - 2 is known since the end of iteration it - 2: it
+      // is read one iteration early, off the critical path
+      int fl3 = 0;
+      for (int it = 0; it < n_it; ++it) {
+        const int t = it - 2;
+        if (fl3) {
+          const bf16* atb = Qs + (t & 3) * TS + tro;
+          accumulate(atb, dSop[t & 1][grp_k][0][lane], dSop[t & 1][grp_k][1][lane]);
+          if (dSlo[t & 1][grp_k]) accumulate(atb, dSop[t & 1][grp_k][2][lane], dSop[t & 1][grp_k][3][lane]);
+        }
         const int tn = it - 1;   // the tile of the next iteration
         fl3 = (tn >= 0 && tn < total) ? Pflag[tn % 3][grp_k] : 0;
+        __syncthreads();
       }
-      if (role == 1 && it + 1 < total) stash(it + 1);
-      __syncthreads();
     }
     // dV = sum P^T dO (role 1), dK = scale * sum dS^T Q (role 3); lane (h, c)
     // holds key kw + c
