@@ -56,8 +56,9 @@ typedef enum {
   MALA_ERR_INVALID_ARG = -1, /* null required pointer, non-positive size, Hq % Hkv != 0,
                                 Nq > Nk, tau < 0 or NaN, scale not finite or <= 0,
                                 num_splits < 1 */
-  MALA_ERR_UNSUPPORTED = -2, /* head_dim not in {64, 128}, or causal == 0 (the paper's
-                                traversal is defined for causal attention only) */
+  MALA_ERR_UNSUPPORTED = -2, /* head_dim not in {64, 128}, causal == 0 (the paper's
+                                traversal is defined for causal attention only), or a
+                                forward/backward K/V slice of 2^32 bytes or more */
   MALA_ERR_WORKSPACE = -3,   /* workspace NULL or smaller than the *_workspace_size query */
   MALA_ERR_HIP = -4          /* a HIP launch/runtime call failed; see mala_last_error() */
 } mala_status;
@@ -102,7 +103,8 @@ const char* mala_last_error(void);
  *   row_tiles: int32 [B, Hq, Nq] or NULL   out: retained tiles in which the row has a
  *              legal key
  *   counters:  int64 [4] or NULL          out: see MALA_CNT_*
- *   causal must be 1.  Requires Nq <= Nk, D in {64, 128}.
+ *   causal must be 1.  Requires Nq <= Nk, D in {64, 128} and Nk * D * 2 < 2^32
+ *   (Nk below 16M tokens at D = 128); otherwise MALA_ERR_UNSUPPORTED.
  */
 int mala_fwd(const void* q, const void* k, const void* v, float* o, float* lse,
              int32_t* row_tiles, int64_t* counters, int B, int Hq, int Hkv, int Nq, int Nk,
@@ -125,6 +127,7 @@ size_t mala_bwd_workspace_size(int B, int Hq, int Hkv, int Nq, int Nk, int D);
  *   row_tiles: int32 [B, Hq, Nq] or NULL out; counters: int64 [4] or NULL out.
  *   workspace: device memory of at least mala_bwd_workspace_size(...) bytes,
  *   16-byte aligned, owned by the caller, not read by the caller afterwards.
+ *   The shape limits of mala_fwd apply.
  */
 int mala_bwd(const void* q, const void* k, const void* v, const float* o, const float* lse,
              const void* dout, float* dq, float* dk, float* dv, int32_t* row_tiles,

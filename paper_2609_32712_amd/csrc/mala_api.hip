@@ -40,6 +40,15 @@ int check_common(int B, int Hq, int Hkv, int Nq, int Nk, int D, int causal, floa
   return MALA_OK;
 }
 
+// The training kernels address one (batch, head) slice from a tile start through
+// buffer resources whose range is a 32-bit byte count: Nk x D bf16 values must fit.
+int check_slice_range(int Nk, int D) {
+  const long long bytes = (long long)Nk * D * 2;
+  if (bytes > 0xffffffffLL)
+    return fail(MALA_ERR_UNSUPPORTED, "Nk x D x 2 = %lld bytes exceeds the 32-bit slice range", bytes);
+  return MALA_OK;
+}
+
 float log2_tau(float tau) { return tau > 0.f ? log2f(tau) : -INFINITY; }
 
 }  // namespace
@@ -78,6 +87,7 @@ int mala_fwd(const void* q, const void* k, const void* v, float* o, float* lse, 
   g_err[0] = 0;
   if (!q || !k || !v || !o || !lse) return fail(MALA_ERR_INVALID_ARG, "null q, k, v, o or lse");
   int st = check_common(B, Hq, Hkv, Nq, Nk, D, causal, scale, tau);
+  if (!st) st = check_slice_range(Nk, D);
   if (st) return st;
   hipStream_t s = (hipStream_t)stream;
   if (counters) {
@@ -115,6 +125,7 @@ int mala_bwd(const void* q, const void* k, const void* v, const float* o, const 
   if (!q || !k || !v || !o || !lse || !dout || !dq || !dk || !dv)
     return fail(MALA_ERR_INVALID_ARG, "null tensor argument");
   int st = check_common(B, Hq, Hkv, Nq, Nk, D, causal, scale, tau);
+  if (!st) st = check_slice_range(Nk, D);
   if (st) return st;
   const size_t need = mala_bwd_workspace_size(B, Hq, Hkv, Nq, Nk, D);
   if (!workspace || workspace_bytes < need)

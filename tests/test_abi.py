@@ -79,6 +79,7 @@ def _fwd(lib, **kw):
     (dict(scale=float("inf")), mala.MALA_ERR_INVALID_ARG),
     (dict(D=96), mala.MALA_ERR_UNSUPPORTED),
     (dict(causal=0), mala.MALA_ERR_UNSUPPORTED),
+    (dict(Nq=64, Nk=1 << 24), mala.MALA_ERR_UNSUPPORTED),   # Nk x D x 2 bytes reach 2^32
 ])
 def test_fwd_rejects_invalid_arguments(lib, kw, status):
     assert _fwd(lib, **kw) == status
