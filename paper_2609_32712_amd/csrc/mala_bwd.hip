@@ -534,6 +534,9 @@ __global__ __launch_bounds__(kDqWaves * 64) void mala_bwd_dq_kernel(BwdParams p)
   // this lane's row vectors: base-2 lse, test threshold, D_q
   float lse2, thr, dvq;
   row_vectors(p, bh, (long)qrow, off, &lse2, &thr, &dvq);
+  f32x16 negd;
+#pragma unroll
+  for (int r = 0; r < 16; ++r) negd[r] = -dvq;
 
   f32x16 acc[DB];
 #pragma unroll
@@ -615,10 +618,13 @@ __global__ __launch_bounds__(kDqWaves * 64) void mala_bwd_dq_kernel(BwdParams p)
       bf16x8 vop[KS];
 #pragma unroll
       for (int kk = 0; kk < KS; ++kk) vop[kk] = load8(vr + sub * kBk * (D + 8) + rd_step<D>(kk));
-      const f32x16 dp = qk_tile<KS>(vop, ob);
+      // dP^T - D: the accumulator starts at -D_q (one row per lane)
+      f32x16 dpd = negd;
+#pragma unroll
+      for (int kk = 0; kk < KS; ++kk) dpd = mfma32(vop[kk], ob[kk], dpd);
       float dsv[16];
 #pragma unroll
-      for (int r = 0; r < 16; ++r) dsv[r] = sv[r] * (dp[r] - dvq);
+      for (int r = 0; r < 16; ++r) dsv[r] = sv[r] * dpd[r];
       // dQ runs this tile without dS's lo term while this row's sum of |dS| over
       // such tiles stays within kLoMassDq (for every row of the wavefront)
       float as = 0.f;
