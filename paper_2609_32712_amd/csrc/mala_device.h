@@ -125,10 +125,6 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, ui
   return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes,
                                            0x00020000);
 }
-__device__ __forceinline__ bf16x8 buf_load8(__amdgpu_buffer_rsrc_t r, uint32_t byte_off) {
-  typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
-  return __builtin_bit_cast(bf16x8, __builtin_amdgcn_raw_buffer_load_b128(r, byte_off, 0, 0));
-}
 __device__ __forceinline__ float buf_load1(__amdgpu_buffer_rsrc_t r, uint32_t byte_off) {
   return __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(r, byte_off, 0, 0));
 }
@@ -201,10 +197,6 @@ __device__ __forceinline__ void wait_vm() { wait_vm_keep<0>(); }
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 __device__ __forceinline__ float fast_log2(float x) { return __builtin_amdgcn_logf(x); }
 
-// Orders LDS traffic inside one wavefront: waits for its outstanding LDS
-// operations and keeps the compiler from moving memory accesses across.
-__device__ __forceinline__ void wave_lds_sync() { asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory"); }
-
 __device__ __forceinline__ bool wave_any(bool p) { return __builtin_amdgcn_ballot_w64(p) != 0; }
 
 __device__ __forceinline__ bf16x8 zero8() {
@@ -216,14 +208,6 @@ __device__ __forceinline__ bf16x8 zero8() {
 
 __device__ __forceinline__ bf16x8 load8(const bf16* p) { return *reinterpret_cast<const bf16x8*>(p); }
 __device__ __forceinline__ void store8(bf16* p, bf16x8 v) { *reinterpret_cast<bf16x8*>(p) = v; }
-
-// fp32 -> bf16 round-to-nearest-even for 8 values.
-__device__ __forceinline__ bf16x8 to_bf16x8(const float* x) {
-  bf16x8 r;
-#pragma unroll
-  for (int i = 0; i < 8; ++i) r[i] = (bf16)x[i];
-  return r;
-}
 
 // Two-term bf16 split of fp32 values: x ~= hi + lo with |x - hi - lo| <= 2^-16 |x|.
 // The post-score products (P V, P^T dO, dS^T Q, dS K) run as two MFMAs, one per
