@@ -436,15 +436,33 @@ __global__ __launch_bounds__(1024) void mala_bwd_dkdv_kernel(BwdParams p) {
       // the decision of tile it - 2 is known since the end of iteration it - 2: it
       // is read one iteration early, off the critical path
       int fl3 = 0;
+      // the Q^T operands of the next iteration's tile, read at the end of this one
+      bf16x8 a[DB][2];
+      auto load_a = [&](int tt) {
+        const bf16* ab = lds_pin(Qs + (tt & 3) * TS + tro);
+#pragma unroll
+        for (int db = 0; db < DB; ++db)
+#pragma unroll
+          for (int ks = 0; ks < 2; ++ks) {
+            const bf16* at = ab + 16 * ks * (D + 8) + tr_step<D>(db);
+            a[db][ks] = cat(lds_read_tr(at), lds_read_tr(at + 8 * (D + 8)));
+          }
+      };
+      auto acc_a = [&](bf16x8 b0, bf16x8 b1) {
+#pragma unroll
+        for (int db = 0; db < DB; ++db)
+#pragma unroll
+          for (int ks = 0; ks < 2; ++ks) acc[db] = mfma32(a[db][ks], ks ? b1 : b0, acc[db]);
+      };
       for (int it = 0; it < n_it; ++it) {
         const int t = it - 2;
         if (fl3) {
-          const bf16* atb = Qs + (t & 3) * TS + tro;
-          accumulate(atb, dSop[t & 1][grp_k][0][lane], dSop[t & 1][grp_k][1][lane]);
-          if (dSlo[t & 1][grp_k]) accumulate(atb, dSop[t & 1][grp_k][2][lane], dSop[t & 1][grp_k][3][lane]);
+          acc_a(dSop[t & 1][grp_k][0][lane], dSop[t & 1][grp_k][1][lane]);
+          if (dSlo[t & 1][grp_k]) acc_a(dSop[t & 1][grp_k][2][lane], dSop[t & 1][grp_k][3][lane]);
         }
         const int tn = it - 1;   // the tile of the next iteration
         fl3 = (tn >= 0 && tn < total) ? Pflag[tn % 3][grp_k] : 0;
+        if (fl3) load_a(tn);
         __syncthreads();
       }
     }
