@@ -41,6 +41,8 @@ TRAIN_CASES = {
     "tiny_d128": dict(spec=dict(kind="train", B=1, Hq=2, Hkv=2, N=37, D=128, beta=2.0, local=1.0),
                       over={}),
     "single_row_d64": dict(spec=dict(kind="train", B=1, Hq=1, Hkv=1, N=1, D=64, beta=1.0), over={}),
+    # the language-model-like supplementary workload (config 6) at a small size
+    "lm_d128_ragged": dict(spec=6, over=dict(N=1000, Hq=4, Hkv=2)),
 }
 TRAIN_TAUS = {
     "cfg1": (0.0, 1e-4, 1e-3),
@@ -50,6 +52,7 @@ TRAIN_TAUS = {
     # tau = 1 would put the only tile exactly on the threshold (P = 1 = tau / L):
     # 0.5 retains and 1.5 skips it in the backward, both unambiguously
     "single_row_d64": (0.0, 0.5, 1.5),
+    "lm_d128_ragged": (0.0, 1e-4, 1.0),
 }
 
 

@@ -15,6 +15,10 @@ stand in for both.  Recipe (identical for every configuration):
   * planted-needle queries: Q_i = g_i + beta * K_{r(i)} with g ~ N(0, 1) and
     r(i) uniform on {0..i}, built from the ROUNDED K of the head's KV head and
     rounded again; optional local term Q_i += alpha * K_{i-1};
+  * language-model-like structure (options of the same generator): needles shared
+    by blocks of rows (rows of block c draw one r(c), uniform on {0 .. first row of
+    the block}), an attention sink (Q_i += sink * K_0), and a Rademacher dO probe
+    (entries +-1 with equal probability);
   * decode queries: q = g + beta * sum of K at 4 distinct random positions.
 
 Arrays are returned as uint16 bf16 bit patterns in [B, H, N, D] layout.
@@ -42,6 +46,12 @@ CONFIGS = {
             taus=(0.0, 1e-4), desc="causal fwd+bwd, GQA 8/2 (one TP=8 share), 131072x128, beta=2"),
     5: dict(kind="decode", B=16, Hq=32, Hkv=8, N=131072, D=128, beta=3.0, needles=4,
             taus=(0.0, 1e-4), desc="decode, 16 x GQA 32/8 over 131072-token caches, 4 needles beta=3"),
+    # supplementary: a workload on which the forward rule can skip (a dominant local
+    # key found in the diagonal tile, needles shared by 32-row blocks, a sink), with
+    # a Rademacher dO for the fidelity measurements
+    6: dict(kind="train", B=1, Hq=8, Hkv=2, N=32768, D=128, beta=2.0, local=2.0,
+            needle_block=32, sink=1.5, do="rademacher", taus=(0.0, 1e-4, 1.0),
+            desc="causal fwd+bwd, GQA 8/2, 32768x128, LM-like: local 2, block needles beta=2, sink 1.5"),
 }
 
 
@@ -120,6 +130,9 @@ class Workload:
         return _normal_bits(self.seed, self.cfg_id, _T_V, b, hkv, (self.N, self.D))
 
     def do_head(self, b, h):
+        if self.spec.get("do") == "rademacher":
+            rng = _rng(self.seed, self.cfg_id, _T_DO, b, h)
+            return bf16_round(rng.integers(0, 2, size=(self.N, self.D)) * 2.0 - 1.0)
         return _normal_bits(self.seed, self.cfg_id, _T_DO, b, h, (self.N, self.D))
 
     def beta(self, h):
@@ -141,12 +154,31 @@ class Workload:
             return bf16_round(g + beta * kf[pos].sum(axis=0))
         N = self.N
         g = rng.standard_normal((N, self.D), dtype=np.float32).astype(np.float64)
-        r = rng.integers(0, np.arange(1, N + 1))        # r(i) uniform on {0..i}
+        nb = int(self.spec.get("needle_block", 1))
+        if nb > 1:   # one needle per block of nb rows, visible to all of them
+            starts = np.arange(0, N, nb)
+            r = np.repeat(rng.integers(0, starts + 1), nb)[:N]
+        else:
+            r = rng.integers(0, np.arange(1, N + 1))    # r(i) uniform on {0..i}
         q = g + beta * kf[r]
         alpha = float(self.spec.get("local", 0.0))
         if alpha:
             q[1:] += alpha * kf[:-1]
+        sink = float(self.spec.get("sink", 0.0))
+        if sink:
+            q += sink * kf[0]
         return bf16_round(q)
+
+    def needle_rows(self, b, h):
+        """Training only: the key r(i) planted in each query row of head (b, h)."""
+        rng = _rng(self.seed, self.cfg_id, _T_Q, b, h)
+        N = self.N
+        rng.standard_normal((N, self.D), dtype=np.float32)
+        nb = int(self.spec.get("needle_block", 1))
+        if nb > 1:
+            starts = np.arange(0, N, nb)
+            return np.repeat(rng.integers(0, starts + 1), nb)[:N]
+        return rng.integers(0, np.arange(1, N + 1))
 
     def needle_positions(self, b, h):
         """Decode only: the planted positions of query head (b, h)."""
