@@ -39,15 +39,15 @@ def log(*a):
 class Train:
     """Device-resident inputs, outputs and workspace of one fwd+bwd workload."""
 
-    def __init__(self, cfg_id, tau):
+    def __init__(self, cfg_id, tau, **over):
         import torch
         import paper_2609_32712_amd as mala
         from workloads import Workload
-        self.w = Workload(cfg_id)
+        self.w = Workload(cfg_id, **over)
         self.tau = tau
         t0 = time.time()
         t = self.w.tensors(threads=16)
-        log("cfg%d inputs generated in %.1fs" % (cfg_id, time.time() - t0))
+        log("cfg%d %s inputs generated in %.1fs" % (cfg_id, over or "", time.time() - t0))
         dev = lambda b: torch.from_numpy(b.view(np.int16)).to("cuda").view(torch.bfloat16)
         self.q, self.k, self.v, self.do = (dev(t[x]) for x in ("q", "k", "v", "do"))
         del t
@@ -78,6 +78,9 @@ class Train:
 
     def counters(self):
         return self.cnt_f.cpu().numpy(), self.cnt_b.cpu().numpy()
+
+    def outputs(self):
+        return {k: getattr(self, k).clone() for k in ("o", "lse", "dq", "dk", "dv")}
 
 
 class Decode:
@@ -137,6 +140,93 @@ def train_flops(cnt_f, cnt_b, D, bq, bk):
 def dense_equivalent_flops(B, Hq, N, D):
     pairs = B * Hq * N * (N + 1) / 2
     return pairs * 4 * D, pairs * 10 * D
+
+
+def head_fidelity(ref, out):
+    """Operator fidelity of one run against the screening-disabled run (tau = 0) of
+    the same operator on the same inputs, per head, following the operator-fidelity
+    protocol of the experiments section and its appendix:
+      * relative L2 error ||X - X_ref|| / ||X_ref|| of O and dQ per query head and of
+        dK and dV per KV head (the norms run over one head's N x d block);
+      * the dense softmax mass omitted by each query row, recovered from the two
+        normalizers as 1 - exp(lse - lse_ref) (Z_R / (Z_R + Z_O) = exp(lse - lse_ref)),
+        averaged over the rows of each query head; also the largest row value.
+    ref, out: dicts of tensors o, dq [B, Hq, N, d], dk, dv [B, Hkv, N, d], lse [B, Hq, N]
+    (any device).  Returns numpy arrays (fractions, not percent)."""
+    import torch
+
+    def rel(k):
+        a, b = ref[k].double(), out[k].double()
+        num = torch.linalg.vector_norm((b - a).flatten(2), dim=2)
+        den = torch.linalg.vector_norm(a.flatten(2), dim=2)
+        return (num / den).flatten().cpu().numpy()
+
+    eps = omitted_mass_rows(ref["lse"], out["lse"])
+    res = {k: rel(k) for k in ("o", "dq", "dk", "dv")}
+    res["omitted_mass"] = eps.mean(dim=2).flatten().cpu().numpy()
+    res["omitted_mass_row_max"] = float(eps.max())
+    return res
+
+
+def omitted_mass_rows(lse_ref, lse):
+    """Dense softmax mass a row omits, from the screened and the screening-disabled
+    normalizers: 1 - Z_R / (Z_R + Z_O) = -expm1(lse - lse_ref), in float64."""
+    import torch
+    return -torch.expm1(lse.double() - lse_ref.double())
+
+
+def mean_p95(x):
+    """Mean and 95th percentile (linear interpolation) over head-level measurements."""
+    x = np.asarray(x, dtype=np.float64)
+    return float(x.mean()), float(np.percentile(x, 95))
+
+
+LM_SWEEP_N = (1024, 2048, 4096, 8192, 16384, 32768)
+LM_SWEEP_TOKENS = 32768        # batch = tokens / N, so every length has the same token count
+LM_SWEEP_TAUS = (1e-4, 1.0)
+
+
+def lm_sweep(reps, lengths=LM_SWEEP_N):
+    """The language-model-like workload (8 query / 2 KV heads, head_dim 128) at context
+    lengths 1K..32K: fwd/bwd time and retained work at tau = 0, 1e-4 and the canonical
+    tau = 1, and the operator fidelity of tau > 0 against tau = 0 (same kernels)."""
+    import torch
+    rows = []
+    for N in lengths:
+        tr = Train(6, 0.0, N=N, B=max(1, LM_SWEEP_TOKENS // N))
+        w = tr.w
+        nrows = w.B * w.Hq * w.N
+        runs = {}
+        for t_ in (0.0,) + LM_SWEEP_TAUS:
+            f = time_calls(lambda: tr.fwd(t_), reps, 1)
+            b = time_calls(lambda: tr.bwd(t_), reps, 1)
+            cf, cb = tr.counters()
+            runs[t_] = dict(fwd=f[0], bwd=b[0], cf=cf, cb=cb, out=tr.outputs())
+        d = runs[0.0]
+        row = {"N": N, "batch": w.B, "q_heads": w.B * w.Hq, "kv_heads": w.B * w.Hkv,
+               "dense_fwd_ms": round(d["fwd"], 4), "dense_bwd_ms": round(d["bwd"], 4)}
+        for t_ in LM_SWEEP_TAUS:
+            r = runs[t_]
+            fid = head_fidelity(d["out"], r["out"])
+            pc = lambda x: [round(100 * v, 5) for v in mean_p95(x)]
+            row["tau=%g" % t_] = {
+                "fwd_ms": round(r["fwd"], 4), "bwd_ms": round(r["bwd"], 4),
+                "speedup_fwd": round(d["fwd"] / r["fwd"], 4),
+                "speedup_bwd": round(d["bwd"] / r["bwd"], 4),
+                "retained_tiles_pct_fwd": round(100.0 * r["cf"][1] / r["cf"][0], 3),
+                "retained_tiles_pct_bwd": round(100.0 * r["cb"][1] / r["cb"][0], 3),
+                "mean_slots_per_query_fwd": round(float(r["cf"][3]) / nrows, 1),
+                "mean_slots_per_query_bwd": round(float(r["cb"][3]) / nrows, 1),
+                "omitted_mass_pct_mean_p95": pc(fid["omitted_mass"]),
+                "omitted_mass_pct_row_max": round(100 * fid["omitted_mass_row_max"], 5),
+                "rel_l2_pct_mean_p95": {k: pc(fid[k]) for k in ("o", "dq", "dk", "dv")},
+            }
+        log("lm N=%d B=%d dense fwd %.3f bwd %.3f | tau=1 fwd %.3f bwd %.3f ms" % (
+            N, w.B, d["fwd"], d["bwd"], runs[1.0]["fwd"], runs[1.0]["bwd"]))
+        rows.append(row)
+        del tr, runs, d
+        torch.cuda.empty_cache()
+    return rows
 
 
 def source_sha(path):
@@ -216,7 +306,8 @@ COUNTER_CMD = ("cd /tmp && export TMPDIR=/tmp && timeout -s KILL 180 rocprofv3 -
                "python $REPO/bench.py --counter-pass")
 TRACE_CMD = ("cd /tmp && export TMPDIR=/tmp && timeout -k 10 600 rocprofv3 --kernel-trace --stats "
              "--output-format csv -d $REPO/gpurun_out/trace_bench -o bench -- "
-             "python $REPO/bench.py --steps 2 --warmup 1 --reps 2 --no-cpu-baseline --no-32k")
+             "python $REPO/bench.py --steps 2 --warmup 1 --reps 2 --no-cpu-baseline --no-32k "
+             "--no-lm")
 
 
 def counter_pass():
@@ -343,7 +434,8 @@ def summarize_mfma(csv_path):
     with open(csv_path) as fh:
         for r in csv.DictReader(fh):
             d = r["Dispatch_Id"]
-            per[d][r["Counter_Name"]] = per[d].get(r["Counter_Name"], 0.0) + float(r["Counter_Value"])
+            c = r["Counter_Name"]
+            per[d][c] = per[d].get(c, 0.0) + float(r["Counter_Value"])
             names[d] = r["Kernel_Name"]
     by = collections.defaultdict(list)
     for d, v in per.items():
@@ -352,7 +444,8 @@ def summarize_mfma(csv_path):
     cmd = COUNTER_CMD.format(c="MfmaUtil MfmaFlopsBF16", d="mfma")
     lines = ["# MFMA utilisation of the 131072-token fwd + bwd kernels", "",
              "Command (from the repository root on one MI355X; `$REPO` is that root):", "",
-             "```", cmd, "python bench.py --summarize-mfma gpurun_out/pmc_mfma/run_counter_collection.csv",
+             "```", cmd,
+             "python bench.py --summarize-mfma gpurun_out/pmc_mfma/run_counter_collection.csv",
              "```", "",
              "`MfmaUtil` = MFMA-busy cycles summed over SIMDs / (active cycles x SIMDs), %; "
              "`MfmaFlopsBF16` = executed bf16 MFMA flops per dispatch (the hi/lo split and "
@@ -377,6 +470,8 @@ def main():
     ap.add_argument("--reps", type=int, default=5, help="event-timed calls per kernel and tau")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-32k", action="store_true")
+    ap.add_argument("--no-lm", action="store_true",
+                    help="skip the language-model-like tau = 1 timing and fidelity sweep")
     ap.add_argument("--counter-pass", action="store_true",
                     help="run only the program profiled for the traffic counters")
     ap.add_argument("--summarize-counters", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"))
@@ -499,19 +594,35 @@ def main():
     if not args.no_32k:
         t3 = Train(3, tau)
         r3 = {}
-        for name, t_ in (("tau", tau), ("dense", 0.0)):
+        for name, t_ in (("tau", tau), ("dense", 0.0), ("tau1", 1.0)):
             r3[name] = (time_calls(lambda: t3.fwd(t_), args.reps, 1),
                         time_calls(lambda: t3.bwd(t_), args.reps, 1), t3.counters())
         (f3, b3, (cf3, cb3)), (f3d, b3d, _) = r3["tau"], r3["dense"]
+        f31, b31, (cf31, cb31) = r3["tau1"]
         detail["32k"] = {
             "fwd_ms": round(f3[0], 3), "bwd_ms": round(b3[0], 3),
             "dense_fwd_ms": round(f3d[0], 3), "dense_bwd_ms": round(b3d[0], 3),
             "speedup_fwd": round(f3d[0] / f3[0], 4), "speedup_bwd": round(b3d[0] / b3[0], 4),
             "retained_tiles_pct_fwd": pct(cf3[1], cf3[0]),
             "retained_tiles_pct_bwd": pct(cb3[1], cb3[0]),
+            "tau1_supplementary": {
+                "fwd_ms": round(f31[0], 3), "bwd_ms": round(b31[0], 3),
+                "speedup_fwd": round(f3d[0] / f31[0], 4),
+                "speedup_bwd": round(b3d[0] / b31[0], 4),
+                "retained_tiles_pct_fwd": pct(cf31[1], cf31[0]),
+                "retained_tiles_pct_bwd": pct(cb31[1], cb31[0]),
+            },
         }
         del t3
         torch.cuda.empty_cache()
+    if not args.no_lm:
+        detail["lm_like_sweep"] = {
+            "note": ("supplementary: language-model-like inputs (local key alpha=2, needles "
+                     "shared by 32-row blocks beta=2, sink 1.5, Rademacher dO), 8 query / 2 KV "
+                     "heads, head_dim 128, batch = 32768 / N; fidelity of tau > 0 against "
+                     "tau = 0 through the same kernels: mean and P95 over heads, in percent"),
+            "rows": lm_sweep(args.reps),
+        }
 
     line = {
         "metric": METRIC,

@@ -122,6 +122,56 @@ def test_forward_skips_are_exercised():
     assert cb[1] <= cf[1]
 
 
+def test_fidelity_measurement_matches_oracle():
+    # The fidelity figures the benchmark reports (per-head relative L2 errors of
+    # tau = 1 against tau = 0, and the omitted mass from the two normalizers),
+    # measured through the kernels, equal the oracle's within the kernels' own error.
+    import bench
+    tau = 1.0
+    w, q, k, v, do = _train_case("lm_d128_ragged", tau)
+    scale = f32(w.scale)
+    bq, bk = mala.mala_geometry(w.D, mala.PASS_FWD)
+    qf, kf, vf, dof = map(bf16_to_f64, (q, k, v, do))
+    Q, K, V, DO = map(dev, (q, k, v, do))
+    ro, rg, ties = {}, {}, None
+    for t in (0.0, tau):
+        of = oracle.mala_fwd(qf, kf, vf, scale, f32(t), bq, bk)
+        ob = oracle.mala_bwd(qf, kf, vf, of["o"], of["lse"], dof, scale, f32(t), bq, bk)
+        ro[t] = {x: torch.from_numpy(np.ascontiguousarray(y)) for x, y in
+                 (("o", of["o"]), ("lse", of["lse"]), ("dq", ob["dq"]), ("dk", ob["dk"]),
+                  ("dv", ob["dv"]))}
+        g = mala.fwd(Q, K, V, scale, t)
+        gb = mala.bwd(Q, K, V, g["o"], g["lse"], DO, scale, t)
+        rg[t] = {"o": g["o"], "lse": g["lse"], "dq": gb["dq"], "dk": gb["dk"], "dv": gb["dv"]}
+        if t > 0:
+            ties = exempt_rows(t, of["tie_abs"])
+    torch.cuda.synchronize()
+    rg = {t: {x: y.cpu().double() for x, y in r.items()} for t, r in rg.items()}
+    fo = bench.head_fidelity(ro[0.0], ro[tau])
+    fg = bench.head_fidelity(rg[0.0], rg[tau])
+    # omitted mass per row: eps = -expm1(lse_t - lse_0) moves by at most the change of
+    # the difference, so twice the largest LSE deviation bounds it (tie rows aside)
+    delta = max(float((rg[t]["lse"] - ro[t]["lse"]).abs().max()) for t in ro)
+    eo = bench.omitted_mass_rows(ro[0.0]["lse"], ro[tau]["lse"]).numpy()
+    eg = bench.omitted_mass_rows(rg[0.0]["lse"], rg[tau]["lse"]).numpy()
+    dev_rows = np.abs(eg - eo)[~ties]
+    print("[fidelity] omitted mass: oracle mean %.3e max %.3e | |gpu-oracle| max %.3e "
+          "(bound %.3e, %d tie rows)" % (eo.mean(), eo.max(), dev_rows.max(), 2 * delta,
+                                         int(ties.sum())), flush=True)
+    assert eo.max() > 0
+    assert dev_rows.max() <= 2 * delta + 1e-12
+    # per-head relative L2: by the triangle inequality the two measurements differ by
+    # at most (e_tau + e_0 (1 + r)) / ||X_0||, e_t = ||X_t(gpu) - X_t(oracle)|| per head
+    for x in ("o", "dq", "dk", "dv"):
+        norm = lambda a: torch.linalg.vector_norm(a.flatten(2), dim=2).flatten().numpy()
+        e_t, e_0 = (norm(rg[t][x] - ro[t][x]) for t in (tau, 0.0))
+        bound = (e_t + e_0 * (1 + fo[x])) / norm(rg[0.0][x])
+        print("[fidelity] rel-L2 %-2s oracle mean %.3e%% | gpu mean %.3e%% | kernel-error "
+              "bound mean %.3e%%" % (x, 100 * fo[x].mean(), 100 * fg[x].mean(),
+                                      100 * bound.mean()), flush=True)
+        assert (np.abs(fg[x] - fo[x]) <= bound * (1 + 1e-9) + 1e-15).all(), x
+
+
 DECODE_CASES = [
     (dict(kind="decode", B=2, Hq=8, Hkv=2, N=3001, D=128, beta=3.0, needles=4), 1, 0.0),
     (dict(kind="decode", B=2, Hq=8, Hkv=2, N=3001, D=128, beta=3.0, needles=4), 4, 1e-4),
@@ -237,6 +287,11 @@ def test_full_config3_sampled(tau):
 @pytest.mark.parametrize("tau", [1e-4, 1.0])
 def test_full_config4_sampled(tau):
     _full_train(4, tau, _blocks(0.25, 0.999), heads=[(0, 6)], kv_head_tail=(0, 1))
+
+
+@pytest.mark.parametrize("tau", [1e-4, 1.0])
+def test_full_config6_sampled(tau):
+    _full_train(6, tau, _blocks(0.3, 0.999), heads=[(0, 2), (0, 7)], kv_head_tail=(0, 1))
 
 
 @pytest.mark.parametrize("tau", [0.0, 1e-4, 1.0])
