@@ -106,9 +106,19 @@ class Decode:
         self.scale = float(np.float32(w.scale))
         self.mala = mala
 
-    def run(self, tau):
+    def run(self, tau, cache_lens=None):
         self.mala.mala_decode(self.q, self.k, self.v, self.o, self.lse, self.ht, self.cnt,
-                              self.splits, self.ws, self.scale, tau)
+                              self.splits, self.ws, self.scale, tau, cache_lens=cache_lens)
+
+
+def ragged_lengths(B, N, seed=7):
+    """Valid cache lengths of a serving batch: uniform on [1, N], the first sequence
+    full and the second holding one token."""
+    lens = np.random.default_rng(seed).integers(1, N + 1, size=B).astype(np.int32)
+    lens[0] = N
+    if B > 1:
+        lens[1] = 1
+    return lens
 
 
 def time_calls(fn, reps, warmup):
@@ -539,6 +549,12 @@ def main():
     cf1, cb1 = tr.counters()
     cd1 = dec.cnt.cpu().numpy()
     log("tau=1 fwd %.2f bwd %.2f decode %.3f ms" % (f1[0], b1[0], d1[0]))
+    # supplementary: the same decode batch with ragged valid cache lengths
+    lens = ragged_lengths(dec.w.B, dec.w.N)
+    cl = torch.from_numpy(lens).to("cuda")
+    dr = time_calls(lambda: dec.run(tau, cl), args.reps, 1)
+    cdr = dec.cnt.cpu().numpy()
+    drd = time_calls(lambda: dec.run(0.0, cl), args.reps, 1)
     rt, rd = res["tau"], res["dense"]
     fl_f, fl_b = train_flops(rt["cf"], rt["cb"], w.D, bq, bk)
     de_f, de_b = dense_equivalent_flops(w.B, w.Hq, w.N, w.D)
@@ -548,6 +564,9 @@ def main():
     cd = rt["cd"]
     dec_bytes = kv_bytes + kv_bytes * cd[2] / max(1, cd[0] / dec.w.g)
     pct = lambda a, b_: round(100.0 * float(a) / max(1.0, float(b_)), 3)
+    # K of every valid key, V of the tiles loaded (counted once per GQA group)
+    rag_kv = float(lens.sum()) * dec.w.Hkv * dec.w.D * 2
+    rag_bytes = rag_kv + rag_kv * cdr[2] / max(1, cdr[0] / dec.w.g)
 
     detail = {
         "128k": {
@@ -574,6 +593,14 @@ def main():
             "v_tiles_loaded_pct": pct(cd[2], cd[0] / dec.w.g),
             "hbm_gbs_algorithmic": round(dec_bytes / (rt["dec"][0] * 1e-3) / 1e9, 1),
             "hbm_frac": round(dec_bytes / (rt["dec"][0] * 1e-3) / 1e9 / PEAK_HBM_GBS, 4),
+            "ragged_lengths_supplementary": {
+                "lens": "uniform on [1, %d], seed 7, first full, second 1 token; total %d"
+                        % (dec.w.N, int(lens.sum())),
+                "ms": round(dr[0], 4), "dense_ms": round(drd[0], 4),
+                "speedup": round(drd[0] / dr[0], 4),
+                "retained_head_tiles_pct": pct(cdr[1], cdr[0]),
+                "hbm_gbs_algorithmic": round(rag_bytes / (dr[0] * 1e-3) / 1e9, 1),
+            },
         },
         "decision_tile": [bq, bk],
         "tau1_supplementary": {

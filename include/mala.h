@@ -142,18 +142,23 @@ size_t mala_decode_workspace_size(int B, int Hq, int D, int num_splits);
  * MALA split-KV decode of one new query token per (batch, query head) against a
  * KV cache of Nk tokens that already includes the token's own key/value.
  *   q: bf16 [B, Hq, D]; k_cache, v_cache: bf16 [B, Hkv, Nk, D]
+ *   cache_lens: int32 [B] device array or NULL: sequence b's cache holds n_b valid
+ *       tokens (rows [0, n_b) of k_cache[b] and v_cache[b]; the rest is not read),
+ *       its query sees them all (L = n_b) and its ceil(n_b / B_k) key tiles are cut
+ *       into the splits as below.  Values are clamped into [0, Nk]; a sequence with
+ *       n_b = 0 gets o = 0 and lse = -inf.  NULL means n_b = Nk for every sequence.
  *   o: fp32 [B, Hq, D] out; lse: fp32 [B, Hq] out
  *   head_tiles: int32 [B, Hq] or NULL out (retained tiles summed over splits)
  *   counters: int64 [4] or NULL out
- *   num_splits >= 1: the key tiles (ceil(Nk / B_k) of them) are cut into
- *   num_splits contiguous ranges of ceil(T / num_splits) tiles; each range starts
- *   from an empty normalizer, so the retained set depends on num_splits.
+ *   num_splits >= 1: a sequence's key tiles (T = ceil(n_b / B_k) of them) are cut
+ *   into num_splits contiguous ranges of ceil(T / num_splits) tiles; each range
+ *   starts from an empty normalizer, so the retained set depends on num_splits.
  *   workspace: at least mala_decode_workspace_size(...) bytes.
  */
-int mala_decode(const void* q, const void* k_cache, const void* v_cache, float* o, float* lse,
-                int32_t* head_tiles, int64_t* counters, int num_splits, void* workspace,
-                size_t workspace_bytes, int B, int Hq, int Hkv, int Nk, int D, float scale,
-                float tau, void* stream);
+int mala_decode(const void* q, const void* k_cache, const void* v_cache,
+                const int32_t* cache_lens, float* o, float* lse, int32_t* head_tiles,
+                int64_t* counters, int num_splits, void* workspace, size_t workspace_bytes,
+                int B, int Hq, int Hkv, int Nk, int D, float scale, float tau, void* stream);
 
 #ifdef __cplusplus
 }

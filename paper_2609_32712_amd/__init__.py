@@ -64,7 +64,7 @@ def load_library():
     lib.mala_bwd.restype = i
     lib.mala_decode_workspace_size.argtypes = [i] * 4
     lib.mala_decode_workspace_size.restype = sz
-    lib.mala_decode.argtypes = [vp] * 7 + [i, vp, sz] + [i] * 5 + [f, f, vp]
+    lib.mala_decode.argtypes = [vp] * 8 + [i, vp, sz] + [i] * 5 + [f, f, vp]
     lib.mala_decode.restype = i
     _lib = lib
     return lib
@@ -144,15 +144,19 @@ def mala_bwd(q, k, v, o, lse, dout, dq, dk, dv, row_tiles, counters, workspace, 
 
 
 def mala_decode(q, k_cache, v_cache, o, lse, head_tiles, counters, num_splits, workspace, scale,
-                tau, stream=None):
+                tau, stream=None, cache_lens=None):
     _dev(q, torch.bfloat16, "q", 3), _dev(k_cache, torch.bfloat16, "k_cache", 4)
     _dev(v_cache, torch.bfloat16, "v_cache", 4), _dev(o, torch.float32, "o", 3)
     _dev(lse, torch.float32, "lse", 2)
     B, Hq, D = q.shape
     Hkv, Nk = k_cache.shape[1], k_cache.shape[2]
-    _check(load_library().mala_decode(_ptr(q), _ptr(k_cache), _ptr(v_cache), _ptr(o), _ptr(lse),
-                                      _ptr(head_tiles), _ptr(counters), num_splits,
-                                      _ptr(workspace),
+    if cache_lens is not None:
+        _dev(cache_lens, torch.int32, "cache_lens", 1)
+        if cache_lens.shape[0] != B:
+            raise ValueError("cache_lens must have one entry per sequence (%d)" % B)
+    _check(load_library().mala_decode(_ptr(q), _ptr(k_cache), _ptr(v_cache), _ptr(cache_lens),
+                                      _ptr(o), _ptr(lse), _ptr(head_tiles), _ptr(counters),
+                                      num_splits, _ptr(workspace),
                                       workspace.numel() * workspace.element_size(), B, Hq, Hkv,
                                       Nk, D, scale, tau, _stream(stream)))
 
@@ -183,7 +187,10 @@ def bwd(q, k, v, o, lse, dout, scale, tau, stats=True, workspace=None, stream=No
     return dict(dq=dq, dk=dk, dv=dv, row_tiles=rt, counters=cnt)
 
 
-def decode(q, k_cache, v_cache, scale, tau, num_splits, stats=True, workspace=None, stream=None):
+def decode(q, k_cache, v_cache, scale, tau, num_splits, stats=True, workspace=None, stream=None,
+           cache_lens=None):
+    """cache_lens: optional int32 [B] device tensor of valid cache tokens per sequence
+    (keys [0, n_b) of k_cache[b] / v_cache[b]); None means every sequence holds Nk."""
     B, Hq, D = q.shape
     o = torch.empty((B, Hq, D), dtype=torch.float32, device=q.device)
     lse = torch.empty((B, Hq), dtype=torch.float32, device=q.device)
@@ -193,7 +200,7 @@ def decode(q, k_cache, v_cache, scale, tau, num_splits, stats=True, workspace=No
         n = mala_decode_workspace_size(B, Hq, D, num_splits)
         workspace = torch.empty(max(n, 16), dtype=torch.uint8, device=q.device)
     mala_decode(q, k_cache, v_cache, o, lse, ht, cnt, num_splits, workspace, scale, tau,
-                stream=stream)
+                stream=stream, cache_lens=cache_lens)
     return dict(o=o, lse=lse, head_tiles=ht, counters=cnt)
 
 

@@ -163,10 +163,10 @@ size_t mala_decode_workspace_size(int B, int Hq, int D, int num_splits) {
   return round_up((size_t)B * Hq * num_splits * (D + mala::kDecStride) * sizeof(float), 256);
 }
 
-int mala_decode(const void* q, const void* k_cache, const void* v_cache, float* o, float* lse,
-                int32_t* head_tiles, int64_t* counters, int num_splits, void* workspace,
-                size_t workspace_bytes, int B, int Hq, int Hkv, int Nk, int D, float scale,
-                float tau, void* stream) {
+int mala_decode(const void* q, const void* k_cache, const void* v_cache,
+                const int32_t* cache_lens, float* o, float* lse, int32_t* head_tiles,
+                int64_t* counters, int num_splits, void* workspace, size_t workspace_bytes,
+                int B, int Hq, int Hkv, int Nk, int D, float scale, float tau, void* stream) {
   g_err[0] = 0;
   if (!q || !k_cache || !v_cache || !o || !lse)
     return fail(MALA_ERR_INVALID_ARG, "null q, k_cache, v_cache, o or lse");
@@ -189,6 +189,7 @@ int mala_decode(const void* q, const void* k_cache, const void* v_cache, float* 
   p.q = (const __bf16*)q;
   p.k = (const __bf16*)k_cache;
   p.v = (const __bf16*)v_cache;
+  p.lens = cache_lens;
   p.part = (float*)workspace;
   p.counters = (unsigned long long*)counters;
   p.B = B; p.Hq = Hq; p.Hkv = Hkv; p.Nk = Nk;
@@ -197,6 +198,7 @@ int mala_decode(const void* q, const void* k_cache, const void* v_cache, float* 
   p.tps = (T + num_splits - 1) / num_splits;
   p.scale2 = scale * mala::kLog2e;
   p.thr2 = log2_tau(tau) - log2f((float)Nk);
+  p.log2tau = log2_tau(tau);
   if ((e = mala::launch_decode(p, D, s)) != hipSuccess) return hip_fail(e, "mala_decode: split launch");
   if ((e = mala::launch_decode_combine((float*)workspace, o, lse, head_tiles, p.counters, B * Hq,
                                        num_splits, D, s)) != hipSuccess)

@@ -6,6 +6,9 @@
 // tile are read once per group.  Decode is HBM-bound: K is always read (score
 // discovery), V only when at least one head of the group retains the tile.
 //
+// With per-sequence cache lengths n_b, sequence b sees keys [0, n_b) (L = n_b) and
+// its ceil(n_b / 32) tiles are cut into the splits as for a cache of n_b tokens.
+//
 // Per 32-key tile, in descending order inside the split:
 //   S^T = K_t Q^T     2 x 4 (D = 128) MFMAs 16x16x32, K loaded straight from HBM
 //                     into the A operand; lane (g, col) holds query head col and
@@ -34,7 +37,16 @@ __global__ __launch_bounds__(64) void mala_decode_split_kernel(DecParams p) {
   const int s = blockIdx.x % p.S;
   const int bhk = blockIdx.x / p.S;
   const int b = bhk / p.Hkv, hkv = bhk % p.Hkv, grp = p.Hq / p.Hkv;
-  const int t_lo = s * p.tps, t_hi = min(p.T, t_lo + p.tps);
+  // this sequence's cache length n (clamped into [0, Nk]), its tiles and split range
+  int n = p.Nk, T = p.T, tps = p.tps;
+  float thr2 = p.thr2;
+  if (p.lens) {
+    n = min(max(p.lens[b], 0), p.Nk);
+    T = (n + kDecBk - 1) / kDecBk;
+    tps = (T + p.S - 1) / p.S;
+    thr2 = p.log2tau - log2f((float)n);   // L = n (n = 0 leaves no tile to test)
+  }
+  const int t_lo = s * tps, t_hi = min(T, t_lo + tps);
   const bool head_valid = col < grp;
   const int hq = hkv * grp + col;
 
@@ -59,8 +71,8 @@ __global__ __launch_bounds__(64) void mala_decode_split_kernel(DecParams p) {
     const long k0 = (long)t * kDecBk + col, k1 = k0 + 16;
 #pragma unroll
     for (int kk = 0; kk < KS; ++kk) {
-      ka[kk] = k0 < p.Nk ? load8(Kp + k0 * D + 32 * kk + 8 * g) : zero8();
-      kb1[kk] = k1 < p.Nk ? load8(Kp + k1 * D + 32 * kk + 8 * g) : zero8();
+      ka[kk] = k0 < n ? load8(Kp + k0 * D + 32 * kk + 8 * g) : zero8();
+      kb1[kk] = k1 < n ? load8(Kp + k1 * D + 32 * kk + 8 * g) : zero8();
     }
   };
   // V of a tile into registers (row-major chunks); written to LDS when needed
@@ -71,7 +83,7 @@ __global__ __launch_bounds__(64) void mala_decode_split_kernel(DecParams p) {
     for (int e = 0; e < VCH; ++e) {
       const int ch = lane + 64 * e;
       const int row = ch / (D / 8), c8 = (ch % (D / 8)) * 8;
-      vr[e] = kb + row < p.Nk ? load8(Vp + (kb + row) * D + c8) : zero8();
+      vr[e] = kb + row < n ? load8(Vp + (kb + row) * D + c8) : zero8();
     }
   };
   // base-2 scores of tile t for this lane's head (8 keys) and their max over the tile
@@ -87,8 +99,8 @@ __global__ __launch_bounds__(64) void mala_decode_split_kernel(DecParams p) {
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
       float x0 = s0[r] * p.scale2, x1 = s1[r] * p.scale2;
-      if (kb + 4 * g + r >= p.Nk) x0 = kNegInf;
-      if (kb + 16 + 4 * g + r >= p.Nk) x1 = kNegInf;
+      if (kb + 4 * g + r >= n) x0 = kNegInf;
+      if (kb + 16 + 4 * g + r >= n) x1 = kNegInf;
       sv[r] = x0;
       sv[4 + r] = x1;
       mt = fmaxf(mt, fmaxf(x0, x1));
@@ -119,8 +131,9 @@ __global__ __launch_bounds__(64) void mala_decode_split_kernel(DecParams p) {
       if (t - 2 >= t_lo) load_k(t - 2);
     }
     const float lse_run = m + fast_log2(l);
-    const bool demand = head_valid && (l == 0.f || (mt - lse_run >= p.thr2));
-    const bool hint = has_next && wave_any(head_valid && (l == 0.f || (mtn - lse_run >= p.thr2 - kHintMargin)));
+    const bool demand = head_valid && (l == 0.f || (mt - lse_run >= thr2));
+    const bool hint =
+        has_next && wave_any(head_valid && (l == 0.f || (mtn - lse_run >= thr2 - kHintMargin)));
     if (wave_any(demand)) {
       __syncthreads();   // the previous tile's transposed reads are done
 #pragma unroll

@@ -66,8 +66,10 @@ struct DecParams {
   const __bf16* v;
   float* part;         // [B, Hq, S, D + kDecStride]
   unsigned long long* counters;
-  int B, Hq, Hkv, Nk, S, T, tps;
+  const int32_t* lens; // [B] valid cache tokens per sequence, or null (all Nk)
+  int B, Hq, Hkv, Nk, S, T, tps;   // T, tps: tiles and tiles per split at length Nk
   float scale2, thr2;  // thr2 = log2(tau) - log2(Nk)
+  float log2tau;       // for the per-sequence thresholds log2(tau) - log2(n_b)
 };
 
 hipError_t launch_fill_zero(void* ptr, size_t bytes, hipStream_t st);

@@ -93,13 +93,15 @@ def test_bwd_and_decode_reject_missing_workspace(lib):
     assert st == mala.MALA_ERR_WORKSPACE
     st = lib.mala_bwd(*([P(16)] * 9), None, None, P(16), 8, 1, 2, 1, 64, 64, 128, 1, 0.1, 0.0, None)
     assert st == mala.MALA_ERR_WORKSPACE
-    st = lib.mala_decode(*([P(16)] * 5), None, None, 4, None, 0, 1, 2, 1, 64, 128, 0.1, 0.0, None)
+    qkv, ol = [P(16)] * 3, [P(16)] * 2     # q, k_cache, v_cache / o, lse (cache_lens NULL)
+    st = lib.mala_decode(*qkv, None, *ol, None, None, 4, None, 0, 1, 2, 1, 64, 128, 0.1, 0.0,
+                         None)
     assert st == mala.MALA_ERR_WORKSPACE
-    st = lib.mala_decode(*([P(16)] * 5), None, None, 0, P(16), 1 << 20, 1, 2, 1, 64, 128, 0.1, 0.0,
-                         None)
+    st = lib.mala_decode(*qkv, None, *ol, None, None, 0, P(16), 1 << 20, 1, 2, 1, 64, 128, 0.1,
+                         0.0, None)
     assert st == mala.MALA_ERR_INVALID_ARG
-    st = lib.mala_decode(*([P(16)] * 5), None, None, 2, P(16), 1 << 20, 1, 32, 1, 64, 128, 0.1, 0.0,
-                         None)
+    st = lib.mala_decode(*qkv, None, *ol, None, None, 2, P(16), 1 << 20, 1, 32, 1, 64, 128, 0.1,
+                         0.0, None)
     assert st == mala.MALA_ERR_UNSUPPORTED
 
 

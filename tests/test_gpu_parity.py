@@ -198,6 +198,64 @@ def test_decode_parity_small(spec, splits, tau):
                   exempt_rows(tau, od["tie_abs"]))
 
 
+VARLEN_DECODE_CASES = [
+    # per-sequence cache lengths: full, ragged, one token, a whole number of tiles,
+    # empty, and one past the capacity (clamped to Nk)
+    (dict(kind="decode", B=6, Hq=8, Hkv=2, N=3001, D=128, beta=3.0, needles=4),
+     [3001, 1777, 1, 64, 0, 5000], 4, 1e-4),
+    (dict(kind="decode", B=3, Hq=4, Hkv=4, N=999, D=64, beta=3.0, needles=4), [999, 33, 500], 3,
+     0.1),
+    (dict(kind="decode", B=4, Hq=16, Hkv=1, N=2048, D=128, beta=2.0, needles=2),
+     [2048, 1000, 31, 1500], 7, 1.0),
+]
+
+
+@pytest.mark.parametrize("spec,lens,splits,tau", VARLEN_DECODE_CASES)
+def test_decode_per_sequence_cache_lengths(spec, lens, splits, tau):
+    # each sequence against the oracle on its own valid prefix of the cache
+    w = Workload(spec)
+    t = w.tensors()
+    scale = f32(w.scale)
+    bk = mala.mala_geometry(w.D, mala.PASS_DECODE)[1]
+    qf, kf, vf = map(bf16_to_f64, (t["q"], t["k"], t["v"]))
+    cl = torch.tensor(lens, dtype=torch.int32, device="cuda")
+    g = mala.decode(dev(t["q"]), dev(t["k"]), dev(t["v"]), scale, tau, splits, cache_lens=cl)
+    torch.cuda.synchronize()
+    o, lse, ht = host(g["o"]), host(g["lse"]), host(g["head_tiles"])
+    legal = 0
+    for b, n in enumerate(lens):
+        n = min(max(n, 0), w.N)
+        if n == 0:
+            assert (o[b] == 0).all() and np.isneginf(lse[b]).all() and (ht[b] == 0).all()
+            continue
+        od = oracle.mala_decode(qf[b:b + 1], kf[b:b + 1, :, :n], vf[b:b + 1, :, :n], scale,
+                                f32(tau), bk, splits)
+        assert_close("decode O seq %d (n=%d)" % (b, n), o[b], od["o"][0])
+        assert np.abs(lse[b] - od["lse"][0]).max() <= LSE_DIAG
+        assert_counts("decode head tiles seq %d" % b, ht[b:b + 1], od["tiles"],
+                      exempt_rows(tau, od["tie_abs"]))
+        legal += -(-n // bk) * w.Hq
+    assert int(host(g["counters"])[0]) == legal
+
+
+def test_decode_full_lengths_match_uniform_path():
+    # cache_lens all equal to Nk is the uniform decode (bitwise at tau = 0, where
+    # the threshold plays no part)
+    spec = dict(kind="decode", B=3, Hq=8, Hkv=2, N=1500, D=128, beta=3.0, needles=4)
+    w = Workload(spec)
+    t = w.tensors()
+    q, k, v = dev(t["q"]), dev(t["k"]), dev(t["v"])
+    cl = torch.full((w.B,), w.N, dtype=torch.int32, device="cuda")
+    for tau in (0.0, 1e-3):
+        a = mala.decode(q, k, v, f32(w.scale), tau, 3)
+        b = mala.decode(q, k, v, f32(w.scale), tau, 3, cache_lens=cl)
+        torch.cuda.synchronize()
+        if tau == 0.0:
+            assert torch.equal(a["o"], b["o"]) and torch.equal(a["lse"], b["lse"])
+        else:
+            np.testing.assert_allclose(host(b["o"]), host(a["o"]), atol=1e-5)
+
+
 def test_decode_splits_cover_dense_at_tau0():
     spec = dict(kind="decode", B=1, Hq=4, Hkv=1, N=2048, D=128, beta=3.0, needles=4)
     w = Workload(spec)
@@ -313,6 +371,34 @@ def test_full_config5_decode_sampled(tau):
         hk = h // w.g
         od = oracle.mala_decode(qf[b:b + 1, h:h + 1], bf16_to_f64(t["k"][b:b + 1, hk:hk + 1]),
                                 bf16_to_f64(t["v"][b:b + 1, hk:hk + 1]), scale, f32(tau), bk, S)
+        assert_close("decode O", o[b, h], od["o"][0, 0])
+        assert abs(lse[b, h] - od["lse"][0, 0]) <= LSE_DIAG
+        assert_counts("decode tiles", ht[b:b + 1, h:h + 1], od["tiles"],
+                      exempt_rows(tau, od["tie_abs"]))
+
+
+@pytest.mark.parametrize("tau", [1e-4, 1.0])
+def test_full_config5_decode_ragged_lengths_sampled(tau):
+    # the serving case: the 131072-token caches holding ragged valid lengths
+    w = Workload(5)
+    print("[full cfg5 ragged tau=%g] generating inputs" % tau, flush=True)
+    t = w.tensors(threads=16)
+    scale = f32(w.scale)
+    bk = mala.mala_geometry(w.D, mala.PASS_DECODE)[1]
+    S = mala.default_num_splits(w.B, w.Hkv, w.N)
+    lens = np.random.default_rng(7).integers(1, w.N + 1, size=w.B).astype(np.int32)
+    lens[0], lens[1] = w.N, 1
+    cl = torch.from_numpy(lens).to("cuda")
+    g = mala.decode(dev(t["q"]), dev(t["k"]), dev(t["v"]), scale, tau, S, cache_lens=cl)
+    torch.cuda.synchronize()
+    o, lse, ht = host(g["o"]), host(g["lse"]), host(g["head_tiles"])
+    qf = bf16_to_f64(t["q"])
+    for b, h in [(0, 5), (1, 0), (2, 17), (9, 31)]:
+        n, hk = int(lens[b]), h // w.g
+        print("[full cfg5 ragged] oracle seq %d head %d n=%d splits %d" % (b, h, n, S), flush=True)
+        od = oracle.mala_decode(qf[b:b + 1, h:h + 1], bf16_to_f64(t["k"][b:b + 1, hk:hk + 1, :n]),
+                                bf16_to_f64(t["v"][b:b + 1, hk:hk + 1, :n]), scale, f32(tau), bk,
+                                S)
         assert_close("decode O", o[b, h], od["o"][0, 0])
         assert abs(lse[b, h] - od["lse"][0, 0]) <= LSE_DIAG
         assert_counts("decode tiles", ht[b:b + 1, h:h + 1], od["tiles"],
