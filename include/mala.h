@@ -134,6 +134,40 @@ int mala_bwd(const void* q, const void* k, const void* v, const float* o, const 
              int64_t* counters, void* workspace, size_t workspace_bytes, int B, int Hq, int Hkv,
              int Nq, int Nk, int D, int causal, float scale, float tau, void* stream);
 
+/*
+ * Packed variable-length batches (the forward of Algorithm 1 per sequence).
+ * num_seqs sequences lie back to back along the token axis: sequence b holds rows
+ * [cu_seqlens[b], cu_seqlens[b + 1]) of every head, attends causally within itself
+ * only (its i-th row sees its rows 0..i, L_q = i + 1) and is tiled from its own
+ * first row, exactly as a batch of one with Nq = Nk = its length.
+ *   q: bf16 [Hq, total, D]; k, v: bf16 [Hkv, total, D] (head-major: the fixed-length
+ *   layout with B = 1 and N = total); o: fp32 [Hq, total, D] out; lse: fp32
+ *   [Hq, total] out; row_tiles: int32 [Hq, total] or NULL out; counters as mala_fwd.
+ *   cu_seqlens: int32 [num_seqs + 1] device array, non-decreasing from 0 to at
+ *   most total; max_seqlen: the longest sequence (the launch is sized by it).
+ *   On the device the starts are clamped into [0, total] and a sequence longer
+ *   than max_seqlen is cut to its first max_seqlen rows; rows that no (cut)
+ *   sequence covers are not written.  Requires max_seqlen <= total, D in {64, 128}
+ *   and total * D * 2 < 2^32.
+ */
+int mala_fwd_varlen(const void* q, const void* k, const void* v, const int32_t* cu_seqlens,
+                    float* o, float* lse, int32_t* row_tiles, int64_t* counters, int num_seqs,
+                    int max_seqlen, int total, int Hq, int Hkv, int D, float scale, float tau,
+                    void* stream);
+
+/*
+ * Packed variable-length batches: mala_bwd (Algorithm 2) per sequence, on the
+ * layout of mala_fwd_varlen (o, lse as it returned them; dout, dq: [Hq, total, D];
+ * dk, dv: fp32 [Hkv, total, D] out).  workspace: at least
+ * mala_bwd_workspace_size(1, Hq, Hkv, total, total, D) bytes.  Rows that no
+ * sequence covers are not written.
+ */
+int mala_bwd_varlen(const void* q, const void* k, const void* v, const int32_t* cu_seqlens,
+                    const float* o, const float* lse, const void* dout, float* dq, float* dk,
+                    float* dv, int32_t* row_tiles, int64_t* counters, void* workspace,
+                    size_t workspace_bytes, int num_seqs, int max_seqlen, int total, int Hq,
+                    int Hkv, int D, float scale, float tau, void* stream);
+
 /* Bytes of device workspace mala_decode needs: fp32 split partials
  * [B, Hq, num_splits, D + 4] (O_s / l_s, lse_s, retained count, pad). */
 size_t mala_decode_workspace_size(int B, int Hq, int D, int num_splits);

@@ -6,8 +6,9 @@ and the current stream.  There is no fallback: if libmala.so is missing or no
 GPU is present, the calls raise.
 
 Low-level functions carry the C names and arguments (mala_fwd, mala_bwd,
-mala_decode, mala_geometry, mala_bwd_workspace_size, mala_decode_workspace_size);
-fwd / bwd / decode allocate their outputs and return them in a dict.
+mala_fwd_varlen, mala_bwd_varlen, mala_decode, mala_geometry,
+mala_bwd_workspace_size, mala_decode_workspace_size); fwd / bwd / fwd_varlen /
+bwd_varlen / decode allocate their outputs and return them in a dict.
 """
 from __future__ import annotations
 
@@ -24,7 +25,8 @@ PASS_FWD, PASS_BWD, PASS_DECODE = 0, 1, 2
 CNT_LEGAL, CNT_RETAINED, CNT_V_TILES, CNT_SLOTS = 0, 1, 2, 3
 
 EXPORTS = ("mala_geometry", "mala_strerror", "mala_last_error", "mala_fwd",
-           "mala_bwd_workspace_size", "mala_bwd", "mala_decode_workspace_size", "mala_decode")
+           "mala_bwd_workspace_size", "mala_bwd", "mala_fwd_varlen", "mala_bwd_varlen",
+           "mala_decode_workspace_size", "mala_decode")
 
 
 class MalaError(RuntimeError):
@@ -62,6 +64,10 @@ def load_library():
     lib.mala_bwd_workspace_size.restype = sz
     lib.mala_bwd.argtypes = [vp] * 12 + [sz] + [i] * 7 + [f, f, vp]
     lib.mala_bwd.restype = i
+    lib.mala_fwd_varlen.argtypes = [vp] * 8 + [i] * 6 + [f, f, vp]
+    lib.mala_fwd_varlen.restype = i
+    lib.mala_bwd_varlen.argtypes = [vp] * 13 + [sz] + [i] * 6 + [f, f, vp]
+    lib.mala_bwd_varlen.restype = i
     lib.mala_decode_workspace_size.argtypes = [i] * 4
     lib.mala_decode_workspace_size.restype = sz
     lib.mala_decode.argtypes = [vp] * 8 + [i, vp, sz] + [i] * 5 + [f, f, vp]
@@ -161,6 +167,55 @@ def mala_decode(q, k_cache, v_cache, o, lse, head_tiles, counters, num_splits, w
                                       Nk, D, scale, tau, _stream(stream)))
 
 
+def _varlen_dims(q, k, cu_seqlens):
+    """(num_seqs, Hq, Hkv, total, D) of a packed batch: q [Hq, total, D], k [Hkv, total, D],
+    cu_seqlens int32 [num_seqs + 1] on the device."""
+    _dev(cu_seqlens, torch.int32, "cu_seqlens", 1)
+    Hq, total, D = q.shape
+    if k.shape[1] != total or cu_seqlens.shape[0] < 2:
+        raise ValueError("inconsistent shapes")
+    return cu_seqlens.shape[0] - 1, Hq, k.shape[0], total, D
+
+
+def mala_fwd_varlen(q, k, v, cu_seqlens, max_seqlen, o, lse, row_tiles, counters, scale, tau,
+                    stream=None):
+    _dev(q, torch.bfloat16, "q", 3), _dev(k, torch.bfloat16, "k", 3), _dev(v, torch.bfloat16, "v", 3)
+    _dev(o, torch.float32, "o", 3), _dev(lse, torch.float32, "lse", 2)
+    S, Hq, Hkv, total, D = _varlen_dims(q, k, cu_seqlens)
+    if tuple(v.shape) != tuple(k.shape) or tuple(o.shape) != tuple(q.shape) or \
+            tuple(lse.shape) != (Hq, total):
+        raise ValueError("inconsistent shapes")
+    if row_tiles is not None:
+        _dev(row_tiles, torch.int32, "row_tiles", 2)
+    if counters is not None:
+        _dev(counters, torch.int64, "counters", 1)
+    _check(load_library().mala_fwd_varlen(_ptr(q), _ptr(k), _ptr(v), _ptr(cu_seqlens), _ptr(o),
+                                          _ptr(lse), _ptr(row_tiles), _ptr(counters), S,
+                                          int(max_seqlen), total, Hq, Hkv, D, scale, tau,
+                                          _stream(stream)))
+
+
+def mala_bwd_varlen(q, k, v, cu_seqlens, max_seqlen, o, lse, dout, dq, dk, dv, row_tiles,
+                    counters, workspace, scale, tau, stream=None):
+    for t, n, dt, nd in ((q, "q", torch.bfloat16, 3), (k, "k", torch.bfloat16, 3),
+                         (v, "v", torch.bfloat16, 3), (o, "o", torch.float32, 3),
+                         (lse, "lse", torch.float32, 2), (dout, "dout", torch.bfloat16, 3),
+                         (dq, "dq", torch.float32, 3), (dk, "dk", torch.float32, 3),
+                         (dv, "dv", torch.float32, 3)):
+        _dev(t, dt, n, nd)
+    S, Hq, Hkv, total, D = _varlen_dims(q, k, cu_seqlens)
+    if (tuple(dq.shape) != tuple(q.shape) or tuple(dout.shape) != tuple(q.shape)
+            or tuple(o.shape) != tuple(q.shape) or tuple(dk.shape) != tuple(k.shape)
+            or tuple(dv.shape) != tuple(k.shape)):
+        raise ValueError("inconsistent shapes")
+    _check(load_library().mala_bwd_varlen(_ptr(q), _ptr(k), _ptr(v), _ptr(cu_seqlens), _ptr(o),
+                                          _ptr(lse), _ptr(dout), _ptr(dq), _ptr(dk), _ptr(dv),
+                                          _ptr(row_tiles), _ptr(counters), _ptr(workspace),
+                                          workspace.numel() * workspace.element_size(), S,
+                                          int(max_seqlen), total, Hq, Hkv, D, scale, tau,
+                                          _stream(stream)))
+
+
 # ---------------------------------------------------------------- allocating wrappers
 def fwd(q, k, v, scale, tau, stats=True, stream=None):
     B, Hq, Nq, D = q.shape
@@ -202,6 +257,35 @@ def decode(q, k_cache, v_cache, scale, tau, num_splits, stats=True, workspace=No
     mala_decode(q, k_cache, v_cache, o, lse, ht, cnt, num_splits, workspace, scale, tau,
                 stream=stream, cache_lens=cache_lens)
     return dict(o=o, lse=lse, head_tiles=ht, counters=cnt)
+
+
+def fwd_varlen(q, k, v, cu_seqlens, max_seqlen, scale, tau, stats=True, stream=None):
+    """Packed batch: q [Hq, total, D], k, v [Hkv, total, D], cu_seqlens int32 [S + 1].
+    Rows that no sequence covers come back as zeros."""
+    Hq, total, D = q.shape
+    o = torch.zeros((Hq, total, D), dtype=torch.float32, device=q.device)
+    lse = torch.zeros((Hq, total), dtype=torch.float32, device=q.device)
+    rt = torch.zeros((Hq, total), dtype=torch.int32, device=q.device) if stats else None
+    cnt = torch.empty(4, dtype=torch.int64, device=q.device) if stats else None
+    mala_fwd_varlen(q, k, v, cu_seqlens, max_seqlen, o, lse, rt, cnt, scale, tau, stream=stream)
+    return dict(o=o, lse=lse, row_tiles=rt, counters=cnt)
+
+
+def bwd_varlen(q, k, v, cu_seqlens, max_seqlen, o, lse, dout, scale, tau, stats=True,
+               workspace=None, stream=None):
+    Hq, total, D = q.shape
+    Hkv = k.shape[0]
+    dq = torch.zeros((Hq, total, D), dtype=torch.float32, device=q.device)
+    dk = torch.zeros((Hkv, total, D), dtype=torch.float32, device=q.device)
+    dv = torch.zeros((Hkv, total, D), dtype=torch.float32, device=q.device)
+    rt = torch.zeros((Hq, total), dtype=torch.int32, device=q.device) if stats else None
+    cnt = torch.empty(4, dtype=torch.int64, device=q.device) if stats else None
+    if workspace is None:
+        n = mala_bwd_workspace_size(1, Hq, Hkv, total, total, D)
+        workspace = torch.empty(max(n, 16), dtype=torch.uint8, device=q.device)
+    mala_bwd_varlen(q, k, v, cu_seqlens, max_seqlen, o, lse, dout, dq, dk, dv, rt, cnt,
+                    workspace, scale, tau, stream=stream)
+    return dict(dq=dq, dk=dk, dv=dv, row_tiles=rt, counters=cnt)
 
 
 def default_num_splits(B, Hkv, Nk, num_cus=256, waves_per_simd=2):

@@ -81,15 +81,16 @@ const char* mala_strerror(int status) {
 
 const char* mala_last_error(void) { return g_err; }
 
-int mala_fwd(const void* q, const void* k, const void* v, float* o, float* lse, int32_t* row_tiles,
-             int64_t* counters, int B, int Hq, int Hkv, int Nq, int Nk, int D, int causal,
-             float scale, float tau, void* stream) {
-  g_err[0] = 0;
-  if (!q || !k || !v || !o || !lse) return fail(MALA_ERR_INVALID_ARG, "null q, k, v, o or lse");
-  int st = check_common(B, Hq, Hkv, Nq, Nk, D, causal, scale, tau);
-  if (!st) st = check_slice_range(Nk, D);
-  if (st) return st;
-  hipStream_t s = (hipStream_t)stream;
+}  // extern "C"
+
+namespace {
+
+// Shared by the fixed-length and packed entry points: B slices (sequences) of
+// Nq / Nk rows each (packed: Nq = Nk = total, the head stride), cu the packed
+// sequence starts or null.
+int run_fwd(const void* q, const void* k, const void* v, const int32_t* cu, int max_len,
+            float* o, float* lse, int32_t* row_tiles, int64_t* counters, int B, int Hq, int Hkv,
+            int Nq, int Nk, int D, float scale, float tau, hipStream_t s) {
   if (counters) {
     hipError_t e = mala::launch_fill_zero(counters, 4 * sizeof(int64_t), s);
     if (e != hipSuccess) return hip_fail(e, "mala_fwd: clearing counters");
@@ -102,13 +103,89 @@ int mala_fwd(const void* q, const void* k, const void* v, float* o, float* lse, 
   p.lse = lse;
   p.row_tiles = row_tiles;
   p.counters = (unsigned long long*)counters;
+  p.cu = cu;
+  p.max_len = cu ? max_len : Nq;
   p.B = B; p.Hq = Hq; p.Hkv = Hkv; p.Nq = Nq; p.Nk = Nk;
   p.scale2 = scale * mala::kLog2e;
   p.log2tau = log2_tau(tau);
-  p.nqblk = (Nq + mala::kFwdRows - 1) / mala::kFwdRows;
+  p.nqblk = (p.max_len + mala::kFwdRows - 1) / mala::kFwdRows;
   hipError_t e = mala::launch_fwd(p, D, s);
   if (e != hipSuccess) return hip_fail(e, "mala_fwd: kernel launch");
   return MALA_OK;
+}
+
+int run_bwd(const void* q, const void* k, const void* v, const int32_t* cu, int max_len,
+            const float* o, const float* lse, const void* dout, float* dq, float* dk, float* dv,
+            int32_t* row_tiles, int64_t* counters, void* workspace, int B, int Hq, int Hkv,
+            int Nq, int Nk, int D, float scale, float tau, hipStream_t s) {
+  hipError_t e;
+  // D_q over every row of the q-shaped tensors (packed: all heads x total rows)
+  const long rows = cu ? (long)Hq * Nq : (long)B * Hq * Nq;
+  if (counters && (e = mala::launch_fill_zero(counters, 4 * sizeof(int64_t), s)) != hipSuccess)
+    return hip_fail(e, "mala_bwd: clearing counters");
+  float* dvec = (float*)workspace;
+  if ((e = mala::launch_bwd_preprocess(o, (const __bf16*)dout, dvec, rows, D, s)) != hipSuccess)
+    return hip_fail(e, "mala_bwd: preprocess launch");
+  mala::BwdParams p;
+  p.q = (const __bf16*)q;
+  p.k = (const __bf16*)k;
+  p.v = (const __bf16*)v;
+  p.dout = (const __bf16*)dout;
+  p.lse = lse;
+  p.dvec = dvec;
+  p.dq = dq; p.dk = dk; p.dv = dv;
+  p.row_tiles = row_tiles;
+  p.counters = (unsigned long long*)counters;
+  p.cu = cu;
+  p.max_len = cu ? max_len : Nq;
+  p.B = B; p.Hq = Hq; p.Hkv = Hkv; p.Nq = Nq; p.Nk = Nk;
+  p.scale = scale;
+  p.scale2 = scale * mala::kLog2e;
+  p.log2tau = log2_tau(tau);
+  p.nkblk = ((cu ? max_len : Nk) + mala::kBwdKeys - 1) / mala::kBwdKeys;
+  p.nqblk = (p.max_len + mala::kDqRows - 1) / mala::kDqRows;
+  if ((e = mala::launch_bwd(p, D, s)) != hipSuccess) return hip_fail(e, "mala_bwd: kernel launch");
+  return MALA_OK;
+}
+
+int check_varlen(const int32_t* cu, int num_seqs, int max_seqlen, int total, int Hq, int Hkv,
+                 int D, float scale, float tau) {
+  if (!cu) return fail(MALA_ERR_INVALID_ARG, "null cu_seqlens");
+  if (num_seqs <= 0 || max_seqlen <= 0 || total <= 0)
+    return fail(MALA_ERR_INVALID_ARG, "non-positive size (num_seqs, max_seqlen, total)");
+  if (max_seqlen > total) return fail(MALA_ERR_INVALID_ARG, "max_seqlen (%d) > total (%d)",
+                                      max_seqlen, total);
+  int st = check_common(1, Hq, Hkv, total, total, D, 1, scale, tau);
+  if (!st) st = check_slice_range(total, D);
+  return st;
+}
+
+}  // namespace
+
+extern "C" {
+
+int mala_fwd(const void* q, const void* k, const void* v, float* o, float* lse, int32_t* row_tiles,
+             int64_t* counters, int B, int Hq, int Hkv, int Nq, int Nk, int D, int causal,
+             float scale, float tau, void* stream) {
+  g_err[0] = 0;
+  if (!q || !k || !v || !o || !lse) return fail(MALA_ERR_INVALID_ARG, "null q, k, v, o or lse");
+  int st = check_common(B, Hq, Hkv, Nq, Nk, D, causal, scale, tau);
+  if (!st) st = check_slice_range(Nk, D);
+  if (st) return st;
+  return run_fwd(q, k, v, nullptr, 0, o, lse, row_tiles, counters, B, Hq, Hkv, Nq, Nk, D, scale,
+                 tau, (hipStream_t)stream);
+}
+
+int mala_fwd_varlen(const void* q, const void* k, const void* v, const int32_t* cu_seqlens,
+                    float* o, float* lse, int32_t* row_tiles, int64_t* counters, int num_seqs,
+                    int max_seqlen, int total, int Hq, int Hkv, int D, float scale, float tau,
+                    void* stream) {
+  g_err[0] = 0;
+  if (!q || !k || !v || !o || !lse) return fail(MALA_ERR_INVALID_ARG, "null q, k, v, o or lse");
+  int st = check_varlen(cu_seqlens, num_seqs, max_seqlen, total, Hq, Hkv, D, scale, tau);
+  if (st) return st;
+  return run_fwd(q, k, v, cu_seqlens, max_seqlen, o, lse, row_tiles, counters, num_seqs, Hq, Hkv,
+                 total, total, D, scale, tau, (hipStream_t)stream);
 }
 
 size_t mala_bwd_workspace_size(int B, int Hq, int Hkv, int Nq, int Nk, int D) {
@@ -131,31 +208,27 @@ int mala_bwd(const void* q, const void* k, const void* v, const float* o, const 
   if (!workspace || workspace_bytes < need)
     return fail(MALA_ERR_WORKSPACE, "mala_bwd needs %zu workspace bytes, got %zu", need, workspace_bytes);
   if (((uintptr_t)workspace) % 16) return fail(MALA_ERR_WORKSPACE, "workspace not 16-byte aligned");
-  hipStream_t s = (hipStream_t)stream;
-  hipError_t e;
-  const long rows = (long)B * Hq * Nq;
-  if (counters && (e = mala::launch_fill_zero(counters, 4 * sizeof(int64_t), s)) != hipSuccess)
-    return hip_fail(e, "mala_bwd: clearing counters");
-  float* dvec = (float*)workspace;
-  if ((e = mala::launch_bwd_preprocess(o, (const __bf16*)dout, dvec, rows, D, s)) != hipSuccess)
-    return hip_fail(e, "mala_bwd: preprocess launch");
-  mala::BwdParams p;
-  p.q = (const __bf16*)q;
-  p.k = (const __bf16*)k;
-  p.v = (const __bf16*)v;
-  p.dout = (const __bf16*)dout;
-  p.lse = lse;
-  p.dvec = dvec;
-  p.dq = dq; p.dk = dk; p.dv = dv;
-  p.row_tiles = row_tiles;
-  p.counters = (unsigned long long*)counters;
-  p.B = B; p.Hq = Hq; p.Hkv = Hkv; p.Nq = Nq; p.Nk = Nk;
-  p.scale = scale;
-  p.scale2 = scale * mala::kLog2e;
-  p.log2tau = log2_tau(tau);
-  p.nkblk = (Nk + mala::kBwdKeys - 1) / mala::kBwdKeys;
-  if ((e = mala::launch_bwd(p, D, s)) != hipSuccess) return hip_fail(e, "mala_bwd: kernel launch");
-  return MALA_OK;
+  return run_bwd(q, k, v, nullptr, 0, o, lse, dout, dq, dk, dv, row_tiles, counters, workspace,
+                 B, Hq, Hkv, Nq, Nk, D, scale, tau, (hipStream_t)stream);
+}
+
+int mala_bwd_varlen(const void* q, const void* k, const void* v, const int32_t* cu_seqlens,
+                    const float* o, const float* lse, const void* dout, float* dq, float* dk,
+                    float* dv, int32_t* row_tiles, int64_t* counters, void* workspace,
+                    size_t workspace_bytes, int num_seqs, int max_seqlen, int total, int Hq,
+                    int Hkv, int D, float scale, float tau, void* stream) {
+  g_err[0] = 0;
+  if (!q || !k || !v || !o || !lse || !dout || !dq || !dk || !dv)
+    return fail(MALA_ERR_INVALID_ARG, "null tensor argument");
+  int st = check_varlen(cu_seqlens, num_seqs, max_seqlen, total, Hq, Hkv, D, scale, tau);
+  if (st) return st;
+  const size_t need = mala_bwd_workspace_size(1, Hq, Hkv, total, total, D);
+  if (!workspace || workspace_bytes < need)
+    return fail(MALA_ERR_WORKSPACE, "mala_bwd_varlen needs %zu workspace bytes, got %zu", need,
+                workspace_bytes);
+  if (((uintptr_t)workspace) % 16) return fail(MALA_ERR_WORKSPACE, "workspace not 16-byte aligned");
+  return run_bwd(q, k, v, cu_seqlens, max_seqlen, o, lse, dout, dq, dk, dv, row_tiles, counters,
+                 workspace, num_seqs, Hq, Hkv, total, total, D, scale, tau, (hipStream_t)stream);
 }
 
 size_t mala_decode_workspace_size(int B, int Hq, int D, int num_splits) {

@@ -153,14 +153,14 @@ __device__ __forceinline__ void probabilities(float (&sv)[16], float scale2, con
 }
 
 // Per-row vectors of a query tile: base-2 lse, test threshold, D_q.
-__device__ __forceinline__ void row_vectors(const BwdParams& p, long bhq, long qq, long off,
-                                            float* lse2, float* thr, float* dv) {
+__device__ __forceinline__ void row_vectors(const BwdParams& p, long qbase, int Nq, long qq,
+                                            long off, float* lse2, float* thr, float* dv) {
 #pragma clang fp contract(off)
-  if (qq < p.Nq) {
-    const float l2 = p.lse[bhq * p.Nq + qq] * kLog2e;
+  if (qq < Nq) {
+    const float l2 = p.lse[qbase + qq] * kLog2e;
     *lse2 = l2;
     *thr = l2 + p.log2tau - log2f((float)(qq + 1 + off));
-    *dv = p.dvec[bhq * p.Nq + qq];
+    *dv = p.dvec[qbase + qq];
   } else {
     *lse2 = 0.f;
     *thr = __builtin_huge_valf();   // padded rows never retain
@@ -208,14 +208,18 @@ __global__ __launch_bounds__(1024) void mala_bwd_dkdv_kernel(BwdParams p) {
   const int bhk = blockIdx.x % BHk;
   const int kblk = blockIdx.x / BHk;       // ascending: the longest key blocks first
   const int b = bhk / p.Hkv, hkv = bhk % p.Hkv, grp = p.Hq / p.Hkv;
-  const long off = (long)p.Nk - p.Nq;
+  const Seg sg = seq_slice(p.cu, p.max_len, p.Nq, p.Nk, b, p.Hq, p.Hkv);
+  const int Nq = sg.Nq, Nk = sg.Nk;
+  const long off = (long)Nk - Nq;
   const int kb0 = kblk * kBwdKeys;
+  if (kb0 >= Nk) return;                   // past the end of a packed sequence
+  const long kbase = sg.kb + (long)hkv * p.Nk;   // key 0 of this (sequence, KV head)
   const int kw = kb0 + grp_k * kBk;        // first key of this wavefront's decision tile
   const int key = kw + c;                  // this lane's key (C-layout column)
 
   const long first_q = (long)kb0 - off;
   const int qi_start = first_q <= 0 ? 0 : (int)(first_q / kBq);
-  const int nqt = (p.Nq + kBq - 1) / kBq;
+  const int nqt = (Nq + kBq - 1) / kBq;
   const int per_head = nqt - qi_start;     // >= 1: key kb0 < Nk is visible to row Nq - 1
   const int total = grp * per_head;
 
@@ -250,17 +254,16 @@ __global__ __launch_bounds__(1024) void mala_bwd_dkdv_kernel(BwdParams p) {
   float plse = 0.f, pdv = 0.f, plg = 0.f;
   bool prow = false;
   auto fetch = [&](int it) {
-    const long bhq = (long)b * p.Hq + hkv * grp + it % grp;
     const int q0 = tile_q0(it);
-    const long r0 = bhq * p.Nq + q0;
+    const long r0 = sg.qb + (long)(hkv * grp + it % grp) * p.Nq + q0;
     if (mt < kBq) {
-      const uint32_t nr = (uint32_t)(p.Nq - q0) * 4u;
+      const uint32_t nr = (uint32_t)(Nq - q0) * 4u;
       plse = buf_load1(make_rsrc(p.lse + r0, nr), mt * 4u);
       pdv = buf_load1(make_rsrc(p.dvec + r0, nr), mt * 4u);
-      prow = q0 + mt < p.Nq;
+      prow = q0 + mt < Nq;
       plg = log2f((float)((long)q0 + mt + 1 + off));
     }
-    const uint32_t nb = (uint32_t)(p.Nq - q0) * (uint32_t)D * 2u;
+    const uint32_t nb = (uint32_t)(Nq - q0) * (uint32_t)D * 2u;
     const auto rq = make_rsrc(p.q + r0 * D, nb), ro = make_rsrc(p.dout + r0 * D, nb);
 #pragma unroll
     for (int u = 0; u < NJ; ++u) {
@@ -298,10 +301,10 @@ __global__ __launch_bounds__(1024) void mala_bwd_dkdv_kernel(BwdParams p) {
     // K rows (role 0, B operand of S = Q K^T) or V rows (role 2, of dP = dO V^T)
     bf16x8 kv[KS];
     {
-      const bf16* src = (role == 0 ? p.k : p.v) + (long)bhk * p.Nk * D;
+      const bf16* src = (role == 0 ? p.k : p.v) + kbase * D;
 #pragma unroll
       for (int kk = 0; kk < KS; ++kk)
-        kv[kk] = key < p.Nk ? load8(src + (long)key * D + 16 * kk + 8 * h) : zero8();
+        kv[kk] = key < Nk ? load8(src + (long)key * D + 16 * kk + 8 * h) : zero8();
     }
     if (role == 0) {
       float fdv = 0.f;   // P mass of this lane's key in tiles run without the lo term
@@ -318,11 +321,11 @@ __global__ __launch_bounds__(1024) void mala_bwd_dkdv_kernel(BwdParams p) {
           // tiles that cross the diagonal or the end of the sequence (or whose keys
           // all lie beyond this tile's rows) take the masked test
           const bool need_mask =
-              ((long)kw + kBk - 1 > (long)q0 + off) || (q0 + kBq > p.Nq) || (kw + kBk > p.Nk);
-          const int klo = key < p.Nk ? (int)((long)key - off - q0) - 4 * h : 1000000;
+              ((long)kw + kBk - 1 > (long)q0 + off) || (q0 + kBq > Nq) || (kw + kBk > Nk);
+          const int klo = key < Nk ? (int)((long)key - off - q0) - 4 * h : 1000000;
           float sv[16];
           const bool dem =
-              offline_entries(sc, p.scale2, need_mask, klo, p.Nq - q0 - 4 * h, rv + kBq, h, sv);
+              offline_entries(sc, p.scale2, need_mask, klo, Nq - q0 - 4 * h, rv + kBq, h, sv);
           const bool ret = wave_any(dem);
           bool with_lo = false;
           if (ret) {
@@ -468,9 +471,9 @@ __global__ __launch_bounds__(1024) void mala_bwd_dkdv_kernel(BwdParams p) {
     }
     // dV = sum P^T dO (role 1), dK = scale * sum dS^T Q (role 3); lane (h, c)
     // holds key kw + c
-    if (key < p.Nk) {
+    if (key < Nk) {
       const float f = role == 1 ? 1.f : p.scale;
-      float* dst = (role == 1 ? p.dv : p.dk) + ((long)bhk * p.Nk + key) * D;
+      float* dst = (role == 1 ? p.dv : p.dk) + (kbase + key) * D;
 #pragma unroll
       for (int db = 0; db < DB; ++db)
 #pragma unroll
@@ -532,26 +535,31 @@ __global__ __launch_bounds__(kDqWaves * 64) void mala_bwd_dq_kernel(BwdParams p)
   const int rdo = rd_base<D>(c, h), tro = tr_base<D>(4 * h + (t16 >> 2), G & 1, t16);
   const int BH = p.B * p.Hq;
   const int bh = blockIdx.x % BH;
-  const int qblk = (p.Nq + kDqRows - 1) / kDqRows - 1 - (int)(blockIdx.x / BH);
+  const int qblk = p.nqblk - 1 - (int)(blockIdx.x / BH);   // longest rows first
   const int b = bh / p.Hq, hq = bh % p.Hq, hkv = hq / (p.Hq / p.Hkv);
-  const long off = (long)p.Nk - p.Nq;
+  const Seg sg = seq_slice(p.cu, p.max_len, p.Nq, p.Nk, b, p.Hq, p.Hkv);
+  const int Nq = sg.Nq, Nk = sg.Nk;
+  if (qblk * kDqRows >= Nq) return;   // past the end of a packed sequence
+  const long off = (long)Nk - Nq;
   const int q0w = qblk * kDqRows + wave * kBq;
   const int qrow = q0w + c;
-  const bool row_valid = qrow < p.Nq;
-  const bf16* Kp = p.k + (long)(b * p.Hkv + hkv) * p.Nk * D;
-  const bf16* Vp = p.v + (long)(b * p.Hkv + hkv) * p.Nk * D;
+  const bool row_valid = qrow < Nq;
+  const long qbase = sg.qb + (long)hq * p.Nq;    // row 0 of this (sequence, head)
+  const long kbase = sg.kb + (long)hkv * p.Nk;
+  const bf16* Kp = p.k + kbase * D;
+  const bf16* Vp = p.v + kbase * D;
 
   // Q and dO rows of this wavefront as B operands (lane column qrow)
   bf16x8 qb[KS], ob[KS];
 #pragma unroll
   for (int kk = 0; kk < KS; ++kk) {
-    const long off_e = ((long)bh * p.Nq + qrow) * D + 16 * kk + 8 * h;
+    const long off_e = (qbase + qrow) * D + 16 * kk + 8 * h;
     qb[kk] = row_valid ? load8(p.q + off_e) : zero8();
     ob[kk] = row_valid ? load8(p.dout + off_e) : zero8();
   }
   // this lane's row vectors: base-2 lse, test threshold, D_q
   float lse2, thr, dvq;
-  row_vectors(p, bh, (long)qrow, off, &lse2, &thr, &dvq);
+  row_vectors(p, qbase, Nq, (long)qrow, off, &lse2, &thr, &dvq);
   f32x16 negd;
 #pragma unroll
   for (int r = 0; r < 16; ++r) negd[r] = -dvq;
@@ -562,10 +570,10 @@ __global__ __launch_bounds__(kDqWaves * 64) void mala_bwd_dq_kernel(BwdParams p)
 #pragma unroll
     for (int r = 0; r < 16; ++r) acc[db][r] = 0.f;
 
-  const int qlast_w = min(q0w + kBq - 1, p.Nq - 1);
-  const int jdiag = (q0w < p.Nq) ? (int)((qlast_w + off) / kBk) : -1;
-  const int nvalid = max(0, min(kBq, p.Nq - q0w));
-  const int qlast_g = min(qblk * kDqRows + kDqRows - 1, p.Nq - 1);
+  const int qlast_w = min(q0w + kBq - 1, Nq - 1);
+  const int jdiag = (q0w < Nq) ? (int)((qlast_w + off) / kBk) : -1;
+  const int nvalid = max(0, min(kBq, Nq - q0w));
+  const int qlast_g = min(qblk * kDqRows + kDqRows - 1, Nq - 1);
   const int ttop = (int)((qlast_g + off) / kFwdStage);
   unsigned n_legal = 0, n_ret = 0;
   int cnt_row = 0;   // retained tiles in which row qrow has a legal key
@@ -583,7 +591,7 @@ __global__ __launch_bounds__(kDqWaves * 64) void mala_bwd_dq_kernel(BwdParams p)
   for (int u = 0; u < NJS; ++u) dma_off[u] = dma_lane_offset<D>(64 * (wave + kDqWaves * u) + lane);
   auto fetch = [&](int t, int buf) {
     const long k0 = (long)t * kFwdStage;
-    const uint32_t nb = (uint32_t)(p.Nk - k0) * (uint32_t)D * 2u;
+    const uint32_t nb = (uint32_t)(Nk - k0) * (uint32_t)D * 2u;
     const i32x4 rk = rsrc_words(Kp + k0 * D, nb), rvv = rsrc_words(Vp + k0 * D, nb);
 #pragma unroll
     for (int u = 0; u < NJS; ++u) {
@@ -621,9 +629,9 @@ __global__ __launch_bounds__(kDqWaves * 64) void mala_bwd_dq_kernel(BwdParams p)
       for (int kk = 0; kk < KS; ++kk) kop[kk] = load8(kr + sub * kBk * (D + 8) + rd_step<D>(kk));
       const f32x16 s = qk_tile<KS>(kop, qb);
       const bool need_mask =
-          (kb + kBk - 1 > (long)q0w + off) || (q0w + kBq > p.Nq) || (kb + kBk > p.Nk);
+          (kb + kBk - 1 > (long)q0w + off) || (q0w + kBq > Nq) || (kb + kBk > Nk);
       const int kmax = (int)((long)qrow + off - kb) - 4 * h;
-      const int klim = (int)min((long)p.Nk - kb, (long)kBk) - 4 * h;
+      const int klim = (int)min((long)Nk - kb, (long)kBk) - 4 * h;
       float sv[16];
       const bool dem = need_mask ? offline_test_t<true>(s, p.scale2, kmax, klim, thr, sv)
                                  : offline_test_t<false>(s, p.scale2, kmax, klim, thr, sv);
@@ -681,7 +689,7 @@ __global__ __launch_bounds__(kDqWaves * 64) void mala_bwd_dq_kernel(BwdParams p)
 
   // dQ = scale * sum dS K; lane (h, c) holds row qrow, columns 32 db + 8 g + 4 h + e
   if (row_valid) {
-    float* dst = p.dq + ((long)bh * p.Nq + qrow) * D;
+    float* dst = p.dq + (qbase + qrow) * D;
 #pragma unroll
     for (int db = 0; db < DB; ++db)
 #pragma unroll
@@ -690,7 +698,7 @@ __global__ __launch_bounds__(kDqWaves * 64) void mala_bwd_dq_kernel(BwdParams p)
                           acc[db][4 * g + 2] * p.scale, acc[db][4 * g + 3] * p.scale};
         *reinterpret_cast<f32x4*>(dst + 32 * db + 8 * g + 4 * h) = v4;
       }
-    if (p.row_tiles && h == 0) p.row_tiles[(long)bh * p.Nq + qrow] = cnt_row;
+    if (p.row_tiles && h == 0) p.row_tiles[qbase + qrow] = cnt_row;
   }
   if (p.counters && lane == 0 && n_legal) {
     atomicAdd(&p.counters[0], (unsigned long long)n_legal);
@@ -701,7 +709,7 @@ __global__ __launch_bounds__(kDqWaves * 64) void mala_bwd_dq_kernel(BwdParams p)
 
 hipError_t launch_bwd(const BwdParams& p, int D, hipStream_t st) {
   dim3 grid_kv((unsigned)p.nkblk * p.B * p.Hkv), block_kv(1024);
-  dim3 grid_q((unsigned)((p.Nq + kDqRows - 1) / kDqRows) * p.B * p.Hq), block_q(kDqWaves * 64);
+  dim3 grid_q((unsigned)p.nqblk * p.B * p.Hq), block_q(kDqWaves * 64);
   if (D == 128) {
     hipLaunchKernelGGL(mala_bwd_dkdv_kernel<128>, grid_kv, block_kv, 0, st, p);
     hipLaunchKernelGGL(mala_bwd_dq_kernel<128>, grid_q, block_q, 0, st, p);

@@ -47,14 +47,19 @@ __global__ __launch_bounds__(kFwdWaves * 64) void mala_fwd_kernel(FwdParams p) {
   const int bh = blockIdx.x % BH;
   const int qblk = p.nqblk - 1 - (int)(blockIdx.x / BH);   // longest rows first
   const int b = bh / p.Hq, hq = bh % p.Hq, hkv = hq / (p.Hq / p.Hkv);
-  const long off = (long)p.Nk - p.Nq;
+  const Seg sg = seq_slice(p.cu, p.max_len, p.Nq, p.Nk, b, p.Hq, p.Hkv);
+  const int Nq = sg.Nq, Nk = sg.Nk;
+  if (qblk * kFwdRows >= Nq) return;   // past the end of a packed sequence
+  const long off = (long)Nk - Nq;
   const int q0w = qblk * kFwdRows + wave * kBq;
   const int qrow = q0w + c;
-  const bool row_valid = qrow < p.Nq;
+  const bool row_valid = qrow < Nq;
 
-  const bf16* Qp = p.q + (long)bh * p.Nq * D;
-  const bf16* Kp = p.k + (long)(b * p.Hkv + hkv) * p.Nk * D;
-  const bf16* Vp = p.v + (long)(b * p.Hkv + hkv) * p.Nk * D;
+  const long qbase = sg.qb + (long)hq * p.Nq;    // row 0 of this (sequence, head)
+  const long kbase = sg.kb + (long)hkv * p.Nk;
+  const bf16* Qp = p.q + qbase * D;
+  const bf16* Kp = p.k + kbase * D;
+  const bf16* Vp = p.v + kbase * D;
 
   // Q^T as the B operand: lane (h, c) holds Q[qrow][16kk + 8h .. +7]
   bf16x8 qreg[KS];
@@ -71,10 +76,10 @@ __global__ __launch_bounds__(kFwdWaves * 64) void mala_fwd_kernel(FwdParams p) {
   int cnt = 0;
   const float thr = p.log2tau - log2f((float)(qrow + 1 + off));   // log2(tau / L_q)
 
-  const int qlast_w = min(q0w + kBq - 1, p.Nq - 1);
-  const int jdiag = (q0w < p.Nq) ? (int)((qlast_w + off) / kBk) : -1;
-  const int nvalid = max(0, min(kBq, p.Nq - q0w));
-  const int qlast_g = min(qblk * kFwdRows + kFwdRows - 1, p.Nq - 1);
+  const int qlast_w = min(q0w + kBq - 1, Nq - 1);
+  const int jdiag = (q0w < Nq) ? (int)((qlast_w + off) / kBk) : -1;
+  const int nvalid = max(0, min(kBq, Nq - q0w));
+  const int qlast_g = min(qblk * kFwdRows + kFwdRows - 1, Nq - 1);
   const int ttop = (int)((qlast_g + off) / kFwdStage);
   unsigned n_legal = 0, n_ret = 0;
 
@@ -90,7 +95,7 @@ __global__ __launch_bounds__(kFwdWaves * 64) void mala_fwd_kernel(FwdParams p) {
   for (int u = 0; u < NJS; ++u) dma_off[u] = dma_lane_offset<D>(64 * (wave + kFwdWaves * u) + lane);
   auto fetch = [&](int t, int buf) {
     const long k0 = (long)t * kFwdStage;
-    const uint32_t nb = (uint32_t)(p.Nk - k0) * (uint32_t)D * 2u;
+    const uint32_t nb = (uint32_t)(Nk - k0) * (uint32_t)D * 2u;
     const i32x4 rk = rsrc_words(Kp + k0 * D, nb), rvv = rsrc_words(Vp + k0 * D, nb);
 #pragma unroll
     for (int u = 0; u < NJS; ++u) {
@@ -132,7 +137,7 @@ __global__ __launch_bounds__(kFwdWaves * 64) void mala_fwd_kernel(FwdParams p) {
           for (int kk = 0; kk < KS; ++kk) s = mfma32(ka[kk], qreg[kk], s);
         }
 
-        const bool need_mask = (kb + kBk - 1 > (long)q0w + off) || (q0w + kBq > p.Nq);
+        const bool need_mask = (kb + kBk - 1 > (long)q0w + off) || (q0w + kBq > Nq);
         float sv[16];
         float mt = kNegInf;
         if (need_mask) {
@@ -216,7 +221,7 @@ __global__ __launch_bounds__(kFwdWaves * 64) void mala_fwd_kernel(FwdParams p) {
   // epilogue: O <- O / l, LSE = (m + log2 l) * ln 2
   if (row_valid) {
     const float inv = 1.f / l;
-    float* op = p.o + ((long)bh * p.Nq + qrow) * D;
+    float* op = p.o + (qbase + qrow) * D;
 #pragma unroll
     for (int db = 0; db < DB; ++db)
 #pragma unroll
@@ -226,8 +231,8 @@ __global__ __launch_bounds__(kFwdWaves * 64) void mala_fwd_kernel(FwdParams p) {
         *reinterpret_cast<f32x4*>(op + 32 * db + 8 * g + 4 * h) = v4;
       }
     if (h == 0) {
-      p.lse[(long)bh * p.Nq + qrow] = (m + fast_log2(l)) * kLn2;
-      if (p.row_tiles) p.row_tiles[(long)bh * p.Nq + qrow] = cnt;
+      p.lse[qbase + qrow] = (m + fast_log2(l)) * kLn2;
+      if (p.row_tiles) p.row_tiles[qbase + qrow] = cnt;
     }
   }
   if (p.counters) {

@@ -29,6 +29,26 @@ constexpr float kLoMassDk = 0.25f;          // dK: sum of |dS| per key
 constexpr float kLoMassDq = 0.25f;          // dQ: sum of |dS| per query row
 constexpr int kDecStride = 4;                // extra floats per decode partial (lse, count, pad)
 
+// Batches come in two layouts.  Fixed length: [B, H, N, D], slice (b, h) at rows
+// (b H + h) N.  Packed (cu non-null): B sequences along the token axis of
+// [H, total, D] tensors (Nq = Nk = total, the head stride), sequence b at rows
+// cu[b] .. cu[b + 1] of every head (clamped into [0, total], at most max_len rows),
+// attending causally within itself and tiled from its own first row.
+struct Seg {
+  int Nq, Nk;   // rows of the sequence (queries, keys)
+  long qb, kb;  // its first row in head 0 of q (o, lse, ...) and of k (v, dk, dv)
+};
+__device__ __forceinline__ Seg seq_slice(const int32_t* cu, int max_len, int Nq, int Nk, int b,
+                                         int Hq, int Hkv) {
+  if (cu) {
+    const int r0 = min(max(cu[b], 0), Nq);
+    const int r1 = min(max(cu[b + 1], r0), Nq);
+    const int n = min(r1 - r0, max_len);
+    return Seg{n, n, (long)r0, (long)r0};
+  }
+  return Seg{Nq, Nk, (long)b * Hq * Nq, (long)b * Hkv * Nk};
+}
+
 struct FwdParams {
   const __bf16* q;
   const __bf16* k;
@@ -37,10 +57,12 @@ struct FwdParams {
   float* lse;
   int32_t* row_tiles;
   unsigned long long* counters;
+  const int32_t* cu;   // packed batches: [B + 1] sequence starts, else null
+  int max_len;         // packed batches: rows per sequence at most
   int B, Hq, Hkv, Nq, Nk;
   float scale2;    // softmax scale * log2(e): scores are kept in base-2 units
   float log2tau;   // log2(tau); -inf for tau == 0
-  int nqblk;       // ceil(Nq / kFwdRows)
+  int nqblk;       // ceil(Nq / kFwdRows) (packed: ceil(max_len / kFwdRows))
 };
 
 struct BwdParams {
@@ -55,9 +77,12 @@ struct BwdParams {
   float* dv;
   int32_t* row_tiles;
   unsigned long long* counters;
+  const int32_t* cu;   // packed batches: [B + 1] sequence starts, else null
+  int max_len;         // packed batches: rows per sequence at most
   int B, Hq, Hkv, Nq, Nk;
   float scale, scale2, log2tau;
-  int nkblk;           // ceil(Nk / kBwdKeys)
+  int nkblk;           // ceil(Nk / kBwdKeys) (packed: ceil(max_len / kBwdKeys))
+  int nqblk;           // ceil(Nq / kDqRows) (packed: ceil(max_len / kDqRows))
 };
 
 struct DecParams {

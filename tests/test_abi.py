@@ -105,6 +105,27 @@ def test_bwd_and_decode_reject_missing_workspace(lib):
     assert st == mala.MALA_ERR_UNSUPPORTED
 
 
+def test_varlen_argument_validation(lib):
+    P = ctypes.c_void_p
+    qkv = [P(16)] * 3
+
+    def fwd(cu, num_seqs, max_len, total, Hq=2, Hkv=1, D=64, tau=0.0):
+        return lib.mala_fwd_varlen(*qkv, cu, P(16), P(16), None, None, num_seqs, max_len, total,
+                                   Hq, Hkv, D, 0.125, tau, None)
+
+    assert fwd(None, 2, 8, 16) == mala.MALA_ERR_INVALID_ARG          # no cu_seqlens
+    assert fwd(P(16), 0, 8, 16) == mala.MALA_ERR_INVALID_ARG         # no sequence
+    assert fwd(P(16), 2, 17, 16) == mala.MALA_ERR_INVALID_ARG        # max_seqlen > total
+    assert fwd(P(16), 2, 8, 16, Hq=3, Hkv=2) == mala.MALA_ERR_INVALID_ARG
+    assert fwd(P(16), 2, 8, 16, D=96) == mala.MALA_ERR_UNSUPPORTED
+    assert fwd(P(16), 2, 8, 1 << 24, D=128) == mala.MALA_ERR_UNSUPPORTED   # slice range
+    assert fwd(P(16), 2, 8, 16, tau=-1.0) == mala.MALA_ERR_INVALID_ARG
+    st = lib.mala_bwd_varlen(*qkv, P(16), *([P(16)] * 6), None, None, P(16), 8, 2, 8, 16, 2, 1,
+                             64, 0.125, 0.0, None)
+    assert st == mala.MALA_ERR_WORKSPACE
+    assert lib.mala_bwd_workspace_size(1, 2, 1, 16, 16, 64) > 8
+
+
 def test_python_binding_requires_device_tensors():
     import torch
     x = torch.zeros(1, 1, 8, 64, dtype=torch.bfloat16)

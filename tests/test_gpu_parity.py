@@ -12,7 +12,7 @@ import torch
 import oracle
 import paper_2609_32712_amd as mala
 from parity_util import (LSE_DIAG, assert_close, assert_counts, dev, exempt_rows, host)
-from workloads import Workload, bf16_to_f64
+from workloads import CONFIGS, Workload, bf16_to_f64
 
 pytestmark = pytest.mark.gpu
 
@@ -170,6 +170,113 @@ def test_fidelity_measurement_matches_oracle():
               "bound mean %.3e%%" % (x, 100 * fo[x].mean(), 100 * fg[x].mean(),
                                       100 * bound.mean()), flush=True)
         assert (np.abs(fg[x] - fo[x]) <= bound * (1 + 1e-9) + 1e-15).all(), x
+
+
+# --------------------------------------------------------------------------
+# packed variable-length batches
+# --------------------------------------------------------------------------
+VARLEN_TRAIN_CASES = {
+    # ragged lengths, one token, a whole tile, several workgroups, a short tail
+    "gqa_d128": (dict(kind="train", B=1, Hq=4, Hkv=2, D=128, beta=2.5, local=2.0),
+                 [300, 1, 64, 513, 37]),
+    "mha_d64": (dict(kind="train", B=1, Hq=2, Hkv=2, D=64, beta=3.0, local=4.0), [1000, 7, 256]),
+}
+
+
+def _packed(spec, lens, seed=0):
+    cu = np.concatenate([[0], np.cumsum(lens)]).astype(np.int32)
+    w = Workload(dict(spec, N=int(cu[-1])), seed=seed)
+    t = w.tensors()
+    return w, cu, {x: t[x][0] for x in ("q", "k", "v", "do")}   # [H, total, D]
+
+
+# (tau = 1 would put a one-token sequence's only entry exactly on its threshold,
+# P = 1 = tau / L, where either decision is correct; 0.5 retains it unambiguously)
+@pytest.mark.parametrize("name,tau", [(n, t) for n in VARLEN_TRAIN_CASES
+                                      for t in (0.0, 1e-3, 0.5)])
+def test_varlen_train_parity(name, tau):
+    # every packed sequence against the oracle run on that sequence alone
+    spec, lens = VARLEN_TRAIN_CASES[name]
+    w, cu, t = _packed(spec, lens)
+    scale = f32(w.scale)
+    bq, bk = mala.mala_geometry(w.D, mala.PASS_FWD)
+    Q, K, V, DO = (dev(t[x]) for x in ("q", "k", "v", "do"))
+    CU = torch.from_numpy(cu).to("cuda")
+    g = mala.fwd_varlen(Q, K, V, CU, max(lens), scale, tau)
+    gb = mala.bwd_varlen(Q, K, V, CU, max(lens), g["o"], g["lse"], DO, scale, tau)
+    torch.cuda.synchronize()
+    o, lse, rt = host(g["o"]), host(g["lse"]), host(g["row_tiles"])
+    dq, dk, dv, rtb = host(gb["dq"]), host(gb["dk"]), host(gb["dv"]), host(gb["row_tiles"])
+    legal = 0
+    for b, n in enumerate(lens):
+        r = slice(int(cu[b]), int(cu[b + 1]))
+        qf, kf, vf, dof = (bf16_to_f64(t[x][None, :, r]) for x in ("q", "k", "v", "do"))
+        of = oracle.mala_fwd(qf, kf, vf, scale, f32(tau), bq, bk)
+        ob = oracle.mala_bwd(qf, kf, vf, of["o"], of["lse"], dof, scale, f32(tau), bq, bk)
+        assert_close("O seq %d (n=%d)" % (b, n), o[:, r], of["o"][0])
+        assert np.abs(lse[:, r] - of["lse"][0]).max() <= LSE_DIAG
+        ex_f = exempt_rows(tau, of["tie_abs"][0])
+        assert_counts("fwd row tiles seq %d" % b, rt[:, r], of["row_tiles"][0], ex_f)
+        ex_b = ex_f | exempt_rows(tau, ob["tie_abs"][0])
+        assert_counts("bwd row tiles seq %d" % b, rtb[:, r], ob["row_tiles"][0], ex_b)
+        assert_close("dQ seq %d" % b, dq[:, r], ob["dq"][0])
+        assert_close("dK seq %d" % b, dk[:, r], ob["dk"][0])
+        assert_close("dV seq %d" % b, dv[:, r], ob["dv"][0])
+        legal += legal_tiles(1, w.Hq, n, n, bq, bk)
+    assert int(host(g["counters"])[0]) == legal and int(host(gb["counters"])[0]) == legal
+
+
+def test_varlen_cut_and_uncovered_rows():
+    # a sequence longer than max_seqlen is cut to its first max_seqlen rows, and rows
+    # that no sequence covers are left as the caller's zeros
+    spec = dict(kind="train", B=1, Hq=2, Hkv=1, N=300, D=128, beta=2.0, local=2.0)
+    w = Workload(spec)
+    t = {x: y[0] for x, y in w.tensors().items()}
+    scale = f32(w.scale)
+    bq, bk = mala.mala_geometry(w.D, mala.PASS_FWD)
+    cu = np.array([0, 150, 250], dtype=np.int32)          # rows 250..299 uncovered
+    Q, K, V, DO = (dev(t[x]) for x in ("q", "k", "v", "do"))
+    CU = torch.from_numpy(cu).to("cuda")
+    g = mala.fwd_varlen(Q, K, V, CU, 120, scale, 1e-3)    # sequence 0 cut to 120 rows
+    gb = mala.bwd_varlen(Q, K, V, CU, 120, g["o"], g["lse"], DO, scale, 1e-3)
+    torch.cuda.synchronize()
+    o, dq, dk = host(g["o"]), host(gb["dq"]), host(gb["dk"])
+    for rows in (slice(120, 150), slice(250, 300)):
+        assert (o[:, rows] == 0).all() and (dq[:, rows] == 0).all() and (dk[:, rows] == 0).all()
+    for r in (slice(0, 120), slice(150, 250)):
+        qf, kf, vf, dof = (bf16_to_f64(t[x][None, :, r]) for x in ("q", "k", "v", "do"))
+        of = oracle.mala_fwd(qf, kf, vf, scale, f32(1e-3), bq, bk)
+        ob = oracle.mala_bwd(qf, kf, vf, of["o"], of["lse"], dof, scale, f32(1e-3), bq, bk)
+        assert_close("O", o[:, r], of["o"][0])
+        assert_close("dK", dk[:, r], ob["dk"][0])
+
+
+@pytest.mark.parametrize("tau", [1e-4, 1.0])
+def test_varlen_full_size_equals_per_sequence_calls(tau):
+    # 32768 packed tokens of the language-model-like inputs: every sequence's
+    # outputs equal, bit for bit, a fixed-length call on that sequence alone (the
+    # same tiles from the sequence's first row, the same arithmetic)
+    lens = [16384, 8192, 4096, 1500, 1024, 1000, 500, 68, 4]
+    w, cu, t = _packed(dict(CONFIGS[6], B=1), lens)
+    scale = f32(w.scale)
+    Q, K, V, DO = (dev(t[x]) for x in ("q", "k", "v", "do"))
+    CU = torch.from_numpy(cu).to("cuda")
+    print("[varlen full] packed fwd + bwd", flush=True)
+    g = mala.fwd_varlen(Q, K, V, CU, max(lens), scale, tau)
+    gb = mala.bwd_varlen(Q, K, V, CU, max(lens), g["o"], g["lse"], DO, scale, tau)
+    torch.cuda.synchronize()
+    for b in range(len(lens)):
+        r = slice(int(cu[b]), int(cu[b + 1]))
+        q1, k1, v1, do1 = (x[None, :, r].contiguous() for x in (Q, K, V, DO))
+        f1 = mala.fwd(q1, k1, v1, scale, tau)
+        b1 = mala.bwd(q1, k1, v1, f1["o"], f1["lse"], do1, scale, tau)
+        torch.cuda.synchronize()
+        pairs = (("o", g["o"], f1["o"]), ("lse", g["lse"], f1["lse"]),
+                 ("row_tiles", g["row_tiles"], f1["row_tiles"]), ("dq", gb["dq"], b1["dq"]),
+                 ("dk", gb["dk"], b1["dk"]), ("dv", gb["dv"], b1["dv"]),
+                 ("bwd row_tiles", gb["row_tiles"], b1["row_tiles"]))
+        for name, a, ref in pairs:
+            assert torch.equal(a[:, r], ref[0]), (b, name)
 
 
 DECODE_CASES = [
