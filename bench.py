@@ -317,7 +317,7 @@ COUNTER_CMD = ("cd /tmp && export TMPDIR=/tmp && timeout -s KILL 180 rocprofv3 -
 TRACE_CMD = ("cd /tmp && export TMPDIR=/tmp && timeout -k 10 600 rocprofv3 --kernel-trace --stats "
              "--output-format csv -d $REPO/gpurun_out/trace_bench -o bench -- "
              "python $REPO/bench.py --steps 2 --warmup 1 --reps 2 --no-cpu-baseline --no-32k "
-             "--no-lm")
+             "--no-lm --no-ragged")
 
 
 def counter_pass():
@@ -339,6 +339,66 @@ def counter_pass():
         tr.bwd(1e-4)
     torch.cuda.synchronize()
     log("counter pass done")
+
+
+SKIP_TAUS = (0.0, 1.0, 1e30)
+SKIP_TRACE_CMD = ("cd /tmp && export TMPDIR=/tmp && timeout -k 10 300 rocprofv3 --kernel-trace "
+                  "--stats --output-format csv -d $REPO/gpurun_out/trace_skip -o skip -- "
+                  "python $REPO/bench.py --skip-pass")
+
+
+def skip_pass():
+    """The program of the skip-cost trace: the 32768-token language-model-like
+    workload (8 query / 2 KV heads), three mala_fwd + mala_bwd calls at each of
+    tau = 0 (dense), 1 (the canonical tolerance) and 1e30 (every backward tile and
+    every forward tile but a row's first skipped: the cost floor of the skip path)."""
+    import torch
+    import paper_2609_32712_amd as mala
+    mala.load_library()
+    tr = Train(6, 0.0)
+    for tau in SKIP_TAUS:
+        for _ in range(3):
+            tr.fwd(tau)
+            tr.bwd(tau)
+        torch.cuda.synchronize()
+        cf, cb = tr.counters()
+        log("tau %g: retained tiles fwd %.2f%% bwd %.2f%%" % (
+            tau, 100.0 * cf[1] / cf[0], 100.0 * cb[1] / cb[0]))
+
+
+def summarize_skip_trace(trace_csv):
+    """profiles/kernels_lm32k_skip_cost.md from the kernel trace of SKIP_TRACE_CMD
+    (every training kernel has 3 dispatches per tau, in the order of SKIP_TAUS)."""
+    import csv
+    import collections
+    with open(trace_csv) as fh:
+        rows = list(csv.DictReader(fh))
+    rows.sort(key=lambda r: int(r["Start_Timestamp"]))
+    dur = collections.defaultdict(list)
+    for r in rows:
+        if "mala_" in r["Kernel_Name"] and "fill_zero" not in r["Kernel_Name"]:
+            dur[r["Kernel_Name"]].append(
+                (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e6)
+    lines = ["# Cost of skipped tiles: the 32768-token language-model-like workload", "",
+             "Command (run from the repository root on one MI355X; `$REPO` is that root):", "",
+             "```", SKIP_TRACE_CMD, "python bench.py --summarize-skip-trace "
+             "gpurun_out/trace_skip/skip_kernel_trace.csv", "```", "",
+             "Mean kernel durations (ms) over 3 calls per tau.  tau = 1e30 skips every "
+             "backward tile and every forward tile but each row's first (the cost floor of "
+             "the skip path: score MFMAs, the test, staging and synchronisation); the last "
+             "column is that floor as a fraction of the dense time.", "",
+             "| kernel | tau 0 (dense) | tau 1 | tau 1e30 (all skipped) | floor / dense |",
+             "|---|---|---|---|---|"]
+    for k, v in sorted(dur.items(), key=lambda kv: -sum(kv[1])):
+        if len(v) != 3 * len(SKIP_TAUS):
+            lines.append("| `%s` | %d dispatches (unexpected) | | | |" % (k, len(v)))
+            continue
+        m = [sum(v[3 * i:3 * i + 3]) / 3 for i in range(len(SKIP_TAUS))]
+        lines.append("| `%s` | %.3f | %.3f | %.3f | %.2f |" % (k.replace("|", "/"), m[0], m[1],
+                                                               m[2], m[2] / m[0]))
+    with open(os.path.join(ROOT, "profiles", "kernels_lm32k_skip_cost.md"), "w") as fh:
+        fh.write("\n".join(lines) + "\n")
+    print("\n".join(lines))
 
 
 def _counter_means(path):
@@ -482,10 +542,15 @@ def main():
     ap.add_argument("--no-32k", action="store_true")
     ap.add_argument("--no-lm", action="store_true",
                     help="skip the language-model-like tau = 1 timing and fidelity sweep")
+    ap.add_argument("--no-ragged", action="store_true",
+                    help="skip the ragged-cache-length decode timing")
     ap.add_argument("--counter-pass", action="store_true",
                     help="run only the program profiled for the traffic counters")
     ap.add_argument("--summarize-counters", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"))
     ap.add_argument("--summarize-trace", metavar="KERNEL_TRACE_CSV")
+    ap.add_argument("--skip-pass", action="store_true",
+                    help="run only the program of the skip-cost trace")
+    ap.add_argument("--summarize-skip-trace", metavar="KERNEL_TRACE_CSV")
     ap.add_argument("--summarize-mfma", metavar="COUNTER_CSV")
     args = ap.parse_args()
     if args.summarize_counters:
@@ -493,6 +558,9 @@ def main():
         return
     if args.summarize_trace:
         summarize_trace(args.summarize_trace)
+        return
+    if args.summarize_skip_trace:
+        summarize_skip_trace(args.summarize_skip_trace)
         return
     if args.summarize_mfma:
         summarize_mfma(args.summarize_mfma)
@@ -504,6 +572,9 @@ def main():
         sys.exit(2)
     if args.counter_pass:
         counter_pass()
+        return
+    if args.skip_pass:
+        skip_pass()
         return
     import torch
     import paper_2609_32712_amd as mala
@@ -550,11 +621,24 @@ def main():
     cd1 = dec.cnt.cpu().numpy()
     log("tau=1 fwd %.2f bwd %.2f decode %.3f ms" % (f1[0], b1[0], d1[0]))
     # supplementary: the same decode batch with ragged valid cache lengths
-    lens = ragged_lengths(dec.w.B, dec.w.N)
-    cl = torch.from_numpy(lens).to("cuda")
-    dr = time_calls(lambda: dec.run(tau, cl), args.reps, 1)
-    cdr = dec.cnt.cpu().numpy()
-    drd = time_calls(lambda: dec.run(0.0, cl), args.reps, 1)
+    ragged = None
+    if not args.no_ragged:
+        lens = ragged_lengths(dec.w.B, dec.w.N)
+        cl = torch.from_numpy(lens).to("cuda")
+        dr = time_calls(lambda: dec.run(tau, cl), args.reps, 1)
+        cdr = dec.cnt.cpu().numpy()
+        drd = time_calls(lambda: dec.run(0.0, cl), args.reps, 1)
+        # K of every valid key, V of the tiles loaded (counted once per GQA group)
+        rag_kv = float(lens.sum()) * dec.w.Hkv * dec.w.D * 2
+        rag_bytes = rag_kv + rag_kv * cdr[2] / max(1, cdr[0] / dec.w.g)
+        ragged = {
+            "lens": "uniform on [1, %d], seed 7, first full, second 1 token; total %d"
+                    % (dec.w.N, int(lens.sum())),
+            "ms": round(dr[0], 4), "dense_ms": round(drd[0], 4),
+            "speedup": round(drd[0] / dr[0], 4),
+            "retained_head_tiles_pct": round(100.0 * cdr[1] / max(1, cdr[0]), 3),
+            "hbm_gbs_algorithmic": round(rag_bytes / (dr[0] * 1e-3) / 1e9, 1),
+        }
     rt, rd = res["tau"], res["dense"]
     fl_f, fl_b = train_flops(rt["cf"], rt["cb"], w.D, bq, bk)
     de_f, de_b = dense_equivalent_flops(w.B, w.Hq, w.N, w.D)
@@ -564,9 +648,6 @@ def main():
     cd = rt["cd"]
     dec_bytes = kv_bytes + kv_bytes * cd[2] / max(1, cd[0] / dec.w.g)
     pct = lambda a, b_: round(100.0 * float(a) / max(1.0, float(b_)), 3)
-    # K of every valid key, V of the tiles loaded (counted once per GQA group)
-    rag_kv = float(lens.sum()) * dec.w.Hkv * dec.w.D * 2
-    rag_bytes = rag_kv + rag_kv * cdr[2] / max(1, cdr[0] / dec.w.g)
 
     detail = {
         "128k": {
@@ -593,14 +674,7 @@ def main():
             "v_tiles_loaded_pct": pct(cd[2], cd[0] / dec.w.g),
             "hbm_gbs_algorithmic": round(dec_bytes / (rt["dec"][0] * 1e-3) / 1e9, 1),
             "hbm_frac": round(dec_bytes / (rt["dec"][0] * 1e-3) / 1e9 / PEAK_HBM_GBS, 4),
-            "ragged_lengths_supplementary": {
-                "lens": "uniform on [1, %d], seed 7, first full, second 1 token; total %d"
-                        % (dec.w.N, int(lens.sum())),
-                "ms": round(dr[0], 4), "dense_ms": round(drd[0], 4),
-                "speedup": round(drd[0] / dr[0], 4),
-                "retained_head_tiles_pct": pct(cdr[1], cdr[0]),
-                "hbm_gbs_algorithmic": round(rag_bytes / (dr[0] * 1e-3) / 1e9, 1),
-            },
+            "ragged_lengths_supplementary": ragged,
         },
         "decision_tile": [bq, bk],
         "tau1_supplementary": {
