@@ -268,7 +268,7 @@ def cpu_baseline(step_ms_model):
     w = Workload(4)
     bq, bk = mala.mala_geometry(w.D, mala.PASS_FWD)
     Tr = -(-w.N // bq)
-    nb = 2 * cores
+    nb = min(Tr, 16 * cores)   # ~10 s of fp64 work on the host cores
     i0 = Tr // 2 - nb // 2
     qf = bf16_to_f64(w.q_head(0, 0))[None, None]
     kf = bf16_to_f64(w.k_head(0, 0))[None, None]
@@ -295,7 +295,7 @@ def cpu_baseline(step_ms_model):
     kd = bf16_to_f64(wd.k_head(0, 0))[None, None]
     vd = bf16_to_f64(wd.v_head(0, 0))[None, None]
     t0 = time.time()
-    nh = 4
+    nh = 8
     for h in range(nh):
         oracle.mala_decode(qd, kd, vd, scale, float(np.float32(1e-4)),
                            mala.mala_geometry(wd.D, mala.PASS_DECODE)[1], sd)
