@@ -196,7 +196,7 @@ LM_SWEEP_TOKENS = 32768        # batch = tokens / N, so every length has the sam
 LM_SWEEP_TAUS = (1e-4, 1.0)
 
 
-def lm_sweep(reps, lengths=LM_SWEEP_N):
+def lm_sweep(reps, warmup, lengths=LM_SWEEP_N):
     """The language-model-like workload (8 query / 2 KV heads, head_dim 128) at context
     lengths 1K..32K: fwd/bwd time and retained work at tau = 0, 1e-4 and the canonical
     tau = 1, and the operator fidelity of tau > 0 against tau = 0 (same kernels)."""
@@ -208,8 +208,8 @@ def lm_sweep(reps, lengths=LM_SWEEP_N):
         nrows = w.B * w.Hq * w.N
         runs = {}
         for t_ in (0.0,) + LM_SWEEP_TAUS:
-            f = time_calls(lambda: tr.fwd(t_), reps, 1)
-            b = time_calls(lambda: tr.bwd(t_), reps, 1)
+            f = time_calls(lambda: tr.fwd(t_), reps, warmup)
+            b = time_calls(lambda: tr.bwd(t_), reps, warmup)
             cf, cb = tr.counters()
             runs[t_] = dict(fwd=f[0], bwd=b[0], cf=cf, cb=cb, out=tr.outputs())
         d = runs[0.0]
@@ -316,8 +316,8 @@ COUNTER_CMD = ("cd /tmp && export TMPDIR=/tmp && timeout -s KILL 180 rocprofv3 -
                "python $REPO/bench.py --counter-pass")
 TRACE_CMD = ("cd /tmp && export TMPDIR=/tmp && timeout -k 10 600 rocprofv3 --kernel-trace --stats "
              "--output-format csv -d $REPO/gpurun_out/trace_bench -o bench -- "
-             "python $REPO/bench.py --steps 2 --warmup 1 --reps 2 --no-cpu-baseline --no-32k "
-             "--no-lm --no-ragged")
+             "python $REPO/bench.py --steps 2 --warmup 1 --reps 2 --kernel-warmup 1 "
+             "--supp-reps 2 --supp-warmup 1 --no-cpu-baseline --no-32k --no-lm --no-ragged")
 
 
 def counter_pass():
@@ -537,7 +537,13 @@ def main():
     ap.add_argument("--steps", type=int, default=5)
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--tau", type=float, default=1e-4)
-    ap.add_argument("--reps", type=int, default=5, help="event-timed calls per kernel and tau")
+    ap.add_argument("--reps", type=int, default=100,
+                    help="event-timed calls per kernel at the measured taus (the paper's 100)")
+    ap.add_argument("--kernel-warmup", type=int, default=25,
+                    help="untimed calls before them (the paper's 25)")
+    ap.add_argument("--supp-reps", type=int, default=20,
+                    help="event-timed calls per kernel for the supplementary fields")
+    ap.add_argument("--supp-warmup", type=int, default=5)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-32k", action="store_true")
     ap.add_argument("--no-lm", action="store_true",
@@ -606,17 +612,18 @@ def main():
     # per-kernel event timings at tau and at tau = 0 (dense through the same kernels)
     res = {}
     for name, t_ in (("tau", tau), ("dense", 0.0)):
-        f = time_calls(lambda: tr.fwd(t_), args.reps, 1)
-        b = time_calls(lambda: tr.bwd(t_), args.reps, 1)
-        d = time_calls(lambda: dec.run(t_), args.reps, 1)
+        f = time_calls(lambda: tr.fwd(t_), args.reps, args.kernel_warmup)
+        b = time_calls(lambda: tr.bwd(t_), args.reps, args.kernel_warmup)
+        d = time_calls(lambda: dec.run(t_), args.reps, args.kernel_warmup)
         cf, cb = tr.counters()
         cd = dec.cnt.cpu().numpy()
         res[name] = dict(fwd=f, bwd=b, dec=d, cf=cf, cb=cb, cd=cd)
         log(name, "fwd %.2f bwd %.2f decode %.3f ms" % (f[0], b[0], d[0]))
     # supplementary: the paper's canonical tolerance tau = 1 on the same inputs
-    f1 = time_calls(lambda: tr.fwd(1.0), args.reps, 1)
-    b1 = time_calls(lambda: tr.bwd(1.0), args.reps, 1)
-    d1 = time_calls(lambda: dec.run(1.0), args.reps, 1)
+    sr, sw = args.supp_reps, args.supp_warmup
+    f1 = time_calls(lambda: tr.fwd(1.0), sr, sw)
+    b1 = time_calls(lambda: tr.bwd(1.0), sr, sw)
+    d1 = time_calls(lambda: dec.run(1.0), sr, sw)
     cf1, cb1 = tr.counters()
     cd1 = dec.cnt.cpu().numpy()
     log("tau=1 fwd %.2f bwd %.2f decode %.3f ms" % (f1[0], b1[0], d1[0]))
@@ -625,9 +632,9 @@ def main():
     if not args.no_ragged:
         lens = ragged_lengths(dec.w.B, dec.w.N)
         cl = torch.from_numpy(lens).to("cuda")
-        dr = time_calls(lambda: dec.run(tau, cl), args.reps, 1)
+        dr = time_calls(lambda: dec.run(tau, cl), sr, sw)
         cdr = dec.cnt.cpu().numpy()
-        drd = time_calls(lambda: dec.run(0.0, cl), args.reps, 1)
+        drd = time_calls(lambda: dec.run(0.0, cl), sr, sw)
         # K of every valid key, V of the tiles loaded (counted once per GQA group)
         rag_kv = float(lens.sum()) * dec.w.Hkv * dec.w.D * 2
         rag_bytes = rag_kv + rag_kv * cdr[2] / max(1, cdr[0] / dec.w.g)
@@ -677,6 +684,9 @@ def main():
             "ragged_lengths_supplementary": ragged,
         },
         "decision_tile": [bq, bk],
+        "timing_protocol": ("HIP events per call; measured taus: mean / median of %d calls after "
+                            "%d untimed; supplementary fields: %d after %d"
+                            % (args.reps, args.kernel_warmup, args.supp_reps, args.supp_warmup)),
         "tau1_supplementary": {
             "fwd_ms": round(f1[0], 3), "bwd_ms": round(b1[0], 3), "decode_ms": round(d1[0], 4),
             "speedup_fwd": round(rd["fwd"][0] / f1[0], 4),
@@ -696,8 +706,9 @@ def main():
         t3 = Train(3, tau)
         r3 = {}
         for name, t_ in (("tau", tau), ("dense", 0.0), ("tau1", 1.0)):
-            r3[name] = (time_calls(lambda: t3.fwd(t_), args.reps, 1),
-                        time_calls(lambda: t3.bwd(t_), args.reps, 1), t3.counters())
+            n_, w_ = (sr, sw) if name == "tau1" else (args.reps, args.kernel_warmup)
+            r3[name] = (time_calls(lambda: t3.fwd(t_), n_, w_),
+                        time_calls(lambda: t3.bwd(t_), n_, w_), t3.counters())
         (f3, b3, (cf3, cb3)), (f3d, b3d, _) = r3["tau"], r3["dense"]
         f31, b31, (cf31, cb31) = r3["tau1"]
         detail["32k"] = {
@@ -722,7 +733,7 @@ def main():
                      "shared by 32-row blocks beta=2, sink 1.5, Rademacher dO), 8 query / 2 KV "
                      "heads, head_dim 128, batch = 32768 / N; fidelity of tau > 0 against "
                      "tau = 0 through the same kernels: mean and P95 over heads, in percent"),
-            "rows": lm_sweep(args.reps),
+            "rows": lm_sweep(sr, sw),
         }
 
     line = {
