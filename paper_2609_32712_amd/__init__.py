@@ -20,7 +20,8 @@ import torch
 _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libmala.so")
 
-MALA_OK, MALA_ERR_INVALID_ARG, MALA_ERR_UNSUPPORTED, MALA_ERR_WORKSPACE, MALA_ERR_HIP = 0, -1, -2, -3, -4
+MALA_OK, MALA_ERR_INVALID_ARG, MALA_ERR_UNSUPPORTED = 0, -1, -2
+MALA_ERR_WORKSPACE, MALA_ERR_HIP = -3, -4
 PASS_FWD, PASS_BWD, PASS_DECODE = 0, 1, 2
 CNT_LEGAL, CNT_RETAINED, CNT_V_TILES, CNT_SLOTS = 0, 1, 2, 3
 
@@ -115,11 +116,13 @@ def mala_decode_workspace_size(B, Hq, D, num_splits):
 
 
 def mala_fwd(q, k, v, o, lse, row_tiles, counters, scale, tau, causal=1, stream=None):
-    _dev(q, torch.bfloat16, "q", 4), _dev(k, torch.bfloat16, "k", 4), _dev(v, torch.bfloat16, "v", 4)
+    for t, n in ((q, "q"), (k, "k"), (v, "v")):
+        _dev(t, torch.bfloat16, n, 4)
     _dev(o, torch.float32, "o", 4), _dev(lse, torch.float32, "lse", 3)
     B, Hq, Nq, D = q.shape
     Hkv, Nk = k.shape[1], k.shape[2]
-    if tuple(v.shape) != tuple(k.shape) or tuple(o.shape) != tuple(q.shape) or tuple(lse.shape) != (B, Hq, Nq):
+    if (tuple(v.shape) != tuple(k.shape) or tuple(o.shape) != tuple(q.shape)
+            or tuple(lse.shape) != (B, Hq, Nq)):
         raise ValueError("inconsistent shapes")
     if row_tiles is not None:
         _dev(row_tiles, torch.int32, "row_tiles", 3)
@@ -179,7 +182,8 @@ def _varlen_dims(q, k, cu_seqlens):
 
 def mala_fwd_varlen(q, k, v, cu_seqlens, max_seqlen, o, lse, row_tiles, counters, scale, tau,
                     stream=None):
-    _dev(q, torch.bfloat16, "q", 3), _dev(k, torch.bfloat16, "k", 3), _dev(v, torch.bfloat16, "v", 3)
+    for t, n in ((q, "q"), (k, "k"), (v, "v")):
+        _dev(t, torch.bfloat16, n, 3)
     _dev(o, torch.float32, "o", 3), _dev(lse, torch.float32, "lse", 2)
     S, Hq, Hkv, total, D = _varlen_dims(q, k, cu_seqlens)
     if tuple(v.shape) != tuple(k.shape) or tuple(o.shape) != tuple(q.shape) or \

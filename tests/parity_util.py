@@ -19,7 +19,8 @@ LSE_DIAG = 1e-3
 
 def dev(bits):
     """uint16 bf16 bit patterns (numpy) -> bf16 tensor on cuda:0."""
-    return torch.from_numpy(np.ascontiguousarray(bits).view(np.int16)).to("cuda").view(torch.bfloat16)
+    t = torch.from_numpy(np.ascontiguousarray(bits).view(np.int16))
+    return t.to("cuda").view(torch.bfloat16)
 
 
 def host(t):

@@ -16,7 +16,8 @@ HEADER = os.path.join(ROOT, "include", "mala.h")
 def declared_functions():
     src = open(HEADER).read()
     src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
-    return sorted(set(re.findall(r"^\s*(?:const\s+)?[\w]+\*?\s+\**(mala_\w+)\s*\(", src, flags=re.M)))
+    decl = r"^\s*(?:const\s+)?[\w]+\*?\s+\**(mala_\w+)\s*\("
+    return sorted(set(re.findall(decl, src, flags=re.M)))
 
 
 @pytest.fixture(scope="module")

@@ -367,7 +367,8 @@ def test_decode_splits_cover_dense_at_tau0():
     spec = dict(kind="decode", B=1, Hq=4, Hkv=1, N=2048, D=128, beta=3.0, needles=4)
     w = Workload(spec)
     t = w.tensors()
-    outs = [mala.decode(dev(t["q"]), dev(t["k"]), dev(t["v"]), f32(w.scale), 0.0, s) for s in (1, 5, 64)]
+    outs = [mala.decode(dev(t["q"]), dev(t["k"]), dev(t["v"]), f32(w.scale), 0.0, s)
+            for s in (1, 5, 64)]
     torch.cuda.synchronize()
     for o in outs[1:]:
         np.testing.assert_allclose(host(o["o"]), host(outs[0]["o"]), atol=1e-5)
@@ -528,4 +529,64 @@ def test_repeat_runs_bitwise_forward_dk_dv():
     assert torch.equal(r1["o"], r2["o"]) and torch.equal(r1["lse"], r2["lse"])
     assert torch.equal(b1["dk"], b2["dk"]) and torch.equal(b1["dv"], b2["dv"])
     assert torch.equal(b1["dq"], b2["dq"])
-    assert torch.equal(b1["row_tiles"], b2["row_tiles"]) and torch.equal(r1["row_tiles"], r2["row_tiles"])
+    assert torch.equal(b1["row_tiles"], b2["row_tiles"])
+    assert torch.equal(r1["row_tiles"], r2["row_tiles"])
+
+
+def test_graph_capture_replays_match_eager():
+    # The library only launches kernels on the caller's stream (counters are
+    # cleared by a kernel, not by hipMemsetAsync, and nothing is allocated), so a
+    # fwd + bwd + decode step captured in a HIP graph replays to the eager results;
+    # every replay is checked, with eager work on the outputs in between.
+    tau = 1e-3
+    w, q, k, v, do = _train_case("gqa_d128_ragged", tau)
+    Q, K, V, DO = map(dev, (q, k, v, do))
+    scale = f32(w.scale)
+    B, Hq, N, D = Q.shape
+    Hkv = K.shape[1]
+    f = dict(dtype=torch.float32, device="cuda")
+    i32 = dict(dtype=torch.int32, device="cuda")
+    o, lse = torch.empty((B, Hq, N, D), **f), torch.empty((B, Hq, N), **f)
+    dq = torch.empty_like(o)
+    dk, dv = torch.empty((B, Hkv, N, D), **f), torch.empty((B, Hkv, N, D), **f)
+    rt, rtb = torch.empty((B, Hq, N), **i32), torch.empty((B, Hq, N), **i32)
+    cf, cb, cd = (torch.empty(4, dtype=torch.int64, device="cuda") for _ in range(3))
+    ws = torch.empty(mala.mala_bwd_workspace_size(B, Hq, Hkv, N, N, D), dtype=torch.uint8,
+                     device="cuda")
+    wd = Workload(dict(kind="decode", B=2, Hq=8, Hkv=2, N=3001, D=128, beta=3.0, needles=4))
+    td = wd.tensors()
+    qd, kd, vd = dev(td["q"]), dev(td["k"]), dev(td["v"])
+    S = 4
+    od, lsed = torch.empty((2, 8, 128), **f), torch.empty((2, 8), **f)
+    ht = torch.empty((2, 8), **i32)
+    wsd = torch.empty(mala.mala_decode_workspace_size(2, 8, 128, S), dtype=torch.uint8,
+                      device="cuda")
+    lens = torch.tensor([3001, 1000], **i32)
+
+    def step():
+        mala.mala_fwd(Q, K, V, o, lse, rt, cf, scale, tau)
+        mala.mala_bwd(Q, K, V, o, lse, DO, dq, dk, dv, rtb, cb, ws, scale, tau)
+        mala.mala_decode(qd, kd, vd, od, lsed, ht, cd, S, wsd, f32(wd.scale), tau,
+                         cache_lens=lens)
+
+    outs = (o, lse, rt, cf, dq, dk, dv, rtb, cb, od, lsed, ht, cd)
+    step()
+    torch.cuda.synchronize()
+    ref = [x.clone() for x in outs]
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):     # warm-up on a side stream before capture
+        step()
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        step()
+    for i in range(3):
+        for x in outs:
+            x.fill_(-7)
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        for a, b in zip(outs, ref):
+            assert torch.equal(a, b), i

@@ -39,19 +39,23 @@ CONFIGS = {
     1: dict(kind="train", B=1, Hq=1, Hkv=1, N=1024, D=64, beta=2.0, local=0.0,
             taus=(0.0, 1e-4, 1e-3), desc="causal fwd+bwd, 1x1x1024x64, needle beta=2"),
     2: dict(kind="train", B=1, Hq=16, Hkv=16, N=8192, D=128, beta=2.0, local=1.0,
-            taus=(0.0, 1e-4, 1e-3), desc="causal fwd+bwd, MHA 16 heads, 8192x128, needle beta=2 + local 1.0"),
+            taus=(0.0, 1e-4, 1e-3),
+            desc="causal fwd+bwd, MHA 16 heads, 8192x128, needle beta=2 + local 1.0"),
     3: dict(kind="train", B=1, Hq=32, Hkv=8, N=32768, D=128, beta=(0.5, 3.0), local=0.0,
             taus=(0.0, 1e-4), desc="causal fwd+bwd, GQA 32/8, 32768x128, per-head beta~U[0.5,3]"),
     4: dict(kind="train", B=1, Hq=8, Hkv=2, N=131072, D=128, beta=2.0, local=0.0,
-            taus=(0.0, 1e-4), desc="causal fwd+bwd, GQA 8/2 (one TP=8 share), 131072x128, beta=2"),
+            taus=(0.0, 1e-4),
+            desc="causal fwd+bwd, GQA 8/2 (one TP=8 share), 131072x128, beta=2"),
     5: dict(kind="decode", B=16, Hq=32, Hkv=8, N=131072, D=128, beta=3.0, needles=4,
-            taus=(0.0, 1e-4), desc="decode, 16 x GQA 32/8 over 131072-token caches, 4 needles beta=3"),
+            taus=(0.0, 1e-4),
+            desc="decode, 16 x GQA 32/8 over 131072-token caches, 4 needles beta=3"),
     # supplementary: a workload on which the forward rule can skip (a dominant local
     # key found in the diagonal tile, needles shared by 32-row blocks, a sink), with
     # a Rademacher dO for the fidelity measurements
     6: dict(kind="train", B=1, Hq=8, Hkv=2, N=32768, D=128, beta=2.0, local=2.0,
             needle_block=32, sink=1.5, do="rademacher", taus=(0.0, 1e-4, 1.0),
-            desc="causal fwd+bwd, GQA 8/2, 32768x128, LM-like: local 2, block needles beta=2, sink 1.5"),
+            desc="causal fwd+bwd, GQA 8/2, 32768x128, LM-like: local 2, block needles beta=2, "
+                 "sink 1.5"),
 }
 
 
