@@ -20,8 +20,9 @@
  *     in BHSD layout (batch, head, sequence, head_dim).  The library never
  *     allocates, frees or retains them.
  *   - Q, K, V, dO, the KV caches and the decode query are bf16 (passed as void*);
- *     O, LSE and the gradients are fp32; LSE is the natural-log normalizer
- *     z_q = log sum_{k in R_q} exp(s_qk) of the retained set R_q.
+ *     O and the gradients are fp32 or bf16 (MALA_OUT_*), LSE is fp32; LSE is the
+ *     natural-log normalizer z_q = log sum_{k in R_q} exp(s_qk) of the retained
+ *     set R_q.
  *   - scale multiplies Q.K in fp32 (the paper absorbs it into Q; it is never
  *     re-rounded to bf16 here); tau >= 0 (tau = 0 runs every tile: dense
  *     attention through the same kernels).
@@ -55,7 +56,7 @@ typedef enum {
   MALA_OK = 0,
   MALA_ERR_INVALID_ARG = -1, /* null required pointer, non-positive size, Hq % Hkv != 0,
                                 Nq > Nk, tau < 0 or NaN, scale not finite or <= 0,
-                                num_splits < 1 */
+                                num_splits < 1, an output type not MALA_OUT_* */
   MALA_ERR_UNSUPPORTED = -2, /* head_dim not in {64, 128}, causal == 0 (the paper's
                                 traversal is defined for causal attention only), or a
                                 forward/backward K/V slice of 2^32 bytes or more */
@@ -79,6 +80,12 @@ enum {
 
 enum { MALA_PASS_FWD = 0, MALA_PASS_BWD = 1, MALA_PASS_DECODE = 2 };
 
+/* Element type of O and of the gradients (the *_dtype arguments).  Outputs are
+ * computed in fp32 and either stored as fp32 or rounded once to bf16 (nearest
+ * even) at the store; LSE is always fp32.  A bf16 O given to the backward enters
+ * D_q = rowsum(O * dO) with its rounding. */
+enum { MALA_OUT_F32 = 0, MALA_OUT_BF16 = 1 };
+
 /* Decision tile of a pass: B_q query rows x B_k keys. */
 typedef struct {
   int32_t block_q;
@@ -98,7 +105,8 @@ const char* mala_last_error(void);
 /*
  * MALA forward (Algorithm 1), also the prefill operator.
  *   q:  bf16 [B, Hq,  Nq, D]        k, v: bf16 [B, Hkv, Nk, D]
- *   o:  fp32 [B, Hq, Nq, D]  out    softmax output renormalised over the retained set
+ *   o:  [B, Hq, Nq, D] out, fp32 or bf16 by out_dtype: softmax output renormalised
+ *       over the retained set
  *   lse: fp32 [B, Hq, Nq]    out    natural-log normalizer z_q = m_q + log l_q
  *   row_tiles: int32 [B, Hq, Nq] or NULL   out: retained tiles in which the row has a
  *              legal key
@@ -106,9 +114,9 @@ const char* mala_last_error(void);
  *   causal must be 1.  Requires Nq <= Nk, D in {64, 128} and Nk * D * 2 < 2^32
  *   (Nk below 16M tokens at D = 128); otherwise MALA_ERR_UNSUPPORTED.
  */
-int mala_fwd(const void* q, const void* k, const void* v, float* o, float* lse,
+int mala_fwd(const void* q, const void* k, const void* v, void* o, float* lse,
              int32_t* row_tiles, int64_t* counters, int B, int Hq, int Hkv, int Nq, int Nk,
-             int D, int causal, float scale, float tau, void* stream);
+             int D, int causal, float scale, float tau, int out_dtype, void* stream);
 
 /* Bytes of device workspace mala_bwd needs for this shape (the per-row
  * D_q = rowsum(O_q * dO_q) vector of Algorithm 2). */
@@ -117,11 +125,12 @@ size_t mala_bwd_workspace_size(int B, int Hq, int Hkv, int Nq, int Nk, int D);
 /*
  * MALA backward (Algorithm 2): gradients of <O, dO> restricted to the tiles that
  * pass the offline test against the saved lse.
- *   q: bf16 [B, Hq, Nq, D]; k, v: bf16 [B, Hkv, Nk, D]; o: fp32 [B, Hq, Nq, D] and
- *   lse: fp32 [B, Hq, Nq] as returned by mala_fwd; dout: bf16 [B, Hq, Nq, D].
- *   dq: fp32 [B, Hq, Nq, D] out; dk, dv: fp32 [B, Hkv, Nk, D] out (dK and dV of a
- *       KV head summed over its GQA group).  No atomics: all three are bitwise
- *       reproducible.  dQ comes from a query-major pass that recomputes the
+ *   q: bf16 [B, Hq, Nq, D]; k, v: bf16 [B, Hkv, Nk, D]; o: [B, Hq, Nq, D] (fp32 or
+ *   bf16 by o_dtype) and lse: fp32 [B, Hq, Nq] as returned by mala_fwd; dout: bf16
+ *   [B, Hq, Nq, D].
+ *   dq: [B, Hq, Nq, D] out; dk, dv: [B, Hkv, Nk, D] out (dK and dV of a KV head
+ *       summed over its GQA group); all three fp32 or bf16 by grad_dtype.  No
+ *       atomics: all three are bitwise reproducible.  dQ comes from a query-major pass that recomputes the
  *       tile scores with the same arithmetic, so it uses exactly the tiles the
  *       key-major dK/dV pass retains;
  *   row_tiles: int32 [B, Hq, Nq] or NULL out; counters: int64 [4] or NULL out.
@@ -129,10 +138,11 @@ size_t mala_bwd_workspace_size(int B, int Hq, int Hkv, int Nq, int Nk, int D);
  *   16-byte aligned, owned by the caller, not read by the caller afterwards.
  *   The shape limits of mala_fwd apply.
  */
-int mala_bwd(const void* q, const void* k, const void* v, const float* o, const float* lse,
-             const void* dout, float* dq, float* dk, float* dv, int32_t* row_tiles,
+int mala_bwd(const void* q, const void* k, const void* v, const void* o, const float* lse,
+             const void* dout, void* dq, void* dk, void* dv, int32_t* row_tiles,
              int64_t* counters, void* workspace, size_t workspace_bytes, int B, int Hq, int Hkv,
-             int Nq, int Nk, int D, int causal, float scale, float tau, void* stream);
+             int Nq, int Nk, int D, int causal, float scale, float tau, int o_dtype,
+             int grad_dtype, void* stream);
 
 /*
  * Packed variable-length batches (the forward of Algorithm 1 per sequence).
@@ -141,7 +151,7 @@ int mala_bwd(const void* q, const void* k, const void* v, const float* o, const 
  * only (its i-th row sees its rows 0..i, L_q = i + 1) and is tiled from its own
  * first row, exactly as a batch of one with Nq = Nk = its length.
  *   q: bf16 [Hq, total, D]; k, v: bf16 [Hkv, total, D] (head-major: the fixed-length
- *   layout with B = 1 and N = total); o: fp32 [Hq, total, D] out; lse: fp32
+ *   layout with B = 1 and N = total); o: [Hq, total, D] out (out_dtype); lse: fp32
  *   [Hq, total] out; row_tiles: int32 [Hq, total] or NULL out; counters as mala_fwd.
  *   cu_seqlens: int32 [num_seqs + 1] device array, non-decreasing from 0 to at
  *   most total; max_seqlen: the longest sequence (the launch is sized by it).
@@ -151,22 +161,23 @@ int mala_bwd(const void* q, const void* k, const void* v, const float* o, const 
  *   and total * D * 2 < 2^32.
  */
 int mala_fwd_varlen(const void* q, const void* k, const void* v, const int32_t* cu_seqlens,
-                    float* o, float* lse, int32_t* row_tiles, int64_t* counters, int num_seqs,
+                    void* o, float* lse, int32_t* row_tiles, int64_t* counters, int num_seqs,
                     int max_seqlen, int total, int Hq, int Hkv, int D, float scale, float tau,
-                    void* stream);
+                    int out_dtype, void* stream);
 
 /*
  * Packed variable-length batches: mala_bwd (Algorithm 2) per sequence, on the
- * layout of mala_fwd_varlen (o, lse as it returned them; dout, dq: [Hq, total, D];
- * dk, dv: fp32 [Hkv, total, D] out).  workspace: at least
+ * layout of mala_fwd_varlen (o, lse as it returned them, o of type o_dtype; dout,
+ * dq: [Hq, total, D]; dk, dv: [Hkv, total, D]; gradients of type grad_dtype).  workspace: at least
  * mala_bwd_workspace_size(1, Hq, Hkv, total, total, D) bytes.  Rows that no
  * sequence covers are not written.
  */
 int mala_bwd_varlen(const void* q, const void* k, const void* v, const int32_t* cu_seqlens,
-                    const float* o, const float* lse, const void* dout, float* dq, float* dk,
-                    float* dv, int32_t* row_tiles, int64_t* counters, void* workspace,
+                    const void* o, const float* lse, const void* dout, void* dq, void* dk,
+                    void* dv, int32_t* row_tiles, int64_t* counters, void* workspace,
                     size_t workspace_bytes, int num_seqs, int max_seqlen, int total, int Hq,
-                    int Hkv, int D, float scale, float tau, void* stream);
+                    int Hkv, int D, float scale, float tau, int o_dtype, int grad_dtype,
+                    void* stream);
 
 /* Bytes of device workspace mala_decode needs: fp32 split partials
  * [B, Hq, num_splits, D + 4] (O_s / l_s, lse_s, retained count, pad). */
@@ -181,7 +192,7 @@ size_t mala_decode_workspace_size(int B, int Hq, int D, int num_splits);
  *       its query sees them all (L = n_b) and its ceil(n_b / B_k) key tiles are cut
  *       into the splits as below.  Values are clamped into [0, Nk]; a sequence with
  *       n_b = 0 gets o = 0 and lse = -inf.  NULL means n_b = Nk for every sequence.
- *   o: fp32 [B, Hq, D] out; lse: fp32 [B, Hq] out
+ *   o: [B, Hq, D] out (fp32 or bf16 by out_dtype); lse: fp32 [B, Hq] out
  *   head_tiles: int32 [B, Hq] or NULL out (retained tiles summed over splits)
  *   counters: int64 [4] or NULL out
  *   num_splits >= 1: a sequence's key tiles (T = ceil(n_b / B_k) of them) are cut
@@ -190,9 +201,10 @@ size_t mala_decode_workspace_size(int B, int Hq, int D, int num_splits);
  *   workspace: at least mala_decode_workspace_size(...) bytes.
  */
 int mala_decode(const void* q, const void* k_cache, const void* v_cache,
-                const int32_t* cache_lens, float* o, float* lse, int32_t* head_tiles,
+                const int32_t* cache_lens, void* o, float* lse, int32_t* head_tiles,
                 int64_t* counters, int num_splits, void* workspace, size_t workspace_bytes,
-                int B, int Hq, int Hkv, int Nk, int D, float scale, float tau, void* stream);
+                int B, int Hq, int Hkv, int Nk, int D, float scale, float tau, int out_dtype,
+                void* stream);
 
 #ifdef __cplusplus
 }

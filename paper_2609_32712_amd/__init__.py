@@ -23,6 +23,7 @@ LIB_PATH = os.path.join(_HERE, "libmala.so")
 MALA_OK, MALA_ERR_INVALID_ARG, MALA_ERR_UNSUPPORTED = 0, -1, -2
 MALA_ERR_WORKSPACE, MALA_ERR_HIP = -3, -4
 PASS_FWD, PASS_BWD, PASS_DECODE = 0, 1, 2
+OUT_F32, OUT_BF16 = 0, 1
 CNT_LEGAL, CNT_RETAINED, CNT_V_TILES, CNT_SLOTS = 0, 1, 2, 3
 
 EXPORTS = ("mala_geometry", "mala_strerror", "mala_last_error", "mala_fwd",
@@ -59,19 +60,19 @@ def load_library():
     lib.mala_strerror.restype = ctypes.c_char_p
     lib.mala_last_error.argtypes = []
     lib.mala_last_error.restype = ctypes.c_char_p
-    lib.mala_fwd.argtypes = [vp] * 7 + [i] * 7 + [f, f, vp]
+    lib.mala_fwd.argtypes = [vp] * 7 + [i] * 7 + [f, f, i, vp]
     lib.mala_fwd.restype = i
     lib.mala_bwd_workspace_size.argtypes = [i] * 6
     lib.mala_bwd_workspace_size.restype = sz
-    lib.mala_bwd.argtypes = [vp] * 12 + [sz] + [i] * 7 + [f, f, vp]
+    lib.mala_bwd.argtypes = [vp] * 12 + [sz] + [i] * 7 + [f, f, i, i, vp]
     lib.mala_bwd.restype = i
-    lib.mala_fwd_varlen.argtypes = [vp] * 8 + [i] * 6 + [f, f, vp]
+    lib.mala_fwd_varlen.argtypes = [vp] * 8 + [i] * 6 + [f, f, i, vp]
     lib.mala_fwd_varlen.restype = i
-    lib.mala_bwd_varlen.argtypes = [vp] * 13 + [sz] + [i] * 6 + [f, f, vp]
+    lib.mala_bwd_varlen.argtypes = [vp] * 13 + [sz] + [i] * 6 + [f, f, i, i, vp]
     lib.mala_bwd_varlen.restype = i
     lib.mala_decode_workspace_size.argtypes = [i] * 4
     lib.mala_decode_workspace_size.restype = sz
-    lib.mala_decode.argtypes = [vp] * 8 + [i, vp, sz] + [i] * 5 + [f, f, vp]
+    lib.mala_decode.argtypes = [vp] * 8 + [i, vp, sz] + [i] * 5 + [f, f, i, vp]
     lib.mala_decode.restype = i
     _lib = lib
     return lib
@@ -96,9 +97,20 @@ def _check(status):
 def _dev(t, dtype, name, dims):
     if not isinstance(t, torch.Tensor) or not t.is_cuda:
         raise TypeError("%s must be a CUDA (HIP) tensor" % name)
-    if t.dtype != dtype or not t.is_contiguous() or t.dim() != dims:
+    ok = t.dtype in dtype if isinstance(dtype, tuple) else t.dtype == dtype
+    if not ok or not t.is_contiguous() or t.dim() != dims:
         raise TypeError("%s must be a contiguous %d-d %s tensor" % (name, dims, dtype))
     return t
+
+
+_OUT = (torch.float32, torch.bfloat16)
+
+
+def _out_code(*ts):
+    """MALA_OUT_* of output tensors that must share one type (fp32 or bf16)."""
+    if len({t.dtype for t in ts}) != 1:
+        raise TypeError("these outputs must share one dtype")
+    return OUT_BF16 if ts[0].dtype == torch.bfloat16 else OUT_F32
 
 
 # ---------------------------------------------------------------- C names
@@ -118,7 +130,7 @@ def mala_decode_workspace_size(B, Hq, D, num_splits):
 def mala_fwd(q, k, v, o, lse, row_tiles, counters, scale, tau, causal=1, stream=None):
     for t, n in ((q, "q"), (k, "k"), (v, "v")):
         _dev(t, torch.bfloat16, n, 4)
-    _dev(o, torch.float32, "o", 4), _dev(lse, torch.float32, "lse", 3)
+    _dev(o, _OUT, "o", 4), _dev(lse, torch.float32, "lse", 3)
     B, Hq, Nq, D = q.shape
     Hkv, Nk = k.shape[1], k.shape[2]
     if (tuple(v.shape) != tuple(k.shape) or tuple(o.shape) != tuple(q.shape)
@@ -130,32 +142,33 @@ def mala_fwd(q, k, v, o, lse, row_tiles, counters, scale, tau, causal=1, stream=
         _dev(counters, torch.int64, "counters", 1)
     _check(load_library().mala_fwd(_ptr(q), _ptr(k), _ptr(v), _ptr(o), _ptr(lse), _ptr(row_tiles),
                                    _ptr(counters), B, Hq, Hkv, Nq, Nk, D, causal, scale, tau,
-                                   _stream(stream)))
+                                   _out_code(o), _stream(stream)))
 
 
 def mala_bwd(q, k, v, o, lse, dout, dq, dk, dv, row_tiles, counters, workspace, scale, tau,
              causal=1, stream=None):
     for t, n, dt, nd in ((q, "q", torch.bfloat16, 4), (k, "k", torch.bfloat16, 4),
-                         (v, "v", torch.bfloat16, 4), (o, "o", torch.float32, 4),
+                         (v, "v", torch.bfloat16, 4), (o, "o", _OUT, 4),
                          (lse, "lse", torch.float32, 3), (dout, "dout", torch.bfloat16, 4),
-                         (dq, "dq", torch.float32, 4), (dk, "dk", torch.float32, 4),
-                         (dv, "dv", torch.float32, 4)):
+                         (dq, "dq", _OUT, 4), (dk, "dk", _OUT, 4), (dv, "dv", _OUT, 4)):
         _dev(t, dt, n, nd)
     B, Hq, Nq, D = q.shape
     Hkv, Nk = k.shape[1], k.shape[2]
     if (tuple(dq.shape) != tuple(q.shape) or tuple(dout.shape) != tuple(q.shape)
-            or tuple(dk.shape) != tuple(k.shape) or tuple(dv.shape) != tuple(k.shape)):
+            or tuple(o.shape) != tuple(q.shape) or tuple(dk.shape) != tuple(k.shape)
+            or tuple(dv.shape) != tuple(k.shape)):
         raise ValueError("inconsistent shapes")
     _check(load_library().mala_bwd(_ptr(q), _ptr(k), _ptr(v), _ptr(o), _ptr(lse), _ptr(dout),
                                    _ptr(dq), _ptr(dk), _ptr(dv), _ptr(row_tiles), _ptr(counters),
                                    _ptr(workspace), workspace.numel() * workspace.element_size(),
-                                   B, Hq, Hkv, Nq, Nk, D, causal, scale, tau, _stream(stream)))
+                                   B, Hq, Hkv, Nq, Nk, D, causal, scale, tau, _out_code(o),
+                                   _out_code(dq, dk, dv), _stream(stream)))
 
 
 def mala_decode(q, k_cache, v_cache, o, lse, head_tiles, counters, num_splits, workspace, scale,
                 tau, stream=None, cache_lens=None):
     _dev(q, torch.bfloat16, "q", 3), _dev(k_cache, torch.bfloat16, "k_cache", 4)
-    _dev(v_cache, torch.bfloat16, "v_cache", 4), _dev(o, torch.float32, "o", 3)
+    _dev(v_cache, torch.bfloat16, "v_cache", 4), _dev(o, _OUT, "o", 3)
     _dev(lse, torch.float32, "lse", 2)
     B, Hq, D = q.shape
     Hkv, Nk = k_cache.shape[1], k_cache.shape[2]
@@ -167,7 +180,7 @@ def mala_decode(q, k_cache, v_cache, o, lse, head_tiles, counters, num_splits, w
                                       _ptr(o), _ptr(lse), _ptr(head_tiles), _ptr(counters),
                                       num_splits, _ptr(workspace),
                                       workspace.numel() * workspace.element_size(), B, Hq, Hkv,
-                                      Nk, D, scale, tau, _stream(stream)))
+                                      Nk, D, scale, tau, _out_code(o), _stream(stream)))
 
 
 def _varlen_dims(q, k, cu_seqlens):
@@ -184,7 +197,7 @@ def mala_fwd_varlen(q, k, v, cu_seqlens, max_seqlen, o, lse, row_tiles, counters
                     stream=None):
     for t, n in ((q, "q"), (k, "k"), (v, "v")):
         _dev(t, torch.bfloat16, n, 3)
-    _dev(o, torch.float32, "o", 3), _dev(lse, torch.float32, "lse", 2)
+    _dev(o, _OUT, "o", 3), _dev(lse, torch.float32, "lse", 2)
     S, Hq, Hkv, total, D = _varlen_dims(q, k, cu_seqlens)
     if tuple(v.shape) != tuple(k.shape) or tuple(o.shape) != tuple(q.shape) or \
             tuple(lse.shape) != (Hq, total):
@@ -196,16 +209,15 @@ def mala_fwd_varlen(q, k, v, cu_seqlens, max_seqlen, o, lse, row_tiles, counters
     _check(load_library().mala_fwd_varlen(_ptr(q), _ptr(k), _ptr(v), _ptr(cu_seqlens), _ptr(o),
                                           _ptr(lse), _ptr(row_tiles), _ptr(counters), S,
                                           int(max_seqlen), total, Hq, Hkv, D, scale, tau,
-                                          _stream(stream)))
+                                          _out_code(o), _stream(stream)))
 
 
 def mala_bwd_varlen(q, k, v, cu_seqlens, max_seqlen, o, lse, dout, dq, dk, dv, row_tiles,
                     counters, workspace, scale, tau, stream=None):
     for t, n, dt, nd in ((q, "q", torch.bfloat16, 3), (k, "k", torch.bfloat16, 3),
-                         (v, "v", torch.bfloat16, 3), (o, "o", torch.float32, 3),
+                         (v, "v", torch.bfloat16, 3), (o, "o", _OUT, 3),
                          (lse, "lse", torch.float32, 2), (dout, "dout", torch.bfloat16, 3),
-                         (dq, "dq", torch.float32, 3), (dk, "dk", torch.float32, 3),
-                         (dv, "dv", torch.float32, 3)):
+                         (dq, "dq", _OUT, 3), (dk, "dk", _OUT, 3), (dv, "dv", _OUT, 3)):
         _dev(t, dt, n, nd)
     S, Hq, Hkv, total, D = _varlen_dims(q, k, cu_seqlens)
     if (tuple(dq.shape) != tuple(q.shape) or tuple(dout.shape) != tuple(q.shape)
@@ -217,13 +229,14 @@ def mala_bwd_varlen(q, k, v, cu_seqlens, max_seqlen, o, lse, dout, dq, dk, dv, r
                                           _ptr(row_tiles), _ptr(counters), _ptr(workspace),
                                           workspace.numel() * workspace.element_size(), S,
                                           int(max_seqlen), total, Hq, Hkv, D, scale, tau,
-                                          _stream(stream)))
+                                          _out_code(o), _out_code(dq, dk, dv), _stream(stream)))
 
 
 # ---------------------------------------------------------------- allocating wrappers
-def fwd(q, k, v, scale, tau, stats=True, stream=None):
+def fwd(q, k, v, scale, tau, stats=True, stream=None, out_dtype=torch.float32):
+    """out_dtype: torch.float32 or torch.bfloat16 for O (LSE is always fp32)."""
     B, Hq, Nq, D = q.shape
-    o = torch.empty((B, Hq, Nq, D), dtype=torch.float32, device=q.device)
+    o = torch.empty((B, Hq, Nq, D), dtype=out_dtype, device=q.device)
     lse = torch.empty((B, Hq, Nq), dtype=torch.float32, device=q.device)
     rt = torch.empty((B, Hq, Nq), dtype=torch.int32, device=q.device) if stats else None
     cnt = torch.empty(4, dtype=torch.int64, device=q.device) if stats else None
@@ -231,12 +244,14 @@ def fwd(q, k, v, scale, tau, stats=True, stream=None):
     return dict(o=o, lse=lse, row_tiles=rt, counters=cnt)
 
 
-def bwd(q, k, v, o, lse, dout, scale, tau, stats=True, workspace=None, stream=None):
+def bwd(q, k, v, o, lse, dout, scale, tau, stats=True, workspace=None, stream=None,
+        grad_dtype=torch.float32):
+    """o as fwd returned it (fp32 or bf16); grad_dtype: fp32 or bf16 dQ, dK, dV."""
     B, Hq, Nq, D = q.shape
     Hkv, Nk = k.shape[1], k.shape[2]
-    dq = torch.empty((B, Hq, Nq, D), dtype=torch.float32, device=q.device)
-    dk = torch.empty((B, Hkv, Nk, D), dtype=torch.float32, device=q.device)
-    dv = torch.empty((B, Hkv, Nk, D), dtype=torch.float32, device=q.device)
+    dq = torch.empty((B, Hq, Nq, D), dtype=grad_dtype, device=q.device)
+    dk = torch.empty((B, Hkv, Nk, D), dtype=grad_dtype, device=q.device)
+    dv = torch.empty((B, Hkv, Nk, D), dtype=grad_dtype, device=q.device)
     rt = torch.empty((B, Hq, Nq), dtype=torch.int32, device=q.device) if stats else None
     cnt = torch.empty(4, dtype=torch.int64, device=q.device) if stats else None
     if workspace is None:
@@ -247,11 +262,11 @@ def bwd(q, k, v, o, lse, dout, scale, tau, stats=True, workspace=None, stream=No
 
 
 def decode(q, k_cache, v_cache, scale, tau, num_splits, stats=True, workspace=None, stream=None,
-           cache_lens=None):
+           cache_lens=None, out_dtype=torch.float32):
     """cache_lens: optional int32 [B] device tensor of valid cache tokens per sequence
     (keys [0, n_b) of k_cache[b] / v_cache[b]); None means every sequence holds Nk."""
     B, Hq, D = q.shape
-    o = torch.empty((B, Hq, D), dtype=torch.float32, device=q.device)
+    o = torch.empty((B, Hq, D), dtype=out_dtype, device=q.device)
     lse = torch.empty((B, Hq), dtype=torch.float32, device=q.device)
     ht = torch.empty((B, Hq), dtype=torch.int32, device=q.device) if stats else None
     cnt = torch.empty(4, dtype=torch.int64, device=q.device) if stats else None
@@ -263,11 +278,12 @@ def decode(q, k_cache, v_cache, scale, tau, num_splits, stats=True, workspace=No
     return dict(o=o, lse=lse, head_tiles=ht, counters=cnt)
 
 
-def fwd_varlen(q, k, v, cu_seqlens, max_seqlen, scale, tau, stats=True, stream=None):
+def fwd_varlen(q, k, v, cu_seqlens, max_seqlen, scale, tau, stats=True, stream=None,
+               out_dtype=torch.float32):
     """Packed batch: q [Hq, total, D], k, v [Hkv, total, D], cu_seqlens int32 [S + 1].
     Rows that no sequence covers come back as zeros."""
     Hq, total, D = q.shape
-    o = torch.zeros((Hq, total, D), dtype=torch.float32, device=q.device)
+    o = torch.zeros((Hq, total, D), dtype=out_dtype, device=q.device)
     lse = torch.zeros((Hq, total), dtype=torch.float32, device=q.device)
     rt = torch.zeros((Hq, total), dtype=torch.int32, device=q.device) if stats else None
     cnt = torch.empty(4, dtype=torch.int64, device=q.device) if stats else None
@@ -276,12 +292,12 @@ def fwd_varlen(q, k, v, cu_seqlens, max_seqlen, scale, tau, stats=True, stream=N
 
 
 def bwd_varlen(q, k, v, cu_seqlens, max_seqlen, o, lse, dout, scale, tau, stats=True,
-               workspace=None, stream=None):
+               workspace=None, stream=None, grad_dtype=torch.float32):
     Hq, total, D = q.shape
     Hkv = k.shape[0]
-    dq = torch.zeros((Hq, total, D), dtype=torch.float32, device=q.device)
-    dk = torch.zeros((Hkv, total, D), dtype=torch.float32, device=q.device)
-    dv = torch.zeros((Hkv, total, D), dtype=torch.float32, device=q.device)
+    dq = torch.zeros((Hq, total, D), dtype=grad_dtype, device=q.device)
+    dk = torch.zeros((Hkv, total, D), dtype=grad_dtype, device=q.device)
+    dv = torch.zeros((Hkv, total, D), dtype=grad_dtype, device=q.device)
     rt = torch.zeros((Hq, total), dtype=torch.int32, device=q.device) if stats else None
     cnt = torch.empty(4, dtype=torch.int64, device=q.device) if stats else None
     if workspace is None:

@@ -89,8 +89,8 @@ namespace {
 // Nq / Nk rows each (packed: Nq = Nk = total, the head stride), cu the packed
 // sequence starts or null.
 int run_fwd(const void* q, const void* k, const void* v, const int32_t* cu, int max_len,
-            float* o, float* lse, int32_t* row_tiles, int64_t* counters, int B, int Hq, int Hkv,
-            int Nq, int Nk, int D, float scale, float tau, hipStream_t s) {
+            void* o, int o_dtype, float* lse, int32_t* row_tiles, int64_t* counters, int B,
+            int Hq, int Hkv, int Nq, int Nk, int D, float scale, float tau, hipStream_t s) {
   if (counters) {
     hipError_t e = mala::launch_fill_zero(counters, 4 * sizeof(int64_t), s);
     if (e != hipSuccess) return hip_fail(e, "mala_fwd: clearing counters");
@@ -100,6 +100,7 @@ int run_fwd(const void* q, const void* k, const void* v, const int32_t* cu, int 
   p.k = (const __bf16*)k;
   p.v = (const __bf16*)v;
   p.o = o;
+  p.o_bf16 = o_dtype == MALA_OUT_BF16;
   p.lse = lse;
   p.row_tiles = row_tiles;
   p.counters = (unsigned long long*)counters;
@@ -115,16 +116,18 @@ int run_fwd(const void* q, const void* k, const void* v, const int32_t* cu, int 
 }
 
 int run_bwd(const void* q, const void* k, const void* v, const int32_t* cu, int max_len,
-            const float* o, const float* lse, const void* dout, float* dq, float* dk, float* dv,
-            int32_t* row_tiles, int64_t* counters, void* workspace, int B, int Hq, int Hkv,
-            int Nq, int Nk, int D, float scale, float tau, hipStream_t s) {
+            const void* o, int o_dtype, const float* lse, const void* dout, void* dq, void* dk,
+            void* dv, int grad_dtype, int32_t* row_tiles, int64_t* counters, void* workspace,
+            int B, int Hq, int Hkv, int Nq, int Nk, int D, float scale, float tau,
+            hipStream_t s) {
   hipError_t e;
   // D_q over every row of the q-shaped tensors (packed: all heads x total rows)
   const long rows = cu ? (long)Hq * Nq : (long)B * Hq * Nq;
   if (counters && (e = mala::launch_fill_zero(counters, 4 * sizeof(int64_t), s)) != hipSuccess)
     return hip_fail(e, "mala_bwd: clearing counters");
   float* dvec = (float*)workspace;
-  if ((e = mala::launch_bwd_preprocess(o, (const __bf16*)dout, dvec, rows, D, s)) != hipSuccess)
+  if ((e = mala::launch_bwd_preprocess(o, o_dtype == MALA_OUT_BF16, (const __bf16*)dout, dvec,
+                                       rows, D, s)) != hipSuccess)
     return hip_fail(e, "mala_bwd: preprocess launch");
   mala::BwdParams p;
   p.q = (const __bf16*)q;
@@ -134,6 +137,7 @@ int run_bwd(const void* q, const void* k, const void* v, const int32_t* cu, int 
   p.lse = lse;
   p.dvec = dvec;
   p.dq = dq; p.dk = dk; p.dv = dv;
+  p.grad_bf16 = grad_dtype == MALA_OUT_BF16;
   p.row_tiles = row_tiles;
   p.counters = (unsigned long long*)counters;
   p.cu = cu;
@@ -145,6 +149,12 @@ int run_bwd(const void* q, const void* k, const void* v, const int32_t* cu, int 
   p.nkblk = ((cu ? max_len : Nk) + mala::kBwdKeys - 1) / mala::kBwdKeys;
   p.nqblk = (p.max_len + mala::kDqRows - 1) / mala::kDqRows;
   if ((e = mala::launch_bwd(p, D, s)) != hipSuccess) return hip_fail(e, "mala_bwd: kernel launch");
+  return MALA_OK;
+}
+
+int check_dtype(int d, const char* what) {
+  if (d != MALA_OUT_F32 && d != MALA_OUT_BF16)
+    return fail(MALA_ERR_INVALID_ARG, "%s must be MALA_OUT_F32 or MALA_OUT_BF16, got %d", what, d);
   return MALA_OK;
 }
 
@@ -164,28 +174,30 @@ int check_varlen(const int32_t* cu, int num_seqs, int max_seqlen, int total, int
 
 extern "C" {
 
-int mala_fwd(const void* q, const void* k, const void* v, float* o, float* lse, int32_t* row_tiles,
+int mala_fwd(const void* q, const void* k, const void* v, void* o, float* lse, int32_t* row_tiles,
              int64_t* counters, int B, int Hq, int Hkv, int Nq, int Nk, int D, int causal,
-             float scale, float tau, void* stream) {
+             float scale, float tau, int out_dtype, void* stream) {
   g_err[0] = 0;
   if (!q || !k || !v || !o || !lse) return fail(MALA_ERR_INVALID_ARG, "null q, k, v, o or lse");
   int st = check_common(B, Hq, Hkv, Nq, Nk, D, causal, scale, tau);
   if (!st) st = check_slice_range(Nk, D);
+  if (!st) st = check_dtype(out_dtype, "out_dtype");
   if (st) return st;
-  return run_fwd(q, k, v, nullptr, 0, o, lse, row_tiles, counters, B, Hq, Hkv, Nq, Nk, D, scale,
-                 tau, (hipStream_t)stream);
+  return run_fwd(q, k, v, nullptr, 0, o, out_dtype, lse, row_tiles, counters, B, Hq, Hkv, Nq, Nk,
+                 D, scale, tau, (hipStream_t)stream);
 }
 
 int mala_fwd_varlen(const void* q, const void* k, const void* v, const int32_t* cu_seqlens,
-                    float* o, float* lse, int32_t* row_tiles, int64_t* counters, int num_seqs,
+                    void* o, float* lse, int32_t* row_tiles, int64_t* counters, int num_seqs,
                     int max_seqlen, int total, int Hq, int Hkv, int D, float scale, float tau,
-                    void* stream) {
+                    int out_dtype, void* stream) {
   g_err[0] = 0;
   if (!q || !k || !v || !o || !lse) return fail(MALA_ERR_INVALID_ARG, "null q, k, v, o or lse");
   int st = check_varlen(cu_seqlens, num_seqs, max_seqlen, total, Hq, Hkv, D, scale, tau);
+  if (!st) st = check_dtype(out_dtype, "out_dtype");
   if (st) return st;
-  return run_fwd(q, k, v, cu_seqlens, max_seqlen, o, lse, row_tiles, counters, num_seqs, Hq, Hkv,
-                 total, total, D, scale, tau, (hipStream_t)stream);
+  return run_fwd(q, k, v, cu_seqlens, max_seqlen, o, out_dtype, lse, row_tiles, counters,
+                 num_seqs, Hq, Hkv, total, total, D, scale, tau, (hipStream_t)stream);
 }
 
 size_t mala_bwd_workspace_size(int B, int Hq, int Hkv, int Nq, int Nk, int D) {
@@ -194,41 +206,48 @@ size_t mala_bwd_workspace_size(int B, int Hq, int Hkv, int Nq, int Nk, int D) {
   return round_up((size_t)B * Hq * Nq * sizeof(float), 256);
 }
 
-int mala_bwd(const void* q, const void* k, const void* v, const float* o, const float* lse,
-             const void* dout, float* dq, float* dk, float* dv, int32_t* row_tiles,
+int mala_bwd(const void* q, const void* k, const void* v, const void* o, const float* lse,
+             const void* dout, void* dq, void* dk, void* dv, int32_t* row_tiles,
              int64_t* counters, void* workspace, size_t workspace_bytes, int B, int Hq, int Hkv,
-             int Nq, int Nk, int D, int causal, float scale, float tau, void* stream) {
+             int Nq, int Nk, int D, int causal, float scale, float tau, int o_dtype,
+             int grad_dtype, void* stream) {
   g_err[0] = 0;
   if (!q || !k || !v || !o || !lse || !dout || !dq || !dk || !dv)
     return fail(MALA_ERR_INVALID_ARG, "null tensor argument");
   int st = check_common(B, Hq, Hkv, Nq, Nk, D, causal, scale, tau);
   if (!st) st = check_slice_range(Nk, D);
+  if (!st) st = check_dtype(o_dtype, "o_dtype");
+  if (!st) st = check_dtype(grad_dtype, "grad_dtype");
   if (st) return st;
   const size_t need = mala_bwd_workspace_size(B, Hq, Hkv, Nq, Nk, D);
   if (!workspace || workspace_bytes < need)
     return fail(MALA_ERR_WORKSPACE, "mala_bwd needs %zu workspace bytes, got %zu", need, workspace_bytes);
   if (((uintptr_t)workspace) % 16) return fail(MALA_ERR_WORKSPACE, "workspace not 16-byte aligned");
-  return run_bwd(q, k, v, nullptr, 0, o, lse, dout, dq, dk, dv, row_tiles, counters, workspace,
-                 B, Hq, Hkv, Nq, Nk, D, scale, tau, (hipStream_t)stream);
+  return run_bwd(q, k, v, nullptr, 0, o, o_dtype, lse, dout, dq, dk, dv, grad_dtype, row_tiles,
+                 counters, workspace, B, Hq, Hkv, Nq, Nk, D, scale, tau, (hipStream_t)stream);
 }
 
 int mala_bwd_varlen(const void* q, const void* k, const void* v, const int32_t* cu_seqlens,
-                    const float* o, const float* lse, const void* dout, float* dq, float* dk,
-                    float* dv, int32_t* row_tiles, int64_t* counters, void* workspace,
+                    const void* o, const float* lse, const void* dout, void* dq, void* dk,
+                    void* dv, int32_t* row_tiles, int64_t* counters, void* workspace,
                     size_t workspace_bytes, int num_seqs, int max_seqlen, int total, int Hq,
-                    int Hkv, int D, float scale, float tau, void* stream) {
+                    int Hkv, int D, float scale, float tau, int o_dtype, int grad_dtype,
+                    void* stream) {
   g_err[0] = 0;
   if (!q || !k || !v || !o || !lse || !dout || !dq || !dk || !dv)
     return fail(MALA_ERR_INVALID_ARG, "null tensor argument");
   int st = check_varlen(cu_seqlens, num_seqs, max_seqlen, total, Hq, Hkv, D, scale, tau);
+  if (!st) st = check_dtype(o_dtype, "o_dtype");
+  if (!st) st = check_dtype(grad_dtype, "grad_dtype");
   if (st) return st;
   const size_t need = mala_bwd_workspace_size(1, Hq, Hkv, total, total, D);
   if (!workspace || workspace_bytes < need)
     return fail(MALA_ERR_WORKSPACE, "mala_bwd_varlen needs %zu workspace bytes, got %zu", need,
                 workspace_bytes);
   if (((uintptr_t)workspace) % 16) return fail(MALA_ERR_WORKSPACE, "workspace not 16-byte aligned");
-  return run_bwd(q, k, v, cu_seqlens, max_seqlen, o, lse, dout, dq, dk, dv, row_tiles, counters,
-                 workspace, num_seqs, Hq, Hkv, total, total, D, scale, tau, (hipStream_t)stream);
+  return run_bwd(q, k, v, cu_seqlens, max_seqlen, o, o_dtype, lse, dout, dq, dk, dv, grad_dtype,
+                 row_tiles, counters, workspace, num_seqs, Hq, Hkv, total, total, D, scale, tau,
+                 (hipStream_t)stream);
 }
 
 size_t mala_decode_workspace_size(int B, int Hq, int D, int num_splits) {
@@ -237,13 +256,15 @@ size_t mala_decode_workspace_size(int B, int Hq, int D, int num_splits) {
 }
 
 int mala_decode(const void* q, const void* k_cache, const void* v_cache,
-                const int32_t* cache_lens, float* o, float* lse, int32_t* head_tiles,
+                const int32_t* cache_lens, void* o, float* lse, int32_t* head_tiles,
                 int64_t* counters, int num_splits, void* workspace, size_t workspace_bytes,
-                int B, int Hq, int Hkv, int Nk, int D, float scale, float tau, void* stream) {
+                int B, int Hq, int Hkv, int Nk, int D, float scale, float tau, int out_dtype,
+                void* stream) {
   g_err[0] = 0;
   if (!q || !k_cache || !v_cache || !o || !lse)
     return fail(MALA_ERR_INVALID_ARG, "null q, k_cache, v_cache, o or lse");
   int st = check_common(B, Hq, Hkv, 1, Nk, D, 1, scale, tau);
+  if (!st) st = check_dtype(out_dtype, "out_dtype");
   if (st) return st;
   if (num_splits < 1) return fail(MALA_ERR_INVALID_ARG, "num_splits must be >= 1");
   if (Hq / Hkv > 16)
@@ -273,8 +294,8 @@ int mala_decode(const void* q, const void* k_cache, const void* v_cache,
   p.thr2 = log2_tau(tau) - log2f((float)Nk);
   p.log2tau = log2_tau(tau);
   if ((e = mala::launch_decode(p, D, s)) != hipSuccess) return hip_fail(e, "mala_decode: split launch");
-  if ((e = mala::launch_decode_combine((float*)workspace, o, lse, head_tiles, p.counters, B * Hq,
-                                       num_splits, D, s)) != hipSuccess)
+  if ((e = mala::launch_decode_combine((float*)workspace, o, out_dtype == MALA_OUT_BF16, lse,
+                                       head_tiles, B * Hq, num_splits, D, s)) != hipSuccess)
     return hip_fail(e, "mala_decode: combine launch");
   return MALA_OK;
 }

@@ -54,34 +54,43 @@ hipError_t launch_fill_zero(void* ptr, size_t bytes, hipStream_t st) {
   return hipGetLastError();
 }
 
-// D_q = sum_d O[q][d] * dO[q][d]; 16 lanes per row.
-template <int D>
-__global__ __launch_bounds__(256) void mala_bwd_preprocess_kernel(const float* o, const bf16* dout,
+// D_q = sum_d O[q][d] * dO[q][d]; 16 lanes per row; O in fp32 or bf16 (OT).
+template <int D, typename OT>
+__global__ __launch_bounds__(256) void mala_bwd_preprocess_kernel(const OT* o, const bf16* dout,
                                                                   float* dvec, long rows) {
   constexpr int PER = D / 16;
   const long row = (long)blockIdx.x * 16 + (threadIdx.x >> 4);
   const int part = threadIdx.x & 15;
   float s = 0.f;
   if (row < rows) {
-    const float* op = o + row * D + part * PER;
+    const OT* op = o + row * D + part * PER;
     const bf16* dp = dout + row * D + part * PER;
 #pragma unroll
-    for (int e = 0; e < PER; ++e) s += op[e] * (float)dp[e];
+    for (int e = 0; e < PER; ++e) s += (float)op[e] * (float)dp[e];
   }
 #pragma unroll
   for (int w = 8; w >= 1; w >>= 1) s += __shfl_xor(s, w, 16);
   if (row < rows && part == 0) dvec[row] = s;
 }
 
-hipError_t launch_bwd_preprocess(const float* o, const bf16* dout, float* dvec, long rows, int D,
-                                 hipStream_t st) {
+template <typename OT>
+static void launch_preprocess_t(const OT* o, const bf16* dout, float* dvec, long rows, int D,
+                                hipStream_t st) {
   const unsigned grid = (unsigned)((rows + 15) / 16);
   if (D == 128)
-    hipLaunchKernelGGL(mala_bwd_preprocess_kernel<128>, dim3(grid), dim3(256), 0, st, o, dout,
-                       dvec, rows);
+    hipLaunchKernelGGL((mala_bwd_preprocess_kernel<128, OT>), dim3(grid), dim3(256), 0, st, o,
+                       dout, dvec, rows);
   else
-    hipLaunchKernelGGL(mala_bwd_preprocess_kernel<64>, dim3(grid), dim3(256), 0, st, o, dout,
-                       dvec, rows);
+    hipLaunchKernelGGL((mala_bwd_preprocess_kernel<64, OT>), dim3(grid), dim3(256), 0, st, o,
+                       dout, dvec, rows);
+}
+
+hipError_t launch_bwd_preprocess(const void* o, bool o_bf16, const bf16* dout, float* dvec,
+                                 long rows, int D, hipStream_t st) {
+  if (o_bf16)
+    launch_preprocess_t(static_cast<const bf16*>(o), dout, dvec, rows, D, st);
+  else
+    launch_preprocess_t(static_cast<const float*>(o), dout, dvec, rows, D, st);
   return hipGetLastError();
 }
 
@@ -473,14 +482,15 @@ __global__ __launch_bounds__(1024) void mala_bwd_dkdv_kernel(BwdParams p) {
     // holds key kw + c
     if (key < Nk) {
       const float f = role == 1 ? 1.f : p.scale;
-      float* dst = (role == 1 ? p.dv : p.dk) + (kbase + key) * D;
+      void* dst = role == 1 ? p.dv : p.dk;
+      const long krow = (kbase + key) * D;
 #pragma unroll
       for (int db = 0; db < DB; ++db)
 #pragma unroll
         for (int g = 0; g < 4; ++g) {
           f32x4 v4 = {acc[db][4 * g] * f, acc[db][4 * g + 1] * f, acc[db][4 * g + 2] * f,
                       acc[db][4 * g + 3] * f};
-          *reinterpret_cast<f32x4*>(dst + 32 * db + 8 * g + 4 * h) = v4;
+          store_out4(dst, krow + 32 * db + 8 * g + 4 * h, v4, p.grad_bf16);
         }
     }
   }
@@ -689,14 +699,14 @@ __global__ __launch_bounds__(kDqWaves * 64) void mala_bwd_dq_kernel(BwdParams p)
 
   // dQ = scale * sum dS K; lane (h, c) holds row qrow, columns 32 db + 8 g + 4 h + e
   if (row_valid) {
-    float* dst = p.dq + (qbase + qrow) * D;
+    const long qr = (qbase + qrow) * D;
 #pragma unroll
     for (int db = 0; db < DB; ++db)
 #pragma unroll
       for (int g = 0; g < 4; ++g) {
         const f32x4 v4 = {acc[db][4 * g] * p.scale, acc[db][4 * g + 1] * p.scale,
                           acc[db][4 * g + 2] * p.scale, acc[db][4 * g + 3] * p.scale};
-        *reinterpret_cast<f32x4*>(dst + 32 * db + 8 * g + 4 * h) = v4;
+        store_out4(p.dq, qr + 32 * db + 8 * g + 4 * h, v4, p.grad_bf16);
       }
     if (p.row_tiles && h == 0) p.row_tiles[qbase + qrow] = cnt_row;
   }

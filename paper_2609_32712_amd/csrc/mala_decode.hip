@@ -206,9 +206,9 @@ __global__ __launch_bounds__(64) void mala_decode_split_kernel(DecParams p) {
 // Normalizer-aware merge of the split partials: lse = logsumexp_s lse_s,
 // o = sum_s exp(lse_s - lse) o_s.  One workgroup per (batch, query head).
 template <int D>
-__global__ __launch_bounds__(64) void mala_decode_combine_kernel(const float* part, float* o,
-                                                                 float* lse, int32_t* head_tiles,
-                                                                 int S) {
+__global__ __launch_bounds__(64) void mala_decode_combine_kernel(const float* part, void* o,
+                                                                 bool o_bf16, float* lse,
+                                                                 int32_t* head_tiles, int S) {
   const long bh = blockIdx.x;
   const float* pp = part + bh * S * (D + kDecStride);
   float mx = kNegInf;
@@ -227,7 +227,10 @@ __global__ __launch_bounds__(64) void mala_decode_combine_kernel(const float* pa
       const float ls = pp[(long)s * (D + kDecStride) + D];
       if (ls != kNegInf) acc += expf(ls - L) * pp[(long)s * (D + kDecStride) + d];
     }
-    o[bh * D + d] = acc;
+    if (o_bf16)
+      static_cast<bf16*>(o)[bh * D + d] = (bf16)acc;   // nearest even
+    else
+      static_cast<float*>(o)[bh * D + d] = acc;
   }
   if (threadIdx.x == 0) {
     lse[bh] = L;
@@ -244,17 +247,15 @@ hipError_t launch_decode(const DecParams& p, int D, hipStream_t st) {
   return hipGetLastError();
 }
 
-hipError_t launch_decode_combine(const float* part, float* o, float* lse, int32_t* head_tiles,
-                                 unsigned long long* counters, int BH, int S, int D,
-                                 hipStream_t st) {
-  (void)counters;
+hipError_t launch_decode_combine(const float* part, void* o, bool o_bf16, float* lse,
+                                 int32_t* head_tiles, int BH, int S, int D, hipStream_t st) {
   dim3 grid((unsigned)BH), block(64);
   if (D == 128)
-    hipLaunchKernelGGL(mala_decode_combine_kernel<128>, grid, block, 0, st, part, o, lse,
-                       head_tiles, S);
+    hipLaunchKernelGGL(mala_decode_combine_kernel<128>, grid, block, 0, st, part, o, o_bf16,
+                       lse, head_tiles, S);
   else
-    hipLaunchKernelGGL(mala_decode_combine_kernel<64>, grid, block, 0, st, part, o, lse,
-                       head_tiles, S);
+    hipLaunchKernelGGL(mala_decode_combine_kernel<64>, grid, block, 0, st, part, o, o_bf16,
+                       lse, head_tiles, S);
   return hipGetLastError();
 }
 

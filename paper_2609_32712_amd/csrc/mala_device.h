@@ -209,6 +209,18 @@ __device__ __forceinline__ bf16x8 zero8() {
 __device__ __forceinline__ bf16x8 load8(const bf16* p) { return *reinterpret_cast<const bf16x8*>(p); }
 __device__ __forceinline__ void store8(bf16* p, bf16x8 v) { *reinterpret_cast<bf16x8*>(p) = v; }
 
+// Four consecutive output values at element index i of an fp32 array, or rounded
+// to bf16 (nearest even) into a bf16 array with the same layout.
+__device__ __forceinline__ void store_out4(void* base, long i, f32x4 v, bool to_bf16) {
+  if (to_bf16) {
+    const bf16x2 a = __builtin_convertvector((f32x2{v[0], v[1]}), bf16x2);
+    const bf16x2 b = __builtin_convertvector((f32x2{v[2], v[3]}), bf16x2);
+    *reinterpret_cast<bf16x4*>(static_cast<bf16*>(base) + i) = bf16x4{a[0], a[1], b[0], b[1]};
+  } else {
+    *reinterpret_cast<f32x4*>(static_cast<float*>(base) + i) = v;
+  }
+}
+
 // Two-term bf16 split of fp32 values: x ~= hi + lo with |x - hi - lo| <= 2^-16 |x|.
 // The post-score products (P V, P^T dO, dS^T Q, dS K) run as two MFMAs, one per
 // term, so the probabilities keep ~16 significant bits instead of bf16's 8.

@@ -221,14 +221,14 @@ __global__ __launch_bounds__(kFwdWaves * 64) void mala_fwd_kernel(FwdParams p) {
   // epilogue: O <- O / l, LSE = (m + log2 l) * ln 2
   if (row_valid) {
     const float inv = 1.f / l;
-    float* op = p.o + (qbase + qrow) * D;
+    const long orow = (qbase + qrow) * D;
 #pragma unroll
     for (int db = 0; db < DB; ++db)
 #pragma unroll
       for (int g = 0; g < 4; ++g) {
         f32x4 v4 = {acc[db][4 * g] * inv, acc[db][4 * g + 1] * inv, acc[db][4 * g + 2] * inv,
                     acc[db][4 * g + 3] * inv};
-        *reinterpret_cast<f32x4*>(op + 32 * db + 8 * g + 4 * h) = v4;
+        store_out4(p.o, orow + 32 * db + 8 * g + 4 * h, v4, p.o_bf16);
       }
     if (h == 0) {
       p.lse[qbase + qrow] = (m + fast_log2(l)) * kLn2;

@@ -53,10 +53,11 @@ struct FwdParams {
   const __bf16* q;
   const __bf16* k;
   const __bf16* v;
-  float* o;
+  void* o;             // fp32, or bf16 when o_bf16
   float* lse;
   int32_t* row_tiles;
   unsigned long long* counters;
+  int o_bf16;
   const int32_t* cu;   // packed batches: [B + 1] sequence starts, else null
   int max_len;         // packed batches: rows per sequence at most
   int B, Hq, Hkv, Nq, Nk;
@@ -72,9 +73,10 @@ struct BwdParams {
   const __bf16* dout;
   const float* lse;
   const float* dvec;   // D_q = rowsum(O_q * dO_q)
-  float* dq;
-  float* dk;
-  float* dv;
+  void* dq;            // fp32, or bf16 when grad_bf16 (dk, dv alike)
+  void* dk;
+  void* dv;
+  int grad_bf16;
   int32_t* row_tiles;
   unsigned long long* counters;
   const int32_t* cu;   // packed batches: [B + 1] sequence starts, else null
@@ -99,12 +101,11 @@ struct DecParams {
 
 hipError_t launch_fill_zero(void* ptr, size_t bytes, hipStream_t st);
 hipError_t launch_fwd(const FwdParams& p, int D, hipStream_t st);
-hipError_t launch_bwd_preprocess(const float* o, const __bf16* dout, float* dvec, long rows, int D,
-                                 hipStream_t st);
+hipError_t launch_bwd_preprocess(const void* o, bool o_bf16, const __bf16* dout, float* dvec,
+                                 long rows, int D, hipStream_t st);
 hipError_t launch_bwd(const BwdParams& p, int D, hipStream_t st);
 hipError_t launch_decode(const DecParams& p, int D, hipStream_t st);
-hipError_t launch_decode_combine(const float* part, float* o, float* lse, int32_t* head_tiles,
-                                 unsigned long long* counters, int BH, int S, int D,
-                                 hipStream_t st);
+hipError_t launch_decode_combine(const float* part, void* o, bool o_bf16, float* lse,
+                                 int32_t* head_tiles, int BH, int S, int D, hipStream_t st);
 
 }  // namespace mala

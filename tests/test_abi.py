@@ -59,12 +59,12 @@ def test_workspace_sizes(lib):
 
 def _fwd(lib, **kw):
     a = dict(q=16, k=16, v=16, o=16, lse=16, B=1, Hq=2, Hkv=1, Nq=64, Nk=64, D=128, causal=1,
-             scale=0.1, tau=1e-3)
+             scale=0.1, tau=1e-3, out=mala.OUT_F32)
     a.update(kw)
     P = lambda x: None if x is None else ctypes.c_void_p(x)
     return lib.mala_fwd(P(a["q"]), P(a["k"]), P(a["v"]), P(a["o"]), P(a["lse"]), None, None,
                         a["B"], a["Hq"], a["Hkv"], a["Nq"], a["Nk"], a["D"], a["causal"],
-                        a["scale"], a["tau"], None)
+                        a["scale"], a["tau"], a["out"], None)
 
 
 @pytest.mark.parametrize("kw,status", [
@@ -81,6 +81,8 @@ def _fwd(lib, **kw):
     (dict(D=96), mala.MALA_ERR_UNSUPPORTED),
     (dict(causal=0), mala.MALA_ERR_UNSUPPORTED),
     (dict(Nq=64, Nk=1 << 24), mala.MALA_ERR_UNSUPPORTED),   # Nk x D x 2 bytes reach 2^32
+    (dict(out=2), mala.MALA_ERR_INVALID_ARG),                # no such output type
+    (dict(out=-1), mala.MALA_ERR_INVALID_ARG),
 ])
 def test_fwd_rejects_invalid_arguments(lib, kw, status):
     assert _fwd(lib, **kw) == status
@@ -90,19 +92,28 @@ def test_fwd_rejects_invalid_arguments(lib, kw, status):
 
 def test_bwd_and_decode_reject_missing_workspace(lib):
     P = ctypes.c_void_p
-    st = lib.mala_bwd(*([P(16)] * 9), None, None, None, 0, 1, 2, 1, 64, 64, 128, 1, 0.1, 0.0, None)
+    f32, b16 = mala.OUT_F32, mala.OUT_BF16
+    st = lib.mala_bwd(*([P(16)] * 9), None, None, None, 0, 1, 2, 1, 64, 64, 128, 1, 0.1, 0.0,
+                      f32, f32, None)
     assert st == mala.MALA_ERR_WORKSPACE
-    st = lib.mala_bwd(*([P(16)] * 9), None, None, P(16), 8, 1, 2, 1, 64, 64, 128, 1, 0.1, 0.0, None)
+    st = lib.mala_bwd(*([P(16)] * 9), None, None, P(16), 8, 1, 2, 1, 64, 64, 128, 1, 0.1, 0.0,
+                      b16, b16, None)
     assert st == mala.MALA_ERR_WORKSPACE
+    st = lib.mala_bwd(*([P(16)] * 9), None, None, P(16), 1 << 20, 1, 2, 1, 64, 64, 128, 1, 0.1,
+                      0.0, f32, 3, None)
+    assert st == mala.MALA_ERR_INVALID_ARG
     qkv, ol = [P(16)] * 3, [P(16)] * 2     # q, k_cache, v_cache / o, lse (cache_lens NULL)
     st = lib.mala_decode(*qkv, None, *ol, None, None, 4, None, 0, 1, 2, 1, 64, 128, 0.1, 0.0,
-                         None)
+                         f32, None)
     assert st == mala.MALA_ERR_WORKSPACE
     st = lib.mala_decode(*qkv, None, *ol, None, None, 0, P(16), 1 << 20, 1, 2, 1, 64, 128, 0.1,
-                         0.0, None)
+                         0.0, f32, None)
+    assert st == mala.MALA_ERR_INVALID_ARG
+    st = lib.mala_decode(*qkv, None, *ol, None, None, 4, P(16), 1 << 20, 1, 2, 1, 64, 128, 0.1,
+                         0.0, 7, None)
     assert st == mala.MALA_ERR_INVALID_ARG
     st = lib.mala_decode(*qkv, None, *ol, None, None, 2, P(16), 1 << 20, 1, 32, 1, 64, 128, 0.1,
-                         0.0, None)
+                         0.0, f32, None)
     assert st == mala.MALA_ERR_UNSUPPORTED
 
 
@@ -112,7 +123,7 @@ def test_varlen_argument_validation(lib):
 
     def fwd(cu, num_seqs, max_len, total, Hq=2, Hkv=1, D=64, tau=0.0):
         return lib.mala_fwd_varlen(*qkv, cu, P(16), P(16), None, None, num_seqs, max_len, total,
-                                   Hq, Hkv, D, 0.125, tau, None)
+                                   Hq, Hkv, D, 0.125, tau, mala.OUT_BF16, None)
 
     assert fwd(None, 2, 8, 16) == mala.MALA_ERR_INVALID_ARG          # no cu_seqlens
     assert fwd(P(16), 0, 8, 16) == mala.MALA_ERR_INVALID_ARG         # no sequence
@@ -122,7 +133,7 @@ def test_varlen_argument_validation(lib):
     assert fwd(P(16), 2, 8, 1 << 24, D=128) == mala.MALA_ERR_UNSUPPORTED   # slice range
     assert fwd(P(16), 2, 8, 16, tau=-1.0) == mala.MALA_ERR_INVALID_ARG
     st = lib.mala_bwd_varlen(*qkv, P(16), *([P(16)] * 6), None, None, P(16), 8, 2, 8, 16, 2, 1,
-                             64, 0.125, 0.0, None)
+                             64, 0.125, 0.0, mala.OUT_F32, mala.OUT_F32, None)
     assert st == mala.MALA_ERR_WORKSPACE
     assert lib.mala_bwd_workspace_size(1, 2, 1, 16, 16, 64) > 8
 

@@ -11,7 +11,8 @@ import torch
 
 import oracle
 import paper_2609_32712_amd as mala
-from parity_util import (LSE_DIAG, assert_close, assert_counts, dev, exempt_rows, host)
+from parity_util import (LSE_DIAG, TOL_MAX, assert_close, assert_counts, dev, exempt_rows,
+                         host)
 from workloads import CONFIGS, Workload, bf16_to_f64
 
 pytestmark = pytest.mark.gpu
@@ -590,3 +591,48 @@ def test_graph_capture_replays_match_eager():
         torch.cuda.synchronize()
         for a, b in zip(outs, ref):
             assert torch.equal(a, b), i
+
+
+@pytest.mark.parametrize("tau", [0.0, 1e-3])
+def test_bf16_outputs(tau):
+    # O and the gradients stored as bf16 are the fp32 results rounded once at the
+    # store (bit for bit); with a bf16 O in D_q = rowsum(O * dO), the gradients meet
+    # the bar against the oracle's backward from that same O, and the bf16-stored
+    # ones within the bar plus one bf16 rounding
+    w, q, k, v, do = _train_case("gqa_d128_ragged", tau)
+    Q, K, V, DO = map(dev, (q, k, v, do))
+    scale = f32(w.scale)
+    bq, bk = mala.mala_geometry(w.D, mala.PASS_FWD)
+    of32 = mala.fwd(Q, K, V, scale, tau)
+    ob16 = mala.fwd(Q, K, V, scale, tau, out_dtype=torch.bfloat16)
+    gf = mala.bwd(Q, K, V, ob16["o"], ob16["lse"], DO, scale, tau)
+    gb = mala.bwd(Q, K, V, ob16["o"], ob16["lse"], DO, scale, tau, grad_dtype=torch.bfloat16)
+    torch.cuda.synchronize()
+    assert torch.equal(ob16["o"], of32["o"].to(torch.bfloat16))
+    assert torch.equal(ob16["lse"], of32["lse"])
+    assert torch.equal(ob16["row_tiles"], of32["row_tiles"])
+    for x in ("dq", "dk", "dv"):
+        assert torch.equal(gb[x], gf[x].to(torch.bfloat16)), x
+    assert torch.equal(gb["row_tiles"], gf["row_tiles"])
+    qf, kf, vf, dof = map(bf16_to_f64, (q, k, v, do))
+    ofr = oracle.mala_fwd(qf, kf, vf, scale, f32(tau), bq, bk)
+    o16 = host(ob16["o"].float())
+    obr = oracle.mala_bwd(qf, kf, vf, o16, ofr["lse"], dof, scale, f32(tau), bq, bk)
+    rounded = {"O": (o16, ofr["o"])}
+    for x, name in (("dq", "dQ"), ("dk", "dK"), ("dv", "dV")):
+        assert_close(name + " (bf16 O)", host(gf[x]), obr[x])
+        rounded[name] = (host(gb[x].float()), obr[x])
+    for name, (got, ref) in rounded.items():
+        err = np.abs(got - ref) - 2.0 ** -8 * np.abs(ref)
+        assert err.max() <= TOL_MAX, (name, float(err.max()))
+
+
+def test_decode_bf16_output():
+    spec = dict(kind="decode", B=2, Hq=8, Hkv=2, N=3001, D=128, beta=3.0, needles=4)
+    w = Workload(spec)
+    t = w.tensors()
+    q, k, v = dev(t["q"]), dev(t["k"]), dev(t["v"])
+    a = mala.decode(q, k, v, f32(w.scale), 1e-4, 4)
+    b = mala.decode(q, k, v, f32(w.scale), 1e-4, 4, out_dtype=torch.bfloat16)
+    torch.cuda.synchronize()
+    assert torch.equal(b["o"], a["o"].to(torch.bfloat16)) and torch.equal(b["lse"], a["lse"])
