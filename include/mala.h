@@ -71,7 +71,8 @@ enum {
   MALA_CNT_RETAINED = 1, /* of those, tiles whose post-score path ran */
   MALA_CNT_V_TILES = 2,  /* forward: V tiles of B_k keys staged by the kernel;
                             backward: dO tiles of B_q rows staged;
-                            decode: V tiles of B_k keys read (once per GQA group) */
+                            decode: V tiles of B_k keys read (once per up to 16
+                            query heads of a GQA group) */
   MALA_CNT_SLOTS = 3     /* post-score key slots summed over query rows: a retained
                             B_q x B_k tile adds B_k slots to each of its valid rows
                             (Attention Cost section; mean slots per query =

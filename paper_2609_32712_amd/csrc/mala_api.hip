@@ -267,8 +267,6 @@ int mala_decode(const void* q, const void* k_cache, const void* v_cache,
   if (!st) st = check_dtype(out_dtype, "out_dtype");
   if (st) return st;
   if (num_splits < 1) return fail(MALA_ERR_INVALID_ARG, "num_splits must be >= 1");
-  if (Hq / Hkv > 16)
-    return fail(MALA_ERR_UNSUPPORTED, "decode supports at most 16 query heads per KV head");
   const size_t need = mala_decode_workspace_size(B, Hq, D, num_splits);
   if (!workspace || workspace_bytes < need)
     return fail(MALA_ERR_WORKSPACE, "mala_decode needs %zu workspace bytes, got %zu", need,
@@ -288,6 +286,7 @@ int mala_decode(const void* q, const void* k_cache, const void* v_cache,
   p.counters = (unsigned long long*)counters;
   p.B = B; p.Hq = Hq; p.Hkv = Hkv; p.Nk = Nk;
   p.S = num_splits;
+  p.nchunk = (Hq / Hkv + 15) / 16;
   p.T = T;
   p.tps = (T + num_splits - 1) / num_splits;
   p.scale2 = scale * mala::kLog2e;

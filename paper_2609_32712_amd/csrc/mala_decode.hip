@@ -2,8 +2,9 @@
 // each split tests its tiles against its own partial normalizer, with L = Nk).
 //
 // One wavefront (= one workgroup) owns one split of one (batch, KV head) and
-// serves all query heads of the GQA group at once, so the K and V bytes of a
-// tile are read once per group.  Decode is HBM-bound: K is always read (score
+// serves up to 16 query heads of the GQA group at once (larger groups take
+// ceil(group / 16) wavefronts), so the K and V bytes of a tile are read once per
+// 16 heads.  Decode is HBM-bound: K is always read (score
 // discovery), V only when at least one head of the group retains the tile.
 //
 // With per-sequence cache lengths n_b, sequence b sees keys [0, n_b) (L = n_b) and
@@ -35,8 +36,10 @@ __global__ __launch_bounds__(64) void mala_decode_split_kernel(DecParams p) {
 
   const int lane = threadIdx.x, g = lane >> 4, col = lane & 15;
   const int s = blockIdx.x % p.S;
-  const int bhk = blockIdx.x / p.S;
+  const int chunk = (blockIdx.x / p.S) % p.nchunk;     // heads 16 chunk .. 16 chunk + 15
+  const int bhk = blockIdx.x / p.S / p.nchunk;
   const int b = bhk / p.Hkv, hkv = bhk % p.Hkv, grp = p.Hq / p.Hkv;
+  const int nh = min(16, grp - 16 * chunk);             // query heads of this wavefront
   // this sequence's cache length n (clamped into [0, Nk]), its tiles and split range
   int n = p.Nk, T = p.T, tps = p.tps;
   float thr2 = p.thr2;
@@ -47,8 +50,8 @@ __global__ __launch_bounds__(64) void mala_decode_split_kernel(DecParams p) {
     thr2 = p.log2tau - log2f((float)n);   // L = n (n = 0 leaves no tile to test)
   }
   const int t_lo = s * tps, t_hi = min(T, t_lo + tps);
-  const bool head_valid = col < grp;
-  const int hq = hkv * grp + col;
+  const bool head_valid = col < nh;
+  const int hq = hkv * grp + 16 * chunk + col;
 
   bf16x8 qreg[KS];
 #pragma unroll
@@ -197,7 +200,7 @@ __global__ __launch_bounds__(64) void mala_decode_split_kernel(DecParams p) {
       atomicAdd(&p.counters[3], (unsigned long long)cnt * kDecBk);
     }
     if (lane == 0) {
-      atomicAdd(&p.counters[0], (unsigned long long)(t_hi > t_lo ? t_hi - t_lo : 0) * grp);
+      atomicAdd(&p.counters[0], (unsigned long long)(t_hi > t_lo ? t_hi - t_lo : 0) * nh);
       if (vloads) atomicAdd(&p.counters[2], (unsigned long long)vloads);
     }
   }
@@ -239,7 +242,7 @@ __global__ __launch_bounds__(64) void mala_decode_combine_kernel(const float* pa
 }
 
 hipError_t launch_decode(const DecParams& p, int D, hipStream_t st) {
-  dim3 grid((unsigned)p.B * p.Hkv * p.S), block(64);
+  dim3 grid((unsigned)p.B * p.Hkv * p.nchunk * p.S), block(64);
   if (D == 128)
     hipLaunchKernelGGL(mala_decode_split_kernel<128>, grid, block, 0, st, p);
   else

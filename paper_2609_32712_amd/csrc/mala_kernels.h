@@ -95,6 +95,7 @@ struct DecParams {
   unsigned long long* counters;
   const int32_t* lens; // [B] valid cache tokens per sequence, or null (all Nk)
   int B, Hq, Hkv, Nk, S, T, tps;   // T, tps: tiles and tiles per split at length Nk
+  int nchunk;          // ceil((Hq / Hkv) / 16): workgroups per (sequence, KV head, split)
   float scale2, thr2;  // thr2 = log2(tau) - log2(Nk)
   float log2tau;       // for the per-sequence thresholds log2(tau) - log2(n_b)
 };

@@ -112,9 +112,9 @@ def test_bwd_and_decode_reject_missing_workspace(lib):
     st = lib.mala_decode(*qkv, None, *ol, None, None, 4, P(16), 1 << 20, 1, 2, 1, 64, 128, 0.1,
                          0.0, 7, None)
     assert st == mala.MALA_ERR_INVALID_ARG
-    st = lib.mala_decode(*qkv, None, *ol, None, None, 2, P(16), 1 << 20, 1, 32, 1, 64, 128, 0.1,
+    st = lib.mala_decode(*qkv, None, *ol, None, None, 2, P(16), 1 << 20, 1, 32, 1, 64, 96, 0.1,
                          0.0, f32, None)
-    assert st == mala.MALA_ERR_UNSUPPORTED
+    assert st == mala.MALA_ERR_UNSUPPORTED       # head_dim 96
 
 
 def test_varlen_argument_validation(lib):

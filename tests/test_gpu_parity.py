@@ -287,6 +287,9 @@ DECODE_CASES = [
     (dict(kind="decode", B=1, Hq=2, Hkv=2, N=999, D=64, beta=3.0, needles=4), 3, 0.1),
     (dict(kind="decode", B=3, Hq=16, Hkv=1, N=64, D=128, beta=2.0, needles=2), 2, 1e-3),
     (dict(kind="decode", B=1, Hq=4, Hkv=4, N=5, D=64, beta=2.0, needles=1), 1, 1.0),
+    # groups of more than 16 query heads (two wavefronts per KV head and split)
+    (dict(kind="decode", B=2, Hq=40, Hkv=2, N=1500, D=128, beta=3.0, needles=4), 3, 1e-3),
+    (dict(kind="decode", B=1, Hq=32, Hkv=1, N=777, D=64, beta=3.0, needles=4), 2, 0.1),
 ]
 
 
