@@ -147,36 +147,44 @@ int mala_bwd(const void* q, const void* k, const void* v, const void* o, const f
 
 /*
  * Packed variable-length batches (the forward of Algorithm 1 per sequence).
- * num_seqs sequences lie back to back along the token axis: sequence b holds rows
- * [cu_seqlens[b], cu_seqlens[b + 1]) of every head, attends causally within itself
- * only (its i-th row sees its rows 0..i, L_q = i + 1) and is tiled from its own
- * first row, exactly as a batch of one with Nq = Nk = its length.
- *   q: bf16 [Hq, total, D]; k, v: bf16 [Hkv, total, D] (head-major: the fixed-length
- *   layout with B = 1 and N = total); o: [Hq, total, D] out (out_dtype); lse: fp32
- *   [Hq, total] out; row_tiles: int32 [Hq, total] or NULL out; counters as mala_fwd.
- *   cu_seqlens: int32 [num_seqs + 1] device array, non-decreasing from 0 to at
- *   most total; max_seqlen: the longest sequence (the launch is sized by it).
- *   On the device the starts are clamped into [0, total] and a sequence longer
- *   than max_seqlen is cut to its first max_seqlen rows; rows that no (cut)
- *   sequence covers are not written.  Requires max_seqlen <= total, D in {64, 128}
- *   and total * D * 2 < 2^32.
+ * num_seqs sequences lie back to back along the token axes: sequence b holds query
+ * rows [cu_seqlens_q[b], cu_seqlens_q[b + 1]) and key / value rows
+ * [cu_seqlens_k[b], cu_seqlens_k[b + 1]) of every head, attends only to its own
+ * keys, causally with bottom-right alignment (with n_q query rows and n_k >= n_q
+ * keys, its i-th query row sees its keys 0 .. i + n_k - n_q, L_q = i + 1 + n_k - n_q:
+ * n_q = n_k is self-attention, n_q < n_k is prefill against a cache), and is tiled
+ * from its own first rows, exactly as a batch of one with Nq = n_q, Nk = n_k.
+ *   q: bf16 [Hq, total_q, D]; k, v: bf16 [Hkv, total_k, D] (head-major: the
+ *   fixed-length layout with B = 1); o: [Hq, total_q, D] out (out_dtype); lse: fp32
+ *   [Hq, total_q] out; row_tiles: int32 [Hq, total_q] or NULL out; counters as mala_fwd.
+ *   cu_seqlens_q, cu_seqlens_k: int32 [num_seqs + 1] device arrays, non-decreasing
+ *   from 0 to at most total_q / total_k; cu_seqlens_k may be NULL (the same rows as
+ *   the queries; then total_k = total_q and max_seqlen_k = max_seqlen_q).
+ *   max_seqlen_q / _k: the longest query / key run (the launch is sized by them).
+ *   On the device the starts are clamped into the totals and a run longer than its
+ *   max_seqlen is cut to its first max_seqlen rows; a sequence with more query rows
+ *   than keys is skipped.  Rows that no (cut, not skipped) sequence covers are not
+ *   written.  Requires max_seqlen_q <= total_q, max_seqlen_k <= total_k,
+ *   total_q <= total_k, D in {64, 128} and total_k * D * 2 < 2^32.
  */
-int mala_fwd_varlen(const void* q, const void* k, const void* v, const int32_t* cu_seqlens,
-                    void* o, float* lse, int32_t* row_tiles, int64_t* counters, int num_seqs,
-                    int max_seqlen, int total, int Hq, int Hkv, int D, float scale, float tau,
+int mala_fwd_varlen(const void* q, const void* k, const void* v, const int32_t* cu_seqlens_q,
+                    const int32_t* cu_seqlens_k, void* o, float* lse, int32_t* row_tiles,
+                    int64_t* counters, int num_seqs, int max_seqlen_q, int max_seqlen_k,
+                    int total_q, int total_k, int Hq, int Hkv, int D, float scale, float tau,
                     int out_dtype, void* stream);
 
 /*
  * Packed variable-length batches: mala_bwd (Algorithm 2) per sequence, on the
  * layout of mala_fwd_varlen (o, lse as it returned them, o of type o_dtype; dout,
- * dq: [Hq, total, D]; dk, dv: [Hkv, total, D]; gradients of type grad_dtype).  workspace: at least
- * mala_bwd_workspace_size(1, Hq, Hkv, total, total, D) bytes.  Rows that no
- * sequence covers are not written.
+ * dq: [Hq, total_q, D]; dk, dv: [Hkv, total_k, D]; gradients of type grad_dtype).
+ * workspace: at least mala_bwd_workspace_size(1, Hq, Hkv, total_q, total_k, D)
+ * bytes.  Rows that no sequence covers are not written.
  */
-int mala_bwd_varlen(const void* q, const void* k, const void* v, const int32_t* cu_seqlens,
-                    const void* o, const float* lse, const void* dout, void* dq, void* dk,
-                    void* dv, int32_t* row_tiles, int64_t* counters, void* workspace,
-                    size_t workspace_bytes, int num_seqs, int max_seqlen, int total, int Hq,
+int mala_bwd_varlen(const void* q, const void* k, const void* v, const int32_t* cu_seqlens_q,
+                    const int32_t* cu_seqlens_k, const void* o, const float* lse,
+                    const void* dout, void* dq, void* dk, void* dv, int32_t* row_tiles,
+                    int64_t* counters, void* workspace, size_t workspace_bytes, int num_seqs,
+                    int max_seqlen_q, int max_seqlen_k, int total_q, int total_k, int Hq,
                     int Hkv, int D, float scale, float tau, int o_dtype, int grad_dtype,
                     void* stream);
 

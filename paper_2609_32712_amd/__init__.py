@@ -66,9 +66,9 @@ def load_library():
     lib.mala_bwd_workspace_size.restype = sz
     lib.mala_bwd.argtypes = [vp] * 12 + [sz] + [i] * 7 + [f, f, i, i, vp]
     lib.mala_bwd.restype = i
-    lib.mala_fwd_varlen.argtypes = [vp] * 8 + [i] * 6 + [f, f, i, vp]
+    lib.mala_fwd_varlen.argtypes = [vp] * 9 + [i] * 8 + [f, f, i, vp]
     lib.mala_fwd_varlen.restype = i
-    lib.mala_bwd_varlen.argtypes = [vp] * 13 + [sz] + [i] * 6 + [f, f, i, i, vp]
+    lib.mala_bwd_varlen.argtypes = [vp] * 14 + [sz] + [i] * 8 + [f, f, i, i, vp]
     lib.mala_bwd_varlen.restype = i
     lib.mala_decode_workspace_size.argtypes = [i] * 4
     lib.mala_decode_workspace_size.restype = sz
@@ -183,53 +183,66 @@ def mala_decode(q, k_cache, v_cache, o, lse, head_tiles, counters, num_splits, w
                                       Nk, D, scale, tau, _out_code(o), _stream(stream)))
 
 
-def _varlen_dims(q, k, cu_seqlens):
-    """(num_seqs, Hq, Hkv, total, D) of a packed batch: q [Hq, total, D], k [Hkv, total, D],
-    cu_seqlens int32 [num_seqs + 1] on the device."""
+def _varlen_dims(q, k, cu_seqlens, max_seqlen, cu_seqlens_k, max_seqlen_k):
+    """Sizes of a packed batch: q [Hq, total_q, D], k [Hkv, total_k, D], the int32
+    [num_seqs + 1] device arrays of query and (optionally) key starts, and the
+    longest runs.  Returns (num_seqs, Hq, Hkv, total_q, total_k, D, max_q, max_k)."""
     _dev(cu_seqlens, torch.int32, "cu_seqlens", 1)
-    Hq, total, D = q.shape
-    if k.shape[1] != total or cu_seqlens.shape[0] < 2:
+    Hq, total_q, D = q.shape
+    Hkv, total_k = k.shape[0], k.shape[1]
+    if cu_seqlens.shape[0] < 2 or k.shape[2] != D:
         raise ValueError("inconsistent shapes")
-    return cu_seqlens.shape[0] - 1, Hq, k.shape[0], total, D
+    if cu_seqlens_k is None:
+        max_seqlen_k = max_seqlen
+    else:
+        _dev(cu_seqlens_k, torch.int32, "cu_seqlens_k", 1)
+        if cu_seqlens_k.shape[0] != cu_seqlens.shape[0] or max_seqlen_k is None:
+            raise ValueError("cu_seqlens_k needs one start per sequence and max_seqlen_k")
+    return (cu_seqlens.shape[0] - 1, Hq, Hkv, total_q, total_k, D, int(max_seqlen),
+            int(max_seqlen_k))
 
 
 def mala_fwd_varlen(q, k, v, cu_seqlens, max_seqlen, o, lse, row_tiles, counters, scale, tau,
-                    stream=None):
+                    stream=None, cu_seqlens_k=None, max_seqlen_k=None):
     for t, n in ((q, "q"), (k, "k"), (v, "v")):
         _dev(t, torch.bfloat16, n, 3)
     _dev(o, _OUT, "o", 3), _dev(lse, torch.float32, "lse", 2)
-    S, Hq, Hkv, total, D = _varlen_dims(q, k, cu_seqlens)
+    S, Hq, Hkv, tq, tk, D, mq, mk = _varlen_dims(q, k, cu_seqlens, max_seqlen, cu_seqlens_k,
+                                                 max_seqlen_k)
     if tuple(v.shape) != tuple(k.shape) or tuple(o.shape) != tuple(q.shape) or \
-            tuple(lse.shape) != (Hq, total):
+            tuple(lse.shape) != (Hq, tq):
         raise ValueError("inconsistent shapes")
     if row_tiles is not None:
         _dev(row_tiles, torch.int32, "row_tiles", 2)
     if counters is not None:
         _dev(counters, torch.int64, "counters", 1)
-    _check(load_library().mala_fwd_varlen(_ptr(q), _ptr(k), _ptr(v), _ptr(cu_seqlens), _ptr(o),
-                                          _ptr(lse), _ptr(row_tiles), _ptr(counters), S,
-                                          int(max_seqlen), total, Hq, Hkv, D, scale, tau,
-                                          _out_code(o), _stream(stream)))
+    _check(load_library().mala_fwd_varlen(_ptr(q), _ptr(k), _ptr(v), _ptr(cu_seqlens),
+                                          _ptr(cu_seqlens_k), _ptr(o), _ptr(lse),
+                                          _ptr(row_tiles), _ptr(counters), S, mq, mk, tq, tk,
+                                          Hq, Hkv, D, scale, tau, _out_code(o), _stream(stream)))
 
 
 def mala_bwd_varlen(q, k, v, cu_seqlens, max_seqlen, o, lse, dout, dq, dk, dv, row_tiles,
-                    counters, workspace, scale, tau, stream=None):
+                    counters, workspace, scale, tau, stream=None, cu_seqlens_k=None,
+                    max_seqlen_k=None):
     for t, n, dt, nd in ((q, "q", torch.bfloat16, 3), (k, "k", torch.bfloat16, 3),
                          (v, "v", torch.bfloat16, 3), (o, "o", _OUT, 3),
                          (lse, "lse", torch.float32, 2), (dout, "dout", torch.bfloat16, 3),
                          (dq, "dq", _OUT, 3), (dk, "dk", _OUT, 3), (dv, "dv", _OUT, 3)):
         _dev(t, dt, n, nd)
-    S, Hq, Hkv, total, D = _varlen_dims(q, k, cu_seqlens)
+    S, Hq, Hkv, tq, tk, D, mq, mk = _varlen_dims(q, k, cu_seqlens, max_seqlen, cu_seqlens_k,
+                                                 max_seqlen_k)
     if (tuple(dq.shape) != tuple(q.shape) or tuple(dout.shape) != tuple(q.shape)
             or tuple(o.shape) != tuple(q.shape) or tuple(dk.shape) != tuple(k.shape)
             or tuple(dv.shape) != tuple(k.shape)):
         raise ValueError("inconsistent shapes")
-    _check(load_library().mala_bwd_varlen(_ptr(q), _ptr(k), _ptr(v), _ptr(cu_seqlens), _ptr(o),
-                                          _ptr(lse), _ptr(dout), _ptr(dq), _ptr(dk), _ptr(dv),
-                                          _ptr(row_tiles), _ptr(counters), _ptr(workspace),
-                                          workspace.numel() * workspace.element_size(), S,
-                                          int(max_seqlen), total, Hq, Hkv, D, scale, tau,
-                                          _out_code(o), _out_code(dq, dk, dv), _stream(stream)))
+    _check(load_library().mala_bwd_varlen(_ptr(q), _ptr(k), _ptr(v), _ptr(cu_seqlens),
+                                          _ptr(cu_seqlens_k), _ptr(o), _ptr(lse), _ptr(dout),
+                                          _ptr(dq), _ptr(dk), _ptr(dv), _ptr(row_tiles),
+                                          _ptr(counters), _ptr(workspace),
+                                          workspace.numel() * workspace.element_size(), S, mq,
+                                          mk, tq, tk, Hq, Hkv, D, scale, tau, _out_code(o),
+                                          _out_code(dq, dk, dv), _stream(stream)))
 
 
 # ---------------------------------------------------------------- allocating wrappers
@@ -279,32 +292,36 @@ def decode(q, k_cache, v_cache, scale, tau, num_splits, stats=True, workspace=No
 
 
 def fwd_varlen(q, k, v, cu_seqlens, max_seqlen, scale, tau, stats=True, stream=None,
-               out_dtype=torch.float32):
-    """Packed batch: q [Hq, total, D], k, v [Hkv, total, D], cu_seqlens int32 [S + 1].
-    Rows that no sequence covers come back as zeros."""
+               out_dtype=torch.float32, cu_seqlens_k=None, max_seqlen_k=None):
+    """Packed batch: q [Hq, total_q, D], k, v [Hkv, total_k, D], cu_seqlens (and, for
+    prefill against cached keys, cu_seqlens_k) int32 [S + 1].  Rows that no sequence
+    covers come back as zeros."""
     Hq, total, D = q.shape
     o = torch.zeros((Hq, total, D), dtype=out_dtype, device=q.device)
     lse = torch.zeros((Hq, total), dtype=torch.float32, device=q.device)
     rt = torch.zeros((Hq, total), dtype=torch.int32, device=q.device) if stats else None
     cnt = torch.empty(4, dtype=torch.int64, device=q.device) if stats else None
-    mala_fwd_varlen(q, k, v, cu_seqlens, max_seqlen, o, lse, rt, cnt, scale, tau, stream=stream)
+    mala_fwd_varlen(q, k, v, cu_seqlens, max_seqlen, o, lse, rt, cnt, scale, tau, stream=stream,
+                    cu_seqlens_k=cu_seqlens_k, max_seqlen_k=max_seqlen_k)
     return dict(o=o, lse=lse, row_tiles=rt, counters=cnt)
 
 
 def bwd_varlen(q, k, v, cu_seqlens, max_seqlen, o, lse, dout, scale, tau, stats=True,
-               workspace=None, stream=None, grad_dtype=torch.float32):
+               workspace=None, stream=None, grad_dtype=torch.float32, cu_seqlens_k=None,
+               max_seqlen_k=None):
     Hq, total, D = q.shape
-    Hkv = k.shape[0]
+    Hkv, total_k = k.shape[0], k.shape[1]
     dq = torch.zeros((Hq, total, D), dtype=grad_dtype, device=q.device)
-    dk = torch.zeros((Hkv, total, D), dtype=grad_dtype, device=q.device)
-    dv = torch.zeros((Hkv, total, D), dtype=grad_dtype, device=q.device)
+    dk = torch.zeros((Hkv, total_k, D), dtype=grad_dtype, device=q.device)
+    dv = torch.zeros((Hkv, total_k, D), dtype=grad_dtype, device=q.device)
     rt = torch.zeros((Hq, total), dtype=torch.int32, device=q.device) if stats else None
     cnt = torch.empty(4, dtype=torch.int64, device=q.device) if stats else None
     if workspace is None:
-        n = mala_bwd_workspace_size(1, Hq, Hkv, total, total, D)
+        n = mala_bwd_workspace_size(1, Hq, Hkv, total, total_k, D)
         workspace = torch.empty(max(n, 16), dtype=torch.uint8, device=q.device)
     mala_bwd_varlen(q, k, v, cu_seqlens, max_seqlen, o, lse, dout, dq, dk, dv, rt, cnt,
-                    workspace, scale, tau, stream=stream)
+                    workspace, scale, tau, stream=stream, cu_seqlens_k=cu_seqlens_k,
+                    max_seqlen_k=max_seqlen_k)
     return dict(dq=dq, dk=dk, dv=dv, row_tiles=rt, counters=cnt)
 
 

@@ -85,10 +85,18 @@ const char* mala_last_error(void) { return g_err; }
 
 namespace {
 
+// Packed batches: the query-row / key-row starts of the sequences (cu null for the
+// fixed-length layout, cu_k null for the same starts as cu) and their longest
+// lengths.
+struct Packed {
+  const int32_t* cu;
+  const int32_t* cu_k;
+  int max_q, max_k;
+};
+
 // Shared by the fixed-length and packed entry points: B slices (sequences) of
-// Nq / Nk rows each (packed: Nq = Nk = total, the head stride), cu the packed
-// sequence starts or null.
-int run_fwd(const void* q, const void* k, const void* v, const int32_t* cu, int max_len,
+// Nq / Nk rows each (packed: Nq, Nk = the query / key totals, the head strides).
+int run_fwd(const void* q, const void* k, const void* v, const Packed& pk,
             void* o, int o_dtype, float* lse, int32_t* row_tiles, int64_t* counters, int B,
             int Hq, int Hkv, int Nq, int Nk, int D, float scale, float tau, hipStream_t s) {
   if (counters) {
@@ -104,8 +112,10 @@ int run_fwd(const void* q, const void* k, const void* v, const int32_t* cu, int 
   p.lse = lse;
   p.row_tiles = row_tiles;
   p.counters = (unsigned long long*)counters;
-  p.cu = cu;
-  p.max_len = cu ? max_len : Nq;
+  p.cu = pk.cu;
+  p.cu_k = pk.cu_k;
+  p.max_len = pk.cu ? pk.max_q : Nq;
+  p.max_len_k = pk.cu ? pk.max_k : Nk;
   p.B = B; p.Hq = Hq; p.Hkv = Hkv; p.Nq = Nq; p.Nk = Nk;
   p.scale2 = scale * mala::kLog2e;
   p.log2tau = log2_tau(tau);
@@ -115,14 +125,14 @@ int run_fwd(const void* q, const void* k, const void* v, const int32_t* cu, int 
   return MALA_OK;
 }
 
-int run_bwd(const void* q, const void* k, const void* v, const int32_t* cu, int max_len,
+int run_bwd(const void* q, const void* k, const void* v, const Packed& pk,
             const void* o, int o_dtype, const float* lse, const void* dout, void* dq, void* dk,
             void* dv, int grad_dtype, int32_t* row_tiles, int64_t* counters, void* workspace,
             int B, int Hq, int Hkv, int Nq, int Nk, int D, float scale, float tau,
             hipStream_t s) {
   hipError_t e;
   // D_q over every row of the q-shaped tensors (packed: all heads x total rows)
-  const long rows = cu ? (long)Hq * Nq : (long)B * Hq * Nq;
+  const long rows = pk.cu ? (long)Hq * Nq : (long)B * Hq * Nq;
   if (counters && (e = mala::launch_fill_zero(counters, 4 * sizeof(int64_t), s)) != hipSuccess)
     return hip_fail(e, "mala_bwd: clearing counters");
   float* dvec = (float*)workspace;
@@ -140,13 +150,15 @@ int run_bwd(const void* q, const void* k, const void* v, const int32_t* cu, int 
   p.grad_bf16 = grad_dtype == MALA_OUT_BF16;
   p.row_tiles = row_tiles;
   p.counters = (unsigned long long*)counters;
-  p.cu = cu;
-  p.max_len = cu ? max_len : Nq;
+  p.cu = pk.cu;
+  p.cu_k = pk.cu_k;
+  p.max_len = pk.cu ? pk.max_q : Nq;
+  p.max_len_k = pk.cu ? pk.max_k : Nk;
   p.B = B; p.Hq = Hq; p.Hkv = Hkv; p.Nq = Nq; p.Nk = Nk;
   p.scale = scale;
   p.scale2 = scale * mala::kLog2e;
   p.log2tau = log2_tau(tau);
-  p.nkblk = ((cu ? max_len : Nk) + mala::kBwdKeys - 1) / mala::kBwdKeys;
+  p.nkblk = (p.max_len_k + mala::kBwdKeys - 1) / mala::kBwdKeys;
   p.nqblk = (p.max_len + mala::kDqRows - 1) / mala::kDqRows;
   if ((e = mala::launch_bwd(p, D, s)) != hipSuccess) return hip_fail(e, "mala_bwd: kernel launch");
   return MALA_OK;
@@ -158,15 +170,18 @@ int check_dtype(int d, const char* what) {
   return MALA_OK;
 }
 
-int check_varlen(const int32_t* cu, int num_seqs, int max_seqlen, int total, int Hq, int Hkv,
-                 int D, float scale, float tau) {
-  if (!cu) return fail(MALA_ERR_INVALID_ARG, "null cu_seqlens");
-  if (num_seqs <= 0 || max_seqlen <= 0 || total <= 0)
+int check_varlen(const int32_t* cu_q, const int32_t* cu_k, int num_seqs, int max_q, int max_k,
+                 int total_q, int total_k, int Hq, int Hkv, int D, float scale, float tau) {
+  if (!cu_q) return fail(MALA_ERR_INVALID_ARG, "null cu_seqlens_q");
+  if (num_seqs <= 0 || max_q <= 0 || max_k <= 0 || total_q <= 0 || total_k <= 0)
     return fail(MALA_ERR_INVALID_ARG, "non-positive size (num_seqs, max_seqlen, total)");
-  if (max_seqlen > total) return fail(MALA_ERR_INVALID_ARG, "max_seqlen (%d) > total (%d)",
-                                      max_seqlen, total);
-  int st = check_common(1, Hq, Hkv, total, total, D, 1, scale, tau);
-  if (!st) st = check_slice_range(total, D);
+  if (max_q > total_q || max_k > total_k)
+    return fail(MALA_ERR_INVALID_ARG, "max_seqlen above its total (%d > %d or %d > %d)", max_q,
+                total_q, max_k, total_k);
+  if (!cu_k && (total_k != total_q || max_k != max_q))
+    return fail(MALA_ERR_INVALID_ARG, "without cu_seqlens_k the key totals must equal the query's");
+  int st = check_common(1, Hq, Hkv, total_q, total_k, D, 1, scale, tau);
+  if (!st) st = check_slice_range(total_k, D);
   return st;
 }
 
@@ -183,21 +198,24 @@ int mala_fwd(const void* q, const void* k, const void* v, void* o, float* lse, i
   if (!st) st = check_slice_range(Nk, D);
   if (!st) st = check_dtype(out_dtype, "out_dtype");
   if (st) return st;
-  return run_fwd(q, k, v, nullptr, 0, o, out_dtype, lse, row_tiles, counters, B, Hq, Hkv, Nq, Nk,
+  return run_fwd(q, k, v, Packed{}, o, out_dtype, lse, row_tiles, counters, B, Hq, Hkv, Nq, Nk,
                  D, scale, tau, (hipStream_t)stream);
 }
 
-int mala_fwd_varlen(const void* q, const void* k, const void* v, const int32_t* cu_seqlens,
-                    void* o, float* lse, int32_t* row_tiles, int64_t* counters, int num_seqs,
-                    int max_seqlen, int total, int Hq, int Hkv, int D, float scale, float tau,
+int mala_fwd_varlen(const void* q, const void* k, const void* v, const int32_t* cu_seqlens_q,
+                    const int32_t* cu_seqlens_k, void* o, float* lse, int32_t* row_tiles,
+                    int64_t* counters, int num_seqs, int max_seqlen_q, int max_seqlen_k,
+                    int total_q, int total_k, int Hq, int Hkv, int D, float scale, float tau,
                     int out_dtype, void* stream) {
   g_err[0] = 0;
   if (!q || !k || !v || !o || !lse) return fail(MALA_ERR_INVALID_ARG, "null q, k, v, o or lse");
-  int st = check_varlen(cu_seqlens, num_seqs, max_seqlen, total, Hq, Hkv, D, scale, tau);
+  int st = check_varlen(cu_seqlens_q, cu_seqlens_k, num_seqs, max_seqlen_q, max_seqlen_k,
+                        total_q, total_k, Hq, Hkv, D, scale, tau);
   if (!st) st = check_dtype(out_dtype, "out_dtype");
   if (st) return st;
-  return run_fwd(q, k, v, cu_seqlens, max_seqlen, o, out_dtype, lse, row_tiles, counters,
-                 num_seqs, Hq, Hkv, total, total, D, scale, tau, (hipStream_t)stream);
+  return run_fwd(q, k, v, Packed{cu_seqlens_q, cu_seqlens_k, max_seqlen_q, max_seqlen_k}, o,
+                 out_dtype, lse, row_tiles, counters, num_seqs, Hq, Hkv, total_q, total_k, D,
+                 scale, tau, (hipStream_t)stream);
 }
 
 size_t mala_bwd_workspace_size(int B, int Hq, int Hkv, int Nq, int Nk, int D) {
@@ -223,31 +241,33 @@ int mala_bwd(const void* q, const void* k, const void* v, const void* o, const f
   if (!workspace || workspace_bytes < need)
     return fail(MALA_ERR_WORKSPACE, "mala_bwd needs %zu workspace bytes, got %zu", need, workspace_bytes);
   if (((uintptr_t)workspace) % 16) return fail(MALA_ERR_WORKSPACE, "workspace not 16-byte aligned");
-  return run_bwd(q, k, v, nullptr, 0, o, o_dtype, lse, dout, dq, dk, dv, grad_dtype, row_tiles,
+  return run_bwd(q, k, v, Packed{}, o, o_dtype, lse, dout, dq, dk, dv, grad_dtype, row_tiles,
                  counters, workspace, B, Hq, Hkv, Nq, Nk, D, scale, tau, (hipStream_t)stream);
 }
 
-int mala_bwd_varlen(const void* q, const void* k, const void* v, const int32_t* cu_seqlens,
-                    const void* o, const float* lse, const void* dout, void* dq, void* dk,
-                    void* dv, int32_t* row_tiles, int64_t* counters, void* workspace,
-                    size_t workspace_bytes, int num_seqs, int max_seqlen, int total, int Hq,
+int mala_bwd_varlen(const void* q, const void* k, const void* v, const int32_t* cu_seqlens_q,
+                    const int32_t* cu_seqlens_k, const void* o, const float* lse,
+                    const void* dout, void* dq, void* dk, void* dv, int32_t* row_tiles,
+                    int64_t* counters, void* workspace, size_t workspace_bytes, int num_seqs,
+                    int max_seqlen_q, int max_seqlen_k, int total_q, int total_k, int Hq,
                     int Hkv, int D, float scale, float tau, int o_dtype, int grad_dtype,
                     void* stream) {
   g_err[0] = 0;
   if (!q || !k || !v || !o || !lse || !dout || !dq || !dk || !dv)
     return fail(MALA_ERR_INVALID_ARG, "null tensor argument");
-  int st = check_varlen(cu_seqlens, num_seqs, max_seqlen, total, Hq, Hkv, D, scale, tau);
+  int st = check_varlen(cu_seqlens_q, cu_seqlens_k, num_seqs, max_seqlen_q, max_seqlen_k,
+                        total_q, total_k, Hq, Hkv, D, scale, tau);
   if (!st) st = check_dtype(o_dtype, "o_dtype");
   if (!st) st = check_dtype(grad_dtype, "grad_dtype");
   if (st) return st;
-  const size_t need = mala_bwd_workspace_size(1, Hq, Hkv, total, total, D);
+  const size_t need = mala_bwd_workspace_size(1, Hq, Hkv, total_q, total_k, D);
   if (!workspace || workspace_bytes < need)
     return fail(MALA_ERR_WORKSPACE, "mala_bwd_varlen needs %zu workspace bytes, got %zu", need,
                 workspace_bytes);
   if (((uintptr_t)workspace) % 16) return fail(MALA_ERR_WORKSPACE, "workspace not 16-byte aligned");
-  return run_bwd(q, k, v, cu_seqlens, max_seqlen, o, o_dtype, lse, dout, dq, dk, dv, grad_dtype,
-                 row_tiles, counters, workspace, num_seqs, Hq, Hkv, total, total, D, scale, tau,
-                 (hipStream_t)stream);
+  return run_bwd(q, k, v, Packed{cu_seqlens_q, cu_seqlens_k, max_seqlen_q, max_seqlen_k}, o,
+                 o_dtype, lse, dout, dq, dk, dv, grad_dtype, row_tiles, counters, workspace,
+                 num_seqs, Hq, Hkv, total_q, total_k, D, scale, tau, (hipStream_t)stream);
 }
 
 size_t mala_decode_workspace_size(int B, int Hq, int D, int num_splits) {

@@ -217,11 +217,11 @@ __global__ __launch_bounds__(1024) void mala_bwd_dkdv_kernel(BwdParams p) {
   const int bhk = blockIdx.x % BHk;
   const int kblk = blockIdx.x / BHk;       // ascending: the longest key blocks first
   const int b = bhk / p.Hkv, hkv = bhk % p.Hkv, grp = p.Hq / p.Hkv;
-  const Seg sg = seq_slice(p.cu, p.max_len, p.Nq, p.Nk, b, p.Hq, p.Hkv);
+  const Seg sg = seq_slice(p, b);
   const int Nq = sg.Nq, Nk = sg.Nk;
   const long off = (long)Nk - Nq;
   const int kb0 = kblk * kBwdKeys;
-  if (kb0 >= Nk) return;                   // past the end of a packed sequence
+  if (kb0 >= Nk || Nq == 0) return;        // past the end of (or a skipped) packed sequence
   const long kbase = sg.kb + (long)hkv * p.Nk;   // key 0 of this (sequence, KV head)
   const int kw = kb0 + grp_k * kBk;        // first key of this wavefront's decision tile
   const int key = kw + c;                  // this lane's key (C-layout column)
@@ -547,7 +547,7 @@ __global__ __launch_bounds__(kDqWaves * 64) void mala_bwd_dq_kernel(BwdParams p)
   const int bh = blockIdx.x % BH;
   const int qblk = p.nqblk - 1 - (int)(blockIdx.x / BH);   // longest rows first
   const int b = bh / p.Hq, hq = bh % p.Hq, hkv = hq / (p.Hq / p.Hkv);
-  const Seg sg = seq_slice(p.cu, p.max_len, p.Nq, p.Nk, b, p.Hq, p.Hkv);
+  const Seg sg = seq_slice(p, b);
   const int Nq = sg.Nq, Nk = sg.Nk;
   if (qblk * kDqRows >= Nq) return;   // past the end of a packed sequence
   const long off = (long)Nk - Nq;

@@ -47,7 +47,7 @@ __global__ __launch_bounds__(kFwdWaves * 64) void mala_fwd_kernel(FwdParams p) {
   const int bh = blockIdx.x % BH;
   const int qblk = p.nqblk - 1 - (int)(blockIdx.x / BH);   // longest rows first
   const int b = bh / p.Hq, hq = bh % p.Hq, hkv = hq / (p.Hq / p.Hkv);
-  const Seg sg = seq_slice(p.cu, p.max_len, p.Nq, p.Nk, b, p.Hq, p.Hkv);
+  const Seg sg = seq_slice(p, b);
   const int Nq = sg.Nq, Nk = sg.Nk;
   if (qblk * kFwdRows >= Nq) return;   // past the end of a packed sequence
   const long off = (long)Nk - Nq;

@@ -30,23 +30,28 @@ constexpr float kLoMassDq = 0.25f;          // dQ: sum of |dS| per query row
 constexpr int kDecStride = 4;                // extra floats per decode partial (lse, count, pad)
 
 // Batches come in two layouts.  Fixed length: [B, H, N, D], slice (b, h) at rows
-// (b H + h) N.  Packed (cu non-null): B sequences along the token axis of
-// [H, total, D] tensors (Nq = Nk = total, the head stride), sequence b at rows
-// cu[b] .. cu[b + 1] of every head (clamped into [0, total], at most max_len rows),
-// attending causally within itself and tiled from its own first row.
+// (b H + h) N.  Packed (cu non-null): B sequences along the token axes of
+// [Hq, Nq, D] queries and [Hkv, Nk, D] keys (Nq, Nk = the totals, the head
+// strides); sequence b holds query rows cu[b] .. cu[b + 1] and key rows
+// cu_k[b] .. cu_k[b + 1] (cu_k null: the same as cu), clamped into the totals and
+// cut to max_len / max_len_k rows; it is a causal problem of its own (bottom-right
+// aligned when it has fewer query rows than keys) tiled from its own first rows.
+// A sequence with more query rows than keys is skipped.
 struct Seg {
   int Nq, Nk;   // rows of the sequence (queries, keys)
   long qb, kb;  // its first row in head 0 of q (o, lse, ...) and of k (v, dk, dv)
 };
-__device__ __forceinline__ Seg seq_slice(const int32_t* cu, int max_len, int Nq, int Nk, int b,
-                                         int Hq, int Hkv) {
-  if (cu) {
-    const int r0 = min(max(cu[b], 0), Nq);
-    const int r1 = min(max(cu[b + 1], r0), Nq);
-    const int n = min(r1 - r0, max_len);
-    return Seg{n, n, (long)r0, (long)r0};
+template <class P>
+__device__ __forceinline__ Seg seq_slice(const P& p, int b) {
+  if (p.cu) {
+    const int32_t* ck = p.cu_k ? p.cu_k : p.cu;
+    const int q0 = min(max(p.cu[b], 0), p.Nq), q1 = min(max(p.cu[b + 1], q0), p.Nq);
+    const int k0 = min(max(ck[b], 0), p.Nk), k1 = min(max(ck[b + 1], k0), p.Nk);
+    const int nk = min(k1 - k0, p.max_len_k);
+    const int nq = min(q1 - q0, p.max_len);
+    return Seg{nq <= nk ? nq : 0, nk, (long)q0, (long)k0};
   }
-  return Seg{Nq, Nk, (long)b * Hq * Nq, (long)b * Hkv * Nk};
+  return Seg{p.Nq, p.Nk, (long)b * p.Hq * p.Nq, (long)b * p.Hkv * p.Nk};
 }
 
 struct FwdParams {
@@ -58,8 +63,9 @@ struct FwdParams {
   int32_t* row_tiles;
   unsigned long long* counters;
   int o_bf16;
-  const int32_t* cu;   // packed batches: [B + 1] sequence starts, else null
-  int max_len;         // packed batches: rows per sequence at most
+  const int32_t* cu;   // packed batches: [B + 1] query-row starts, else null
+  const int32_t* cu_k; // packed batches: [B + 1] key-row starts, or null (= cu)
+  int max_len, max_len_k;   // packed batches: query / key rows per sequence at most
   int B, Hq, Hkv, Nq, Nk;
   float scale2;    // softmax scale * log2(e): scores are kept in base-2 units
   float log2tau;   // log2(tau); -inf for tau == 0
@@ -79,11 +85,12 @@ struct BwdParams {
   int grad_bf16;
   int32_t* row_tiles;
   unsigned long long* counters;
-  const int32_t* cu;   // packed batches: [B + 1] sequence starts, else null
-  int max_len;         // packed batches: rows per sequence at most
+  const int32_t* cu;   // packed batches: [B + 1] query-row starts, else null
+  const int32_t* cu_k; // packed batches: [B + 1] key-row starts, or null (= cu)
+  int max_len, max_len_k;   // packed batches: query / key rows per sequence at most
   int B, Hq, Hkv, Nq, Nk;
   float scale, scale2, log2tau;
-  int nkblk;           // ceil(Nk / kBwdKeys) (packed: ceil(max_len / kBwdKeys))
+  int nkblk;           // ceil(Nk / kBwdKeys) (packed: ceil(max_len_k / kBwdKeys))
   int nqblk;           // ceil(Nq / kDqRows) (packed: ceil(max_len / kDqRows))
 };
 

@@ -121,9 +121,13 @@ def test_varlen_argument_validation(lib):
     P = ctypes.c_void_p
     qkv = [P(16)] * 3
 
-    def fwd(cu, num_seqs, max_len, total, Hq=2, Hkv=1, D=64, tau=0.0):
-        return lib.mala_fwd_varlen(*qkv, cu, P(16), P(16), None, None, num_seqs, max_len, total,
-                                   Hq, Hkv, D, 0.125, tau, mala.OUT_BF16, None)
+    def fwd(cu, num_seqs, max_len, total, Hq=2, Hkv=1, D=64, tau=0.0, cu_k=None, max_k=None,
+            total_k=None):
+        max_k = max_len if max_k is None else max_k
+        total_k = total if total_k is None else total_k
+        return lib.mala_fwd_varlen(*qkv, cu, cu_k, P(16), P(16), None, None, num_seqs, max_len,
+                                   max_k, total, total_k, Hq, Hkv, D, 0.125, tau, mala.OUT_BF16,
+                                   None)
 
     assert fwd(None, 2, 8, 16) == mala.MALA_ERR_INVALID_ARG          # no cu_seqlens
     assert fwd(P(16), 0, 8, 16) == mala.MALA_ERR_INVALID_ARG         # no sequence
@@ -132,8 +136,11 @@ def test_varlen_argument_validation(lib):
     assert fwd(P(16), 2, 8, 16, D=96) == mala.MALA_ERR_UNSUPPORTED
     assert fwd(P(16), 2, 8, 1 << 24, D=128) == mala.MALA_ERR_UNSUPPORTED   # slice range
     assert fwd(P(16), 2, 8, 16, tau=-1.0) == mala.MALA_ERR_INVALID_ARG
-    st = lib.mala_bwd_varlen(*qkv, P(16), *([P(16)] * 6), None, None, P(16), 8, 2, 8, 16, 2, 1,
-                             64, 0.125, 0.0, mala.OUT_F32, mala.OUT_F32, None)
+    assert fwd(P(16), 2, 8, 16, max_k=9) == mala.MALA_ERR_INVALID_ARG     # key sizes without cu_k
+    assert fwd(P(16), 2, 8, 16, cu_k=P(16), max_k=40, total_k=32) == mala.MALA_ERR_INVALID_ARG
+    assert fwd(P(16), 2, 8, 16, cu_k=P(16), total_k=8) == mala.MALA_ERR_INVALID_ARG  # Nq > Nk
+    st = lib.mala_bwd_varlen(*qkv, P(16), None, *([P(16)] * 6), None, None, P(16), 8, 2, 8, 8,
+                             16, 16, 2, 1, 64, 0.125, 0.0, mala.OUT_F32, mala.OUT_F32, None)
     assert st == mala.MALA_ERR_WORKSPACE
     assert lib.mala_bwd_workspace_size(1, 2, 1, 16, 16, 64) > 8
 

@@ -252,6 +252,53 @@ def test_varlen_cut_and_uncovered_rows():
         assert_close("dK", dk[:, r], ob["dk"][0])
 
 
+@pytest.mark.parametrize("tau", [0.0, 1e-3, 0.5])
+def test_varlen_prefill_parity(tau):
+    # packed prefill against cached keys: sequence b has lens_k[b] keys and its last
+    # lens_q[b] rows as queries (bottom-right aligned); one sequence is skipped
+    # because it has more query rows than keys, and its rows stay zero
+    lens_k = [300, 64, 513, 40, 3]
+    lens_q = [100, 64, 1, 17, 5]
+    spec = dict(kind="train", B=1, Hq=4, Hkv=2, D=128, beta=2.5, local=2.0)
+    cuk = np.concatenate([[0], np.cumsum(lens_k)]).astype(np.int32)
+    cuq = np.concatenate([[0], np.cumsum(lens_q)]).astype(np.int32)
+    w = Workload(dict(spec, N=int(cuk[-1])))
+    t = {x: y[0] for x, y in w.tensors().items()}
+    rows = np.concatenate([np.arange(cuk[b + 1] - nq, cuk[b + 1]) for b, nq in enumerate(lens_q)])
+    q = np.ascontiguousarray(t["q"][:, rows])
+    do = np.ascontiguousarray(t["do"][:, rows])
+    k, v = t["k"], t["v"]
+    scale = f32(w.scale)
+    bq, bk = mala.mala_geometry(w.D, mala.PASS_FWD)
+    Q, K, V, DO = dev(q), dev(k), dev(v), dev(do)
+    CUQ, CUK = (torch.from_numpy(c).to("cuda") for c in (cuq, cuk))
+    kw = dict(cu_seqlens_k=CUK, max_seqlen_k=max(lens_k))
+    g = mala.fwd_varlen(Q, K, V, CUQ, max(lens_q), scale, tau, **kw)
+    gb = mala.bwd_varlen(Q, K, V, CUQ, max(lens_q), g["o"], g["lse"], DO, scale, tau, **kw)
+    torch.cuda.synchronize()
+    o, lse, rt = host(g["o"]), host(g["lse"]), host(g["row_tiles"])
+    dq, dk, dv = host(gb["dq"]), host(gb["dk"]), host(gb["dv"])
+    legal = 0
+    for b, (nq, nk) in enumerate(zip(lens_q, lens_k)):
+        rq, rk = slice(int(cuq[b]), int(cuq[b + 1])), slice(int(cuk[b]), int(cuk[b + 1]))
+        if nq > nk:
+            assert (o[:, rq] == 0).all() and (dq[:, rq] == 0).all() and (dk[:, rk] == 0).all()
+            continue
+        qf, dof = bf16_to_f64(q[None, :, rq]), bf16_to_f64(do[None, :, rq])
+        kf, vf = bf16_to_f64(k[None, :, rk]), bf16_to_f64(v[None, :, rk])
+        of = oracle.mala_fwd(qf, kf, vf, scale, f32(tau), bq, bk)
+        ob = oracle.mala_bwd(qf, kf, vf, of["o"], of["lse"], dof, scale, f32(tau), bq, bk)
+        assert_close("O seq %d (%d of %d)" % (b, nq, nk), o[:, rq], of["o"][0])
+        assert np.abs(lse[:, rq] - of["lse"][0]).max() <= LSE_DIAG
+        ex_f = exempt_rows(tau, of["tie_abs"][0])
+        assert_counts("fwd row tiles seq %d" % b, rt[:, rq], of["row_tiles"][0], ex_f)
+        assert_close("dQ seq %d" % b, dq[:, rq], ob["dq"][0])
+        assert_close("dK seq %d" % b, dk[:, rk], ob["dk"][0])
+        assert_close("dV seq %d" % b, dv[:, rk], ob["dv"][0])
+        legal += legal_tiles(1, w.Hq, nq, nk, bq, bk)
+    assert int(host(g["counters"])[0]) == legal and int(host(gb["counters"])[0]) == legal
+
+
 @pytest.mark.parametrize("tau", [1e-4, 1.0])
 def test_varlen_full_size_equals_per_sequence_calls(tau):
     # 32768 packed tokens of the language-model-like inputs: every sequence's
