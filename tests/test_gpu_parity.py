@@ -106,6 +106,15 @@ def test_train_parity_small(name, tau):
     _check_train(w, q, k, v, do, tau)
 
 
+@pytest.mark.parametrize("name,tau,seed", [(n, t, sd) for n in ("gqa_d128_ragged",
+                                                                   "local_d64_ragged",
+                                                                   "lm_d128_ragged")
+                                            for t in (1e-3, 1.0) for sd in (1, 2)])
+def test_train_parity_other_seeds(name, tau, seed):
+    w, q, k, v, do = _train_case(name, tau, seed=seed)
+    _check_train(w, q, k, v, do, tau)
+
+
 @pytest.mark.parametrize("Nq,tau", [(200, 0.0), (200, 0.05), (77, 1.0)])
 def test_prefill_against_longer_cache(Nq, tau):
     w, q, k, v, do = _train_case("gqa_d128_ragged", tau, Nq=Nq)
