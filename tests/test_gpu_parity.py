@@ -695,3 +695,30 @@ def test_decode_bf16_output():
     b = mala.decode(q, k, v, f32(w.scale), 1e-4, 4, out_dtype=torch.bfloat16)
     torch.cuda.synchronize()
     assert torch.equal(b["o"], a["o"].to(torch.bfloat16)) and torch.equal(b["lse"], a["lse"])
+
+
+def test_concurrent_streams_match_sequential():
+    # the library keeps no device state between calls: two forward + backward calls
+    # on two streams at once give the results of the calls run one after the other
+    tau = 1e-3
+    cases = [_train_case("gqa_d128_ragged", tau), _train_case("local_d64_ragged", tau)]
+    dev_in = [tuple(map(dev, c[1:])) + (f32(c[0].scale),) for c in cases]
+
+    def run(Q, K, V, DO, scale):
+        f = mala.fwd(Q, K, V, scale, tau)
+        b = mala.bwd(Q, K, V, f["o"], f["lse"], DO, scale, tau)
+        return [f["o"], f["lse"], f["row_tiles"], b["dq"], b["dk"], b["dv"], b["row_tiles"]]
+
+    ref = [run(*a) for a in dev_in]
+    torch.cuda.synchronize()
+    streams = [torch.cuda.Stream(), torch.cuda.Stream()]
+    outs = [None, None]
+    for i in range(2):
+        streams[i].wait_stream(torch.cuda.current_stream())
+    for i, (s, a) in enumerate(zip(streams, dev_in)):
+        with torch.cuda.stream(s):
+            outs[i] = run(*a)
+    torch.cuda.synchronize()
+    for r, o in zip(ref, outs):
+        for x, y in zip(r, o):
+            assert torch.equal(x, y)
