@@ -312,10 +312,10 @@ def cpu_baseline(step_ms_model):
 
 
 COUNTER_CMD = ("cd /tmp && export TMPDIR=/tmp && timeout -s KILL 180 rocprofv3 --pmc {c} "
-               "--output-format csv -d $REPO/gpurun_out/pmc_{d} -o run -- "
+               "--output-format csv -d $OUT/pmc_{d} -o run -- "
                "python $REPO/bench.py --counter-pass")
 TRACE_CMD = ("cd /tmp && export TMPDIR=/tmp && timeout -k 10 600 rocprofv3 --kernel-trace --stats "
-             "--output-format csv -d $REPO/gpurun_out/trace_bench -o bench -- "
+             "--output-format csv -d $OUT/trace_bench -o bench -- "
              "python $REPO/bench.py --steps 2 --warmup 1 --reps 2 --kernel-warmup 1 "
              "--supp-reps 2 --supp-warmup 1 --no-cpu-baseline --no-32k --no-lm --no-ragged")
 
@@ -343,7 +343,7 @@ def counter_pass():
 
 SKIP_TAUS = (0.0, 1.0, 1e30)
 SKIP_TRACE_CMD = ("cd /tmp && export TMPDIR=/tmp && timeout -k 10 300 rocprofv3 --kernel-trace "
-                  "--stats --output-format csv -d $REPO/gpurun_out/trace_skip -o skip -- "
+                  "--stats --output-format csv -d $OUT/trace_skip -o skip -- "
                   "python $REPO/bench.py --skip-pass")
 
 
@@ -380,9 +380,10 @@ def summarize_skip_trace(trace_csv):
             dur[r["Kernel_Name"]].append(
                 (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e6)
     lines = ["# Cost of skipped tiles: the 32768-token language-model-like workload", "",
-             "Command (run from the repository root on one MI355X; `$REPO` is that root):", "",
+             "Command (run from the repository root on one MI355X; `$REPO` is that root, "
+             "`$OUT` an output directory):", "",
              "```", SKIP_TRACE_CMD, "python bench.py --summarize-skip-trace "
-             "gpurun_out/trace_skip/skip_kernel_trace.csv", "```", "",
+             "$OUT/trace_skip/skip_kernel_trace.csv", "```", "",
              "Mean kernel durations (ms) over 3 calls per tau.  tau = 1e30 skips every "
              "backward tile and every forward tile but each row's first (the cost floor of "
              "the skip path: score MFMAs, the test, staging and synchronisation); the last "
@@ -446,8 +447,8 @@ def summarize_counters(fetch_csv, write_csv):
            "commands": [COUNTER_CMD.format(c="FETCH_SIZE", d="fetch"),
                         COUNTER_CMD.format(c="WRITE_SIZE", d="write"),
                         "python bench.py --summarize-counters "
-                        "gpurun_out/pmc_fetch/run_counter_collection.csv "
-                        "gpurun_out/pmc_write/run_counter_collection.csv"]}
+                        "$OUT/pmc_fetch/run_counter_collection.csv "
+                        "$OUT/pmc_write/run_counter_collection.csv"]}
     with open(os.path.join(ROOT, "profiles", "mala_bwd_traffic_128k.json"), "w") as fh:
         json.dump(out, fh, indent=1)
     print("mala_bwd HBM bytes per launch %.3f GB (fetch x%.1f, write x%.1f)"
@@ -469,9 +470,10 @@ def summarize_trace(trace_csv):
         dur[r["Kernel_Name"]].append((int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e6)
     ms = lambda v: sum(v) / len(v) if v else float("nan")
     lines = ["# Kernel time of one bench run: 131072-token fwd + bwd and decode", "",
-             "Command (run from the repository root on one MI355X; `$REPO` is that root):", "",
+             "Command (run from the repository root on one MI355X; `$REPO` is that root, "
+             "`$OUT` an output directory):", "",
              "```", TRACE_CMD, "python bench.py --summarize-trace "
-             "gpurun_out/trace_bench/bench_kernel_trace.csv", "```", "",
+             "$OUT/trace_bench/bench_kernel_trace.csv", "```", "",
              "Durations in milliseconds from the rocprofv3 kernel trace.  Each operator is "
              "called 12 times: dispatches 1-6 at tau = 1e-4 (the bench step and its "
              "event-timed calls), 7-9 at tau = 0 (dense through the same kernels), 10-12 at "
@@ -513,9 +515,10 @@ def summarize_mfma(csv_path):
             by[names[d]].append(v)
     cmd = COUNTER_CMD.format(c="MfmaUtil MfmaFlopsBF16", d="mfma")
     lines = ["# MFMA utilisation of the 131072-token fwd + bwd kernels", "",
-             "Command (from the repository root on one MI355X; `$REPO` is that root):", "",
+             "Command (from the repository root on one MI355X; `$REPO` is that root, `$OUT` an "
+             "output directory):", "",
              "```", cmd,
-             "python bench.py --summarize-mfma gpurun_out/pmc_mfma/run_counter_collection.csv",
+             "python bench.py --summarize-mfma $OUT/pmc_mfma/run_counter_collection.csv",
              "```", "",
              "`MfmaUtil` = MFMA-busy cycles summed over SIMDs / (active cycles x SIMDs), %; "
              "`MfmaFlopsBF16` = executed bf16 MFMA flops per dispatch (the hi/lo split and "
