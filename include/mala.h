@@ -17,8 +17,9 @@
  *
  * Conventions shared by every entry point
  *   - All tensor arguments are DEVICE pointers, owned by the caller, contiguous,
- *     in BHSD layout (batch, head, sequence, head_dim).  The library never
- *     allocates, frees or retains them.
+ *     in BHSD layout (batch, head, sequence, head_dim; the packed entry points use
+ *     [head, token, head_dim]).  The library never allocates, frees or retains
+ *     them.
  *   - Q, K, V, dO, the KV caches and the decode query are bf16 (passed as void*);
  *     O and the gradients are fp32 or bf16 (MALA_OUT_*), LSE is fp32; LSE is the
  *     natural-log normalizer z_q = log sum_{k in R_q} exp(s_qk) of the retained
@@ -38,8 +39,10 @@
  *     reported by the caller's next synchronisation.  Calls are re-entrant; the
  *     library keeps no state between calls.
  *   - Statistics pointers (row_tiles, head_tiles, counters) may be NULL.  When
- *     given they are OVERWRITTEN by the call (the library clears them first on
- *     the same stream).  No mask or retained-tile index is ever materialised.
+ *     given they are OVERWRITTEN by the call: the counters are cleared first on
+ *     the same stream, and per-row / per-head statistics are written for every
+ *     row and head the call computes.  No mask or retained-tile index is ever
+ *     materialised.
  */
 #ifndef MALA_H
 #define MALA_H
