@@ -534,6 +534,46 @@ def summarize_mfma(csv_path):
     print("\n".join(lines))
 
 
+def summarize_pipes(csv_path):
+    """profiles/pipe_util_128k.md from a `rocprofv3 --pmc VALUBusy MfmaUtil LdsUtil`
+    pass over --counter-pass: how busy each pipe of the CU is during each kernel
+    (rocprofv3's derived counters, % of the kernel's active cycles)."""
+    import csv
+    import collections
+    per = collections.defaultdict(dict)
+    names = {}
+    with open(csv_path) as fh:
+        for r in csv.DictReader(fh):
+            d = r["Dispatch_Id"]
+            c = r["Counter_Name"]
+            per[d][c] = per[d].get(c, 0.0) + float(r["Counter_Value"])
+            names[d] = r["Kernel_Name"]
+    by = collections.defaultdict(list)
+    for d, v in per.items():
+        if "mala" in names[d] and "fill_zero" not in names[d]:
+            by[names[d]].append(v)
+    cmd = COUNTER_CMD.format(c="VALUBusy MfmaUtil LdsUtil", d="pipes")
+    lines = ["# Pipe utilisation of the 131072-token fwd + bwd kernels", "",
+             "Command (from the repository root on one MI355X; `$REPO` is that root, `$OUT` an "
+             "output directory):", "",
+             "```", cmd,
+             "python bench.py --summarize-pipes $OUT/pmc_pipes/run_counter_collection.csv",
+             "```", "",
+             "`VALUBusy` = cycles issuing vector-ALU instructions per CU / active cycles; "
+             "`MfmaUtil` = MFMA-busy cycles per SIMD / active cycles; `LdsUtil` = cycles the "
+             "LDS is active per CU / active cycles (all %, mean over the dispatches).", "",
+             "| kernel | dispatches | VALUBusy % | MfmaUtil % | LdsUtil % |",
+             "|---|---|---|---|---|"]
+    for k, vs in sorted(by.items()):
+        m = lambda c: sum(v.get(c, 0.0) for v in vs) / len(vs)
+        lines.append("| `%s` | %d | %.1f | %.1f | %.1f |" % (k.replace("|", "/"), len(vs),
+                                                          m("VALUBusy"), m("MfmaUtil"),
+                                                          m("LdsUtil")))
+    with open(os.path.join(ROOT, "profiles", "pipe_util_128k.md"), "w") as fh:
+        fh.write("\n".join(lines) + "\n")
+    print("\n".join(lines))
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -561,6 +601,7 @@ def main():
                     help="run only the program of the skip-cost trace")
     ap.add_argument("--summarize-skip-trace", metavar="KERNEL_TRACE_CSV")
     ap.add_argument("--summarize-mfma", metavar="COUNTER_CSV")
+    ap.add_argument("--summarize-pipes", metavar="COUNTER_CSV")
     args = ap.parse_args()
     if args.summarize_counters:
         summarize_counters(*args.summarize_counters)
@@ -573,6 +614,9 @@ def main():
         return
     if args.summarize_mfma:
         summarize_mfma(args.summarize_mfma)
+        return
+    if args.summarize_pipes:
+        summarize_pipes(args.summarize_pipes)
         return
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU only: the MALA operator is built and measured on a "
