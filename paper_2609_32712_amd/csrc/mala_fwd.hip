@@ -18,9 +18,10 @@
 //                         equivalent to the natural-log test), rows with l == 0
 //                         always retain; one ballot makes the branch wave-uniform;
 //   retained path         lazy rescale of O and l (only when some row's max grew by
-//                         more than 2^8), P = exp2(S - m) split into two bf16 terms,
-//                         O^T += V^T P^T (2 x 8 MFMAs, V^T operand through
-//                         ds_read_b64_tr_b16).
+//                         more than 2^8), P = exp2(S - m) as a bf16 hi term, plus a
+//                         lo term when the tile holds more than kFwdLoShare of some
+//                         row's normalizer, O^T += V^T P^T (8 MFMAs per term, V^T
+//                         operand through ds_read_b64_tr_b16).
 // A skipped tile costs its QK MFMAs, one max reduction and one compare.
 #include "mala_device.h"
 #include "mala_kernels.h"
@@ -189,12 +190,22 @@ __global__ __launch_bounds__(kFwdWaves * 64) void mala_fwd_kernel(FwdParams p) {
         float ps4[4];
 #pragma unroll
         for (int g = 0; g < 4; ++g) ps4[g] = (sv[4 * g] + sv[4 * g + 1]) + (sv[4 * g + 2] + sv[4 * g + 3]);
-        l += halves_sum((ps4[0] + ps4[1]) + (ps4[2] + ps4[3]));
-        // P as two bf16 terms: the backward's D = rowsum(O * dO) cancels against
-        // dP for dominant keys, so O must be accurate well beyond one bf16 rounding
+        const float ps = halves_sum((ps4[0] + ps4[1]) + (ps4[2] + ps4[3]));
+        l += ps;
+        // P as two bf16 terms where it matters: the backward's D = rowsum(O * dO)
+        // cancels against dP for dominant keys, so their probabilities must be
+        // accurate well beyond one bf16 rounding.  A tile whose mass is a small
+        // share of every row's retained normalizer (this tile included) runs the
+        // high term only.
+        const bool need_lo = wave_any(ps > kFwdLoShare * l);
         bf16x8 ph[2], pl[2];
-        split_bf16x8(sv, ph[0], pl[0]);
-        split_bf16x8(sv + 8, ph[1], pl[1]);
+        if (need_lo) {
+          split_bf16x8(sv, ph[0], pl[0]);
+          split_bf16x8(sv + 8, ph[1], pl[1]);
+        } else {
+          ph[0] = hi_bf16x8(sv);
+          ph[1] = hi_bf16x8(sv + 8);
+        }
         // O^T[d][q] += V^T[d][key] P^T[key][q]; V^T rows through transposed LDS reads
         bf16x8 va[DB][2];
 #pragma unroll
@@ -208,10 +219,12 @@ __global__ __launch_bounds__(kFwdWaves * 64) void mala_fwd_kernel(FwdParams p) {
         for (int ks = 0; ks < 2; ++ks)
 #pragma unroll
           for (int db = 0; db < DB; ++db) acc[db] = mfma32(va[db][ks], ph[ks], acc[db]);
+        if (need_lo) {
 #pragma unroll
-        for (int ks = 0; ks < 2; ++ks)
+          for (int ks = 0; ks < 2; ++ks)
 #pragma unroll
-          for (int db = 0; db < DB; ++db) acc[db] = mfma32(va[db][ks], pl[ks], acc[db]);
+            for (int db = 0; db < DB; ++db) acc[db] = mfma32(va[db][ks], pl[ks], acc[db]);
+        }
       }
     }
     wait_vm();

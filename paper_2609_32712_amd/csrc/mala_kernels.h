@@ -27,6 +27,12 @@ constexpr int kBwdKeys = 128;                // keys per dK/dV workgroup (4 key 
 constexpr float kLoMassDv = 1.0f / 16;      // dV: P mass per key
 constexpr float kLoMassDk = 0.25f;          // dK: sum of |dS| per key
 constexpr float kLoMassDq = 0.25f;          // dQ: sum of |dS| per query row
+// Forward: the lo term of P runs on a tile only if, for some row of the wavefront,
+// the tile's mass exceeds this share of the row's retained normalizer (the tile
+// included).  The tiles that hold a row's dominant keys then keep ~16 significant
+// bits; every other tile adds at most 2^-9 x its share of the row's mass as
+// rounding error, and such errors of many small tiles do not line up.
+constexpr float kFwdLoShare = 1.0f / 64;
 constexpr int kDecStride = 4;                // extra floats per decode partial (lse, count, pad)
 
 // Batches come in two layouts.  Fixed length: [B, H, N, D], slice (b, h) at rows
