@@ -662,12 +662,15 @@ __global__ __launch_bounds__(kDqWaves * 64) void mala_bwd_dq_kernel(BwdParams p)
 #pragma unroll
       for (int r = 0; r < 16; ++r) dsv[r] = sv[r] * dpd[r];
       // dQ runs this tile without dS's lo term while this row's sum of |dS| over
-      // such tiles stays within kLoMassDq (for every row of the wavefront)
+      // such tiles stays within kLoMassDq (for every row of the wavefront); a tile
+      // holding more than kLoTileDq of some row's |dS| always takes the lo term, so
+      // that the budget goes to the many small tiles
       float as = 0.f;
 #pragma unroll
       for (int r = 0; r < 16; ++r) as += fabsf(dsv[r]);
-      const float fq_new = fdq + halves_sum(as);
-      const bool with_lo = wave_any(fq_new > kLoMassDq);
+      const float as_row = halves_sum(as);
+      const float fq_new = fdq + as_row;
+      const bool with_lo = wave_any(fq_new > kLoMassDq || as_row > kLoTileDq);
       if (!with_lo) fdq = fq_new;
       // dQ^T[d][q] += K^T[d][key] dS^T[key][q]: k-step ks takes C registers
       // 8 ks .. 8 ks + 7 as the B operand, K^T through transposed reads of the same

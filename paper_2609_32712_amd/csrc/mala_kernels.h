@@ -26,7 +26,8 @@ constexpr int kBwdKeys = 128;                // keys per dK/dV workgroup (4 key 
 // times the softmax scale).
 constexpr float kLoMassDv = 1.0f / 16;      // dV: P mass per key
 constexpr float kLoMassDk = 0.25f;          // dK: sum of |dS| per key
-constexpr float kLoMassDq = 0.25f;          // dQ: sum of |dS| per query row
+constexpr float kLoMassDq = 1.0f;           // dQ: sum of |dS| per query row
+constexpr float kLoTileDq = kLoMassDq / 16;  // dQ: |dS| of one tile and row, above it lo always
 // Forward: the lo term of P runs on a tile only if, for some row of the wavefront,
 // the tile's mass exceeds this share of the row's retained normalizer (the tile
 // included).  The tiles that hold a row's dominant keys then keep ~16 significant
