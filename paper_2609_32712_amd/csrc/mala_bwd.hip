@@ -377,12 +377,14 @@ __global__ __launch_bounds__(1024) void mala_bwd_dkdv_kernel(BwdParams p) {
             for (int e = 0; e < 4; ++e) ds[4 * g + e] = p4[e] * (dp[4 * g + e] - d4[e]);
           }
           // dK runs this tile without dS's lo term while the key's sum of |dS| in
-          // such tiles stays within kLoMassDk (for every key of the tile)
+          // such tiles stays within kLoMassDk (for every key of the tile); a tile
+          // holding more than kLoTileDk of some key's |dS| always takes the lo term
           float as = 0.f;
 #pragma unroll
           for (int r = 0; r < 16; ++r) as += fabsf(ds[r]);
-          const float fk_new = fdk + halves_sum(as);
-          const bool with_lo = wave_any(fk_new > kLoMassDk);
+          const float as_key = halves_sum(as);
+          const float fk_new = fdk + as_key;
+          const bool with_lo = wave_any(fk_new > kLoMassDk || as_key > kLoTileDk);
           if (!with_lo) fdk = fk_new;
           bf16x8 xh[2], xl[2];
           if (with_lo) {

@@ -26,6 +26,7 @@ constexpr int kBwdKeys = 128;                // keys per dK/dV workgroup (4 key 
 // times the softmax scale).
 constexpr float kLoMassDv = 1.0f / 16;      // dV: P mass per key
 constexpr float kLoMassDk = 0.25f;          // dK: sum of |dS| per key
+constexpr float kLoTileDk = kLoMassDk / 16;  // dK: |dS| of one tile and key, above it lo always
 constexpr float kLoMassDq = 1.0f;           // dQ: sum of |dS| per query row
 constexpr float kLoTileDq = kLoMassDq / 16;  // dQ: |dS| of one tile and row, above it lo always
 // Forward: the lo term of P runs on a tile only if, for some row of the wavefront,
