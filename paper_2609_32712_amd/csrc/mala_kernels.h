@@ -23,7 +23,10 @@ constexpr int kBwdKeys = 128;                // keys per dK/dV workgroup (4 key 
 // of the tiles run without it stays within a budget, and out of dQ (dS) while the
 // same holds for every query row.  Since |lo| <= 2^-8 |hi + lo|, the added error
 // of a dV (dK, dQ) element is at most 2^-8 x budget x the largest |dO| (|Q|, |K|,
-// times the softmax scale).
+// times the softmax scale).  For dK and dQ, a tile whose own sum of |dS| for some
+// key (row) exceeds 1/16 of the budget always takes the lo term without drawing on
+// the budget, which is thereby kept for the many small tiles; the bound holds as
+// before.
 constexpr float kLoMassDv = 1.0f / 16;      // dV: P mass per key
 constexpr float kLoMassDk = 0.25f;          // dK: sum of |dS| per key
 constexpr float kLoTileDk = kLoMassDk / 16;  // dK: |dS| of one tile and key, above it lo always
