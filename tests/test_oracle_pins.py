@@ -10,6 +10,9 @@ None of these tests compares the oracle with a retyped copy of itself:
   * support nesting (Offline Sparse Probability paragraph);
   * the first legal tile is always retained (empty-state convention);
   * closed-form cases: the two-token boundary and uniform scores (tests/golden);
+  * the per-row tie distances (how close some tile's decisive test value T came to
+    tau; they decide which rows the GPU tests exempt from count parity) against T
+    from the direct sums and against the closed forms of the golden cases;
   * GQA equals MHA on repeated K/V; decode with one split equals the forward's
     last row; the split merge equals softmax restricted to the retained set;
   * MALA gradients at tau > 0 against finite differences of the softmax restricted
@@ -55,10 +58,13 @@ def softmax_rows(S, keep=None):
 def direct_sum_forward(S, tau, bq, bk):
     """The forward rule with direct sums: Z^(t) = sum of exp(s) over retained keys,
     ratio r = exp(tile row max) / Z^(t), skip iff r < tau / L for every row with a
-    legal key in the tile; blocks visited from the diagonal downwards."""
+    legal key in the tile; blocks visited from the diagonal downwards.  Also returns
+    each tile's decisive value T = max over those rows of L * r (+inf while one of
+    them has Z = 0), NaN for tiles that are not visited."""
     Nq, Nk = S.shape
     Tr, Tc = -(-Nq // bq), -(-Nk // bk)
     keep = np.full((Tr, Tc), -1, dtype=np.int8)
+    Tval = np.full((Tr, Tc), np.nan)
     R = np.zeros((Nq, Nk), dtype=bool)
     L = np.arange(Nq) + 1 + (Nk - Nq)
     for i in range(Tr):
@@ -68,32 +74,38 @@ def direct_sum_forward(S, tau, bq, bk):
         for j in range(top, -1, -1):
             cols = range(j * bk, min(Nk, (j + 1) * bk))
             demand = False
+            T = -math.inf
             for r in rows:
                 legal = [c for c in cols if np.isfinite(S[r, c])]
                 if not legal:
                     continue
                 if Z[r] == 0.0:
                     demand = True
+                    T = math.inf
                     continue
                 ratio = math.exp(max(S[r, c] for c in legal)) / Z[r]
                 if ratio >= tau / L[r]:
                     demand = True
+                T = max(T, L[r] * ratio)
             keep[i, j] = int(demand)
+            Tval[i, j] = T
             if demand:
                 for r in rows:
                     for c in cols:
                         if np.isfinite(S[r, c]):
                             Z[r] += math.exp(S[r, c])
                             R[r, c] = True
-    return keep, R
+    return keep, R, Tval
 
 
 def direct_sum_backward(S, lse, tau, bq, bk):
     """The offline rule with probabilities: tile (j, i) retained iff some valid entry
-    has exp(s - lse) >= tau / L."""
+    has exp(s - lse) >= tau / L.  Also returns each tile's decisive value
+    T = max over its valid entries of L * exp(s - lse) (NaN without a valid entry)."""
     Nq, Nk = S.shape
     Tr, Tc = -(-Nq // bq), -(-Nk // bk)
     keep = np.full((Tr, Tc), -1, dtype=np.int8)
+    Tval = np.full((Tr, Tc), np.nan)
     L = np.arange(Nq) + 1 + (Nk - Nq)
     for i in range(Tr):
         for j in range(Tc):
@@ -104,7 +116,22 @@ def direct_sum_backward(S, lse, tau, bq, bk):
                 continue
             P = np.exp(blk - lse[rs, None])
             keep[i, j] = int((P >= tau / L[rs, None]).any())
-    return keep
+            Tval[i, j] = float((L[rs, None] * P).max())
+    return keep, Tval
+
+
+def row_tie_distances(Tval, Nq, bq, tau):
+    """Per query row: the smallest |T - tau| and |T / tau - 1| over the finite decisive
+    values of the tiles of its query block (+inf if there is none)."""
+    ta = np.full(Nq, np.inf)
+    tr = np.full(Nq, np.inf)
+    for i in range(Tval.shape[0]):
+        t = Tval[i][np.isfinite(Tval[i])]
+        if t.size:
+            rows = slice(i * bq, min(Nq, (i + 1) * bq))
+            ta[rows] = np.abs(t - tau).min()
+            tr[rows] = np.abs(t / tau - 1).min()
+    return ta, tr
 
 
 def rand_inputs(rng, B, Hq, Hkv, Nq, Nk, D, spread=1.0):
@@ -202,13 +229,64 @@ def test_forward_and_backward_decisions_match_direct_sums(bq, bk, tau):
     N, scale = q.shape[2], 1.0
     f = oracle.mala_fwd(q, k, v, scale, tau, bq, bk, want_tiles=True)
     S = scores(q[0, 0], k[0, 0], scale)
-    keep, R = direct_sum_forward(S, tau, bq, bk)
+    keep, R, _ = direct_sum_forward(S, tau, bq, bk)
     np.testing.assert_array_equal(f["tile_keep"][0, 0], keep)
     P, lse = softmax_rows(S, R)
     np.testing.assert_allclose(f["o"][0, 0], P @ v[0, 0], rtol=0, atol=1e-11)
     np.testing.assert_allclose(f["lse"][0, 0], lse, rtol=0, atol=1e-11)
     b = oracle.mala_bwd(q, k, v, f["o"], f["lse"], do, scale, tau, bq, bk, want_tiles=True)
-    np.testing.assert_array_equal(b["tile_keep"][0, 0], direct_sum_backward(S, lse, tau, bq, bk))
+    np.testing.assert_array_equal(b["tile_keep"][0, 0], direct_sum_backward(S, lse, tau, bq, bk)[0])
+
+
+def _assert_ties(got_abs, got_rel, exp_abs, exp_rel, what):
+    # both sides are fp64; their T values differ by the order of the sums only
+    for got, exp, name in ((got_abs, exp_abs, "tie_abs"), (got_rel, exp_rel, "tie_rel")):
+        got, exp = np.asarray(got, dtype=np.float64), np.asarray(exp, dtype=np.float64)
+        assert (np.isinf(got) == np.isinf(exp)).all(), (what, name, got, exp)
+        fin = np.isfinite(exp)
+        np.testing.assert_allclose(got[fin], exp[fin], rtol=1e-9, atol=1e-13,
+                                   err_msg="%s %s" % (what, name))
+
+
+@pytest.mark.parametrize("bq,bk", [(1, 1), (2, 4), (4, 2), (3, 5), (4, 8)])
+@pytest.mark.parametrize("tau", [1e-3, 0.05, 1.0, 4.0])
+def test_tie_distances_match_direct_sums(bq, bk, tau):
+    # the oracle's per-row tie distance (min |T - tau| and |T/tau - 1| over the tiles
+    # of the row's query block) decides which rows the GPU parity tests exempt from
+    # count parity; here T comes from the direct sums instead of the m / l recurrence
+    q, k, v, do = _decision_inputs(bq, bk, tau)
+    scale = 1.0
+    f = oracle.mala_fwd(q, k, v, scale, tau, bq, bk)
+    S = scores(q[0, 0], k[0, 0], scale)
+    N = S.shape[0]
+    _, R, Tf = direct_sum_forward(S, tau, bq, bk)
+    _assert_ties(f["tie_abs"][0, 0], f["tie_rel"][0, 0], *row_tie_distances(Tf, N, bq, tau),
+                 "forward")
+    _, lse = softmax_rows(S, R)
+    b = oracle.mala_bwd(q, k, v, f["o"], f["lse"], do, scale, tau, bq, bk)
+    _, Tb = direct_sum_backward(S, lse, tau, bq, bk)
+    _assert_ties(b["tie_abs"][0, 0], b["tie_rel"][0, 0], *row_tie_distances(Tb, N, bq, tau),
+                 "backward")
+
+
+def test_tie_distances_on_gqa_prefill_and_ragged_blocks():
+    # several heads of a group, fewer query rows than keys and a partial last block:
+    # the tie distances still follow the direct sums row by row
+    rng = np.random.default_rng(17)
+    q, k, v, do = needle_inputs(rng, 41, 6, 3.0, local=2.0, Hq=4, Hkv=2)
+    q, do = q[:, :, -29:].copy(), do[:, :, -29:].copy()
+    tau, scale, bq, bk = 0.02, 0.8, 4, 6
+    f = oracle.mala_fwd(q, k, v, scale, tau, bq, bk)
+    b = oracle.mala_bwd(q, k, v, f["o"], f["lse"], do, scale, tau, bq, bk)
+    for h in range(4):
+        S = scores(q[0, h], k[0, h // 2], scale)
+        _, R, Tf = direct_sum_forward(S, tau, bq, bk)
+        _assert_ties(f["tie_abs"][0, h], f["tie_rel"][0, h], *row_tie_distances(Tf, 29, bq, tau),
+                     "forward head %d" % h)
+        _, lse = softmax_rows(S, R)
+        _, Tb = direct_sum_backward(S, lse, tau, bq, bk)
+        _assert_ties(b["tie_abs"][0, h], b["tie_rel"][0, h], *row_tie_distances(Tb, 29, bq, tau),
+                     "backward head %d" % h)
 
 
 def test_some_decision_cases_actually_skip():
@@ -344,6 +422,17 @@ def test_two_token_closed_form(case):
     keep = f["tile_keep"][0, 0]
     assert keep[1, 1] == 1 and keep[0, 0] == 1
     assert keep[1, 0] == case["row1_keeps_key0"]
+    # decisive values (golden "tie_rules"): forward T(1,0) = 2 exp(-delta); row 0 only
+    # has its diagonal tile, tested in the empty state
+    e = math.exp(-delta)
+    _assert_ties(f["tie_abs"][0, 0], f["tie_rel"][0, 0], [math.inf, abs(2 * e - tau)],
+                 [math.inf, abs(2 * e / tau - 1)], "forward")
+    kept = case["row1_keeps_key0"]
+    t10, t11 = (2 * e / (1 + e), 2 / (1 + e)) if kept else (2 * e, 2.0)
+    bt = oracle.mala_bwd(q, k, v, f["o"], f["lse"], do, 1.0, tau, 1, 1)
+    _assert_ties(bt["tie_abs"][0, 0], bt["tie_rel"][0, 0],
+                 [abs(1 - tau), min(abs(t10 - tau), abs(t11 - tau))],
+                 [abs(1 / tau - 1), min(abs(t10 / tau - 1), abs(t11 / tau - 1))], "backward")
     if not case["row1_keeps_key0"]:
         assert f["o"][0, 0, 1, 0] == -2.0 and abs(f["lse"][0, 0, 1] - a) < 1e-15
         o, lse = oracle.dense_fwd(q, k, v, 1.0)
@@ -380,6 +469,17 @@ def test_uniform_scores_closed_form(case):
         assert abs(f["lse"][0, 0, r] - math.log(n)) < 1e-14
         np.testing.assert_allclose(f["o"][0, 0, r], v[0, 0, L - n: L].mean(axis=0), atol=1e-14)
         assert b["row_tiles"][0, 0, r] == case["backward_kept"][r]
+        # decisive values (golden "tie_rules"): forward T in {L / n : n = 1 ..
+        # min(n_f, L - 1)}, backward T = L / n_f on every tile of the row
+        Ts = [L / m for m in range(1, min(n, L - 1) + 1)]
+        fa = min((abs(t - tau) for t in Ts), default=math.inf)
+        fr = min((abs(t / tau - 1) for t in Ts), default=math.inf)
+        _assert_ties([f["tie_abs"][0, 0, r]], [f["tie_rel"][0, 0, r]], [fa], [fr], "fwd row %d" % r)
+        _assert_ties([b["tie_abs"][0, 0, r]], [b["tie_rel"][0, 0, r]], [abs(L / n - tau)],
+                     [abs(L / n / tau - 1)], "bwd row %d" % r)
+    if tau == 1.0:
+        # every backward T equals tau: each row lies in the tie band
+        assert (b["tie_abs"] <= 1e-12).all()
 
 
 # --------------------------------------------------------------------------
@@ -410,14 +510,21 @@ def test_decode_split_rule_and_merge(splits, tau):
     T = -(-Nk // bk)
     tps = -(-T // splits)
     keep = np.zeros(T, dtype=np.int8)
+    Tvals = []                                        # decisive values of non-empty tests
     for sp in range(splits):                          # direct sums, per split
         Z = 0.0
         for t in range(min(T, (sp + 1) * tps) - 1, sp * tps - 1, -1):
             blk = s[t * bk: (t + 1) * bk]
+            if Z > 0.0:
+                Tvals.append(Nk * math.exp(blk.max()) / Z)
             if Z == 0.0 or math.exp(blk.max()) / Z >= tau / Nk:
                 keep[t] = 1
                 Z += np.exp(blk).sum()
     np.testing.assert_array_equal(d["keep"][0, 0], keep)
+    if tau > 0:
+        _assert_ties(d["tie_abs"][0], d["tie_rel"][0],
+                     [min((abs(t - tau) for t in Tvals), default=math.inf)],
+                     [min((abs(t / tau - 1) for t in Tvals), default=math.inf)], "decode")
     Rk = np.repeat(keep.astype(bool), bk)[:Nk]
     p = np.exp(s[Rk] - s[Rk].max())
     np.testing.assert_allclose(d["o"][0, 0], (p / p.sum()) @ v[0, 0][Rk], rtol=0, atol=1e-12)
