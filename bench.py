@@ -61,8 +61,8 @@ class Train:
         i32 = dict(dtype=torch.int32, device="cuda")
         self.rt_f = torch.empty((w.B, w.Hq, w.N), **i32)
         self.rt_b = torch.empty((w.B, w.Hq, w.N), **i32)
-        self.cnt_f = torch.empty(4, dtype=torch.int64, device="cuda")
-        self.cnt_b = torch.empty(4, dtype=torch.int64, device="cuda")
+        self.cnt_f = torch.empty(mala.NUM_COUNTERS, dtype=torch.int64, device="cuda")
+        self.cnt_b = torch.empty(mala.NUM_COUNTERS, dtype=torch.int64, device="cuda")
         n = mala.mala_bwd_workspace_size(w.B, w.Hq, w.Hkv, w.N, w.N, w.D)
         self.ws = torch.empty(n, dtype=torch.uint8, device="cuda")
         self.scale = float(np.float32(w.scale))
@@ -100,7 +100,7 @@ class Decode:
         self.o = torch.empty((w.B, w.Hq, w.D), dtype=torch.float32, device="cuda")
         self.lse = torch.empty((w.B, w.Hq), dtype=torch.float32, device="cuda")
         self.ht = torch.empty((w.B, w.Hq), dtype=torch.int32, device="cuda")
-        self.cnt = torch.empty(4, dtype=torch.int64, device="cuda")
+        self.cnt = torch.empty(mala.NUM_COUNTERS, dtype=torch.int64, device="cuda")
         n = mala.mala_decode_workspace_size(w.B, w.Hq, w.D, self.splits)
         self.ws = torch.empty(n, dtype=torch.uint8, device="cuda")
         self.scale = float(np.float32(w.scale))
@@ -145,6 +145,94 @@ def train_flops(cnt_f, cnt_b, D, bq, bk):
     fwd = (cnt_f[0] + cnt_f[1]) * slots * 2 * D
     bwd = (cnt_b[0] * 2 + cnt_b[1] * 8) * slots * D
     return float(fwd), float(bwd)
+
+
+def cpu_model():
+    """The host CPU's model name (first processor in /proc/cpuinfo), or None."""
+    try:
+        with open("/proc/cpuinfo") as fh:
+            for ln in fh:
+                if ln.lower().startswith("model name"):
+                    return ln.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return None
+
+
+def operator_memory(tr, tau):
+    """Device memory (MiB) that one call of each allocating wrapper takes beyond the
+    inputs already resident: torch.cuda.max_memory_allocated around the call minus
+    the memory allocated before it.  That is the call's outputs and workspace; the
+    library itself allocates nothing."""
+    import torch
+    mala = tr.mala
+    mib = lambda x: round(x / 2 ** 20, 2)
+
+    def peak(fn):
+        torch.cuda.synchronize()
+        base = torch.cuda.memory_allocated()
+        torch.cuda.reset_peak_memory_stats()
+        out = fn()
+        torch.cuda.synchronize()
+        return out, torch.cuda.max_memory_allocated() - base
+
+    res = {}
+    for name, dt in (("fp32_outputs", torch.float32), ("bf16_outputs", torch.bfloat16)):
+        f, mf = peak(lambda: mala.fwd(tr.q, tr.k, tr.v, tr.scale, tau, out_dtype=dt))
+        b, mb = peak(lambda: mala.bwd(tr.q, tr.k, tr.v, f["o"], f["lse"], tr.do, tr.scale, tau,
+                                      grad_dtype=dt))
+        res[name] = {"fwd_mib": mib(mf), "bwd_mib": mib(mb)}
+        del f, b
+    torch.cuda.empty_cache()
+    return res
+
+
+def train_config(cfg_id, taus, reps, warmup):
+    """One training workload: fwd / bwd latency (HIP events, mean and median of reps
+    calls after warmup) at tau = 0 (dense through the same kernels) and at each tau,
+    the speed-ups over dense, the retained work and the V / dO loads the retained
+    tiles needed, executed and dense-equivalent TFLOP/s, and the operators' device
+    memory."""
+    import torch
+    from workloads import CONFIGS
+    tr = Train(cfg_id, 0.0)
+    w = tr.w
+    mala = tr.mala
+    bq, bk = mala.mala_geometry(w.D, mala.PASS_FWD)
+    de_f, de_b = dense_equivalent_flops(w.B, w.Hq, w.N, w.D)
+    rows = w.B * w.Hq * w.N
+    pct = lambda a, b_: round(100.0 * float(a) / max(1.0, float(b_)), 3)
+    res = {}
+    for t_ in (0.0,) + tuple(x for x in taus if x != 0.0):
+        f = time_calls(lambda: tr.fwd(t_), reps, warmup)
+        b = time_calls(lambda: tr.bwd(t_), reps, warmup)
+        res[t_] = (f, b) + tuple(tr.counters())
+    out = {"workload": CONFIGS[cfg_id]["desc"], "shape": [w.B, w.Hq, w.Hkv, w.N, w.D]}
+    f0, b0 = res[0.0][0][0], res[0.0][1][0]
+    for t_, (f, b, cf, cb) in res.items():
+        fl_f, fl_b = train_flops(cf, cb, w.D, bq, bk)
+        out["tau=%g" % t_] = {
+            "fwd_ms": round(f[0], 4), "fwd_ms_median": round(f[1], 4),
+            "bwd_ms": round(b[0], 4), "bwd_ms_median": round(b[1], 4),
+            "speedup_fwd": round(f0 / f[0], 4), "speedup_bwd": round(b0 / b[0], 4),
+            "retained_tiles_pct_fwd": pct(cf[1], cf[0]),
+            "retained_tiles_pct_bwd": pct(cb[1], cb[0]),
+            "v_tiles_needed_pct_fwd": pct(cf[5], cf[2]),
+            "do_tiles_needed_pct_bwd": pct(cb[5], cb[2]),
+            "mean_slots_per_query_fwd": round(float(cf[3]) / rows, 1),
+            "mean_slots_per_query_bwd": round(float(cb[3]) / rows, 1),
+            "executed_tflops_fwd": round(fl_f / (f[0] * 1e-3) / 1e12, 1),
+            "executed_tflops_bwd": round(fl_b / (b[0] * 1e-3) / 1e12, 1),
+            "dense_equiv_tflops_fwd": round(de_f / (f[0] * 1e-3) / 1e12, 1),
+            "dense_equiv_tflops_bwd": round(de_b / (b[0] * 1e-3) / 1e12, 1),
+        }
+    out["operator_memory"] = operator_memory(tr, taus[0])
+    log("cfg%d dense fwd %.3f bwd %.3f ms | %s" % (
+        cfg_id, f0, b0, " ".join("tau=%g fwd %.3f bwd %.3f" % (t_, r[0][0], r[1][0])
+                                 for t_, r in res.items() if t_)))
+    del tr, res
+    torch.cuda.empty_cache()
+    return out
 
 
 def dense_equivalent_flops(B, Hq, N, D):

@@ -67,19 +67,40 @@ typedef enum {
   MALA_ERR_HIP = -4          /* a HIP launch/runtime call failed; see mala_last_error() */
 } mala_status;
 
-/* Indices into the int64 counters[4] array that every entry point can fill. */
+/* Indices into the int64 counters[MALA_NUM_COUNTERS] array that every entry point
+ * can fill (a NULL counters pointer skips them; otherwise all eight are cleared on
+ * the stream and then written).  "Tile" means a decision tile (B_q x B_k, or 1 x B_k
+ * per query head in decode). */
 enum {
   MALA_CNT_LEGAL = 0,    /* decision tiles holding at least one legal (causal) entry,
                             per query head */
-  MALA_CNT_RETAINED = 1, /* of those, tiles whose post-score path ran */
-  MALA_CNT_V_TILES = 2,  /* forward: V tiles of B_k keys staged by the kernel;
-                            backward: dO tiles of B_q rows staged;
-                            decode: V tiles of B_k keys read (once per up to 16
-                            query heads of a GQA group) */
-  MALA_CNT_SLOTS = 3     /* post-score key slots summed over query rows: a retained
+  MALA_CNT_RETAINED = 1, /* of those, tiles whose post-score path ran (backward: as
+                            counted by the query-major dQ pass) */
+  MALA_CNT_V_TILES = 2,  /* forward: V tiles of B_k keys staged (a workgroup of 256
+                            query rows stages every key tile it visits);
+                            backward: dO tiles of B_q rows staged by the key-major pass;
+                            decode: V tiles of B_k keys fetched (once per up to 16 query
+                            heads of a GQA group, look-ahead fetches included) */
+  MALA_CNT_SLOTS = 3,    /* post-score key slots summed over query rows: a retained
                             B_q x B_k tile adds B_k slots to each of its valid rows
                             (Attention Cost section; mean slots per query =
                             counters[3] / number of query rows) */
+  MALA_CNT_RETAINED_KV = 4, /* backward only: retained tiles as counted by the key-major
+                               dK/dV pass (0 in forward and decode) */
+  MALA_CNT_V_NEEDED = 5, /* the loads of MALA_CNT_V_TILES that a retained tile used:
+                            forward: (workgroup, key tile) pairs with a retained tile;
+                            backward: (key-major workgroup, query tile) pairs with a
+                            retained tile; decode: fetched V tiles that some head of
+                            the group retained */
+  MALA_CNT_SET_HASH = 6, /* fingerprint of the retained set: the sum modulo 2^64 of
+                            splitmix64(b << 52 | h << 40 | i << 20 | j) over the
+                            retained tiles (sequence b, query head h, query tile i,
+                            key tile j of the sequence's own tiling; decode: i = 0, j =
+                            the key tile); backward: of the query-major dQ pass */
+  MALA_CNT_SET_HASH_KV = 7, /* backward only: the same fingerprint from the key-major
+                               dK/dV pass (equal to MALA_CNT_SET_HASH exactly when the
+                               two passes retain the same tiles, up to a 2^-64 chance) */
+  MALA_NUM_COUNTERS = 8
 };
 
 enum { MALA_PASS_FWD = 0, MALA_PASS_BWD = 1, MALA_PASS_DECODE = 2 };
@@ -114,7 +135,7 @@ const char* mala_last_error(void);
  *   lse: fp32 [B, Hq, Nq]    out    natural-log normalizer z_q = m_q + log l_q
  *   row_tiles: int32 [B, Hq, Nq] or NULL   out: retained tiles in which the row has a
  *              legal key
- *   counters:  int64 [4] or NULL          out: see MALA_CNT_*
+ *   counters:  int64 [MALA_NUM_COUNTERS] or NULL   out: see MALA_CNT_*
  *   causal must be 1.  Requires Nq <= Nk, D in {64, 128} and Nk * D * 2 < 2^32
  *   (Nk below 16M tokens at D = 128); otherwise MALA_ERR_UNSUPPORTED.
  */
@@ -137,7 +158,8 @@ size_t mala_bwd_workspace_size(int B, int Hq, int Hkv, int Nq, int Nk, int D);
  *       atomics: all three are bitwise reproducible.  dQ comes from a query-major pass that recomputes the
  *       tile scores with the same arithmetic, so it uses exactly the tiles the
  *       key-major dK/dV pass retains;
- *   row_tiles: int32 [B, Hq, Nq] or NULL out; counters: int64 [4] or NULL out.
+ *   row_tiles: int32 [B, Hq, Nq] or NULL out; counters: int64 [MALA_NUM_COUNTERS]
+ *   or NULL out.
  *   workspace: device memory of at least mala_bwd_workspace_size(...) bytes,
  *   16-byte aligned, owned by the caller, not read by the caller afterwards.
  *   The shape limits of mala_fwd apply.
@@ -206,7 +228,7 @@ size_t mala_decode_workspace_size(int B, int Hq, int D, int num_splits);
  *       n_b = 0 gets o = 0 and lse = -inf.  NULL means n_b = Nk for every sequence.
  *   o: [B, Hq, D] out (fp32 or bf16 by out_dtype); lse: fp32 [B, Hq] out
  *   head_tiles: int32 [B, Hq] or NULL out (retained tiles summed over splits)
- *   counters: int64 [4] or NULL out
+ *   counters: int64 [MALA_NUM_COUNTERS] or NULL out
  *   num_splits >= 1: a sequence's key tiles (T = ceil(n_b / B_k) of them) are cut
  *   into num_splits contiguous ranges of ceil(T / num_splits) tiles; each range
  *   starts from an empty normalizer, so the retained set depends on num_splits.

@@ -25,6 +25,8 @@ MALA_ERR_WORKSPACE, MALA_ERR_HIP = -3, -4
 PASS_FWD, PASS_BWD, PASS_DECODE = 0, 1, 2
 OUT_F32, OUT_BF16 = 0, 1
 CNT_LEGAL, CNT_RETAINED, CNT_V_TILES, CNT_SLOTS = 0, 1, 2, 3
+CNT_RETAINED_KV, CNT_V_NEEDED, CNT_SET_HASH, CNT_SET_HASH_KV = 4, 5, 6, 7
+NUM_COUNTERS = 8
 
 EXPORTS = ("mala_geometry", "mala_strerror", "mala_last_error", "mala_fwd",
            "mala_bwd_workspace_size", "mala_bwd", "mala_fwd_varlen", "mala_bwd_varlen",
@@ -94,16 +96,54 @@ def _check(status):
         raise MalaError(status, detail)
 
 
-def _dev(t, dtype, name, dims):
-    if not isinstance(t, torch.Tensor) or not t.is_cuda:
-        raise TypeError("%s must be a CUDA (HIP) tensor" % name)
+_OUT = (torch.float32, torch.bfloat16)
+
+
+def _spec(t, name, dtype, shape, optional=False):
+    """Check a tensor argument's type, dtype, exact shape and contiguity (raises
+    TypeError / ValueError); the device is checked by _on_device afterwards."""
+    if t is None:
+        if optional:
+            return None
+        raise TypeError("%s is required" % name)
+    if not isinstance(t, torch.Tensor):
+        raise TypeError("%s must be a torch tensor" % name)
     ok = t.dtype in dtype if isinstance(dtype, tuple) else t.dtype == dtype
-    if not ok or not t.is_contiguous() or t.dim() != dims:
-        raise TypeError("%s must be a contiguous %d-d %s tensor" % (name, dims, dtype))
+    if not ok:
+        raise TypeError("%s must have dtype %s, got %s" % (name, dtype, t.dtype))
+    if tuple(t.shape) != tuple(shape):
+        raise ValueError("%s must have shape %s, got %s" % (name, tuple(shape), tuple(t.shape)))
+    if not t.is_contiguous():
+        raise ValueError("%s must be contiguous" % name)
     return t
 
 
-_OUT = (torch.float32, torch.bfloat16)
+def _dims(t, name, ndim):
+    if not isinstance(t, torch.Tensor):
+        raise TypeError("%s must be a torch tensor" % name)
+    if t.dim() != ndim:
+        raise ValueError("%s must be %d-d, got shape %s" % (name, ndim, tuple(t.shape)))
+    return tuple(t.shape)
+
+
+def _on_device(named):
+    """Every given tensor (None skipped) is a CUDA (HIP) tensor on one device."""
+    dev = None
+    for name, t in named:
+        if t is None:
+            continue
+        if not t.is_cuda:
+            raise TypeError("%s must be a CUDA (HIP) tensor" % name)
+        if dev is None:
+            dev = t.device
+        elif t.device != dev:
+            raise TypeError("%s is on %s, the other tensors on %s" % (name, t.device, dev))
+
+
+def _workspace(ws):
+    if not isinstance(ws, torch.Tensor) or not ws.is_contiguous():
+        raise TypeError("workspace must be a contiguous tensor")
+    return ws
 
 
 def _out_code(*ts):
@@ -127,37 +167,50 @@ def mala_decode_workspace_size(B, Hq, D, num_splits):
     return int(load_library().mala_decode_workspace_size(B, Hq, D, num_splits))
 
 
+def _stats_specs(row_tiles, counters, rows_shape):
+    _spec(row_tiles, "row_tiles", torch.int32, rows_shape, optional=True)
+    _spec(counters, "counters", torch.int64, (NUM_COUNTERS,), optional=True)
+
+
+def _fwd_specs(q, k, v, o, lse, row_tiles, counters):
+    B, Hq, Nq, D = _dims(q, "q", 4)
+    _spec(q, "q", torch.bfloat16, (B, Hq, Nq, D))
+    _, Hkv, Nk, _ = _dims(k, "k", 4)
+    _spec(k, "k", torch.bfloat16, (B, Hkv, Nk, D))
+    _spec(v, "v", torch.bfloat16, (B, Hkv, Nk, D))
+    _spec(o, "o", _OUT, (B, Hq, Nq, D))
+    _spec(lse, "lse", torch.float32, (B, Hq, Nq))
+    _stats_specs(row_tiles, counters, (B, Hq, Nq))
+    return B, Hq, Hkv, Nq, Nk, D
+
+
 def mala_fwd(q, k, v, o, lse, row_tiles, counters, scale, tau, causal=1, stream=None):
-    for t, n in ((q, "q"), (k, "k"), (v, "v")):
-        _dev(t, torch.bfloat16, n, 4)
-    _dev(o, _OUT, "o", 4), _dev(lse, torch.float32, "lse", 3)
-    B, Hq, Nq, D = q.shape
-    Hkv, Nk = k.shape[1], k.shape[2]
-    if (tuple(v.shape) != tuple(k.shape) or tuple(o.shape) != tuple(q.shape)
-            or tuple(lse.shape) != (B, Hq, Nq)):
-        raise ValueError("inconsistent shapes")
-    if row_tiles is not None:
-        _dev(row_tiles, torch.int32, "row_tiles", 3)
-    if counters is not None:
-        _dev(counters, torch.int64, "counters", 1)
+    B, Hq, Hkv, Nq, Nk, D = _fwd_specs(q, k, v, o, lse, row_tiles, counters)
+    _on_device((("q", q), ("k", k), ("v", v), ("o", o), ("lse", lse), ("row_tiles", row_tiles),
+                ("counters", counters)))
     _check(load_library().mala_fwd(_ptr(q), _ptr(k), _ptr(v), _ptr(o), _ptr(lse), _ptr(row_tiles),
                                    _ptr(counters), B, Hq, Hkv, Nq, Nk, D, causal, scale, tau,
                                    _out_code(o), _stream(stream)))
 
 
+def _bwd_specs(q, k, v, o, lse, dout, dq, dk, dv, row_tiles, counters, workspace):
+    B, Hq, Hkv, Nq, Nk, D = _fwd_specs(q, k, v, o, lse, row_tiles, counters)
+    _spec(dout, "dout", torch.bfloat16, (B, Hq, Nq, D))
+    _spec(dq, "dq", _OUT, (B, Hq, Nq, D))
+    _spec(dk, "dk", _OUT, (B, Hkv, Nk, D))
+    _spec(dv, "dv", _OUT, (B, Hkv, Nk, D))
+    _out_code(dq, dk, dv)
+    _workspace(workspace)
+    return B, Hq, Hkv, Nq, Nk, D
+
+
 def mala_bwd(q, k, v, o, lse, dout, dq, dk, dv, row_tiles, counters, workspace, scale, tau,
              causal=1, stream=None):
-    for t, n, dt, nd in ((q, "q", torch.bfloat16, 4), (k, "k", torch.bfloat16, 4),
-                         (v, "v", torch.bfloat16, 4), (o, "o", _OUT, 4),
-                         (lse, "lse", torch.float32, 3), (dout, "dout", torch.bfloat16, 4),
-                         (dq, "dq", _OUT, 4), (dk, "dk", _OUT, 4), (dv, "dv", _OUT, 4)):
-        _dev(t, dt, n, nd)
-    B, Hq, Nq, D = q.shape
-    Hkv, Nk = k.shape[1], k.shape[2]
-    if (tuple(dq.shape) != tuple(q.shape) or tuple(dout.shape) != tuple(q.shape)
-            or tuple(o.shape) != tuple(q.shape) or tuple(dk.shape) != tuple(k.shape)
-            or tuple(dv.shape) != tuple(k.shape)):
-        raise ValueError("inconsistent shapes")
+    B, Hq, Hkv, Nq, Nk, D = _bwd_specs(q, k, v, o, lse, dout, dq, dk, dv, row_tiles, counters,
+                                       workspace)
+    _on_device((("q", q), ("k", k), ("v", v), ("o", o), ("lse", lse), ("dout", dout),
+                ("dq", dq), ("dk", dk), ("dv", dv), ("row_tiles", row_tiles),
+                ("counters", counters), ("workspace", workspace)))
     _check(load_library().mala_bwd(_ptr(q), _ptr(k), _ptr(v), _ptr(o), _ptr(lse), _ptr(dout),
                                    _ptr(dq), _ptr(dk), _ptr(dv), _ptr(row_tiles), _ptr(counters),
                                    _ptr(workspace), workspace.numel() * workspace.element_size(),
@@ -165,17 +218,31 @@ def mala_bwd(q, k, v, o, lse, dout, dq, dk, dv, row_tiles, counters, workspace, 
                                    _out_code(dq, dk, dv), _stream(stream)))
 
 
+def _decode_specs(q, k_cache, v_cache, o, lse, head_tiles, counters, workspace, cache_lens):
+    B, Hq, D = _dims(q, "q", 3)
+    _spec(q, "q", torch.bfloat16, (B, Hq, D))
+    _, Hkv, Nk, _ = _dims(k_cache, "k_cache", 4)
+    _spec(k_cache, "k_cache", torch.bfloat16, (B, Hkv, Nk, D))
+    _spec(v_cache, "v_cache", torch.bfloat16, (B, Hkv, Nk, D))
+    _spec(o, "o", _OUT, (B, Hq, D))
+    _spec(lse, "lse", torch.float32, (B, Hq))
+    _spec(head_tiles, "head_tiles", torch.int32, (B, Hq), optional=True)
+    _spec(counters, "counters", torch.int64, (NUM_COUNTERS,), optional=True)
+    _spec(cache_lens, "cache_lens", torch.int32, (B,), optional=True)
+    if workspace is not None:
+        _workspace(workspace)
+    return B, Hq, Hkv, Nk, D
+
+
 def mala_decode(q, k_cache, v_cache, o, lse, head_tiles, counters, num_splits, workspace, scale,
                 tau, stream=None, cache_lens=None):
-    _dev(q, torch.bfloat16, "q", 3), _dev(k_cache, torch.bfloat16, "k_cache", 4)
-    _dev(v_cache, torch.bfloat16, "v_cache", 4), _dev(o, _OUT, "o", 3)
-    _dev(lse, torch.float32, "lse", 2)
-    B, Hq, D = q.shape
-    Hkv, Nk = k_cache.shape[1], k_cache.shape[2]
-    if cache_lens is not None:
-        _dev(cache_lens, torch.int32, "cache_lens", 1)
-        if cache_lens.shape[0] != B:
-            raise ValueError("cache_lens must have one entry per sequence (%d)" % B)
+    B, Hq, Hkv, Nk, D = _decode_specs(q, k_cache, v_cache, o, lse, head_tiles, counters,
+                                      workspace, cache_lens)
+    if workspace is None:
+        raise TypeError("workspace is required")
+    _on_device((("q", q), ("k_cache", k_cache), ("v_cache", v_cache), ("o", o), ("lse", lse),
+                ("head_tiles", head_tiles), ("counters", counters), ("workspace", workspace),
+                ("cache_lens", cache_lens)))
     _check(load_library().mala_decode(_ptr(q), _ptr(k_cache), _ptr(v_cache), _ptr(cache_lens),
                                       _ptr(o), _ptr(lse), _ptr(head_tiles), _ptr(counters),
                                       num_splits, _ptr(workspace),
@@ -183,39 +250,39 @@ def mala_decode(q, k_cache, v_cache, o, lse, head_tiles, counters, num_splits, w
                                       Nk, D, scale, tau, _out_code(o), _stream(stream)))
 
 
-def _varlen_dims(q, k, cu_seqlens, max_seqlen, cu_seqlens_k, max_seqlen_k):
-    """Sizes of a packed batch: q [Hq, total_q, D], k [Hkv, total_k, D], the int32
-    [num_seqs + 1] device arrays of query and (optionally) key starts, and the
-    longest runs.  Returns (num_seqs, Hq, Hkv, total_q, total_k, D, max_q, max_k)."""
-    _dev(cu_seqlens, torch.int32, "cu_seqlens", 1)
-    Hq, total_q, D = q.shape
-    Hkv, total_k = k.shape[0], k.shape[1]
-    if cu_seqlens.shape[0] < 2 or k.shape[2] != D:
-        raise ValueError("inconsistent shapes")
+def _varlen_specs(q, k, v, cu_seqlens, max_seqlen, cu_seqlens_k, max_seqlen_k, o, lse,
+                  row_tiles, counters):
+    """Sizes of a packed batch: q [Hq, total_q, D], k, v [Hkv, total_k, D], the int32
+    [num_seqs + 1] arrays of query and (optionally) key starts, and the longest runs.
+    Returns (num_seqs, Hq, Hkv, total_q, total_k, D, max_q, max_k)."""
+    Hq, tq, D = _dims(q, "q", 3)
+    _spec(q, "q", torch.bfloat16, (Hq, tq, D))
+    Hkv, tk, _ = _dims(k, "k", 3)
+    _spec(k, "k", torch.bfloat16, (Hkv, tk, D))
+    _spec(v, "v", torch.bfloat16, (Hkv, tk, D))
+    (n1,) = _dims(cu_seqlens, "cu_seqlens", 1)
+    _spec(cu_seqlens, "cu_seqlens", torch.int32, (n1,))
+    if n1 < 2:
+        raise ValueError("cu_seqlens needs at least one sequence (two entries)")
     if cu_seqlens_k is None:
         max_seqlen_k = max_seqlen
     else:
-        _dev(cu_seqlens_k, torch.int32, "cu_seqlens_k", 1)
-        if cu_seqlens_k.shape[0] != cu_seqlens.shape[0] or max_seqlen_k is None:
-            raise ValueError("cu_seqlens_k needs one start per sequence and max_seqlen_k")
-    return (cu_seqlens.shape[0] - 1, Hq, Hkv, total_q, total_k, D, int(max_seqlen),
-            int(max_seqlen_k))
+        _spec(cu_seqlens_k, "cu_seqlens_k", torch.int32, (n1,))
+        if max_seqlen_k is None:
+            raise ValueError("cu_seqlens_k needs max_seqlen_k")
+    _spec(o, "o", _OUT, (Hq, tq, D))
+    _spec(lse, "lse", torch.float32, (Hq, tq))
+    _stats_specs(row_tiles, counters, (Hq, tq))
+    return n1 - 1, Hq, Hkv, tq, tk, D, int(max_seqlen), int(max_seqlen_k)
 
 
 def mala_fwd_varlen(q, k, v, cu_seqlens, max_seqlen, o, lse, row_tiles, counters, scale, tau,
                     stream=None, cu_seqlens_k=None, max_seqlen_k=None):
-    for t, n in ((q, "q"), (k, "k"), (v, "v")):
-        _dev(t, torch.bfloat16, n, 3)
-    _dev(o, _OUT, "o", 3), _dev(lse, torch.float32, "lse", 2)
-    S, Hq, Hkv, tq, tk, D, mq, mk = _varlen_dims(q, k, cu_seqlens, max_seqlen, cu_seqlens_k,
-                                                 max_seqlen_k)
-    if tuple(v.shape) != tuple(k.shape) or tuple(o.shape) != tuple(q.shape) or \
-            tuple(lse.shape) != (Hq, tq):
-        raise ValueError("inconsistent shapes")
-    if row_tiles is not None:
-        _dev(row_tiles, torch.int32, "row_tiles", 2)
-    if counters is not None:
-        _dev(counters, torch.int64, "counters", 1)
+    S, Hq, Hkv, tq, tk, D, mq, mk = _varlen_specs(q, k, v, cu_seqlens, max_seqlen, cu_seqlens_k,
+                                                  max_seqlen_k, o, lse, row_tiles, counters)
+    _on_device((("q", q), ("k", k), ("v", v), ("cu_seqlens", cu_seqlens),
+                ("cu_seqlens_k", cu_seqlens_k), ("o", o), ("lse", lse),
+                ("row_tiles", row_tiles), ("counters", counters)))
     _check(load_library().mala_fwd_varlen(_ptr(q), _ptr(k), _ptr(v), _ptr(cu_seqlens),
                                           _ptr(cu_seqlens_k), _ptr(o), _ptr(lse),
                                           _ptr(row_tiles), _ptr(counters), S, mq, mk, tq, tk,
@@ -225,17 +292,18 @@ def mala_fwd_varlen(q, k, v, cu_seqlens, max_seqlen, o, lse, row_tiles, counters
 def mala_bwd_varlen(q, k, v, cu_seqlens, max_seqlen, o, lse, dout, dq, dk, dv, row_tiles,
                     counters, workspace, scale, tau, stream=None, cu_seqlens_k=None,
                     max_seqlen_k=None):
-    for t, n, dt, nd in ((q, "q", torch.bfloat16, 3), (k, "k", torch.bfloat16, 3),
-                         (v, "v", torch.bfloat16, 3), (o, "o", _OUT, 3),
-                         (lse, "lse", torch.float32, 2), (dout, "dout", torch.bfloat16, 3),
-                         (dq, "dq", _OUT, 3), (dk, "dk", _OUT, 3), (dv, "dv", _OUT, 3)):
-        _dev(t, dt, n, nd)
-    S, Hq, Hkv, tq, tk, D, mq, mk = _varlen_dims(q, k, cu_seqlens, max_seqlen, cu_seqlens_k,
-                                                 max_seqlen_k)
-    if (tuple(dq.shape) != tuple(q.shape) or tuple(dout.shape) != tuple(q.shape)
-            or tuple(o.shape) != tuple(q.shape) or tuple(dk.shape) != tuple(k.shape)
-            or tuple(dv.shape) != tuple(k.shape)):
-        raise ValueError("inconsistent shapes")
+    S, Hq, Hkv, tq, tk, D, mq, mk = _varlen_specs(q, k, v, cu_seqlens, max_seqlen, cu_seqlens_k,
+                                                  max_seqlen_k, o, lse, row_tiles, counters)
+    _spec(dout, "dout", torch.bfloat16, (Hq, tq, D))
+    _spec(dq, "dq", _OUT, (Hq, tq, D))
+    _spec(dk, "dk", _OUT, (Hkv, tk, D))
+    _spec(dv, "dv", _OUT, (Hkv, tk, D))
+    _out_code(dq, dk, dv)
+    _workspace(workspace)
+    _on_device((("q", q), ("k", k), ("v", v), ("cu_seqlens", cu_seqlens),
+                ("cu_seqlens_k", cu_seqlens_k), ("o", o), ("lse", lse), ("dout", dout),
+                ("dq", dq), ("dk", dk), ("dv", dv), ("row_tiles", row_tiles),
+                ("counters", counters), ("workspace", workspace)))
     _check(load_library().mala_bwd_varlen(_ptr(q), _ptr(k), _ptr(v), _ptr(cu_seqlens),
                                           _ptr(cu_seqlens_k), _ptr(o), _ptr(lse), _ptr(dout),
                                           _ptr(dq), _ptr(dk), _ptr(dv), _ptr(row_tiles),
@@ -252,7 +320,7 @@ def fwd(q, k, v, scale, tau, stats=True, stream=None, out_dtype=torch.float32):
     o = torch.empty((B, Hq, Nq, D), dtype=out_dtype, device=q.device)
     lse = torch.empty((B, Hq, Nq), dtype=torch.float32, device=q.device)
     rt = torch.empty((B, Hq, Nq), dtype=torch.int32, device=q.device) if stats else None
-    cnt = torch.empty(4, dtype=torch.int64, device=q.device) if stats else None
+    cnt = torch.empty(NUM_COUNTERS, dtype=torch.int64, device=q.device) if stats else None
     mala_fwd(q, k, v, o, lse, rt, cnt, scale, tau, stream=stream)
     return dict(o=o, lse=lse, row_tiles=rt, counters=cnt)
 
@@ -266,7 +334,7 @@ def bwd(q, k, v, o, lse, dout, scale, tau, stats=True, workspace=None, stream=No
     dk = torch.empty((B, Hkv, Nk, D), dtype=grad_dtype, device=q.device)
     dv = torch.empty((B, Hkv, Nk, D), dtype=grad_dtype, device=q.device)
     rt = torch.empty((B, Hq, Nq), dtype=torch.int32, device=q.device) if stats else None
-    cnt = torch.empty(4, dtype=torch.int64, device=q.device) if stats else None
+    cnt = torch.empty(NUM_COUNTERS, dtype=torch.int64, device=q.device) if stats else None
     if workspace is None:
         n = mala_bwd_workspace_size(B, Hq, Hkv, Nq, Nk, D)
         workspace = torch.empty(max(n, 16), dtype=torch.uint8, device=q.device)
@@ -282,7 +350,7 @@ def decode(q, k_cache, v_cache, scale, tau, num_splits, stats=True, workspace=No
     o = torch.empty((B, Hq, D), dtype=out_dtype, device=q.device)
     lse = torch.empty((B, Hq), dtype=torch.float32, device=q.device)
     ht = torch.empty((B, Hq), dtype=torch.int32, device=q.device) if stats else None
-    cnt = torch.empty(4, dtype=torch.int64, device=q.device) if stats else None
+    cnt = torch.empty(NUM_COUNTERS, dtype=torch.int64, device=q.device) if stats else None
     if workspace is None:
         n = mala_decode_workspace_size(B, Hq, D, num_splits)
         workspace = torch.empty(max(n, 16), dtype=torch.uint8, device=q.device)
@@ -300,7 +368,7 @@ def fwd_varlen(q, k, v, cu_seqlens, max_seqlen, scale, tau, stats=True, stream=N
     o = torch.zeros((Hq, total, D), dtype=out_dtype, device=q.device)
     lse = torch.zeros((Hq, total), dtype=torch.float32, device=q.device)
     rt = torch.zeros((Hq, total), dtype=torch.int32, device=q.device) if stats else None
-    cnt = torch.empty(4, dtype=torch.int64, device=q.device) if stats else None
+    cnt = torch.empty(NUM_COUNTERS, dtype=torch.int64, device=q.device) if stats else None
     mala_fwd_varlen(q, k, v, cu_seqlens, max_seqlen, o, lse, rt, cnt, scale, tau, stream=stream,
                     cu_seqlens_k=cu_seqlens_k, max_seqlen_k=max_seqlen_k)
     return dict(o=o, lse=lse, row_tiles=rt, counters=cnt)
@@ -315,7 +383,7 @@ def bwd_varlen(q, k, v, cu_seqlens, max_seqlen, o, lse, dout, scale, tau, stats=
     dk = torch.zeros((Hkv, total_k, D), dtype=grad_dtype, device=q.device)
     dv = torch.zeros((Hkv, total_k, D), dtype=grad_dtype, device=q.device)
     rt = torch.zeros((Hq, total), dtype=torch.int32, device=q.device) if stats else None
-    cnt = torch.empty(4, dtype=torch.int64, device=q.device) if stats else None
+    cnt = torch.empty(NUM_COUNTERS, dtype=torch.int64, device=q.device) if stats else None
     if workspace is None:
         n = mala_bwd_workspace_size(1, Hq, Hkv, total, total_k, D)
         workspace = torch.empty(max(n, 16), dtype=torch.uint8, device=q.device)

@@ -100,7 +100,7 @@ int run_fwd(const void* q, const void* k, const void* v, const Packed& pk,
             void* o, int o_dtype, float* lse, int32_t* row_tiles, int64_t* counters, int B,
             int Hq, int Hkv, int Nq, int Nk, int D, float scale, float tau, hipStream_t s) {
   if (counters) {
-    hipError_t e = mala::launch_fill_zero(counters, 4 * sizeof(int64_t), s);
+    hipError_t e = mala::launch_fill_zero(counters, mala::kNumCounters * sizeof(int64_t), s);
     if (e != hipSuccess) return hip_fail(e, "mala_fwd: clearing counters");
   }
   mala::FwdParams p;
@@ -133,7 +133,7 @@ int run_bwd(const void* q, const void* k, const void* v, const Packed& pk,
   hipError_t e;
   // D_q over every row of the q-shaped tensors (packed: all heads x total rows)
   const long rows = pk.cu ? (long)Hq * Nq : (long)B * Hq * Nq;
-  if (counters && (e = mala::launch_fill_zero(counters, 4 * sizeof(int64_t), s)) != hipSuccess)
+  if (counters && (e = mala::launch_fill_zero(counters, mala::kNumCounters * sizeof(int64_t), s)) != hipSuccess)
     return hip_fail(e, "mala_bwd: clearing counters");
   float* dvec = (float*)workspace;
   if ((e = mala::launch_bwd_preprocess(o, o_dtype == MALA_OUT_BF16, (const __bf16*)dout, dvec,
@@ -294,7 +294,7 @@ int mala_decode(const void* q, const void* k_cache, const void* v_cache,
   if (((uintptr_t)workspace) % 16) return fail(MALA_ERR_WORKSPACE, "workspace not 16-byte aligned");
   hipStream_t s = (hipStream_t)stream;
   hipError_t e;
-  if (counters && (e = mala::launch_fill_zero(counters, 4 * sizeof(int64_t), s)) != hipSuccess)
+  if (counters && (e = mala::launch_fill_zero(counters, mala::kNumCounters * sizeof(int64_t), s)) != hipSuccess)
     return hip_fail(e, "mala_decode: clearing counters");
   const int T = (Nk + mala::kDecBk - 1) / mala::kDecBk;
   mala::DecParams p;

@@ -317,6 +317,8 @@ __global__ __launch_bounds__(1024) void mala_bwd_dkdv_kernel(BwdParams p) {
     }
     if (role == 0) {
       float fdv = 0.f;   // P mass of this lane's key in tiles run without the lo term
+      unsigned n_ret_kv = 0;          // statistics: tiles this key group retains
+      unsigned long long hsum = 0;    // and their fingerprints
       for (int it = 0; it < n_it; ++it) {
         if (it < total) {
           // tile it: score discovery, offline test, P
@@ -353,8 +355,16 @@ __global__ __launch_bounds__(1024) void mala_bwd_dkdv_kernel(BwdParams p) {
             if (!with_lo) fdv = fv_new;
           }
           if (lane == 0) Pflag[it % 3][grp_k] = ret ? (with_lo ? 3 : 1) : 0;
+          if (ret && p.counters) {
+            ++n_ret_kv;
+            hsum += tile_hash(b, hkv * grp + it % grp, q0 / kBq, kw / kBk);
+          }
         }
         iteration_end(it);
+      }
+      if (p.counters && lane == 0 && n_ret_kv) {
+        atomicAdd(&p.counters[kCntRetainedKV], (unsigned long long)n_ret_kv);
+        atomicAdd(&p.counters[kCntSetHashKV], hsum);
       }
     } else {
       float fdk = 0.f;   // sum of |dS| of this lane's key in tiles run without the lo term
@@ -422,10 +432,13 @@ __global__ __launch_bounds__(1024) void mala_bwd_dkdv_kernel(BwdParams p) {
         }
     };
     if (role == 1) {
+      unsigned n_do = 0;   // statistics: query tiles whose dO some key group needed
       for (int it = 0; it < n_it; ++it) {
         if (it + 1 < total) fetch(it + 1);
         const int t = it - 1;
         const int pf = (t >= 0 && t < total) ? Pflag[t % 3][grp_k] : 0;
+        if (p.counters && grp_k == 0 && t >= 0 && t < total)
+          n_do += (Pflag[t % 3][0] | Pflag[t % 3][1] | Pflag[t % 3][2] | Pflag[t % 3][3]) ? 1 : 0;
         if (pf) {
           float pv[16];
 #pragma unroll
@@ -446,6 +459,8 @@ __global__ __launch_bounds__(1024) void mala_bwd_dkdv_kernel(BwdParams p) {
         if (it + 1 < total) stash(it + 1);
         __syncthreads();
       }
+      if (p.counters && grp_k == 0 && lane == 0)
+        atomicAdd(&p.counters[kCntVNeeded], (unsigned long long)n_do);
     } else {
       // the decision of tile it - 2 is known since the end of iteration it - 2: it
       // is read one iteration early, off the critical path
@@ -496,7 +511,7 @@ __global__ __launch_bounds__(1024) void mala_bwd_dkdv_kernel(BwdParams p) {
         }
     }
   }
-  if (p.counters && tid == 0) atomicAdd(&p.counters[2], (unsigned long long)total);
+  if (p.counters && tid == 0) atomicAdd(&p.counters[kCntVTiles], (unsigned long long)total);
 }
 
 // Offline test of one tile in the transposed C layout of the dQ pass: the lane
@@ -588,6 +603,7 @@ __global__ __launch_bounds__(kDqWaves * 64) void mala_bwd_dq_kernel(BwdParams p)
   const int qlast_g = min(qblk * kDqRows + kDqRows - 1, Nq - 1);
   const int ttop = (int)((qlast_g + off) / kFwdStage);
   unsigned n_legal = 0, n_ret = 0;
+  unsigned long long hsum = 0;   // fingerprints of the retained tiles
   int cnt_row = 0;   // retained tiles in which row qrow has a legal key
   float fdq = 0.f;   // this row's sum of |dS| in tiles run without the lo term
 
@@ -649,6 +665,7 @@ __global__ __launch_bounds__(kDqWaves * 64) void mala_bwd_dq_kernel(BwdParams p)
                                  : offline_test_t<false>(s, p.scale2, kmax, klim, thr, sv);
       if (!wave_any(dem)) continue;
       ++n_ret;
+      if (p.counters) hsum += tile_hash(b, hq, q0w / kBq, j);
       cnt_row += (row_valid && kb <= (long)qrow + off) ? 1 : 0;
       // P^T = exp2(s * scale2 - lse2), the key-major kernel's arithmetic
 #pragma unroll
@@ -716,9 +733,10 @@ __global__ __launch_bounds__(kDqWaves * 64) void mala_bwd_dq_kernel(BwdParams p)
     if (p.row_tiles && h == 0) p.row_tiles[qbase + qrow] = cnt_row;
   }
   if (p.counters && lane == 0 && n_legal) {
-    atomicAdd(&p.counters[0], (unsigned long long)n_legal);
-    atomicAdd(&p.counters[1], (unsigned long long)n_ret);
-    atomicAdd(&p.counters[3], (unsigned long long)n_ret * kBk * nvalid);
+    atomicAdd(&p.counters[kCntLegal], (unsigned long long)n_legal);
+    atomicAdd(&p.counters[kCntRetained], (unsigned long long)n_ret);
+    atomicAdd(&p.counters[kCntSlots], (unsigned long long)n_ret * kBk * nvalid);
+    if (hsum) atomicAdd(&p.counters[kCntSetHash], hsum);
   }
 }
 

@@ -66,7 +66,8 @@ __global__ __launch_bounds__(64) void mala_decode_split_kernel(DecParams p) {
 #pragma unroll
   for (int db = 0; db < NDB; ++db) acc[db] = f32x4{0.f, 0.f, 0.f, 0.f};
   int cnt = 0;
-  unsigned vloads = 0;
+  unsigned vloads = 0, vfetch = 0;   // V tiles consumed / fetched (statistics)
+  unsigned long long hsum = 0;       // fingerprints of this head's retained tiles
 
   // K of a tile as A operands: rows kb + col (block 0) and kb + 16 + col (block 1)
   bf16x8 ka[KS], kb1[KS];
@@ -125,6 +126,7 @@ __global__ __launch_bounds__(64) void mala_decode_split_kernel(DecParams p) {
     load_k(t_hi - 1);
     mt = scores(t_hi - 1, sv);
     load_v(t_hi - 1);     // the first tile of a split is always retained (l = 0)
+    ++vfetch;
     if (t_hi - 2 >= t_lo) load_k(t_hi - 2);
   }
   for (int t = t_hi - 1; t >= t_lo; --t) {
@@ -165,6 +167,7 @@ __global__ __launch_bounds__(64) void mala_decode_split_kernel(DecParams p) {
         l = alpha * l + ps;
         m = m_new;
         ++cnt;
+        if (p.counters) hsum += tile_hash(b, hq, 0, t);
       }
       bf16x8 ph, pl;
       split_bf16x8(sv, ph, pl);
@@ -176,32 +179,39 @@ __global__ __launch_bounds__(64) void mala_decode_split_kernel(DecParams p) {
         acc[db] = mfma16(a, pl, acc[db]);
       }
     }
-    if (hint) load_v(t - 1);
+    if (hint) {
+      load_v(t - 1);
+      ++vfetch;
+    }
 #pragma unroll
     for (int r = 0; r < 8; ++r) sv[r] = sn[r];
     mt = mtn;
   }
 
-  // partial of this split: O / l, lse (natural log) and the retained-tile count
+  // partial of this split: O / l, lse (natural log) and the retained-tile count.  A
+  // split without tiles has l = 0 (o = 0, lse = -inf: the merge skips it); a NaN or
+  // Inf input leaves l NaN, which must reach the merge as NaN, not as an empty split.
   float* pp = p.part + (((long)b * p.Hq + hq) * p.S + s) * (D + kDecStride);
   if (head_valid) {
-    const float inv = l > 0.f ? 1.f / l : 0.f;
+    const float inv = l != 0.f ? 1.f / l : 0.f;
 #pragma unroll
     for (int db = 0; db < NDB; ++db)
       *reinterpret_cast<f32x4*>(pp + 16 * db + 4 * g) = acc[db] * inv;
     if (g == 0) {
-      pp[D] = l > 0.f ? (m + fast_log2(l)) * kLn2 : kNegInf;
+      pp[D] = l != 0.f ? (m + fast_log2(l)) * kLn2 : kNegInf;
       pp[D + 1] = __int_as_float(cnt);
     }
   }
   if (p.counters) {
     if (head_valid && g == 0 && cnt) {
-      atomicAdd(&p.counters[1], (unsigned long long)cnt);
-      atomicAdd(&p.counters[3], (unsigned long long)cnt * kDecBk);
+      atomicAdd(&p.counters[kCntRetained], (unsigned long long)cnt);
+      atomicAdd(&p.counters[kCntSlots], (unsigned long long)cnt * kDecBk);
+      atomicAdd(&p.counters[kCntSetHash], hsum);
     }
     if (lane == 0) {
-      atomicAdd(&p.counters[0], (unsigned long long)(t_hi > t_lo ? t_hi - t_lo : 0) * nh);
-      if (vloads) atomicAdd(&p.counters[2], (unsigned long long)vloads);
+      atomicAdd(&p.counters[kCntLegal], (unsigned long long)(t_hi > t_lo ? t_hi - t_lo : 0) * nh);
+      if (vfetch) atomicAdd(&p.counters[kCntVTiles], (unsigned long long)vfetch);
+      if (vloads) atomicAdd(&p.counters[kCntVNeeded], (unsigned long long)vloads);
     }
   }
 }

@@ -38,6 +38,8 @@ __global__ __launch_bounds__(kFwdWaves * 64) void mala_fwd_kernel(FwdParams p) {
   // is processed
   __shared__ __attribute__((aligned(16))) bf16 Ks[2 * STAGE];
   __shared__ __attribute__((aligned(16))) bf16 Vs[2 * STAGE];
+  // statistics: per stage buffer, whether some wavefront retained each decision tile
+  __shared__ int vneed[2][kFwdStage / kBk];
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -82,7 +84,10 @@ __global__ __launch_bounds__(kFwdWaves * 64) void mala_fwd_kernel(FwdParams p) {
   const int nvalid = max(0, min(kBq, Nq - q0w));
   const int qlast_g = min(qblk * kFwdRows + kFwdRows - 1, Nq - 1);
   const int ttop = (int)((qlast_g + off) / kFwdStage);
-  unsigned n_legal = 0, n_ret = 0;
+  unsigned n_legal = 0, n_ret = 0, n_vneed = 0;
+  unsigned long long hsum = 0;   // fingerprints of the retained tiles
+  const bool stats = p.counters != nullptr;
+  if (stats && tid < 2 * (kFwdStage / kBk)) vneed[tid / (kFwdStage / kBk)][tid % (kFwdStage / kBk)] = 0;
 
   // K / V stages move with buffer loads straight into LDS (keys past the end read
   // as zeros): wavefront w issues the 64-position loads w, w + 8, ... of each slot.
@@ -168,6 +173,10 @@ __global__ __launch_bounds__(kFwdWaves * 64) void mala_fwd_kernel(FwdParams p) {
         if (!wave_any(demand)) continue;    // skipped: m, l and O unchanged
         ++n_ret;
         cnt += voter ? 1 : 0;
+        if (stats) {
+          hsum += tile_hash(b, hq, q0w / kBq, j);
+          if (lane == 0) vneed[buf][sub] = 1;
+        }
 
         // Lazy rescaling: a row's reference m moves only when some row of the
         // wavefront would otherwise see P = exp2(s - m) above 2^8; O and l are then
@@ -229,6 +238,15 @@ __global__ __launch_bounds__(kFwdWaves * 64) void mala_fwd_kernel(FwdParams p) {
     }
     wait_vm();
     __syncthreads();
+    if (stats && tid == 0) {
+      // the V tiles of this stage that some wavefront needed; cleared for the stage
+      // after next (the next stage uses the other buffer)
+#pragma unroll
+      for (int u = 0; u < kFwdStage / kBk; ++u) {
+        n_vneed += vneed[buf][u];
+        vneed[buf][u] = 0;
+      }
+    }
   }
 
   // epilogue: O <- O / l, LSE = (m + log2 l) * ln 2
@@ -248,13 +266,17 @@ __global__ __launch_bounds__(kFwdWaves * 64) void mala_fwd_kernel(FwdParams p) {
       if (p.row_tiles) p.row_tiles[qbase + qrow] = cnt;
     }
   }
-  if (p.counters) {
+  if (stats) {
     if (lane == 0 && n_legal) {
-      atomicAdd(&p.counters[0], (unsigned long long)n_legal);
-      atomicAdd(&p.counters[1], (unsigned long long)n_ret);
-      atomicAdd(&p.counters[3], (unsigned long long)n_ret * kBk * nvalid);
+      atomicAdd(&p.counters[kCntLegal], (unsigned long long)n_legal);
+      atomicAdd(&p.counters[kCntRetained], (unsigned long long)n_ret);
+      atomicAdd(&p.counters[kCntSlots], (unsigned long long)n_ret * kBk * nvalid);
+      if (hsum) atomicAdd(&p.counters[kCntSetHash], hsum);
     }
-    if (tid == 0) atomicAdd(&p.counters[2], (unsigned long long)(ttop + 1) * (kFwdStage / kBk));
+    if (tid == 0) {
+      atomicAdd(&p.counters[kCntVTiles], (unsigned long long)(ttop + 1) * (kFwdStage / kBk));
+      atomicAdd(&p.counters[kCntVNeeded], (unsigned long long)n_vneed);
+    }
   }
 }
 

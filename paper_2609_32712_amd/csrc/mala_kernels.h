@@ -40,6 +40,31 @@ constexpr float kLoTileDq = kLoMassDq / 16;  // dQ: |dS| of one tile and row, ab
 constexpr float kFwdLoShare = 1.0f / 64;
 constexpr int kDecStride = 4;                // extra floats per decode partial (lse, count, pad)
 
+// Statistics counters (int64 each; the indices of MALA_CNT_* in mala.h).
+constexpr int kNumCounters = 8;
+enum {
+  kCntLegal = 0, kCntRetained = 1, kCntVTiles = 2, kCntSlots = 3,
+  kCntRetainedKV = 4, kCntVNeeded = 5, kCntSetHash = 6, kCntSetHashKV = 7
+};
+
+// Fingerprint of one retained decision tile: splitmix64 (Steele, Lea and Flood's
+// SplitMix generator, its output mixing function) of the tile's coordinates
+// (sequence b, query head h, query tile i, key tile j of the sequence's own
+// tiling) packed as b << 52 | h << 40 | i << 20 | j.  A pass sums the fingerprints
+// of the tiles it retains modulo 2^64; the sum does not depend on the order of the
+// tiles, and two passes that retain different sets of tiles differ in it except
+// with probability ~2^-64.  It lets the statistics compare the retained sets of
+// two passes (or of a pass and an independent implementation) tile by tile
+// without storing them.
+__device__ __forceinline__ unsigned long long tile_hash(int b, int h, int i, int j) {
+  unsigned long long z = ((unsigned long long)b << 52) | ((unsigned long long)h << 40) |
+                         ((unsigned long long)i << 20) | (unsigned long long)j;
+  z += 0x9E3779B97F4A7C15ull;
+  z = (z ^ (z >> 30)) * 0xBF58476D1CE4E5B9ull;
+  z = (z ^ (z >> 27)) * 0x94D049BB133111EBull;
+  return z ^ (z >> 31);
+}
+
 // Batches come in two layouts.  Fixed length: [B, H, N, D], slice (b, h) at rows
 // (b H + h) N.  Packed (cu non-null): B sequences along the token axes of
 // [Hq, Nq, D] queries and [Hkv, Nk, D] keys (Nq, Nk = the totals, the head

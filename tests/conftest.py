@@ -14,6 +14,16 @@ def pytest_configure(config):
     config.addinivalue_line("markers", "slow: long-running CPU test")
 
 
+def pytest_terminal_summary(terminalreporter):
+    # the count-parity figures of the GPU tests (tie-band exemptions, differing rows)
+    mod = sys.modules.get("parity_util")
+    lines = mod.count_summary() if mod is not None else []
+    if lines:
+        terminalreporter.write_sep("-", "retained-tile count parity")
+        for ln in lines:
+            terminalreporter.write_line(ln)
+
+
 @pytest.fixture(scope="session")
 def gpu_available():
     import torch

@@ -4,10 +4,18 @@ the tolerance bar and the decision-count comparison with the tie band.
 The bar (for bf16 inputs, fp32 accumulation, against the fp64 oracle):
   * O, dQ, dK, dV: max-abs <= 1e-2 and mean-abs <= 1e-3;
   * per-row retained-tile counts equal the oracle's, except on rows whose query
-    block (forward) or whose tiles (backward) saw a test value T with
+    block (forward) or whose tiles (backward) saw a decisive test value T with
     |T - tau| <= 1e-5 in the oracle's own trajectory (tau > 0 only): there two
     correct finite-precision implementations may decide differently.
+Beyond that rule, every comparison of counts reports the fraction of rows the
+absolute band exempts, the fraction inside the relative band |T / tau - 1| <= 1e-5
+(a diagnostic: at tau = 1e-4 the absolute band is +-10% of tau), and the rows
+that actually differ; at most 1% of the rows (and at least one) may differ.  The
+figures are collected and printed at the end of the pytest run.
 """
+import math
+import os
+
 import numpy as np
 import torch
 
@@ -15,6 +23,10 @@ TOL_MAX = 1e-2
 TOL_MEAN = 1e-3
 TIE_BAND = 1e-5
 LSE_DIAG = 1e-3
+MAX_DIFFER_FRAC = 0.01
+
+# one entry per count comparison: (test, name, rows, exempt, relative band, differing)
+COUNT_LOG = []
 
 
 def dev(bits):
@@ -40,19 +52,86 @@ def assert_close(name, got, ref, where=None):
     return mx, mean
 
 
-def exempt_rows(tau, *ties):
-    """Rows exempt from count parity: any given tie array within the band (tau > 0)."""
-    ex = np.zeros(np.shape(ties[0]), dtype=bool)
+def ties(out, sl=()):
+    """The (tie_abs, tie_rel) pair of an oracle result dict, optionally sliced."""
+    return np.asarray(out["tie_abs"])[sl], np.asarray(out["tie_rel"])[sl]
+
+
+def tie_masks(tau, *pairs):
+    """Rows exempt from count parity (|T - tau| <= TIE_BAND for a tile of the row in
+    any given oracle trajectory, tau > 0) and rows inside the relative band
+    |T / tau - 1| <= TIE_BAND.  pairs: (tie_abs, tie_rel) arrays of one shape."""
+    ex = np.zeros(np.shape(pairs[0][0]), dtype=bool)
+    rel = np.zeros_like(ex)
     if tau > 0:
-        for t in ties:
-            ex |= np.nan_to_num(np.asarray(t), nan=np.inf) <= TIE_BAND
+        for a, r in pairs:
+            ex |= np.nan_to_num(np.asarray(a, dtype=np.float64), nan=np.inf) <= TIE_BAND
+            rel |= np.nan_to_num(np.asarray(r, dtype=np.float64), nan=np.inf) <= TIE_BAND
+    return ex, rel
+
+
+def assert_counts(name, got, ref, tau, *pairs):
+    """Per-row retained-tile counts: equal outside the tie band, and at most
+    MAX_DIFFER_FRAC of the rows (at least one) differing inside it.  Returns the
+    exempt mask."""
+    got = np.asarray(got)
+    ref = np.asarray(ref)
+    ex, rel = tie_masks(tau, *pairs)
+    differ = got != ref
+    bad = differ & ~ex
+    assert not bad.any(), "%s: %d rows differ outside the tie band (first %s: gpu %s oracle %s)" % (
+        name, int(bad.sum()), np.argwhere(bad)[:3].tolist(), got[bad][:3], ref[bad][:3])
+    n = int(got.size)
+    nd = int(differ.sum())
+    test = os.environ.get("PYTEST_CURRENT_TEST", "").split(" ")[0]
+    COUNT_LOG.append((test, name, n, float(ex.mean()), float(rel.mean()), nd))
+    print("[counts] %-22s rows %8d | exempt %.4f | relative band %.4f | differing %d"
+          % (name, n, ex.mean(), rel.mean(), nd), flush=True)
+    assert nd <= max(1, math.ceil(MAX_DIFFER_FRAC * n)), \
+        "%s: %d of %d rows differ inside the tie band" % (name, nd, n)
     return ex
 
 
-def assert_counts(name, got, ref, exempt):
-    got = np.asarray(got)
-    ref = np.asarray(ref)
-    bad = (got != ref) & ~exempt
-    assert not bad.any(), "%s: %d rows differ outside the tie band (first %s: gpu %s oracle %s)" % (
-        name, int(bad.sum()), np.argwhere(bad)[:3].tolist(), got[bad][:3], ref[bad][:3])
-    return float(exempt.mean())
+def count_summary():
+    """Lines summarising COUNT_LOG for the end of the test run."""
+    if not COUNT_LOG:
+        return []
+    rows = sum(e[2] for e in COUNT_LOG)
+    differ = sum(e[5] for e in COUNT_LOG)
+    w_ex = sum(e[2] * e[3] for e in COUNT_LOG) / rows
+    w_rel = sum(e[2] * e[4] for e in COUNT_LOG) / rows
+    lines = ["retained-tile count parity: %d comparisons, %d rows; exempt by |T - tau| <= 1e-5: "
+             "%.4f of rows (largest in one comparison %.4f); inside |T / tau - 1| <= 1e-5: %.4f "
+             "(largest %.4f); rows that differ: %d"
+             % (len(COUNT_LOG), rows, w_ex, max(e[3] for e in COUNT_LOG), w_rel,
+                max(e[4] for e in COUNT_LOG), differ)]
+    top = sorted(COUNT_LOG, key=lambda e: -e[3])[:5]
+    for t, name, n, ex, rel, nd in top:
+        if ex > 0:
+            lines.append("  exempt %.4f rel %.4f differ %d rows %d  %s %s"
+                         % (ex, rel, nd, n, t.split("::")[-1], name))
+    return lines
+
+
+def _splitmix64(z):
+    # the output function of Steele, Lea and Flood's SplitMix64 generator (uint64)
+    with np.errstate(over="ignore"):
+        z = z + np.uint64(0x9E3779B97F4A7C15)
+        z = (z ^ (z >> np.uint64(30))) * np.uint64(0xBF58476D1CE4E5B9)
+        z = (z ^ (z >> np.uint64(27))) * np.uint64(0x94D049BB133111EB)
+        return z ^ (z >> np.uint64(31))
+
+
+def set_fingerprint(keep, b0=0):
+    """The retained-set fingerprint the library reports (MALA_CNT_SET_HASH) of an
+    oracle decision array: keep [B, H, Tr, Tc] (forward / backward tile_keep) or
+    [B, H, T] (decode keep, query tile 0), 1 = retained; b0 offsets the sequence
+    index.  Sum modulo 2^64 of splitmix64(b << 52 | h << 40 | i << 20 | j), returned
+    as a signed 64-bit value like the int64 counters."""
+    keep = np.asarray(keep)
+    if keep.ndim == 3:
+        keep = keep[:, :, None, :]
+    b, h, i, j = (x.astype(np.uint64) for x in np.nonzero(keep == 1))
+    z = ((b + np.uint64(b0)) << np.uint64(52)) | (h << np.uint64(40)) | (i << np.uint64(20)) | j
+    total = int(_splitmix64(z).sum(dtype=np.uint64)) if z.size else 0
+    return total - (1 << 64) if total >= (1 << 63) else total

@@ -150,3 +150,140 @@ def test_python_binding_requires_device_tensors():
     x = torch.zeros(1, 1, 8, 64, dtype=torch.bfloat16)
     with pytest.raises(TypeError):
         mala.fwd(x, x, x, 0.125, 0.0)
+
+
+# ---------------------------------------------------------------------------
+# the Python binding checks every tensor argument (dtype, exact shape, contiguity,
+# then device) before it calls the library; on the CPU the shape and dtype checks
+# raise first, and tensors with the right shapes fail the device check
+# ---------------------------------------------------------------------------
+def _tensors(spec, over):
+    import torch
+    out = {}
+    for name, (shape, dtype) in spec.items():
+        x = over.get(name, shape)
+        if isinstance(x, tuple):
+            out[name] = torch.zeros(x, dtype=over.get(name + "_dtype", dtype))
+        else:
+            out[name] = x
+    return out
+
+
+def _fwd_spec():
+    import torch
+    bf, f32, i32, i64 = torch.bfloat16, torch.float32, torch.int32, torch.int64
+    return {"q": ((1, 4, 64, 128), bf), "k": ((1, 2, 64, 128), bf), "v": ((1, 2, 64, 128), bf),
+            "o": ((1, 4, 64, 128), f32), "lse": ((1, 4, 64), f32),
+            "row_tiles": ((1, 4, 64), i32), "counters": ((mala.NUM_COUNTERS,), i64)}
+
+
+def _bwd_spec():
+    import torch
+    sp = _fwd_spec()
+    sp.update({"dout": ((1, 4, 64, 128), torch.bfloat16), "dq": ((1, 4, 64, 128), torch.float32),
+               "dk": ((1, 2, 64, 128), torch.float32), "dv": ((1, 2, 64, 128), torch.float32),
+               "workspace": ((4096,), torch.uint8)})
+    return sp
+
+
+def _dec_spec():
+    import torch
+    bf, f32, i32, i64 = torch.bfloat16, torch.float32, torch.int32, torch.int64
+    return {"q": ((2, 8, 128), bf), "k_cache": ((2, 2, 300, 128), bf),
+            "v_cache": ((2, 2, 300, 128), bf), "o": ((2, 8, 128), f32), "lse": ((2, 8), f32),
+            "head_tiles": ((2, 8), i32), "counters": ((mala.NUM_COUNTERS,), i64),
+            "workspace": ((1 << 16,), torch.uint8), "cache_lens": ((2,), i32)}
+
+
+def _call_fwd(over):
+    t = _tensors(_fwd_spec(), over)
+    mala.mala_fwd(t["q"], t["k"], t["v"], t["o"], t["lse"], t["row_tiles"], t["counters"],
+                  0.088, 1e-3)
+
+
+def _call_bwd(over):
+    t = _tensors(_bwd_spec(), over)
+    mala.mala_bwd(t["q"], t["k"], t["v"], t["o"], t["lse"], t["dout"], t["dq"], t["dk"], t["dv"],
+                  t["row_tiles"], t["counters"], t["workspace"], 0.088, 1e-3)
+
+
+def _call_dec(over):
+    t = _tensors(_dec_spec(), over)
+    mala.mala_decode(t["q"], t["k_cache"], t["v_cache"], t["o"], t["lse"], t["head_tiles"],
+                     t["counters"], 2, t["workspace"], 0.088, 1e-3, cache_lens=t["cache_lens"])
+
+
+@pytest.mark.parametrize("over", [
+    dict(k=(2, 2, 64, 128)), dict(k=(1, 2, 64, 64)), dict(v=(1, 2, 65, 128)),
+    dict(v=(1, 1, 64, 128)), dict(o=(1, 4, 64, 64)), dict(o=(1, 4, 63, 128)),
+    dict(lse=(1, 4, 63)), dict(lse=(4, 64)), dict(row_tiles=(1, 4, 65)), dict(counters=(4,)),
+    dict(q=(4, 64, 128)),
+])
+def test_binding_fwd_rejects_shape_mismatch(over):
+    with pytest.raises(ValueError):
+        _call_fwd(over)
+
+
+@pytest.mark.parametrize("over", [
+    dict(dout=(1, 4, 64, 64)), dict(dq=(1, 4, 32, 128)), dict(dk=(1, 4, 64, 128)),
+    dict(dv=(2, 2, 64, 128)), dict(lse=(1, 2, 64)), dict(k=(1, 2, 64, 64)),
+])
+def test_binding_bwd_rejects_shape_mismatch(over):
+    with pytest.raises(ValueError):
+        _call_bwd(over)
+
+
+@pytest.mark.parametrize("over", [
+    dict(k_cache=(1, 2, 300, 128)), dict(k_cache=(2, 2, 300, 64)), dict(v_cache=(2, 2, 299, 128)),
+    dict(o=(2, 8, 64)), dict(o=(8, 128)), dict(lse=(2, 4)), dict(head_tiles=(2, 7)),
+    dict(cache_lens=(3,)), dict(counters=(4,)),
+])
+def test_binding_decode_rejects_shape_mismatch(over):
+    with pytest.raises(ValueError):
+        _call_dec(over)
+
+
+def test_binding_rejects_dtype_mismatch():
+    import torch
+    for call, over in ((_call_fwd, dict(q_dtype=torch.float32)),
+                       (_call_fwd, dict(lse_dtype=torch.bfloat16)),
+                       (_call_fwd, dict(counters_dtype=torch.int32)),
+                       (_call_fwd, dict(row_tiles_dtype=torch.int64)),
+                       (_call_bwd, dict(dout_dtype=torch.float32)),
+                       (_call_bwd, dict(dk_dtype=torch.bfloat16)),      # dq fp32, dk bf16
+                       (_call_dec, dict(k_cache_dtype=torch.float16)),
+                       (_call_dec, dict(cache_lens_dtype=torch.int64))):
+        with pytest.raises(TypeError):
+            call(over)
+
+
+def test_binding_rejects_non_contiguous_and_host_tensors():
+    import torch
+    o = torch.zeros(1, 4, 128, 64, dtype=torch.float32).transpose(2, 3)
+    with pytest.raises(ValueError):
+        _call_fwd(dict(o=o))
+    # every shape right: the tensors live on the host, which the device check rejects
+    for call in (_call_fwd, _call_bwd, _call_dec):
+        with pytest.raises(TypeError, match="CUDA"):
+            call({})
+
+
+def test_binding_varlen_checks():
+    import torch
+    bf = torch.bfloat16
+    q, k = torch.zeros(4, 100, 64, dtype=bf), torch.zeros(2, 100, 64, dtype=bf)
+    o, lse = torch.zeros(4, 100, 64), torch.zeros(4, 100)
+    cu = torch.tensor([0, 40, 100], dtype=torch.int32)
+    args = lambda **kw: dict(dict(q=q, k=k, v=k, cu_seqlens=cu, max_seqlen=60, o=o, lse=lse,
+                                  row_tiles=None, counters=None, scale=0.125, tau=0.0), **kw)
+    with pytest.raises(TypeError):
+        mala.mala_fwd_varlen(**args(cu_seqlens=cu.long()))
+    with pytest.raises(ValueError):
+        mala.mala_fwd_varlen(**args(cu_seqlens_k=torch.tensor([0, 100], dtype=torch.int32),
+                                    max_seqlen_k=100))
+    with pytest.raises(ValueError):
+        mala.mala_fwd_varlen(**args(v=torch.zeros(2, 100, 128, dtype=bf)))
+    with pytest.raises(ValueError):
+        mala.mala_fwd_varlen(**args(lse=torch.zeros(4, 99)))
+    with pytest.raises(TypeError, match="CUDA"):
+        mala.mala_fwd_varlen(**args())

@@ -11,8 +11,8 @@ import torch
 
 import oracle
 import paper_2609_32712_amd as mala
-from parity_util import (LSE_DIAG, TOL_MAX, assert_close, assert_counts, dev, exempt_rows,
-                         host)
+from parity_util import (LSE_DIAG, TOL_MAX, assert_close, assert_counts, dev, host,
+                         set_fingerprint, tie_masks, ties)
 from workloads import CONFIGS, Workload, bf16_to_f64
 
 pytestmark = pytest.mark.gpu
@@ -48,7 +48,9 @@ TRAIN_CASES = {
 TRAIN_TAUS = {
     "cfg1": (0.0, 1e-4, 1e-3),
     "local_d64_ragged": (0.0, 1e-2, 0.3, 1.0),
-    "gqa_d128_ragged": (0.0, 1e-3, 0.1, 1.0),
+    # 1e-40 is an fp32 denormal (log2 tau = -132.9: nothing is skipped); 1e30 keeps
+    # only each row's first tile in the forward and no tile in the backward
+    "gqa_d128_ragged": (0.0, 1e-40, 1e-3, 0.1, 1.0, 1e30),
     "tiny_d128": (0.0, 0.5),
     # tau = 1 would put the only tile exactly on the threshold (P = 1 = tau / L):
     # 0.5 retains and 1.5 skips it in the backward, both unambiguously
@@ -67,13 +69,27 @@ def _train_case(name, tau, Nq=None, seed=0):
     return w, q, k, v, do
 
 
+def counters(t):
+    """An int64 counters tensor as Python ints (the fingerprints use all 64 bits)."""
+    return [int(x) for x in t.cpu().numpy()]
+
+
+def _check_backward_passes_agree(cb):
+    # the key-major dK/dV pass and the query-major dQ pass take the same decisions:
+    # equal retained counts and equal fingerprints of the retained tile sets
+    assert cb[mala.CNT_RETAINED_KV] == cb[mala.CNT_RETAINED], cb
+    assert cb[mala.CNT_SET_HASH_KV] == cb[mala.CNT_SET_HASH], cb
+    assert 0 <= cb[mala.CNT_V_NEEDED] <= cb[mala.CNT_V_TILES], cb
+
+
 def _check_train(w, q, k, v, do, tau):
     scale = f32(w.scale)
     bq, bk = mala.mala_geometry(w.D, mala.PASS_FWD)
     assert (bq, bk) == mala.mala_geometry(w.D, mala.PASS_BWD)
     qf, kf, vf, dof = map(bf16_to_f64, (q, k, v, do))
     of = oracle.mala_fwd(qf, kf, vf, scale, f32(tau), bq, bk, want_tiles=True)
-    ob = oracle.mala_bwd(qf, kf, vf, of["o"], of["lse"], dof, scale, f32(tau), bq, bk)
+    ob = oracle.mala_bwd(qf, kf, vf, of["o"], of["lse"], dof, scale, f32(tau), bq, bk,
+                         want_tiles=True)
     Q, K, V, DO = map(dev, (q, k, v, do))
     g = mala.fwd(Q, K, V, scale, tau)
     gb = mala.bwd(Q, K, V, g["o"], g["lse"], DO, scale, tau)
@@ -81,22 +97,28 @@ def _check_train(w, q, k, v, do, tau):
     assert_close("O", host(g["o"]), of["o"])
     lse_err = np.abs(host(g["lse"]) - of["lse"]).max()
     assert lse_err <= LSE_DIAG, lse_err
-    ex_f = exempt_rows(tau, of["tie_abs"])
-    assert_counts("fwd row tiles", host(g["row_tiles"]), of["row_tiles"], ex_f)
-    ex_b = ex_f | exempt_rows(tau, ob["tie_abs"])
-    assert_counts("bwd row tiles", host(gb["row_tiles"]), ob["row_tiles"], ex_b)
+    ex_f = assert_counts("fwd row tiles", host(g["row_tiles"]), of["row_tiles"], tau, ties(of))
+    ex_b = assert_counts("bwd row tiles", host(gb["row_tiles"]), ob["row_tiles"], tau, ties(of),
+                         ties(ob))
     assert_close("dQ", host(gb["dq"]), ob["dq"])
     assert_close("dK", host(gb["dk"]), ob["dk"])
     assert_close("dV", host(gb["dv"]), ob["dv"])
     B, Hq, Nq, D = q.shape
     Nk = k.shape[2]
-    cf = host(g["counters"]).astype(np.int64)
-    assert cf[0] == legal_tiles(B, Hq, Nq, Nk, bq, bk)
-    assert cf[1] <= cf[0] and (tau > 0 or cf[1] == cf[0])
+    cf, cb = counters(g["counters"]), counters(gb["counters"])
+    legal = legal_tiles(B, Hq, Nq, Nk, bq, bk)
+    assert cf[mala.CNT_LEGAL] == legal and cb[mala.CNT_LEGAL] == legal
+    assert cf[mala.CNT_RETAINED] <= legal and (tau > 0 or cf[mala.CNT_RETAINED] == legal)
+    assert 0 < cf[mala.CNT_V_NEEDED] <= cf[mala.CNT_V_TILES]
+    assert cf[mala.CNT_RETAINED_KV] == 0 and cf[mala.CNT_SET_HASH_KV] == 0
+    _check_backward_passes_agree(cb)
+    # outside the tie band the retained sets equal the oracle's tile for tile
     if not ex_f.any():
-        assert cf[1] == int((of["tile_keep"] == 1).sum())
-    cb = host(gb["counters"]).astype(np.int64)
-    assert cb[0] == cf[0] and cb[1] <= cb[0]
+        assert cf[mala.CNT_RETAINED] == int((of["tile_keep"] == 1).sum())
+        assert cf[mala.CNT_SET_HASH] == set_fingerprint(of["tile_keep"])
+    if not ex_b.any():
+        assert cb[mala.CNT_RETAINED] == int((ob["tile_keep"] == 1).sum())
+        assert cb[mala.CNT_SET_HASH] == set_fingerprint(ob["tile_keep"])
     return ex_f.mean(), ex_b.mean()
 
 
@@ -143,7 +165,7 @@ def test_fidelity_measurement_matches_oracle():
     bq, bk = mala.mala_geometry(w.D, mala.PASS_FWD)
     qf, kf, vf, dof = map(bf16_to_f64, (q, k, v, do))
     Q, K, V, DO = map(dev, (q, k, v, do))
-    ro, rg, ties = {}, {}, None
+    ro, rg, tie_rows = {}, {}, None
     for t in (0.0, tau):
         of = oracle.mala_fwd(qf, kf, vf, scale, f32(t), bq, bk)
         ob = oracle.mala_bwd(qf, kf, vf, of["o"], of["lse"], dof, scale, f32(t), bq, bk)
@@ -154,7 +176,7 @@ def test_fidelity_measurement_matches_oracle():
         gb = mala.bwd(Q, K, V, g["o"], g["lse"], DO, scale, t)
         rg[t] = {"o": g["o"], "lse": g["lse"], "dq": gb["dq"], "dk": gb["dk"], "dv": gb["dv"]}
         if t > 0:
-            ties = exempt_rows(t, of["tie_abs"])
+            tie_rows = tie_masks(t, ties(of))[0]
     torch.cuda.synchronize()
     rg = {t: {x: y.cpu().double() for x, y in r.items()} for t, r in rg.items()}
     fo = bench.head_fidelity(ro[0.0], ro[tau])
@@ -164,10 +186,10 @@ def test_fidelity_measurement_matches_oracle():
     delta = max(float((rg[t]["lse"] - ro[t]["lse"]).abs().max()) for t in ro)
     eo = bench.omitted_mass_rows(ro[0.0]["lse"], ro[tau]["lse"]).numpy()
     eg = bench.omitted_mass_rows(rg[0.0]["lse"], rg[tau]["lse"]).numpy()
-    dev_rows = np.abs(eg - eo)[~ties]
+    dev_rows = np.abs(eg - eo)[~tie_rows]
     print("[fidelity] omitted mass: oracle mean %.3e max %.3e | |gpu-oracle| max %.3e "
           "(bound %.3e, %d tie rows)" % (eo.mean(), eo.max(), dev_rows.max(), 2 * delta,
-                                         int(ties.sum())), flush=True)
+                                         int(tie_rows.sum())), flush=True)
     assert eo.max() > 0
     assert dev_rows.max() <= 2 * delta + 1e-12
     # per-head relative L2: by the triangle inequality the two measurements differ by
@@ -217,23 +239,35 @@ def test_varlen_train_parity(name, tau):
     torch.cuda.synchronize()
     o, lse, rt = host(g["o"]), host(g["lse"]), host(g["row_tiles"])
     dq, dk, dv, rtb = host(gb["dq"]), host(gb["dk"]), host(gb["dv"]), host(gb["row_tiles"])
-    legal = 0
+    legal, fp_f, fp_b, any_ex_f, any_ex_b = 0, 0, 0, False, False
     for b, n in enumerate(lens):
         r = slice(int(cu[b]), int(cu[b + 1]))
         qf, kf, vf, dof = (bf16_to_f64(t[x][None, :, r]) for x in ("q", "k", "v", "do"))
-        of = oracle.mala_fwd(qf, kf, vf, scale, f32(tau), bq, bk)
-        ob = oracle.mala_bwd(qf, kf, vf, of["o"], of["lse"], dof, scale, f32(tau), bq, bk)
+        of = oracle.mala_fwd(qf, kf, vf, scale, f32(tau), bq, bk, want_tiles=True)
+        ob = oracle.mala_bwd(qf, kf, vf, of["o"], of["lse"], dof, scale, f32(tau), bq, bk,
+                             want_tiles=True)
         assert_close("O seq %d (n=%d)" % (b, n), o[:, r], of["o"][0])
         assert np.abs(lse[:, r] - of["lse"][0]).max() <= LSE_DIAG
-        ex_f = exempt_rows(tau, of["tie_abs"][0])
-        assert_counts("fwd row tiles seq %d" % b, rt[:, r], of["row_tiles"][0], ex_f)
-        ex_b = ex_f | exempt_rows(tau, ob["tie_abs"][0])
-        assert_counts("bwd row tiles seq %d" % b, rtb[:, r], ob["row_tiles"][0], ex_b)
+        ex_f = assert_counts("fwd row tiles seq %d" % b, rt[:, r], of["row_tiles"][0], tau,
+                             ties(of, 0))
+        ex_b = assert_counts("bwd row tiles seq %d" % b, rtb[:, r], ob["row_tiles"][0], tau,
+                             ties(of, 0), ties(ob, 0))
         assert_close("dQ seq %d" % b, dq[:, r], ob["dq"][0])
         assert_close("dK seq %d" % b, dk[:, r], ob["dk"][0])
         assert_close("dV seq %d" % b, dv[:, r], ob["dv"][0])
         legal += legal_tiles(1, w.Hq, n, n, bq, bk)
-    assert int(host(g["counters"])[0]) == legal and int(host(gb["counters"])[0]) == legal
+        fp_f += set_fingerprint(of["tile_keep"], b0=b)
+        fp_b += set_fingerprint(ob["tile_keep"], b0=b)
+        any_ex_f |= bool(ex_f.any())
+        any_ex_b |= bool(ex_b.any())
+    cf, cb = counters(g["counters"]), counters(gb["counters"])
+    assert cf[mala.CNT_LEGAL] == legal and cb[mala.CNT_LEGAL] == legal
+    _check_backward_passes_agree(cb)
+    wrap = lambda x: (x + (1 << 63)) % (1 << 64) - (1 << 63)    # sum modulo 2^64, signed
+    if not any_ex_f:
+        assert cf[mala.CNT_SET_HASH] == wrap(fp_f)
+    if not any_ex_b:
+        assert cb[mala.CNT_SET_HASH] == wrap(fp_b)
 
 
 def test_varlen_cut_and_uncovered_rows():
@@ -299,13 +333,14 @@ def test_varlen_prefill_parity(tau):
         ob = oracle.mala_bwd(qf, kf, vf, of["o"], of["lse"], dof, scale, f32(tau), bq, bk)
         assert_close("O seq %d (%d of %d)" % (b, nq, nk), o[:, rq], of["o"][0])
         assert np.abs(lse[:, rq] - of["lse"][0]).max() <= LSE_DIAG
-        ex_f = exempt_rows(tau, of["tie_abs"][0])
-        assert_counts("fwd row tiles seq %d" % b, rt[:, rq], of["row_tiles"][0], ex_f)
+        assert_counts("fwd row tiles seq %d" % b, rt[:, rq], of["row_tiles"][0], tau, ties(of, 0))
         assert_close("dQ seq %d" % b, dq[:, rq], ob["dq"][0])
         assert_close("dK seq %d" % b, dk[:, rk], ob["dk"][0])
         assert_close("dV seq %d" % b, dv[:, rk], ob["dv"][0])
         legal += legal_tiles(1, w.Hq, nq, nk, bq, bk)
-    assert int(host(g["counters"])[0]) == legal and int(host(gb["counters"])[0]) == legal
+    cb = counters(gb["counters"])
+    assert counters(g["counters"])[mala.CNT_LEGAL] == legal and cb[mala.CNT_LEGAL] == legal
+    _check_backward_passes_agree(cb)
 
 
 @pytest.mark.parametrize("tau", [1e-4, 1.0])
@@ -349,6 +384,31 @@ DECODE_CASES = [
 ]
 
 
+def _decode_v_needed(keep, Hkv):
+    """V tiles a decode wavefront consumes, from the oracle's decisions keep [B, Hq, T]:
+    one per (sequence, KV head, chunk of up to 16 query heads of its group, key tile)
+    in which some head of the chunk retains the tile."""
+    keep = np.asarray(keep)
+    B, Hq, T = keep.shape
+    grp = Hq // Hkv
+    n = 0
+    for hk in range(Hkv):
+        for c0 in range(0, grp, 16):
+            heads = slice(hk * grp + c0, hk * grp + min(grp, c0 + 16))
+            n += int((keep[:, heads] == 1).any(axis=1).sum())
+    return n
+
+
+def _check_decode_counters(cd, keep_b, ex, Hkv):
+    """keep_b: [(b, keep [1, Hq, T_b])] of the oracle; ex: the exempt heads."""
+    assert 0 < cd[mala.CNT_V_NEEDED] <= cd[mala.CNT_V_TILES], cd
+    assert cd[mala.CNT_RETAINED_KV] == 0 and cd[mala.CNT_SET_HASH_KV] == 0
+    if not np.asarray(ex).any():
+        fp = sum(set_fingerprint(kp, b0=b) for b, kp in keep_b)
+        assert cd[mala.CNT_SET_HASH] == (fp + (1 << 63)) % (1 << 64) - (1 << 63)
+        assert cd[mala.CNT_V_NEEDED] == sum(_decode_v_needed(kp, Hkv) for _, kp in keep_b)
+
+
 @pytest.mark.parametrize("spec,splits,tau", DECODE_CASES)
 def test_decode_parity_small(spec, splits, tau):
     w = Workload(spec)
@@ -356,13 +416,15 @@ def test_decode_parity_small(spec, splits, tau):
     scale = f32(w.scale)
     bk = mala.mala_geometry(w.D, mala.PASS_DECODE)[1]
     qf, kf, vf = map(bf16_to_f64, (t["q"], t["k"], t["v"]))
-    od = oracle.mala_decode(qf, kf, vf, scale, f32(tau), bk, splits)
+    od = oracle.mala_decode(qf, kf, vf, scale, f32(tau), bk, splits, want_tiles=True)
     g = mala.decode(dev(t["q"]), dev(t["k"]), dev(t["v"]), scale, tau, splits)
     torch.cuda.synchronize()
     assert_close("decode O", host(g["o"]), od["o"])
     assert np.abs(host(g["lse"]) - od["lse"]).max() <= LSE_DIAG
-    assert_counts("decode head tiles", host(g["head_tiles"]), od["tiles"],
-                  exempt_rows(tau, od["tie_abs"]))
+    ex = assert_counts("decode head tiles", host(g["head_tiles"]), od["tiles"], tau, ties(od))
+    cd = counters(g["counters"])
+    assert cd[mala.CNT_LEGAL] == w.B * w.Hq * -(-w.N // bk)
+    _check_decode_counters(cd, [(b, od["keep"][b:b + 1]) for b in range(w.B)], ex, w.Hkv)
 
 
 VARLEN_DECODE_CASES = [
@@ -389,20 +451,23 @@ def test_decode_per_sequence_cache_lengths(spec, lens, splits, tau):
     g = mala.decode(dev(t["q"]), dev(t["k"]), dev(t["v"]), scale, tau, splits, cache_lens=cl)
     torch.cuda.synchronize()
     o, lse, ht = host(g["o"]), host(g["lse"]), host(g["head_tiles"])
-    legal = 0
+    legal, keeps, exs = 0, [], []
     for b, n in enumerate(lens):
         n = min(max(n, 0), w.N)
         if n == 0:
             assert (o[b] == 0).all() and np.isneginf(lse[b]).all() and (ht[b] == 0).all()
             continue
         od = oracle.mala_decode(qf[b:b + 1], kf[b:b + 1, :, :n], vf[b:b + 1, :, :n], scale,
-                                f32(tau), bk, splits)
+                                f32(tau), bk, splits, want_tiles=True)
         assert_close("decode O seq %d (n=%d)" % (b, n), o[b], od["o"][0])
         assert np.abs(lse[b] - od["lse"][0]).max() <= LSE_DIAG
-        assert_counts("decode head tiles seq %d" % b, ht[b:b + 1], od["tiles"],
-                      exempt_rows(tau, od["tie_abs"]))
+        exs.append(assert_counts("decode head tiles seq %d" % b, ht[b:b + 1], od["tiles"], tau,
+                                 ties(od)).any())
+        keeps.append((b, od["keep"]))
         legal += -(-n // bk) * w.Hq
-    assert int(host(g["counters"])[0]) == legal
+    cd = counters(g["counters"])
+    assert cd[mala.CNT_LEGAL] == legal
+    _check_decode_counters(cd, keeps, exs, w.Hkv)
 
 
 def test_decode_full_lengths_match_uniform_path():
@@ -438,7 +503,17 @@ def test_decode_splits_cover_dense_at_tau0():
 # --------------------------------------------------------------------------
 # full-size workloads: sampled outputs in the benchmark's launch configuration
 # --------------------------------------------------------------------------
-def _full_train(cfg_id, tau, sample_blocks, heads, kv_head_tail, seed=0):
+def _full_train(cfg_id, tau, sample_heads, sample_fracs, kv, rows_from, key_fracs, seed=0):
+    """One workload in the benchmark's launch configuration, against the oracle on:
+      * sampled query blocks (sample_fracs of the blocks) of sampled query heads:
+        O, LSE, forward and backward retained counts, dQ;
+      * one KV head kv = (b, h_kv) with every query head of its GQA group: O, LSE and
+        forward counts on every query row from rows_from * N on, then dK and dV on two
+        key tiles at each of key_fracs (at or after rows_from * N: such keys are seen
+        only by rows the oracle forward covered), accumulated over all those rows and
+        heads the way the key-major pass accumulates them;
+    and the two backward passes' retained counts and fingerprints against each
+    other."""
     w = Workload(cfg_id, seed=seed)
     print("[full cfg%d tau=%g] generating inputs" % (cfg_id, tau), flush=True)
     t = w.tensors(threads=16)
@@ -450,74 +525,87 @@ def _full_train(cfg_id, tau, sample_blocks, heads, kv_head_tail, seed=0):
     g = mala.fwd(Q, K, V, scale, tau)
     gb = mala.bwd(Q, K, V, g["o"], g["lse"], DO, scale, tau)
     torch.cuda.synchronize()
+    _check_backward_passes_agree(counters(gb["counters"]))
     o_gpu, lse_gpu, rt_gpu = host(g["o"]), host(g["lse"]), host(g["row_tiles"])
     dq_gpu, rtb_gpu = host(gb["dq"]), host(gb["row_tiles"])
     dk_gpu, dv_gpu = host(gb["dk"]), host(gb["dv"])
     del Q, K, V, DO, g, gb
-    Tr = -(-N // bq)
+    Tr, Tc = -(-N // bq), -(-N // bk)
     grp = w.g
+    f64 = lambda x, b_, h0, h1: bf16_to_f64(t[x][b_:b_ + 1, h0:h1])
     # sampled query blocks of sampled heads: forward, dQ and counts
-    for (b, h) in heads:
+    for (b, h) in sample_heads:
         hk = h // grp
-        qf = bf16_to_f64(t["q"][b:b + 1, h:h + 1])
-        kf = bf16_to_f64(t["k"][b:b + 1, hk:hk + 1])
-        vf = bf16_to_f64(t["v"][b:b + 1, hk:hk + 1])
-        dof = bf16_to_f64(t["do"][b:b + 1, h:h + 1])
-        for i in sample_blocks(Tr):
+        qf, dof = f64("q", b, h, h + 1), f64("do", b, h, h + 1)
+        kf, vf = f64("k", b, hk, hk + 1), f64("v", b, hk, hk + 1)
+        for i in sorted({min(Tr - 1, int(f * Tr)) for f in sample_fracs}):
             print("[full cfg%d] oracle head %d block %d" % (cfg_id, h, i), flush=True)
             rows = slice(i * bq, min(N, (i + 1) * bq))
             of = oracle.mala_fwd(qf, kf, vf, scale, f32(tau), bq, bk, blocks=(i, i + 1))
             ob = oracle.mala_bwd(qf, kf, vf, of["o"], of["lse"], dof, scale, f32(tau), bq, bk,
                                  qblocks=(i, i + 1), kblocks=(0, 0))
-            assert_close("O blk %d" % i, o_gpu[b, h, rows], of["o"][0, 0, rows])
-            assert np.abs(lse_gpu[b, h, rows] - of["lse"][0, 0, rows]).max() <= LSE_DIAG
-            ex_f = exempt_rows(tau, of["tie_abs"][0, 0, rows])
-            assert_counts("fwd tiles", rt_gpu[b, h, rows], of["row_tiles"][0, 0, rows], ex_f)
-            ex_b = ex_f | exempt_rows(tau, ob["tie_abs"][0, 0, rows])
-            assert_counts("bwd tiles", rtb_gpu[b, h, rows], ob["row_tiles"][0, 0, rows], ex_b)
-            assert_close("dQ blk %d" % i, dq_gpu[b, h, rows], ob["dq"][0, 0, rows])
-    # dK, dV of the last key blocks of one KV head: they see only the last rows
-    b, hk = kv_head_tail
-    Tc = -(-N // bk)
-    last = 2
-    r0 = (Tc - last) * bk
-    qf = bf16_to_f64(t["q"][b:b + 1, hk * grp:(hk + 1) * grp])
-    kf = bf16_to_f64(t["k"][b:b + 1, hk:hk + 1])
-    vf = bf16_to_f64(t["v"][b:b + 1, hk:hk + 1])
-    dof = bf16_to_f64(t["do"][b:b + 1, hk * grp:(hk + 1) * grp])
-    print("[full cfg%d] oracle dK/dV of the last %d key blocks of kv head %d" % (cfg_id, last, hk),
-          flush=True)
-    of = oracle.mala_fwd(qf, kf, vf, scale, f32(tau), bq, bk, blocks=(r0 // bq, Tr))
-    o_in = np.nan_to_num(of["o"])
-    lse_in = np.nan_to_num(of["lse"])
-    ob = oracle.mala_bwd(qf, kf, vf, o_in, lse_in, dof, scale, f32(tau), bq, bk,
-                         qblocks=(0, 0), kblocks=(Tc - last, Tc))
-    assert_close("dK tail", dk_gpu[b, hk, r0:], ob["dk"][0, 0, r0:])
-    assert_close("dV tail", dv_gpu[b, hk, r0:], ob["dv"][0, 0, r0:])
+            sl = (0, 0, rows)
+            assert_close("O blk %d" % i, o_gpu[b, h, rows], of["o"][sl])
+            assert np.abs(lse_gpu[b, h, rows] - of["lse"][sl]).max() <= LSE_DIAG
+            assert_counts("fwd tiles", rt_gpu[b, h, rows], of["row_tiles"][sl], tau, ties(of, sl))
+            assert_counts("bwd tiles", rtb_gpu[b, h, rows], ob["row_tiles"][sl], tau,
+                          ties(of, sl), ties(ob, sl))
+            assert_close("dQ blk %d" % i, dq_gpu[b, h, rows], ob["dq"][sl])
+    # one KV head and its whole query-head group
+    b, hk = kv
+    h0, h1 = hk * grp, (hk + 1) * grp
+    i0 = int(rows_from * Tr)
+    r0 = i0 * bq
+    qf, dof = f64("q", b, h0, h1), f64("do", b, h0, h1)
+    kf, vf = f64("k", b, hk, hk + 1), f64("v", b, hk, hk + 1)
+    print("[full cfg%d] oracle forward of kv head %d (%d query heads), rows %d.." %
+          (cfg_id, hk, grp, r0), flush=True)
+    of = oracle.mala_fwd(qf, kf, vf, scale, f32(tau), bq, bk, blocks=(i0, Tr))
+    sl = (0, slice(None), slice(r0, N))
+    assert_close("O group", o_gpu[b, h0:h1, r0:], of["o"][sl])
+    assert np.abs(lse_gpu[b, h0:h1, r0:] - of["lse"][sl]).max() <= LSE_DIAG
+    assert_counts("fwd tiles group", rt_gpu[b, h0:h1, r0:], of["row_tiles"][sl], tau,
+                  ties(of, sl))
+    o_in, lse_in = np.nan_to_num(of["o"]), np.nan_to_num(of["lse"])
+    j_lo = -(-r0 // bk)
+    for j in sorted({min(Tc - 2, max(j_lo, int(f * Tc))) for f in key_fracs}):
+        print("[full cfg%d] oracle dK/dV of key tiles %d-%d (kv head %d)" % (cfg_id, j, j + 1, hk),
+              flush=True)
+        ob = oracle.mala_bwd(qf, kf, vf, o_in, lse_in, dof, scale, f32(tau), bq, bk,
+                             qblocks=(0, 0), kblocks=(j, j + 2))
+        r = slice(j * bk, min(N, (j + 2) * bk))
+        assert_close("dK keys %d.." % (j * bk), dk_gpu[b, hk, r], ob["dk"][0, 0, r])
+        assert_close("dV keys %d.." % (j * bk), dv_gpu[b, hk, r], ob["dv"][0, 0, r])
 
 
-def _blocks(*fracs):
-    return lambda Tr: sorted({min(Tr - 1, int(f * Tr)) for f in fracs})
+EDGES = (0.0, 0.5, 1.0)   # key tiles at the start, the middle and the end
 
 
 @pytest.mark.parametrize("tau", [0.0, 1e-4, 1e-3])
 def test_full_config2_sampled(tau):
-    _full_train(2, tau, _blocks(0.0, 0.37, 0.999), heads=[(0, 3), (0, 12)], kv_head_tail=(0, 5))
+    _full_train(2, tau, [(0, 3), (0, 12)], (0.0, 0.37, 0.999), kv=(0, 5), rows_from=0.0,
+                key_fracs=EDGES)
 
 
-@pytest.mark.parametrize("tau", [0.0, 1e-4])
+@pytest.mark.parametrize("tau", [0.0, 1e-4, 1.0])
 def test_full_config3_sampled(tau):
-    _full_train(3, tau, _blocks(0.5, 0.999), heads=[(0, 1), (0, 30)], kv_head_tail=(0, 7))
+    # heads 28..31 of KV head 7; their needle strengths beta_h differ
+    _full_train(3, tau, [(0, 1), (0, 30)], (0.5, 0.999), kv=(0, 7), rows_from=0.0,
+                key_fracs=EDGES)
 
 
 @pytest.mark.parametrize("tau", [1e-4, 1.0])
 def test_full_config4_sampled(tau):
-    _full_train(4, tau, _blocks(0.25, 0.999), heads=[(0, 6)], kv_head_tail=(0, 1))
+    # the key tiles from 15/16 of the sequence on accumulate over ~1000 query tiles of
+    # each of the 4 query heads of the group
+    _full_train(4, tau, [(0, 6)], (0.25, 0.999), kv=(0, 1), rows_from=15 / 16,
+                key_fracs=(15 / 16, 31 / 32, 1.0))
 
 
 @pytest.mark.parametrize("tau", [1e-4, 1.0])
 def test_full_config6_sampled(tau):
-    _full_train(6, tau, _blocks(0.3, 0.999), heads=[(0, 2), (0, 7)], kv_head_tail=(0, 1))
+    _full_train(6, tau, [(0, 2), (0, 7)], (0.3, 0.999), kv=(0, 1), rows_from=0.0,
+                key_fracs=EDGES)
 
 
 @pytest.mark.parametrize("tau", [0.0, 1e-4, 1.0])
@@ -541,8 +629,7 @@ def test_full_config5_decode_sampled(tau):
                                 bf16_to_f64(t["v"][b:b + 1, hk:hk + 1]), scale, f32(tau), bk, S)
         assert_close("decode O", o[b, h], od["o"][0, 0])
         assert abs(lse[b, h] - od["lse"][0, 0]) <= LSE_DIAG
-        assert_counts("decode tiles", ht[b:b + 1, h:h + 1], od["tiles"],
-                      exempt_rows(tau, od["tie_abs"]))
+        assert_counts("decode tiles", ht[b:b + 1, h:h + 1], od["tiles"], tau, ties(od))
 
 
 @pytest.mark.parametrize("tau", [1e-4, 1.0])
@@ -569,8 +656,107 @@ def test_full_config5_decode_ragged_lengths_sampled(tau):
                                 S)
         assert_close("decode O", o[b, h], od["o"][0, 0])
         assert abs(lse[b, h] - od["lse"][0, 0]) <= LSE_DIAG
-        assert_counts("decode tiles", ht[b:b + 1, h:h + 1], od["tiles"],
-                      exempt_rows(tau, od["tie_abs"]))
+        assert_counts("decode tiles", ht[b:b + 1, h:h + 1], od["tiles"], tau, ties(od))
+
+
+# --------------------------------------------------------------------------
+# non-finite inputs: the kernels finish, the outputs that depend on a NaN / Inf
+# input are non-finite, and the outputs of tiles that never touch it are bitwise
+# those of the clean inputs (tau = 0: every tile is retained, so a row with a NaN
+# state cannot change another row's decisions).  Inside a 32 x 32 tile that holds
+# the bad value, masked entries may become NaN too (their zero probability meets
+# the NaN in an MFMA product), so whole tiles are compared.
+# --------------------------------------------------------------------------
+def _nonfinite_case():
+    w, q, k, v, do = _train_case("gqa_d128_ragged", 0.0)
+    return w, [np.array(x) for x in (q, k, v, do)]
+
+
+def _run_train(w, q, k, v, do, tau=0.0):
+    Q, K, V, DO = map(dev, (q, k, v, do))
+    g = mala.fwd(Q, K, V, f32(w.scale), tau)
+    gb = mala.bwd(Q, K, V, g["o"], g["lse"], DO, f32(w.scale), tau)
+    torch.cuda.synchronize()
+    return {x: y.cpu() for x, y in list(g.items()) + list(gb.items()) if x != "counters"}
+
+
+NAN_BITS, INF_BITS = np.uint16(0x7FC0), np.uint16(0x7F80)   # bf16 NaN and +Inf
+
+
+@pytest.mark.parametrize("tensor", ["q", "do"])
+def test_nan_in_a_query_row_propagates(tensor):
+    w, (q, k, v, do) = _nonfinite_case()
+    clean = _run_train(w, q, k, v, do)
+    b, h, r = 1, 3, 333                    # query head 3 reads KV head 1
+    x = {"q": q, "do": do}[tensor]
+    x[b, h, r, 5] = NAN_BITS
+    bad = _run_train(w, q, k, v, do)
+    hk = h // w.g
+    t0 = r // 32 * 32                        # first row / key of r's 32-row tile
+    # the row's own outputs
+    assert torch.isnan(bad["dq"][b, h, r]).all()
+    if tensor == "q":
+        assert torch.isnan(bad["o"][b, h, r]).all() and torch.isnan(bad["lse"][b, h, r])
+    # every key up to the row feeds the row's gradient: dK and dV are NaN there
+    assert (~torch.isfinite(bad["dk"][b, hk, :r + 1])).any(dim=-1).all()
+    assert (~torch.isfinite(bad["dv"][b, hk, :r + 1])).any(dim=-1).all()
+    # untouched: the rows of the other 32-row tiles (the rows of r's own tile share
+    # its wavefront's rescaling and lo-term ballots, so their last bits may move),
+    # keys after r's tile, other KV heads and sequences
+    rows = torch.ones(w.N, dtype=torch.bool)
+    rows[t0:t0 + 32] = False
+    others = [hh for hh in range(w.Hq) if hh != h]
+    for name in ("o", "lse", "dq", "row_tiles"):
+        if name in ("o", "lse", "row_tiles") and tensor == "do":
+            assert torch.equal(bad[name], clean[name]), name     # dO plays no part
+            continue
+        sel = slice(None) if name == "row_tiles" else rows     # tau = 0: counts unchanged
+        assert torch.equal(bad[name][b, h, sel], clean[name][b, h, sel]), name
+        assert torch.equal(bad[name][:, others], clean[name][:, others]), name
+        assert torch.equal(bad[name][1 - b], clean[name][1 - b]), name
+    for name in ("dk", "dv"):
+        assert torch.equal(bad[name][b, hk, t0 + 32:], clean[name][b, hk, t0 + 32:]), name
+        assert torch.equal(bad[name][b, 1 - hk], clean[name][b, 1 - hk]), name
+        assert torch.equal(bad[name][1 - b], clean[name][1 - b]), name
+
+
+def test_inf_in_a_value_row_propagates():
+    w, (q, k, v, do) = _nonfinite_case()
+    clean = _run_train(w, q, k, v, do)
+    b, hk, c = 0, 1, 250
+    v[b, hk, c, 7] = INF_BITS
+    bad = _run_train(w, q, k, v, do)
+    heads = range(hk * w.g, (hk + 1) * w.g)
+    t0 = c // 32 * 32
+    for h in heads:
+        # every row that sees key c (retained at tau = 0) has a non-finite output
+        assert (~torch.isfinite(bad["o"][b, h, c:])).any(dim=-1).all()
+        # rows of the query tiles before key c's tile never touch it
+        assert torch.equal(bad["o"][b, h, :t0], clean["o"][b, h, :t0])
+        assert torch.equal(bad["lse"][b, h], clean["lse"][b, h])   # V plays no part in LSE
+    others = [h for h in range(w.Hq) if h not in heads]
+    for name in ("o", "lse", "dq", "dk", "dv"):
+        assert torch.equal(bad[name][1 - b], clean[name][1 - b]), name
+    for name in ("o", "dq"):
+        assert torch.equal(bad[name][:, others], clean[name][:, others]), name
+
+
+def test_nan_in_a_decode_query_propagates():
+    spec = dict(kind="decode", B=2, Hq=8, Hkv=2, N=3001, D=128, beta=3.0, needles=4)
+    w = Workload(spec)
+    t = {x: np.array(y) for x, y in w.tensors().items()}
+    run = lambda: {x: y.cpu() for x, y in mala.decode(dev(t["q"]), dev(t["k"]), dev(t["v"]),
+                                                       f32(w.scale), 0.0, 4).items()}
+    clean = run()
+    torch.cuda.synchronize()
+    t["q"][1, 5, 9] = NAN_BITS
+    bad = run()
+    torch.cuda.synchronize()
+    assert torch.isnan(bad["o"][1, 5]).all() and torch.isnan(bad["lse"][1, 5])
+    keep = torch.ones(2, 8, dtype=torch.bool)
+    keep[1, 5] = False
+    assert torch.equal(bad["o"][keep], clean["o"][keep])
+    assert torch.equal(bad["lse"][keep], clean["lse"][keep])
 
 
 # --------------------------------------------------------------------------
@@ -610,7 +796,8 @@ def test_graph_capture_replays_match_eager():
     dq = torch.empty_like(o)
     dk, dv = torch.empty((B, Hkv, N, D), **f), torch.empty((B, Hkv, N, D), **f)
     rt, rtb = torch.empty((B, Hq, N), **i32), torch.empty((B, Hq, N), **i32)
-    cf, cb, cd = (torch.empty(4, dtype=torch.int64, device="cuda") for _ in range(3))
+    cf, cb, cd = (torch.empty(mala.NUM_COUNTERS, dtype=torch.int64, device="cuda")
+                  for _ in range(3))
     ws = torch.empty(mala.mala_bwd_workspace_size(B, Hq, Hkv, N, N, D), dtype=torch.uint8,
                      device="cuda")
     wd = Workload(dict(kind="decode", B=2, Hq=8, Hkv=2, N=3001, D=128, beta=3.0, needles=4))
