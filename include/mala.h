@@ -240,6 +240,34 @@ int mala_decode(const void* q, const void* k_cache, const void* v_cache,
                 int B, int Hq, int Hkv, int Nk, int D, float scale, float tau, int out_dtype,
                 void* stream);
 
+/* Bytes of the decode buffer that libmala.so keeps on every GPU it runs on (see
+ * mala_decode_noalloc). */
+#define MALA_DECODE_SCRATCH_BYTES (16u << 20)
+
+/*
+ * mala_decode for callers that cannot allocate device memory: code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc.  The same
+ * computation, arguments and results as mala_decode, without the workspace: the
+ * split partials live in a buffer of MALA_DECODE_SCRATCH_BYTES that the library
+ * holds on each GPU until the process ends (a file-scope device array, not a
+ * hipMalloc).  The call itself allocates and frees nothing; its first call on a
+ * device looks up the buffer's address on that device (the device of `stream`, or
+ * the current device for the null stream).
+ *   Limit: mala_decode_workspace_size(B, Hq, D, num_splits) must not exceed
+ *   MALA_DECODE_SCRATCH_BYTES (16 MiB: e.g. 16 sequences x 32 heads x 64 splits at
+ *   D = 128 do not fit, x 32 splits do); a larger call returns MALA_ERR_WORKSPACE
+ *   and launches nothing.
+ *   Sharing: all calls on one GPU use that GPU's one buffer, which keeps the last
+ *   call's partials (every partial a call reads is written by the same call, so
+ *   nothing needs clearing).  Calls ordered on one stream are safe; calls that may
+ *   run at the same time on one GPU (different streams, or different threads
+ *   without ordering) race on the buffer and must not be issued.
+ */
+int mala_decode_noalloc(const void* q, const void* k_cache, const void* v_cache,
+                        const int32_t* cache_lens, void* o, float* lse, int32_t* head_tiles,
+                        int64_t* counters, int num_splits, int B, int Hq, int Hkv, int Nk, int D,
+                        float scale, float tau, int out_dtype, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

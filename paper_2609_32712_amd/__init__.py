@@ -6,7 +6,7 @@ and the current stream.  There is no fallback: if libmala.so is missing or no
 GPU is present, the calls raise.
 
 Low-level functions carry the C names and arguments (mala_fwd, mala_bwd,
-mala_fwd_varlen, mala_bwd_varlen, mala_decode, mala_geometry,
+mala_fwd_varlen, mala_bwd_varlen, mala_decode, mala_decode_noalloc, mala_geometry,
 mala_bwd_workspace_size, mala_decode_workspace_size); fwd / bwd / fwd_varlen /
 bwd_varlen / decode allocate their outputs and return them in a dict.
 """
@@ -30,7 +30,8 @@ NUM_COUNTERS = 8
 
 EXPORTS = ("mala_geometry", "mala_strerror", "mala_last_error", "mala_fwd",
            "mala_bwd_workspace_size", "mala_bwd", "mala_fwd_varlen", "mala_bwd_varlen",
-           "mala_decode_workspace_size", "mala_decode")
+           "mala_decode_workspace_size", "mala_decode", "mala_decode_noalloc")
+DECODE_SCRATCH_BYTES = 16 << 20   # MALA_DECODE_SCRATCH_BYTES
 
 
 class MalaError(RuntimeError):
@@ -76,6 +77,8 @@ def load_library():
     lib.mala_decode_workspace_size.restype = sz
     lib.mala_decode.argtypes = [vp] * 8 + [i, vp, sz] + [i] * 5 + [f, f, i, vp]
     lib.mala_decode.restype = i
+    lib.mala_decode_noalloc.argtypes = [vp] * 8 + [i] * 6 + [f, f, i, vp]
+    lib.mala_decode_noalloc.restype = i
     _lib = lib
     return lib
 
@@ -248,6 +251,23 @@ def mala_decode(q, k_cache, v_cache, o, lse, head_tiles, counters, num_splits, w
                                       num_splits, _ptr(workspace),
                                       workspace.numel() * workspace.element_size(), B, Hq, Hkv,
                                       Nk, D, scale, tau, _out_code(o), _stream(stream)))
+
+
+def mala_decode_noalloc(q, k_cache, v_cache, o, lse, head_tiles, counters, num_splits, scale,
+                        tau, stream=None, cache_lens=None):
+    """mala_decode without a workspace: the split partials use the library's own
+    buffer of DECODE_SCRATCH_BYTES on the GPU (for callers that cannot allocate).
+    Neither this function nor the library allocates device memory; calls that may
+    overlap on one GPU race on that buffer."""
+    B, Hq, Hkv, Nk, D = _decode_specs(q, k_cache, v_cache, o, lse, head_tiles, counters, None,
+                                      cache_lens)
+    _on_device((("q", q), ("k_cache", k_cache), ("v_cache", v_cache), ("o", o), ("lse", lse),
+                ("head_tiles", head_tiles), ("counters", counters), ("cache_lens", cache_lens)))
+    _check(load_library().mala_decode_noalloc(_ptr(q), _ptr(k_cache), _ptr(v_cache),
+                                              _ptr(cache_lens), _ptr(o), _ptr(lse),
+                                              _ptr(head_tiles), _ptr(counters), num_splits, B, Hq,
+                                              Hkv, Nk, D, scale, tau, _out_code(o),
+                                              _stream(stream)))
 
 
 def _varlen_specs(q, k, v, cu_seqlens, max_seqlen, cu_seqlens_k, max_seqlen_k, o, lse,

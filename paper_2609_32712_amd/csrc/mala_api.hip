@@ -5,6 +5,8 @@
 #include <stdio.h>
 #include <string.h>
 
+#include <mutex>
+
 #include "mala.h"
 #include "mala_device.h"
 #include "mala_kernels.h"
@@ -185,6 +187,89 @@ int check_varlen(const int32_t* cu_q, const int32_t* cu_k, int num_seqs, int max
   return st;
 }
 
+int check_decode(const void* q, const void* k_cache, const void* v_cache, const void* o,
+                 const float* lse, int num_splits, int B, int Hq, int Hkv, int Nk, int D,
+                 float scale, float tau, int out_dtype) {
+  if (!q || !k_cache || !v_cache || !o || !lse)
+    return fail(MALA_ERR_INVALID_ARG, "null q, k_cache, v_cache, o or lse");
+  int st = check_common(B, Hq, Hkv, 1, Nk, D, 1, scale, tau);
+  if (!st) st = check_dtype(out_dtype, "out_dtype");
+  if (st) return st;
+  if (num_splits < 1) return fail(MALA_ERR_INVALID_ARG, "num_splits must be >= 1");
+  return MALA_OK;
+}
+
+// The split kernel writes every partial [B, Hq, num_splits, D + 4] (also for splits
+// without tiles: o = 0, lse = -inf) before the merge kernel reads it, so the buffer
+// needs no clearing.
+int run_decode(const void* q, const void* k_cache, const void* v_cache, const int32_t* cache_lens,
+               void* o, float* lse, int32_t* head_tiles, int64_t* counters, int num_splits,
+               float* part, int B, int Hq, int Hkv, int Nk, int D, float scale, float tau,
+               int out_dtype, hipStream_t s) {
+  hipError_t e;
+  if (counters &&
+      (e = mala::launch_fill_zero(counters, mala::kNumCounters * sizeof(int64_t), s)) != hipSuccess)
+    return hip_fail(e, "mala_decode: clearing counters");
+  const int T = (Nk + mala::kDecBk - 1) / mala::kDecBk;
+  mala::DecParams p;
+  p.q = (const __bf16*)q;
+  p.k = (const __bf16*)k_cache;
+  p.v = (const __bf16*)v_cache;
+  p.lens = cache_lens;
+  p.part = part;
+  p.counters = (unsigned long long*)counters;
+  p.B = B; p.Hq = Hq; p.Hkv = Hkv; p.Nk = Nk;
+  p.S = num_splits;
+  p.nchunk = (Hq / Hkv + 15) / 16;
+  p.T = T;
+  p.tps = (T + num_splits - 1) / num_splits;
+  p.scale2 = scale * mala::kLog2e;
+  p.thr2 = log2_tau(tau) - log2f((float)Nk);
+  p.log2tau = log2_tau(tau);
+  if ((e = mala::launch_decode(p, D, s)) != hipSuccess) return hip_fail(e, "mala_decode: split launch");
+  if ((e = mala::launch_decode_combine(part, o, out_dtype == MALA_OUT_BF16, lse, head_tiles,
+                                       B * Hq, num_splits, D, s)) != hipSuccess)
+    return hip_fail(e, "mala_decode: combine launch");
+  return MALA_OK;
+}
+
+// The decode buffer of mala_decode_noalloc: a file-scope device array that every GPU
+// the library runs on holds until the process ends.  In host code `scratch` names a
+// host-side stand-in, not the array's device address: the address on a device comes
+// from hipGetSymbolAddress, looked up once per device (with that device current) and
+// kept in g_scratch; only that address is passed to kernels.
+constexpr size_t kDecodeScratchBytes = MALA_DECODE_SCRATCH_BYTES;
+static __device__ __align__(256) unsigned char scratch[kDecodeScratchBytes];
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch[kMaxDevices];
+
+// The device address of `scratch` on the device of stream s (the current device for
+// the null stream).
+int scratch_address(hipStream_t s, void** out) {
+  int dev = 0;
+  hipError_t e = s ? hipStreamGetDevice(s, &dev) : hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_fail(e, "mala_decode_noalloc: device of the stream");
+  if (dev < 0 || dev >= kMaxDevices)
+    return fail(MALA_ERR_UNSUPPORTED, "mala_decode_noalloc: device %d beyond %d", dev, kMaxDevices);
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch[dev]) {
+    int cur = 0;
+    if ((e = hipGetDevice(&cur)) != hipSuccess) return hip_fail(e, "mala_decode_noalloc: hipGetDevice");
+    if (cur != dev && (e = hipSetDevice(dev)) != hipSuccess)
+      return hip_fail(e, "mala_decode_noalloc: hipSetDevice");
+    void* ptr = nullptr;
+    const hipError_t eg = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+    if (cur != dev && (e = hipSetDevice(cur)) != hipSuccess)
+      return hip_fail(e, "mala_decode_noalloc: restoring the current device");
+    if (eg != hipSuccess) return hip_fail(eg, "mala_decode_noalloc: hipGetSymbolAddress");
+    if (!ptr) return fail(MALA_ERR_HIP, "mala_decode_noalloc: no device address for the buffer");
+    g_scratch[dev] = ptr;
+  }
+  *out = g_scratch[dev];
+  return MALA_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -281,42 +366,38 @@ int mala_decode(const void* q, const void* k_cache, const void* v_cache,
                 int B, int Hq, int Hkv, int Nk, int D, float scale, float tau, int out_dtype,
                 void* stream) {
   g_err[0] = 0;
-  if (!q || !k_cache || !v_cache || !o || !lse)
-    return fail(MALA_ERR_INVALID_ARG, "null q, k_cache, v_cache, o or lse");
-  int st = check_common(B, Hq, Hkv, 1, Nk, D, 1, scale, tau);
-  if (!st) st = check_dtype(out_dtype, "out_dtype");
+  int st = check_decode(q, k_cache, v_cache, o, lse, num_splits, B, Hq, Hkv, Nk, D, scale, tau,
+                        out_dtype);
   if (st) return st;
-  if (num_splits < 1) return fail(MALA_ERR_INVALID_ARG, "num_splits must be >= 1");
   const size_t need = mala_decode_workspace_size(B, Hq, D, num_splits);
   if (!workspace || workspace_bytes < need)
     return fail(MALA_ERR_WORKSPACE, "mala_decode needs %zu workspace bytes, got %zu", need,
                 workspace_bytes);
   if (((uintptr_t)workspace) % 16) return fail(MALA_ERR_WORKSPACE, "workspace not 16-byte aligned");
+  return run_decode(q, k_cache, v_cache, cache_lens, o, lse, head_tiles, counters, num_splits,
+                    (float*)workspace, B, Hq, Hkv, Nk, D, scale, tau, out_dtype,
+                    (hipStream_t)stream);
+}
+
+int mala_decode_noalloc(const void* q, const void* k_cache, const void* v_cache,
+                        const int32_t* cache_lens, void* o, float* lse, int32_t* head_tiles,
+                        int64_t* counters, int num_splits, int B, int Hq, int Hkv, int Nk, int D,
+                        float scale, float tau, int out_dtype, void* stream) {
+  g_err[0] = 0;
+  int st = check_decode(q, k_cache, v_cache, o, lse, num_splits, B, Hq, Hkv, Nk, D, scale, tau,
+                        out_dtype);
+  if (st) return st;
+  const size_t need = mala_decode_workspace_size(B, Hq, D, num_splits);
+  if (need > kDecodeScratchBytes)
+    return fail(MALA_ERR_WORKSPACE,
+                "mala_decode_noalloc: the split partials need %zu bytes, more than the library's "
+                "%zu-byte decode buffer (use mala_decode with a workspace, or fewer splits)",
+                need, kDecodeScratchBytes);
+  void* part = nullptr;
   hipStream_t s = (hipStream_t)stream;
-  hipError_t e;
-  if (counters && (e = mala::launch_fill_zero(counters, mala::kNumCounters * sizeof(int64_t), s)) != hipSuccess)
-    return hip_fail(e, "mala_decode: clearing counters");
-  const int T = (Nk + mala::kDecBk - 1) / mala::kDecBk;
-  mala::DecParams p;
-  p.q = (const __bf16*)q;
-  p.k = (const __bf16*)k_cache;
-  p.v = (const __bf16*)v_cache;
-  p.lens = cache_lens;
-  p.part = (float*)workspace;
-  p.counters = (unsigned long long*)counters;
-  p.B = B; p.Hq = Hq; p.Hkv = Hkv; p.Nk = Nk;
-  p.S = num_splits;
-  p.nchunk = (Hq / Hkv + 15) / 16;
-  p.T = T;
-  p.tps = (T + num_splits - 1) / num_splits;
-  p.scale2 = scale * mala::kLog2e;
-  p.thr2 = log2_tau(tau) - log2f((float)Nk);
-  p.log2tau = log2_tau(tau);
-  if ((e = mala::launch_decode(p, D, s)) != hipSuccess) return hip_fail(e, "mala_decode: split launch");
-  if ((e = mala::launch_decode_combine((float*)workspace, o, out_dtype == MALA_OUT_BF16, lse,
-                                       head_tiles, B * Hq, num_splits, D, s)) != hipSuccess)
-    return hip_fail(e, "mala_decode: combine launch");
-  return MALA_OK;
+  if ((st = scratch_address(s, &part)) != MALA_OK) return st;
+  return run_decode(q, k_cache, v_cache, cache_lens, o, lse, head_tiles, counters, num_splits,
+                    (float*)part, B, Hq, Hkv, Nk, D, scale, tau, out_dtype, s);
 }
 
 }  // extern "C"

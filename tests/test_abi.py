@@ -287,3 +287,19 @@ def test_binding_varlen_checks():
         mala.mala_fwd_varlen(**args(lse=torch.zeros(4, 99)))
     with pytest.raises(TypeError, match="CUDA"):
         mala.mala_fwd_varlen(**args())
+
+
+def test_decode_noalloc_rejects_sizes_beyond_its_buffer(lib):
+    # 16 sequences x 32 heads x 64 splits of (128 + 4) floats exceed the 16 MiB buffer:
+    # rejected before any HIP call (so also without a GPU); 32 splits fit
+    P = ctypes.c_void_p
+    qkv, ol = [P(16)] * 3, [P(16)] * 2
+    need64 = mala.mala_decode_workspace_size(16, 32, 128, 64)
+    assert need64 > mala.DECODE_SCRATCH_BYTES >= mala.mala_decode_workspace_size(16, 32, 128, 32)
+    st = lib.mala_decode_noalloc(*qkv, None, *ol, None, None, 64, 16, 32, 8, 131072, 128, 0.088,
+                                 1e-4, mala.OUT_F32, None)
+    assert st == mala.MALA_ERR_WORKSPACE
+    assert "buffer" in lib.mala_last_error().decode()
+    st = lib.mala_decode_noalloc(*qkv, None, *ol, None, None, 0, 16, 32, 8, 131072, 128, 0.088,
+                                 1e-4, mala.OUT_F32, None)
+    assert st == mala.MALA_ERR_INVALID_ARG       # num_splits < 1, before the size check
