@@ -187,7 +187,7 @@ def operator_memory(tr, tau):
     return res
 
 
-def train_config(cfg_id, taus, reps, warmup):
+def train_config(cfg_id, taus, reps, warmup, supp_taus=(), supp=None, memory=True):
     """One training workload: fwd / bwd latency (HIP events, mean and median of reps
     calls after warmup) at tau = 0 (dense through the same kernels) and at each tau,
     the speed-ups over dense, the retained work and the V / dO loads the retained
@@ -204,14 +204,15 @@ def train_config(cfg_id, taus, reps, warmup):
     pct = lambda a, b_: round(100.0 * float(a) / max(1.0, float(b_)), 3)
     res = {}
     for t_ in (0.0,) + tuple(x for x in taus if x != 0.0):
-        f = time_calls(lambda: tr.fwd(t_), reps, warmup)
-        b = time_calls(lambda: tr.bwd(t_), reps, warmup)
+        n_, w_ = supp if t_ in supp_taus else (reps, warmup)
+        f = time_calls(lambda: tr.fwd(t_), n_, w_)
+        b = time_calls(lambda: tr.bwd(t_), n_, w_)
         res[t_] = (f, b) + tuple(tr.counters())
     out = {"workload": CONFIGS[cfg_id]["desc"], "shape": [w.B, w.Hq, w.Hkv, w.N, w.D]}
     f0, b0 = res[0.0][0][0], res[0.0][1][0]
     for t_, (f, b, cf, cb) in res.items():
         fl_f, fl_b = train_flops(cf, cb, w.D, bq, bk)
-        out["tau=%g" % t_] = {
+        out["tau=%g" % t_ + (" (supplementary)" if t_ in supp_taus else "")] = {
             "fwd_ms": round(f[0], 4), "fwd_ms_median": round(f[1], 4),
             "bwd_ms": round(b[0], 4), "bwd_ms_median": round(b[1], 4),
             "speedup_fwd": round(f0 / f[0], 4), "speedup_bwd": round(b0 / b[0], 4),
@@ -226,7 +227,8 @@ def train_config(cfg_id, taus, reps, warmup):
             "dense_equiv_tflops_fwd": round(de_f / (f[0] * 1e-3) / 1e12, 1),
             "dense_equiv_tflops_bwd": round(de_b / (b[0] * 1e-3) / 1e12, 1),
         }
-    out["operator_memory"] = operator_memory(tr, taus[0])
+    if memory:
+        out["operator_memory"] = operator_memory(tr, taus[0])
     log("cfg%d dense fwd %.3f bwd %.3f ms | %s" % (
         cfg_id, f0, b0, " ".join("tau=%g fwd %.3f bwd %.3f" % (t_, r[0][0], r[1][0])
                                  for t_, r in res.items() if t_)))
@@ -332,11 +334,11 @@ def source_sha(path):
         return hashlib.sha256(fh.read()).hexdigest()[:16]
 
 
-def traffic_from_profiles(kernel_src):
-    """HBM bytes per launch of the backward operator from the committed rocprofv3
-    counter summary (FETCH_SIZE x 2.0 + WRITE_SIZE x 1.0, calibrated on a plain
-    copy), or None if the kernel source changed since the counters were taken."""
-    p = os.path.join(ROOT, "profiles", "mala_bwd_traffic_128k.json")
+TRAFFIC_FILES = {"bwd": "mala_bwd_traffic_128k.json", "decode": "mala_decode_traffic_128k.json"}
+
+
+def _traffic(which, kernel_src):
+    p = os.path.join(ROOT, "profiles", TRAFFIC_FILES[which])
     if not os.path.exists(p):
         return None
     with open(p) as fh:
@@ -346,8 +348,25 @@ def traffic_from_profiles(kernel_src):
     return float(d["bytes_per_launch"])
 
 
+def traffic_from_profiles(kernel_src):
+    """HBM bytes per launch of the backward operator from the committed rocprofv3
+    counter summary (FETCH_SIZE and WRITE_SIZE, each scaled by what it reads for a
+    plain copy), or None if the kernel source changed since the counters were taken."""
+    return _traffic("bwd", kernel_src)
+
+
+def decode_traffic_from_profiles(kernel_src):
+    """HBM bytes per mala_decode call (split + merge kernels) from the committed
+    counter summary, or None if the decode source changed since it was taken."""
+    return _traffic("decode", kernel_src)
+
+
 def cpu_baseline(step_ms_model):
-    """Time the fp64 oracle on a bounded sample of the same step and scale it up."""
+    """Time the fp64 oracle on a bounded sample of the same step and scale it up by
+    tile counts: the last nb query blocks of one head of the 131072-token workload
+    (forward, then the backward's dQ sweep over those blocks), the backward's dK/dV
+    sweep over the last nb key blocks (the rows that see them are exactly the rows
+    of the sampled forward), and whole decode calls of a few query heads."""
     import oracle
     from workloads import Workload, bf16_to_f64
     import paper_2609_32712_amd as mala
@@ -356,27 +375,33 @@ def cpu_baseline(step_ms_model):
     w = Workload(4)
     bq, bk = mala.mala_geometry(w.D, mala.PASS_FWD)
     Tr = -(-w.N // bq)
-    nb = min(Tr, 16 * cores)   # ~10 s of fp64 work on the host cores
-    i0 = Tr // 2 - nb // 2
+    nb = min(Tr, 8 * cores)
+    i0 = Tr - nb
     qf = bf16_to_f64(w.q_head(0, 0))[None, None]
     kf = bf16_to_f64(w.k_head(0, 0))[None, None]
     vf = bf16_to_f64(w.v_head(0, 0))[None, None]
     dof = bf16_to_f64(w.do_head(0, 0))[None, None]
     scale = float(np.float32(w.scale))
+    tau = float(np.float32(1e-4))
     t0 = time.time()
-    of = oracle.mala_fwd(qf, kf, vf, scale, float(np.float32(1e-4)), bq, bk, blocks=(i0, i0 + nb),
-                         heads=[(0, 0)])
+    of = oracle.mala_fwd(qf, kf, vf, scale, tau, bq, bk, blocks=(i0, Tr), heads=[(0, 0)])
     t_f = time.time() - t0
+    o_in, lse_in = np.nan_to_num(of["o"]), np.nan_to_num(of["lse"])
     t0 = time.time()
-    oracle.mala_bwd(qf, kf, vf, np.nan_to_num(of["o"]), np.nan_to_num(of["lse"]), dof, scale,
-                    float(np.float32(1e-4)), bq, bk, qblocks=(i0, i0 + nb), kblocks=(0, 0))
-    t_b = time.time() - t0
-    # sampled tiles: blocks i0..i0+nb-1 each see (i + 1) key tiles; the whole step
-    # has Hq * Tr (Tr + 1) / 2 tiles; the dQ-only sweep is half of the backward work
-    sample_tiles = sum(i + 1 for i in range(i0, i0 + nb))
+    oracle.mala_bwd(qf, kf, vf, o_in, lse_in, dof, scale, tau, bq, bk, qblocks=(i0, Tr),
+                    kblocks=(0, 0))
+    t_q = time.time() - t0
+    t0 = time.time()
+    oracle.mala_bwd(qf, kf, vf, o_in, lse_in, dof, scale, tau, bq, bk, qblocks=(0, 0),
+                    kblocks=(i0, Tr))
+    t_k = time.time() - t0
+    # tiles: query block i sees i + 1 key tiles, key block j is seen by Tr - j query
+    # tiles; the whole step has Hq * Tr (Tr + 1) / 2 of them on either side
+    q_tiles = sum(i + 1 for i in range(i0, Tr))
+    k_tiles = sum(Tr - j for j in range(i0, Tr))
     total_tiles = w.Hq * Tr * (Tr + 1) / 2
-    ms_fwd = t_f * 1e3 * total_tiles / sample_tiles
-    ms_bwd = 2 * t_b * 1e3 * total_tiles / sample_tiles
+    ms_fwd = t_f * 1e3 * total_tiles / q_tiles
+    ms_bwd = (t_q / q_tiles + t_k / k_tiles) * 1e3 * total_tiles
     wd = Workload(5)
     sd = mala.default_num_splits(wd.B, wd.Hkv, wd.N)
     qd = bf16_to_f64(wd.q_head(0, 0))[None, None]
@@ -385,17 +410,18 @@ def cpu_baseline(step_ms_model):
     t0 = time.time()
     nh = 8
     for h in range(nh):
-        oracle.mala_decode(qd, kd, vd, scale, float(np.float32(1e-4)),
-                           mala.mala_geometry(wd.D, mala.PASS_DECODE)[1], sd)
+        oracle.mala_decode(qd, kd, vd, scale, tau, mala.mala_geometry(wd.D, mala.PASS_DECODE)[1],
+                           sd)
     t_d = (time.time() - t0) / nh
     ms_dec = t_d * 1e3 * wd.B * wd.Hq
     total = ms_fwd + ms_bwd + ms_dec
     return {"value": round(total, 1), "unit": "ms", "cores": cores, "kind": "oracle",
-            "sample": ("fp64 C oracle (OpenMP over query blocks) on %d consecutive query blocks "
-                       "of head 0 of the 131072-token workload (fwd %.1fs, dQ sweep %.1fs, scaled "
-                       "by total/sampled tiles, x2 for the dK/dV sweep) plus %d decode heads "
-                       "(%.2fs each, x%d heads); extrapolated to one full step"
-                       % (nb, t_f, t_b, nh, t_d, wd.B * wd.Hq)),
+            "cpu_model": cpu_model(),
+            "sample": ("fp64 C oracle (OpenMP) on head 0 of the 131072-token workload: forward "
+                       "of the last %d query blocks %.1fs, dQ sweep of those blocks %.1fs, dK/dV "
+                       "sweep of the last %d key blocks %.1fs, scaled by total / sampled tiles; "
+                       "decode of %d query heads (%.2fs each, x%d heads); extrapolated to one "
+                       "full step" % (nb, t_f, t_q, nb, t_k, nh, t_d, wd.B * wd.Hq)),
             "fwd_ms": round(ms_fwd, 1), "bwd_ms": round(ms_bwd, 1), "decode_ms": round(ms_dec, 1)}
 
 
@@ -405,13 +431,15 @@ COUNTER_CMD = ("cd /tmp && export TMPDIR=/tmp && timeout -s KILL 180 rocprofv3 -
 TRACE_CMD = ("cd /tmp && export TMPDIR=/tmp && timeout -k 10 600 rocprofv3 --kernel-trace --stats "
              "--output-format csv -d $OUT/trace_bench -o bench -- "
              "python $REPO/bench.py --steps 2 --warmup 1 --reps 2 --kernel-warmup 1 "
-             "--supp-reps 2 --supp-warmup 1 --no-cpu-baseline --no-32k --no-lm --no-ragged")
+             "--supp-reps 2 --supp-warmup 1 --no-cpu-baseline --no-32k --no-lm --no-ragged "
+             "--no-small --no-memory")
 
 
-def counter_pass():
+def counter_pass(which="bwd"):
     """The program the traffic counters are taken on: a plain 512 MiB device copy
-    (the calibration kernel), then two mala_fwd + mala_bwd calls of the
-    131072-token workload."""
+    (the calibration kernel), then two mala_fwd + mala_bwd calls of the 131072-token
+    workload (which = "bwd") or two mala_decode calls of the 16 x 131072-token decode
+    workload (which = "decode"), tau = 1e-4."""
     import torch
     import paper_2609_32712_amd as mala
     mala.load_library()
@@ -421,10 +449,15 @@ def counter_pass():
     y.copy_(x)
     torch.cuda.synchronize()
     del x, y
-    tr = Train(4, 1e-4)
-    for _ in range(2):
-        tr.fwd(1e-4)
-        tr.bwd(1e-4)
+    if which == "decode":
+        dec = Decode(5, 1e-4)
+        for _ in range(2):
+            dec.run(1e-4)
+    else:
+        tr = Train(4, 1e-4)
+        for _ in range(2):
+            tr.fwd(1e-4)
+            tr.bwd(1e-4)
     torch.cuda.synchronize()
     log("counter pass done")
 
@@ -507,10 +540,23 @@ def _counter_means(path):
     return {k: sum(v) / len(v) for k, v in by.items()}
 
 
-def summarize_counters(fetch_csv, write_csv):
-    """profiles/mala_bwd_traffic_128k.json: HBM bytes per mala_bwd launch from the
-    FETCH_SIZE and WRITE_SIZE passes, each scaled by what the counter reads for the
-    512 MiB copy of the same run."""
+COUNTED = {
+    "bwd": dict(prefix="mala_bwd", src="mala_bwd.hip", flag="--counter-pass",
+                summarize="--summarize-counters",
+                workload="mala_bwd on the 131072-token share (8 q / 2 kv heads, d 128), tau 1e-4"),
+    "decode": dict(prefix="mala_decode", src="mala_decode.hip", flag="--decode-counter-pass",
+                   summarize="--summarize-decode-counters",
+                   workload="mala_decode, 16 x 32 q / 8 kv heads over 131072-token caches, d 128, "
+                            "tau 1e-4, 16 splits (split + merge kernels)"),
+}
+
+
+def summarize_counters(fetch_csv, write_csv, which="bwd"):
+    """profiles/mala_<which>_traffic_128k.json: HBM bytes per launch of the backward
+    operator (which = "bwd") or of a decode call ("decode") from the FETCH_SIZE and
+    WRITE_SIZE passes, each scaled by what the counter reads for the 512 MiB copy of
+    the same run."""
+    c = COUNTED[which]
     f, w = _counter_means(fetch_csv), _counter_means(write_csv)
     copy = [k for k in f if "copy" in k.lower()]
     if not copy:
@@ -520,27 +566,25 @@ def summarize_counters(fetch_csv, write_csv):
     fscale, wscale = round(kib / f[copy], 1), round(kib / w[copy], 1)
     kernels, total = {}, 0.0
     for k in sorted(f):
-        if "mala_bwd" in k or "mala_fill_zero" in k:
+        if c["prefix"] in k or "mala_fill_zero" in k:
             b = (f[k] * fscale + w.get(k, 0.0) * wscale) * 1024
-            if "mala_bwd" in k:
+            if c["prefix"] in k:
                 total += b
             kernels[k] = {"fetch_kib": f[k], "write_kib": w.get(k, 0.0), "bytes": b}
-    out = {"source_sha": source_sha(os.path.join(ROOT, "paper_2609_32712_amd", "csrc",
-                                                 "mala_bwd.hip")),
+    cmd = COUNTER_CMD.replace("--counter-pass", c["flag"])
+    out = {"source_sha": source_sha(os.path.join(ROOT, "paper_2609_32712_amd", "csrc", c["src"])),
            "bytes_per_launch": total, "fetch_scale": fscale, "write_scale": wscale,
            "kernels": kernels,
            "calibration": {"copy_kernel": copy, "copy_bytes": 512 << 20,
                            "copy_fetch_kib": f[copy], "copy_write_kib": w[copy]},
-           "workload": "mala_bwd on the 131072-token share (8 q / 2 kv heads, d 128), tau 1e-4",
-           "commands": [COUNTER_CMD.format(c="FETCH_SIZE", d="fetch"),
-                        COUNTER_CMD.format(c="WRITE_SIZE", d="write"),
-                        "python bench.py --summarize-counters "
-                        "$OUT/pmc_fetch/run_counter_collection.csv "
-                        "$OUT/pmc_write/run_counter_collection.csv"]}
-    with open(os.path.join(ROOT, "profiles", "mala_bwd_traffic_128k.json"), "w") as fh:
+           "workload": c["workload"],
+           "commands": [cmd.format(c="FETCH_SIZE", d="fetch"), cmd.format(c="WRITE_SIZE", d="write"),
+                        "python bench.py %s $OUT/pmc_fetch/run_counter_collection.csv "
+                        "$OUT/pmc_write/run_counter_collection.csv" % c["summarize"]]}
+    with open(os.path.join(ROOT, "profiles", TRAFFIC_FILES[which]), "w") as fh:
         json.dump(out, fh, indent=1)
-    print("mala_bwd HBM bytes per launch %.3f GB (fetch x%.1f, write x%.1f)"
-          % (total / 1e9, fscale, wscale))
+    print("%s HBM bytes per launch %.3f GB (fetch x%.1f, write x%.1f)"
+          % (c["prefix"], total / 1e9, fscale, wscale))
 
 
 def summarize_trace(trace_csv):
@@ -677,6 +721,10 @@ def main():
     ap.add_argument("--supp-warmup", type=int, default=5)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-32k", action="store_true")
+    ap.add_argument("--no-small", action="store_true",
+                    help="skip the 1024- and 8192-token workloads")
+    ap.add_argument("--no-memory", action="store_true",
+                    help="skip the per-call device memory measurement")
     ap.add_argument("--no-lm", action="store_true",
                     help="skip the language-model-like tau = 1 timing and fidelity sweep")
     ap.add_argument("--no-ragged", action="store_true",
@@ -684,6 +732,9 @@ def main():
     ap.add_argument("--counter-pass", action="store_true",
                     help="run only the program profiled for the traffic counters")
     ap.add_argument("--summarize-counters", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"))
+    ap.add_argument("--decode-counter-pass", action="store_true",
+                    help="run only the decode program profiled for the traffic counters")
+    ap.add_argument("--summarize-decode-counters", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"))
     ap.add_argument("--summarize-trace", metavar="KERNEL_TRACE_CSV")
     ap.add_argument("--skip-pass", action="store_true",
                     help="run only the program of the skip-cost trace")
@@ -693,6 +744,9 @@ def main():
     args = ap.parse_args()
     if args.summarize_counters:
         summarize_counters(*args.summarize_counters)
+        return
+    if args.summarize_decode_counters:
+        summarize_counters(*args.summarize_decode_counters, which="decode")
         return
     if args.summarize_trace:
         summarize_trace(args.summarize_trace)
@@ -711,8 +765,8 @@ def main():
               "single MI355X (heads and batch shard with no exchange; see the design notes).",
               file=sys.stderr)
         sys.exit(2)
-    if args.counter_pass:
-        counter_pass()
+    if args.counter_pass or args.decode_counter_pass:
+        counter_pass("decode" if args.decode_counter_pass else "bwd")
         return
     if args.skip_pass:
         skip_pass()
@@ -770,9 +824,9 @@ def main():
         dr = time_calls(lambda: dec.run(tau, cl), sr, sw)
         cdr = dec.cnt.cpu().numpy()
         drd = time_calls(lambda: dec.run(0.0, cl), sr, sw)
-        # K of every valid key, V of the tiles loaded (counted once per GQA group)
-        rag_kv = float(lens.sum()) * dec.w.Hkv * dec.w.D * 2
-        rag_bytes = rag_kv + rag_kv * cdr[2] / max(1, cdr[0] / dec.w.g)
+        # K of every valid key, V of the tiles fetched
+        rag_bytes = (float(lens.sum()) * dec.w.Hkv * dec.w.D * 2
+                     + float(cdr[mala.CNT_V_TILES]) * 32 * dec.w.D * 2)
         ragged = {
             "lens": "uniform on [1, %d], seed 7, first full, second 1 token; total %d"
                     % (dec.w.N, int(lens.sum())),
@@ -786,9 +840,14 @@ def main():
     de_f, de_b = dense_equivalent_flops(w.B, w.Hq, w.N, w.D)
     bwd_ms = rt["bwd"][0]
     achieved = fl_b / (bwd_ms * 1e-3) / 1e12
-    kv_bytes = dec.w.B * dec.w.Hkv * dec.w.N * dec.w.D * 2
     cd = rt["cd"]
-    dec_bytes = kv_bytes + kv_bytes * cd[2] / max(1, cd[0] / dec.w.g)
+    dw = dec.w
+    tile_bytes = mala.mala_geometry(dw.D, mala.PASS_DECODE)[1] * dw.D * 2
+    # K tiles read (one per decode wavefront and tile: nchunk wavefronts per KV head)
+    k_tiles = dw.B * dw.Hkv * (-(-dw.g // 16)) * (-(-dw.N // mala.mala_geometry(dw.D, 2)[1]))
+    dec_bytes = (k_tiles + cd[mala.CNT_V_TILES]) * tile_bytes
+    dec_traffic = decode_traffic_from_profiles(
+        os.path.join(ROOT, "paper_2609_32712_amd", "csrc", "mala_decode.hip"))
     pct = lambda a, b_: round(100.0 * float(a) / max(1.0, float(b_)), 3)
 
     detail = {
@@ -800,6 +859,8 @@ def main():
             "speedup_bwd": round(rd["bwd"][0] / rt["bwd"][0], 4),
             "retained_tiles_pct_fwd": pct(rt["cf"][1], rt["cf"][0]),
             "retained_tiles_pct_bwd": pct(rt["cb"][1], rt["cb"][0]),
+            "v_tiles_needed_pct_fwd": pct(rt["cf"][5], rt["cf"][2]),
+            "do_tiles_needed_pct_bwd": pct(rt["cb"][5], rt["cb"][2]),
             "mean_slots_per_query_fwd": round(float(rt["cf"][3]) / (w.B * w.Hq * w.N), 1),
             "mean_slots_per_query_bwd": round(float(rt["cb"][3]) / (w.B * w.Hq * w.N), 1),
             "executed_tflops_fwd": round(fl_f / (rt["fwd"][0] * 1e-3) / 1e12, 1),
@@ -813,9 +874,18 @@ def main():
             "speedup": round(rd["dec"][0] / rt["dec"][0], 4),
             "num_splits": dec.splits,
             "retained_head_tiles_pct": pct(cd[1], cd[0]),
-            "v_tiles_loaded_pct": pct(cd[2], cd[0] / dec.w.g),
+            "v_tiles_fetched_pct": pct(cd[mala.CNT_V_TILES], k_tiles),
+            "v_tiles_consumed_pct": pct(cd[mala.CNT_V_NEEDED], k_tiles),
+            "bytes_algorithmic": float(dec_bytes),
             "hbm_gbs_algorithmic": round(dec_bytes / (rt["dec"][0] * 1e-3) / 1e9, 1),
-            "hbm_frac": round(dec_bytes / (rt["dec"][0] * 1e-3) / 1e9 / PEAK_HBM_GBS, 4),
+            "hbm_frac_algorithmic": round(dec_bytes / (rt["dec"][0] * 1e-3) / 1e9 / PEAK_HBM_GBS,
+                                          4),
+            "bytes_counters": dec_traffic,
+            "hbm_gbs_counters": (round(dec_traffic / (rt["dec"][0] * 1e-3) / 1e9, 1)
+                                 if dec_traffic else None),
+            "hbm_frac": round((dec_traffic or dec_bytes) / (rt["dec"][0] * 1e-3) / 1e9
+                              / PEAK_HBM_GBS, 4),
+            "hbm_frac_source": "counters" if dec_traffic else "algorithmic",
             "ragged_lengths_supplementary": ragged,
         },
         "decision_tile": [bq, bk],
@@ -829,39 +899,28 @@ def main():
             "speedup_decode": round(rd["dec"][0] / d1[0], 4),
             "retained_tiles_pct_fwd": pct(cf1[1], cf1[0]),
             "retained_tiles_pct_bwd": pct(cb1[1], cb1[0]),
+            "v_tiles_needed_pct_fwd": pct(cf1[5], cf1[2]),
+            "do_tiles_needed_pct_bwd": pct(cb1[5], cb1[2]),
             "retained_head_tiles_pct_decode": pct(cd1[1], cd1[0]),
-            "v_tiles_loaded_pct_decode": pct(cd1[2], cd1[0] / dec.w.g),
+            "v_tiles_fetched_pct_decode": pct(cd1[2], k_tiles),
+            "v_tiles_consumed_pct_decode": pct(cd1[5], k_tiles),
             "mean_slots_per_query_fwd": round(float(cf1[3]) / (w.B * w.Hq * w.N), 1),
             "mean_slots_per_query_bwd": round(float(cb1[3]) / (w.B * w.Hq * w.N), 1),
         },
     }
+    if not args.no_memory:
+        detail["128k"]["operator_memory"] = operator_memory(tr, tau)
     del tr
     torch.cuda.empty_cache()
+    rw = (args.reps, args.kernel_warmup)
+    if not args.no_small:
+        # the two smaller workloads at their tolerance sweeps (tau = 0 is measured too)
+        detail["cfg1_1024"] = train_config(1, (1e-4, 1e-3), *rw, memory=not args.no_memory)
+        detail["cfg2_8192"] = train_config(2, (1e-4, 1e-3), *rw, memory=not args.no_memory)
     if not args.no_32k:
-        t3 = Train(3, tau)
-        r3 = {}
-        for name, t_ in (("tau", tau), ("dense", 0.0), ("tau1", 1.0)):
-            n_, w_ = (sr, sw) if name == "tau1" else (args.reps, args.kernel_warmup)
-            r3[name] = (time_calls(lambda: t3.fwd(t_), n_, w_),
-                        time_calls(lambda: t3.bwd(t_), n_, w_), t3.counters())
-        (f3, b3, (cf3, cb3)), (f3d, b3d, _) = r3["tau"], r3["dense"]
-        f31, b31, (cf31, cb31) = r3["tau1"]
-        detail["32k"] = {
-            "fwd_ms": round(f3[0], 3), "bwd_ms": round(b3[0], 3),
-            "dense_fwd_ms": round(f3d[0], 3), "dense_bwd_ms": round(b3d[0], 3),
-            "speedup_fwd": round(f3d[0] / f3[0], 4), "speedup_bwd": round(b3d[0] / b3[0], 4),
-            "retained_tiles_pct_fwd": pct(cf3[1], cf3[0]),
-            "retained_tiles_pct_bwd": pct(cb3[1], cb3[0]),
-            "tau1_supplementary": {
-                "fwd_ms": round(f31[0], 3), "bwd_ms": round(b31[0], 3),
-                "speedup_fwd": round(f3d[0] / f31[0], 4),
-                "speedup_bwd": round(b3d[0] / b31[0], 4),
-                "retained_tiles_pct_fwd": pct(cf31[1], cf31[0]),
-                "retained_tiles_pct_bwd": pct(cb31[1], cb31[0]),
-            },
-        }
-        del t3
-        torch.cuda.empty_cache()
+        # the 32768-token GQA workload at tau (and the canonical tau = 1, supplementary)
+        detail["32k"] = train_config(3, (tau, 1.0), *rw, supp_taus=(1.0,), supp=(sr, sw),
+                                     memory=not args.no_memory)
     if not args.no_lm:
         detail["lm_like_sweep"] = {
             "note": ("supplementary: language-model-like inputs (local key alpha=2, needles "
