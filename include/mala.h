@@ -78,15 +78,19 @@ enum {
                             counted by the query-major dQ pass) */
   MALA_CNT_V_TILES = 2,  /* forward: V tiles of B_k keys staged (a workgroup of 256
                             query rows stages every key tile it visits);
-                            backward: dO tiles of B_q rows staged by the key-major pass;
+                            backward: dO tiles of B_q rows staged by the key-major pass
+                            (a workgroup of 128 keys stages only the query tiles that
+                            some of its key tiles retain);
                             decode: V tiles of B_k keys fetched (once per up to 16 query
                             heads of a GQA group, look-ahead fetches included) */
   MALA_CNT_SLOTS = 3,    /* post-score key slots summed over query rows: a retained
                             B_q x B_k tile adds B_k slots to each of its valid rows
                             (Attention Cost section; mean slots per query =
                             counters[3] / number of query rows) */
-  MALA_CNT_RETAINED_KV = 4, /* backward only: retained tiles as counted by the key-major
-                               dK/dV pass (0 in forward and decode) */
+  MALA_CNT_RETAINED_KV = 4, /* backward only: of the tiles the dQ pass retained, those
+                               whose offline test the key-major dK/dV pass, recomputing
+                               it, confirms (equal to MALA_CNT_RETAINED when the two
+                               passes agree; 0 in forward and decode) */
   MALA_CNT_V_NEEDED = 5, /* the loads of MALA_CNT_V_TILES that a retained tile used:
                             forward: (workgroup, key tile) pairs with a retained tile;
                             backward: (key-major workgroup, query tile) pairs with a
@@ -97,9 +101,9 @@ enum {
                             retained tiles (sequence b, query head h, query tile i,
                             key tile j of the sequence's own tiling; decode: i = 0, j =
                             the key tile); backward: of the query-major dQ pass */
-  MALA_CNT_SET_HASH_KV = 7, /* backward only: the same fingerprint from the key-major
-                               dK/dV pass (equal to MALA_CNT_SET_HASH exactly when the
-                               two passes retain the same tiles, up to a 2^-64 chance) */
+  MALA_CNT_SET_HASH_KV = 7, /* backward only: the same fingerprint over the tiles of
+                               MALA_CNT_RETAINED_KV (equal to MALA_CNT_SET_HASH when the
+                               key-major pass confirms every tile, up to a 2^-64 chance) */
   MALA_NUM_COUNTERS = 8
 };
 
@@ -143,9 +147,17 @@ int mala_fwd(const void* q, const void* k, const void* v, void* o, float* lse,
              int32_t* row_tiles, int64_t* counters, int B, int Hq, int Hkv, int Nq, int Nk,
              int D, int causal, float scale, float tau, int out_dtype, void* stream);
 
-/* Bytes of device workspace mala_bwd needs for this shape (the per-row
- * D_q = rowsum(O_q * dO_q) vector of Algorithm 2). */
+/* Bytes of device workspace mala_bwd needs for this shape: the per-row
+ * D_q = rowsum(O_q * dO_q) vector of Algorithm 2 (B Hq Nq floats) and the tile
+ * decisions that the query-major dQ pass hands to the key-major dK/dV pass (one byte
+ * per query tile of B_q rows, query head and block of 128 keys: B Hq ceil(Nq / B_q)
+ * ceil(Nk / 128) bytes, ~32 MB at B = 1, Hq = 8, Nq = Nk = 131072). */
 size_t mala_bwd_workspace_size(int B, int Hq, int Hkv, int Nq, int Nk, int D);
+
+/* Bytes of device workspace mala_bwd_varlen needs: Hq total_q floats of D_q and
+ * Hq (total_q / B_q + num_seqs) ceil(max_seqlen_k / 128) decision bytes. */
+size_t mala_bwd_varlen_workspace_size(int num_seqs, int max_seqlen_k, int total_q, int Hq,
+                                      int Hkv, int D);
 
 /*
  * MALA backward (Algorithm 2): gradients of <O, dO> restricted to the tiles that
@@ -155,13 +167,16 @@ size_t mala_bwd_workspace_size(int B, int Hq, int Hkv, int Nq, int Nk, int D);
  *   [B, Hq, Nq, D].
  *   dq: [B, Hq, Nq, D] out; dk, dv: [B, Hkv, Nk, D] out (dK and dV of a KV head
  *       summed over its GQA group); all three fp32 or bf16 by grad_dtype.  No
- *       atomics: all three are bitwise reproducible.  dQ comes from a query-major pass that recomputes the
- *       tile scores with the same arithmetic, so it uses exactly the tiles the
- *       key-major dK/dV pass retains;
+ *       atomics: all three are bitwise reproducible.  dQ comes from a query-major
+ *       pass that takes every tile decision; the key-major dK/dV pass processes
+ *       only the query tiles that pass retained for some of its keys;
  *   row_tiles: int32 [B, Hq, Nq] or NULL out; counters: int64 [MALA_NUM_COUNTERS]
  *   or NULL out.
  *   workspace: device memory of at least mala_bwd_workspace_size(...) bytes,
- *   16-byte aligned, owned by the caller, not read by the caller afterwards.
+ *   16-byte aligned, owned by the caller, not read by the caller afterwards (its
+ *   contents on entry do not matter: every byte the call reads it writes first).
+ *   The dQ pass runs first and decides every tile; the key-major pass follows its
+ *   decisions, so both use exactly the same tiles.
  *   The shape limits of mala_fwd apply.
  */
 int mala_bwd(const void* q, const void* k, const void* v, const void* o, const float* lse,
@@ -202,8 +217,8 @@ int mala_fwd_varlen(const void* q, const void* k, const void* v, const int32_t* 
  * Packed variable-length batches: mala_bwd (Algorithm 2) per sequence, on the
  * layout of mala_fwd_varlen (o, lse as it returned them, o of type o_dtype; dout,
  * dq: [Hq, total_q, D]; dk, dv: [Hkv, total_k, D]; gradients of type grad_dtype).
- * workspace: at least mala_bwd_workspace_size(1, Hq, Hkv, total_q, total_k, D)
- * bytes.  Rows that no sequence covers are not written.
+ * workspace: at least mala_bwd_varlen_workspace_size(num_seqs, max_seqlen_k, total_q,
+ * Hq, Hkv, D) bytes.  Rows that no sequence covers are not written.
  */
 int mala_bwd_varlen(const void* q, const void* k, const void* v, const int32_t* cu_seqlens_q,
                     const int32_t* cu_seqlens_k, const void* o, const float* lse,

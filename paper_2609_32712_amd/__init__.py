@@ -7,7 +7,8 @@ GPU is present, the calls raise.
 
 Low-level functions carry the C names and arguments (mala_fwd, mala_bwd,
 mala_fwd_varlen, mala_bwd_varlen, mala_decode, mala_decode_noalloc, mala_geometry,
-mala_bwd_workspace_size, mala_decode_workspace_size); fwd / bwd / fwd_varlen /
+mala_bwd_workspace_size, mala_bwd_varlen_workspace_size, mala_decode_workspace_size);
+fwd / bwd / fwd_varlen /
 bwd_varlen / decode allocate their outputs and return them in a dict.
 """
 from __future__ import annotations
@@ -30,7 +31,8 @@ NUM_COUNTERS = 8
 
 EXPORTS = ("mala_geometry", "mala_strerror", "mala_last_error", "mala_fwd",
            "mala_bwd_workspace_size", "mala_bwd", "mala_fwd_varlen", "mala_bwd_varlen",
-           "mala_decode_workspace_size", "mala_decode", "mala_decode_noalloc")
+           "mala_decode_workspace_size", "mala_decode", "mala_decode_noalloc",
+           "mala_bwd_varlen_workspace_size")
 DECODE_SCRATCH_BYTES = 16 << 20   # MALA_DECODE_SCRATCH_BYTES
 
 
@@ -67,6 +69,8 @@ def load_library():
     lib.mala_fwd.restype = i
     lib.mala_bwd_workspace_size.argtypes = [i] * 6
     lib.mala_bwd_workspace_size.restype = sz
+    lib.mala_bwd_varlen_workspace_size.argtypes = [i] * 6
+    lib.mala_bwd_varlen_workspace_size.restype = sz
     lib.mala_bwd.argtypes = [vp] * 12 + [sz] + [i] * 7 + [f, f, i, i, vp]
     lib.mala_bwd.restype = i
     lib.mala_fwd_varlen.argtypes = [vp] * 9 + [i] * 8 + [f, f, i, vp]
@@ -164,6 +168,11 @@ def mala_geometry(head_dim, pass_):
 
 def mala_bwd_workspace_size(B, Hq, Hkv, Nq, Nk, D):
     return int(load_library().mala_bwd_workspace_size(B, Hq, Hkv, Nq, Nk, D))
+
+
+def mala_bwd_varlen_workspace_size(num_seqs, max_seqlen_k, total_q, Hq, Hkv, D):
+    return int(load_library().mala_bwd_varlen_workspace_size(num_seqs, max_seqlen_k, total_q, Hq,
+                                                             Hkv, D))
 
 
 def mala_decode_workspace_size(B, Hq, D, num_splits):
@@ -405,7 +414,8 @@ def bwd_varlen(q, k, v, cu_seqlens, max_seqlen, o, lse, dout, scale, tau, stats=
     rt = torch.zeros((Hq, total), dtype=torch.int32, device=q.device) if stats else None
     cnt = torch.empty(NUM_COUNTERS, dtype=torch.int64, device=q.device) if stats else None
     if workspace is None:
-        n = mala_bwd_workspace_size(1, Hq, Hkv, total, total_k, D)
+        mk = max_seqlen if cu_seqlens_k is None else max_seqlen_k
+        n = mala_bwd_varlen_workspace_size(cu_seqlens.shape[0] - 1, int(mk), total, Hq, Hkv, D)
         workspace = torch.empty(max(n, 16), dtype=torch.uint8, device=q.device)
     mala_bwd_varlen(q, k, v, cu_seqlens, max_seqlen, o, lse, dout, dq, dk, dv, rt, cnt,
                     workspace, scale, tau, stream=stream, cu_seqlens_k=cu_seqlens_k,

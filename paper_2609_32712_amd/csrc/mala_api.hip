@@ -30,6 +30,19 @@ int hip_fail(hipError_t e, const char* where) {
 
 size_t round_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 
+// Backward workspace: D_q = rowsum(O_q * dO_q) for every query row, then the dQ pass's
+// tile decisions for the key-major pass (one byte per query tile, query head and
+// 128-key block; query-tile rows as mask_rows gives them).
+size_t dvec_bytes(long rows) { return round_up((size_t)rows * sizeof(float), 256); }
+int mask_rows(bool packed, int B, int Nq) {
+  return packed ? Nq / mala::kBq + B : B * ((Nq + mala::kBq - 1) / mala::kBq);
+}
+size_t bwd_workspace(bool packed, int B, int Hq, int Hkv, int Nq, int max_k) {
+  const long rows = packed ? (long)Hq * Nq : (long)B * Hq * Nq;
+  const size_t nkblk = (size_t)(max_k + mala::kBwdKeys - 1) / mala::kBwdKeys;
+  return dvec_bytes(rows) + round_up((size_t)Hq * nkblk * mask_rows(packed, B, Nq), 256);
+}
+
 int check_common(int B, int Hq, int Hkv, int Nq, int Nk, int D, int causal, float scale, float tau) {
   if (B <= 0 || Hq <= 0 || Hkv <= 0 || Nq <= 0 || Nk <= 0)
     return fail(MALA_ERR_INVALID_ARG, "non-positive size (B, Hq, Hkv, Nq, Nk)");
@@ -162,6 +175,8 @@ int run_bwd(const void* q, const void* k, const void* v, const Packed& pk,
   p.log2tau = log2_tau(tau);
   p.nkblk = (p.max_len_k + mala::kBwdKeys - 1) / mala::kBwdKeys;
   p.nqblk = (p.max_len + mala::kDqRows - 1) / mala::kDqRows;
+  p.mask = (uint8_t*)workspace + dvec_bytes(rows);
+  p.mask_rows = mask_rows(pk.cu != nullptr, B, Nq);
   if ((e = mala::launch_bwd(p, D, s)) != hipSuccess) return hip_fail(e, "mala_bwd: kernel launch");
   return MALA_OK;
 }
@@ -304,9 +319,16 @@ int mala_fwd_varlen(const void* q, const void* k, const void* v, const int32_t* 
 }
 
 size_t mala_bwd_workspace_size(int B, int Hq, int Hkv, int Nq, int Nk, int D) {
-  (void)Hkv; (void)Nk; (void)D;
-  if (B <= 0 || Hq <= 0 || Nq <= 0) return 0;
-  return round_up((size_t)B * Hq * Nq * sizeof(float), 256);
+  (void)D;
+  if (B <= 0 || Hq <= 0 || Hkv <= 0 || Nq <= 0 || Nk <= 0) return 0;
+  return bwd_workspace(false, B, Hq, Hkv, Nq, Nk);
+}
+
+size_t mala_bwd_varlen_workspace_size(int num_seqs, int max_seqlen_k, int total_q, int Hq,
+                                      int Hkv, int D) {
+  (void)D;
+  if (num_seqs <= 0 || max_seqlen_k <= 0 || total_q <= 0 || Hq <= 0 || Hkv <= 0) return 0;
+  return bwd_workspace(true, num_seqs, Hq, Hkv, total_q, max_seqlen_k);
 }
 
 int mala_bwd(const void* q, const void* k, const void* v, const void* o, const float* lse,
@@ -345,7 +367,7 @@ int mala_bwd_varlen(const void* q, const void* k, const void* v, const int32_t* 
   if (!st) st = check_dtype(o_dtype, "o_dtype");
   if (!st) st = check_dtype(grad_dtype, "grad_dtype");
   if (st) return st;
-  const size_t need = mala_bwd_workspace_size(1, Hq, Hkv, total_q, total_k, D);
+  const size_t need = mala_bwd_varlen_workspace_size(num_seqs, max_seqlen_k, total_q, Hq, Hkv, D);
   if (!workspace || workspace_bytes < need)
     return fail(MALA_ERR_WORKSPACE, "mala_bwd_varlen needs %zu workspace bytes, got %zu", need,
                 workspace_bytes);

@@ -186,8 +186,9 @@ __global__ __launch_bounds__(1024) void mala_bwd_dkdv_kernel(BwdParams p) {
   constexpr int NI = (kBq * RC + 63) / 64;          // 64-chunk LDS-DMA loads per tile
   constexpr int TS = NI * 64 * 8;                   // tile slot stride (elements)
   static_assert(TS >= TILE, "slot holds the tile");
-  // rings of query tiles: Q_t is read at iterations t and t + 2, dO_t and the row
-  // vectors at iterations t + 1
+  static_assert(kDkdvChunk % 256 == 0, "whole sweep iterations per compacting thread");
+  // rings of query tiles: Q_k is read at steps k and k + 1, dO_k and the row vectors
+  // at step k + 1 (k counts the processed tiles)
   __shared__ __attribute__((aligned(16))) bf16 Qs[4 * TS];
   __shared__ __attribute__((aligned(16))) bf16 dOs[3 * TS];
   __shared__ __attribute__((aligned(16))) float rowv[3][3][kBq];   // lse2, threshold, D_q
@@ -197,16 +198,28 @@ __global__ __launch_bounds__(1024) void mala_bwd_dkdv_kernel(BwdParams p) {
   __shared__ __attribute__((aligned(16))) bf16x8 dSop[2][4][4][64];
   __shared__ int Pflag[3][4];    // 0 skipped, 1 retained, 3 retained with P's lo term
   __shared__ int dSlo[2][4];     // dS of the tile needs its lo term
+  // the processed tiles of the current chunk of the sweep: (iteration - chunk start)
+  // << 4 | the tile's decisions for the four key groups
+  __shared__ uint16_t plist[kDkdvChunk];
+  __shared__ int wsum[5];      // per-wavefront counts of the compaction, then the total
 
   // Sixteen wavefronts, four per 32 keys [32 g, +32) of the block (g = w % 4, so a
-  // key group's four wavefronts share one SIMD), in a pipeline over query tiles:
-  //   role 0, iteration t:  S_t = Q_t K^T, offline test, P_t (fp32) -> LDS
-  //   role 1, iteration t+1: dV^T += dO_t^T P_t (16 MFMAs)
-  //   role 2, iteration t+1: dP_t = dO_t V^T, dS_t = P_t (dP_t - D) -> LDS
-  //   role 3, iteration t+2: dK^T += Q_t^T dS_t (16 MFMAs)
-  // Each role runs its own loop (one barrier per iteration, the same count in all
-  // roles), so that the register allocation of one role carries no values of
-  // another: no wavefront needs more than 128 registers and four share a SIMD.
+  // key group's four wavefronts share one SIMD), in a pipeline over the query tiles
+  // that some key group retains (processed tile k):
+  //   role 0, step k:   S_k = Q_k K^T, P_k (fp32) -> LDS
+  //   role 1, step k+1: dV^T += dO_k^T P_k (16 MFMAs)
+  //   role 2, step k+1: dP_k = dO_k V^T, dS_k = P_k (dP_k - D) -> LDS
+  //   role 3, step k+2: dK^T += Q_k^T dS_k (16 MFMAs)
+  // Each role runs its own loop (one barrier per step, the same count in all roles),
+  // so that the register allocation of one role carries no values of another: no
+  // wavefront needs more than 128 registers and four share a SIMD.
+  //
+  // The tile decisions are the dQ pass's (it runs first and records, per query tile,
+  // head and 128-key block, which of the four 32-key tiles it retained): a query tile
+  // that no key group retains costs no score MFMAs, no Q / dO load and no pipeline
+  // step here.  Role 0 still evaluates the offline test on the tiles it processes and
+  // counts those it confirms (a statistic: equal to the retained count when the two
+  // passes agree).
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int role = wave >> 2, grp_k = wave & 3;
@@ -234,43 +247,40 @@ __global__ __launch_bounds__(1024) void mala_bwd_dkdv_kernel(BwdParams p) {
 
   // Query tiles are swept from the last one down to the block's diagonal, the
   // heads of the group innermost (iteration it: tile nqt - 1 - it / grp, head
-  // it % grp): the offline test does not depend on the order, and all co-resident
-  // workgroups of the same KV head then step through the same Q / dO tiles in
-  // lockstep, so that one fetch from HBM serves the whole XCD through its L2.
-  // The dV wavefronts (role 1, which wait longest at the barrier) move the tiles
-  // with buffer loads straight into LDS: the 64 lanes of one load fill
-  // 64 consecutive 16-byte positions of the tile's slot, each lane fetching the
-  // chunk that the LDS layout keeps there (row padding positions and the slack at
-  // the slot's end receive harmless data); the range check reads rows past the end
-  // of the sequence as zeros.  Loads for tile t + 1 are issued at the start of
-  // iteration t in the compiler-tracked form, so the dV wavefront waits for them at
-  // its first read of the dO tile (after reading and splitting P): that also holds
-  // its MFMAs back until the S wavefronts' dependent chains are under way, which
-  // measured faster than the untracked form with the wait at the barrier.
+  // it % grp): all co-resident workgroups of the same KV head then step through the
+  // same Q / dO tiles in near lockstep, so that one fetch from HBM serves the XCD
+  // through its L2.  The dV wavefronts (role 1, which wait longest at the barrier)
+  // move the tiles with buffer loads straight into LDS: the 64 lanes of one load fill
+  // 64 consecutive 16-byte positions of the tile's slot, each lane fetching the chunk
+  // that the LDS layout keeps there (row padding positions and the slack at the
+  // slot's end receive harmless data); the range check reads rows past the end of the
+  // sequence as zeros.  Loads for tile k + 1 are issued at the start of step k in the
+  // compiler-tracked form, so the dV wavefront waits for them at its first read of the
+  // dO tile (after reading and splitting P): that also holds its MFMAs back until the
+  // S wavefronts' dependent chains are under way, which measured faster than the
+  // untracked form with the wait at the barrier.
   auto tile_q0 = [&](int it) { return (nqt - 1 - it / grp) * kBq; };
+  const int mrow0 = mask_row0(p, b, sg);
+  // decisions of iteration it (query tile nqt - 1 - it / grp, head it % grp): bit g for
+  // key group g
+  auto decisions = [&](int it) {
+    return (int)p.mask[mask_index(p, mrow0 + nqt - 1 - it / grp, hkv * grp + it % grp, kblk)];
+  };
   const bool mover = role == 1;
   const int mt = tid & 255;                  // thread index within the moving role
   const int mw = grp_k;                      // moving wavefront 0..3: loads mw, mw + 4, ...
   constexpr int NJ = (NI + 3) / 4;           // loads per moving wavefront and tile
-  uint32_t dma_off[NJ];
-#pragma unroll
-  for (int u = 0; u < NJ; ++u) {
-    const int pos = 64 * (mw + 4 * u) + lane;          // chunk position in the slot
-    const int row = pos / RC, pc = pos % RC;
-    const int L = pc < D / 8 ? pc / (D / 32) + 4 * (pc % (D / 32)) : 0;   // logical chunk
-    dma_off[u] = (uint32_t)(row * D + 8 * L) * 2u;
-  }
-  float plse = 0.f, pdv = 0.f, plg = 0.f;
-  bool prow = false;
-  auto fetch = [&](int it) {
+  float plse = 0.f, pdv = 0.f;
+  int pq0 = 0;                               // first row of the staged tile
+  // Q / dO tiles of iteration it into ring slot k
+  auto fetch = [&](int it, int k) {
     const int q0 = tile_q0(it);
+    pq0 = q0;
     const long r0 = sg.qb + (long)(hkv * grp + it % grp) * p.Nq + q0;
     if (mt < kBq) {
       const uint32_t nr = (uint32_t)(Nq - q0) * 4u;
       plse = buf_load1(make_rsrc(p.lse + r0, nr), mt * 4u);
       pdv = buf_load1(make_rsrc(p.dvec + r0, nr), mt * 4u);
-      prow = q0 + mt < Nq;
-      plg = log2f((float)((long)q0 + mt + 1 + off));
     }
     const uint32_t nb = (uint32_t)(Nq - q0) * (uint32_t)D * 2u;
     const auto rq = make_rsrc(p.q + r0 * D, nb), ro = make_rsrc(p.dout + r0 * D, nb);
@@ -278,34 +288,72 @@ __global__ __launch_bounds__(1024) void mala_bwd_dkdv_kernel(BwdParams p) {
     for (int u = 0; u < NJ; ++u) {
       const int j = mw + 4 * u;
       if (j < NI) {
-        buf_load_lds16_tracked(rq, dma_off[u], Qs + (it & 3) * TS + 512 * j);
-        buf_load_lds16_tracked(ro, dma_off[u], dOs + (it % 3) * TS + 512 * j);
+        // the chunk this lane fetches so that LDS position 64 j + lane holds it
+        const int pos = 64 * j + lane;
+        const int row = pos / RC, pc = pos % RC;
+        const int L = pc < D / 8 ? pc / (D / 32) + 4 * (pc % (D / 32)) : 0;   // logical chunk
+        const uint32_t off_b = (uint32_t)(row * D + 8 * L) * 2u;
+        buf_load_lds16_tracked(rq, off_b, Qs + (k & 3) * TS + 512 * j);
+        buf_load_lds16_tracked(ro, off_b, dOs + (k % 3) * TS + 512 * j);
       }
     }
   };
-  auto stash = [&](int it) {
+  auto stash = [&](int k) {
     if (mt < kBq) {
       // the same arithmetic as row_vectors (the query-major kernel must agree bitwise)
 #pragma clang fp contract(off)
+      const bool prow = pq0 + mt < Nq;
+      const float plg = log2f((float)((long)pq0 + mt + 1 + off));
       const float l2 = plse * kLog2e;
-      rowv[it % 3][0][mt] = prow ? l2 : 0.f;
-      rowv[it % 3][1][mt] = prow ? l2 + p.log2tau - plg : __builtin_huge_valf();
-      rowv[it % 3][2][mt] = prow ? pdv : 0.f;
+      rowv[k % 3][0][mt] = prow ? l2 : 0.f;
+      rowv[k % 3][1][mt] = prow ? l2 + p.log2tau - plg : __builtin_huge_valf();
+      rowv[k % 3][2][mt] = prow ? pdv : 0.f;
     }
     wait_vm();
   };
-  // the iteration's end: stage the next tile, then the barrier (every role passes
-  // the same number of barriers)
-  auto iteration_end = [&](int) { __syncthreads(); };
+  // Compacts iterations [c0, c0 + kDkdvChunk) of the sweep into plist and returns how
+  // many there are (every thread calls it; the dP / dS wavefronts, which hold the
+  // least state, do the work: sixteen iterations per thread and a prefix sum of the
+  // processed counts over the four wavefronts).  The pipeline over the chunk then
+  // starts at step -1, in which the first tile is staged.
+  auto begin_chunk = [&](int c0) {
+    if (role == 2) {
+      const int t2 = tid & 255, w2 = wave & 3;
+      constexpr int PER = kDkdvChunk / 256;
+      int dec[PER], cnt = 0;
+#pragma unroll
+      for (int u = 0; u < PER; ++u) {
+        const int it = c0 + PER * t2 + u;
+        dec[u] = it < total ? decisions(it) : 0;
+        cnt += dec[u] != 0;
+      }
+      int x = cnt;   // inclusive scan over the wavefront
+#pragma unroll
+      for (int d = 1; d < 64; d <<= 1) {
+        const int y = __shfl_up(x, d);
+        if (lane >= d) x += y;
+      }
+      if (lane == 63) wsum[w2] = x;
+      __syncthreads();
+      int before = 0, np = 0;
+#pragma unroll
+      for (int w = 0; w < 4; ++w) {
+        const int s_ = wsum[w];
+        before += w < w2 ? s_ : 0;
+        np += s_;
+      }
+      int pos = before + x - cnt;
+#pragma unroll
+      for (int u = 0; u < PER; ++u)
+        if (dec[u]) plist[pos++] = (uint16_t)(((PER * t2 + u) << 4) | dec[u]);
+      if (tid == 512) wsum[4] = np;
+    } else {
+      __syncthreads();
+    }
+    __syncthreads();
+    return __builtin_amdgcn_readfirstlane(wsum[4]);
+  };
 
-  if (mover) {
-    fetch(0);
-    stash(0);
-  }
-  __syncthreads();
-  (void)mover;
-
-  const int n_it = total + 2;
   if (role == 0 || role == 2) {
     // K rows (role 0, B operand of S = Q K^T) or V rows (role 2, of dP = dO V^T)
     bf16x8 kv[KS];
@@ -317,50 +365,60 @@ __global__ __launch_bounds__(1024) void mala_bwd_dkdv_kernel(BwdParams p) {
     }
     if (role == 0) {
       float fdv = 0.f;   // P mass of this lane's key in tiles run without the lo term
-      unsigned n_ret_kv = 0;          // statistics: tiles this key group retains
+      unsigned n_ret_kv = 0;          // statistics: processed tiles whose test this pass confirms
       unsigned long long hsum = 0;    // and their fingerprints
-      for (int it = 0; it < n_it; ++it) {
-        if (it < total) {
-          // tile it: score discovery, offline test, P
-          const int q0 = tile_q0(it);
-          const float* rv = &rowv[it % 3][0][0];
-          bf16x8 qa[KS];
-          const bf16* qr = lds_pin(Qs + (it & 3) * TS + rdo);
+      for (int c0 = 0; c0 < total; c0 += kDkdvChunk) {
+        const int np = begin_chunk(c0);
+        if (!np) continue;
+        // the list entry of the next step, read during this one (the step's closing
+        // barrier waits for it, so the next step finds it in place)
+        int e_next = plist[0];
+        for (int k = -1; k < np + 2; ++k) {
+          if (k >= 0 && k < np) {
+            const int e = __builtin_amdgcn_readfirstlane(e_next);
+            if (k + 1 < np) e_next = plist[k + 1];
+            const int it = c0 + (e >> 4);
+            const bool ret = (e >> grp_k) & 1;
+            bool with_lo = false;
+            if (ret) {
+              // tile k: score discovery, offline test (statistics), P
+              const int q0 = tile_q0(it);
+              const float* rv = &rowv[k % 3][0][0];
+              bf16x8 qa[KS];
+              const bf16* qr = lds_pin(Qs + (k & 3) * TS + rdo);
 #pragma unroll
-          for (int kk = 0; kk < KS; ++kk) qa[kk] = load8(qr + rd_step<D>(kk));
-          const f32x16 sc = qk_tile<KS>(qa, kv);
-          // tiles that cross the diagonal or the end of the sequence (or whose keys
-          // all lie beyond this tile's rows) take the masked test
-          const bool need_mask =
-              ((long)kw + kBk - 1 > (long)q0 + off) || (q0 + kBq > Nq) || (kw + kBk > Nk);
-          const int klo = key < Nk ? (int)((long)key - off - q0) - 4 * h : 1000000;
-          float sv[16];
-          const bool dem =
-              offline_entries(sc, p.scale2, need_mask, klo, Nq - q0 - 4 * h, rv + kBq, h, sv);
-          const bool ret = wave_any(dem);
-          bool with_lo = false;
-          if (ret) {
-            probabilities(sv, p.scale2, rv, h);
+              for (int kk = 0; kk < KS; ++kk) qa[kk] = load8(qr + rd_step<D>(kk));
+              const f32x16 sc = qk_tile<KS>(qa, kv);
+              // tiles that cross the diagonal or the end of the sequence (or whose keys
+              // all lie beyond this tile's rows) take the masked test
+              const bool need_mask =
+                  ((long)kw + kBk - 1 > (long)q0 + off) || (q0 + kBq > Nq) || (kw + kBk > Nk);
+              const int klo = key < Nk ? (int)((long)key - off - q0) - 4 * h : 1000000;
+              float sv[16];
+              const bool dem =
+                  offline_entries(sc, p.scale2, need_mask, klo, Nq - q0 - 4 * h, rv + kBq, h, sv);
+              if (p.counters && wave_any(dem)) {
+                ++n_ret_kv;
+                hsum += tile_hash(b, hkv * grp + it % grp, q0 / kBq, kw / kBk);
+              }
+              probabilities(sv, p.scale2, rv, h);
 #pragma unroll
-            for (int g = 0; g < 4; ++g)
-              Pf[it & 1][grp_k][g][lane] =
-                  f32x4{sv[4 * g], sv[4 * g + 1], sv[4 * g + 2], sv[4 * g + 3]};
-            // dV runs this tile without P's lo term while the key's P mass in such
-            // tiles stays within kLoMassDv (for every key of the tile)
-            float ps = 0.f;
+              for (int g = 0; g < 4; ++g)
+                Pf[k & 1][grp_k][g][lane] =
+                    f32x4{sv[4 * g], sv[4 * g + 1], sv[4 * g + 2], sv[4 * g + 3]};
+              // dV runs this tile without P's lo term while the key's P mass in such
+              // tiles stays within kLoMassDv (for every key of the tile)
+              float ps = 0.f;
 #pragma unroll
-            for (int r = 0; r < 16; ++r) ps += sv[r];
-            const float fv_new = fdv + halves_sum(ps);
-            with_lo = wave_any(fv_new > kLoMassDv);
-            if (!with_lo) fdv = fv_new;
+              for (int r = 0; r < 16; ++r) ps += sv[r];
+              const float fv_new = fdv + halves_sum(ps);
+              with_lo = wave_any(fv_new > kLoMassDv);
+              if (!with_lo) fdv = fv_new;
+            }
+            if (lane == 0) Pflag[k % 3][grp_k] = ret ? (with_lo ? 3 : 1) : 0;
           }
-          if (lane == 0) Pflag[it % 3][grp_k] = ret ? (with_lo ? 3 : 1) : 0;
-          if (ret && p.counters) {
-            ++n_ret_kv;
-            hsum += tile_hash(b, hkv * grp + it % grp, q0 / kBq, kw / kBk);
-          }
+          __syncthreads();
         }
-        iteration_end(it);
       }
       if (p.counters && lane == 0 && n_ret_kv) {
         atomicAdd(&p.counters[kCntRetainedKV], (unsigned long long)n_ret_kv);
@@ -368,49 +426,53 @@ __global__ __launch_bounds__(1024) void mala_bwd_dkdv_kernel(BwdParams p) {
       }
     } else {
       float fdk = 0.f;   // sum of |dS| of this lane's key in tiles run without the lo term
-      for (int it = 0; it < n_it; ++it) {
-        const int t = it - 1;
-        if (t >= 0 && t < total && Pflag[t % 3][grp_k]) {
-          // tile t: dP = dO V^T; dS = P (dP - D) -> LDS as hi / lo B operands
-          const float* rv = &rowv[t % 3][0][0];
-          bf16x8 oa[KS];
-          const bf16* orr = lds_pin(dOs + (t % 3) * TS + rdo);
+      for (int c0 = 0; c0 < total; c0 += kDkdvChunk) {
+        const int np = begin_chunk(c0);
+        if (!np) continue;
+        for (int k = -1; k < np + 2; ++k) {
+          const int t = k - 1;
+          if (t >= 0 && t < np && Pflag[t % 3][grp_k]) {
+            // tile t: dP = dO V^T; dS = P (dP - D) -> LDS as hi / lo B operands
+            const float* rv = &rowv[t % 3][0][0];
+            bf16x8 oa[KS];
+            const bf16* orr = lds_pin(dOs + (t % 3) * TS + rdo);
 #pragma unroll
-          for (int kk = 0; kk < KS; ++kk) oa[kk] = load8(orr + rd_step<D>(kk));
-          const f32x16 dp = qk_tile<KS>(oa, kv);
-          float ds[16];
+            for (int kk = 0; kk < KS; ++kk) oa[kk] = load8(orr + rd_step<D>(kk));
+            const f32x16 dp = qk_tile<KS>(oa, kv);
+            float ds[16];
 #pragma unroll
-          for (int g = 0; g < 4; ++g) {
-            const f32x4 p4 = Pf[t & 1][grp_k][g][lane];
-            const f32x4 d4 = *reinterpret_cast<const f32x4*>(rv + 2 * kBq + 8 * g + 4 * h);
+            for (int g = 0; g < 4; ++g) {
+              const f32x4 p4 = Pf[t & 1][grp_k][g][lane];
+              const f32x4 d4 = *reinterpret_cast<const f32x4*>(rv + 2 * kBq + 8 * g + 4 * h);
 #pragma unroll
-            for (int e = 0; e < 4; ++e) ds[4 * g + e] = p4[e] * (dp[4 * g + e] - d4[e]);
+              for (int e = 0; e < 4; ++e) ds[4 * g + e] = p4[e] * (dp[4 * g + e] - d4[e]);
+            }
+            // dK runs this tile without dS's lo term while the key's sum of |dS| in
+            // such tiles stays within kLoMassDk (for every key of the tile); a tile
+            // holding more than kLoTileDk of some key's |dS| always takes the lo term
+            float as = 0.f;
+#pragma unroll
+            for (int r = 0; r < 16; ++r) as += fabsf(ds[r]);
+            const float as_key = halves_sum(as);
+            const float fk_new = fdk + as_key;
+            const bool with_lo = wave_any(fk_new > kLoMassDk || as_key > kLoTileDk);
+            if (!with_lo) fdk = fk_new;
+            bf16x8 xh[2], xl[2];
+            if (with_lo) {
+              split_bf16x8(ds, xh[0], xl[0]);
+              split_bf16x8(ds + 8, xh[1], xl[1]);
+              dSop[t & 1][grp_k][2][lane] = xl[0];
+              dSop[t & 1][grp_k][3][lane] = xl[1];
+            } else {
+              xh[0] = hi_bf16x8(ds);
+              xh[1] = hi_bf16x8(ds + 8);
+            }
+            dSop[t & 1][grp_k][0][lane] = xh[0];
+            dSop[t & 1][grp_k][1][lane] = xh[1];
+            if (lane == 0) dSlo[t & 1][grp_k] = with_lo ? 1 : 0;
           }
-          // dK runs this tile without dS's lo term while the key's sum of |dS| in
-          // such tiles stays within kLoMassDk (for every key of the tile); a tile
-          // holding more than kLoTileDk of some key's |dS| always takes the lo term
-          float as = 0.f;
-#pragma unroll
-          for (int r = 0; r < 16; ++r) as += fabsf(ds[r]);
-          const float as_key = halves_sum(as);
-          const float fk_new = fdk + as_key;
-          const bool with_lo = wave_any(fk_new > kLoMassDk || as_key > kLoTileDk);
-          if (!with_lo) fdk = fk_new;
-          bf16x8 xh[2], xl[2];
-          if (with_lo) {
-            split_bf16x8(ds, xh[0], xl[0]);
-            split_bf16x8(ds + 8, xh[1], xl[1]);
-            dSop[t & 1][grp_k][2][lane] = xl[0];
-            dSop[t & 1][grp_k][3][lane] = xl[1];
-          } else {
-            xh[0] = hi_bf16x8(ds);
-            xh[1] = hi_bf16x8(ds + 8);
-          }
-          dSop[t & 1][grp_k][0][lane] = xh[0];
-          dSop[t & 1][grp_k][1][lane] = xh[1];
-          if (lane == 0) dSlo[t & 1][grp_k] = with_lo ? 1 : 0;
+          __syncthreads();
         }
-        iteration_end(it);
       }
     }
   } else {
@@ -432,67 +494,84 @@ __global__ __launch_bounds__(1024) void mala_bwd_dkdv_kernel(BwdParams p) {
         }
     };
     if (role == 1) {
-      unsigned n_do = 0;   // statistics: query tiles whose dO some key group needed
-      for (int it = 0; it < n_it; ++it) {
-        if (it + 1 < total) fetch(it + 1);
-        const int t = it - 1;
-        const int pf = (t >= 0 && t < total) ? Pflag[t % 3][grp_k] : 0;
-        if (p.counters && grp_k == 0 && t >= 0 && t < total)
-          n_do += (Pflag[t % 3][0] | Pflag[t % 3][1] | Pflag[t % 3][2] | Pflag[t % 3][3]) ? 1 : 0;
-        if (pf) {
-          float pv[16];
-#pragma unroll
-          for (int g = 0; g < 4; ++g) {
-            const f32x4 p4 = Pf[t & 1][grp_k][g][lane];
-#pragma unroll
-            for (int e = 0; e < 4; ++e) pv[4 * g + e] = p4[e];
+      unsigned n_do = 0;   // statistics: dO tiles staged (some key group retained the tile)
+      for (int c0 = 0; c0 < total; c0 += kDkdvChunk) {
+        const int np = begin_chunk(c0);
+        if (!np) continue;
+        n_do += np;
+        int e_next = plist[0];   // the entry to fetch next, read a step ahead
+        for (int k = -1; k < np + 2; ++k) {
+          if (k + 1 < np) {
+            fetch(c0 + (__builtin_amdgcn_readfirstlane(e_next) >> 4), k + 1);
+            if (k + 2 < np) e_next = plist[k + 2];
           }
-          const bf16* atb = dOs + (t % 3) * TS + tro;
-          accumulate(atb, hi_bf16x8(pv), hi_bf16x8(pv + 8));
-          if (pf & 2) {
-            bf16x8 hh[2], bl[2];
-            split_bf16x8(pv, hh[0], bl[0]);
-            split_bf16x8(pv + 8, hh[1], bl[1]);
-            accumulate(atb, bl[0], bl[1]);
+          const int t = k - 1;
+          const int pf = (t >= 0 && t < np) ? Pflag[t % 3][grp_k] : 0;
+          if (pf) {
+            float pv[16];
+#pragma unroll
+            for (int g = 0; g < 4; ++g) {
+              const f32x4 p4 = Pf[t & 1][grp_k][g][lane];
+#pragma unroll
+              for (int e = 0; e < 4; ++e) pv[4 * g + e] = p4[e];
+            }
+            const bf16* atb = dOs + (t % 3) * TS + tro;
+            accumulate(atb, hi_bf16x8(pv), hi_bf16x8(pv + 8));
+            if (pf & 2) {
+              bf16x8 hh[2], bl[2];
+              split_bf16x8(pv, hh[0], bl[0]);
+              split_bf16x8(pv + 8, hh[1], bl[1]);
+              accumulate(atb, bl[0], bl[1]);
+            }
           }
+          if (k + 1 < np) stash(k + 1);
+          __syncthreads();
         }
-        if (it + 1 < total) stash(it + 1);
-        __syncthreads();
       }
-      if (p.counters && grp_k == 0 && lane == 0)
+      if (p.counters && grp_k == 0 && lane == 0 && n_do) {
+        atomicAdd(&p.counters[kCntVTiles], (unsigned long long)n_do);
         atomicAdd(&p.counters[kCntVNeeded], (unsigned long long)n_do);
+      }
     } else {
-      // the decision of tile it - 2 is known since the end of iteration it - 2: it
-      // is read one iteration early, off the critical path
+      // the decision of tile k - 2 is known since the end of step k - 2: it is read one
+      // step early, off the critical path
       int fl3 = 0;
-      // the Q^T operands of the next iteration's tile, read at the end of this one
-      bf16x8 a[DB][2];
-      auto load_a = [&](int tt) {
+      // the Q^T operands of the next step's tile for its first k-step, read at the end
+      // of this step (the second k-step's are read in the step itself: holding both
+      // across the barrier would exceed the registers of four wavefronts per SIMD)
+      bf16x8 a0[DB], a1[DB];
+      auto load_a = [&](int tt, int ks, bf16x8 (&a)[DB]) {
         const bf16* ab = lds_pin(Qs + (tt & 3) * TS + tro);
 #pragma unroll
-        for (int db = 0; db < DB; ++db)
-#pragma unroll
-          for (int ks = 0; ks < 2; ++ks) {
-            const bf16* at = ab + 16 * ks * (D + 8) + tr_step<D>(db);
-            a[db][ks] = cat(lds_read_tr(at), lds_read_tr(at + 8 * (D + 8)));
-          }
+        for (int db = 0; db < DB; ++db) {
+          const bf16* at = ab + 16 * ks * (D + 8) + tr_step<D>(db);
+          a[db] = cat(lds_read_tr(at), lds_read_tr(at + 8 * (D + 8)));
+        }
       };
       auto acc_a = [&](bf16x8 b0, bf16x8 b1) {
 #pragma unroll
-        for (int db = 0; db < DB; ++db)
+        for (int db = 0; db < DB; ++db) acc[db] = mfma32(a0[db], b0, acc[db]);
 #pragma unroll
-          for (int ks = 0; ks < 2; ++ks) acc[db] = mfma32(a[db][ks], ks ? b1 : b0, acc[db]);
+        for (int db = 0; db < DB; ++db) acc[db] = mfma32(a1[db], b1, acc[db]);
       };
-      for (int it = 0; it < n_it; ++it) {
-        const int t = it - 2;
-        if (fl3) {
-          acc_a(dSop[t & 1][grp_k][0][lane], dSop[t & 1][grp_k][1][lane]);
-          if (dSlo[t & 1][grp_k]) acc_a(dSop[t & 1][grp_k][2][lane], dSop[t & 1][grp_k][3][lane]);
+      for (int c0 = 0; c0 < total; c0 += kDkdvChunk) {
+        const int np = begin_chunk(c0);
+        if (!np) continue;
+        fl3 = 0;
+        for (int k = -1; k < np + 2; ++k) {
+          const int t = k - 2;
+          if (fl3) {
+            // the dS operands first: the first k-step's MFMAs wait only for them
+            const bf16x8 b0 = dSop[t & 1][grp_k][0][lane], b1 = dSop[t & 1][grp_k][1][lane];
+            load_a(t, 1, a1);
+            acc_a(b0, b1);
+            if (dSlo[t & 1][grp_k]) acc_a(dSop[t & 1][grp_k][2][lane], dSop[t & 1][grp_k][3][lane]);
+          }
+          const int tn = k - 1;   // the tile of the next step
+          fl3 = (tn >= 0 && tn < np) ? Pflag[tn % 3][grp_k] : 0;
+          if (fl3) load_a(tn, 0, a0);
+          __syncthreads();
         }
-        const int tn = it - 1;   // the tile of the next iteration
-        fl3 = (tn >= 0 && tn < total) ? Pflag[tn % 3][grp_k] : 0;
-        if (fl3) load_a(tn);
-        __syncthreads();
       }
     }
     // dV = sum P^T dO (role 1), dK = scale * sum dS^T Q (role 3); lane (h, c)
@@ -511,7 +590,6 @@ __global__ __launch_bounds__(1024) void mala_bwd_dkdv_kernel(BwdParams p) {
         }
     }
   }
-  if (p.counters && tid == 0) atomicAdd(&p.counters[kCntVTiles], (unsigned long long)total);
 }
 
 // Offline test of one tile in the transposed C layout of the dQ pass: the lane
@@ -605,8 +683,19 @@ __global__ __launch_bounds__(kDqWaves * 64) void mala_bwd_dq_kernel(BwdParams p)
   unsigned n_legal = 0, n_ret = 0;
   unsigned long long hsum = 0;   // fingerprints of the retained tiles
   int cnt_row = 0;   // retained tiles in which row qrow has a legal key
+  // The decisions for the key-major pass: one byte per 128-key block of this
+  // wavefront's query tile and head, bit j % 4 for key tile j, the blocks contiguous
+  // (mask_index).  A stage covers key tiles 2t and 2t + 1, half of block t / 2; the
+  // block's byte is complete after its lower stage (t even) and goes into lane
+  // (t / 2) % 64 of pack; after block 64 m the group of 64 blocks goes out in one
+  // coalesced store (the first group only up to the workgroup's top block).  Every
+  // block up to the diagonal is written (blocks above this wavefront's diagonal get
+  // zero), so the buffer needs no clearing.
+  uint8_t* mrow = p.mask + mask_index(p, mask_row0(p, b, sg) + q0w / kBq, hq, 0);
+  const bool mwave = q0w < Nq;               // this wavefront has query rows
+  int nib = 0, stored = 0;
+  uint32_t pack = 0;
   float fdq = 0.f;   // this row's sum of |dS| in tiles run without the lo term
-
   // K / V stages move with buffer loads straight into LDS (keys past the end read
   // as zeros): wavefront w issues the 64-position loads w, w + 8, ... of each slot.
   // The loads of stage t - 1 overlap the compute of stage t (untracked form) and
@@ -663,7 +752,9 @@ __global__ __launch_bounds__(kDqWaves * 64) void mala_bwd_dq_kernel(BwdParams p)
       float sv[16];
       const bool dem = need_mask ? offline_test_t<true>(s, p.scale2, kmax, klim, thr, sv)
                                  : offline_test_t<false>(s, p.scale2, kmax, klim, thr, sv);
-      if (!wave_any(dem)) continue;
+      const bool ret = wave_any(dem);
+      nib |= (ret ? 1 : 0) << (j & 3);
+      if (!ret) continue;
       ++n_ret;
       if (p.counters) hsum += tile_hash(b, hq, q0w / kBq, j);
       cnt_row += (row_valid && kb <= (long)qrow + off) ? 1 : 0;
@@ -715,7 +806,25 @@ __global__ __launch_bounds__(kDqWaves * 64) void mala_bwd_dq_kernel(BwdParams p)
       }
     }
     __builtin_amdgcn_s_setprio(0);
-    wait_vm();
+    if (!(t & 1) && mwave) {
+      // block t / 2 is complete
+      const int blk = t >> 1;
+      if (lane == (blk & 63)) pack = (uint32_t)nib;
+      nib = 0;
+      if (!(blk & 63)) {
+        // the group's blocks blk .. blk + 63, up to the workgroup's top block ttop / 2
+        if (lane <= (ttop >> 1) - blk) mrow[blk + lane] = (uint8_t)pack;
+        stored = 1;
+      }
+    }
+    // the next stage's loads have landed; a decision store issued in this stage
+    // (issued after those loads: vector memory operations complete in order) may
+    // still be in flight
+    if (stored)
+      wait_vm_keep<1>();
+    else
+      wait_vm();
+    stored = 0;
     __syncthreads();
   }
 
@@ -743,12 +852,13 @@ __global__ __launch_bounds__(kDqWaves * 64) void mala_bwd_dq_kernel(BwdParams p)
 hipError_t launch_bwd(const BwdParams& p, int D, hipStream_t st) {
   dim3 grid_kv((unsigned)p.nkblk * p.B * p.Hkv), block_kv(1024);
   dim3 grid_q((unsigned)p.nqblk * p.B * p.Hq), block_q(kDqWaves * 64);
+  // the dQ pass first: it records the tile decisions that the key-major pass follows
   if (D == 128) {
-    hipLaunchKernelGGL(mala_bwd_dkdv_kernel<128>, grid_kv, block_kv, 0, st, p);
     hipLaunchKernelGGL(mala_bwd_dq_kernel<128>, grid_q, block_q, 0, st, p);
+    hipLaunchKernelGGL(mala_bwd_dkdv_kernel<128>, grid_kv, block_kv, 0, st, p);
   } else {
-    hipLaunchKernelGGL(mala_bwd_dkdv_kernel<64>, grid_kv, block_kv, 0, st, p);
     hipLaunchKernelGGL(mala_bwd_dq_kernel<64>, grid_q, block_q, 0, st, p);
+    hipLaunchKernelGGL(mala_bwd_dkdv_kernel<64>, grid_kv, block_kv, 0, st, p);
   }
   return hipGetLastError();
 }

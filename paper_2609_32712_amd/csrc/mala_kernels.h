@@ -17,6 +17,7 @@ constexpr int kDqWaves = 8;                  // wavefronts per dQ workgroup (2 p
 constexpr int kDqRows = kDqWaves * kBq;      // 256 query rows per workgroup
 constexpr int kFwdStage = 64;                // keys per K/V stage in LDS (forward and dQ)
 constexpr int kBwdKeys = 128;                // keys per dK/dV workgroup (4 key groups x kBk)
+constexpr int kDkdvChunk = 4096;             // sweep iterations the dK/dV kernel compacts at once
 // Budgets of the low bf16 term in the backward.  P and dS enter the MFMAs as
 // hi + lo (two bf16 terms, 2^-16 relative).  The lo term of a tile is left out of
 // dV (P) or dK (dS) while, for every key of the tile, the P mass or the sum of |dS|
@@ -128,7 +129,24 @@ struct BwdParams {
   float scale, scale2, log2tau;
   int nkblk;           // ceil(Nk / kBwdKeys) (packed: ceil(max_len_k / kBwdKeys))
   int nqblk;           // ceil(Nq / kDqRows) (packed: ceil(max_len / kDqRows))
+  // Tile decisions of the dQ pass for the key-major pass: one byte per (query-tile row,
+  // query head, 128-key block) at mask_index, bit j % 4 for the block's key tile j.
+  uint8_t* mask;
+  int mask_rows;       // query-tile rows: B ceil(Nq / kBq) (packed: total_q / kBq + B)
 };
+
+// Byte of the decisions of query-tile row `row` (mask_row0 + query tile), query head
+// hq and key block jb: the key blocks of one row and head are contiguous.
+__device__ __forceinline__ size_t mask_index(const BwdParams& p, int row, int hq, int jb) {
+  return ((size_t)row * p.Hq + hq) * p.nkblk + jb;
+}
+
+// First query-tile row of sequence b in the decision bytes: b ceil(Nq / kBq) for the
+// fixed-length layout; floor(q0 / kBq) + b for packed sequences starting at row q0
+// (disjoint ranges: sequence b has at most ceil(n_b / kBq) tiles).
+__device__ __forceinline__ int mask_row0(const BwdParams& p, int b, const Seg& sg) {
+  return p.cu ? (int)(sg.qb / kBq) + b : b * ((p.Nq + kBq - 1) / kBq);
+}
 
 struct DecParams {
   const __bf16* q;

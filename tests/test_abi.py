@@ -51,7 +51,9 @@ def test_geometry(lib):
 
 
 def test_workspace_sizes(lib):
-    assert mala.mala_bwd_workspace_size(1, 8, 2, 1000, 1000, 128) >= 4 * 8 * 1000
+    # D_q (B Hq Nq floats) and one decision byte per query tile, head and 128-key block
+    assert mala.mala_bwd_workspace_size(1, 8, 2, 1000, 1000, 128) >= 4 * 8 * 1000 + 8 * 32 * 8
+    assert mala.mala_bwd_workspace_size(1, 8, 2, 131072, 131072, 128) >= 8 * 4096 * 1024
     assert mala.mala_bwd_workspace_size(0, 8, 2, 1000, 1000, 128) == 0
     assert mala.mala_decode_workspace_size(16, 32, 128, 8) >= 16 * 32 * 8 * 130 * 4
     assert mala.mala_decode_workspace_size(16, 32, 96, 8) == 0
@@ -143,6 +145,11 @@ def test_varlen_argument_validation(lib):
                              16, 16, 2, 1, 64, 0.125, 0.0, mala.OUT_F32, mala.OUT_F32, None)
     assert st == mala.MALA_ERR_WORKSPACE
     assert lib.mala_bwd_workspace_size(1, 2, 1, 16, 16, 64) > 8
+    # the varlen workspace: D_q for every row and the decision bytes of each sequence's
+    # query tiles (up to total / 32 + num_seqs tile rows) per head and 128-key block
+    dq_bytes = 4 * 2 * 1000
+    assert lib.mala_bwd_varlen_workspace_size(3, 600, 1000, 2, 1, 64) >= dq_bytes + 2 * 5 * (31 + 3)
+    assert lib.mala_bwd_varlen_workspace_size(0, 600, 1000, 2, 1, 64) == 0
 
 
 def test_python_binding_requires_device_tensors():

@@ -39,6 +39,10 @@ TRAIN_CASES = {
                                        local=4.0), over={}),
     "gqa_d128_ragged": dict(spec=dict(kind="train", B=2, Hq=4, Hkv=2, N=700, D=128, beta=2.5,
                                       local=2.0), over={}),
+    # 16 query heads per KV head: the key-major sweep of the early key blocks holds 375
+    # query tiles x 16 heads = 6000 iterations, more than one compaction chunk (4096)
+    "gqa16_chunks": dict(spec=dict(kind="train", B=1, Hq=16, Hkv=1, N=12000, D=128, beta=2.0,
+                                   local=2.0), over={}),
     "tiny_d128": dict(spec=dict(kind="train", B=1, Hq=2, Hkv=2, N=37, D=128, beta=2.0, local=1.0),
                       over={}),
     "single_row_d64": dict(spec=dict(kind="train", B=1, Hq=1, Hkv=1, N=1, D=64, beta=1.0), over={}),
@@ -55,6 +59,8 @@ TRAIN_TAUS = {
     # tau = 1 would put the only tile exactly on the threshold (P = 1 = tau / L):
     # 0.5 retains and 1.5 skips it in the backward, both unambiguously
     "single_row_d64": (0.0, 0.5, 1.5),
+    # 1e30: every backward tile is skipped (empty compaction chunks, zero gradients)
+    "gqa16_chunks": (1e-3, 1.0, 1e30),
     "lm_d128_ragged": (0.0, 1e-4, 1.0),
 }
 
