@@ -147,6 +147,17 @@ def train_flops(cnt_f, cnt_b, D, bq, bk):
     return float(fwd), float(bwd)
 
 
+def dense_do_tiles(B, Hq, Hkv, N, bq=32, bwd_keys=128):
+    """The dO tiles the key-major backward pass would load if it retained every tile
+    (N_q = N_k = N): a workgroup of bwd_keys keys of one KV head visits every query
+    tile of its GQA group's heads from its own first key on.  The denominator of the
+    loaded percentage."""
+    d = 0
+    for k0 in range(0, N, bwd_keys):
+        d += (N + bq - 1) // bq - k0 // bq
+    return B * Hkv * (Hq // Hkv) * d
+
+
 def cpu_model():
     """The host CPU's model name (first processor in /proc/cpuinfo), or None."""
     try:
@@ -202,6 +213,7 @@ def train_config(cfg_id, taus, reps, warmup, supp_taus=(), supp=None, memory=Tru
     de_f, de_b = dense_equivalent_flops(w.B, w.Hq, w.N, w.D)
     rows = w.B * w.Hq * w.N
     pct = lambda a, b_: round(100.0 * float(a) / max(1.0, float(b_)), 3)
+    do_dense = dense_do_tiles(w.B, w.Hq, w.Hkv, w.N)
     res = {}
     for t_ in (0.0,) + tuple(x for x in taus if x != 0.0):
         n_, w_ = supp if t_ in supp_taus else (reps, warmup)
@@ -219,7 +231,7 @@ def train_config(cfg_id, taus, reps, warmup, supp_taus=(), supp=None, memory=Tru
             "retained_tiles_pct_fwd": pct(cf[1], cf[0]),
             "retained_tiles_pct_bwd": pct(cb[1], cb[0]),
             "v_tiles_needed_pct_fwd": pct(cf[5], cf[2]),
-            "do_tiles_needed_pct_bwd": pct(cb[5], cb[2]),
+            "do_tiles_loaded_pct_bwd": pct(cb[2], do_dense),
             "mean_slots_per_query_fwd": round(float(cf[3]) / rows, 1),
             "mean_slots_per_query_bwd": round(float(cb[3]) / rows, 1),
             "executed_tflops_fwd": round(fl_f / (f[0] * 1e-3) / 1e12, 1),
@@ -849,6 +861,7 @@ def main():
     dec_traffic = decode_traffic_from_profiles(
         os.path.join(ROOT, "paper_2609_32712_amd", "csrc", "mala_decode.hip"))
     pct = lambda a, b_: round(100.0 * float(a) / max(1.0, float(b_)), 3)
+    do_dense = dense_do_tiles(w.B, w.Hq, w.Hkv, w.N)
 
     detail = {
         "128k": {
@@ -860,7 +873,7 @@ def main():
             "retained_tiles_pct_fwd": pct(rt["cf"][1], rt["cf"][0]),
             "retained_tiles_pct_bwd": pct(rt["cb"][1], rt["cb"][0]),
             "v_tiles_needed_pct_fwd": pct(rt["cf"][5], rt["cf"][2]),
-            "do_tiles_needed_pct_bwd": pct(rt["cb"][5], rt["cb"][2]),
+            "do_tiles_loaded_pct_bwd": pct(rt["cb"][2], do_dense),
             "mean_slots_per_query_fwd": round(float(rt["cf"][3]) / (w.B * w.Hq * w.N), 1),
             "mean_slots_per_query_bwd": round(float(rt["cb"][3]) / (w.B * w.Hq * w.N), 1),
             "executed_tflops_fwd": round(fl_f / (rt["fwd"][0] * 1e-3) / 1e12, 1),
@@ -900,7 +913,7 @@ def main():
             "retained_tiles_pct_fwd": pct(cf1[1], cf1[0]),
             "retained_tiles_pct_bwd": pct(cb1[1], cb1[0]),
             "v_tiles_needed_pct_fwd": pct(cf1[5], cf1[2]),
-            "do_tiles_needed_pct_bwd": pct(cb1[5], cb1[2]),
+            "do_tiles_loaded_pct_bwd": pct(cb1[2], do_dense),
             "retained_head_tiles_pct_decode": pct(cd1[1], cd1[0]),
             "v_tiles_fetched_pct_decode": pct(cd1[2], k_tiles),
             "v_tiles_consumed_pct_decode": pct(cd1[5], k_tiles),

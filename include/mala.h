@@ -151,7 +151,13 @@ int mala_fwd(const void* q, const void* k, const void* v, void* o, float* lse,
  * D_q = rowsum(O_q * dO_q) vector of Algorithm 2 (B Hq Nq floats) and the tile
  * decisions that the query-major dQ pass hands to the key-major dK/dV pass (one byte
  * per query tile of B_q rows, query head and block of 128 keys: B Hq ceil(Nq / B_q)
- * ceil(Nk / 128) bytes, ~32 MB at B = 1, Hq = 8, Nq = Nk = 131072). */
+ * ceil(Nk / 128) bytes, ~32 MB at B = 1, Hq = 8, Nq = Nk = 131072).  Shapes with
+ * fewer than 1024 key blocks in all (B Hkv ceil(Nk / 128)) run each key block's
+ * sweep over the query tiles in up to P parts of at least 1024 (query tile, head)
+ * iterations on workgroups of their own, so that one long sweep does not set the
+ * time alone; the workspace then also holds the parts' fp32 dK and dV sums
+ * (P x 2 x B Hkv Nk D floats, ~268 MB at B = 1, Hq = 8, Hkv = 2, Nq = Nk = 32768,
+ * P = 4), which a last pass adds in part order.  0 for an invalid shape. */
 size_t mala_bwd_workspace_size(int B, int Hq, int Hkv, int Nq, int Nk, int D);
 
 /* Bytes of device workspace mala_bwd_varlen needs: Hq total_q floats of D_q and

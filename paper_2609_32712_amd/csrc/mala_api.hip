@@ -37,10 +37,40 @@ size_t dvec_bytes(long rows) { return round_up((size_t)rows * sizeof(float), 256
 int mask_rows(bool packed, int B, int Nq) {
   return packed ? Nq / mala::kBq + B : B * ((Nq + mala::kBq - 1) / mala::kBq);
 }
-size_t bwd_workspace(bool packed, int B, int Hq, int Hkv, int Nq, int max_k) {
-  const long rows = packed ? (long)Hq * Nq : (long)B * Hq * Nq;
+size_t mask_bytes(bool packed, int B, int Hq, int Nq, int max_k) {
   const size_t nkblk = (size_t)(max_k + mala::kBwdKeys - 1) / mala::kBwdKeys;
-  return dvec_bytes(rows) + round_up((size_t)Hq * nkblk * mask_rows(packed, B, Nq), 256);
+  return round_up((size_t)Hq * nkblk * mask_rows(packed, B, Nq), 256);
+}
+// Parts of the dK/dV sweeps (fixed-length batches): one per sweep when the key
+// blocks alone give kDkdvSplitGroups workgroups; otherwise parts of the smallest
+// power of two >= kDkdvPartMin iterations that gives at most ~kDkdvSplitGroups
+// parts over all sweeps, so that a long sweep (the first key blocks', or one that
+// retains every tile) no longer sets the kernel's time alone.
+void dkdv_split(int B, int Hq, int Hkv, int Nq, int Nk, int* psize, int* nparts) {
+  const int grp = Hq / Hkv, nkblk = (Nk + mala::kBwdKeys - 1) / mala::kBwdKeys;
+  *psize = 1 << 30;
+  *nparts = 1;
+  if ((long)nkblk * B * Hkv >= mala::kDkdvSplitGroups) return;
+  long total = 0;
+  for (int j = 0; j < nkblk; ++j) total += mala::dkdv_iterations(Nq, Nk, j * mala::kBwdKeys, grp);
+  total *= (long)B * Hkv;
+  const int longest = mala::dkdv_iterations(Nq, Nk, 0, grp);
+  long ps = mala::kDkdvPartMin;
+  while (ps * 2 * mala::kDkdvSplitGroups <= total) ps *= 2;
+  if (ps >= longest) return;
+  *psize = (int)ps;
+  *nparts = (int)((longest + ps - 1) / ps);
+}
+// fp32 partial dV and dK of every part of the split sweeps (fixed-length batches)
+size_t part_bytes(int B, int Hq, int Hkv, int Nq, int Nk, int D) {
+  int psize, nparts;
+  dkdv_split(B, Hq, Hkv, Nq, Nk, &psize, &nparts);
+  return nparts > 1 ? round_up((size_t)nparts * 2 * B * Hkv * Nk * D * sizeof(float), 256) : 0;
+}
+size_t bwd_workspace(bool packed, int B, int Hq, int Hkv, int Nq, int max_k, int D) {
+  const long rows = packed ? (long)Hq * Nq : (long)B * Hq * Nq;
+  return dvec_bytes(rows) + mask_bytes(packed, B, Hq, Nq, max_k) +
+         (packed ? 0 : part_bytes(B, Hq, Hkv, Nq, max_k, D));
 }
 
 int check_common(int B, int Hq, int Hkv, int Nq, int Nk, int D, int causal, float scale, float tau) {
@@ -177,6 +207,13 @@ int run_bwd(const void* q, const void* k, const void* v, const Packed& pk,
   p.nqblk = (p.max_len + mala::kDqRows - 1) / mala::kDqRows;
   p.mask = (uint8_t*)workspace + dvec_bytes(rows);
   p.mask_rows = mask_rows(pk.cu != nullptr, B, Nq);
+  p.psize = 1 << 30;
+  p.nparts = 1;
+  p.part = nullptr;
+  if (!pk.cu) {
+    dkdv_split(B, Hq, Hkv, Nq, Nk, &p.psize, &p.nparts);
+    p.part = (float*)((char*)p.mask + mask_bytes(false, B, Hq, Nq, Nk));
+  }
   if ((e = mala::launch_bwd(p, D, s)) != hipSuccess) return hip_fail(e, "mala_bwd: kernel launch");
   return MALA_OK;
 }
@@ -319,16 +356,16 @@ int mala_fwd_varlen(const void* q, const void* k, const void* v, const int32_t* 
 }
 
 size_t mala_bwd_workspace_size(int B, int Hq, int Hkv, int Nq, int Nk, int D) {
-  (void)D;
-  if (B <= 0 || Hq <= 0 || Hkv <= 0 || Nq <= 0 || Nk <= 0) return 0;
-  return bwd_workspace(false, B, Hq, Hkv, Nq, Nk);
+  if (B <= 0 || Hq <= 0 || Hkv <= 0 || Nq <= 0 || Nk <= 0 || Hq % Hkv || Nq > Nk ||
+      (D != 64 && D != 128))
+    return 0;
+  return bwd_workspace(false, B, Hq, Hkv, Nq, Nk, D);
 }
 
 size_t mala_bwd_varlen_workspace_size(int num_seqs, int max_seqlen_k, int total_q, int Hq,
                                       int Hkv, int D) {
-  (void)D;
   if (num_seqs <= 0 || max_seqlen_k <= 0 || total_q <= 0 || Hq <= 0 || Hkv <= 0) return 0;
-  return bwd_workspace(true, num_seqs, Hq, Hkv, total_q, max_seqlen_k);
+  return bwd_workspace(true, num_seqs, Hq, Hkv, total_q, max_seqlen_k, D);
 }
 
 int mala_bwd(const void* q, const void* k, const void* v, const void* o, const float* lse,

@@ -25,6 +25,8 @@
 // offline test sees the key-major kernel's scores.  dQ needs no atomics and is
 // bitwise reproducible.
 // A skipped tile costs its QK MFMAs and the test in both kernels.
+#include <algorithm>
+
 #include "mala_device.h"
 #include "mala_kernels.h"
 
@@ -227,8 +229,9 @@ __global__ __launch_bounds__(1024) void mala_bwd_dkdv_kernel(BwdParams p) {
   // lane bases of the LDS tile reads: operand rows (row c) and transposed rows
   const int rdo = rd_base<D>(c, h), tro = tr_base<D>(4 * h + (t16 >> 2), G & 1, t16);
   const int BHk = p.B * p.Hkv;
+  const int part = blockIdx.x / (p.nkblk * BHk);   // part of the sweep (split sweeps)
   const int bhk = blockIdx.x % BHk;
-  const int kblk = blockIdx.x / BHk;       // ascending: the longest key blocks first
+  const int kblk = (blockIdx.x / BHk) % p.nkblk;   // ascending: the longest key blocks first
   const int b = bhk / p.Hkv, hkv = bhk % p.Hkv, grp = p.Hq / p.Hkv;
   const Seg sg = seq_slice(p, b);
   const int Nq = sg.Nq, Nk = sg.Nk;
@@ -239,11 +242,15 @@ __global__ __launch_bounds__(1024) void mala_bwd_dkdv_kernel(BwdParams p) {
   const int kw = kb0 + grp_k * kBk;        // first key of this wavefront's decision tile
   const int key = kw + c;                  // this lane's key (C-layout column)
 
-  const long first_q = (long)kb0 - off;
-  const int qi_start = first_q <= 0 ? 0 : (int)(first_q / kBq);
   const int nqt = (Nq + kBq - 1) / kBq;
-  const int per_head = nqt - qi_start;     // >= 1: key kb0 < Nk is visible to row Nq - 1
-  const int total = grp * per_head;
+  // >= grp: key kb0 < Nk is visible to row Nq - 1
+  const int total = dkdv_iterations(Nq, Nk, kb0, grp);
+  // this workgroup's part of the sweep; the parts of a split sweep share the lo-term
+  // budgets of the key (each part keeps 1 / parts of them), so the error bound of
+  // the whole sweep holds
+  const int it0 = part * p.psize, it1 = min(total, it0 + p.psize);
+  if (it0 >= total) return;
+  const float budget_share = 1.f / (float)((total + p.psize - 1) / p.psize);
 
   // Query tiles are swept from the last one down to the block's diagonal, the
   // heads of the group innermost (iteration it: tile nqt - 1 - it / grp, head
@@ -324,7 +331,7 @@ __global__ __launch_bounds__(1024) void mala_bwd_dkdv_kernel(BwdParams p) {
 #pragma unroll
       for (int u = 0; u < PER; ++u) {
         const int it = c0 + PER * t2 + u;
-        dec[u] = it < total ? decisions(it) : 0;
+        dec[u] = it < it1 ? decisions(it) : 0;
         cnt += dec[u] != 0;
       }
       int x = cnt;   // inclusive scan over the wavefront
@@ -367,7 +374,7 @@ __global__ __launch_bounds__(1024) void mala_bwd_dkdv_kernel(BwdParams p) {
       float fdv = 0.f;   // P mass of this lane's key in tiles run without the lo term
       unsigned n_ret_kv = 0;          // statistics: processed tiles whose test this pass confirms
       unsigned long long hsum = 0;    // and their fingerprints
-      for (int c0 = 0; c0 < total; c0 += kDkdvChunk) {
+      for (int c0 = it0; c0 < it1; c0 += kDkdvChunk) {
         const int np = begin_chunk(c0);
         if (!np) continue;
         // the list entry of the next step, read during this one (the step's closing
@@ -412,7 +419,7 @@ __global__ __launch_bounds__(1024) void mala_bwd_dkdv_kernel(BwdParams p) {
 #pragma unroll
               for (int r = 0; r < 16; ++r) ps += sv[r];
               const float fv_new = fdv + halves_sum(ps);
-              with_lo = wave_any(fv_new > kLoMassDv);
+              with_lo = wave_any(fv_new > kLoMassDv * budget_share);
               if (!with_lo) fdv = fv_new;
             }
             if (lane == 0) Pflag[k % 3][grp_k] = ret ? (with_lo ? 3 : 1) : 0;
@@ -426,7 +433,7 @@ __global__ __launch_bounds__(1024) void mala_bwd_dkdv_kernel(BwdParams p) {
       }
     } else {
       float fdk = 0.f;   // sum of |dS| of this lane's key in tiles run without the lo term
-      for (int c0 = 0; c0 < total; c0 += kDkdvChunk) {
+      for (int c0 = it0; c0 < it1; c0 += kDkdvChunk) {
         const int np = begin_chunk(c0);
         if (!np) continue;
         for (int k = -1; k < np + 2; ++k) {
@@ -455,7 +462,7 @@ __global__ __launch_bounds__(1024) void mala_bwd_dkdv_kernel(BwdParams p) {
             for (int r = 0; r < 16; ++r) as += fabsf(ds[r]);
             const float as_key = halves_sum(as);
             const float fk_new = fdk + as_key;
-            const bool with_lo = wave_any(fk_new > kLoMassDk || as_key > kLoTileDk);
+            const bool with_lo = wave_any(fk_new > kLoMassDk * budget_share || as_key > kLoTileDk);
             if (!with_lo) fdk = fk_new;
             bf16x8 xh[2], xl[2];
             if (with_lo) {
@@ -495,7 +502,7 @@ __global__ __launch_bounds__(1024) void mala_bwd_dkdv_kernel(BwdParams p) {
     };
     if (role == 1) {
       unsigned n_do = 0;   // statistics: dO tiles staged (some key group retained the tile)
-      for (int c0 = 0; c0 < total; c0 += kDkdvChunk) {
+      for (int c0 = it0; c0 < it1; c0 += kDkdvChunk) {
         const int np = begin_chunk(c0);
         if (!np) continue;
         n_do += np;
@@ -554,7 +561,7 @@ __global__ __launch_bounds__(1024) void mala_bwd_dkdv_kernel(BwdParams p) {
 #pragma unroll
         for (int db = 0; db < DB; ++db) acc[db] = mfma32(a1[db], b1, acc[db]);
       };
-      for (int c0 = 0; c0 < total; c0 += kDkdvChunk) {
+      for (int c0 = it0; c0 < it1; c0 += kDkdvChunk) {
         const int np = begin_chunk(c0);
         if (!np) continue;
         fl3 = 0;
@@ -576,9 +583,13 @@ __global__ __launch_bounds__(1024) void mala_bwd_dkdv_kernel(BwdParams p) {
     }
     // dV = sum P^T dO (role 1), dK = scale * sum dS^T Q (role 3); lane (h, c)
     // holds key kw + c
+    // (split sweeps: this part's fp32 sums to its slots of the partial buffer)
     if (key < Nk) {
       const float f = role == 1 ? 1.f : p.scale;
-      void* dst = role == 1 ? p.dv : p.dk;
+      const bool split = p.nparts > 1;
+      void* dst = split ? (void*)(p.part + (size_t)(2 * part + (role == 1 ? 0 : 1)) *
+                                               ((size_t)p.B * p.Hkv * p.Nk) * D)
+                        : (role == 1 ? p.dv : p.dk);
       const long krow = (kbase + key) * D;
 #pragma unroll
       for (int db = 0; db < DB; ++db)
@@ -586,7 +597,7 @@ __global__ __launch_bounds__(1024) void mala_bwd_dkdv_kernel(BwdParams p) {
         for (int g = 0; g < 4; ++g) {
           f32x4 v4 = {acc[db][4 * g] * f, acc[db][4 * g + 1] * f, acc[db][4 * g + 2] * f,
                       acc[db][4 * g + 3] * f};
-          store_out4(dst, krow + 32 * db + 8 * g + 4 * h, v4, p.grad_bf16);
+          store_out4(dst, krow + 32 * db + 8 * g + 4 * h, v4, split ? 0 : p.grad_bf16);
         }
     }
   }
@@ -849,16 +860,45 @@ __global__ __launch_bounds__(kDqWaves * 64) void mala_bwd_dq_kernel(BwdParams p)
   }
 }
 
+// Sum of the parts of split dK/dV sweeps in part order (fixed-length batches): one
+// thread per four columns of a K-shaped row; a row's key block has
+// ceil(iterations / psize) parts.
+template <int D>
+__global__ __launch_bounds__(256) void mala_bwd_dkdv_reduce_kernel(BwdParams p) {
+  const long rows = (long)p.B * p.Hkv * p.Nk;
+  const long n4 = rows * (D / 4);
+  const size_t slot = (size_t)rows * D;
+  const int grp = p.Hq / p.Hkv;
+  for (long i = (long)blockIdx.x * blockDim.x + threadIdx.x; i < n4;
+       i += (long)gridDim.x * blockDim.x) {
+    const long row = i / (D / 4);
+    const long e = row * D + (i % (D / 4)) * 4;
+    const int kb0 = (int)(row % p.Nk) / kBwdKeys * kBwdKeys;
+    const int np = (dkdv_iterations(p.Nq, p.Nk, kb0, grp) + p.psize - 1) / p.psize;
+    f32x4 sv = {0.f, 0.f, 0.f, 0.f}, sk = {0.f, 0.f, 0.f, 0.f};
+    for (int q = 0; q < np; ++q) {
+      sv += *reinterpret_cast<const f32x4*>(p.part + (size_t)(2 * q) * slot + e);
+      sk += *reinterpret_cast<const f32x4*>(p.part + (size_t)(2 * q + 1) * slot + e);
+    }
+    store_out4(p.dv, e, sv, p.grad_bf16);
+    store_out4(p.dk, e, sk, p.grad_bf16);
+  }
+}
+
 hipError_t launch_bwd(const BwdParams& p, int D, hipStream_t st) {
-  dim3 grid_kv((unsigned)p.nkblk * p.B * p.Hkv), block_kv(1024);
+  dim3 grid_kv((unsigned)p.nkblk * p.B * p.Hkv * p.nparts), block_kv(1024);
   dim3 grid_q((unsigned)p.nqblk * p.B * p.Hq), block_q(kDqWaves * 64);
+  const long n4 = (long)p.B * p.Hkv * p.Nk * (D / 4);
+  dim3 grid_r((unsigned)std::min<long>((n4 + 255) / 256, 8192));
   // the dQ pass first: it records the tile decisions that the key-major pass follows
   if (D == 128) {
     hipLaunchKernelGGL(mala_bwd_dq_kernel<128>, grid_q, block_q, 0, st, p);
     hipLaunchKernelGGL(mala_bwd_dkdv_kernel<128>, grid_kv, block_kv, 0, st, p);
+    if (p.nparts > 1) hipLaunchKernelGGL(mala_bwd_dkdv_reduce_kernel<128>, grid_r, dim3(256), 0, st, p);
   } else {
     hipLaunchKernelGGL(mala_bwd_dq_kernel<64>, grid_q, block_q, 0, st, p);
     hipLaunchKernelGGL(mala_bwd_dkdv_kernel<64>, grid_kv, block_kv, 0, st, p);
+    if (p.nparts > 1) hipLaunchKernelGGL(mala_bwd_dkdv_reduce_kernel<64>, grid_r, dim3(256), 0, st, p);
   }
   return hipGetLastError();
 }

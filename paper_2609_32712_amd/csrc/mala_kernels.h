@@ -18,6 +18,11 @@ constexpr int kDqRows = kDqWaves * kBq;      // 256 query rows per workgroup
 constexpr int kFwdStage = 64;                // keys per K/V stage in LDS (forward and dQ)
 constexpr int kBwdKeys = 128;                // keys per dK/dV workgroup (4 key groups x kBk)
 constexpr int kDkdvChunk = 4096;             // sweep iterations the dK/dV kernel compacts at once
+// Below kDkdvSplitGroups key-block workgroups (batch x KV heads x key blocks) the
+// dK/dV sweeps are split into parts of at least kDkdvPartMin iterations, run by
+// workgroups of their own, and summed by a reduction pass (fixed-length batches).
+constexpr int kDkdvSplitGroups = 1024;
+constexpr int kDkdvPartMin = 1024;
 // Budgets of the low bf16 term in the backward.  P and dS enter the MFMAs as
 // hi + lo (two bf16 terms, 2^-16 relative).  The lo term of a tile is left out of
 // dV (P) or dK (dS) while, for every key of the tile, the P mass or the sum of |dS|
@@ -133,7 +138,21 @@ struct BwdParams {
   // query head, 128-key block) at mask_index, bit j % 4 for the block's key tile j.
   uint8_t* mask;
   int mask_rows;       // query-tile rows: B ceil(Nq / kBq) (packed: total_q / kBq + B)
+  // Split key-block sweeps: part p of a block takes iterations [p psize, (p + 1) psize)
+  // and, when nparts > 1, writes its fp32 dV and dK sums to part[(2 p + {0, 1}) rows + row]
+  // (rows = B Hkv Nk rows of D floats), which the reduction pass adds up in order.
+  int psize, nparts;
+  float* part;
 };
+
+// Iterations of the dK/dV sweep of the key block starting at key kb0 of a sequence
+// (Nq query rows, the last aligned with the last of Nk keys): every (query tile, head
+// of the GQA group) from the last query tile down to the block's diagonal.
+__host__ __device__ inline int dkdv_iterations(int Nq, int Nk, int kb0, int grp) {
+  const long first_q = (long)kb0 - ((long)Nk - Nq);
+  const int qi_start = first_q <= 0 ? 0 : (int)(first_q / kBq);
+  return grp * ((Nq + kBq - 1) / kBq - qi_start);
+}
 
 // Byte of the decisions of query-tile row `row` (mask_row0 + query tile), query head
 // hq and key block jb: the key blocks of one row and head are contiguous.

@@ -135,3 +135,28 @@ def set_fingerprint(keep, b0=0):
     z = ((b + np.uint64(b0)) << np.uint64(52)) | (h << np.uint64(40)) | (i << np.uint64(20)) | j
     total = int(_splitmix64(z).sum(dtype=np.uint64)) if z.size else 0
     return total - (1 << 64) if total >= (1 << 63) else total
+
+
+def fwd_v_loads(keep, rows_per_group=256, bq=32):
+    """(workgroup, key tile) pairs of the forward in which some query tile of the
+    workgroup retains the key tile (the V tiles a retained tile uses), for an oracle
+    tile_keep [B, H, Tr, Tc]: a workgroup owns rows_per_group consecutive query rows
+    of one head."""
+    keep = np.asarray(keep) == 1
+    B, H, Tr, Tc = keep.shape
+    g = rows_per_group // bq
+    pad = (-Tr) % g
+    k = np.concatenate([keep, np.zeros((B, H, pad, Tc), bool)], axis=2) if pad else keep
+    return int(k.reshape(B, H, -1, g, Tc).any(axis=3).sum())
+
+
+def bwd_do_loads(keep, keys_per_group=128, bk=32):
+    """dO tiles the key-major backward pass loads for an oracle tile_keep [B, Hq, Tr,
+    Tc]: a workgroup owns keys_per_group consecutive keys of one KV head and loads a
+    query tile of a query head iff that tile retains one of its key tiles."""
+    keep = np.asarray(keep) == 1
+    B, H, Tr, Tc = keep.shape
+    g = keys_per_group // bk
+    pad = (-Tc) % g
+    k = np.concatenate([keep, np.zeros((B, H, Tr, pad), bool)], axis=3) if pad else keep
+    return int(k.reshape(B, H, Tr, -1, g).any(axis=4).sum())

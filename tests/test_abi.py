@@ -55,6 +55,13 @@ def test_workspace_sizes(lib):
     assert mala.mala_bwd_workspace_size(1, 8, 2, 1000, 1000, 128) >= 4 * 8 * 1000 + 8 * 32 * 8
     assert mala.mala_bwd_workspace_size(1, 8, 2, 131072, 131072, 128) >= 8 * 4096 * 1024
     assert mala.mala_bwd_workspace_size(0, 8, 2, 1000, 1000, 128) == 0
+    assert mala.mala_bwd_workspace_size(1, 8, 3, 1000, 1000, 128) == 0
+    assert mala.mala_bwd_workspace_size(1, 8, 2, 1000, 1000, 96) == 0
+    # few key-block workgroups (2 KV heads x 256 blocks): the sweeps run in 4 parts
+    # whose fp32 partial dV / dK the workspace holds; 2048 workgroups: no parts
+    assert mala.mala_bwd_workspace_size(1, 8, 2, 32768, 32768, 128) >= 4 * 2 * 2 * 32768 * 128 * 4
+    assert mala.mala_bwd_workspace_size(1, 8, 2, 131072, 131072, 128) < (
+        8 * 131072 * 4 + 8 * 4096 * 1024 + 2 ** 20)
     assert mala.mala_decode_workspace_size(16, 32, 128, 8) >= 16 * 32 * 8 * 130 * 4
     assert mala.mala_decode_workspace_size(16, 32, 96, 8) == 0
 

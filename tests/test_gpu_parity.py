@@ -11,7 +11,8 @@ import torch
 
 import oracle
 import paper_2609_32712_amd as mala
-from parity_util import (LSE_DIAG, TOL_MAX, assert_close, assert_counts, dev, host,
+from parity_util import (LSE_DIAG, TOL_MAX, assert_close, assert_counts, bwd_do_loads, dev,
+                         fwd_v_loads, host,
                          set_fingerprint, tie_masks, ties)
 from workloads import CONFIGS, Workload, bf16_to_f64
 
@@ -85,7 +86,8 @@ def _check_backward_passes_agree(cb):
     # equal retained counts and equal fingerprints of the retained tile sets
     assert cb[mala.CNT_RETAINED_KV] == cb[mala.CNT_RETAINED], cb
     assert cb[mala.CNT_SET_HASH_KV] == cb[mala.CNT_SET_HASH], cb
-    assert 0 <= cb[mala.CNT_V_NEEDED] <= cb[mala.CNT_V_TILES], cb
+    # the key-major pass loads a dO tile only for the query tiles it processes
+    assert cb[mala.CNT_V_NEEDED] == cb[mala.CNT_V_TILES] >= 0, cb
 
 
 def _check_train(w, q, k, v, do, tau):
@@ -122,9 +124,12 @@ def _check_train(w, q, k, v, do, tau):
     if not ex_f.any():
         assert cf[mala.CNT_RETAINED] == int((of["tile_keep"] == 1).sum())
         assert cf[mala.CNT_SET_HASH] == set_fingerprint(of["tile_keep"])
+        # (workgroup, key tile) pairs in which some wavefront retained the tile
+        assert cf[mala.CNT_V_NEEDED] == fwd_v_loads(of["tile_keep"])
     if not ex_b.any():
         assert cb[mala.CNT_RETAINED] == int((ob["tile_keep"] == 1).sum())
         assert cb[mala.CNT_SET_HASH] == set_fingerprint(ob["tile_keep"])
+        assert cb[mala.CNT_V_TILES] == bwd_do_loads(ob["tile_keep"])
     return ex_f.mean(), ex_b.mean()
 
 
@@ -349,11 +354,30 @@ def test_varlen_prefill_parity(tau):
     _check_backward_passes_agree(cb)
 
 
+def _dkdv_splits(B, Hq, Hkv, N, groups=1024, part_min=1024, keys=128, bq=32):
+    """Whether a fixed-length backward call of this causal shape splits its dK/dV
+    sweeps (the rule of the library's launch: fewer than `groups` key-block
+    workgroups, and a first sweep longer than the part size)."""
+    nkblk = -(-N // keys)
+    if nkblk * B * Hkv >= groups:
+        return False
+    grp, nqt = Hq // Hkv, -(-N // bq)
+    total = B * Hkv * sum(grp * (nqt - (j * keys) // bq) for j in range(nkblk))
+    ps = part_min
+    while ps * 2 * groups <= total:
+        ps *= 2
+    return ps < grp * nqt
+
+
 @pytest.mark.parametrize("tau", [1e-4, 1.0])
 def test_varlen_full_size_equals_per_sequence_calls(tau):
     # 32768 packed tokens of the language-model-like inputs: every sequence's
     # outputs equal, bit for bit, a fixed-length call on that sequence alone (the
-    # same tiles from the sequence's first row, the same arithmetic)
+    # same tiles from the sequence's first row, the same arithmetic).  Except dK and
+    # dV where the fixed-length call splits its key-block sweeps (few key-block
+    # workgroups): its parts add their sums afterwards and share the lo-term budgets,
+    # so the two agree within the sum of their error bounds (2^-8 x budget x the
+    # largest |dO| or scale |Q|, per path)
     lens = [16384, 8192, 4096, 1500, 1024, 1000, 500, 68, 4]
     w, cu, t = _packed(dict(CONFIGS[6], B=1), lens)
     scale = f32(w.scale)
@@ -371,10 +395,16 @@ def test_varlen_full_size_equals_per_sequence_calls(tau):
         torch.cuda.synchronize()
         pairs = (("o", g["o"], f1["o"]), ("lse", g["lse"], f1["lse"]),
                  ("row_tiles", g["row_tiles"], f1["row_tiles"]), ("dq", gb["dq"], b1["dq"]),
-                 ("dk", gb["dk"], b1["dk"]), ("dv", gb["dv"], b1["dv"]),
                  ("bwd row_tiles", gb["row_tiles"], b1["row_tiles"]))
         for name, a, ref in pairs:
             assert torch.equal(a[:, r], ref[0]), (b, name)
+        split = _dkdv_splits(1, w.Hq, w.Hkv, lens[b])
+        for name, a, ref in (("dk", gb["dk"], b1["dk"]), ("dv", gb["dv"], b1["dv"])):
+            if split:
+                err = (a[:, r] - ref[0]).abs().max().item()
+                assert err <= 2e-3, (b, name, err)
+            else:
+                assert torch.equal(a[:, r], ref[0]), (b, name)
 
 
 DECODE_CASES = [
