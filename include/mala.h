@@ -153,7 +153,7 @@ int mala_fwd(const void* q, const void* k, const void* v, void* o, float* lse,
  * per query tile of B_q rows, query head and block of 128 keys: B Hq ceil(Nq / B_q)
  * ceil(Nk / 128) bytes, ~32 MB at B = 1, Hq = 8, Nq = Nk = 131072).  Shapes with
  * fewer than 1024 key blocks in all (B Hkv ceil(Nk / 128)) run each key block's
- * sweep over the query tiles in up to P parts of at least 1024 (query tile, head)
+ * sweep over the query tiles in up to P parts of at least 512 (query tile, head)
  * iterations on workgroups of their own, so that one long sweep does not set the
  * time alone; the workspace then also holds the parts' fp32 dK and dV sums
  * (P x 2 x B Hkv Nk D floats, ~268 MB at B = 1, Hq = 8, Hkv = 2, Nq = Nk = 32768,

@@ -22,7 +22,7 @@ constexpr int kDkdvChunk = 4096;             // sweep iterations the dK/dV kerne
 // dK/dV sweeps are split into parts of at least kDkdvPartMin iterations, run by
 // workgroups of their own, and summed by a reduction pass (fixed-length batches).
 constexpr int kDkdvSplitGroups = 1024;
-constexpr int kDkdvPartMin = 1024;
+constexpr int kDkdvPartMin = 512;
 // Budgets of the low bf16 term in the backward.  P and dS enter the MFMAs as
 // hi + lo (two bf16 terms, 2^-16 relative).  The lo term of a tile is left out of
 // dV (P) or dK (dS) while, for every key of the tile, the P mass or the sum of |dS|

@@ -354,7 +354,7 @@ def test_varlen_prefill_parity(tau):
     _check_backward_passes_agree(cb)
 
 
-def _dkdv_splits(B, Hq, Hkv, N, groups=1024, part_min=1024, keys=128, bq=32):
+def _dkdv_splits(B, Hq, Hkv, N, groups=1024, part_min=512, keys=128, bq=32):
     """Whether a fixed-length backward call of this causal shape splits its dK/dV
     sweeps (the rule of the library's launch: fewer than `groups` key-block
     workgroups, and a first sweep longer than the part size)."""
