@@ -68,13 +68,24 @@ class Train:
         self.scale = float(np.float32(w.scale))
         self.mala = mala
 
-    def fwd(self, tau):
-        self.mala.mala_fwd(self.q, self.k, self.v, self.o, self.lse, self.rt_f, self.cnt_f,
+    # The timed calls leave out the optional statistics (per-row tile counts and the
+    # counters); stats() repeats the fwd + bwd pair with them, which takes exactly the
+    # same decisions.
+    def fwd(self, tau, stats=False):
+        self.mala.mala_fwd(self.q, self.k, self.v, self.o, self.lse,
+                           self.rt_f if stats else None, self.cnt_f if stats else None,
                            self.scale, tau)
 
-    def bwd(self, tau):
+    def bwd(self, tau, stats=False):
         self.mala.mala_bwd(self.q, self.k, self.v, self.o, self.lse, self.do, self.dq, self.dk,
-                           self.dv, self.rt_b, self.cnt_b, self.ws, self.scale, tau)
+                           self.dv, self.rt_b if stats else None, self.cnt_b if stats else None,
+                           self.ws, self.scale, tau)
+
+    def stats(self, tau):
+        """The counters of one fwd + bwd pair at tau (with the statistics on)."""
+        self.fwd(tau, True)
+        self.bwd(tau, True)
+        return self.counters()
 
     def counters(self):
         return self.cnt_f.cpu().numpy(), self.cnt_b.cpu().numpy()
@@ -106,9 +117,15 @@ class Decode:
         self.scale = float(np.float32(w.scale))
         self.mala = mala
 
-    def run(self, tau, cache_lens=None):
-        self.mala.mala_decode(self.q, self.k, self.v, self.o, self.lse, self.ht, self.cnt,
+    def run(self, tau, cache_lens=None, stats=False):
+        self.mala.mala_decode(self.q, self.k, self.v, self.o, self.lse,
+                              self.ht if stats else None, self.cnt if stats else None,
                               self.splits, self.ws, self.scale, tau, cache_lens=cache_lens)
+
+    def stats(self, tau, cache_lens=None):
+        """The counters of one decode call at tau (with the statistics on)."""
+        self.run(tau, cache_lens, True)
+        return self.cnt.cpu().numpy()
 
 
 def ragged_lengths(B, N, seed=7):
@@ -121,11 +138,23 @@ def ragged_lengths(B, N, seed=7):
     return lens
 
 
-def time_calls(fn, reps, warmup):
-    """Mean and median per-call device time (ms) from HIP events on the current stream."""
+MIN_WARM_MS = 50.0   # --min-warm-ms
+
+
+def time_calls(fn, reps, warmup, min_warm_ms=None):
+    """Mean and median per-call device time (ms) from HIP events on the current stream.
+    The untimed calls run until both `warmup` calls and `min_warm_ms` of wall time have
+    passed: a few calls of a sub-millisecond kernel leave the GPU at its idle clock,
+    and the first timed calls of such a kernel then run ~10% slow."""
     import torch
-    for _ in range(warmup):
+    min_warm_ms = MIN_WARM_MS if min_warm_ms is None else min_warm_ms
+    t0 = time.time()
+    n = 0
+    while n < warmup or (time.time() - t0) * 1e3 < min_warm_ms:
         fn()
+        n += 1
+        if n >= warmup:
+            torch.cuda.synchronize()
     ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
           for _ in range(reps)]
     for a, b in ev:
@@ -219,7 +248,7 @@ def train_config(cfg_id, taus, reps, warmup, supp_taus=(), supp=None, memory=Tru
         n_, w_ = supp if t_ in supp_taus else (reps, warmup)
         f = time_calls(lambda: tr.fwd(t_), n_, w_)
         b = time_calls(lambda: tr.bwd(t_), n_, w_)
-        res[t_] = (f, b) + tuple(tr.counters())
+        res[t_] = (f, b) + tuple(tr.stats(t_))
     out = {"workload": CONFIGS[cfg_id]["desc"], "shape": [w.B, w.Hq, w.Hkv, w.N, w.D]}
     f0, b0 = res[0.0][0][0], res[0.0][1][0]
     for t_, (f, b, cf, cb) in res.items():
@@ -312,7 +341,7 @@ def lm_sweep(reps, warmup, lengths=LM_SWEEP_N):
         for t_ in (0.0,) + LM_SWEEP_TAUS:
             f = time_calls(lambda: tr.fwd(t_), reps, warmup)
             b = time_calls(lambda: tr.bwd(t_), reps, warmup)
-            cf, cb = tr.counters()
+            cf, cb = tr.stats(t_)
             runs[t_] = dict(fwd=f[0], bwd=b[0], cf=cf, cb=cb, out=tr.outputs())
         d = runs[0.0]
         row = {"N": N, "batch": w.B, "q_heads": w.B * w.Hq, "kv_heads": w.B * w.Hkv,
@@ -444,7 +473,7 @@ TRACE_CMD = ("cd /tmp && export TMPDIR=/tmp && timeout -k 10 600 rocprofv3 --ker
              "--output-format csv -d $OUT/trace_bench -o bench -- "
              "python $REPO/bench.py --steps 2 --warmup 1 --reps 2 --kernel-warmup 1 "
              "--supp-reps 2 --supp-warmup 1 --no-cpu-baseline --no-32k --no-lm --no-ragged "
-             "--no-small --no-memory")
+             "--no-small --no-memory --min-warm-ms 0 --no-stats-timing")
 
 
 def counter_pass(which="bwd"):
@@ -493,15 +522,16 @@ def skip_pass():
         for _ in range(3):
             tr.fwd(tau)
             tr.bwd(tau)
+        cf, cb = tr.stats(tau)   # a fourth call, with the statistics
         torch.cuda.synchronize()
-        cf, cb = tr.counters()
         log("tau %g: retained tiles fwd %.2f%% bwd %.2f%%" % (
             tau, 100.0 * cf[1] / cf[0], 100.0 * cb[1] / cb[0]))
 
 
 def summarize_skip_trace(trace_csv):
     """profiles/kernels_lm32k_skip_cost.md from the kernel trace of SKIP_TRACE_CMD
-    (every training kernel has 3 dispatches per tau, in the order of SKIP_TAUS)."""
+    (every training kernel has 4 dispatches per tau, in the order of SKIP_TAUS: 3
+    without the statistics, then 1 with them)."""
     import csv
     import collections
     with open(trace_csv) as fh:
@@ -517,17 +547,19 @@ def summarize_skip_trace(trace_csv):
              "`$OUT` an output directory):", "",
              "```", SKIP_TRACE_CMD, "python bench.py --summarize-skip-trace "
              "$OUT/trace_skip/skip_kernel_trace.csv", "```", "",
-             "Mean kernel durations (ms) over 3 calls per tau.  tau = 1e30 skips every "
+             "Mean kernel durations (ms) over 3 calls per tau (without the optional "
+             "statistics).  tau = 1e30 skips every "
              "backward tile and every forward tile but each row's first (the cost floor of "
              "the skip path: score MFMAs, the test, staging and synchronisation); the last "
              "column is that floor as a fraction of the dense time.", "",
              "| kernel | tau 0 (dense) | tau 1 | tau 1e30 (all skipped) | floor / dense |",
              "|---|---|---|---|---|"]
     for k, v in sorted(dur.items(), key=lambda kv: -sum(kv[1])):
-        if len(v) != 3 * len(SKIP_TAUS):
+        # per tau: 3 calls without the statistics, then the one with them (left out)
+        if len(v) != 4 * len(SKIP_TAUS):
             lines.append("| `%s` | %d dispatches (unexpected) | | | |" % (k, len(v)))
             continue
-        m = [sum(v[3 * i:3 * i + 3]) / 3 for i in range(len(SKIP_TAUS))]
+        m = [sum(v[4 * i:4 * i + 3]) / 3 for i in range(len(SKIP_TAUS))]
         lines.append("| `%s` | %.3f | %.3f | %.3f | %.2f |" % (k.replace("|", "/"), m[0], m[1],
                                                                m[2], m[2] / m[0]))
     with open(os.path.join(ROOT, "profiles", "kernels_lm32k_skip_cost.md"), "w") as fh:
@@ -602,8 +634,9 @@ def summarize_counters(fetch_csv, write_csv, which="bwd"):
 def summarize_trace(trace_csv):
     """profiles/kernels_128k_train_and_decode.md from the rocprofv3 kernel trace of
     TRACE_CMD.  That run calls each operator 3 times at tau = 1e-4 (1 warm-up + 2
-    timed steps), then 3 times at each of tau = 1e-4, 0 and 1 (1 warm-up + 2 event-
-    timed calls), so every kernel has 12 dispatches in that order."""
+    timed steps), then at each of tau = 1e-4, 0 and 1 3 times without the
+    statistics (1 warm-up + 2 event-timed calls) and once with them, so every kernel
+    has 15 dispatches in that order."""
     import csv
     import collections
     with open(trace_csv) as fh:
@@ -619,16 +652,18 @@ def summarize_trace(trace_csv):
              "```", TRACE_CMD, "python bench.py --summarize-trace "
              "$OUT/trace_bench/bench_kernel_trace.csv", "```", "",
              "Durations in milliseconds from the rocprofv3 kernel trace.  Each operator is "
-             "called 12 times: dispatches 1-6 at tau = 1e-4 (the bench step and its "
-             "event-timed calls), 7-9 at tau = 0 (dense through the same kernels), 10-12 at "
-             "tau = 1.", "",
+             "called 15 times: dispatches 1-6 at tau = 1e-4 (the bench step and its "
+             "event-timed calls) and 7 with the optional statistics, 8-10 at tau = 0 (dense "
+             "through the same kernels) and 11 with the statistics, 12-14 at tau = 1 and 15 "
+             "with the statistics.  The mean columns leave out the calls with the "
+             "statistics.", "",
              "| kernel | calls | mean ms, tau 1e-4 | mean ms, tau 0 | mean ms, tau 1 | total ms |",
              "|---|---|---|---|---|---|"]
     for k, v in sorted(dur.items(), key=lambda kv: -sum(kv[1])):
         n = len(v)
-        if n % 12 == 0:
-            m = n // 12
-            cells = (ms(v[:6 * m]), ms(v[6 * m:9 * m]), ms(v[9 * m:]))
+        if n % 15 == 0:
+            m = n // 15
+            cells = (ms(v[:6 * m]), ms(v[7 * m:10 * m]), ms(v[11 * m:14 * m]))
             lines.append("| `%s` | %d | %.3f | %.3f | %.3f | %.3f |"
                          % ((k.replace("|", "/"), n) + cells + (sum(v),)))
         else:
@@ -732,6 +767,10 @@ def main():
                     help="event-timed calls per kernel for the supplementary fields")
     ap.add_argument("--supp-warmup", type=int, default=5)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--min-warm-ms", type=float, default=50.0,
+                    help="untimed calls before each event-timed series: at least this long")
+    ap.add_argument("--no-stats-timing", action="store_true",
+                    help="leave out the timing of the calls with the optional statistics")
     ap.add_argument("--no-32k", action="store_true")
     ap.add_argument("--no-small", action="store_true",
                     help="skip the 1024- and 8192-token workloads")
@@ -754,6 +793,8 @@ def main():
     ap.add_argument("--summarize-mfma", metavar="COUNTER_CSV")
     ap.add_argument("--summarize-pipes", metavar="COUNTER_CSV")
     args = ap.parse_args()
+    global MIN_WARM_MS
+    MIN_WARM_MS = args.min_warm_ms
     if args.summarize_counters:
         summarize_counters(*args.summarize_counters)
         return
@@ -816,8 +857,8 @@ def main():
         f = time_calls(lambda: tr.fwd(t_), args.reps, args.kernel_warmup)
         b = time_calls(lambda: tr.bwd(t_), args.reps, args.kernel_warmup)
         d = time_calls(lambda: dec.run(t_), args.reps, args.kernel_warmup)
-        cf, cb = tr.counters()
-        cd = dec.cnt.cpu().numpy()
+        cf, cb = tr.stats(t_)
+        cd = dec.stats(t_)
         res[name] = dict(fwd=f, bwd=b, dec=d, cf=cf, cb=cb, cd=cd)
         log(name, "fwd %.2f bwd %.2f decode %.3f ms" % (f[0], b[0], d[0]))
     # supplementary: the paper's canonical tolerance tau = 1 on the same inputs
@@ -825,16 +866,27 @@ def main():
     f1 = time_calls(lambda: tr.fwd(1.0), sr, sw)
     b1 = time_calls(lambda: tr.bwd(1.0), sr, sw)
     d1 = time_calls(lambda: dec.run(1.0), sr, sw)
-    cf1, cb1 = tr.counters()
-    cd1 = dec.cnt.cpu().numpy()
+    cf1, cb1 = tr.stats(1.0)
+    cd1 = dec.stats(1.0)
     log("tau=1 fwd %.2f bwd %.2f decode %.3f ms" % (f1[0], b1[0], d1[0]))
+    # the same calls with the optional statistics (per-row tile counts and counters)
+    with_stats = None
+    if not args.no_stats_timing:
+        fs = time_calls(lambda: tr.fwd(tau, True), sr, sw)
+        bs = time_calls(lambda: tr.bwd(tau, True), sr, sw)
+        ds = time_calls(lambda: dec.run(tau, None, True), sr, sw)
+        with_stats = {"note": "the 131072-token fwd / bwd and the decode at tau with row tile "
+                              "counts and counters requested (the timed calls above leave "
+                              "them out; the statistics come from one extra call each)",
+                      "fwd_ms": round(fs[0], 3), "bwd_ms": round(bs[0], 3),
+                      "decode_ms": round(ds[0], 4)}
     # supplementary: the same decode batch with ragged valid cache lengths
     ragged = None
     if not args.no_ragged:
         lens = ragged_lengths(dec.w.B, dec.w.N)
         cl = torch.from_numpy(lens).to("cuda")
         dr = time_calls(lambda: dec.run(tau, cl), sr, sw)
-        cdr = dec.cnt.cpu().numpy()
+        cdr = dec.stats(tau, cl)
         drd = time_calls(lambda: dec.run(0.0, cl), sr, sw)
         # K of every valid key, V of the tiles fetched
         rag_bytes = (float(lens.sum()) * dec.w.Hkv * dec.w.D * 2
@@ -903,8 +955,12 @@ def main():
         },
         "decision_tile": [bq, bk],
         "timing_protocol": ("HIP events per call; measured taus: mean / median of %d calls after "
-                            "%d untimed; supplementary fields: %d after %d"
-                            % (args.reps, args.kernel_warmup, args.supp_reps, args.supp_warmup)),
+                            "%d untimed (and at least %g ms of untimed calls); supplementary "
+                            "fields: %d after %d; the timed calls leave out the optional "
+                            "statistics, which one extra call per setting records"
+                            % (args.reps, args.kernel_warmup, args.min_warm_ms, args.supp_reps,
+                               args.supp_warmup)),
+        "with_statistics": with_stats,
         "tau1_supplementary": {
             "fwd_ms": round(f1[0], 3), "bwd_ms": round(b1[0], 3), "decode_ms": round(d1[0], 4),
             "speedup_fwd": round(rd["fwd"][0] / f1[0], 4),

@@ -204,6 +204,7 @@ __global__ __launch_bounds__(1024) void mala_bwd_dkdv_kernel(BwdParams p) {
   // << 4 | the tile's decisions for the four key groups
   __shared__ uint16_t plist[kDkdvChunk];
   __shared__ int wsum[5];      // per-wavefront counts of the compaction, then the total
+  __shared__ unsigned long long bcnt[kNumCounters];   // the workgroup's counter sums
 
   // Sixteen wavefronts, four per 32 keys [32 g, +32) of the block (g = w % 4, so a
   // key group's four wavefronts share one SIMD), in a pipeline over the query tiles
@@ -251,6 +252,7 @@ __global__ __launch_bounds__(1024) void mala_bwd_dkdv_kernel(BwdParams p) {
   const int it0 = part * p.psize, it1 = min(total, it0 + p.psize);
   if (it0 >= total) return;
   const float budget_share = 1.f / (float)((total + p.psize - 1) / p.psize);
+  if (p.counters) blk_init(bcnt);
 
   // Query tiles are swept from the last one down to the block's diagonal, the
   // heads of the group innermost (iteration it: tile nqt - 1 - it / grp, head
@@ -427,9 +429,9 @@ __global__ __launch_bounds__(1024) void mala_bwd_dkdv_kernel(BwdParams p) {
           __syncthreads();
         }
       }
-      if (p.counters && lane == 0 && n_ret_kv) {
-        atomicAdd(&p.counters[kCntRetainedKV], (unsigned long long)n_ret_kv);
-        atomicAdd(&p.counters[kCntSetHashKV], hsum);
+      if (p.counters && lane == 0) {
+        blk_add(bcnt, kCntRetainedKV, n_ret_kv);
+        blk_add(bcnt, kCntSetHashKV, hsum);
       }
     } else {
       float fdk = 0.f;   // sum of |dS| of this lane's key in tiles run without the lo term
@@ -535,9 +537,9 @@ __global__ __launch_bounds__(1024) void mala_bwd_dkdv_kernel(BwdParams p) {
           __syncthreads();
         }
       }
-      if (p.counters && grp_k == 0 && lane == 0 && n_do) {
-        atomicAdd(&p.counters[kCntVTiles], (unsigned long long)n_do);
-        atomicAdd(&p.counters[kCntVNeeded], (unsigned long long)n_do);
+      if (p.counters && grp_k == 0 && lane == 0) {
+        blk_add(bcnt, kCntVTiles, n_do);
+        blk_add(bcnt, kCntVNeeded, n_do);
       }
     } else {
       // the decision of tile k - 2 is known since the end of step k - 2: it is read one
@@ -601,6 +603,8 @@ __global__ __launch_bounds__(1024) void mala_bwd_dkdv_kernel(BwdParams p) {
         }
     }
   }
+  // every role ends here, after the same number of barriers
+  if (p.counters) blk_flush(bcnt, p.counters);
 }
 
 // Offline test of one tile in the transposed C layout of the dQ pass: the lane
@@ -643,6 +647,7 @@ __global__ __launch_bounds__(kDqWaves * 64) void mala_bwd_dq_kernel(BwdParams p)
   constexpr int STAGE = tile_elems<D>(kFwdStage);
   __shared__ __attribute__((aligned(16))) bf16 Ks[2 * STAGE];
   __shared__ __attribute__((aligned(16))) bf16 Vs[2 * STAGE];
+  __shared__ unsigned long long bcnt[kNumCounters];   // the workgroup's counter sums
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -664,6 +669,7 @@ __global__ __launch_bounds__(kDqWaves * 64) void mala_bwd_dq_kernel(BwdParams p)
   const long kbase = sg.kb + (long)hkv * p.Nk;
   const bf16* Kp = p.k + kbase * D;
   const bf16* Vp = p.v + kbase * D;
+  if (p.counters) blk_init(bcnt);
 
   // Q and dO rows of this wavefront as B operands (lane column qrow)
   bf16x8 qb[KS], ob[KS];
@@ -852,11 +858,14 @@ __global__ __launch_bounds__(kDqWaves * 64) void mala_bwd_dq_kernel(BwdParams p)
       }
     if (p.row_tiles && h == 0) p.row_tiles[qbase + qrow] = cnt_row;
   }
-  if (p.counters && lane == 0 && n_legal) {
-    atomicAdd(&p.counters[kCntLegal], (unsigned long long)n_legal);
-    atomicAdd(&p.counters[kCntRetained], (unsigned long long)n_ret);
-    atomicAdd(&p.counters[kCntSlots], (unsigned long long)n_ret * kBk * nvalid);
-    if (hsum) atomicAdd(&p.counters[kCntSetHash], hsum);
+  if (p.counters) {
+    if (lane == 0) {
+      blk_add(bcnt, kCntLegal, n_legal);
+      blk_add(bcnt, kCntRetained, n_ret);
+      blk_add(bcnt, kCntSlots, (unsigned long long)n_ret * kBk * nvalid);
+      blk_add(bcnt, kCntSetHash, hsum);
+    }
+    blk_flush(bcnt, p.counters);
   }
 }
 

@@ -38,8 +38,11 @@ __global__ __launch_bounds__(kFwdWaves * 64) void mala_fwd_kernel(FwdParams p) {
   // is processed
   __shared__ __attribute__((aligned(16))) bf16 Ks[2 * STAGE];
   __shared__ __attribute__((aligned(16))) bf16 Vs[2 * STAGE];
-  // statistics: per stage buffer, whether some wavefront retained each decision tile
+  // statistics: per stage buffer and decision tile, t + 1 once some wavefront
+  // retained the tile of stage t (stage-tagged: no clearing between stages); the
+  // workgroup's counter sums
   __shared__ int vneed[2][kFwdStage / kBk];
+  __shared__ unsigned long long bcnt[kNumCounters];
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -87,7 +90,10 @@ __global__ __launch_bounds__(kFwdWaves * 64) void mala_fwd_kernel(FwdParams p) {
   unsigned n_legal = 0, n_ret = 0, n_vneed = 0;
   unsigned long long hsum = 0;   // fingerprints of the retained tiles
   const bool stats = p.counters != nullptr;
-  if (stats && tid < 2 * (kFwdStage / kBk)) vneed[tid / (kFwdStage / kBk)][tid % (kFwdStage / kBk)] = 0;
+  if (stats) {
+    if (tid < 2 * (kFwdStage / kBk)) vneed[tid / (kFwdStage / kBk)][tid % (kFwdStage / kBk)] = 0;
+    blk_init(bcnt);
+  }
 
   // K / V stages move with buffer loads straight into LDS (keys past the end read
   // as zeros): wavefront w issues the 64-position loads w, w + 8, ... of each slot.
@@ -123,6 +129,10 @@ __global__ __launch_bounds__(kFwdWaves * 64) void mala_fwd_kernel(FwdParams p) {
     const bf16* kr = lds_pin(Ks + buf * STAGE + rdo);
     const bf16* vtb = lds_pin(Vs + buf * STAGE + tro);
 
+    // statistics: the tag each retained tile of this stage found in vneed (t + 1:
+    // another wavefront marked it first); compared after the stage, so that the
+    // exchange's result is not waited for in the middle of the tile's work
+    int vtag[2] = {t + 1, t + 1};
     if (2 * t <= jdiag) {
       // the two tiles in descending key order: the high half first
 #pragma unroll
@@ -175,7 +185,8 @@ __global__ __launch_bounds__(kFwdWaves * 64) void mala_fwd_kernel(FwdParams p) {
         cnt += voter ? 1 : 0;
         if (stats) {
           hsum += tile_hash(b, hq, q0w / kBq, j);
-          if (lane == 0) vneed[buf][sub] = 1;
+          // the first wavefront to retain this tile of the stage counts its V tile
+          if (lane == 0) vtag[sub] = atomicExch(&vneed[buf][sub], t + 1);
         }
 
         // Lazy rescaling: a row's reference m moves only when some row of the
@@ -238,15 +249,7 @@ __global__ __launch_bounds__(kFwdWaves * 64) void mala_fwd_kernel(FwdParams p) {
     }
     wait_vm();
     __syncthreads();
-    if (stats && tid == 0) {
-      // the V tiles of this stage that some wavefront needed; cleared for the stage
-      // after next (the next stage uses the other buffer)
-#pragma unroll
-      for (int u = 0; u < kFwdStage / kBk; ++u) {
-        n_vneed += vneed[buf][u];
-        vneed[buf][u] = 0;
-      }
-    }
+    n_vneed += (vtag[0] != t + 1) + (vtag[1] != t + 1);
   }
 
   // epilogue: O <- O / l, LSE = (m + log2 l) * ln 2
@@ -267,16 +270,15 @@ __global__ __launch_bounds__(kFwdWaves * 64) void mala_fwd_kernel(FwdParams p) {
     }
   }
   if (stats) {
-    if (lane == 0 && n_legal) {
-      atomicAdd(&p.counters[kCntLegal], (unsigned long long)n_legal);
-      atomicAdd(&p.counters[kCntRetained], (unsigned long long)n_ret);
-      atomicAdd(&p.counters[kCntSlots], (unsigned long long)n_ret * kBk * nvalid);
-      if (hsum) atomicAdd(&p.counters[kCntSetHash], hsum);
+    if (lane == 0) {
+      blk_add(bcnt, kCntLegal, n_legal);
+      blk_add(bcnt, kCntRetained, n_ret);
+      blk_add(bcnt, kCntSlots, (unsigned long long)n_ret * kBk * nvalid);
+      blk_add(bcnt, kCntSetHash, hsum);
+      blk_add(bcnt, kCntVNeeded, n_vneed);
     }
-    if (tid == 0) {
-      atomicAdd(&p.counters[kCntVTiles], (unsigned long long)(ttop + 1) * (kFwdStage / kBk));
-      atomicAdd(&p.counters[kCntVNeeded], (unsigned long long)n_vneed);
-    }
+    if (tid == 0) blk_add(bcnt, kCntVTiles, (unsigned long long)(ttop + 1) * (kFwdStage / kBk));
+    blk_flush(bcnt, p.counters);
   }
 }
 

@@ -71,6 +71,23 @@ __device__ __forceinline__ unsigned long long tile_hash(int b, int h, int i, int
   return z ^ (z >> 31);
 }
 
+// Statistics of one workgroup: its wavefronts add into an LDS copy of the counters
+// (blk_add, LDS atomics), then one thread per counter adds the workgroup's sums to
+// the global counters (blk_flush).  Same-address global atomics from every
+// wavefront of a grid serialise at the L2; one per counter and workgroup keeps
+// their count small.  blk_init runs before a barrier that precedes every blk_add;
+// every thread of the workgroup calls blk_flush.
+__device__ __forceinline__ void blk_init(unsigned long long* s) {
+  if (threadIdx.x < kNumCounters) s[threadIdx.x] = 0;
+}
+__device__ __forceinline__ void blk_add(unsigned long long* s, int i, unsigned long long x) {
+  if (x) atomicAdd(&s[i], x);
+}
+__device__ __forceinline__ void blk_flush(unsigned long long* s, unsigned long long* g) {
+  __syncthreads();
+  if (threadIdx.x < kNumCounters && s[threadIdx.x]) atomicAdd(&g[threadIdx.x], s[threadIdx.x]);
+}
+
 // Batches come in two layouts.  Fixed length: [B, H, N, D], slice (b, h) at rows
 // (b H + h) N.  Packed (cu non-null): B sequences along the token axes of
 // [Hq, Nq, D] queries and [Hkv, Nk, D] keys (Nq, Nk = the totals, the head
