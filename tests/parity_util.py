@@ -160,3 +160,20 @@ def bwd_do_loads(keep, keys_per_group=128, bk=32):
     pad = (-Tc) % g
     k = np.concatenate([keep, np.zeros((B, H, Tr, pad), bool)], axis=3) if pad else keep
     return int(k.reshape(B, H, Tr, -1, g).any(axis=4).sum())
+
+
+def dkdv_splits(B, Hq, Hkv, Nq, Nk=None, groups=1024, part_min=512, keys=128, bq=32):
+    """Whether a fixed-length backward call of this causal shape splits its dK/dV
+    sweeps (the rule of the library's launch: fewer than `groups` key-block
+    workgroups, and a first sweep longer than the part size)."""
+    Nk = Nq if Nk is None else Nk
+    nkblk = -(-Nk // keys)
+    if nkblk * B * Hkv >= groups:
+        return False
+    grp, nqt = Hq // Hkv, -(-Nq // bq)
+    first = lambda j: max(0, j * keys - (Nk - Nq)) // bq
+    total = B * Hkv * sum(grp * (nqt - first(j)) for j in range(nkblk))
+    ps = part_min
+    while ps * 2 * groups <= total:
+        ps *= 2
+    return ps < grp * nqt

@@ -8,6 +8,7 @@ import re
 import pytest
 
 import paper_2609_32712_amd as mala
+from parity_util import dkdv_splits
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 HEADER = os.path.join(ROOT, "include", "mala.h")
@@ -62,6 +63,20 @@ def test_workspace_sizes(lib):
     assert mala.mala_bwd_workspace_size(1, 8, 2, 32768, 32768, 128) >= 4 * 2 * 2 * 32768 * 128 * 4
     assert mala.mala_bwd_workspace_size(1, 8, 2, 131072, 131072, 128) < (
         8 * 131072 * 4 + 8 * 4096 * 1024 + 2 ** 20)
+
+
+def test_split_rule_of_the_tests_matches_the_library(lib):
+    # the GPU tests' mirror of the launch rule (parity_util.dkdv_splits) against the
+    # library: the backward workspace holds partial sums exactly when sweeps split
+    ru = lambda x: (x + 255) // 256 * 256
+    shapes = [(1, 16, 1, 12000, 12000), (2, 8, 1, 6000, 6000), (1, 16, 1, 5000, 12000),
+              (1, 8, 2, 32768, 32768), (1, 8, 2, 16384, 16384), (1, 8, 2, 8192, 8192),
+              (1, 8, 2, 4096, 4096), (1, 8, 2, 131072, 131072), (1, 32, 8, 32768, 32768),
+              (1, 1, 1, 1024, 1024), (4, 8, 2, 8192, 8192), (1, 4, 1, 3000, 9000)]
+    for B, Hq, Hkv, Nq, Nk in shapes:
+        base = ru(B * Hq * Nq * 4) + ru(Hq * -(-Nk // 128) * B * -(-Nq // 32))
+        split = mala.mala_bwd_workspace_size(B, Hq, Hkv, Nq, Nk, 128) > base
+        assert split == dkdv_splits(B, Hq, Hkv, Nq, Nk), (B, Hq, Hkv, Nq, Nk)
     assert mala.mala_decode_workspace_size(16, 32, 128, 8) >= 16 * 32 * 8 * 130 * 4
     assert mala.mala_decode_workspace_size(16, 32, 96, 8) == 0
 

@@ -12,7 +12,7 @@ import torch
 import oracle
 import paper_2609_32712_amd as mala
 from parity_util import (LSE_DIAG, TOL_MAX, assert_close, assert_counts, bwd_do_loads, dev,
-                         fwd_v_loads, host,
+                         dkdv_splits, fwd_v_loads, host,
                          set_fingerprint, tie_masks, ties)
 from workloads import CONFIGS, Workload, bf16_to_f64
 
@@ -49,6 +49,10 @@ TRAIN_CASES = {
     "single_row_d64": dict(spec=dict(kind="train", B=1, Hq=1, Hkv=1, N=1, D=64, beta=1.0), over={}),
     # the language-model-like supplementary workload (config 6) at a small size
     "lm_d128_ragged": dict(spec=6, over=dict(N=1000, Hq=4, Hkv=2)),
+    # two sequences, d = 64, 47 key blocks of one KV head each: the key-block sweeps run
+    # in parts (1504 iterations in the first, parts of 512) summed by the reduction
+    "split_d64_b2": dict(spec=dict(kind="train", B=2, Hq=8, Hkv=1, N=6000, D=64, beta=2.0,
+                                   local=2.0), over={}),
 }
 TRAIN_TAUS = {
     "cfg1": (0.0, 1e-4, 1e-3),
@@ -63,6 +67,7 @@ TRAIN_TAUS = {
     # 1e30: every backward tile is skipped (empty compaction chunks, zero gradients)
     "gqa16_chunks": (1e-3, 1.0, 1e30),
     "lm_d128_ragged": (0.0, 1e-4, 1.0),
+    "split_d64_b2": (0.0, 1e-3, 1.0),
 }
 
 
@@ -152,6 +157,20 @@ def test_train_parity_other_seeds(name, tau, seed):
 def test_prefill_against_longer_cache(Nq, tau):
     w, q, k, v, do = _train_case("gqa_d128_ragged", tau, Nq=Nq)
     _check_train(w, q, k, v, do, tau)
+
+
+@pytest.mark.parametrize("tau", [1e-3, 1.0])
+def test_prefill_with_split_sweeps(tau):
+    # 5000 new rows against 12000 keys, 16 query heads on one KV head: the key-block
+    # sweeps (from each block's first visible query tile) run in parts
+    w, q, k, v, do = _train_case("gqa16_chunks", tau, Nq=5000)
+    assert dkdv_splits(1, 16, 1, 5000, 12000)
+    _check_train(w, q, k, v, do, tau)
+
+
+def test_split_cases_split():
+    # the parity cases meant for the split sweeps do split under the launch rule
+    assert dkdv_splits(1, 16, 1, 12000) and dkdv_splits(2, 8, 1, 6000)
 
 
 def test_forward_skips_are_exercised():
@@ -354,19 +373,6 @@ def test_varlen_prefill_parity(tau):
     _check_backward_passes_agree(cb)
 
 
-def _dkdv_splits(B, Hq, Hkv, N, groups=1024, part_min=512, keys=128, bq=32):
-    """Whether a fixed-length backward call of this causal shape splits its dK/dV
-    sweeps (the rule of the library's launch: fewer than `groups` key-block
-    workgroups, and a first sweep longer than the part size)."""
-    nkblk = -(-N // keys)
-    if nkblk * B * Hkv >= groups:
-        return False
-    grp, nqt = Hq // Hkv, -(-N // bq)
-    total = B * Hkv * sum(grp * (nqt - (j * keys) // bq) for j in range(nkblk))
-    ps = part_min
-    while ps * 2 * groups <= total:
-        ps *= 2
-    return ps < grp * nqt
 
 
 @pytest.mark.parametrize("tau", [1e-4, 1.0])
@@ -398,7 +404,7 @@ def test_varlen_full_size_equals_per_sequence_calls(tau):
                  ("bwd row_tiles", gb["row_tiles"], b1["row_tiles"]))
         for name, a, ref in pairs:
             assert torch.equal(a[:, r], ref[0]), (b, name)
-        split = _dkdv_splits(1, w.Hq, w.Hkv, lens[b])
+        split = dkdv_splits(1, w.Hq, w.Hkv, lens[b])
         for name, a, ref in (("dk", gb["dk"], b1["dk"]), ("dv", gb["dv"], b1["dv"])):
             if split:
                 err = (a[:, r] - ref[0]).abs().max().item()
