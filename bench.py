@@ -227,6 +227,21 @@ def operator_memory(tr, tau):
     return res
 
 
+def time_train(tr, taus, timing):
+    """fwd and bwd latencies of a Train at each tau, grouped by operator: first every
+    forward series, then every backward series (each after an untimed forward at its
+    tau, whose O and LSE it takes), so that each series follows the same kind of work
+    (a series timed right after seconds of another operator ran at a lower clock).
+    timing(tau) gives (reps, warmup).  Returns {tau: (fwd, bwd, cf, cb)}."""
+    fw = {t_: time_calls(lambda: tr.fwd(t_), *timing(t_)) for t_ in taus}
+    out = {}
+    for t_ in taus:
+        tr.fwd(t_)
+        b = time_calls(lambda: tr.bwd(t_), *timing(t_))
+        out[t_] = (fw[t_], b) + tuple(tr.stats(t_))
+    return out
+
+
 def train_config(cfg_id, taus, reps, warmup, supp_taus=(), supp=None, memory=True):
     """One training workload: fwd / bwd latency (HIP events, mean and median of reps
     calls after warmup) at tau = 0 (dense through the same kernels) and at each tau,
@@ -243,12 +258,8 @@ def train_config(cfg_id, taus, reps, warmup, supp_taus=(), supp=None, memory=Tru
     rows = w.B * w.Hq * w.N
     pct = lambda a, b_: round(100.0 * float(a) / max(1.0, float(b_)), 3)
     do_dense = dense_do_tiles(w.B, w.Hq, w.Hkv, w.N)
-    res = {}
-    for t_ in (0.0,) + tuple(x for x in taus if x != 0.0):
-        n_, w_ = supp if t_ in supp_taus else (reps, warmup)
-        f = time_calls(lambda: tr.fwd(t_), n_, w_)
-        b = time_calls(lambda: tr.bwd(t_), n_, w_)
-        res[t_] = (f, b) + tuple(tr.stats(t_))
+    res = time_train(tr, (0.0,) + tuple(x for x in taus if x != 0.0),
+                     lambda t_: supp if t_ in supp_taus else (reps, warmup))
     out = {"workload": CONFIGS[cfg_id]["desc"], "shape": [w.B, w.Hq, w.Hkv, w.N, w.D]}
     f0, b0 = res[0.0][0][0], res[0.0][1][0]
     for t_, (f, b, cf, cb) in res.items():
@@ -338,10 +349,9 @@ def lm_sweep(reps, warmup, lengths=LM_SWEEP_N):
         w = tr.w
         nrows = w.B * w.Hq * w.N
         runs = {}
-        for t_ in (0.0,) + LM_SWEEP_TAUS:
-            f = time_calls(lambda: tr.fwd(t_), reps, warmup)
-            b = time_calls(lambda: tr.bwd(t_), reps, warmup)
-            cf, cb = tr.stats(t_)
+        for t_, (f, b, cf, cb) in time_train(tr, (0.0,) + LM_SWEEP_TAUS,
+                                             lambda t_: (reps, warmup)).items():
+            tr.stats(t_)   # the outputs at t_ for the fidelity figures
             runs[t_] = dict(fwd=f[0], bwd=b[0], cf=cf, cb=cb, out=tr.outputs())
         d = runs[0.0]
         row = {"N": N, "batch": w.B, "q_heads": w.B * w.Hq, "kv_heads": w.B * w.Hkv,
@@ -634,9 +644,10 @@ def summarize_counters(fetch_csv, write_csv, which="bwd"):
 def summarize_trace(trace_csv):
     """profiles/kernels_128k_train_and_decode.md from the rocprofv3 kernel trace of
     TRACE_CMD.  That run calls each operator 3 times at tau = 1e-4 (1 warm-up + 2
-    timed steps), then at each of tau = 1e-4, 0 and 1 3 times without the
-    statistics (1 warm-up + 2 event-timed calls) and once with them, so every kernel
-    has 15 dispatches in that order."""
+    timed steps), then 3 times at each of tau = 1e-4, 0 and 1 (1 warm-up + 2
+    event-timed calls), so that dispatches 1-6, 7-9 and 10-12 of every kernel are those
+    taus; the dispatches after them (the untimed forwards before the backward
+    series, the calls with the statistics) are left out."""
     import csv
     import collections
     with open(trace_csv) as fh:
@@ -651,19 +662,17 @@ def summarize_trace(trace_csv):
              "`$OUT` an output directory):", "",
              "```", TRACE_CMD, "python bench.py --summarize-trace "
              "$OUT/trace_bench/bench_kernel_trace.csv", "```", "",
-             "Durations in milliseconds from the rocprofv3 kernel trace.  Each operator is "
-             "called 15 times: dispatches 1-6 at tau = 1e-4 (the bench step and its "
-             "event-timed calls) and 7 with the optional statistics, 8-10 at tau = 0 (dense "
-             "through the same kernels) and 11 with the statistics, 12-14 at tau = 1 and 15 "
-             "with the statistics.  The mean columns leave out the calls with the "
-             "statistics.", "",
+             "Durations in milliseconds from the rocprofv3 kernel trace.  Dispatches 1-6 "
+             "of each kernel are at tau = 1e-4 (the bench step and its event-timed calls), "
+             "7-9 at tau = 0 (dense through the same kernels), 10-12 at tau = 1; the "
+             "dispatches after them (the untimed forward before each backward series, one "
+             "call per tau with the optional statistics) are left out of the means.", "",
              "| kernel | calls | mean ms, tau 1e-4 | mean ms, tau 0 | mean ms, tau 1 | total ms |",
              "|---|---|---|---|---|---|"]
     for k, v in sorted(dur.items(), key=lambda kv: -sum(kv[1])):
         n = len(v)
-        if n % 15 == 0:
-            m = n // 15
-            cells = (ms(v[:6 * m]), ms(v[7 * m:10 * m]), ms(v[11 * m:14 * m]))
+        if n in (15, 18):
+            cells = (ms(v[:6]), ms(v[6:9]), ms(v[9:12]))
             lines.append("| `%s` | %d | %.3f | %.3f | %.3f | %.3f |"
                          % ((k.replace("|", "/"), n) + cells + (sum(v),)))
         else:
@@ -851,24 +860,28 @@ def main():
     torch.cuda.synchronize()
     ms_per_step = (time.perf_counter() - t0) * 1e3 / args.steps
 
-    # per-kernel event timings at tau and at tau = 0 (dense through the same kernels)
-    res = {}
-    for name, t_ in (("tau", tau), ("dense", 0.0)):
-        f = time_calls(lambda: tr.fwd(t_), args.reps, args.kernel_warmup)
-        b = time_calls(lambda: tr.bwd(t_), args.reps, args.kernel_warmup)
-        d = time_calls(lambda: dec.run(t_), args.reps, args.kernel_warmup)
-        cf, cb = tr.stats(t_)
-        cd = dec.stats(t_)
-        res[name] = dict(fwd=f, bwd=b, dec=d, cf=cf, cb=cb, cd=cd)
-        log(name, "fwd %.2f bwd %.2f decode %.3f ms" % (f[0], b[0], d[0]))
-    # supplementary: the paper's canonical tolerance tau = 1 on the same inputs
+    # per-kernel event timings at tau, at tau = 0 (dense through the same kernels) and
+    # at the paper's canonical tau = 1 (supplementary), grouped by operator: every
+    # forward series, then every backward series (each after an untimed forward at
+    # its tau), then every decode series, then one call each with the statistics
     sr, sw = args.supp_reps, args.supp_warmup
-    f1 = time_calls(lambda: tr.fwd(1.0), sr, sw)
-    b1 = time_calls(lambda: tr.bwd(1.0), sr, sw)
-    d1 = time_calls(lambda: dec.run(1.0), sr, sw)
-    cf1, cb1 = tr.stats(1.0)
-    cd1 = dec.stats(1.0)
-    log("tau=1 fwd %.2f bwd %.2f decode %.3f ms" % (f1[0], b1[0], d1[0]))
+    series = (("tau", tau, args.reps, args.kernel_warmup),
+              ("dense", 0.0, args.reps, args.kernel_warmup), ("tau1", 1.0, sr, sw))
+    res = {name: {} for name, _, _, _ in series}
+    for name, t_, n_, w_ in series:
+        res[name]["fwd"] = time_calls(lambda: tr.fwd(t_), n_, w_)
+    for name, t_, n_, w_ in series:
+        tr.fwd(t_)
+        res[name]["bwd"] = time_calls(lambda: tr.bwd(t_), n_, w_)
+    for name, t_, n_, w_ in series:
+        res[name]["dec"] = time_calls(lambda: dec.run(t_), n_, w_)
+    for name, t_, _, _ in series:
+        res[name]["cf"], res[name]["cb"] = tr.stats(t_)
+        res[name]["cd"] = dec.stats(t_)
+        log(name, "fwd %.2f bwd %.2f decode %.3f ms" % (res[name]["fwd"][0], res[name]["bwd"][0],
+                                                        res[name]["dec"][0]))
+    r1 = res.pop("tau1")
+    f1, b1, d1, cf1, cb1, cd1 = (r1[x] for x in ("fwd", "bwd", "dec", "cf", "cb", "cd"))
     # the same calls with the optional statistics (per-row tile counts and counters)
     with_stats = None
     if not args.no_stats_timing:
