@@ -1,30 +1,35 @@
-// MALA backward (Algorithm 2) for gfx950, as two kernels that take identical
-// tile decisions.
+// MALA backward (Algorithm 2) for gfx950, as two kernels that use the same tile
+// decisions.
 //
-// mala_bwd_dkdv_kernel (key-major, Algorithm 2's traversal): one workgroup owns 128
-// keys of one (batch, KV head) and keeps their dK and dV in registers for the whole
-// kernel (no atomics, bitwise reproducible); it sweeps the query tiles of every
-// query head of the GQA group from the end down to the diagonal.  Sixteen
-// wavefronts, four roles per 32 keys on one SIMD, pipelined over the query tiles:
-// role 0 takes the tile decision and forms P (fp32, handed on through LDS), role 1
-// accumulates dV one tile later and moves the query tiles into LDS, role 2 forms
-// dP and dS, role 3 accumulates dK two tiles later (dS handed on as bf16 operands).
-//   S = Q_i K_w^T         8 MFMAs (lane = one key column, 16 query rows)
+// mala_bwd_dq_kernel (query-major, like the forward) runs first and takes every
+// tile decision: one workgroup = 8 wavefronts = 256 query rows; K and V stream
+// through double-buffered LDS.  It computes the transposed products (S^T = K Q^T,
+// dP^T = V dO^T, dQ^T += K^T dS^T), so that a lane holds one query row and dS feeds
+// the dQ MFMA straight from registers.  It records its decisions, one byte per
+// (query tile, query head, 128-key block), for the key-major kernel.  dQ needs no
+// atomics and is bitwise reproducible.
+//   S^T = K_w Q_i^T       8 MFMAs per 32 x 32 tile
 //   offline test          retain iff some valid entry has
 //                         s - lse_q >= log2(tau) - log2(L_q) (base-2 units); ballot
-//   retained path         P = exp2(S - lse), dV^T += dO_i^T P; dP = dO_i V_w^T,
-//                         dS = P (dP - D_q), dK^T += Q_i^T dS.  P and dS enter the
-//                         MFMAs as two bf16 terms (hi + lo) unless an error budget
-//                         allows the hi term alone; the A operands come through
-//                         ds_read_b64_tr_b16.
-// mala_bwd_dq_kernel (query-major, like the forward): one workgroup = 8 wavefronts
-// = 256 query rows; K and V stream through double-buffered LDS.  It computes the
-// transposed products (S^T = K Q^T, dP^T = V dO^T, dQ^T += K^T dS^T), so that a
-// lane holds one query row and dS feeds the dQ MFMA straight from registers; an
-// MFMA with its operands exchanged gives the transposed scores bit for bit, so the
-// offline test sees the key-major kernel's scores.  dQ needs no atomics and is
-// bitwise reproducible.
-// A skipped tile costs its QK MFMAs and the test in both kernels.
+//   retained path         P = exp2(S - lse); dP^T = V dO^T; dS = P (dP - D_q);
+//                         dQ^T += K^T dS^T
+// mala_bwd_dkdv_kernel (key-major, Algorithm 2's traversal): one workgroup owns 128
+// keys of one (batch, KV head) and keeps their dK and dV in registers (no atomics,
+// bitwise reproducible); it sweeps the query tiles of every query head of the GQA
+// group from the end down to the diagonal, stepping only through the query tiles
+// that the dQ kernel retained for some of its four key tiles.  Sixteen wavefronts,
+// four roles per 32 keys on one SIMD, pipelined over those tiles: role 0 forms P
+// (fp32, handed on through LDS) and re-runs the offline test as a check, role 1
+// accumulates dV one tile later and moves the query tiles into LDS, role 2 forms dP
+// and dS, role 3 accumulates dK two tiles later (dS handed on as bf16 operands).
+// On small grids the sweeps run in parts whose sums mala_bwd_dkdv_reduce_kernel
+// adds.  An MFMA with its operands exchanged gives the transposed scores bit for
+// bit, so both kernels see the same scores.
+// P and dS enter the post-score MFMAs as two bf16 terms (hi + lo) unless an error
+// budget allows the hi term alone; the transposed A operands come through
+// ds_read_b64_tr_b16.  A skipped tile costs its QK MFMAs and the test in the dQ
+// kernel and nothing in the key-major kernel unless a neighbouring key tile of the
+// same query tile is retained.
 #include <algorithm>
 
 #include "mala_device.h"
