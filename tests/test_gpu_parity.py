@@ -821,13 +821,15 @@ def test_repeat_runs_bitwise_forward_dk_dv():
     assert torch.equal(r1["row_tiles"], r2["row_tiles"])
 
 
-def test_graph_capture_replays_match_eager():
+@pytest.mark.parametrize("name", ["gqa_d128_ragged", "split_d64_b2"])
+def test_graph_capture_replays_match_eager(name):
     # The library only launches kernels on the caller's stream (counters are
     # cleared by a kernel, not by hipMemsetAsync, and nothing is allocated), so a
     # fwd + bwd + decode step captured in a HIP graph replays to the eager results;
-    # every replay is checked, with eager work on the outputs in between.
+    # every replay is checked, with eager work on the outputs in between (the second
+    # case runs the split key-block sweeps and their reduction pass).
     tau = 1e-3
-    w, q, k, v, do = _train_case("gqa_d128_ragged", tau)
+    w, q, k, v, do = _train_case(name, tau)
     Q, K, V, DO = map(dev, (q, k, v, do))
     scale = f32(w.scale)
     B, Hq, N, D = Q.shape
@@ -913,6 +915,22 @@ def test_bf16_outputs(tau):
     for name, (got, ref) in rounded.items():
         err = np.abs(got - ref) - 2.0 ** -8 * np.abs(ref)
         assert err.max() <= TOL_MAX, (name, float(err.max()))
+
+
+@pytest.mark.parametrize("tau", [1e-3, 1.0])
+def test_bf16_gradients_with_split_sweeps(tau):
+    # split key-block sweeps: the parts' fp32 sums are added by the reduction pass,
+    # which rounds once at the store, so bf16 dK / dV are the fp32 ones rounded
+    w, q, k, v, do = _train_case("split_d64_b2", tau)
+    assert dkdv_splits(2, 8, 1, 6000)
+    Q, K, V, DO = map(dev, (q, k, v, do))
+    scale = f32(w.scale)
+    f = mala.fwd(Q, K, V, scale, tau)
+    gf = mala.bwd(Q, K, V, f["o"], f["lse"], DO, scale, tau)
+    gb = mala.bwd(Q, K, V, f["o"], f["lse"], DO, scale, tau, grad_dtype=torch.bfloat16)
+    torch.cuda.synchronize()
+    for x in ("dq", "dk", "dv"):
+        assert torch.equal(gb[x], gf[x].to(torch.bfloat16)), x
 
 
 def test_decode_bf16_output():
