@@ -11,14 +11,22 @@
 // its ceil(n_b / 32) tiles are cut into the splits as for a cache of n_b tokens.
 //
 // Per 32-key tile, in descending order inside the split:
-//   S^T = K_t Q^T     2 x 4 (D = 128) MFMAs 16x16x32, K loaded straight from HBM
-//                     into the A operand; lane (g, col) holds query head col and
-//                     8 of the 32 keys; K is prefetched two tiles ahead
+//   S^T = K_t Q^T     2 x 4 (D = 128) MFMAs 16x16x32; K arrives in registers in
+//                     whole contiguous rows (1 KB per load instruction), passes
+//                     through LDS and is read back as the A operands; lane
+//                     (g, col) holds query head col and 8 of the 32 keys; K is
+//                     prefetched two tiles ahead
 //   test              per head against that head's running (m, l) of the split
 //   retained (any)    V tile (fetched one tile ahead when a look-ahead test says
 //                     it may be needed) -> LDS; per head P = exp2(S - m_new) (0 for
 //                     heads that skip); O^T += V^T P^T with V^T through
 //                     ds_read_b64_tr_b16.
+// Every K and V load is a streaming buffer load (each byte is read once per call)
+// that is always issued: rows past the cache length, tiles outside the split and V
+// tiles the look-ahead test rules out have a resource of 0 bytes, read as zeros and
+// move no data.  With no load under a
+// branch, the compiler's waits count exactly the loads a step needs, so the next
+// K tile and the next V tile stay in flight while a tile is processed.
 // Partials (O / l, lse, count) go to the workspace; a second kernel merges the
 // splits with the normalizer-aware (log-sum-exp weighted) reduction.
 #include "mala_device.h"
@@ -32,6 +40,7 @@ __global__ __launch_bounds__(64) void mala_decode_split_kernel(DecParams p) {
   constexpr int NDB = D / 16;  // 16-row blocks of O^T
   constexpr int LD = D + 8;
   constexpr int VCH = kDecBk * D / 8 / 64;   // 16-byte V chunks per lane per tile
+  __shared__ __attribute__((aligned(16))) bf16 Ks[kDecBk * LD];
   __shared__ __attribute__((aligned(16))) bf16 Vs[kDecBk * LD];
 
   const int lane = threadIdx.x, g = lane >> 4, col = lane & 15;
@@ -57,6 +66,7 @@ __global__ __launch_bounds__(64) void mala_decode_split_kernel(DecParams p) {
 #pragma unroll
   for (int kk = 0; kk < KS; ++kk)
     qreg[kk] = head_valid ? load8(p.q + ((long)b * p.Hq + hq) * D + 32 * kk + 8 * g) : zero8();
+  wait_vm();   // no wait for these loads is left for the tile loop
 
   const bf16* Kp = p.k + (long)bhk * p.Nk * D;
   const bf16* Vp = p.v + (long)bhk * p.Nk * D;
@@ -69,34 +79,45 @@ __global__ __launch_bounds__(64) void mala_decode_split_kernel(DecParams p) {
   unsigned vloads = 0, vfetch = 0;   // V tiles consumed / fetched (statistics)
   unsigned long long hsum = 0;       // fingerprints of this head's retained tiles
 
-  // K of a tile as A operands: rows kb + col (block 0) and kb + 16 + col (block 1)
-  bf16x8 ka[KS], kb1[KS];
-  auto load_k = [&](int t) {
-    const long k0 = (long)t * kDecBk + col, k1 = k0 + 16;
-#pragma unroll
-    for (int kk = 0; kk < KS; ++kk) {
-      ka[kk] = k0 < n ? load8(Kp + k0 * D + 32 * kk + 8 * g) : zero8();
-      kb1[kk] = k1 < n ? load8(Kp + k1 * D + 32 * kk + 8 * g) : zero8();
-    }
+  // A K or V tile in registers as whole rows: lane chunk e holds the 16 bytes at
+  // byte 16 (lane + 64 e) of the tile, row (lane + 64 e) / (D / 8).  The resource
+  // covers the tile's rows below n when the tile is wanted and nothing otherwise.
+  auto tile_rsrc = [&](const bf16* base, int t, bool want) {
+    const long k0 = (long)max(t, 0) * kDecBk;
+    const long rows = want && t >= 0 ? min((long)kDecBk, (long)n - k0) : 0;
+    return make_rsrc(base + k0 * D, (uint32_t)(rows > 0 ? rows * D * 2 : 0));
   };
-  // V of a tile into registers (row-major chunks); written to LDS when needed
-  bf16x8 vr[VCH];
-  auto load_v = [&](int t) {
-    const long kb = (long)t * kDecBk;
+  bf16x8 kr[VCH], vr[VCH];
+  auto load_k = [&](int t) {
+    const auto r = tile_rsrc(Kp, t, t >= t_lo);
+#pragma unroll
+    for (int e = 0; e < VCH; ++e) kr[e] = buf_load8_stream(r, 16u * (lane + 64 * e));
+  };
+  auto load_v = [&](int t, bool want) {
+    const auto r = tile_rsrc(Vp, t, want && t >= t_lo);
+#pragma unroll
+    for (int e = 0; e < VCH; ++e) vr[e] = buf_load8_stream(r, 16u * (lane + 64 * e));
+  };
+  // tile rows to LDS (row stride LD keeps the operand reads below conflict-free)
+  auto to_lds = [&](bf16* dst, const bf16x8 (&x)[VCH]) {
 #pragma unroll
     for (int e = 0; e < VCH; ++e) {
       const int ch = lane + 64 * e;
-      const int row = ch / (D / 8), c8 = (ch % (D / 8)) * 8;
-      vr[e] = kb + row < n ? load8(Vp + (kb + row) * D + c8) : zero8();
+      store8(dst + (ch / (D / 8)) * LD + (ch % (D / 8)) * 8, x[e]);
     }
   };
-  // base-2 scores of tile t for this lane's head (8 keys) and their max over the tile
+  // Base-2 scores of the tile whose K is in kr, for this lane's head (8 keys), and
+  // their max over the tile; the next K tile (t - 1) starts loading as soon as kr
+  // is in LDS.  One wavefront per workgroup: its LDS accesses complete in issue
+  // order, so the reads below see the stores and the next stores follow the reads.
   auto scores = [&](int t, float (&sv)[8]) {
+    to_lds(Ks, kr);
+    load_k(t - 1);
     f32x4 s0 = {0.f, 0.f, 0.f, 0.f}, s1 = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int kk = 0; kk < KS; ++kk) {
-      s0 = mfma16(ka[kk], qreg[kk], s0);
-      s1 = mfma16(kb1[kk], qreg[kk], s1);
+      s0 = mfma16(load8(Ks + col * LD + 32 * kk + 8 * g), qreg[kk], s0);
+      s1 = mfma16(load8(Ks + (16 + col) * LD + 32 * kk + 8 * g), qreg[kk], s1);
     }
     const long kb = (long)t * kDecBk;
     float mt = kNegInf;
@@ -124,30 +145,24 @@ __global__ __launch_bounds__(64) void mala_decode_split_kernel(DecParams p) {
   float mt = kNegInf, mtn = kNegInf;
   if (t_hi > t_lo) {
     load_k(t_hi - 1);
-    mt = scores(t_hi - 1, sv);
-    load_v(t_hi - 1);     // the first tile of a split is always retained (l = 0)
+    mt = scores(t_hi - 1, sv);   // also starts K of t_hi - 2
+    load_v(t_hi - 1, true);      // the first tile of a split is always retained (l = 0)
     ++vfetch;
-    if (t_hi - 2 >= t_lo) load_k(t_hi - 2);
   }
   for (int t = t_hi - 1; t >= t_lo; --t) {
     const bool has_next = t - 1 >= t_lo;
-    if (has_next) {
-      mtn = scores(t - 1, sn);
-      if (t - 2 >= t_lo) load_k(t - 2);
-    }
+    mtn = scores(t - 1, sn);     // zeros past the split's first tile, not used then
     const float lse_run = m + fast_log2(l);
     const bool demand = head_valid && (l == 0.f || (mt - lse_run >= thr2));
     const bool hint =
         has_next && wave_any(head_valid && (l == 0.f || (mtn - lse_run >= thr2 - kHintMargin)));
-    if (wave_any(demand)) {
-      __syncthreads();   // the previous tile's transposed reads are done
-#pragma unroll
-      for (int e = 0; e < VCH; ++e) {
-        const int ch = lane + 64 * e;
-        const int row = ch / (D / 8), c8 = (ch % (D / 8)) * 8;
-        store8(Vs + row * LD + c8, vr[e]);
-      }
-      __syncthreads();
+    // V of tile t goes to LDS, and V of t - 1 (if the look-ahead test wants it) starts
+    // loading into the freed registers before tile t's update runs
+    const bool any_demand = wave_any(demand);
+    if (any_demand) to_lds(Vs, vr);
+    load_v(t - 1, hint);
+    vfetch += hint ? 1u : 0u;
+    if (any_demand) {
       ++vloads;
       float alpha = 1.f, m_new = m;
       if (demand) {
@@ -178,10 +193,6 @@ __global__ __launch_bounds__(64) void mala_decode_split_kernel(DecParams p) {
         acc[db] = mfma16(a, ph, acc[db] * alpha);
         acc[db] = mfma16(a, pl, acc[db]);
       }
-    }
-    if (hint) {
-      load_v(t - 1);
-      ++vfetch;
     }
 #pragma unroll
     for (int r = 0; r < 8; ++r) sv[r] = sn[r];
