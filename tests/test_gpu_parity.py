@@ -512,6 +512,34 @@ def test_decode_per_sequence_cache_lengths(spec, lens, splits, tau):
     _check_decode_counters(cd, keeps, exs, w.Hkv)
 
 
+@pytest.mark.parametrize("tau", [0.0, 1e-3])
+def test_decode_never_reads_cache_rows_past_a_length(tau):
+    # rows at and past a sequence's cache length play no part: filling them with NaN
+    # leaves every output and statistic bitwise unchanged (lengths off the 32-key
+    # grid, so each sequence ends in a ragged tile, and one sequence shorter than
+    # one split's share of the tiles)
+    spec = dict(kind="decode", B=3, Hq=8, Hkv=2, N=3001, D=128, beta=3.0, needles=4)
+    w = Workload(spec)
+    t = {x: np.array(y) for x, y in w.tensors().items()}
+    lens = [3001, 1000, 37]
+    cl = torch.tensor(lens, dtype=torch.int32, device="cuda")
+
+    def run():
+        g = mala.decode(dev(t["q"]), dev(t["k"]), dev(t["v"]), f32(w.scale), tau, 4,
+                        cache_lens=cl)
+        torch.cuda.synchronize()
+        return {x: y.cpu() for x, y in g.items()}
+
+    clean = run()
+    for b, n in enumerate(lens):
+        t["k"][b, :, n:] = NAN_BITS
+        t["v"][b, :, n:] = NAN_BITS
+    bad = run()
+    assert torch.isfinite(bad["o"]).all()
+    for name in clean:
+        assert torch.equal(bad[name], clean[name]), name
+
+
 def test_decode_full_lengths_match_uniform_path():
     # cache_lens all equal to Nk is the uniform decode (bitwise at tau = 0, where
     # the threshold plays no part)
