@@ -259,4 +259,18 @@ __device__ __forceinline__ bf16x8 hi_bf16x8(const float* x) {
   return hi;
 }
 
+// The low bf16 terms of x given its high terms hi (as hi_bf16x8 returned them).
+__device__ __forceinline__ bf16x8 lo_bf16x8(const float* x, bf16x8 hi) {
+  bf16x8 lo;
+#pragma unroll
+  for (int i = 0; i < 8; i += 2) {
+    const uint32_t u = __builtin_bit_cast(uint32_t, bf16x2{hi[i], hi[i + 1]});
+    const float h0 = __uint_as_float(u << 16), h1 = __uint_as_float(u & 0xffff0000u);
+    const bf16x2 l2 = __builtin_convertvector((f32x2{x[i] - h0, x[i + 1] - h1}), bf16x2);
+    lo[i] = l2[0];
+    lo[i + 1] = l2[1];
+  }
+  return lo;
+}
+
 }  // namespace mala

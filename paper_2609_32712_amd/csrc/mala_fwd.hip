@@ -183,6 +183,16 @@ __global__ __launch_bounds__(kFwdWaves * 64) void mala_fwd_kernel(FwdParams p) {
         if (!wave_any(demand)) continue;    // skipped: m, l and O unchanged
         ++n_ret;
         cnt += voter ? 1 : 0;
+        // O^T[d][q] += V^T[d][key] P^T[key][q]; V^T rows through transposed LDS reads,
+        // issued before the softmax work so that their latency hides under it
+        bf16x8 va[DB][2];
+#pragma unroll
+        for (int db = 0; db < DB; ++db)
+#pragma unroll
+          for (int ks = 0; ks < 2; ++ks) {
+            const bf16* vt = vtb + (sub * kBk + 16 * ks) * (D + 8) + tr_step<D>(db);
+            va[db][ks] = cat(lds_read_tr(vt), lds_read_tr(vt + 8 * (D + 8)));
+          }
         if (stats) {
           hsum += tile_hash(b, hq, q0w / kBq, j);
           // the first wavefront to retain this tile of the stage counts its V tile
@@ -218,28 +228,13 @@ __global__ __launch_bounds__(kFwdWaves * 64) void mala_fwd_kernel(FwdParams p) {
         // share of every row's retained normalizer (this tile included) runs the
         // high term only.
         const bool need_lo = wave_any(ps > kFwdLoShare * l);
-        bf16x8 ph[2], pl[2];
-        if (need_lo) {
-          split_bf16x8(sv, ph[0], pl[0]);
-          split_bf16x8(sv + 8, ph[1], pl[1]);
-        } else {
-          ph[0] = hi_bf16x8(sv);
-          ph[1] = hi_bf16x8(sv + 8);
-        }
-        // O^T[d][q] += V^T[d][key] P^T[key][q]; V^T rows through transposed LDS reads
-        bf16x8 va[DB][2];
-#pragma unroll
-        for (int db = 0; db < DB; ++db)
-#pragma unroll
-          for (int ks = 0; ks < 2; ++ks) {
-            const bf16* vt = vtb + (sub * kBk + 16 * ks) * (D + 8) + tr_step<D>(db);
-            va[db][ks] = cat(lds_read_tr(vt), lds_read_tr(vt + 8 * (D + 8)));
-          }
+        const bf16x8 ph[2] = {hi_bf16x8(sv), hi_bf16x8(sv + 8)};
 #pragma unroll
         for (int ks = 0; ks < 2; ++ks)
 #pragma unroll
           for (int db = 0; db < DB; ++db) acc[db] = mfma32(va[db][ks], ph[ks], acc[db]);
         if (need_lo) {
+          const bf16x8 pl[2] = {lo_bf16x8(sv, ph[0]), lo_bf16x8(sv + 8, ph[1])};
 #pragma unroll
           for (int ks = 0; ks < 2; ++ks)
 #pragma unroll
