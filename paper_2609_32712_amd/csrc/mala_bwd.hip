@@ -3,7 +3,9 @@
 //
 // mala_bwd_dq_kernel (query-major, like the forward) runs first and takes every
 // tile decision: one workgroup = 8 wavefronts = 256 query rows; K and V stream
-// through double-buffered LDS.  It computes the transposed products (S^T = K Q^T,
+// through double-buffered LDS one 128-key block at a time (four decision tiles per
+// wavefront between barriers, which evens out the work of wavefronts that retain
+// different numbers of tiles).  It computes the transposed products (S^T = K Q^T,
 // dP^T = V dO^T, dQ^T += K^T dS^T), so that a lane holds one query row and dS feeds
 // the dQ MFMA straight from registers.  It records its decisions, one byte per
 // (query tile, query head, 128-key block), for the key-major kernel.  dQ needs no
@@ -649,7 +651,10 @@ template <int D>
 __global__ __launch_bounds__(kDqWaves * 64) void mala_bwd_dq_kernel(BwdParams p) {
   constexpr int KS = D / 16;
   constexpr int DB = D / 32;
-  constexpr int STAGE = tile_elems<D>(kFwdStage);
+  constexpr int kDqStage = kBwdKeys;             // keys per K / V stage: one 128-key block
+  constexpr int TPS = kDqStage / kBk;            // decision tiles per stage
+  constexpr int STAGE = tile_elems<D>(kDqStage);
+  static_assert(TPS == 4, "a stage is one decision byte's block");
   __shared__ __attribute__((aligned(16))) bf16 Ks[2 * STAGE];
   __shared__ __attribute__((aligned(16))) bf16 Vs[2 * STAGE];
   __shared__ unsigned long long bcnt[kNumCounters];   // the workgroup's counter sums
@@ -701,16 +706,16 @@ __global__ __launch_bounds__(kDqWaves * 64) void mala_bwd_dq_kernel(BwdParams p)
   const int jdiag = (q0w < Nq) ? (int)((qlast_w + off) / kBk) : -1;
   const int nvalid = max(0, min(kBq, Nq - q0w));
   const int qlast_g = min(qblk * kDqRows + kDqRows - 1, Nq - 1);
-  const int ttop = (int)((qlast_g + off) / kFwdStage);
+  const int ttop = (int)((qlast_g + off) / kDqStage);
   unsigned n_legal = 0, n_ret = 0;
   unsigned long long hsum = 0;   // fingerprints of the retained tiles
   int cnt_row = 0;   // retained tiles in which row qrow has a legal key
   // The decisions for the key-major pass: one byte per 128-key block of this
   // wavefront's query tile and head, bit j % 4 for key tile j, the blocks contiguous
-  // (mask_index).  A stage covers key tiles 2t and 2t + 1, half of block t / 2; the
-  // block's byte is complete after its lower stage (t even) and goes into lane
-  // (t / 2) % 64 of pack; after block 64 m the group of 64 blocks goes out in one
-  // coalesced store (the first group only up to the workgroup's top block).  Every
+  // (mask_index).  Stage t is block t (key tiles 4t .. 4t + 3); the block's byte is
+  // complete after the stage and goes into lane t % 64 of pack; after block 64 m the
+  // group of 64 blocks goes out in one coalesced store (the first group only up to
+  // the workgroup's top block).  Every
   // block up to the diagonal is written (blocks above this wavefront's diagonal get
   // zero), so the buffer needs no clearing.
   uint8_t* mrow = p.mask + mask_index(p, mask_row0(p, b, sg) + q0w / kBq, hq, 0);
@@ -729,7 +734,7 @@ __global__ __launch_bounds__(kDqWaves * 64) void mala_bwd_dq_kernel(BwdParams p)
 #pragma unroll
   for (int u = 0; u < NJS; ++u) dma_off[u] = dma_lane_offset<D>(64 * (wave + kDqWaves * u) + lane);
   auto fetch = [&](int t, int buf) {
-    const long k0 = (long)t * kFwdStage;
+    const long k0 = (long)t * kDqStage;
     const uint32_t nb = (uint32_t)(Nk - k0) * (uint32_t)D * 2u;
     const i32x4 rk = rsrc_words(Kp + k0 * D, nb), rvv = rsrc_words(Vp + k0 * D, nb);
 #pragma unroll
@@ -755,11 +760,11 @@ __global__ __launch_bounds__(kDqWaves * 64) void mala_bwd_dq_kernel(BwdParams p)
     const bf16* vr = lds_pin(Vb + rdo);
     const bf16* ktb = lds_pin(Kb + tro);
     // the two wavefronts of a SIMD keep pace: the one with more of the stage left
-    // issues first (priority 2, then 1 for the second tile, 0 at the barrier)
+    // issues first (priority 2 for the first two tiles, then 1, 0 at the barrier)
 #pragma unroll 1
-    for (int sub = 1; sub >= 0; --sub) {
-      if (sub) __builtin_amdgcn_s_setprio(2); else __builtin_amdgcn_s_setprio(1);
-      const int j = 2 * t + sub;
+    for (int sub = TPS - 1; sub >= 0; --sub) {
+      if (sub > 1) __builtin_amdgcn_s_setprio(2); else __builtin_amdgcn_s_setprio(1);
+      const int j = TPS * t + sub;
       if (j > jdiag) continue;
       const long kb = (long)j * kBk;
       ++n_legal;
@@ -828,14 +833,14 @@ __global__ __launch_bounds__(kDqWaves * 64) void mala_bwd_dq_kernel(BwdParams p)
       }
     }
     __builtin_amdgcn_s_setprio(0);
-    if (!(t & 1) && mwave) {
-      // block t / 2 is complete
-      const int blk = t >> 1;
+    if (mwave) {
+      // block t is complete
+      const int blk = t;
       if (lane == (blk & 63)) pack = (uint32_t)nib;
       nib = 0;
       if (!(blk & 63)) {
-        // the group's blocks blk .. blk + 63, up to the workgroup's top block ttop / 2
-        if (lane <= (ttop >> 1) - blk) mrow[blk + lane] = (uint8_t)pack;
+        // the group's blocks blk .. blk + 63, up to the workgroup's top block ttop
+        if (lane <= ttop - blk) mrow[blk + lane] = (uint8_t)pack;
         stored = 1;
       }
     }
