@@ -1,8 +1,9 @@
 """Build libmala.so (HIP, gfx950 only) in-tree.
 
 Every .hip file under csrc/ is compiled with hipcc for gfx950 and linked into
-paper_2609_32712_amd/libmala.so next to this file.  Packed-fp32 instruction
-selection is switched off for all device code.  The forward kernel is scheduled
+paper_2609_32712_amd/libmala.so next to this file; probe/mfma_probe.hip becomes
+libmala_probe.so, the benchmark's MFMA-rate probe (not part of the library's
+ABI).  Packed-fp32 instruction selection is switched off for all device code.  The forward kernel is scheduled
 with LLVM's iterative ILP strategy, which measured ~2% faster on every forward
 workload (same instructions and results, another order); the other kernels
 measured no better with any of the strategies and keep the default.
@@ -20,6 +21,7 @@ ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 OBJ = os.path.join(ROOT, "_build")
 LIB = os.path.join(HERE, "libmala.so")
+PROBE_LIB = os.path.join(HERE, "libmala_probe.so")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = ["--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC",
          "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
@@ -48,8 +50,16 @@ def build(verbose: bool = False) -> str:
     tmp = LIB + ".tmp%d" % os.getpid()
     subprocess.check_call([HIPCC, "--offload-arch=gfx950", "-shared", "-fPIC", *objs, "-o", tmp])
     os.replace(tmp, LIB)
+    # the benchmark's MFMA-rate probe, a library of its own (not part of the ABI)
+    probe_src = os.path.join(HERE, "probe", "mfma_probe.hip")
+    probe_tmp = PROBE_LIB + ".tmp%d" % os.getpid()
+    r = subprocess.run([HIPCC, *FLAGS, "-shared", probe_src, "-o", probe_tmp],
+                       capture_output=True, text=True)
+    if r.returncode != 0:
+        raise RuntimeError("hipcc failed for %s:\n%s" % (probe_src, r.stdout + r.stderr))
+    os.replace(probe_tmp, PROBE_LIB)
     if verbose:
-        print("built", LIB)
+        print("built", LIB, "and", PROBE_LIB)
     return LIB
 
 
