@@ -673,6 +673,7 @@ __global__ __launch_bounds__(kDqWaves * 64) void mala_bwd_dq_kernel(BwdParams p)
   if (qblk * kDqRows >= Nq) return;   // past the end of a packed sequence
   const long off = (long)Nk - Nq;
   const int q0w = qblk * kDqRows + wave * kBq;
+  const int offi = Nk - Nq;   // off as an int (|off| < 2^31)
   const int qrow = q0w + c;
   const bool row_valid = qrow < Nq;
   const long qbase = sg.qb + (long)hq * p.Nq;    // row 0 of this (sequence, head)
@@ -709,7 +710,8 @@ __global__ __launch_bounds__(kDqWaves * 64) void mala_bwd_dq_kernel(BwdParams p)
   const int ttop = (int)((qlast_g + off) / kDqStage);
   unsigned n_legal = 0, n_ret = 0;
   unsigned long long hsum = 0;   // fingerprints of the retained tiles
-  int cnt_row = 0;   // retained tiles in which row qrow has a legal key
+  int cnt_row = 0;   // retained diagonal tiles in which row qrow has a legal key
+  unsigned n_ret_m = 0;  // retained diagonal tiles
   // The decisions for the key-major pass: one byte per 128-key block of this
   // wavefront's query tile and head, bit j % 4 for key tile j, the blocks contiguous
   // (mask_index).  Stage t is block t (key tiles 4t .. 4t + 3); the block's byte is
@@ -766,16 +768,15 @@ __global__ __launch_bounds__(kDqWaves * 64) void mala_bwd_dq_kernel(BwdParams p)
       if (sub > 1) __builtin_amdgcn_s_setprio(2); else __builtin_amdgcn_s_setprio(1);
       const int j = TPS * t + sub;
       if (j > jdiag) continue;
-      const long kb = (long)j * kBk;
+      const int kb = j * kBk;
       ++n_legal;
       bf16x8 kop[KS];
 #pragma unroll
       for (int kk = 0; kk < KS; ++kk) kop[kk] = load8(kr + sub * kBk * (D + 8) + rd_step<D>(kk));
       const f32x16 s = qk_tile<KS>(kop, qb);
-      const bool need_mask =
-          (kb + kBk - 1 > (long)q0w + off) || (q0w + kBq > Nq) || (kb + kBk > Nk);
-      const int kmax = (int)((long)qrow + off - kb) - 4 * h;
-      const int klim = (int)min((long)Nk - kb, (long)kBk) - 4 * h;
+      const bool need_mask = (kb + kBk - 1 > q0w + offi) || (q0w + kBq > Nq) || (kb + kBk > Nk);
+      const int kmax = qrow + offi - kb - 4 * h;
+      const int klim = min(Nk - kb, kBk) - 4 * h;
       float sv[16];
       const bool dem = need_mask ? offline_test_t<true>(s, p.scale2, kmax, klim, thr, sv)
                                  : offline_test_t<false>(s, p.scale2, kmax, klim, thr, sv);
@@ -784,7 +785,12 @@ __global__ __launch_bounds__(kDqWaves * 64) void mala_bwd_dq_kernel(BwdParams p)
       if (!ret) continue;
       ++n_ret;
       if (p.counters) hsum += tile_hash(b, hq, q0w / kBq, j);
-      cnt_row += (row_valid && kb <= (long)qrow + off) ? 1 : 0;
+      // off the diagonal and the sequence end every row has a legal key: those tiles
+      // are counted per wavefront
+      if (need_mask) {
+        ++n_ret_m;
+        cnt_row += (row_valid && kb <= qrow + offi) ? 1 : 0;
+      }
       // P^T = exp2(s * scale2 - lse2), the key-major kernel's arithmetic
 #pragma unroll
       for (int r = 0; r < 16; ++r) sv[r] = fast_exp2(__builtin_fmaf(sv[r], p.scale2, -lse2));
@@ -866,7 +872,7 @@ __global__ __launch_bounds__(kDqWaves * 64) void mala_bwd_dq_kernel(BwdParams p)
                           acc[db][4 * g + 2] * p.scale, acc[db][4 * g + 3] * p.scale};
         store_out4(p.dq, qr + 32 * db + 8 * g + 4 * h, v4, p.grad_bf16);
       }
-    if (p.row_tiles && h == 0) p.row_tiles[qbase + qrow] = cnt_row;
+    if (p.row_tiles && h == 0) p.row_tiles[qbase + qrow] = cnt_row + (int)(n_ret - n_ret_m);
   }
   if (p.counters) {
     if (lane == 0) {

@@ -57,6 +57,7 @@ __global__ __launch_bounds__(kFwdWaves * 64) void mala_fwd_kernel(FwdParams p) {
   const int Nq = sg.Nq, Nk = sg.Nk;
   if (qblk * kFwdRows >= Nq) return;   // past the end of a packed sequence
   const long off = (long)Nk - Nq;
+  const int offi = Nk - Nq;   // off as an int (|off| < 2^31)
   const int q0w = qblk * kFwdRows + wave * kBq;
   const int qrow = q0w + c;
   const bool row_valid = qrow < Nq;
@@ -79,7 +80,8 @@ __global__ __launch_bounds__(kFwdWaves * 64) void mala_fwd_kernel(FwdParams p) {
   for (int db = 0; db < DB; ++db)
 #pragma unroll
     for (int r = 0; r < 16; ++r) acc[db][r] = 0.f;
-  int cnt = 0;
+  int cnt = 0;          // retained diagonal tiles in which this row has a legal key
+  unsigned n_ret_m = 0;  // retained diagonal tiles
   const float thr = p.log2tau - log2f((float)(qrow + 1 + off));   // log2(tau / L_q)
 
   const int qlast_w = min(q0w + kBq - 1, Nq - 1);
@@ -139,7 +141,7 @@ __global__ __launch_bounds__(kFwdWaves * 64) void mala_fwd_kernel(FwdParams p) {
       for (int sub = 1; sub >= 0; --sub) {
         const int j = 2 * t + sub;
         if (j > jdiag) continue;            // above this wavefront's diagonal
-        const long kb = (long)j * kBk;
+        const int kb = j * kBk;
         ++n_legal;
         // score discovery (all K operands are read from LDS first)
         f32x16 s;
@@ -153,12 +155,12 @@ __global__ __launch_bounds__(kFwdWaves * 64) void mala_fwd_kernel(FwdParams p) {
           for (int kk = 0; kk < KS; ++kk) s = mfma32(ka[kk], qreg[kk], s);
         }
 
-        const bool need_mask = (kb + kBk - 1 > (long)q0w + off) || (q0w + kBq > Nq);
+        const bool need_mask = (kb + kBk - 1 > q0w + offi) || (q0w + kBq > Nq);
         float sv[16];
         float mt = kNegInf;
         if (need_mask) {
           // keys of this lane: kb + 8 (r / 4) + 4 h + r % 4; legal iff key <= qrow + off
-          const int lim = row_valid ? (int)((long)qrow + off - kb) - 4 * h : -1000000;
+          const int lim = row_valid ? qrow + offi - kb - 4 * h : -1000000;
 #pragma unroll
           for (int r = 0; r < 16; ++r) {
             const float x = (8 * (r >> 2) + (r & 3) <= lim) ? s[r] : kNegInf;
@@ -178,11 +180,15 @@ __global__ __launch_bounds__(kFwdWaves * 64) void mala_fwd_kernel(FwdParams p) {
 
         // the online test (rows with no legal key in the tile do not vote); m + log2(l)
         // is log2 of the retained normalizer whichever reference m the row uses
-        const bool voter = row_valid && (kb <= qrow + off);
-        const bool demand = voter && (l == 0.f || (mt - m - fast_log2(l) >= thr));
+        const bool voter = row_valid & (kb <= qrow + offi);
+        const bool demand = voter & ((l == 0.f) | (mt - m - fast_log2(l) >= thr));
         if (!wave_any(demand)) continue;    // skipped: m, l and O unchanged
         ++n_ret;
-        cnt += voter ? 1 : 0;
+        // off the diagonal every valid row votes: those tiles are counted per wavefront
+        if (need_mask) {
+          ++n_ret_m;
+          cnt += voter ? 1 : 0;
+        }
         // O^T[d][q] += V^T[d][key] P^T[key][q]; V^T rows through transposed LDS reads,
         // issued before the softmax work so that their latency hides under it
         bf16x8 va[DB][2];
@@ -261,7 +267,7 @@ __global__ __launch_bounds__(kFwdWaves * 64) void mala_fwd_kernel(FwdParams p) {
       }
     if (h == 0) {
       p.lse[qbase + qrow] = (m + fast_log2(l)) * kLn2;
-      if (p.row_tiles) p.row_tiles[qbase + qrow] = cnt;
+      if (p.row_tiles) p.row_tiles[qbase + qrow] = cnt + (int)(n_ret - n_ret_m);
     }
   }
   if (stats) {
