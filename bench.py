@@ -39,15 +39,15 @@ def log(*a):
 class Train:
     """Device-resident inputs, outputs and workspace of one fwd+bwd workload."""
 
-    def __init__(self, cfg_id, tau, **over):
+    def __init__(self, name, tau, **over):
         import torch
         import paper_2609_32712_amd as mala
         from workloads import Workload
-        self.w = Workload(cfg_id, **over)
+        self.w = Workload(name, **over)
         self.tau = tau
         t0 = time.time()
         t = self.w.tensors(threads=16)
-        log("cfg%d %s inputs generated in %.1fs" % (cfg_id, over or "", time.time() - t0))
+        log("%s %s inputs generated in %.1fs" % (name, over or "", time.time() - t0))
         dev = lambda b: torch.from_numpy(b.view(np.int16)).to("cuda").view(torch.bfloat16)
         self.q, self.k, self.v, self.do = (dev(t[x]) for x in ("q", "k", "v", "do"))
         del t
@@ -95,14 +95,14 @@ class Train:
 
 
 class Decode:
-    def __init__(self, cfg_id, tau, splits=None):
+    def __init__(self, name, tau, splits=None):
         import torch
         import paper_2609_32712_amd as mala
         from workloads import Workload
-        self.w = Workload(cfg_id)
+        self.w = Workload(name)
         t0 = time.time()
         t = self.w.tensors(threads=16)
-        log("cfg%d inputs generated in %.1fs" % (cfg_id, time.time() - t0))
+        log("%s inputs generated in %.1fs" % (name, time.time() - t0))
         dev = lambda b: torch.from_numpy(b.view(np.int16)).to("cuda").view(torch.bfloat16)
         self.q, self.k, self.v = (dev(t[x]) for x in ("q", "k", "v"))
         del t
@@ -242,15 +242,15 @@ def time_train(tr, taus, timing):
     return out
 
 
-def train_config(cfg_id, taus, reps, warmup, supp_taus=(), supp=None, memory=True):
+def train_workload(name, taus, reps, warmup, supp_taus=(), supp=None, memory=True):
     """One training workload: fwd / bwd latency (HIP events, mean and median of reps
     calls after warmup) at tau = 0 (dense through the same kernels) and at each tau,
     the speed-ups over dense, the retained work and the V / dO loads the retained
     tiles needed, executed and dense-equivalent TFLOP/s, and the operators' device
     memory."""
     import torch
-    from workloads import CONFIGS
-    tr = Train(cfg_id, 0.0)
+    from workloads import WORKLOADS
+    tr = Train(name, 0.0)
     w = tr.w
     mala = tr.mala
     bq, bk = mala.mala_geometry(w.D, mala.PASS_FWD)
@@ -260,7 +260,7 @@ def train_config(cfg_id, taus, reps, warmup, supp_taus=(), supp=None, memory=Tru
     do_dense = dense_do_tiles(w.B, w.Hq, w.Hkv, w.N)
     res = time_train(tr, (0.0,) + tuple(x for x in taus if x != 0.0),
                      lambda t_: supp if t_ in supp_taus else (reps, warmup))
-    out = {"workload": CONFIGS[cfg_id]["desc"], "shape": [w.B, w.Hq, w.Hkv, w.N, w.D]}
+    out = {"workload": WORKLOADS[name]["desc"], "shape": [w.B, w.Hq, w.Hkv, w.N, w.D]}
     f0, b0 = res[0.0][0][0], res[0.0][1][0]
     for t_, (f, b, cf, cb) in res.items():
         fl_f, fl_b = train_flops(cf, cb, w.D, bq, bk)
@@ -281,8 +281,8 @@ def train_config(cfg_id, taus, reps, warmup, supp_taus=(), supp=None, memory=Tru
         }
     if memory:
         out["operator_memory"] = operator_memory(tr, taus[0])
-    log("cfg%d dense fwd %.3f bwd %.3f ms | %s" % (
-        cfg_id, f0, b0, " ".join("tau=%g fwd %.3f bwd %.3f" % (t_, r[0][0], r[1][0])
+    log("%s dense fwd %.3f bwd %.3f ms | %s" % (
+        name, f0, b0, " ".join("tau=%g fwd %.3f bwd %.3f" % (t_, r[0][0], r[1][0])
                                  for t_, r in res.items() if t_)))
     del tr, res
     torch.cuda.empty_cache()
@@ -345,7 +345,7 @@ def lm_sweep(reps, warmup, lengths=LM_SWEEP_N):
     import torch
     rows = []
     for N in lengths:
-        tr = Train(6, 0.0, N=N, B=max(1, LM_SWEEP_TOKENS // N))
+        tr = Train("lm_like_gqa8x2_32k", 0.0, N=N, B=max(1, LM_SWEEP_TOKENS // N))
         w = tr.w
         nrows = w.B * w.Hq * w.N
         runs = {}
@@ -381,12 +381,12 @@ def lm_sweep(reps, warmup, lengths=LM_SWEEP_N):
 
 
 def mfma_probe(reps=5, blocks=256 * 12, iters=4096):
-    """The bf16 MFMA rate this box sustains under a pure MFMA load: libmala_probe.so
+    """The bf16 MFMA rate this machine sustains under a pure MFMA load: libmala_probe.so
     runs chains of v_mfma_f32_32x32x16_bf16 with operands in registers and no memory
     traffic (three wavefronts per SIMD, 256 x 12 workgroups of four), timed with HIP
     events on the current stream; the implied clock is the rate over 1024 flops per
     SIMD per cycle (32x32x16 x 2 flops in 32 cycles) x 1024 SIMDs.  Context for the
-    box's power state, not the roofline's peak.  None if the probe is not built."""
+    machine's power state, not the roofline's peak.  None if the probe is not built."""
     import ctypes
     import torch
     path = os.path.join(ROOT, "paper_2609_32712_amd", "libmala_probe.so")
@@ -416,8 +416,8 @@ def mfma_probe(reps=5, blocks=256 * 12, iters=4096):
             "implied_mfma_clock_ghz": round(tflops * 1e12 / (1024.0 * 1024.0) / 1e9, 3),
             "ms": round(ms, 3),
             "note": "independent v_mfma_f32_32x32x16_bf16 chains, operands in registers, "
-                    "no memory traffic, on every CU: the rate this box sustains under a pure "
-                    "MFMA load (its power management lowers the clock on some boxes; the "
+                    "no memory traffic, on every CU: the rate this machine sustains under a pure "
+                    "MFMA load (its power management lowers the clock on some machines; the "
                     "attention kernels, at 38-54% MFMA issue, run at ~2.0-2.3 GHz)"}
 
 
@@ -464,7 +464,7 @@ def cpu_baseline(step_ms_model):
     import paper_2609_32712_amd as mala
     oracle.build()
     cores = int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1))
-    w = Workload(4)
+    w = Workload("gqa8x2_128k")
     bq, bk = mala.mala_geometry(w.D, mala.PASS_FWD)
     Tr = -(-w.N // bq)
     nb = min(Tr, 8 * cores)
@@ -494,7 +494,7 @@ def cpu_baseline(step_ms_model):
     total_tiles = w.Hq * Tr * (Tr + 1) / 2
     ms_fwd = t_f * 1e3 * total_tiles / q_tiles
     ms_bwd = (t_q / q_tiles + t_k / k_tiles) * 1e3 * total_tiles
-    wd = Workload(5)
+    wd = Workload("decode_gqa32x8_128k")
     sd = mala.default_num_splits(wd.B, wd.Hkv, wd.N)
     qd = bf16_to_f64(wd.q_head(0, 0))[None, None]
     kd = bf16_to_f64(wd.k_head(0, 0))[None, None]
@@ -542,11 +542,11 @@ def counter_pass(which="bwd"):
     torch.cuda.synchronize()
     del x, y
     if which == "decode":
-        dec = Decode(5, 1e-4)
+        dec = Decode("decode_gqa32x8_128k", 1e-4)
         for _ in range(2):
             dec.run(1e-4)
     else:
-        tr = Train(4, 1e-4)
+        tr = Train("gqa8x2_128k", 1e-4)
         for _ in range(2):
             tr.fwd(1e-4)
             tr.bwd(1e-4)
@@ -568,7 +568,7 @@ def skip_pass():
     import torch
     import paper_2609_32712_amd as mala
     mala.load_library()
-    tr = Train(6, 0.0)
+    tr = Train("lm_like_gqa8x2_32k", 0.0)
     for tau in SKIP_TAUS:
         for _ in range(3):
             tr.fwd(tau)
@@ -880,8 +880,8 @@ def main():
     mala.load_library()
     tau = args.tau
 
-    tr = Train(4, tau)
-    dec = Decode(5, tau)
+    tr = Train("gqa8x2_128k", tau)
+    dec = Decode("decode_gqa32x8_128k", tau)
     w = tr.w
     bq, bk = mala.mala_geometry(w.D, mala.PASS_FWD)
 
@@ -1038,11 +1038,11 @@ def main():
     rw = (args.reps, args.kernel_warmup)
     if not args.no_small:
         # the two smaller workloads at their tolerance sweeps (tau = 0 is measured too)
-        detail["cfg1_1024"] = train_config(1, (1e-4, 1e-3), *rw, memory=not args.no_memory)
-        detail["cfg2_8192"] = train_config(2, (1e-4, 1e-3), *rw, memory=not args.no_memory)
+        detail["needle_1k_d64"] = train_workload("needle_1k_d64", (1e-4, 1e-3), *rw, memory=not args.no_memory)
+        detail["mha16_8k"] = train_workload("mha16_8k", (1e-4, 1e-3), *rw, memory=not args.no_memory)
     if not args.no_32k:
         # the 32768-token GQA workload at tau (and the canonical tau = 1, supplementary)
-        detail["32k"] = train_config(3, (tau, 1.0), *rw, supp_taus=(1.0,), supp=(sr, sw),
+        detail["32k"] = train_workload("gqa32x8_32k", (tau, 1.0), *rw, supp_taus=(1.0,), supp=(sr, sw),
                                      memory=not args.no_memory)
     if not args.no_lm:
         detail["lm_like_sweep"] = {

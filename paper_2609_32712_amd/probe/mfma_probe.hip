@@ -1,8 +1,9 @@
 // Measurement probe for the benchmark: the rate at which one MI355X runs
 // v_mfma_f32_32x32x16_bf16 when nothing else limits it (operands in registers, four
 // independent accumulator chains per wavefront, three wavefronts per SIMD, no memory
-// traffic in the loop).  It states the practical MFMA ceiling and clock of the box a
-// benchmark ran on, beside the rated 2.5 PFLOP/s that the roofline fraction uses.
+// traffic in the loop).  It states the practical MFMA ceiling and clock of the
+// machine a benchmark ran on, beside the rated 2.5 PFLOP/s that the roofline
+// fraction uses.
 // Not part of libmala.so.
 #include <hip/hip_runtime.h>
 

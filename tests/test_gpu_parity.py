@@ -14,7 +14,7 @@ import paper_2609_32712_amd as mala
 from parity_util import (LSE_DIAG, TOL_MAX, assert_close, assert_counts, bwd_do_loads, dev,
                          dkdv_splits, fwd_v_loads, host,
                          set_fingerprint, tie_masks, ties)
-from workloads import CONFIGS, Workload, bf16_to_f64
+from workloads import WORKLOADS, Workload, bf16_to_f64
 
 pytestmark = pytest.mark.gpu
 
@@ -35,7 +35,7 @@ def legal_tiles(B, Hq, Nq, Nk, bq, bk):
 # small cases: every element
 # --------------------------------------------------------------------------
 TRAIN_CASES = {
-    "cfg1": dict(spec=1, over={}),
+    "needle_1k_d64": dict(spec="needle_1k_d64", over={}),
     "local_d64_ragged": dict(spec=dict(kind="train", B=1, Hq=2, Hkv=1, N=1000, D=64, beta=3.0,
                                        local=4.0), over={}),
     "gqa_d128_ragged": dict(spec=dict(kind="train", B=2, Hq=4, Hkv=2, N=700, D=128, beta=2.5,
@@ -47,15 +47,15 @@ TRAIN_CASES = {
     "tiny_d128": dict(spec=dict(kind="train", B=1, Hq=2, Hkv=2, N=37, D=128, beta=2.0, local=1.0),
                       over={}),
     "single_row_d64": dict(spec=dict(kind="train", B=1, Hq=1, Hkv=1, N=1, D=64, beta=1.0), over={}),
-    # the language-model-like supplementary workload (config 6) at a small size
-    "lm_d128_ragged": dict(spec=6, over=dict(N=1000, Hq=4, Hkv=2)),
+    # the language-model-like supplementary workload at a small size
+    "lm_d128_ragged": dict(spec="lm_like_gqa8x2_32k", over=dict(N=1000, Hq=4, Hkv=2)),
     # two sequences, d = 64, 47 key blocks of one KV head each: the key-block sweeps run
     # in parts (1504 iterations in the first, parts of 512) summed by the reduction
     "split_d64_b2": dict(spec=dict(kind="train", B=2, Hq=8, Hkv=1, N=6000, D=64, beta=2.0,
                                    local=2.0), over={}),
 }
 TRAIN_TAUS = {
-    "cfg1": (0.0, 1e-4, 1e-3),
+    "needle_1k_d64": (0.0, 1e-4, 1e-3),
     "local_d64_ragged": (0.0, 1e-2, 0.3, 1.0),
     # 1e-40 is an fp32 denormal (log2 tau = -132.9: nothing is skipped); 1e30 keeps
     # only each row's first tile in the forward and no tile in the backward
@@ -385,7 +385,7 @@ def test_varlen_full_size_equals_per_sequence_calls(tau):
     # so the two agree within the sum of their error bounds (2^-8 x budget x the
     # largest |dO| or scale |Q|, per path)
     lens = [16384, 8192, 4096, 1500, 1024, 1000, 500, 68, 4]
-    w, cu, t = _packed(dict(CONFIGS[6], B=1), lens)
+    w, cu, t = _packed(dict(WORKLOADS["lm_like_gqa8x2_32k"], B=1), lens)
     scale = f32(w.scale)
     Q, K, V, DO = (dev(t[x]) for x in ("q", "k", "v", "do"))
     CU = torch.from_numpy(cu).to("cuda")
@@ -573,7 +573,7 @@ def test_decode_splits_cover_dense_at_tau0():
 # --------------------------------------------------------------------------
 # full-size workloads: sampled outputs in the benchmark's launch configuration
 # --------------------------------------------------------------------------
-def _full_train(cfg_id, tau, sample_heads, sample_fracs, kv, rows_from, key_fracs, seed=0):
+def _full_train(name, tau, sample_heads, sample_fracs, kv, rows_from, key_fracs, seed=0):
     """One workload in the benchmark's launch configuration, against the oracle on:
       * sampled query blocks (sample_fracs of the blocks) of sampled query heads:
         O, LSE, forward and backward retained counts, dQ;
@@ -584,14 +584,14 @@ def _full_train(cfg_id, tau, sample_heads, sample_fracs, kv, rows_from, key_frac
         heads the way the key-major pass accumulates them;
     and the two backward passes' retained counts and fingerprints against each
     other."""
-    w = Workload(cfg_id, seed=seed)
-    print("[full cfg%d tau=%g] generating inputs" % (cfg_id, tau), flush=True)
+    w = Workload(name, seed=seed)
+    print("[full %s tau=%g] generating inputs" % (name, tau), flush=True)
     t = w.tensors(threads=16)
     scale = f32(w.scale)
     bq, bk = mala.mala_geometry(w.D, mala.PASS_FWD)
     N, D = w.N, w.D
     Q, K, V, DO = map(dev, (t["q"], t["k"], t["v"], t["do"]))
-    print("[full cfg%d] gpu fwd+bwd" % cfg_id, flush=True)
+    print("[full %s] gpu fwd+bwd" % name, flush=True)
     g = mala.fwd(Q, K, V, scale, tau)
     gb = mala.bwd(Q, K, V, g["o"], g["lse"], DO, scale, tau)
     torch.cuda.synchronize()
@@ -609,7 +609,7 @@ def _full_train(cfg_id, tau, sample_heads, sample_fracs, kv, rows_from, key_frac
         qf, dof = f64("q", b, h, h + 1), f64("do", b, h, h + 1)
         kf, vf = f64("k", b, hk, hk + 1), f64("v", b, hk, hk + 1)
         for i in sorted({min(Tr - 1, int(f * Tr)) for f in sample_fracs}):
-            print("[full cfg%d] oracle head %d block %d" % (cfg_id, h, i), flush=True)
+            print("[full %s] oracle head %d block %d" % (name, h, i), flush=True)
             rows = slice(i * bq, min(N, (i + 1) * bq))
             of = oracle.mala_fwd(qf, kf, vf, scale, f32(tau), bq, bk, blocks=(i, i + 1))
             ob = oracle.mala_bwd(qf, kf, vf, of["o"], of["lse"], dof, scale, f32(tau), bq, bk,
@@ -628,8 +628,8 @@ def _full_train(cfg_id, tau, sample_heads, sample_fracs, kv, rows_from, key_frac
     r0 = i0 * bq
     qf, dof = f64("q", b, h0, h1), f64("do", b, h0, h1)
     kf, vf = f64("k", b, hk, hk + 1), f64("v", b, hk, hk + 1)
-    print("[full cfg%d] oracle forward of kv head %d (%d query heads), rows %d.." %
-          (cfg_id, hk, grp, r0), flush=True)
+    print("[full %s] oracle forward of kv head %d (%d query heads), rows %d.." %
+          (name, hk, grp, r0), flush=True)
     of = oracle.mala_fwd(qf, kf, vf, scale, f32(tau), bq, bk, blocks=(i0, Tr))
     sl = (0, slice(None), slice(r0, N))
     assert_close("O group", o_gpu[b, h0:h1, r0:], of["o"][sl])
@@ -639,7 +639,7 @@ def _full_train(cfg_id, tau, sample_heads, sample_fracs, kv, rows_from, key_frac
     o_in, lse_in = np.nan_to_num(of["o"]), np.nan_to_num(of["lse"])
     j_lo = -(-r0 // bk)
     for j in sorted({min(Tc - 2, max(j_lo, int(f * Tc))) for f in key_fracs}):
-        print("[full cfg%d] oracle dK/dV of key tiles %d-%d (kv head %d)" % (cfg_id, j, j + 1, hk),
+        print("[full %s] oracle dK/dV of key tiles %d-%d (kv head %d)" % (name, j, j + 1, hk),
               flush=True)
         ob = oracle.mala_bwd(qf, kf, vf, o_in, lse_in, dof, scale, f32(tau), bq, bk,
                              qblocks=(0, 0), kblocks=(j, j + 2))
@@ -652,36 +652,36 @@ EDGES = (0.0, 0.5, 1.0)   # key tiles at the start, the middle and the end
 
 
 @pytest.mark.parametrize("tau", [0.0, 1e-4, 1e-3])
-def test_full_config2_sampled(tau):
-    _full_train(2, tau, [(0, 3), (0, 12)], (0.0, 0.37, 0.999), kv=(0, 5), rows_from=0.0,
+def test_full_mha16_8k_sampled(tau):
+    _full_train("mha16_8k", tau, [(0, 3), (0, 12)], (0.0, 0.37, 0.999), kv=(0, 5), rows_from=0.0,
                 key_fracs=EDGES)
 
 
 @pytest.mark.parametrize("tau", [0.0, 1e-4, 1.0])
-def test_full_config3_sampled(tau):
+def test_full_gqa32x8_32k_sampled(tau):
     # heads 28..31 of KV head 7; their needle strengths beta_h differ
-    _full_train(3, tau, [(0, 1), (0, 30)], (0.5, 0.999), kv=(0, 7), rows_from=0.0,
+    _full_train("gqa32x8_32k", tau, [(0, 1), (0, 30)], (0.5, 0.999), kv=(0, 7), rows_from=0.0,
                 key_fracs=EDGES)
 
 
 @pytest.mark.parametrize("tau", [1e-4, 1.0])
-def test_full_config4_sampled(tau):
+def test_full_gqa8x2_128k_sampled(tau):
     # the key tiles from 15/16 of the sequence on accumulate over ~1000 query tiles of
     # each of the 4 query heads of the group
-    _full_train(4, tau, [(0, 6)], (0.25, 0.999), kv=(0, 1), rows_from=15 / 16,
+    _full_train("gqa8x2_128k", tau, [(0, 6)], (0.25, 0.999), kv=(0, 1), rows_from=15 / 16,
                 key_fracs=(15 / 16, 31 / 32, 1.0))
 
 
 @pytest.mark.parametrize("tau", [1e-4, 1.0])
-def test_full_config6_sampled(tau):
-    _full_train(6, tau, [(0, 2), (0, 7)], (0.3, 0.999), kv=(0, 1), rows_from=0.0,
+def test_full_lm_like_gqa8x2_32k_sampled(tau):
+    _full_train("lm_like_gqa8x2_32k", tau, [(0, 2), (0, 7)], (0.3, 0.999), kv=(0, 1), rows_from=0.0,
                 key_fracs=EDGES)
 
 
 @pytest.mark.parametrize("tau", [0.0, 1e-4, 1.0])
-def test_full_config5_decode_sampled(tau):
-    w = Workload(5)
-    print("[full cfg5 tau=%g] generating inputs" % tau, flush=True)
+def test_full_decode_gqa32x8_128k_sampled(tau):
+    w = Workload("decode_gqa32x8_128k")
+    print("[full decode_gqa32x8_128k tau=%g] generating inputs" % tau, flush=True)
     t = w.tensors(threads=16)
     scale = f32(w.scale)
     bk = mala.mala_geometry(w.D, mala.PASS_DECODE)[1]
@@ -691,7 +691,7 @@ def test_full_config5_decode_sampled(tau):
     o, lse, ht = host(g["o"]), host(g["lse"]), host(g["head_tiles"])
     rng = np.random.default_rng(5)
     pairs = [(int(rng.integers(w.B)), int(rng.integers(w.Hq))) for _ in range(6)]
-    print("[full cfg5] oracle on", pairs, "splits", S, flush=True)
+    print("[full decode_gqa32x8_128k] oracle on", pairs, "splits", S, flush=True)
     qf = bf16_to_f64(t["q"])
     for b, h in pairs:
         hk = h // w.g
@@ -703,10 +703,10 @@ def test_full_config5_decode_sampled(tau):
 
 
 @pytest.mark.parametrize("tau", [1e-4, 1.0])
-def test_full_config5_decode_ragged_lengths_sampled(tau):
+def test_full_decode_gqa32x8_128k_ragged_lengths_sampled(tau):
     # the serving case: the 131072-token caches holding ragged valid lengths
-    w = Workload(5)
-    print("[full cfg5 ragged tau=%g] generating inputs" % tau, flush=True)
+    w = Workload("decode_gqa32x8_128k")
+    print("[full decode_gqa32x8_128k ragged tau=%g] generating inputs" % tau, flush=True)
     t = w.tensors(threads=16)
     scale = f32(w.scale)
     bk = mala.mala_geometry(w.D, mala.PASS_DECODE)[1]
@@ -720,7 +720,7 @@ def test_full_config5_decode_ragged_lengths_sampled(tau):
     qf = bf16_to_f64(t["q"])
     for b, h in [(0, 5), (1, 0), (2, 17), (9, 31)]:
         n, hk = int(lens[b]), h // w.g
-        print("[full cfg5 ragged] oracle seq %d head %d n=%d splits %d" % (b, h, n, S), flush=True)
+        print("[full decode_gqa32x8_128k ragged] oracle seq %d head %d n=%d splits %d" % (b, h, n, S), flush=True)
         od = oracle.mala_decode(qf[b:b + 1, h:h + 1], bf16_to_f64(t["k"][b:b + 1, hk:hk + 1, :n]),
                                 bf16_to_f64(t["v"][b:b + 1, hk:hk + 1, :n]), scale, f32(tau), bk,
                                 S)

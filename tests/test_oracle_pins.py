@@ -549,11 +549,11 @@ def test_bf16_rounding_is_round_to_nearest_even():
 
 
 def test_workload_generator_shapes_and_needles():
-    w = Workload(1)
+    w = Workload("needle_1k_d64")
     t = w.tensors()
     assert t["q"].shape == (1, 1, 1024, 64) and t["do"].shape == (1, 1, 1024, 64)
-    np.testing.assert_array_equal(Workload(1).tensors()["q"], t["q"])   # seeded
-    w5 = Workload(5, N=512, B=2)
+    np.testing.assert_array_equal(Workload("needle_1k_d64").tensors()["q"], t["q"])   # seeded
+    w5 = Workload("decode_gqa32x8_128k", N=512, B=2)
     q = bf16_to_f64(w5.q_head(1, 5))
     k = bf16_to_f64(w5.k_head(1, 5 // 4))
     pos = w5.needle_positions(1, 5)

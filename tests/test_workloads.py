@@ -2,11 +2,11 @@
 language-model-like supplementary workload its structure."""
 import numpy as np
 
-from workloads import CONFIGS, Workload, bf16_round, bf16_to_f64
+from workloads import WORKLOADS, Workload, bf16_round, bf16_to_f64
 
 
 def _small(**over):
-    spec = dict(CONFIGS[6])
+    spec = dict(WORKLOADS["lm_like_gqa8x2_32k"])
     spec.update(dict(N=300, Hq=2, Hkv=1, D=64), **over)
     return Workload(spec, seed=3)
 
@@ -47,7 +47,7 @@ def test_rademacher_probe():
 
 def test_existing_configurations_unchanged_by_the_new_options():
     # the default paths draw exactly as before: no block needles, no sink, normal dO
-    w = Workload(dict(CONFIGS[2], N=64, Hq=1, Hkv=1))
+    w = Workload(dict(WORKLOADS["mha16_8k"], N=64, Hq=1, Hkv=1))
     g = w.do_head(0, 0)
     assert bf16_to_f64(g).std() > 0.5 and len(np.unique(g)) > 100
     r = w.needle_rows(0, 0)

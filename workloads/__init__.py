@@ -4,11 +4,12 @@ arithmetic: it only draws random numbers and rounds them to bf16.
 
 The paper measures operator latency on unspecified inputs and operator fidelity
 on hidden states of a 14B checkpoint that is not available; these generators
-stand in for both.  Recipe (identical for every configuration):
+stand in for both.  Recipe (identical for every workload):
 
   * one independent PCG64 stream per (tensor, batch, head), seeded with
-    ``numpy.random.default_rng([seed, config_id, tensor_id, b, h])``, so any
-    single head can be regenerated without drawing the others;
+    ``numpy.random.default_rng([seed, stream_id, tensor_id, b, h])`` (stream_id
+    fixed per named workload, 0 for specs given as dicts), so any single head can
+    be regenerated without drawing the others;
   * standard normals drawn as float32 (PCG64 + ziggurat), combined in float64,
     and rounded to bf16 with round-to-nearest-even;
   * K and V ~ N(0, 1); dO ~ N(0, 1);
@@ -34,29 +35,32 @@ import torch
 # tensor ids of the per-slice streams
 _T_K, _T_V, _T_Q, _T_DO, _T_BETA, _T_POS = 1, 2, 3, 4, 5, 6
 
-# The five workloads.  "kind": "train" (fwd + bwd) or "decode".
-CONFIGS = {
-    1: dict(kind="train", B=1, Hq=1, Hkv=1, N=1024, D=64, beta=2.0, local=0.0,
+# The named workloads.  "kind": "train" (fwd + bwd) or "decode".
+WORKLOADS = {
+    "needle_1k_d64": dict(kind="train", B=1, Hq=1, Hkv=1, N=1024, D=64, beta=2.0, local=0.0,
             taus=(0.0, 1e-4, 1e-3), desc="causal fwd+bwd, 1x1x1024x64, needle beta=2"),
-    2: dict(kind="train", B=1, Hq=16, Hkv=16, N=8192, D=128, beta=2.0, local=1.0,
+    "mha16_8k": dict(kind="train", B=1, Hq=16, Hkv=16, N=8192, D=128, beta=2.0, local=1.0,
             taus=(0.0, 1e-4, 1e-3),
             desc="causal fwd+bwd, MHA 16 heads, 8192x128, needle beta=2 + local 1.0"),
-    3: dict(kind="train", B=1, Hq=32, Hkv=8, N=32768, D=128, beta=(0.5, 3.0), local=0.0,
+    "gqa32x8_32k": dict(kind="train", B=1, Hq=32, Hkv=8, N=32768, D=128, beta=(0.5, 3.0), local=0.0,
             taus=(0.0, 1e-4), desc="causal fwd+bwd, GQA 32/8, 32768x128, per-head beta~U[0.5,3]"),
-    4: dict(kind="train", B=1, Hq=8, Hkv=2, N=131072, D=128, beta=2.0, local=0.0,
+    "gqa8x2_128k": dict(kind="train", B=1, Hq=8, Hkv=2, N=131072, D=128, beta=2.0, local=0.0,
             taus=(0.0, 1e-4),
             desc="causal fwd+bwd, GQA 8/2 (one TP=8 share), 131072x128, beta=2"),
-    5: dict(kind="decode", B=16, Hq=32, Hkv=8, N=131072, D=128, beta=3.0, needles=4,
+    "decode_gqa32x8_128k": dict(kind="decode", B=16, Hq=32, Hkv=8, N=131072, D=128, beta=3.0, needles=4,
             taus=(0.0, 1e-4),
             desc="decode, 16 x GQA 32/8 over 131072-token caches, 4 needles beta=3"),
     # supplementary: a workload on which the forward rule can skip (a dominant local
     # key found in the diagonal tile, needles shared by 32-row blocks, a sink), with
     # a Rademacher dO for the fidelity measurements
-    6: dict(kind="train", B=1, Hq=8, Hkv=2, N=32768, D=128, beta=2.0, local=2.0,
+    "lm_like_gqa8x2_32k": dict(kind="train", B=1, Hq=8, Hkv=2, N=32768, D=128, beta=2.0, local=2.0,
             needle_block=32, sink=1.5, do="rademacher", taus=(0.0, 1e-4, 1.0),
             desc="causal fwd+bwd, GQA 8/2, 32768x128, LM-like: local 2, block needles beta=2, "
                  "sink 1.5"),
 }
+# the random-stream id of each named workload (part of every generator seed)
+STREAM = {"needle_1k_d64": 1, "mha16_8k": 2, "gqa32x8_32k": 3, "gqa8x2_128k": 4,
+          "decode_gqa32x8_128k": 5, "lm_like_gqa8x2_32k": 6}
 
 
 def bf16_round(x: np.ndarray) -> np.ndarray:
@@ -91,28 +95,29 @@ def bf16_to_f64(bits: np.ndarray) -> np.ndarray:
     return b.view(np.float32).astype(np.float64)
 
 
-def _rng(seed, cfg_id, tensor, b, h):
-    return np.random.default_rng([int(seed), int(cfg_id), tensor, int(b), int(h)])
+def _rng(seed, stream, tensor, b, h):
+    return np.random.default_rng([int(seed), int(stream), tensor, int(b), int(h)])
 
 
-def _normal(seed, cfg_id, tensor, b, h, shape):
-    return _rng(seed, cfg_id, tensor, b, h).standard_normal(shape, dtype=np.float32)
+def _normal(seed, stream, tensor, b, h, shape):
+    return _rng(seed, stream, tensor, b, h).standard_normal(shape, dtype=np.float32)
 
 
-def _normal_bits(seed, cfg_id, tensor, b, h, shape):
-    return bf16_round(_normal(seed, cfg_id, tensor, b, h, shape))
+def _normal_bits(seed, stream, tensor, b, h, shape):
+    return bf16_round(_normal(seed, stream, tensor, b, h, shape))
 
 
 class Workload:
-    """Lazily generated inputs of one configuration (any subset of heads)."""
+    """Lazily generated inputs of one workload (any subset of heads): a name of
+    WORKLOADS or a spec dict."""
 
-    def __init__(self, cfg, seed: int = 0, **overrides):
-        if isinstance(cfg, int):
-            self.cfg_id = cfg
-            spec = dict(CONFIGS[cfg])
+    def __init__(self, workload, seed: int = 0, **overrides):
+        if isinstance(workload, str):
+            self.stream = STREAM[workload]
+            spec = dict(WORKLOADS[workload])
         else:
-            spec = dict(cfg)
-            self.cfg_id = int(spec.pop("id", 0))
+            spec = dict(workload)
+            self.stream = int(spec.pop("id", 0))
         spec.update(overrides)
         self.spec = spec
         self.seed = seed
@@ -127,29 +132,29 @@ class Workload:
     def k_head(self, b, hkv):
         key = (b, hkv)
         if key not in self._k:
-            self._k[key] = _normal_bits(self.seed, self.cfg_id, _T_K, b, hkv, (self.N, self.D))
+            self._k[key] = _normal_bits(self.seed, self.stream, _T_K, b, hkv, (self.N, self.D))
         return self._k[key]
 
     def v_head(self, b, hkv):
-        return _normal_bits(self.seed, self.cfg_id, _T_V, b, hkv, (self.N, self.D))
+        return _normal_bits(self.seed, self.stream, _T_V, b, hkv, (self.N, self.D))
 
     def do_head(self, b, h):
         if self.spec.get("do") == "rademacher":
-            rng = _rng(self.seed, self.cfg_id, _T_DO, b, h)
+            rng = _rng(self.seed, self.stream, _T_DO, b, h)
             return bf16_round(rng.integers(0, 2, size=(self.N, self.D)) * 2.0 - 1.0)
-        return _normal_bits(self.seed, self.cfg_id, _T_DO, b, h, (self.N, self.D))
+        return _normal_bits(self.seed, self.stream, _T_DO, b, h, (self.N, self.D))
 
     def beta(self, h):
         beta = self.spec["beta"]
         if isinstance(beta, tuple):
             lo, hi = beta
-            return float(_rng(self.seed, self.cfg_id, _T_BETA, 0, h).uniform(lo, hi))
+            return float(_rng(self.seed, self.stream, _T_BETA, 0, h).uniform(lo, hi))
         return float(beta)
 
     def q_head(self, b, h):
         """Planted-needle query rows for a training workload (or the decode query)."""
         kf = bf16_to_f64(self.k_head(b, h // self.g))
-        rng = _rng(self.seed, self.cfg_id, _T_Q, b, h)
+        rng = _rng(self.seed, self.stream, _T_Q, b, h)
         beta = self.beta(h)
         if self.kind == "decode":
             g = rng.standard_normal(self.D, dtype=np.float32).astype(np.float64)
@@ -175,7 +180,7 @@ class Workload:
 
     def needle_rows(self, b, h):
         """Training only: the key r(i) planted in each query row of head (b, h)."""
-        rng = _rng(self.seed, self.cfg_id, _T_Q, b, h)
+        rng = _rng(self.seed, self.stream, _T_Q, b, h)
         N = self.N
         rng.standard_normal((N, self.D), dtype=np.float32)
         nb = int(self.spec.get("needle_block", 1))
@@ -186,7 +191,7 @@ class Workload:
 
     def needle_positions(self, b, h):
         """Decode only: the planted positions of query head (b, h)."""
-        rng = _rng(self.seed, self.cfg_id, _T_Q, b, h)
+        rng = _rng(self.seed, self.stream, _T_Q, b, h)
         rng.standard_normal(self.D, dtype=np.float32)
         return np.sort(rng.choice(self.N, size=self.spec.get("needles", 4), replace=False))
 
