@@ -411,11 +411,24 @@ __global__ __launch_bounds__(1024) void mala_bwd_dkdv_kernel(BwdParams p) {
                   ((long)kw + kBk - 1 > (long)q0 + off) || (q0 + kBq > Nq) || (kw + kBk > Nk);
               const int klo = key < Nk ? (int)((long)key - off - q0) - 4 * h : 1000000;
               float sv[16];
-              const bool dem =
-                  offline_entries(sc, p.scale2, need_mask, klo, Nq - q0 - 4 * h, rv + kBq, h, sv);
-              if (p.counters && wave_any(dem)) {
-                ++n_ret_kv;
-                hsum += tile_hash(b, hkv * grp + it % grp, q0 / kBq, kw / kBk);
+              if (p.counters) {
+                // the offline test again, as a statistic: it confirms the dQ pass's decision
+                const bool dem =
+                    offline_entries(sc, p.scale2, need_mask, klo, Nq - q0 - 4 * h, rv + kBq, h, sv);
+                if (wave_any(dem)) {
+                  ++n_ret_kv;
+                  hsum += tile_hash(b, hkv * grp + it % grp, q0 / kBq, kw / kBk);
+                }
+              } else if (need_mask) {
+                const int qlim = Nq - q0 - 4 * h;
+#pragma unroll
+                for (int g = 0; g < 4; ++g)
+#pragma unroll
+                  for (int e = 0; e < 4; ++e)
+                    sv[4 * g + e] = (8 * g + e >= klo) && (8 * g + e < qlim) ? sc[4 * g + e] : kNegInf;
+              } else {
+#pragma unroll
+                for (int r = 0; r < 16; ++r) sv[r] = sc[r];
               }
               probabilities(sv, p.scale2, rv, h);
 #pragma unroll

@@ -849,6 +849,27 @@ def test_repeat_runs_bitwise_forward_dk_dv():
     assert torch.equal(r1["row_tiles"], r2["row_tiles"])
 
 
+@pytest.mark.parametrize("name,tau,Nq", [("gqa_d128_ragged", 0.1, None), ("local_d64_ragged", 0.3, None),
+                                         ("tiny_d128", 1e-3, None), ("split_d64_b2", 1e-3, None),
+                                         ("lm_d128_ragged", 1.0, None), ("gqa_d128_ragged", 0.05, 77)])
+def test_statistics_leave_outputs_unchanged(name, tau, Nq):
+    # The optional statistics (row tile counts, counters) take work of their own in
+    # the kernels (the key-major pass re-runs the offline test on its tiles only when
+    # counters are requested, and masks the scores without it otherwise): the
+    # outputs are the same bits either way (also for a prefill of the last Nq rows).
+    w, q, k, v, do = _train_case(name, tau, Nq=Nq)
+    Q, K, V, DO = map(dev, (q, k, v, do))
+    s = f32(w.scale)
+    f1 = mala.fwd(Q, K, V, s, tau)
+    f0 = mala.fwd(Q, K, V, s, tau, stats=False)
+    b1 = mala.bwd(Q, K, V, f1["o"], f1["lse"], DO, s, tau)
+    b0 = mala.bwd(Q, K, V, f1["o"], f1["lse"], DO, s, tau, stats=False)
+    torch.cuda.synchronize()
+    assert torch.equal(f1["o"], f0["o"]) and torch.equal(f1["lse"], f0["lse"])
+    for x in ("dq", "dk", "dv"):
+        assert torch.equal(b1[x], b0[x]), x
+
+
 @pytest.mark.parametrize("name", ["gqa_d128_ragged", "split_d64_b2"])
 def test_graph_capture_replays_match_eager(name):
     # The library only launches kernels on the caller's stream (counters are
