@@ -21,9 +21,10 @@
 // group from the end down to the diagonal, stepping only through the query tiles
 // that the dQ kernel retained for some of its four key tiles.  Sixteen wavefronts,
 // four roles per 32 keys on one SIMD, pipelined over those tiles: role 0 forms P
-// (fp32, handed on through LDS) and re-runs the offline test as a check, role 1
-// accumulates dV one tile later and moves the query tiles into LDS, role 2 forms dP
-// and dS, role 3 accumulates dK two tiles later (dS handed on as bf16 operands).
+// (fp32, handed on through LDS) and, when counters are requested, re-runs the
+// offline test as a check; role 1 accumulates dV one tile later and moves the query
+// tiles into LDS; role 2 forms dP and dS; role 3 accumulates dK two tiles later (dS
+// handed on as bf16 operands).
 // On small grids the sweeps run in parts whose sums mala_bwd_dkdv_reduce_kernel
 // adds.  An MFMA with its operands exchanged gives the transposed scores bit for
 // bit, so both kernels see the same scores.
@@ -227,9 +228,9 @@ __global__ __launch_bounds__(1024) void mala_bwd_dkdv_kernel(BwdParams p) {
   // The tile decisions are the dQ pass's (it runs first and records, per query tile,
   // head and 128-key block, which of the four 32-key tiles it retained): a query tile
   // that no key group retains costs no score MFMAs, no Q / dO load and no pipeline
-  // step here.  Role 0 still evaluates the offline test on the tiles it processes and
-  // counts those it confirms (a statistic: equal to the retained count when the two
-  // passes agree).
+  // step here.  When counters are requested, role 0 also evaluates the offline test on
+  // the tiles it processes and counts those it confirms (a statistic: equal to the
+  // retained count when the two passes agree).
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int role = wave >> 2, grp_k = wave & 3;
