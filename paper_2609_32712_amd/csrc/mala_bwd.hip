@@ -201,7 +201,9 @@ __global__ __launch_bounds__(1024) void mala_bwd_dkdv_kernel(BwdParams p) {
   // at step k + 1 (k counts the processed tiles)
   __shared__ __attribute__((aligned(16))) bf16 Qs[4 * TS];
   __shared__ __attribute__((aligned(16))) bf16 dOs[3 * TS];
-  __shared__ __attribute__((aligned(16))) float rowv[3][3][kBq];   // lse2, threshold, D_q
+  // per-row vectors of the ring's tiles: lse2, test threshold (written only when
+  // counters are requested), -D_q
+  __shared__ __attribute__((aligned(16))) float rowv[3][3][kBq];
   // hand-offs per key group: P in fp32 as [buf][group][C registers 4g .. 4g+3][lane];
   // dS as the B operands [buf][group][hi0, hi1, lo0, lo1][lane]
   __shared__ __attribute__((aligned(16))) f32x4 Pf[2][4][4][64];
@@ -320,11 +322,13 @@ __global__ __launch_bounds__(1024) void mala_bwd_dkdv_kernel(BwdParams p) {
       // the same arithmetic as row_vectors (the query-major kernel must agree bitwise)
 #pragma clang fp contract(off)
       const bool prow = pq0 + mt < Nq;
-      const float plg = log2f((float)((long)pq0 + mt + 1 + off));
       const float l2 = plse * kLog2e;
       rowv[k % 3][0][mt] = prow ? l2 : 0.f;
-      rowv[k % 3][1][mt] = prow ? l2 + p.log2tau - plg : __builtin_huge_valf();
-      rowv[k % 3][2][mt] = prow ? pdv : 0.f;
+      if (p.counters) {   // the threshold feeds only the statistics' re-run of the test
+        const float plg = log2f((float)((long)pq0 + mt + 1 + off));
+        rowv[k % 3][1][mt] = prow ? l2 + p.log2tau - plg : __builtin_huge_valf();
+      }
+      rowv[k % 3][2][mt] = prow ? -pdv : 0.f;   // -D: the dP accumulator starts there
     }
     wait_vm();
   };
@@ -468,14 +472,23 @@ __global__ __launch_bounds__(1024) void mala_bwd_dkdv_kernel(BwdParams p) {
             const bf16* orr = lds_pin(dOs + (t % 3) * TS + rdo);
 #pragma unroll
             for (int kk = 0; kk < KS; ++kk) oa[kk] = load8(orr + rd_step<D>(kk));
-            const f32x16 dp = qk_tile<KS>(oa, kv);
+            // dP - D: the accumulator starts at -D of each row (C layout: register 4 g + e
+            // holds row 8 g + 4 h + e)
+            f32x16 dpd;
+#pragma unroll
+            for (int g = 0; g < 4; ++g) {
+              const f32x4 d4 = *reinterpret_cast<const f32x4*>(rv + 2 * kBq + 8 * g + 4 * h);
+#pragma unroll
+              for (int e = 0; e < 4; ++e) dpd[4 * g + e] = d4[e];
+            }
+#pragma unroll
+            for (int kk = 0; kk < KS; ++kk) dpd = mfma32(oa[kk], kv[kk], dpd);
             float ds[16];
 #pragma unroll
             for (int g = 0; g < 4; ++g) {
               const f32x4 p4 = Pf[t & 1][grp_k][g][lane];
-              const f32x4 d4 = *reinterpret_cast<const f32x4*>(rv + 2 * kBq + 8 * g + 4 * h);
 #pragma unroll
-              for (int e = 0; e < 4; ++e) ds[4 * g + e] = p4[e] * (dp[4 * g + e] - d4[e]);
+              for (int e = 0; e < 4; ++e) ds[4 * g + e] = p4[e] * dpd[4 * g + e];
             }
             // dK runs this tile without dS's lo term while the key's sum of |dS| in
             // such tiles stays within kLoMassDk (for every key of the tile); a tile
